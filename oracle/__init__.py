@@ -1,0 +1,147 @@
+"""Oracle: plain CPU definition of the propagate path (test infrastructure).
+
+This package is TEST INFRASTRUCTURE. Only ``tests/``, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py`` may import it. The HIP library
+and its Python binding never import it, and it imports nothing from them.
+
+The arithmetic lives in ``oracle.c`` (plain C loops, fp64 accumulation),
+compiled with gcc into ``liboracle.so``. This module only marshals numpy
+arrays through ctypes. Every function follows Eq. (1) of the paper
+(Section 2, "Neighborhood Aggregation") with gamma = identity, or the
+"Global Pooling" / "Mini-batch Handling" paragraphs of Section 2.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+MSG = {"src": 0, "diff": 1}
+AGGR = {"sum": 0, "mean": 1, "max": 2}
+_ERR = {-1: "invalid argument", -2: "index out of range", -3: "non-finite input"}
+
+_lib = None
+
+
+def build(src: str = _SRC, out: str = _LIB_PATH) -> str:
+    """Compile the oracle with gcc (no fast-math, no FMA contraction)."""
+    cmd = ["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-std=c11", "-fPIC",
+           "-shared", "-Wall", "-Werror", src, "-o", out + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+def load(path: str | None = None) -> ctypes.CDLL:
+    """Load a compiled oracle library; build the default one if absent."""
+    global _lib
+    if path is not None:
+        return _bind(ctypes.CDLL(path))
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        _lib = _bind(ctypes.CDLL(_LIB_PATH))
+    return _lib
+
+
+def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
+    p, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.oracle_degree.argtypes = [p, i64, i64, p]
+    lib.oracle_coo_to_csr.argtypes = [p, i64, i64, p, p, p]
+    lib.oracle_gcn_norm.argtypes = [p, p, i64, i64, p]
+    lib.oracle_propagate.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p]
+    lib.oracle_global_pool.argtypes = [p, i64, i64, p, i64, i32, p, p, p]
+    for fn in (lib.oracle_degree, lib.oracle_coo_to_csr, lib.oracle_gcn_norm,
+               lib.oracle_propagate, lib.oracle_global_pool):
+        fn.restype = ctypes.c_int
+    return lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise ValueError(f"oracle {what}: {_ERR.get(rc, rc)}")
+
+
+def _ei(edge_index) -> np.ndarray:
+    ei = np.ascontiguousarray(edge_index, dtype=np.int64)
+    if ei.ndim != 2 or ei.shape[0] != 2:
+        raise ValueError("edge_index must be [2, E]")
+    return ei
+
+
+def degree(edge_index, N: int, lib=None) -> np.ndarray:
+    """In-degree of every node: incoming edges counted with multiplicity."""
+    lib = lib or load()
+    ei = _ei(edge_index)
+    deg = np.empty(N, np.int64)
+    _check(lib.oracle_degree(_ptr(ei), ei.shape[1], N, _ptr(deg)), "degree")
+    return deg
+
+
+def coo_to_csr(edge_index, N: int, lib=None):
+    """Stable target-sorted CSR: (rowptr [N+1], col [E], perm [E]), all int64."""
+    lib = lib or load()
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    rowptr = np.empty(N + 1, np.int64)
+    col = np.empty(E, np.int64)
+    perm = np.empty(E, np.int64)
+    _check(lib.oracle_coo_to_csr(_ptr(ei), E, N, _ptr(rowptr), _ptr(col), _ptr(perm)), "coo_to_csr")
+    return rowptr, col, perm
+
+
+def gcn_norm(edge_index, N: int, edge_weight=None, lib=None) -> np.ndarray:
+    """fp64 GCN edge normalisation dinv_j * w_k * dinv_i (self-loops already present)."""
+    lib = lib or load()
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    w = None if edge_weight is None else np.ascontiguousarray(edge_weight, dtype=np.float64)
+    norm = np.empty(E, np.float64)
+    _check(lib.oracle_gcn_norm(_ptr(ei), _ptr(w), E, N, _ptr(norm)), "gcn_norm")
+    return norm
+
+
+def propagate(x, edge_index, edge_weight=None, msg: str = "src", aggr: str = "sum", lib=None):
+    """Eq. (1) with gamma = identity. Returns (out fp64 [N,F], argmax int64 [N,F] or None,
+    sabs fp64 [N,F] = sum |message| (per degree for mean))."""
+    lib = lib or load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.ndim != 2:
+        raise ValueError("x must be [N, F]")
+    N, F = x.shape
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    w = None if edge_weight is None else np.ascontiguousarray(edge_weight, dtype=np.float32)
+    out = np.empty((N, F), np.float64)
+    sabs = np.empty((N, F), np.float64)
+    arg = np.empty((N, F), np.int64) if aggr == "max" else None
+    _check(lib.oracle_propagate(_ptr(x), N, F, _ptr(ei), E, _ptr(w), MSG[msg], AGGR[aggr],
+                                _ptr(out), _ptr(arg), _ptr(sabs)), "propagate")
+    return out, arg, sabs
+
+
+def global_pool(x, batch, B: int, aggr: str = "sum", lib=None):
+    """Per-graph readout over a non-decreasing assignment vector.
+    Returns (out fp64 [B,F], argmax node id int64 [B,F] or None, sabs)."""
+    lib = lib or load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    N, F = x.shape
+    batch = np.ascontiguousarray(batch, dtype=np.int64)
+    if batch.shape != (N,):
+        raise ValueError("batch must be [N]")
+    out = np.empty((B, F), np.float64)
+    sabs = np.empty((B, F), np.float64)
+    arg = np.empty((B, F), np.int64) if aggr == "max" else None
+    _check(lib.oracle_global_pool(_ptr(x), N, F, _ptr(batch), B, AGGR[aggr], _ptr(out),
+                                  _ptr(arg), _ptr(sabs)), "global_pool")
+    return out, arg, sabs

@@ -1,0 +1,226 @@
+/*
+ * Oracle for the message-passing propagate path of PyTorch Geometric
+ * (Fey & Lenssen, "Fast Graph Representation Learning with PyTorch
+ * Geometric", ICLR-W 2019).
+ *
+ * TEST INFRASTRUCTURE. This file is the plain, slow, obviously correct CPU
+ * definition that the HIP library is checked against. Only the test suite,
+ * the smoke check and the benchmark's cpu_baseline leg may load it; the
+ * library never calls it. It shares no source, header, table or helper with
+ * the HIP library.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fPIC -shared (no fast-math, no OpenMP).
+ * On x86-64 float arithmetic is IEEE single precision with no excess
+ * precision, so a C `float` product or difference is one correctly rounded
+ * fp32 operation.
+ *
+ * Conventions (readings of the paper, Section 2):
+ *  - A graph is G = (X, (I, E)); X is [N, F] row-major fp32, I is the COO
+ *    index matrix stored as int64 [2, E] row-major.
+ *  - Row 0 of I is the source j, row 1 the target i: Eq. (1) aggregates
+ *    phi(x_i, x_j, e_{j,i}) over j in N(i), i.e. along edges j -> i.
+ *  - Multi-edges count with multiplicity (multiset semantics).
+ *  - An empty neighbourhood aggregates to 0; its argmax is the sentinel E
+ *    (propagate) or N (pooling).
+ *  - max: messages are compared in fp32 after mapping -0.0 to +0.0; among
+ *    equal maxima the lowest edge id (first in COO order) wins.
+ *  - mean divides by the number of incoming edges, also when weighted.
+ *  - Inputs must be finite; a NaN or Inf input returns ORACLE_ERR_NONFINITE.
+ *
+ * Sum and mean accumulate in fp64 (the message w * x_j of two fp32 numbers
+ * is exact in fp64). Alongside every sum the oracle returns S = sum of
+ * |message| per output element, the scale of the fp32 rounding error that
+ * any reordering of the same sum may carry.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+
+#define ORACLE_OK 0
+#define ORACLE_ERR_ARG (-1)
+#define ORACLE_ERR_INDEX (-2)
+#define ORACLE_ERR_NONFINITE (-3)
+
+/* message kinds phi (Eq. 1) */
+#define ORACLE_MSG_SRC 0  /* x_j, times w_{j,i} when a weight is given */
+#define ORACLE_MSG_DIFF 1 /* x_j - x_i (EdgeConv-style) */
+
+/* aggregations (the permutation-invariant operator of Eq. 1) */
+#define ORACLE_SUM 0
+#define ORACLE_MEAN 1
+#define ORACLE_MAX 2
+
+int oracle_abi_version(void) { return 1; }
+
+static int check_index_range(const int64_t *idx, int64_t count, int64_t bound) {
+    for (int64_t k = 0; k < count; ++k)
+        if (idx[k] < 0 || idx[k] >= bound) return ORACLE_ERR_INDEX;
+    return ORACLE_OK;
+}
+
+/* In-degree: deg[i] = number of edges whose target is i (Eq. 1's |N(i)|,
+ * counted with multiplicity). */
+int oracle_degree(const int64_t *edge_index, int64_t E, int64_t N, int64_t *deg) {
+    if (E < 0 || N < 0 || (E > 0 && !edge_index) || (N > 0 && !deg)) return ORACLE_ERR_ARG;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    for (int64_t i = 0; i < N; ++i) deg[i] = 0;
+    for (int64_t k = 0; k < E; ++k) deg[dst[k]] += 1;
+    return ORACLE_OK;
+}
+
+/* Compressed-row (CSR) form of the COO edge list, rows = targets
+ * (Appendix A: the row-ordered, "coalesced" layout that sparse-matrix
+ * multiplication needs). Counting sort, stable by construction: inside a
+ * row the edges keep ascending original edge id.
+ *   rowptr [N+1], col [E] = source of each CSR slot, perm [E] = edge id. */
+int oracle_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N,
+                      int64_t *rowptr, int64_t *col, int64_t *perm) {
+    if (E < 0 || N < 0 || !rowptr || (E > 0 && (!edge_index || !col || !perm))) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    for (int64_t i = 0; i <= N; ++i) rowptr[i] = 0;
+    for (int64_t k = 0; k < E; ++k) rowptr[dst[k] + 1] += 1;
+    for (int64_t i = 0; i < N; ++i) rowptr[i + 1] += rowptr[i];
+    int64_t *next = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+    if (!next) return ORACLE_ERR_ARG;
+    for (int64_t i = 0; i < N; ++i) next[i] = rowptr[i];
+    for (int64_t k = 0; k < E; ++k) {
+        int64_t p = next[dst[k]]++;
+        col[p] = src[k];
+        perm[p] = k;
+    }
+    free(next);
+    return ORACLE_OK;
+}
+
+/* GCN normalisation (the GCN operator of Section 2, as used by the configs):
+ * on an edge list that already holds the self-loops,
+ *   d_i    = sum of w_k over edges k with target i   (w = 1 when absent),
+ *   dinv_i = 1 / sqrt(d_i), or 0 when d_i = 0,
+ *   norm_k = dinv_j * w_k * dinv_i          for edge k = (j -> i),
+ * all in fp64. */
+int oracle_gcn_norm(const int64_t *edge_index, const double *w, int64_t E, int64_t N, double *norm) {
+    if (E < 0 || N < 0 || (E > 0 && (!edge_index || !norm))) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    double *d = (double *)calloc((size_t)(N > 0 ? N : 1), sizeof(double));
+    if (!d) return ORACLE_ERR_ARG;
+    for (int64_t k = 0; k < E; ++k) d[dst[k]] += w ? w[k] : 1.0;
+    for (int64_t i = 0; i < N; ++i) d[i] = d[i] > 0.0 ? 1.0 / sqrt(d[i]) : 0.0;
+    for (int64_t k = 0; k < E; ++k) norm[k] = d[src[k]] * (w ? w[k] : 1.0) * d[dst[k]];
+    free(d);
+    return ORACLE_OK;
+}
+
+/* Shared by propagate and pooling: reduce messages m_k (k = 0..E-1, in
+ * order) into rows tgt[k]. The message of element (k, f) is built by
+ * the caller-supplied source row, weight and (for DIFF) target row. */
+static int reduce_edges(const float *x, int64_t N_src, int64_t F,
+                        const int64_t *src, const int64_t *tgt, int64_t E, int64_t N_out,
+                        const float *w, int msg, int aggr,
+                        double *out, int64_t *argmax, double *sabs, int64_t sentinel) {
+    int64_t *cnt = (int64_t *)calloc((size_t)(N_out > 0 ? N_out : 1), sizeof(int64_t));
+    float *best = (float *)malloc((size_t)((N_out * F) > 0 ? N_out * F : 1) * sizeof(float));
+    if (!cnt || !best) { free(cnt); free(best); return ORACLE_ERR_ARG; }
+    for (int64_t t = 0; t < N_out * F; ++t) {
+        out[t] = 0.0;
+        if (sabs) sabs[t] = 0.0;
+        if (argmax) argmax[t] = sentinel;
+        best[t] = 0.0f;
+    }
+    for (int64_t k = 0; k < E; ++k) {
+        const int64_t j = src[k], i = tgt[k];
+        cnt[i] += 1;
+        for (int64_t f = 0; f < F; ++f) {
+            const float xj = x[j * F + f];
+            const int64_t o = i * F + f;
+            if (aggr == ORACLE_MAX) {
+                float m;
+                if (msg == ORACLE_MSG_DIFF) m = xj - x[i * F + f];
+                else if (w) m = w[k] * xj;
+                else m = xj;
+                if (m == 0.0f) m = 0.0f; /* -0.0 -> +0.0 */
+                if (argmax[o] == sentinel || m > best[o]) {
+                    best[o] = m;
+                    argmax[o] = k;
+                }
+            } else {
+                double m;
+                if (msg == ORACLE_MSG_DIFF) m = (double)xj - (double)x[i * F + f];
+                else if (w) m = (double)w[k] * (double)xj;
+                else m = (double)xj;
+                out[o] += m;
+                if (sabs) sabs[o] += fabs(m);
+            }
+        }
+    }
+    for (int64_t i = 0; i < N_out; ++i) {
+        for (int64_t f = 0; f < F; ++f) {
+            const int64_t o = i * F + f;
+            if (aggr == ORACLE_MAX) {
+                out[o] = cnt[i] > 0 ? (double)best[o] : 0.0;
+            } else if (aggr == ORACLE_MEAN && cnt[i] > 0) {
+                out[o] = out[o] / (double)cnt[i];
+                if (sabs) sabs[o] = sabs[o] / (double)cnt[i];
+            }
+        }
+    }
+    free(cnt);
+    free(best);
+    return ORACLE_OK;
+}
+
+static int all_finite(const float *a, int64_t n) {
+    for (int64_t t = 0; t < n; ++t)
+        if (!isfinite(a[t])) return 0;
+    return 1;
+}
+
+/* Propagate, Eq. (1) with gamma = identity:
+ *   out_i = AGG_{k : I[1,k] = i} phi_k,
+ *   phi_k = x_j (SRC), w_k * x_j (SRC with weight), or x_j - x_i (DIFF),
+ * for every feature column. out is fp64 [N,F]; argmax (int64 [N,F], max
+ * only, else may be NULL) holds the winning edge id; sabs (nullable) holds
+ * sum |phi| (divided by the degree for mean). */
+int oracle_propagate(const float *x, int64_t N, int64_t F,
+                     const int64_t *edge_index, int64_t E, const float *w,
+                     int msg, int aggr, double *out, int64_t *argmax, double *sabs) {
+    if (N < 0 || F < 0 || E < 0) return ORACLE_ERR_ARG;
+    if (msg != ORACLE_MSG_SRC && msg != ORACLE_MSG_DIFF) return ORACLE_ERR_ARG;
+    if (aggr != ORACLE_SUM && aggr != ORACLE_MEAN && aggr != ORACLE_MAX) return ORACLE_ERR_ARG;
+    if (msg == ORACLE_MSG_DIFF && w) return ORACLE_ERR_ARG;
+    if (aggr == ORACLE_MAX && N * F > 0 && !argmax) return ORACLE_ERR_ARG;
+    if (N * F > 0 && (!x || !out)) return ORACLE_ERR_ARG;
+    if (E > 0 && !edge_index) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    if (!all_finite(x, N * F) || (w && !all_finite(w, E))) return ORACLE_ERR_NONFINITE;
+    return reduce_edges(x, N, F, src, dst, E, N, w, msg, aggr, out, argmax, sabs, E);
+}
+
+/* Global pooling (Section 2, "Global Pooling" and "Mini-batch Handling"):
+ * out_g = AGG_{n : batch[n] = g} x_n, for B graphs. The assignment vector
+ * batch must be non-decreasing. argmax holds the winning node id, N if the
+ * graph is empty. */
+int oracle_global_pool(const float *x, int64_t N, int64_t F, const int64_t *batch, int64_t B,
+                       int aggr, double *out, int64_t *argmax, double *sabs) {
+    if (N < 0 || F < 0 || B < 0) return ORACLE_ERR_ARG;
+    if (aggr != ORACLE_SUM && aggr != ORACLE_MEAN && aggr != ORACLE_MAX) return ORACLE_ERR_ARG;
+    if (aggr == ORACLE_MAX && B * F > 0 && !argmax) return ORACLE_ERR_ARG;
+    if (N > 0 && !batch) return ORACLE_ERR_ARG;
+    if (B * F > 0 && !out) return ORACLE_ERR_ARG;
+    if (check_index_range(batch, N, B)) return ORACLE_ERR_INDEX;
+    for (int64_t n = 1; n < N; ++n)
+        if (batch[n] < batch[n - 1]) return ORACLE_ERR_ARG;
+    if (!all_finite(x, N * F)) return ORACLE_ERR_NONFINITE;
+    int64_t *node = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+    if (!node) return ORACLE_ERR_ARG;
+    for (int64_t n = 0; n < N; ++n) node[n] = n;
+    int rc = reduce_edges(x, N, F, node, batch, N, B, NULL, ORACLE_MSG_SRC, aggr, out, argmax, sabs, N);
+    free(node);
+    return rc;
+}

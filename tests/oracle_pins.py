@@ -1,0 +1,332 @@
+"""Pins that tie the oracle to something other than itself.
+
+Each pin checks the oracle against an independent source: hand-derived
+values (tests/golden/tiny_hand.json), dense linear algebra in numpy,
+CPU torch scatter routines, closed forms and invariants of Eq. (1).
+Every pin is a function of the oracle library handle, so the mutation test
+can run the same pins against deliberately broken copies of the oracle.
+"""
+from __future__ import annotations
+
+import json
+import os
+
+import numpy as np
+import torch
+
+import oracle
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "tiny_hand.json")
+
+
+def golden():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+def dense_adjacency(ei, N, w=None):
+    """A[i, j] = sum of weights of edges j -> i (dense fp64)."""
+    A = np.zeros((N, N))
+    np.add.at(A, (ei[1], ei[0]), 1.0 if w is None else np.asarray(w, np.float64))
+    return A
+
+
+def circulant(N, half_k):
+    """k-regular symmetric graph (k = 2 half_k): i -> i +- 1..half_k mod N."""
+    src, dst = [], []
+    for i in range(N):
+        for s in range(1, half_k + 1):
+            for j in ((i + s) % N, (i - s) % N):
+                src.append(j)
+                dst.append(i)
+    return np.array([src, dst], np.int64)
+
+
+def small_cases():
+    """Tiny random multigraphs with duplicates, self-loops and isolated nodes."""
+    rng = np.random.default_rng(1234)
+    cases = []
+    for N, E in ((1, 0), (1, 3), (5, 0), (7, 20), (16, 60), (33, 200), (64, 90)):
+        F = int(rng.integers(1, 6))
+        ei = synth.random_coo(rng, N, E)
+        x = rng.standard_normal((N, F)).astype(np.float32)
+        w = rng.standard_normal(E).astype(np.float32)
+        cases.append((N, F, ei, x, w))
+    return cases
+
+
+# ----------------------------------------------------------------- pins
+
+def pin_golden_propagate(lib):
+    g = golden()["propagate"]
+    x = np.array(g["x"], np.float32)
+    ei = np.array(g["edge_index"], np.int64)
+    w = np.array(g["edge_weight"], np.float32)
+    N = g["N"]
+    assert (oracle.degree(ei, N, lib=lib) == np.array(g["degree"])).all()
+    rp, col, perm = oracle.coo_to_csr(ei, N, lib=lib)
+    assert (rp == g["csr_rowptr"]).all() and (col == g["csr_col"]).all() and (perm == g["csr_perm"]).all()
+    out, _, _ = oracle.propagate(x, ei, aggr="sum", lib=lib)
+    assert np.array_equal(out, np.array(g["src_sum"]))
+    out, _, _ = oracle.propagate(x, ei, aggr="mean", lib=lib)
+    assert np.allclose(out * 3.0, np.array(g["src_mean_times_3"]), rtol=1e-15, atol=0)
+    out, arg, _ = oracle.propagate(x, ei, aggr="max", lib=lib)
+    assert np.array_equal(out, np.array(g["src_max"])) and np.array_equal(arg, np.array(g["src_argmax"]))
+    out, _, _ = oracle.propagate(x, ei, w, aggr="sum", lib=lib)
+    assert np.array_equal(out, np.array(g["weighted_sum"]))
+    out, arg, _ = oracle.propagate(x, ei, w, aggr="max", lib=lib)
+    assert np.array_equal(out, np.array(g["weighted_max"])) and np.array_equal(arg, np.array(g["weighted_argmax"]))
+    out, _, _ = oracle.propagate(x, ei, msg="diff", aggr="sum", lib=lib)
+    assert np.array_equal(out, np.array(g["diff_sum"]))
+    out, arg, _ = oracle.propagate(x, ei, msg="diff", aggr="max", lib=lib)
+    assert np.array_equal(out, np.array(g["diff_max"])) and np.array_equal(arg, np.array(g["diff_argmax"]))
+
+
+def pin_golden_pool(lib):
+    g = golden()
+    x = np.array(g["propagate"]["x"], np.float32)
+    p = g["pool"]
+    batch = np.array(p["batch"], np.int64)
+    for aggr in ("sum", "mean", "max"):
+        out, arg, _ = oracle.global_pool(x, batch, p["B"], aggr, lib=lib)
+        assert np.array_equal(out, np.array(p[aggr])), aggr
+        if aggr == "max":
+            assert np.array_equal(arg, np.array(p["argmax"]))
+
+
+def pin_golden_gcn_norm(lib):
+    g = golden()["gcn_norm_path3"]
+    ei = np.array(g["edge_index"], np.int64)
+    norm = oracle.gcn_norm(ei, g["N"], lib=lib)
+    assert np.allclose(norm * norm, g["norm_squared"], rtol=1e-14, atol=0)
+    assert np.allclose(norm, g["norm"], rtol=1e-14, atol=0)
+
+
+def pin_golden_gcn_norm_directed(lib):
+    g = golden()["gcn_norm_directed"]
+    ei = np.array(g["edge_index"], np.int64)
+    norm = oracle.gcn_norm(ei, g["N"], lib=lib)
+    assert np.allclose(norm * norm, g["norm_squared"], rtol=1e-14, atol=0)
+    assert np.array_equal(oracle.degree(ei, g["N"], lib=lib), g["degree_with_loops"])
+
+
+def pin_golden_signed_zero(lib):
+    g = golden()["signed_zero_max"]
+    x = np.array(g["x"], np.float32)
+    ei = np.array(g["edge_index"], np.int64)
+    out, arg, _ = oracle.propagate(x, ei, aggr="max", lib=lib)
+    assert np.array_equal(out, np.array(g["max"])) and np.array_equal(arg, np.array(g["argmax"]))
+    assert not np.signbit(out[2, 0])
+
+
+def pin_degree_and_csr_library(lib):
+    """np.bincount and a stable argsort are independent definitions."""
+    for N, F, ei, x, w in small_cases():
+        deg = oracle.degree(ei, N, lib=lib)
+        assert np.array_equal(deg, np.bincount(ei[1], minlength=N))
+        assert deg.sum() == ei.shape[1]
+        rp, col, perm = oracle.coo_to_csr(ei, N, lib=lib)
+        ref_perm = np.argsort(ei[1], kind="stable")
+        assert np.array_equal(perm, ref_perm)
+        assert np.array_equal(col, ei[0][ref_perm])
+        assert np.array_equal(rp, np.concatenate([[0], np.cumsum(np.bincount(ei[1], minlength=N))]))
+
+
+def pin_sum_mean_dense(lib):
+    """Sum = dense A @ X (fp64 matmul); mean = D^-1 A X; weighted and diff forms."""
+    for N, F, ei, x, w in small_cases():
+        x64 = x.astype(np.float64)
+        deg = np.bincount(ei[1], minlength=N).astype(np.float64)
+        for weighted in (False, True):
+            A = dense_adjacency(ei, N, w if weighted else None)
+            ref = A @ x64
+            out, _, sabs = oracle.propagate(x, ei, w if weighted else None, aggr="sum", lib=lib)
+            assert np.allclose(out, ref, rtol=1e-12, atol=1e-12)
+            Aabs = dense_adjacency(ei, N, np.abs(w) if weighted else None)
+            assert np.allclose(sabs, Aabs @ np.abs(x64), rtol=1e-12, atol=1e-12)
+            out, _, _ = oracle.propagate(x, ei, w if weighted else None, aggr="mean", lib=lib)
+            ref_mean = np.where(deg[:, None] > 0, ref / np.maximum(deg, 1)[:, None], 0.0)
+            assert np.allclose(out, ref_mean, rtol=1e-12, atol=1e-12)
+        # diff: sum_j (x_j - x_i) = A x - deg * x_i
+        A = dense_adjacency(ei, N)
+        out, _, _ = oracle.propagate(x, ei, msg="diff", aggr="sum", lib=lib)
+        assert np.allclose(out, A @ x64 - deg[:, None] * x64, rtol=1e-12, atol=1e-12)
+
+
+def pin_torch_scatter(lib):
+    """CPU torch index_add_ / scatter_reduce give sum, mean and amax."""
+    for N, F, ei, x, w in small_cases():
+        E = ei.shape[1]
+        xt = torch.from_numpy(x.astype(np.float64))
+        msg = xt[torch.from_numpy(ei[0])] * torch.from_numpy(w.astype(np.float64))[:, None]
+        idx = torch.from_numpy(ei[1])
+        ref = torch.zeros(N, F, dtype=torch.float64).index_add_(0, idx, msg).numpy()
+        out, _, _ = oracle.propagate(x, ei, w, aggr="sum", lib=lib)
+        assert np.allclose(out, ref, rtol=1e-12, atol=1e-12)
+        ref = torch.zeros(N, F, dtype=torch.float64).scatter_reduce(
+            0, idx[:, None].expand(E, F), msg, "mean", include_self=False).numpy()
+        out, _, _ = oracle.propagate(x, ei, w, aggr="mean", lib=lib)
+        assert np.allclose(out, ref, rtol=1e-12, atol=1e-12)
+        m32 = torch.from_numpy(x)[torch.from_numpy(ei[0])]
+        ref = torch.zeros(N, F, dtype=torch.float32).scatter_reduce(
+            0, idx[:, None].expand(E, F), m32, "amax", include_self=False).numpy()
+        out, _, _ = oracle.propagate(x, ei, aggr="max", lib=lib)
+        assert np.array_equal(out.astype(np.float32), ref)
+
+
+def pin_max_bruteforce(lib):
+    """Max/argmax by scanning a masked message tensor; lowest edge id wins ties."""
+    rng = np.random.default_rng(99)
+    for N, F, ei, x, w in small_cases():
+        # quantise features so that exact ties occur often
+        xq = np.round(x * 2).astype(np.float32) * np.float32(0.5)
+        E = ei.shape[1]
+        for kind in ("src", "weighted", "diff"):
+            if kind == "src":
+                m = xq[ei[0]]
+            elif kind == "weighted":
+                wq = np.round(w * 2).astype(np.float32) * np.float32(0.5)
+                m = (wq[:, None] * xq[ei[0]]).astype(np.float32)
+            else:
+                m = (xq[ei[0]] - xq[ei[1]]).astype(np.float32)
+            m = np.where(m == 0, np.float32(0), m)
+            ref = np.zeros((N, F), np.float32)
+            ref_arg = np.full((N, F), E, np.int64)
+            for i in range(N):
+                ks = np.nonzero(ei[1] == i)[0]
+                if ks.size:
+                    sub = m[ks]
+                    ref[i] = sub.max(axis=0)
+                    ref_arg[i] = ks[np.argmax(sub == ref[i][None, :], axis=0)]
+            out, arg, _ = oracle.propagate(
+                xq, ei, wq if kind == "weighted" else None,
+                msg="diff" if kind == "diff" else "src", aggr="max", lib=lib)
+            assert np.array_equal(out.astype(np.float32), ref), kind
+            assert np.array_equal(arg, ref_arg), kind
+            has = arg < E
+            if has.any():
+                fidx = np.broadcast_to(np.arange(F), arg.shape)
+                assert np.array_equal(m[arg[has], fidx[has]], out.astype(np.float32)[has])
+    del rng
+
+
+def pin_gcn_norm_closed_forms(lib):
+    """k-regular + self-loops gives 1/(k+1); symmetry; dense D^-1/2 (A) D^-1/2;
+    and the eigen-identity  A_hat sqrt(d) = sqrt(d)."""
+    for N, hk in ((5, 1), (12, 2), (40, 3)):
+        ei = synth.with_self_loops(circulant(N, hk), N)
+        norm = oracle.gcn_norm(ei, N, lib=lib)
+        assert np.allclose(norm, 1.0 / (2 * hk + 1), rtol=1e-15, atol=0)
+    rng = np.random.default_rng(7)
+    for N, M in ((6, 5), (30, 60), (80, 200)):
+        pairs = synth.uniform_pairs(N, M, rng)
+        ei = synth.with_self_loops(synth.symmetrize(pairs), N)
+        for weighted in (False, True):
+            w = rng.uniform(0.5, 2.0, M) if weighted else None
+            wfull = None if w is None else np.concatenate([w, w, np.ones(N)])
+            norm = oracle.gcn_norm(ei, N, wfull, lib=lib)
+            A = dense_adjacency(ei, N, wfull)
+            d = A.sum(axis=1)
+            Dm = np.diag(1.0 / np.sqrt(d))
+            Ahat = Dm @ A @ Dm
+            ref = Ahat[ei[1], ei[0]] / A[ei[1], ei[0]] * (1.0 if wfull is None else wfull)
+            assert np.allclose(norm, ref, rtol=1e-13, atol=0)
+            # symmetry: edge u->v and v->u share the norm
+            E2 = 2 * M
+            assert np.allclose(norm[:M], norm[M:E2], rtol=1e-15, atol=0)
+            # eigen-identity through the oracle's own propagate
+            x = np.repeat(np.sqrt(d)[:, None], 3, axis=1).astype(np.float32)
+            out, _, sabs = oracle.propagate(x, ei, norm.astype(np.float32), aggr="sum", lib=lib)
+            assert np.allclose(out, np.sqrt(d)[:, None], rtol=2e-6, atol=0)
+    # isolated node (no self-loop) -> its outgoing edges get norm 0
+    ei = np.array([[0, 1], [1, 1]], np.int64)
+    norm = oracle.gcn_norm(ei, 3, lib=lib)
+    assert norm[0] == 0.0 and abs(norm[1] - 0.5) <= 1e-15
+
+
+def pin_invariants(lib):
+    """Permutation invariance, sum = mean * deg, isolated nodes, block-diagonal
+    batching (no messages between disconnected graphs) and the DIFF identity."""
+    rng = np.random.default_rng(5)
+    for N, F, ei, x, w in small_cases():
+        E = ei.shape[1]
+        p = rng.permutation(E)
+        eip, wp = ei[:, p], w[p]
+        s1, _, _ = oracle.propagate(x, ei, w, aggr="sum", lib=lib)
+        s2, _, _ = oracle.propagate(x, eip, wp, aggr="sum", lib=lib)
+        assert np.allclose(s1, s2, rtol=1e-12, atol=1e-12)
+        m1, _, _ = oracle.propagate(x, ei, w, aggr="mean", lib=lib)
+        deg = np.bincount(ei[1], minlength=N)
+        assert np.allclose(m1 * deg[:, None], s1, rtol=1e-12, atol=1e-12)
+        mx1, a1, _ = oracle.propagate(x, ei, w, aggr="max", lib=lib)
+        mx2, a2, _ = oracle.propagate(x, eip, wp, aggr="max", lib=lib)
+        assert np.array_equal(mx1, mx2)
+        # random normal data has no ties: the winning edge maps through p
+        ok = a2 < E
+        assert np.array_equal(p[a2[ok]], a1[ok]) and np.array_equal(a1[~ok], a2[~ok])
+        iso = deg == 0
+        for aggr in ("sum", "mean", "max"):
+            o, a, _ = oracle.propagate(x, ei, w, aggr=aggr, lib=lib)
+            assert (o[iso] == 0).all() and not np.signbit(o[iso]).any()
+            if aggr == "max":
+                assert (a[iso] == E).all()
+        # diff mean = mean(x_j) - x_i where deg > 0
+        md, _, _ = oracle.propagate(x, ei, msg="diff", aggr="mean", lib=lib)
+        ms, _, _ = oracle.propagate(x, ei, aggr="mean", lib=lib)
+        has = deg > 0
+        assert np.allclose(md[has], ms[has] - x[has].astype(np.float64), rtol=1e-12, atol=1e-12)
+    # block-diagonal batch = concatenation of per-graph results
+    parts, xs, off = [], [], 0
+    for n, e in ((5, 9), (1, 0), (8, 20), (3, 4)):
+        parts.append(synth.random_coo(rng, n, e) + off)
+        xs.append(rng.standard_normal((n, 3)).astype(np.float32))
+        off += n
+    ei = np.concatenate(parts, axis=1)
+    x = np.concatenate(xs)
+    for aggr in ("sum", "mean", "max"):
+        whole, warg, _ = oracle.propagate(x, ei, aggr=aggr, lib=lib)
+        off, eoff = 0, 0
+        for pe, px in zip(parts, xs):
+            n, e = px.shape[0], pe.shape[1]
+            sub, sarg, _ = oracle.propagate(px, pe - off, aggr=aggr, lib=lib)
+            assert np.array_equal(whole[off:off + n], sub)
+            if aggr == "max":
+                got = warg[off:off + n]
+                assert np.array_equal(np.where(sarg == e, ei.shape[1], sarg + eoff), got)
+            off += n
+            eoff += e
+
+
+def pin_pool_relations(lib):
+    """Pooling equals propagate over the bipartite edges n -> N + batch[n];
+    sum over graphs = column sums; one graph = a full reduction."""
+    rng = np.random.default_rng(11)
+    for sizes in ((3, 0, 4, 1), (1,), (10, 7, 0, 0, 2)):
+        B = len(sizes)
+        batch = np.repeat(np.arange(B), sizes).astype(np.int64)
+        N = batch.size
+        F = 3
+        x = rng.standard_normal((N, F)).astype(np.float32)
+        xe = np.concatenate([x, np.zeros((B, F), np.float32)])
+        ei = np.stack([np.arange(N), N + batch]).astype(np.int64)
+        for aggr in ("sum", "mean", "max"):
+            out, arg, _ = oracle.global_pool(x, batch, B, aggr, lib=lib)
+            ref, rarg, _ = oracle.propagate(xe, ei, aggr=aggr, lib=lib)
+            assert np.array_equal(out, ref[N:])
+            if aggr == "max":
+                assert np.array_equal(arg, rarg[N:])
+        s, _, _ = oracle.global_pool(x, batch, B, "sum", lib=lib)
+        assert np.allclose(s.sum(axis=0), x.astype(np.float64).sum(axis=0), rtol=1e-12, atol=1e-12)
+    x = rng.standard_normal((25, 4)).astype(np.float32)
+    b = np.zeros(25, np.int64)
+    out, _, _ = oracle.global_pool(x, b, 1, "mean", lib=lib)
+    assert np.allclose(out[0], x.astype(np.float64).mean(axis=0), rtol=1e-12)
+    out, arg, _ = oracle.global_pool(x, b, 1, "max", lib=lib)
+    assert np.array_equal(out[0], x.max(axis=0)) and np.array_equal(arg[0], x.argmax(axis=0))
+
+
+ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_golden_gcn_norm_directed,
+            pin_golden_signed_zero,
+            pin_degree_and_csr_library, pin_sum_mean_dense, pin_torch_scatter, pin_max_bruteforce,
+            pin_gcn_norm_closed_forms, pin_invariants, pin_pool_relations]

@@ -1,0 +1,55 @@
+"""Generated workloads have the stated shapes (CPU only)."""
+import numpy as np
+
+import synth
+
+
+def _simple(ei, N):
+    keys = ei[0] * N + ei[1]
+    return np.unique(keys).size == keys.size and not (ei[0] == ei[1]).any()
+
+
+def test_config1_shape():
+    c = synth.make_config(1)
+    assert c["x"].shape == (2708, 16) and c["x"].dtype == np.float32
+    assert c["edge_index"].shape == (2, 10556) and _simple(c["edge_index"], 2708)
+    assert c["edge_index_gcn"].shape == (2, 13264)
+    # symmetric: every edge has its reverse
+    ei = c["edge_index"]
+    assert np.array_equal(np.sort(ei[0] * 2708 + ei[1]), np.sort(ei[1] * 2708 + ei[0]))
+
+
+def test_config2_shape():
+    c = synth.make_config(2)
+    assert c["edge_index"].shape == (2, 88648) and _simple(c["edge_index"], 19717)
+    assert c["edge_index_gcn"].shape == (2, 108365)
+    assert c["x64"].shape == (19717, 64) and c["x500"].shape == (19717, 500)
+    deg = np.bincount(c["edge_index"][1], minlength=19717)
+    assert deg.max() > 50 * np.median(deg[deg > 0])  # heavy tail
+
+
+def test_config3_shape():
+    c = synth.make_config(3)
+    assert c["B"] == 128 and c["batch"].shape == (c["N"],)
+    assert (np.diff(c["batch"]) >= 0).all() and c["sizes"].min() >= 10 and c["sizes"].max() <= 40
+    ei = c["edge_index"]
+    assert (c["batch"][ei[0]] == c["batch"][ei[1]]).all()  # block-diagonal
+    assert 1.5 < ei.shape[1] / 2 / c["N"] < 3.0
+
+
+def test_config4_shape():
+    c = synth.make_config(4)
+    ei = c["edge_index"]
+    assert ei.shape == (2, 262144) and c["x"].shape == (16384, 64)
+    assert (np.bincount(ei[1], minlength=16384) == 16).all()
+    assert ((ei[0] // 1024) == (ei[1] // 1024)).all() and not (ei[0] == ei[1]).any()
+    es = c["edge_index_shuffled"]
+    assert np.array_equal(np.sort(es[0] * 16384 + es[1]), np.sort(ei[0] * 16384 + ei[1]))
+
+
+def test_config5_recipe_small():
+    c = synth.config5_large_power_law(pairs=200_000, N=5000, F=8)
+    ei = c["edge_index_gcn"]
+    assert ei.shape == (2, 400_000 + 5000)
+    assert _simple(ei[:, ~(ei[0] == ei[1])], 5000)
+    assert (ei[0] == ei[1]).sum() == 5000
