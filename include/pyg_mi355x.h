@@ -1,0 +1,182 @@
+/*
+ * pyg_mi355x.h -- C ABI of the MI355X (gfx950) message-passing library.
+ *
+ * The library computes the propagate path of PyTorch Geometric (Fey &
+ * Lenssen, "Fast Graph Representation Learning with PyTorch Geometric",
+ * 2019): an edge-parallel gather of source-node features followed by a
+ * permutation-invariant scatter-reduce into target nodes, Eq. (1) of
+ * Section 2 with gamma = identity, plus the preprocessing and readout steps
+ * that use the same reduce.
+ *
+ * Graph format (Section 2, "Overview"): G = (X, (I, E)).
+ *   x           node features [N, F], row-major, fp32 or bf16.
+ *   edge_index  I in COO form, int64 [2, E], row-major: row 0 = source j,
+ *               row 1 = target i; edge k carries phi(x_i, x_j, e_{j,i}) to i.
+ *   edge_weight one scalar edge feature per edge (D = 1), fp32 [E], optional.
+ *
+ * Conventions shared by every call:
+ *   - Every array pointer is a DEVICE pointer (hipMalloc'd, coarse-grained),
+ *     owned by the caller. The library never allocates memory; scratch space
+ *     comes from the caller through (ws, ws_bytes), sized by the matching
+ *     *_workspace query. A too-small workspace returns PYG_ERR_WORKSPACE.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream). All calls
+ *     are asynchronous on that stream. Argument errors are detected on the
+ *     host and returned before any device work is enqueued; PYG_ERR_HIP means
+ *     a launch failed. Faults inside kernels surface at the caller's next
+ *     synchronisation.
+ *   - Outputs are fully overwritten, never accumulated into.
+ *   - Node ids must lie in [0, N). Out-of-range ids are undefined behaviour
+ *     unless rejected beforehand with pyg_validate_coo / pyg_validate_batch.
+ *   - Sizes: N < 2^31 and E < 2^31 (int32 CSR columns and positions);
+ *     larger sizes return PYG_ERR_UNSUPPORTED. N = 0, E = 0 or F = 0 are
+ *     valid.
+ *   - Calls are stateless and reentrant; concurrent calls on different
+ *     streams must not share a workspace.
+ */
+#ifndef PYG_MI355X_H
+#define PYG_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PYG_OK = 0,
+    PYG_ERR_INVALID_ARG = -1, /* NULL / negative / inconsistent argument */
+    PYG_ERR_INDEX_RANGE = -2, /* reserved for range failures reported by validation wrappers */
+    PYG_ERR_WORKSPACE = -3,   /* ws_bytes below the *_workspace size */
+    PYG_ERR_HIP = -4,         /* a HIP launch or runtime call failed */
+    PYG_ERR_UNSUPPORTED = -5  /* size or combination outside the supported range */
+} pyg_status;
+
+typedef enum { PYG_F32 = 0, PYG_BF16 = 1 } pyg_dtype;
+
+/* The permutation-invariant aggregation of Eq. (1): sum, mean or max. */
+typedef enum { PYG_SUM = 0, PYG_MEAN = 1, PYG_MAX = 2 } pyg_aggr;
+
+/* The message function phi of Eq. (1):
+ *   PYG_MSG_SRC   phi = x_j, or w_k * x_j when a weight is given;
+ *   PYG_MSG_DIFF  phi = x_j - x_i (the EdgeConv message, Section 2). */
+typedef enum { PYG_MSG_SRC = 0, PYG_MSG_DIFF = 1 } pyg_msg;
+
+/* Kernel choice (Appendix A contrasts the two schemes):
+ *   PYG_KERNEL_COO_ATOMIC   gather/scatter over the unsorted COO with
+ *                           hardware atomics; needs no preprocessing;
+ *   PYG_KERNEL_CSR_SEGMENT  target-sorted (CSR) segment reduction; needs the
+ *                           CSR built once by pyg_coo_to_csr; deterministic;
+ *   PYG_KERNEL_AUTO         CSR when a CSR is passed, else COO. */
+typedef enum { PYG_KERNEL_AUTO = 0, PYG_KERNEL_COO_ATOMIC = 1, PYG_KERNEL_CSR_SEGMENT = 2 } pyg_kernel;
+
+/* A target-sorted CSR built by pyg_coo_to_csr (device pointers).
+ *   rowptr [N+1]  rowptr[i]..rowptr[i+1] are the CSR slots of target i;
+ *   col    [E]    source node of each slot;
+ *   perm   [E]    COO edge id of each slot (ascending inside a row);
+ *   weight [E]    CSR-ordered edge weight, or NULL when unweighted;
+ *   chunk         edges per work unit of the segment kernel, 0 = default. */
+typedef struct {
+    const int64_t *rowptr;
+    const int32_t *col;
+    const int64_t *perm;
+    const float *weight;
+    int64_t N;
+    int64_t E;
+    int64_t chunk;
+} pyg_csr;
+
+/* Human-readable text for a status code (static storage, never NULL). */
+const char *pyg_strerror(int status);
+
+/* ABI version of this header (incremented on incompatible change). */
+int pyg_abi_version(void);
+
+/* In-degree deg[i] = number of edges whose target is i, counted with
+ * multiplicity (|N(i)| in Eq. (1); the denominator of mean).
+ *   edge_index int64 [2,E] (device), deg int64 [N] (device, output). */
+int pyg_degree(const int64_t *edge_index, int64_t E, int64_t N, int64_t *deg, void *stream);
+
+/* Workspace bytes needed by pyg_coo_to_csr for (E, N). */
+int pyg_coo_to_csr_workspace(int64_t E, int64_t N, size_t *bytes);
+
+/* Target-sorted CSR of the COO edge list (the row-ordered, "coalesced"
+ * layout of Appendix A, built once as preprocessing). The sort is stable:
+ * inside a row the slots keep ascending COO edge id, so the result is
+ * unique and bit-reproducible.
+ *   edge_index  int64 [2,E]        input;
+ *   edge_weight fp32 [E] or NULL   input, COO order;
+ *   rowptr      int64 [N+1]        output;
+ *   col         int32 [E]          output;
+ *   perm        int64 [E]          output;
+ *   weight_csr  fp32 [E] or NULL   output, = edge_weight[perm] (requires
+ *                                  edge_weight, ignored when it is NULL). */
+int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, const float *edge_weight,
+                   int64_t *rowptr, int32_t *col, int64_t *perm, float *weight_csr,
+                   void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_gcn_norm for N nodes. */
+int pyg_gcn_norm_workspace(int64_t N, size_t *bytes);
+
+/* GCN edge normalisation for the GCN operator of Section 2, on an edge list
+ * that already contains the self-loops:
+ *   d_i = sum of w_k over edges with target i (w = 1 when edge_weight is NULL),
+ *   norm_k = d_j^-1/2 * w_k * d_i^-1/2 for edge k = (j -> i), 0 where d = 0.
+ * Computed in fp64 and rounded once to fp32.
+ *   norm fp32 [E] output in COO order. */
+int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight, int64_t E, int64_t N,
+                 float *norm, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_propagate for this shape, aggregation and
+ * kernel (pass the same chunk as csr->chunk; 0 = default). */
+int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int kernel,
+                            int64_t chunk, size_t *bytes);
+
+/* Propagate, Eq. (1) of Section 2 with gamma = identity:
+ *   out[i, f] = AGG over edges k = (j -> i) of phi_k[f],
+ * phi from `msg` (w_k * x_j when a weight is given), AGG from `aggr`.
+ *   x           [N,F] fp32 or bf16 (dtype), 16-byte aligned rows give the
+ *               vector path (F * sizeof(dtype) % 16 == 0), otherwise scalar;
+ *   edge_index  [2,E] COO (required by the COO kernel; may be NULL for CSR);
+ *   edge_weight fp32 [E] COO order or NULL. With the CSR kernel the weights
+ *               are read from csr->weight, which must be non-NULL exactly
+ *               when edge_weight is non-NULL. Not allowed with PYG_MSG_DIFF;
+ *   csr         CSR from pyg_coo_to_csr or NULL;
+ *   out         [N,F] in x's dtype; fp32 accumulation, one rounding to bf16;
+ *   argmax      int64 [N,F], required for PYG_MAX and NULL otherwise: the COO
+ *               edge id of the winning message.
+ * Semantics: an empty neighbourhood gives 0 and argmax = E. mean divides by
+ * the number of incoming edges. max compares fp32 messages with -0.0 taken
+ * as +0.0; equal maxima resolve to the lowest edge id. Max, argmax and every
+ * CSR result are bit-reproducible; COO sum/mean use float atomics and may
+ * differ in the last bits between runs (Appendix A notes the same of GPU
+ * scatter). `out` must not overlap `x`. */
+int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F,
+                  const int64_t *edge_index, int64_t E, const float *edge_weight,
+                  const pyg_csr *csr, int msg, int aggr, int kernel,
+                  void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_global_pool. */
+int pyg_global_pool_workspace(int dtype, int64_t N, int64_t F, int64_t B, int aggr, size_t *bytes);
+
+/* Global pooling (Section 2, "Global Pooling" with the assignment vector of
+ * "Mini-batch Handling"): out[g, f] = AGG over nodes n with batch[n] = g of
+ * x[n, f], for B graphs.
+ *   batch int64 [N], non-decreasing, values in [0, B);
+ *   out   [B,F] in x's dtype; argmax int64 [B,F] (PYG_MAX only): node id,
+ *         N for an empty graph. */
+int pyg_global_pool(const void *x, int dtype, int64_t N, int64_t F, const int64_t *batch, int64_t B,
+                    int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
+
+/* Count COO entries outside [0, N) into *bad_count (int64, device). */
+int pyg_validate_coo(const int64_t *edge_index, int64_t E, int64_t N, int64_t *bad_count, void *stream);
+
+/* Count batch entries outside [0, B) or smaller than their predecessor into
+ * *bad_count (int64, device). */
+int pyg_validate_batch(const int64_t *batch, int64_t N, int64_t B, int64_t *bad_count, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PYG_MI355X_H */

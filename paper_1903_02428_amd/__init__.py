@@ -1,0 +1,31 @@
+"""MI355X (gfx950) propagate path of PyTorch Geometric, as a C-ABI HIP library.
+
+This package is a thin Python binding over ``libpyg_mi355x.so``: it checks
+tensor arguments, marshals pointers through ctypes and passes torch's current
+HIP stream. Every step of the computation runs in the library's own HIP
+kernels; PyTorch only provides device memory and streams. There is no CPU
+fallback: without the built library every call raises.
+
+The C entry points and their semantics are documented in
+``include/pyg_mi355x.h``; the names here mirror them without the ``pyg_``
+prefix.
+"""
+from __future__ import annotations
+
+from .binding import (  # noqa: F401
+    CSR,
+    LibraryMissing,
+    PygError,
+    abi_version,
+    coo_to_csr,
+    degree,
+    gcn_norm,
+    global_pool,
+    library,
+    library_path,
+    propagate,
+    propagate_workspace_bytes,
+    strerror,
+    validate_batch,
+    validate_coo,
+)

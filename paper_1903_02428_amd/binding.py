@@ -1,0 +1,270 @@
+"""ctypes binding of libpyg_mi355x.so (argument marshalling only)."""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch  # loads the HIP runtime the library must share, before the library itself
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_NAME = "libpyg_mi355x.so"
+
+PYG_OK = 0
+DTYPE = {torch.float32: 0, torch.bfloat16: 1}
+AGGR = {"sum": 0, "mean": 1, "max": 2}
+MSG = {"src": 0, "diff": 1}
+KERNEL = {"auto": 0, "coo": 1, "csr": 2}
+
+EXPORTED = [
+    "pyg_strerror", "pyg_abi_version", "pyg_degree", "pyg_coo_to_csr_workspace", "pyg_coo_to_csr",
+    "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_propagate_workspace", "pyg_propagate",
+    "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
+]
+
+
+class LibraryMissing(RuntimeError):
+    """The HIP library has not been built (run __graft_entry__.build())."""
+
+
+class PygError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {strerror(status)} (status {status})")
+        self.status = status
+
+
+class _Csr(ctypes.Structure):
+    _fields_ = [("rowptr", ctypes.c_void_p), ("col", ctypes.c_void_p), ("perm", ctypes.c_void_p),
+                ("weight", ctypes.c_void_p), ("N", ctypes.c_int64), ("E", ctypes.c_int64),
+                ("chunk", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return os.path.join(_HERE, LIB_NAME)
+
+
+def library() -> ctypes.CDLL:
+    """Load the library (once). Raises LibraryMissing if it was never built."""
+    global _lib
+    if _lib is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise LibraryMissing(f"{path} not found: build it with paper_1903_02428_amd.build.build()")
+        lib = ctypes.CDLL(path)
+        p, i64, i32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)
+        lib.pyg_strerror.argtypes, lib.pyg_strerror.restype = [i32], ctypes.c_char_p
+        lib.pyg_abi_version.argtypes, lib.pyg_abi_version.restype = [], i32
+        sigs = {
+            "pyg_degree": [p, i64, i64, p, p],
+            "pyg_coo_to_csr_workspace": [i64, i64, sz],
+            "pyg_coo_to_csr": [p, i64, i64, p, p, p, p, p, p, ctypes.c_size_t, p],
+            "pyg_gcn_norm_workspace": [i64, sz],
+            "pyg_gcn_norm": [p, p, i64, i64, p, p, ctypes.c_size_t, p],
+            "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
+            "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
+                              ctypes.c_size_t, p],
+            "pyg_global_pool_workspace": [i32, i64, i64, i64, i32, sz],
+            "pyg_global_pool": [p, i32, i64, i64, p, i64, i32, p, p, p, ctypes.c_size_t, p],
+            "pyg_validate_coo": [p, i64, i64, p, p],
+            "pyg_validate_batch": [p, i64, i64, p, p],
+        }
+        for name, args in sigs.items():
+            fn = getattr(lib, name)
+            fn.argtypes, fn.restype = args, i32
+        _lib = lib
+    return _lib
+
+
+def strerror(status: int) -> str:
+    return library().pyg_strerror(int(status)).decode()
+
+
+def abi_version() -> int:
+    return int(library().pyg_abi_version())
+
+
+def _check(rc: int, what: str):
+    if rc != PYG_OK:
+        raise PygError(rc, what)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need_cuda(name, t, dtype=None, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a HIP device, got {t.device}")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _edge_index(edge_index):
+    _need_cuda("edge_index", edge_index, torch.int64, 2)
+    if edge_index.shape[0] != 2:
+        raise ValueError("edge_index must be [2, E]")
+    return edge_index.shape[1]
+
+
+def _workspace(nbytes: int, device):
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def _size(fn, *args) -> int:
+    out = ctypes.c_size_t(0)
+    _check(fn(*args, ctypes.byref(out)), fn.__name__)
+    return int(out.value)
+
+
+@dataclass
+class CSR:
+    """Target-sorted CSR built on the device by pyg_coo_to_csr."""
+    rowptr: torch.Tensor   # int64 [N+1]
+    col: torch.Tensor      # int32 [E]
+    perm: torch.Tensor     # int64 [E]
+    weight: torch.Tensor | None  # fp32 [E] CSR order
+    N: int
+    E: int
+    chunk: int = 0
+
+    def _c(self) -> _Csr:
+        return _Csr(self.rowptr.data_ptr(), self.col.data_ptr() if self.E else None,
+                    self.perm.data_ptr() if self.E else None,
+                    None if self.weight is None else self.weight.data_ptr(), self.N, self.E, self.chunk)
+
+
+def degree(edge_index: torch.Tensor, num_nodes: int) -> torch.Tensor:
+    E = _edge_index(edge_index)
+    deg = torch.empty(num_nodes, dtype=torch.int64, device=edge_index.device)
+    _check(library().pyg_degree(_ptr(edge_index), E, num_nodes, _ptr(deg), _stream(edge_index.device)), "pyg_degree")
+    return deg
+
+
+def coo_to_csr(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None,
+               chunk: int = 0) -> CSR:
+    lib = library()
+    E = _edge_index(edge_index)
+    dev = edge_index.device
+    if edge_weight is not None:
+        _need_cuda("edge_weight", edge_weight, torch.float32, 1)
+        if edge_weight.shape[0] != E:
+            raise ValueError("edge_weight must be [E]")
+    rowptr = torch.empty(num_nodes + 1, dtype=torch.int64, device=dev)
+    col = torch.empty(E, dtype=torch.int32, device=dev)
+    perm = torch.empty(E, dtype=torch.int64, device=dev)
+    wcsr = torch.empty(E, dtype=torch.float32, device=dev) if edge_weight is not None else None
+    nbytes = _size(lib.pyg_coo_to_csr_workspace, E, num_nodes)
+    ws = _workspace(nbytes, dev)
+    _check(lib.pyg_coo_to_csr(_ptr(edge_index), E, num_nodes, _ptr(edge_weight), _ptr(rowptr), _ptr(col),
+                              _ptr(perm), _ptr(wcsr), _ptr(ws), nbytes, _stream(dev)), "pyg_coo_to_csr")
+    return CSR(rowptr, col, perm, wcsr, num_nodes, E, chunk)
+
+
+def gcn_norm(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None) -> torch.Tensor:
+    lib = library()
+    E = _edge_index(edge_index)
+    dev = edge_index.device
+    if edge_weight is not None:
+        _need_cuda("edge_weight", edge_weight, torch.float32, 1)
+    norm = torch.empty(E, dtype=torch.float32, device=dev)
+    nbytes = _size(lib.pyg_gcn_norm_workspace, num_nodes)
+    ws = _workspace(nbytes, dev)
+    _check(lib.pyg_gcn_norm(_ptr(edge_index), _ptr(edge_weight), E, num_nodes, _ptr(norm), _ptr(ws), nbytes,
+                            _stream(dev)), "pyg_gcn_norm")
+    return norm
+
+
+def propagate_workspace_bytes(x: torch.Tensor, E: int, aggr: str, kernel: str, chunk: int = 0) -> int:
+    return _size(library().pyg_propagate_workspace, DTYPE[x.dtype], x.shape[0], x.shape[1], E, AGGR[aggr],
+                 KERNEL[kernel], chunk)
+
+
+def propagate(x: torch.Tensor, edge_index: torch.Tensor | None = None, edge_weight: torch.Tensor | None = None,
+              csr: CSR | None = None, aggr: str = "sum", msg: str = "src", kernel: str = "auto",
+              out: torch.Tensor | None = None, argmax: torch.Tensor | None = None,
+              workspace: torch.Tensor | None = None):
+    """Eq. (1) with gamma = identity. Returns (out, argmax or None)."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    if x.dtype not in DTYPE:
+        raise ValueError("x must be float32 or bfloat16")
+    N, F = x.shape
+    dev = x.device
+    if edge_index is not None:
+        E = _edge_index(edge_index)
+    elif csr is not None:
+        E = csr.E
+    else:
+        raise ValueError("need edge_index or csr")
+    if csr is not None and (csr.N != N or csr.E != E):
+        raise ValueError("csr does not match x / edge_index")
+    if edge_weight is not None:
+        _need_cuda("edge_weight", edge_weight, torch.float32, 1)
+    if aggr not in AGGR or msg not in MSG or kernel not in KERNEL:
+        raise ValueError("bad aggr / msg / kernel")
+    if out is None:
+        out = torch.empty_like(x)
+    if aggr == "max" and argmax is None:
+        argmax = torch.empty((N, F), dtype=torch.int64, device=dev)
+    if aggr != "max":
+        argmax = None
+    use = "coo" if kernel == "coo" or (kernel == "auto" and csr is None) else "csr"
+    chunk = csr.chunk if (csr is not None and use == "csr") else 0
+    nbytes = propagate_workspace_bytes(x, E, aggr, use, chunk)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, dev)
+    c = csr._c() if csr is not None else None
+    rc = lib.pyg_propagate(_ptr(x), DTYPE[x.dtype], N, F, _ptr(edge_index), E, _ptr(edge_weight),
+                           ctypes.byref(c) if c is not None else None, MSG[msg], AGGR[aggr], KERNEL[kernel],
+                           _ptr(out), _ptr(argmax), _ptr(workspace), workspace.numel(), _stream(dev))
+    _check(rc, "pyg_propagate")
+    return out, argmax
+
+
+def global_pool(x: torch.Tensor, batch: torch.Tensor, num_graphs: int, aggr: str = "sum"):
+    """Per-graph readout over a sorted assignment vector. Returns (out, argmax or None)."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    _need_cuda("batch", batch, torch.int64, 1)
+    N, F = x.shape
+    if batch.shape[0] != N:
+        raise ValueError("batch must be [N]")
+    dev = x.device
+    out = torch.empty((num_graphs, F), dtype=x.dtype, device=dev)
+    argmax = torch.empty((num_graphs, F), dtype=torch.int64, device=dev) if aggr == "max" else None
+    nbytes = _size(lib.pyg_global_pool_workspace, DTYPE[x.dtype], N, F, num_graphs, AGGR[aggr])
+    ws = _workspace(nbytes, dev)
+    _check(lib.pyg_global_pool(_ptr(x), DTYPE[x.dtype], N, F, _ptr(batch), num_graphs, AGGR[aggr], _ptr(out),
+                               _ptr(argmax), _ptr(ws), nbytes, _stream(dev)), "pyg_global_pool")
+    return out, argmax
+
+
+def validate_coo(edge_index: torch.Tensor, num_nodes: int) -> int:
+    """Number of edge_index entries outside [0, num_nodes) (synchronises)."""
+    E = _edge_index(edge_index)
+    bad = torch.empty(1, dtype=torch.int64, device=edge_index.device)
+    _check(library().pyg_validate_coo(_ptr(edge_index), E, num_nodes, _ptr(bad), _stream(edge_index.device)),
+           "pyg_validate_coo")
+    return int(bad.item())
+
+
+def validate_batch(batch: torch.Tensor, num_graphs: int) -> int:
+    """Number of batch entries out of range or out of order (synchronises)."""
+    _need_cuda("batch", batch, torch.int64, 1)
+    bad = torch.empty(1, dtype=torch.int64, device=batch.device)
+    _check(library().pyg_validate_batch(_ptr(batch), batch.shape[0], num_graphs, _ptr(bad), _stream(batch.device)),
+           "pyg_validate_batch")
+    return int(bad.item())

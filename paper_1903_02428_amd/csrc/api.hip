@@ -1,0 +1,161 @@
+// C ABI entry points for propagate and global pooling: host-side argument
+// checks, workspace sizing and kernel choice. Every check runs before any
+// device work is enqueued.
+#include "common.hpp"
+
+namespace pyg {
+namespace {
+
+constexpr int64_t kMax32 = int64_t(1) << 31;
+
+bool valid_dtype(int dt) { return dt == PYG_F32 || dt == PYG_BF16; }
+bool valid_aggr(int a) { return a == PYG_SUM || a == PYG_MEAN || a == PYG_MAX; }
+int64_t dtype_size(int dt) { return dt == PYG_BF16 ? 2 : 4; }
+
+bool overlaps(const void *a, int64_t abytes, const void *b, int64_t bbytes) {
+    if (!a || !b || abytes <= 0 || bbytes <= 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + static_cast<uintptr_t>(bbytes) && b0 < a0 + static_cast<uintptr_t>(abytes);
+}
+
+// Graph offsets of a sorted assignment vector: ptr[g] = first n with batch[n] >= g.
+__global__ void k_batch_ptr(const int64_t *__restrict__ batch, int64_t N, int64_t B, int64_t *__restrict__ ptr) {
+    for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g <= B; g += (int64_t)gridDim.x * blockDim.x) {
+        int64_t lo = 0, hi = N;
+        while (lo < hi) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            if (batch[mid] < g) lo = mid + 1;
+            else hi = mid;
+        }
+        ptr[g] = lo;
+    }
+}
+
+}  // namespace
+}  // namespace pyg
+
+using namespace pyg;
+
+extern "C" const char *pyg_strerror(int status) {
+    switch (status) {
+        case PYG_OK: return "success";
+        case PYG_ERR_INVALID_ARG: return "invalid argument";
+        case PYG_ERR_INDEX_RANGE: return "index out of range";
+        case PYG_ERR_WORKSPACE: return "workspace too small";
+        case PYG_ERR_HIP: return "HIP runtime or launch error";
+        case PYG_ERR_UNSUPPORTED: return "unsupported size or combination";
+        default: return "unknown status";
+    }
+}
+
+extern "C" int pyg_abi_version(void) { return 1; }
+
+extern "C" int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int kernel, int64_t chunk,
+                                       size_t *bytes) {
+    if (!bytes || !valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0 || chunk < 0) return PYG_ERR_INVALID_ARG;
+    if (kernel != PYG_KERNEL_AUTO && kernel != PYG_KERNEL_COO_ATOMIC && kernel != PYG_KERNEL_CSR_SEGMENT)
+        return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
+    const size_t coo = coo_workspace(dtype, N, F, aggr);
+    const size_t csr = segment_workspace(E, F, aggr, chunk);
+    *bytes = kernel == PYG_KERNEL_COO_ATOMIC ? coo : (kernel == PYG_KERNEL_CSR_SEGMENT ? csr : (coo > csr ? coo : csr));
+    return PYG_OK;
+}
+
+extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                             const float *edge_weight, const pyg_csr *csr, int msg, int aggr, int kernel, void *out,
+                             int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0) return PYG_ERR_INVALID_ARG;
+    if (msg != PYG_MSG_SRC && msg != PYG_MSG_DIFF) return PYG_ERR_INVALID_ARG;
+    if (kernel != PYG_KERNEL_AUTO && kernel != PYG_KERNEL_COO_ATOMIC && kernel != PYG_KERNEL_CSR_SEGMENT)
+        return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
+    if (msg == PYG_MSG_DIFF && edge_weight) return PYG_ERR_INVALID_ARG;
+    if ((aggr == PYG_MAX) != (argmax != nullptr) && N * F > 0) return PYG_ERR_INVALID_ARG;
+    if (aggr != PYG_MAX && argmax) return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && (!x || !out)) return PYG_ERR_INVALID_ARG;
+    if (E > 0 && N == 0) return PYG_ERR_INVALID_ARG;
+    const int64_t xbytes = N * F * dtype_size(dtype);
+    if (overlaps(x, xbytes, out, xbytes)) return PYG_ERR_INVALID_ARG;
+    if (argmax && (overlaps(argmax, N * F * 8, x, xbytes) || overlaps(argmax, N * F * 8, out, xbytes)))
+        return PYG_ERR_INVALID_ARG;
+    if (kernel == PYG_KERNEL_CSR_SEGMENT && !csr) return PYG_ERR_INVALID_ARG;
+    const bool use_csr = kernel == PYG_KERNEL_CSR_SEGMENT || (kernel == PYG_KERNEL_AUTO && csr);
+    if (use_csr) {
+        if (csr->N != N || csr->E != E || !csr->rowptr || csr->chunk < 0) return PYG_ERR_INVALID_ARG;
+        if (E > 0 && (!csr->col || (aggr == PYG_MAX && !csr->perm))) return PYG_ERR_INVALID_ARG;
+        if ((edge_weight != nullptr) != (csr->weight != nullptr)) return PYG_ERR_INVALID_ARG;
+    } else if (E > 0 && !edge_index) {
+        return PYG_ERR_INVALID_ARG;
+    }
+    size_t need;
+    PYG_TRY(pyg_propagate_workspace(dtype, N, F, E, aggr, use_csr ? PYG_KERNEL_CSR_SEGMENT : PYG_KERNEL_COO_ATOMIC,
+                                    use_csr ? csr->chunk : 0, &need));
+    if (ws_bytes < need || (need > 256 && !ws)) return PYG_ERR_WORKSPACE;
+    if (N * F == 0) return PYG_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!use_csr) return coo_propagate(x, dtype, N, F, edge_index, E, edge_weight, msg, aggr, out, argmax, ws, ws_bytes, s);
+    SegmentArgs a{};
+    a.x = x;
+    a.dtype = dtype;
+    a.F = F;
+    a.rowptr = csr->rowptr;
+    a.col = csr->col;
+    a.weight = edge_weight ? csr->weight : nullptr;
+    a.perm = csr->perm;
+    a.n_rows = N;
+    a.E = E;
+    a.msg = msg;
+    a.aggr = aggr;
+    a.chunk = csr->chunk;
+    a.sentinel = E;
+    a.out = out;
+    a.argmax = argmax;
+    return segment_reduce(a, ws, ws_bytes, s);
+}
+
+extern "C" int pyg_global_pool_workspace(int dtype, int64_t N, int64_t F, int64_t B, int aggr, size_t *bytes) {
+    if (!bytes || !valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || B < 0) return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || B >= kMax32) return PYG_ERR_UNSUPPORTED;
+    *bytes = align_up(static_cast<size_t>(B + 1) * sizeof(int64_t), 256) + segment_workspace(N, F, aggr, 0);
+    return PYG_OK;
+}
+
+extern "C" int pyg_global_pool(const void *x, int dtype, int64_t N, int64_t F, const int64_t *batch, int64_t B, int aggr,
+                               void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || B < 0) return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || B >= kMax32) return PYG_ERR_UNSUPPORTED;
+    if ((aggr == PYG_MAX) != (argmax != nullptr) && B * F > 0) return PYG_ERR_INVALID_ARG;
+    if (aggr != PYG_MAX && argmax) return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && !x) return PYG_ERR_INVALID_ARG;
+    if (B * F > 0 && !out) return PYG_ERR_INVALID_ARG;
+    if (N > 0 && (!batch || B == 0)) return PYG_ERR_INVALID_ARG;
+    const int64_t esz = dtype_size(dtype);
+    if (overlaps(x, N * F * esz, out, B * F * esz)) return PYG_ERR_INVALID_ARG;
+    size_t need;
+    PYG_TRY(pyg_global_pool_workspace(dtype, N, F, B, aggr, &need));
+    if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
+    if (B * F == 0) return PYG_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int64_t *ptr = static_cast<int64_t *>(ws);
+    const size_t ptr_bytes = align_up(static_cast<size_t>(B + 1) * sizeof(int64_t), 256);
+    k_batch_ptr<<<grid_for(B + 1, kBlock), kBlock, 0, s>>>(batch, N, B, ptr);
+    PYG_LAUNCH_CHECK();
+    SegmentArgs a{};
+    a.x = x;
+    a.dtype = dtype;
+    a.F = F;
+    a.rowptr = ptr;
+    a.col = nullptr;   // slot n reads node n
+    a.weight = nullptr;
+    a.perm = nullptr;  // argmax reports the node id
+    a.n_rows = B;
+    a.E = N;
+    a.msg = PYG_MSG_SRC;
+    a.aggr = aggr;
+    a.chunk = 0;
+    a.sentinel = N;
+    a.out = out;
+    a.argmax = argmax;
+    return segment_reduce(a, static_cast<char *>(ws) + ptr_bytes, ws_bytes - ptr_bytes, s);
+}

@@ -1,0 +1,124 @@
+// Shared device/host helpers of the gfx950 propagate library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "pyg_mi355x.h"
+
+namespace pyg {
+
+constexpr int kWave = 64;   // CDNA wavefront width
+constexpr int kBlock = 256; // threads per workgroup for every kernel (4 waves)
+
+#define PYG_LAUNCH_CHECK()                                      \
+    do {                                                        \
+        if (hipGetLastError() != hipSuccess) return PYG_ERR_HIP; \
+    } while (0)
+
+#define PYG_TRY(expr)                  \
+    do {                               \
+        int _rc = (expr);              \
+        if (_rc != PYG_OK) return _rc; \
+    } while (0)
+
+static inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Carves aligned sub-buffers out of one caller workspace.
+struct Carver {
+    char *base;
+    size_t used = 0;
+    explicit Carver(void *p) : base(static_cast<char *>(p)) {}
+    template <typename T>
+    T *take(size_t count) {
+        used = align_up(used, 256);
+        T *p = reinterpret_cast<T *>(base ? base + used : nullptr);
+        used += count * sizeof(T);
+        return p;
+    }
+};
+
+static inline unsigned grid_for(int64_t work, int64_t per_block, int64_t cap = 1 << 20) {
+    int64_t g = (work + per_block - 1) / per_block;
+    if (g < 1) g = 1;
+    if (g > cap) g = cap;
+    return static_cast<unsigned>(g);
+}
+
+// ---------------------------------------------------------------- numerics
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// fp32 -> bf16 with round-to-nearest-even (inputs are finite).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+// Monotone map of finite floats to uint32 (a < b  <=>  key(a) < key(b)).
+__device__ __forceinline__ uint32_t order_key(float f) {
+    uint32_t u = __float_as_uint(f);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float order_key_inv(uint32_t k) {
+    uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+    return __uint_as_float(u);
+}
+
+// -0.0 -> +0.0 so that zeros tie when comparing for max.
+__device__ __forceinline__ float canon_zero(float m) { return m == 0.0f ? 0.0f : m; }
+
+// ------------------------------------------------------------ small kernels
+
+template <typename T>
+__global__ void k_fill(T *__restrict__ p, int64_t n, T v) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+template <typename T>
+static inline int fill(T *p, int64_t n, T v, hipStream_t s) {
+    if (n <= 0) return PYG_OK;
+    k_fill<T><<<grid_for(n, kBlock * 4), kBlock, 0, s>>>(p, n, v);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
+
+// ---------------------------------------------------------- internal API
+
+// Exclusive (or inclusive) prefix sum of n elements; `in` may equal `out`.
+// Scratch: scan_workspace_elems(n) elements of T.
+size_t scan_workspace_elems(int64_t n);
+int scan_u32(const uint32_t *in, uint32_t *out, int64_t n, bool inclusive, uint32_t *ws, hipStream_t s);
+int scan_i64(const int64_t *in, int64_t *out, int64_t n, bool inclusive, int64_t *ws, hipStream_t s);
+
+// Target-sorted segment reduction shared by propagate (CSR) and pooling.
+struct SegmentArgs {
+    const void *x;      // source rows [n_src, F]
+    int dtype;
+    int64_t F;
+    const int64_t *rowptr; // [n_rows + 1]
+    const int32_t *col;    // [E] source row per slot; NULL = identity (slot id)
+    const float *weight;   // [E] or NULL
+    const int64_t *perm;   // [E] id reported by argmax; NULL = slot id
+    int64_t n_rows;
+    int64_t E;
+    int msg;
+    int aggr;
+    int64_t chunk;
+    int64_t sentinel;   // argmax of an empty row
+    void *out;          // [n_rows, F]
+    int64_t *argmax;    // [n_rows, F] or NULL
+};
+int64_t segment_chunk(int64_t E, int64_t requested);
+size_t segment_workspace(int64_t E, int64_t F, int aggr, int64_t chunk);
+int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t s);
+
+// Unsorted-COO gather/scatter with hardware atomics.
+size_t coo_workspace(int dtype, int64_t N, int64_t F, int aggr);
+int coo_propagate(const void *x, int dtype, int64_t N, int64_t F, const int64_t *ei, int64_t E, const float *w, int msg,
+                  int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, hipStream_t s);
+
+}  // namespace pyg

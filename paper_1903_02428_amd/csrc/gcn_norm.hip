@@ -1,0 +1,62 @@
+// GCN edge normalisation (the GCN operator listed in Section 2):
+//   d_i = sum_{k: target(k) = i} w_k,  dinv_i = d_i^-1/2 (0 if d_i = 0),
+//   norm_k = dinv_j * w_k * dinv_i.
+// The degree sums in fp64 hardware atomics; dinv and the edge product are
+// fp64 too, rounded once to fp32 at the end. With unit weights every fp64
+// step is order-independent, so the result is reproducible bit for bit.
+#include "common.hpp"
+
+namespace pyg {
+namespace {
+
+__global__ void k_weighted_degree(const int64_t *__restrict__ dst, const float *__restrict__ w, int64_t E,
+                                  double *__restrict__ d) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < E; k += (int64_t)gridDim.x * blockDim.x)
+        unsafeAtomicAdd(&d[dst[k]], w ? static_cast<double>(w[k]) : 1.0);
+}
+
+__global__ void k_inv_sqrt(double *__restrict__ d, int64_t N) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x) {
+        const double v = d[i];
+        d[i] = v > 0.0 ? 1.0 / sqrt(v) : 0.0;
+    }
+}
+
+__global__ void k_edge_norm(const int64_t *__restrict__ src, const int64_t *__restrict__ dst, const float *__restrict__ w,
+                            int64_t E, const double *__restrict__ dinv, float *__restrict__ norm) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < E; k += (int64_t)gridDim.x * blockDim.x) {
+        const double wk = w ? static_cast<double>(w[k]) : 1.0;
+        norm[k] = static_cast<float>(dinv[src[k]] * wk * dinv[dst[k]]);
+    }
+}
+
+}  // namespace
+}  // namespace pyg
+
+using namespace pyg;
+
+extern "C" int pyg_gcn_norm_workspace(int64_t N, size_t *bytes) {
+    if (N < 0 || !bytes) return PYG_ERR_INVALID_ARG;
+    *bytes = align_up(static_cast<size_t>(N) * sizeof(double), 256) + 256;
+    return PYG_OK;
+}
+
+extern "C" int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight, int64_t E, int64_t N,
+                            float *norm, void *ws, size_t ws_bytes, void *stream) {
+    if (E < 0 || N < 0 || (E > 0 && (!edge_index || !norm || N == 0))) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    size_t need;
+    pyg_gcn_norm_workspace(N, &need);
+    if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
+    if (E == 0) return PYG_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    double *d = static_cast<double *>(ws);
+    PYG_TRY(fill<double>(d, N, 0.0, s));
+    k_weighted_degree<<<grid_for(E, kBlock * 8), kBlock, 0, s>>>(edge_index + E, edge_weight, E, d);
+    PYG_LAUNCH_CHECK();
+    k_inv_sqrt<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(d, N);
+    PYG_LAUNCH_CHECK();
+    k_edge_norm<<<grid_for(E, kBlock * 8), kBlock, 0, s>>>(edge_index, edge_index + E, edge_weight, E, d, norm);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}

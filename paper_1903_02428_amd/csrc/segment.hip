@@ -1,0 +1,465 @@
+// Target-sorted (CSR) segment reduction on gfx950: the propagate kernel
+// that reads a row-ordered edge list, and the same machinery for global
+// pooling (rows = graphs, slots = nodes).
+//
+// Work split: the E CSR slots are cut into equal chunks of `chunk` slots and
+// each 64-lane wavefront owns one chunk, so every wavefront gathers the same
+// number of source rows whatever the degree skew. A row whose degree is at
+// most `chunk` is reduced entirely by the wavefront whose chunk holds its
+// first slot (it may run past the chunk end). A longer row is cut at chunk
+// boundaries; each wavefront writes its piece as a partial and a second
+// kernel folds the pieces in chunk order. Every reduction order is fixed, so
+// results are bit-reproducible.
+//
+// Inside a wavefront: L lanes cover one feature row (16-byte vectors when
+// rows are 16-byte aligned), S = 64 / L sub-groups take successive edges of
+// the row, each lane keeps U gathers in flight, and the sub-groups are
+// combined with a butterfly of cross-lane shuffles. Column indices and
+// weights are read once per 64 edges, coalesced, and handed to sub-groups
+// through ds_bpermute. There is no matrix-core work: aggregation is not a
+// dense contraction.
+#include "common.hpp"
+
+namespace pyg {
+namespace {
+
+struct SegParams {
+    const void *x;
+    int64_t F;      // row stride of x, out and partials (elements)
+    int64_t fbase;  // first feature of this launch's window
+    int64_t fcnt;   // features in the window
+    const int64_t *rowptr;
+    const int32_t *col;
+    const float *w;
+    const int64_t *perm;
+    int64_t n_rows;
+    int64_t E;
+    int64_t chunk;
+    int64_t nchunks;
+    int lg_l;  // log2 of lanes per feature row
+    int mean;
+    int64_t sentinel;
+    void *out;
+    int64_t *argmax;
+    float *part_val;
+    int32_t *part_pos;
+    int32_t *head_row;
+};
+
+// ------------------------------------------------------- lane vector types
+template <typename T, bool VEC> struct Lane;
+template <> struct Lane<float, true> {  // 4 x fp32 = 16 B
+    using R = float4;
+    static constexpr int N = 4;
+    __device__ static R load(const float *p) { return *reinterpret_cast<const R *>(p); }
+    __device__ static R zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+    __device__ static float get(const R &r, int e) { return e == 0 ? r.x : e == 1 ? r.y : e == 2 ? r.z : r.w; }
+    __device__ static void store(float *p, const float (&v)[N]) { *reinterpret_cast<R *>(p) = make_float4(v[0], v[1], v[2], v[3]); }
+};
+template <> struct Lane<uint16_t, true> {  // 8 x bf16 = 16 B
+    using R = uint4;
+    static constexpr int N = 8;
+    __device__ static R load(const uint16_t *p) { return *reinterpret_cast<const R *>(p); }
+    __device__ static R zero() { return make_uint4(0, 0, 0, 0); }
+    __device__ static float get(const R &r, int e) {
+        const uint32_t w = (e >> 1) == 0 ? r.x : (e >> 1) == 1 ? r.y : (e >> 1) == 2 ? r.z : r.w;
+        return (e & 1) ? __uint_as_float(w & 0xFFFF0000u) : __uint_as_float(w << 16);
+    }
+    __device__ static void store(uint16_t *p, const float (&v)[N]) {
+        uint32_t o[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = uint32_t(f32_to_bf16_rne(v[2 * i])) | (uint32_t(f32_to_bf16_rne(v[2 * i + 1])) << 16);
+        *reinterpret_cast<R *>(p) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+};
+template <> struct Lane<float, false> {
+    using R = float;
+    static constexpr int N = 1;
+    __device__ static R load(const float *p) { return *p; }
+    __device__ static R zero() { return 0.f; }
+    __device__ static float get(const R &r, int) { return r; }
+    __device__ static void store(float *p, const float (&v)[N]) { *p = v[0]; }
+};
+template <> struct Lane<uint16_t, false> {
+    using R = uint16_t;
+    static constexpr int N = 1;
+    __device__ static R load(const uint16_t *p) { return *p; }
+    __device__ static R zero() { return 0; }
+    __device__ static float get(const R &r, int) { return bf16_bits_to_f32(r); }
+    __device__ static void store(uint16_t *p, const float (&v)[N]) { *p = f32_to_bf16_rne(v[0]); }
+};
+
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+    const uint64_t u = static_cast<uint64_t>(v);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32));
+    return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
+}
+
+// First index i in [0, len) with a[i] >= key; a is non-decreasing and
+// a[len - 1] >= key. 64-ary search: one coalesced probe per lane per level.
+__device__ int64_t wave_lower_bound(const int64_t *__restrict__ a, int64_t len, int64_t key, int lane) {
+    int64_t lo = 0, hi = len;
+    while (hi - lo > kWave) {
+        const int64_t step = (hi - lo + kWave - 1) / kWave;
+        int64_t idx = lo + (int64_t)(lane + 1) * step - 1;
+        if (idx > hi - 1) idx = hi - 1;
+        const uint64_t m = __ballot(a[idx] >= key);
+        if (m == 0) return len - 1;  // not monotone: malformed input, stay in bounds
+        const int lf = __ffsll(static_cast<unsigned long long>(m)) - 1;
+        const int64_t nhi = lo + (int64_t)(lf + 1) * step;
+        lo = lo + (int64_t)lf * step;
+        hi = nhi < hi ? nhi : hi;
+    }
+    const int64_t idx = lo + lane;
+    const uint64_t m = __ballot(idx >= hi || a[idx] >= key);
+    return m ? lo + (__ffsll(static_cast<unsigned long long>(m)) - 1) : len - 1;
+}
+
+constexpr int kFull = 0, kPartial = 1;
+constexpr int kMsgSrc = 0, kMsgWeighted = 1, kMsgDiff = 2;
+
+// Reduce slots [s, t) of row r; write the row (kFull) or a partial (kPartial).
+template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT>
+__device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int64_t s, int64_t t, int kind,
+                                             int64_t slot, int lane) {
+    using LN = Lane<T, VEC>;
+    using R = typename LN::R;
+    constexpr int EP = LN::N;
+    const T *__restrict__ x = static_cast<const T *>(p.x);
+    const int L = 1 << p.lg_l;
+    const int S = kWave >> p.lg_l;
+    const int q = lane & (L - 1);
+    const int sg = lane >> p.lg_l;
+
+    int64_t f0[NS];
+    bool act[NS];
+#pragma unroll
+    for (int sl = 0; sl < NS; ++sl) {
+        const int64_t fo = ((int64_t)sl * L + q) * EP;
+        act[sl] = fo < p.fcnt;
+        f0[sl] = p.fbase + fo;
+    }
+    float acc[NS][EP];
+    int32_t pos[NS][EP];
+#pragma unroll
+    for (int sl = 0; sl < NS; ++sl)
+#pragma unroll
+        for (int e = 0; e < EP; ++e) {
+            acc[sl][e] = 0.f;
+            pos[sl][e] = -1;
+        }
+    R xi[NS];
+    if constexpr (MSG == kMsgDiff) {
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(x + r * p.F + f0[sl]) : LN::zero();
+    }
+
+    for (int64_t base = s; base < t; base += kWave) {
+        const int n = static_cast<int>(uniform64((t - base) < kWave ? (t - base) : kWave));
+        int myc = 0;
+        float myw = 1.f;
+        if (lane < n) {
+            myc = IDENT ? static_cast<int>(base + lane) : p.col[base + lane];
+            if constexpr (MSG == kMsgWeighted) myw = p.w[base + lane];
+        }
+        for (int st = 0; st < n; st += S * U) {
+            int jj[U];
+            float ww[U];
+            bool ok[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = st + u * S + sg;
+                ok[u] = idx < n;
+                jj[u] = __shfl(myc, idx & (kWave - 1), kWave);
+                if constexpr (MSG == kMsgWeighted) ww[u] = __shfl(myw, idx & (kWave - 1), kWave);
+            }
+            R v[U][NS];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int sl = 0; sl < NS; ++sl)
+                    v[u][sl] = (ok[u] && act[sl]) ? LN::load(x + (int64_t)jj[u] * p.F + f0[sl]) : LN::zero();
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (!ok[u]) continue;
+                const int32_t here = static_cast<int32_t>(base + st + u * S + sg);
+#pragma unroll
+                for (int sl = 0; sl < NS; ++sl)
+#pragma unroll
+                    for (int e = 0; e < EP; ++e) {
+                        const float xv = LN::get(v[u][sl], e);
+                        if constexpr (MAXA) {
+                            float m;
+                            if constexpr (MSG == kMsgDiff) m = xv - LN::get(xi[sl], e);
+                            else if constexpr (MSG == kMsgWeighted) m = ww[u] * xv;
+                            else m = xv;
+                            m = canon_zero(m);
+                            if (pos[sl][e] < 0 || m > acc[sl][e]) {
+                                acc[sl][e] = m;
+                                pos[sl][e] = here;
+                            }
+                        } else {
+                            if constexpr (MSG == kMsgDiff) acc[sl][e] += xv - LN::get(xi[sl], e);
+                            else if constexpr (MSG == kMsgWeighted) acc[sl][e] = fmaf(ww[u], xv, acc[sl][e]);
+                            else acc[sl][e] += xv;
+                        }
+                    }
+            }
+        }
+    }
+
+    // butterfly across sub-groups (fixed order -> deterministic)
+    for (int off = L; off < kWave; off <<= 1) {
+#pragma unroll
+        for (int sl = 0; sl < NS; ++sl)
+#pragma unroll
+            for (int e = 0; e < EP; ++e) {
+                const float o = __shfl_xor(acc[sl][e], off, kWave);
+                if constexpr (MAXA) {
+                    const int32_t op = __shfl_xor(pos[sl][e], off, kWave);
+                    if (op >= 0 && (pos[sl][e] < 0 || o > acc[sl][e] || (o == acc[sl][e] && op < pos[sl][e]))) {
+                        acc[sl][e] = o;
+                        pos[sl][e] = op;
+                    }
+                } else {
+                    acc[sl][e] += o;
+                }
+            }
+    }
+    if (sg != 0) return;
+
+#pragma unroll
+    for (int sl = 0; sl < NS; ++sl) {
+        if (!act[sl]) continue;
+        if (kind == kPartial) {
+            float *pv = p.part_val + slot * p.F + f0[sl];
+#pragma unroll
+            for (int e = 0; e < EP; ++e) pv[e] = acc[sl][e];
+            if constexpr (MAXA) {
+                int32_t *pp = p.part_pos + slot * p.F + f0[sl];
+#pragma unroll
+                for (int e = 0; e < EP; ++e) pp[e] = pos[sl][e];
+            }
+            continue;
+        }
+        float v[EP];
+        const int64_t deg = t - s;
+#pragma unroll
+        for (int e = 0; e < EP; ++e) {
+            if constexpr (MAXA) v[e] = pos[sl][e] >= 0 ? acc[sl][e] : 0.f;
+            else v[e] = (p.mean && deg > 0) ? acc[sl][e] / static_cast<float>(deg) : acc[sl][e];
+        }
+        LN::store(static_cast<T *>(p.out) + r * p.F + f0[sl], v);
+        if constexpr (MAXA) {
+            int64_t *ap = p.argmax + r * p.F + f0[sl];
+#pragma unroll
+            for (int e = 0; e < EP; ++e) {
+                const int32_t ps = pos[sl][e];
+                ap[e] = ps < 0 ? p.sentinel : (p.perm ? p.perm[ps] : static_cast<int64_t>(ps));
+            }
+        }
+    }
+}
+
+template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT>
+__global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
+    if (c >= p.nchunks) return;
+    const int64_t e0 = c * p.chunk;
+    const int64_t e1 = (e0 + p.chunk) < p.E ? (e0 + p.chunk) : p.E;
+    const bool last = c == p.nchunks - 1;
+    const int64_t rA = uniform64(wave_lower_bound(p.rowptr, p.n_rows + 1, e0, lane));
+    const int64_t rpA = uniform64(p.rowptr[rA]);
+    int32_t head = -1;
+
+    // a long row that started in an earlier chunk: reduce its piece here
+    if (rA > 0 && rpA > e0) {
+        const int64_t s0 = uniform64(p.rowptr[rA - 1]);
+        if (rpA - s0 > p.chunk)
+            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT>(p, rA - 1, e0, rpA < e1 ? rpA : e1, kPartial, 2 * c, lane);
+    }
+    // rows whose first slot lies in [e0, e1) (the last chunk also takes the
+    // empty rows that start at E)
+    int64_t rb = rA;
+    int64_t rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
+    for (int64_t r = rA; r < p.n_rows; ++r) {
+        if (r + 1 - rb >= kWave) {
+            rb = r;
+            rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
+        }
+        const int64_t s = uniform64(__shfl(rp, (int)(r - rb), kWave));
+        const int64_t t = uniform64(__shfl(rp, (int)(r + 1 - rb), kWave));
+        if (!last && s >= e1) break;
+        if (t - s > p.chunk) {
+            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT>(p, r, s, e1, kPartial, 2 * c + 1, lane);
+            head = static_cast<int32_t>(r);
+            break;
+        }
+        reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT>(p, r, s, t, kFull, 0, lane);
+    }
+    if (lane == 0) p.head_row[c] = head;
+}
+
+// Fold the pieces of every long row, one wavefront per chunk that starts one.
+template <typename T, bool MAXA>
+__global__ __launch_bounds__(kBlock) void k_segment_fixup(SegParams p) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
+    if (c >= p.nchunks) return;
+    const int64_t r = p.head_row[c];
+    if (r < 0) return;
+    const int64_t s = p.rowptr[r], t = p.rowptr[r + 1];
+    const int64_t cB = (t - 1) / p.chunk;
+    T *out = static_cast<T *>(p.out);
+    for (int64_t fo = lane; fo < p.fcnt; fo += kWave) {
+        const int64_t f = p.fbase + fo;
+        float v = p.part_val[(2 * c + 1) * p.F + f];
+        int32_t ps = MAXA ? p.part_pos[(2 * c + 1) * p.F + f] : 0;
+        for (int64_t cc = c + 1; cc <= cB; ++cc) {
+            const float o = p.part_val[(2 * cc) * p.F + f];
+            if constexpr (MAXA) {
+                if (o > v) {  // later pieces hold later slots: strict > keeps the lowest
+                    v = o;
+                    ps = p.part_pos[(2 * cc) * p.F + f];
+                }
+            } else {
+                v += o;
+            }
+        }
+        if (!MAXA && p.mean) v = v / static_cast<float>(t - s);
+        if constexpr (sizeof(T) == 2) out[r * p.F + f] = f32_to_bf16_rne(v);
+        else out[r * p.F + f] = v;
+        if constexpr (MAXA) p.argmax[r * p.F + f] = p.perm ? p.perm[ps] : static_cast<int64_t>(ps);
+    }
+}
+
+// No slots at all: every row is empty (0, and the sentinel for argmax).
+template <typename T>
+__global__ void k_empty_rows(T *__restrict__ out, int64_t *__restrict__ argmax, int64_t n, int64_t sentinel) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        out[i] = T(0);
+        if (argmax) argmax[i] = sentinel;
+    }
+}
+
+template <typename T, bool VEC, int NS, int MSG, bool MAXA, bool IDENT>
+int launch_window(const SegParams &p, hipStream_t s) {
+    constexpr int U = NS == 1 ? 8 : (NS == 2 ? 4 : 2);
+    const unsigned grid = static_cast<unsigned>((p.nchunks + (kBlock / kWave) - 1) / (kBlock / kWave));
+    k_segment<T, VEC, NS, U, MSG, MAXA, IDENT><<<grid, kBlock, 0, s>>>(p);
+    PYG_LAUNCH_CHECK();
+    if (p.nchunks > 1) {
+        k_segment_fixup<T, MAXA><<<grid, kBlock, 0, s>>>(p);
+        PYG_LAUNCH_CHECK();
+    }
+    return PYG_OK;
+}
+
+template <typename T, bool VEC, int MSG, bool MAXA, bool IDENT>
+int launch_ns(const SegParams &p, int ns, hipStream_t s) {
+    if (ns == 1) return launch_window<T, VEC, 1, MSG, MAXA, IDENT>(p, s);
+    if (ns == 2) return launch_window<T, VEC, 2, MSG, MAXA, IDENT>(p, s);
+    return launch_window<T, VEC, 4, MSG, MAXA, IDENT>(p, s);
+}
+
+template <typename T, bool VEC, bool MAXA>
+int launch_msg(const SegParams &p, int msg, bool ident, int ns, hipStream_t s) {
+    if (ident) return launch_ns<T, VEC, kMsgSrc, MAXA, true>(p, ns, s);
+    if (msg == kMsgDiff) return launch_ns<T, VEC, kMsgDiff, MAXA, false>(p, ns, s);
+    if (msg == kMsgWeighted) return launch_ns<T, VEC, kMsgWeighted, MAXA, false>(p, ns, s);
+    return launch_ns<T, VEC, kMsgSrc, MAXA, false>(p, ns, s);
+}
+
+template <typename T>
+int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
+    const bool maxa = a.aggr == PYG_MAX;
+    if (a.E == 0) {
+        k_empty_rows<T><<<grid_for(a.n_rows * a.F, kBlock * 4), kBlock, 0, s>>>(
+            static_cast<T *>(a.out), maxa ? a.argmax : nullptr, a.n_rows * a.F, a.sentinel);
+        PYG_LAUNCH_CHECK();
+        return PYG_OK;
+    }
+    const int64_t row_bytes = a.F * (int64_t)sizeof(T);
+    const bool vec = row_bytes % 16 == 0 && (reinterpret_cast<uintptr_t>(a.x) % 16) == 0 &&
+                     (reinterpret_cast<uintptr_t>(a.out) % 16) == 0;
+    const int ep = vec ? 16 / (int)sizeof(T) : 1;
+    const int64_t nvec = a.F / ep;  // lane vectors per row
+    int lg = 0;
+    while ((1 << lg) < nvec && lg < 6) ++lg;
+    p.lg_l = lg;
+    const int mk = a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc);
+    const bool ident = a.col == nullptr;
+    const int64_t per_window = 4 * kWave;  // lane vectors covered by one launch (NS = 4)
+    for (int64_t v0 = 0; v0 < nvec; v0 += per_window) {
+        const int64_t vn = (nvec - v0) < per_window ? (nvec - v0) : per_window;
+        const int ns = vn <= kWave ? 1 : (vn <= 2 * kWave ? 2 : 4);
+        p.fbase = v0 * ep;
+        p.fcnt = vn * ep;
+        int rc;
+        if (vec) rc = maxa ? launch_msg<T, true, true>(p, mk, ident, ns, s) : launch_msg<T, true, false>(p, mk, ident, ns, s);
+        else rc = maxa ? launch_msg<T, false, true>(p, mk, ident, ns, s) : launch_msg<T, false, false>(p, mk, ident, ns, s);
+        if (rc != PYG_OK) return rc;
+    }
+    return PYG_OK;
+}
+
+struct SegWs {
+    float *part_val;
+    int32_t *part_pos;
+    int32_t *head_row;
+    size_t bytes;
+};
+
+SegWs carve_segment(void *base, int64_t E, int64_t F, int aggr, int64_t chunk) {
+    const int64_t nchunks = E > 0 ? (E + chunk - 1) / chunk : 0;
+    Carver c(base);
+    SegWs w{};
+    w.part_val = c.take<float>(2 * nchunks * F);
+    w.part_pos = c.take<int32_t>(aggr == PYG_MAX ? 2 * nchunks * F : 0);
+    w.head_row = c.take<int32_t>(nchunks);
+    w.bytes = c.used + 256;
+    return w;
+}
+
+}  // namespace
+
+int64_t segment_chunk(int64_t E, int64_t requested) {
+    if (requested > 0) return requested;
+    int64_t c = 64;
+    while (c < 4096 && c * 32768 < E) c <<= 1;
+    return c;
+}
+
+size_t segment_workspace(int64_t E, int64_t F, int aggr, int64_t chunk) {
+    return carve_segment(nullptr, E, F, aggr, segment_chunk(E, chunk)).bytes;
+}
+
+int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t s) {
+    if (a.n_rows == 0 || a.F == 0) return PYG_OK;
+    const int64_t chunk = segment_chunk(a.E, a.chunk);
+    const SegWs w = carve_segment(ws, a.E, a.F, a.aggr, chunk);
+    if (ws_bytes < w.bytes || !ws) return PYG_ERR_WORKSPACE;
+    SegParams p{};
+    p.x = a.x;
+    p.F = a.F;
+    p.rowptr = a.rowptr;
+    p.col = a.col;
+    p.w = a.weight;
+    p.perm = a.perm;
+    p.n_rows = a.n_rows;
+    p.E = a.E;
+    p.chunk = chunk;
+    p.nchunks = a.E > 0 ? (a.E + chunk - 1) / chunk : 0;
+    p.mean = a.aggr == PYG_MEAN;
+    p.sentinel = a.sentinel;
+    p.out = a.out;
+    p.argmax = a.argmax;
+    p.part_val = w.part_val;
+    p.part_pos = w.part_pos;
+    p.head_row = w.head_row;
+    return a.dtype == PYG_BF16 ? run_typed<uint16_t>(a, p, s) : run_typed<float>(a, p, s);
+}
+
+}  // namespace pyg

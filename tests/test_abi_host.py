@@ -1,0 +1,147 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before any device work."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pyg_mi355x.h")
+
+PYG_OK, INVALID, WORKSPACE, UNSUPPORTED = 0, -1, -3, -5
+FAKE = ctypes.c_void_p(0x10000)  # never dereferenced: every call below fails its host checks
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_1903_02428_amd as pyg
+    if not os.path.exists(pyg.library_path()):
+        from paper_1903_02428_amd import build
+        build.build()
+    return pyg.library()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(pyg_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = header_functions()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in the header but not exported"
+    import paper_1903_02428_amd.binding as b
+    assert sorted(b.EXPORTED) == names
+
+
+def test_version_and_strerror(lib):
+    import paper_1903_02428_amd as pyg
+    assert pyg.abi_version() == 1
+    for code, text in ((0, "success"), (-1, "invalid argument"), (-3, "workspace too small"),
+                       (-4, "HIP runtime or launch error"), (-5, "unsupported size or combination"), (7, "unknown status")):
+        assert pyg.strerror(code) == text
+
+
+def _ws(fn, *args):
+    out = ctypes.c_size_t(0)
+    rc = fn(*args, ctypes.byref(out))
+    return rc, out.value
+
+
+def test_workspace_queries_monotone(lib):
+    last = 0
+    for E in (0, 1, 1000, 10**6, 10**8):
+        rc, b = _ws(lib.pyg_coo_to_csr_workspace, E, 5000)
+        assert rc == PYG_OK and b >= last
+        last = b
+    last = 0
+    for N in (1, 100, 10**5):
+        rc, b = _ws(lib.pyg_gcn_norm_workspace, N)
+        assert rc == PYG_OK and b >= N * 8 and b >= last
+        last = b
+    for kernel in (0, 1, 2):
+        for aggr in (0, 1, 2):
+            last = 0
+            for E in (0, 100, 10**5, 10**7):
+                rc, b = _ws(lib.pyg_propagate_workspace, 0, 1000, 64, E, aggr, kernel, 0)
+                assert rc == PYG_OK and b >= last
+                last = b
+    assert _ws(lib.pyg_propagate_workspace, 5, 10, 4, 10, 0, 0, 0)[0] == INVALID  # bad dtype
+    assert _ws(lib.pyg_propagate_workspace, 0, 10, 4, 10, 9, 0, 0)[0] == INVALID  # bad aggr
+    assert _ws(lib.pyg_propagate_workspace, 0, 2**31, 4, 10, 0, 0, 0)[0] == UNSUPPORTED
+    assert _ws(lib.pyg_coo_to_csr_workspace, -1, 4)[0] == INVALID
+
+
+def prop(lib, x=FAKE, dtype=0, N=10, F=4, ei=FAKE, E=20, w=None, csr=None, msg=0, aggr=0, kernel=1,
+         out=ctypes.c_void_p(0x20000), argmax=None, ws=FAKE, ws_bytes=1 << 40):
+    return lib.pyg_propagate(x, dtype, N, F, ei, E, w, csr, msg, aggr, kernel, out, argmax, ws, ws_bytes, None)
+
+
+def test_propagate_rejects_bad_arguments(lib):
+    from paper_1903_02428_amd.binding import _Csr
+    assert prop(lib, dtype=3) == INVALID
+    assert prop(lib, aggr=7) == INVALID
+    assert prop(lib, msg=4) == INVALID
+    assert prop(lib, kernel=9) == INVALID
+    assert prop(lib, N=-1) == INVALID
+    assert prop(lib, F=-2) == INVALID
+    assert prop(lib, E=-5) == INVALID
+    assert prop(lib, N=2**31) == UNSUPPORTED
+    assert prop(lib, E=2**31) == UNSUPPORTED
+    assert prop(lib, msg=1, w=FAKE) == INVALID                        # weighted diff
+    assert prop(lib, aggr=2, argmax=None) == INVALID                  # max needs argmax
+    assert prop(lib, aggr=0, argmax=ctypes.c_void_p(0x90000)) == INVALID  # argmax only for max
+    assert prop(lib, x=None) == INVALID
+    assert prop(lib, out=None) == INVALID
+    assert prop(lib, ei=None) == INVALID                              # COO kernel needs edges
+    assert prop(lib, N=0, E=5) == INVALID                             # edges into no nodes
+    assert prop(lib, out=ctypes.c_void_p(0x10000 + 8)) == INVALID     # out overlaps x
+    assert prop(lib, kernel=2, csr=None) == INVALID                   # CSR kernel needs a CSR
+    bad_n = _Csr(0x30000, 0x40000, 0x50000, None, 11, 20, 0)
+    assert prop(lib, kernel=2, csr=ctypes.byref(bad_n)) == INVALID    # CSR of another graph
+    no_w = _Csr(0x30000, 0x40000, 0x50000, None, 10, 20, 0)
+    assert prop(lib, kernel=2, csr=ctypes.byref(no_w), w=FAKE) == INVALID  # weights missing in CSR
+    no_perm = _Csr(0x30000, 0x40000, None, None, 10, 20, 0)
+    assert prop(lib, kernel=2, csr=ctypes.byref(no_perm), aggr=2, argmax=ctypes.c_void_p(0x90000)) == INVALID
+    neg_chunk = _Csr(0x30000, 0x40000, 0x50000, None, 10, 20, -1)
+    assert prop(lib, kernel=2, csr=ctypes.byref(neg_chunk)) == INVALID
+    assert prop(lib, ws_bytes=0, aggr=1) == WORKSPACE
+    assert prop(lib, ws=None, aggr=1) == WORKSPACE
+
+
+def test_other_entry_points_reject_bad_arguments(lib):
+    assert lib.pyg_degree(None, 5, 4, FAKE, None) == INVALID
+    assert lib.pyg_degree(FAKE, 5, 4, None, None) == INVALID
+    assert lib.pyg_degree(FAKE, 5, 2**31, FAKE, None) == UNSUPPORTED
+    assert lib.pyg_coo_to_csr(FAKE, 5, 4, None, None, FAKE, FAKE, None, FAKE, 1 << 30, None) == INVALID
+    assert lib.pyg_coo_to_csr(FAKE, 5, 4, None, FAKE, FAKE, FAKE, None, FAKE, 0, None) == WORKSPACE
+    assert lib.pyg_gcn_norm(FAKE, None, 5, 4, FAKE, FAKE, 0, None) == WORKSPACE
+    assert lib.pyg_gcn_norm(None, None, 5, 4, FAKE, FAKE, 1 << 20, None) == INVALID
+    assert lib.pyg_global_pool(FAKE, 0, 10, 4, FAKE, 3, 2, ctypes.c_void_p(0x90000), None, FAKE, 1 << 30, None) == INVALID
+    assert lib.pyg_global_pool(FAKE, 0, 10, 4, None, 3, 0, ctypes.c_void_p(0x90000), None, FAKE, 1 << 30, None) == INVALID
+    assert lib.pyg_global_pool(FAKE, 0, 10, 4, FAKE, 3, 0, ctypes.c_void_p(0x90000), None, FAKE, 0, None) == WORKSPACE
+    assert lib.pyg_global_pool(FAKE, 1, 10, 4, FAKE, 0, 0, ctypes.c_void_p(0x90000), None, FAKE, 1 << 30, None) == INVALID
+    assert lib.pyg_validate_coo(None, 5, 4, FAKE, None) == INVALID
+    assert lib.pyg_validate_batch(FAKE, 5, 4, None, None) == INVALID
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    import paper_1903_02428_amd.binding as b
+    monkeypatch.setattr(b, "_lib", None)
+    monkeypatch.setattr(b, "_HERE", str(tmp_path))
+    with pytest.raises(b.LibraryMissing):
+        b.library()
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+
+    import paper_1903_02428_amd as pyg
+    x = torch.zeros(4, 2)
+    ei = torch.zeros(2, 3, dtype=torch.int64)
+    with pytest.raises(ValueError):
+        pyg.propagate(x, ei)
+    with pytest.raises(ValueError):
+        pyg.degree(ei, 4)
