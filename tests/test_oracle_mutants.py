@@ -1,12 +1,14 @@
 """Plant plausible mistakes in copies of the oracle and check that the pins
 catch every one (CPU only; the real oracle source is never modified)."""
-import multiprocessing
+import concurrent.futures as cf
+import json
 import os
+import subprocess
+import sys
 
 import pytest
 
 import oracle
-from tests.oracle_pins import ALL_PINS
 
 # (name, original text, mutated text); each original must occur in oracle.c
 MUTANTS = [
@@ -39,34 +41,36 @@ MUTANTS = [
 
 
 @pytest.fixture(scope="module")
-def source():
+def outcomes(tmp_path_factory):
+    """Compile every mutant and run all pins against it in a fresh process
+    (a mutant that corrupts memory only kills its own process, which also
+    counts as caught)."""
     with open(os.path.join(os.path.dirname(oracle.__file__), "oracle.c")) as f:
-        return f.read()
+        source = f.read()
+    d = tmp_path_factory.mktemp("mutants")
+    runner = os.path.join(os.path.dirname(os.path.abspath(__file__)), "mutant_runner.py")
 
-
-@pytest.mark.parametrize("name,orig,mut", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_pins_catch_mutant(tmp_path, source, name, orig, mut):
-    assert source.count(orig) == 1, f"mutation site for {name} not unique"
-    src = tmp_path / f"{name}.c"
-    src.write_text(source.replace(orig, mut))
-    libpath = oracle.build(str(src), str(tmp_path / f"lib{name}.so"))
-    # run the pins in a forked child so a mutant that corrupts memory cannot
-    # take the test process down (a crash also counts as caught)
-    ctx = multiprocessing.get_context("fork")
-    recv, send = ctx.Pipe(duplex=False)
-    proc = ctx.Process(target=_run_pins, args=(libpath, send))
-    proc.start()
-    proc.join(120)
-    caught = recv.recv() if proc.exitcode == 0 and recv.poll() else ["<crashed>"]
-    assert caught, f"no pin catches mutant {name}"
-
-
-def _run_pins(libpath, send):
-    lib = oracle.load(libpath)
-    caught = []
-    for pin in ALL_PINS:
+    def one(m):
+        name, orig, mut = m
+        if source.count(orig) != 1:
+            return name, None
+        src = d / f"{name}.c"
+        src.write_text(source.replace(orig, mut))
+        libpath = oracle.build(str(src), str(d / f"lib{name}.so"))
         try:
-            pin(lib)
-        except (AssertionError, ValueError, IndexError):
-            caught.append(pin.__name__)
-    send.send(caught)
+            r = subprocess.run([sys.executable, runner, libpath], capture_output=True, text=True, timeout=300)
+        except subprocess.TimeoutExpired:
+            return name, ["<timeout>"]
+        if r.returncode != 0:
+            return name, [f"<exit {r.returncode}>"]
+        return name, json.loads(r.stdout.strip().splitlines()[-1])
+
+    with cf.ThreadPoolExecutor(4) as ex:
+        return dict(ex.map(one, MUTANTS))
+
+
+@pytest.mark.parametrize("name", [m[0] for m in MUTANTS])
+def test_pins_catch_mutant(outcomes, name):
+    caught = outcomes[name]
+    assert caught is not None, f"mutation site for {name} is not unique in oracle.c"
+    assert caught, f"no pin catches mutant {name}"

@@ -165,8 +165,11 @@ def test_csr_and_max_are_deterministic(pyg):
 
 
 def test_permutation_invariance(pyg):
+    # a simple graph (no duplicate edges) with continuous features has no ties,
+    # so the winning edge must map through the permutation
     rng = np.random.default_rng(8)
-    ei, x, w = graph(500, 6000, 8, 32)
+    ei = synth.random_coo(rng, 500, 6000, duplicates=False)
+    x = rng.standard_normal((500, 32)).astype(np.float32)
     p = rng.permutation(ei.shape[1])
     for kernel in ("coo", "csr"):
         m1, a1 = pyg.propagate(to_dev(x), to_dev(ei), kernel=kernel, aggr="max",
