@@ -1,0 +1,266 @@
+#!/usr/bin/env python3
+"""Benchmark of the propagate hot path on one MI355X.
+
+Workload: the large power-law graph (Chung-Lu degree exponent 2.1, N=232,965,
+~114.6M directed edges plus N self-loops, mean in-degree ~493), F=128 fp32
+features. One step is one pass of the whole path on that graph, inputs
+already resident in HBM:
+
+    degree -> gcn_norm -> coo_to_csr (with the norms) -> propagate
+    (gcn_norm-weighted sum, CSR segment kernel) -> global mean pool
+
+`value` is E*F of the step's propagate divided by the step time
+(edges*features/s). The `roofline` object covers the dominant call, the CSR
+propagate, timed with HIP events on the launch stream inside the timed steps.
+`cpu_baseline` times the oracle (single-threaded plain C loop) on a bounded
+sample of the same workload. `detail` adds per-call times and the COO-vs-CSR,
+fp32-vs-bf16 and sum-vs-mean comparison.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--chunk", type=int, default=0, help="edges per CSR work chunk (0 = library default)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-detail", action="store_true")
+    ap.add_argument("--cpu-sample-rows", type=float, default=0.08, help="fraction of target rows in the CPU sample")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def b_alg_csr(N, E, F, s_x, weighted=True, s_out=None):
+    """Algorithmic bytes of one CSR propagate: row pointers, int32 columns,
+    weights, one source-row gather per edge, one output write."""
+    s_out = s_x if s_out is None else s_out
+    return 8 * (N + 1) + 4 * E + (4 * E if weighted else 0) + E * F * s_x + N * F * s_out
+
+
+def b_alg_coo(N, E, F, s_x, weighted=True):
+    """Algorithmic bytes of one COO propagate: int64 source and target, weights,
+    one gather per edge, one output write."""
+    return 16 * E + (4 * E if weighted else 0) + E * F * s_x + N * F * s_x
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the multi-GPU design is described but not built)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1903_02428_amd as pyg
+    import synth
+
+    if not os.path.exists(pyg.library_path()):
+        from paper_1903_02428_amd import build
+        build.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    t0 = time.time()
+    c = synth.make_config(5, seed=args.seed)
+    N, F = c["N"], c["F"]
+    ei_np, x_np = c["edge_index_gcn"], c["x"]
+    E = ei_np.shape[1]
+    log(f"generated {c['name']}: N={N} E={E} F={F} in {time.time() - t0:.1f}s")
+
+    ei = torch.from_numpy(ei_np).to(dev)
+    x = torch.from_numpy(x_np).to(dev)
+    batch = torch.zeros(N, dtype=torch.int64, device=dev)  # one graph: whole-graph readout
+
+    # all outputs and workspaces allocated once, outside the timed region
+    deg = torch.empty(N, dtype=torch.int64, device=dev)
+    norm = torch.empty(E, dtype=torch.float32, device=dev)
+    csr = pyg.CSR(torch.empty(N + 1, dtype=torch.int64, device=dev), torch.empty(E, dtype=torch.int32, device=dev),
+                  torch.empty(E, dtype=torch.int64, device=dev), torch.empty(E, dtype=torch.float32, device=dev),
+                  N, E, args.chunk)
+    out = torch.empty_like(x)
+    pooled = torch.empty(1, F, dtype=torch.float32, device=dev)
+    lib = pyg.library()
+    import ctypes
+    sz = ctypes.c_size_t()
+    lib.pyg_coo_to_csr_workspace(E, N, ctypes.byref(sz))
+    ws_csr = torch.empty(sz.value, dtype=torch.uint8, device=dev)
+    lib.pyg_gcn_norm_workspace(N, ctypes.byref(sz))
+    ws_norm = torch.empty(sz.value, dtype=torch.uint8, device=dev)
+    ws_prop = torch.empty(pyg.propagate_workspace_bytes(x, E, "sum", "csr", args.chunk), dtype=torch.uint8, device=dev)
+    lib.pyg_global_pool_workspace(0, N, F, 1, 1, ctypes.byref(sz))
+    ws_pool = torch.empty(sz.value, dtype=torch.uint8, device=dev)
+
+    names = ["degree", "gcn_norm", "coo_to_csr", "propagate", "global_pool"]
+    ev = {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
+    times = {n: [] for n in names}
+
+    def step(record):
+        def mark(n, i):
+            if record:
+                ev[n][i].record()
+        mark("degree", 0)
+        pyg.degree(ei, N, out=deg)
+        mark("degree", 1)
+        mark("gcn_norm", 0)
+        pyg.gcn_norm(ei, N, out=norm, workspace=ws_norm)
+        mark("gcn_norm", 1)
+        mark("coo_to_csr", 0)
+        pyg.coo_to_csr(ei, N, norm, chunk=args.chunk, out=csr, workspace=ws_csr)
+        mark("coo_to_csr", 1)
+        mark("propagate", 0)
+        pyg.propagate(x, ei, norm, csr=csr, aggr="sum", out=out, workspace=ws_prop)
+        mark("propagate", 1)
+        mark("global_pool", 0)
+        pyg.global_pool(out, batch, 1, "mean", out=pooled, workspace=ws_pool)
+        mark("global_pool", 1)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+
+    wall = 0.0
+    for k in range(args.steps):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        step(True)
+        torch.cuda.synchronize()
+        wall += time.perf_counter() - t1
+        for n in names:
+            times[n].append(ev[n][0].elapsed_time(ev[n][1]))
+    ms_per_step = wall / args.steps * 1e3
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+
+    t_prop = float(np.mean(times["propagate"])) * 1e-3
+    balg = b_alg_csr(N, E, F, 4)
+    achieved = balg / t_prop / 1e9
+    value = E * F / (ms_per_step * 1e-3)
+
+    result = {
+        "metric": "propagate throughput: edges·features/s and achieved HBM GB/s (% of peak)",
+        "value": value,
+        "unit": "edges·features/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "large power-law graph (Chung-Lu gamma=2.1), gcn_norm-weighted sum, CSR segment kernel",
+                   "N": N, "E": E, "F": F, "seed": args.seed, "chunk": args.chunk or "default",
+                   "step": "degree+gcn_norm+coo_to_csr+propagate(sum,csr)+global_pool(mean)"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "pyg_propagate CSR segment (k_segment + k_segment_fixup), fp32 weighted sum",
+                     "bytes_per_launch": balg, "avg_launch_ms": t_prop * 1e3},
+        "detail": {"per_call_ms": {n: float(np.mean(times[n])) for n in names},
+                   "propagate_edges_features_per_s": E * F / t_prop},
+    }
+
+    if not args.no_detail:
+        result["detail"]["variants"] = variants(pyg, torch, x, ei, norm, csr, N, E, F, dev)
+    if not (args.no_detail and args.no_cpu_baseline):
+        import oracle
+        w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)  # the oracle's own weights
+    if not args.no_detail:
+        result["detail"]["parity_sampled"] = sampled_parity(x_np, ei_np, w_ref, out, N)
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(x_np, ei_np, w_ref, N, F, args.cpu_sample_rows, args.seed)
+    print(json.dumps(result), flush=True)
+
+
+def timed(torch, fn, reps=10):
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    fn()
+    ts = []
+    for _ in range(reps):
+        s.record()
+        fn()
+        e.record()
+        e.synchronize()
+        ts.append(s.elapsed_time(e))
+    return float(np.median(ts))
+
+
+def variants(pyg, torch, x, ei, norm, csr, N, E, F, dev):
+    """Propagate-only times: CSR vs COO, fp32 vs bf16 storage, sum vs mean."""
+    xb = x.to(torch.bfloat16)
+    res = {}
+    for dtname, xx, s in (("f32", x, 4), ("bf16", xb, 2)):
+        o = torch.empty_like(xx)
+        for aggr in ("sum", "mean"):
+            for kernel in ("csr", "coo"):
+                ws = torch.empty(pyg.propagate_workspace_bytes(xx, E, aggr, kernel, csr.chunk), dtype=torch.uint8,
+                                 device=dev)
+                ms = timed(torch, lambda: pyg.propagate(xx, ei, norm, csr=csr if kernel == "csr" else None, aggr=aggr,
+                                                        kernel=kernel, out=o, workspace=ws))
+                b = b_alg_csr(N, E, F, s) if kernel == "csr" else b_alg_coo(N, E, F, s)
+                res[f"{kernel}-{aggr}-{dtname}"] = {"ms": ms, "edges_features_per_s": E * F / (ms * 1e-3),
+                                                   "alg_GBps": b / (ms * 1e-3) / 1e9,
+                                                   "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    return res
+
+
+def sampled_parity(x_np, ei_np, w_ref, out, N, rows=200):
+    """The step's output (device gcn_norm -> CSR -> propagate) on a few sampled
+    rows against the oracle chain (oracle gcn_norm -> oracle propagate)."""
+    import oracle
+    rng = np.random.default_rng(123)
+    sample = rng.choice(N, rows, replace=False)
+    keep = np.isin(ei_np[1], sample)
+    sub = ei_np[:, keep]
+    w = w_ref[keep]
+    ref, _, sabs = oracle.propagate(x_np, sub, w, aggr="sum")
+    got = out.cpu().numpy()[sample].astype(np.float64)
+    bound = 1e-5 * sabs[sample] + 1e-6
+    ratio = float((np.abs(got - ref[sample]) / bound).max())
+    return {"rows": rows, "worst_error_over_bound": ratio, "ok": ratio <= 1.0}
+
+
+def cpu_baseline(x_np, ei_np, w_ref, N, F, frac, seed):
+    """The oracle (single-threaded plain C loop, fp64 accumulation) timed on a
+    bounded sample: all edges into a random fraction of the target rows."""
+    import oracle
+    rng = np.random.default_rng([seed, 99])
+    rows = rng.choice(N, int(N * frac), replace=False)
+    keep = np.isin(ei_np[1], rows)
+    sub = np.ascontiguousarray(ei_np[:, keep])
+    w = w_ref[keep]
+    Es = sub.shape[1]
+    t = time.perf_counter()
+    oracle.propagate(x_np, sub, w, aggr="sum")
+    dt = time.perf_counter() - t
+    return {"value": Es * F / dt, "unit": "edges·features/s", "cores": 1, "kind": "oracle",
+            "sample": f"gcn_norm-weighted sum over the {Es} edges into {len(rows)} random target rows "
+                      f"({frac:.0%} of rows) of the same graph, F={F}, {dt:.1f}s",
+            "host": platform.processor() or platform.machine(), "host_cpus": os.cpu_count()}
+
+
+if __name__ == "__main__":
+    main()

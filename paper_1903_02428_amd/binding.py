@@ -146,15 +146,17 @@ class CSR:
                     None if self.weight is None else self.weight.data_ptr(), self.N, self.E, self.chunk)
 
 
-def degree(edge_index: torch.Tensor, num_nodes: int) -> torch.Tensor:
+def degree(edge_index: torch.Tensor, num_nodes: int, out: torch.Tensor | None = None) -> torch.Tensor:
     E = _edge_index(edge_index)
-    deg = torch.empty(num_nodes, dtype=torch.int64, device=edge_index.device)
+    deg = torch.empty(num_nodes, dtype=torch.int64, device=edge_index.device) if out is None else out
     _check(library().pyg_degree(_ptr(edge_index), E, num_nodes, _ptr(deg), _stream(edge_index.device)), "pyg_degree")
     return deg
 
 
 def coo_to_csr(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None,
-               chunk: int = 0) -> CSR:
+               chunk: int = 0, out: CSR | None = None, workspace: torch.Tensor | None = None) -> CSR:
+    """Build the CSR; `out` (a CSR of the same shape) and `workspace` may be
+    passed to reuse device buffers."""
     lib = library()
     E = _edge_index(edge_index)
     dev = edge_index.device
@@ -162,26 +164,35 @@ def coo_to_csr(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tens
         _need_cuda("edge_weight", edge_weight, torch.float32, 1)
         if edge_weight.shape[0] != E:
             raise ValueError("edge_weight must be [E]")
-    rowptr = torch.empty(num_nodes + 1, dtype=torch.int64, device=dev)
-    col = torch.empty(E, dtype=torch.int32, device=dev)
-    perm = torch.empty(E, dtype=torch.int64, device=dev)
-    wcsr = torch.empty(E, dtype=torch.float32, device=dev) if edge_weight is not None else None
+    if out is not None:
+        if out.N != num_nodes or out.E != E or ((out.weight is None) != (edge_weight is None)):
+            raise ValueError("out CSR has another shape")
+        rowptr, col, perm, wcsr = out.rowptr, out.col, out.perm, out.weight
+    else:
+        rowptr = torch.empty(num_nodes + 1, dtype=torch.int64, device=dev)
+        col = torch.empty(E, dtype=torch.int32, device=dev)
+        perm = torch.empty(E, dtype=torch.int64, device=dev)
+        wcsr = torch.empty(E, dtype=torch.float32, device=dev) if edge_weight is not None else None
     nbytes = _size(lib.pyg_coo_to_csr_workspace, E, num_nodes)
-    ws = _workspace(nbytes, dev)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
     _check(lib.pyg_coo_to_csr(_ptr(edge_index), E, num_nodes, _ptr(edge_weight), _ptr(rowptr), _ptr(col),
                               _ptr(perm), _ptr(wcsr), _ptr(ws), nbytes, _stream(dev)), "pyg_coo_to_csr")
+    if out is not None:
+        out.chunk = chunk
+        return out
     return CSR(rowptr, col, perm, wcsr, num_nodes, E, chunk)
 
 
-def gcn_norm(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None) -> torch.Tensor:
+def gcn_norm(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None,
+             out: torch.Tensor | None = None, workspace: torch.Tensor | None = None) -> torch.Tensor:
     lib = library()
     E = _edge_index(edge_index)
     dev = edge_index.device
     if edge_weight is not None:
         _need_cuda("edge_weight", edge_weight, torch.float32, 1)
-    norm = torch.empty(E, dtype=torch.float32, device=dev)
+    norm = torch.empty(E, dtype=torch.float32, device=dev) if out is None else out
     nbytes = _size(lib.pyg_gcn_norm_workspace, num_nodes)
-    ws = _workspace(nbytes, dev)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
     _check(lib.pyg_gcn_norm(_ptr(edge_index), _ptr(edge_weight), E, num_nodes, _ptr(norm), _ptr(ws), nbytes,
                             _stream(dev)), "pyg_gcn_norm")
     return norm
@@ -234,7 +245,9 @@ def propagate(x: torch.Tensor, edge_index: torch.Tensor | None = None, edge_weig
     return out, argmax
 
 
-def global_pool(x: torch.Tensor, batch: torch.Tensor, num_graphs: int, aggr: str = "sum"):
+def global_pool(x: torch.Tensor, batch: torch.Tensor, num_graphs: int, aggr: str = "sum",
+                out: torch.Tensor | None = None, argmax: torch.Tensor | None = None,
+                workspace: torch.Tensor | None = None):
     """Per-graph readout over a sorted assignment vector. Returns (out, argmax or None)."""
     lib = library()
     _need_cuda("x", x, None, 2)
@@ -243,10 +256,14 @@ def global_pool(x: torch.Tensor, batch: torch.Tensor, num_graphs: int, aggr: str
     if batch.shape[0] != N:
         raise ValueError("batch must be [N]")
     dev = x.device
-    out = torch.empty((num_graphs, F), dtype=x.dtype, device=dev)
-    argmax = torch.empty((num_graphs, F), dtype=torch.int64, device=dev) if aggr == "max" else None
+    if out is None:
+        out = torch.empty((num_graphs, F), dtype=x.dtype, device=dev)
+    if aggr == "max" and argmax is None:
+        argmax = torch.empty((num_graphs, F), dtype=torch.int64, device=dev)
+    if aggr != "max":
+        argmax = None
     nbytes = _size(lib.pyg_global_pool_workspace, DTYPE[x.dtype], N, F, num_graphs, AGGR[aggr])
-    ws = _workspace(nbytes, dev)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
     _check(lib.pyg_global_pool(_ptr(x), DTYPE[x.dtype], N, F, _ptr(batch), num_graphs, AGGR[aggr], _ptr(out),
                                _ptr(argmax), _ptr(ws), nbytes, _stream(dev)), "pyg_global_pool")
     return out, argmax

@@ -1,0 +1,96 @@
+"""Parity at the full size of the large power-law workload (N=232,965,
+E~114.8M with self-loops, F=128), in the launch configuration the benchmark
+times. Degree, CSR and gcn_norm are compared with the oracle element by
+element; propagate on sampled target rows (hubs that span many work chunks
+included), whose oracle values are computed from the edges into those rows."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from tests.parity import bf16_round, check_max, check_sum, to_dev
+
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(900)]
+
+
+@pytest.fixture(scope="module")
+def pyg():
+    import paper_1903_02428_amd as m
+    assert torch.cuda.is_available()
+    m.library()
+    return m
+
+
+@pytest.fixture(scope="module")
+def c5():
+    c = synth.make_config(5)
+    print(f"[c5] generated N={c['N']} E={c['edge_index_gcn'].shape[1]}", flush=True)
+    return c
+
+
+@pytest.fixture(scope="module")
+def dev_graph(pyg, c5):
+    ei_np = c5["edge_index_gcn"]
+    N = c5["N"]
+    ei = to_dev(ei_np)
+    w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)
+    csr = pyg.coo_to_csr(ei, N, to_dev(w_ref))
+    return ei, w_ref, csr
+
+
+def test_c5_degree_csr_norm_full(pyg, c5, dev_graph):
+    ei_np, N = c5["edge_index_gcn"], c5["N"]
+    ei, w_ref, csr = dev_graph
+    assert np.array_equal(pyg.degree(ei, N).cpu().numpy(), oracle.degree(ei_np, N))
+    rp, col, perm = oracle.coo_to_csr(ei_np, N)
+    assert np.array_equal(csr.rowptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.perm.cpu().numpy(), perm)
+    assert np.array_equal(csr.col.cpu().numpy().astype(np.int64), col)
+    del col
+    assert np.array_equal(csr.weight.cpu().numpy(), w_ref[perm])
+    # unit weights: every fp64 step is order-independent -> identical to the rounded oracle
+    assert np.array_equal(pyg.gcn_norm(ei, N).cpu().numpy(), w_ref)
+
+
+def sample_rows(c5, n=1500):
+    ei_np, N = c5["edge_index_gcn"], c5["N"]
+    deg = np.bincount(ei_np[1], minlength=N)
+    rng = np.random.default_rng(77)
+    hubs = np.argsort(deg)[-12:]             # rows split across many chunks
+    light = np.argsort(deg, kind="stable")[:12]
+    rows = np.unique(np.concatenate([rng.choice(N, n, replace=False), hubs, light]))
+    keep = np.isin(ei_np[1], rows)
+    return rows, keep
+
+
+@pytest.mark.parametrize("kernel", ["csr", "coo"])
+def test_c5_propagate_sampled(pyg, c5, dev_graph, kernel):
+    ei_np, x_np, N = c5["edge_index_gcn"], c5["x"], c5["N"]
+    ei, w_ref, csr = dev_graph
+    rows, keep = sample_rows(c5)
+    sub = ei_np[:, keep]
+    kidx = np.nonzero(keep)[0]
+    w_sub = w_ref[keep]
+    x32 = to_dev(x_np)
+    w = to_dev(w_ref)
+    cases = [("sum", torch.float32, w), ("mean", torch.float32, w), ("sum", torch.bfloat16, w),
+             ("mean", torch.bfloat16, w), ("max", torch.float32, None)]
+    for aggr, dt, wt in cases:
+        xx = x32.to(dt)
+        use = None
+        if kernel == "csr":  # the unweighted run reads the same CSR without its weights
+            use = csr if wt is not None else pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E)
+        out, arg = pyg.propagate(xx, ei, wt, csr=use, aggr=aggr, kernel=kernel)
+        torch.cuda.synchronize()
+        xin = x_np if dt == torch.float32 else bf16_round(x_np)
+        ref, rarg, sabs = oracle.propagate(xin, sub, w_sub if wt is not None else None, aggr=aggr)
+        what = f"C5 {kernel} {aggr} {dt}"
+        got = out[to_dev(rows)]
+        if aggr == "max":
+            rarg_full = np.where(rarg[rows] < sub.shape[1], kidx[np.minimum(rarg[rows], sub.shape[1] - 1)],
+                                 ei_np.shape[1])
+            check_max(got, arg[to_dev(rows)], ref[rows], rarg_full, what=what)
+        else:
+            check_sum(got, ref[rows], sabs[rows], dt == torch.bfloat16, what)
+        print(f"[c5] {what} ok", flush=True)
