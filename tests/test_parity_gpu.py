@@ -206,7 +206,8 @@ def test_global_pool(pyg, aggr, dtype):
 
 def test_validate(pyg):
     ei = to_dev(np.array([[0, 5, -1, 2], [1, 1, 1, 9]], np.int64))
-    assert pyg.validate_coo(ei, 6) == 3
+    assert pyg.validate_coo(ei, 6) == 2   # -1 and 9
+    assert pyg.validate_coo(ei, 5) == 3   # 5, -1 and 9
     assert pyg.validate_coo(ei, 10) == 1
     assert pyg.validate_batch(to_dev(np.array([0, 0, 1, 1, 3], np.int64)), 4) == 0
     assert pyg.validate_batch(to_dev(np.array([0, 2, 1, 1, 4], np.int64)), 4) == 2
