@@ -107,8 +107,10 @@ def main():
     sz = ctypes.c_size_t()
     lib.pyg_coo_to_csr_workspace(E, N, ctypes.byref(sz))
     ws_csr = torch.empty(sz.value, dtype=torch.uint8, device=dev)
-    lib.pyg_gcn_norm_workspace(N, ctypes.byref(sz))
+    lib.pyg_gcn_norm_workspace(E, N, ctypes.byref(sz))
     ws_norm = torch.empty(sz.value, dtype=torch.uint8, device=dev)
+    lib.pyg_degree_workspace(E, N, ctypes.byref(sz))
+    ws_deg = torch.empty(sz.value, dtype=torch.uint8, device=dev)
     ws_prop = torch.empty(pyg.propagate_workspace_bytes(x, E, "sum", "csr", args.chunk), dtype=torch.uint8, device=dev)
     lib.pyg_global_pool_workspace(0, N, F, 1, 1, ctypes.byref(sz))
     ws_pool = torch.empty(sz.value, dtype=torch.uint8, device=dev)
@@ -122,7 +124,7 @@ def main():
             if record:
                 ev[n][i].record()
         mark("degree", 0)
-        pyg.degree(ei, N, out=deg)
+        pyg.degree(ei, N, out=deg, workspace=ws_deg)
         mark("degree", 1)
         mark("gcn_norm", 0)
         pyg.gcn_norm(ei, N, out=norm, workspace=ws_norm)

@@ -92,10 +92,15 @@ const char *pyg_strerror(int status);
 /* ABI version of this header (incremented on incompatible change). */
 int pyg_abi_version(void);
 
+/* Workspace bytes needed by pyg_degree for (E, N). */
+int pyg_degree_workspace(int64_t E, int64_t N, size_t *bytes);
+
 /* In-degree deg[i] = number of edges whose target is i, counted with
  * multiplicity (|N(i)| in Eq. (1); the denominator of mean).
- *   edge_index int64 [2,E] (device), deg int64 [N] (device, output). */
-int pyg_degree(const int64_t *edge_index, int64_t E, int64_t N, int64_t *deg, void *stream);
+ *   edge_index int64 [2,E] (device), deg int64 [N] (device, output).
+ * Counted in on-chip histograms over slices of the node range; exact. */
+int pyg_degree(const int64_t *edge_index, int64_t E, int64_t N, int64_t *deg, void *ws, size_t ws_bytes,
+               void *stream);
 
 /* Workspace bytes needed by pyg_coo_to_csr for (E, N). */
 int pyg_coo_to_csr_workspace(int64_t E, int64_t N, size_t *bytes);
@@ -115,8 +120,8 @@ int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, const float 
                    int64_t *rowptr, int32_t *col, int64_t *perm, float *weight_csr,
                    void *ws, size_t ws_bytes, void *stream);
 
-/* Workspace bytes needed by pyg_gcn_norm for N nodes. */
-int pyg_gcn_norm_workspace(int64_t N, size_t *bytes);
+/* Workspace bytes needed by pyg_gcn_norm for (E, N). */
+int pyg_gcn_norm_workspace(int64_t E, int64_t N, size_t *bytes);
 
 /* GCN edge normalisation for the GCN operator of Section 2, on an edge list
  * that already contains the self-loops:

@@ -17,7 +17,8 @@ MSG = {"src": 0, "diff": 1}
 KERNEL = {"auto": 0, "coo": 1, "csr": 2}
 
 EXPORTED = [
-    "pyg_strerror", "pyg_abi_version", "pyg_degree", "pyg_coo_to_csr_workspace", "pyg_coo_to_csr",
+    "pyg_strerror", "pyg_abi_version", "pyg_degree_workspace", "pyg_degree", "pyg_coo_to_csr_workspace",
+    "pyg_coo_to_csr",
     "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_propagate_workspace", "pyg_propagate",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
 ]
@@ -58,10 +59,11 @@ def library() -> ctypes.CDLL:
         lib.pyg_strerror.argtypes, lib.pyg_strerror.restype = [i32], ctypes.c_char_p
         lib.pyg_abi_version.argtypes, lib.pyg_abi_version.restype = [], i32
         sigs = {
-            "pyg_degree": [p, i64, i64, p, p],
+            "pyg_degree_workspace": [i64, i64, sz],
+            "pyg_degree": [p, i64, i64, p, p, ctypes.c_size_t, p],
             "pyg_coo_to_csr_workspace": [i64, i64, sz],
             "pyg_coo_to_csr": [p, i64, i64, p, p, p, p, p, p, ctypes.c_size_t, p],
-            "pyg_gcn_norm_workspace": [i64, sz],
+            "pyg_gcn_norm_workspace": [i64, i64, sz],
             "pyg_gcn_norm": [p, p, i64, i64, p, p, ctypes.c_size_t, p],
             "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
@@ -146,10 +148,16 @@ class CSR:
                     None if self.weight is None else self.weight.data_ptr(), self.N, self.E, self.chunk)
 
 
-def degree(edge_index: torch.Tensor, num_nodes: int, out: torch.Tensor | None = None) -> torch.Tensor:
+def degree(edge_index: torch.Tensor, num_nodes: int, out: torch.Tensor | None = None,
+           workspace: torch.Tensor | None = None) -> torch.Tensor:
+    lib = library()
     E = _edge_index(edge_index)
-    deg = torch.empty(num_nodes, dtype=torch.int64, device=edge_index.device) if out is None else out
-    _check(library().pyg_degree(_ptr(edge_index), E, num_nodes, _ptr(deg), _stream(edge_index.device)), "pyg_degree")
+    dev = edge_index.device
+    deg = torch.empty(num_nodes, dtype=torch.int64, device=dev) if out is None else out
+    nbytes = _size(lib.pyg_degree_workspace, E, num_nodes)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
+    _check(lib.pyg_degree(_ptr(edge_index), E, num_nodes, _ptr(deg), _ptr(ws), ws.numel(), _stream(dev)),
+           "pyg_degree")
     return deg
 
 
@@ -191,7 +199,7 @@ def gcn_norm(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor
     if edge_weight is not None:
         _need_cuda("edge_weight", edge_weight, torch.float32, 1)
     norm = torch.empty(E, dtype=torch.float32, device=dev) if out is None else out
-    nbytes = _size(lib.pyg_gcn_norm_workspace, num_nodes)
+    nbytes = _size(lib.pyg_gcn_norm_workspace, E, num_nodes)
     ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
     _check(lib.pyg_gcn_norm(_ptr(edge_index), _ptr(edge_weight), E, num_nodes, _ptr(norm), _ptr(ws), nbytes,
                             _stream(dev)), "pyg_gcn_norm")

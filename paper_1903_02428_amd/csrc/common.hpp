@@ -94,6 +94,11 @@ size_t scan_workspace_elems(int64_t n);
 int scan_u32(const uint32_t *in, uint32_t *out, int64_t n, bool inclusive, uint32_t *ws, hipStream_t s);
 int scan_i64(const int64_t *in, int64_t *out, int64_t n, bool inclusive, int64_t *ws, hipStream_t s);
 
+// In-degree histograms (LDS-sliced, deterministic); scratch degree_workspace(E, N) bytes.
+size_t degree_workspace(int64_t E, int64_t N);
+int count_targets_i64(const int64_t *dst, int64_t E, int64_t N, int64_t *out, void *ws, hipStream_t s);
+int count_targets_f64(const int64_t *dst, int64_t E, int64_t N, double *out, void *ws, hipStream_t s);
+
 // Target-sorted segment reduction shared by propagate (CSR) and pooling.
 struct SegmentArgs {
     const void *x;      // source rows [n_src, F]

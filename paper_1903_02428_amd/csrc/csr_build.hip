@@ -2,32 +2,148 @@
 //
 // The CSR is the row-ordered ("coalesced") layout that Appendix A says a
 // sparse-matrix product needs and that should be built once, as
-// preprocessing. Here it is built on the GPU with a stable LSD radix sort of
-// the target ids (digit-major tile histograms, a device scan, then a
-// tile-ordered scatter that ranks equal digits with wavefront ballots), so
-// the slots of a row keep ascending COO edge id and the result is unique.
+// preprocessing. It is built here with a stable LSD radix sort of the target
+// ids that carries (edge id, source, weight) as payload, so no pass gathers
+// at random:
+//   per pass  k_radix_hist     digit counts per tile, digit-major
+//             device scan      -> global offset of every (digit, tile)
+//             k_radix_scatter  each wavefront ranks its 1024 keys against
+//                              wave-private LDS counters (ballot match on
+//                              the digit bits), the tile combines the four
+//                              waves in order, stages a tile-local
+//                              permutation in LDS and writes every digit run
+//                              contiguously.
+//   then      k_row_bounds     rowptr from the key changes of the sorted keys.
+// Elements keep their order inside equal digits in every pass, so the slots
+// of a row end in ascending COO edge id and the result is unique.
+//
+// In-degree counting uses LDS-privatised histograms over slices of the node
+// range (no global atomics on the edge stream): every workgroup counts the
+// targets of one edge partition that fall into its slice, then writes its
+// counters once; a reduce pass sums the partitions in a fixed order.
 #include "common.hpp"
 
 namespace pyg {
 namespace {
 
-constexpr int kTileItems = 16;
-constexpr int64_t kTile = (int64_t)kBlock * kTileItems;  // elements per radix tile
-constexpr int kMaxDigitBits = 8;
+constexpr int kItems = 16;                                  // keys per thread per tile
+constexpr int kWaveKeys = kWave * kItems;                   // keys ranked by one wavefront
+constexpr int64_t kTile = (int64_t)kBlock * kItems;         // keys per tile (4096)
+constexpr int kMaxDigitBits = 9;
+constexpr int kMaxRadix = 1 << kMaxDigitBits;
+constexpr int kWaves = kBlock / kWave;
 
-__global__ void k_count_targets(const int64_t *__restrict__ dst, int64_t E, unsigned long long *__restrict__ cnt) {
-    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < E; k += (int64_t)gridDim.x * blockDim.x)
-        atomicAdd(&cnt[dst[k]], 1ull);
+// ------------------------------------------------------------------ degree
+
+// Count targets of edge partition blockIdx.y that fall in node slice
+// blockIdx.x; write the slice's counters to partial[y][node]. One workgroup
+// of 1024 threads holds a whole slice in LDS, so each thread keeps 8 target
+// loads in flight.
+constexpr int kHistThreads = 1024;
+constexpr int kHistUnroll = 8;
+
+__global__ __launch_bounds__(kHistThreads) void k_hist_slice(const int64_t *__restrict__ dst, int64_t E, int64_t N,
+                                                             int64_t slice, int64_t part_len,
+                                                             uint32_t *__restrict__ partial) {
+    extern __shared__ uint32_t cnt[];
+    const int64_t n0 = (int64_t)blockIdx.x * slice;
+    const int64_t n1 = (n0 + slice) < N ? (n0 + slice) : N;
+    const int64_t len = n1 - n0;
+    for (int64_t i = threadIdx.x; i < len; i += kHistThreads) cnt[i] = 0;
+    __syncthreads();
+    const int64_t e0 = (int64_t)blockIdx.y * part_len;
+    const int64_t e1 = (e0 + part_len) < E ? (e0 + part_len) : E;
+    int64_t k = e0 + threadIdx.x;
+    for (; k + (kHistUnroll - 1) * kHistThreads < e1; k += kHistUnroll * kHistThreads) {
+        int64_t d[kHistUnroll];
+#pragma unroll
+        for (int u = 0; u < kHistUnroll; ++u) d[u] = dst[k + u * kHistThreads] - n0;
+#pragma unroll
+        for (int u = 0; u < kHistUnroll; ++u)
+            if (static_cast<uint64_t>(d[u]) < static_cast<uint64_t>(len)) atomicAdd(&cnt[d[u]], 1u);
+    }
+    for (; k < e1; k += kHistThreads) {
+        const int64_t d = dst[k] - n0;
+        if (static_cast<uint64_t>(d) < static_cast<uint64_t>(len)) atomicAdd(&cnt[d], 1u);
+    }
+    __syncthreads();
+    uint32_t *out = partial + (int64_t)blockIdx.y * N + n0;
+    for (int64_t i = threadIdx.x; i < len; i += kHistThreads) out[i] = cnt[i];
 }
 
-__device__ __forceinline__ uint32_t load_key(const int64_t *dst64, const uint32_t *keys, int64_t i) {
-    return dst64 ? static_cast<uint32_t>(dst64[i]) : keys[i];
+// deg[i] = sum over partitions of partial[p][i] (fixed order).
+template <typename Out>
+__global__ void k_hist_reduce(const uint32_t *__restrict__ partial, int64_t N, int64_t parts, Out *__restrict__ out) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x) {
+        uint64_t s = 0;
+        for (int64_t p = 0; p < parts; ++p) s += partial[p * N + i];
+        out[i] = static_cast<Out>(s);
+    }
 }
+
+struct HistPlan {
+    int64_t slice, nslices, parts, part_len;
+    size_t lds;
+};
+
+HistPlan hist_plan(int64_t E, int64_t N) {
+    static const int lds_limit = [] {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+            v = 64 * 1024;
+        return v < 160 * 1024 ? v : 160 * 1024;
+    }();
+    HistPlan h{};
+    h.slice = (lds_limit - 1024) / 4;
+    if (h.slice > N) h.slice = N > 0 ? N : 1;
+    h.nslices = (N + h.slice - 1) / h.slice;
+    if (h.nslices < 1) h.nslices = 1;
+    // about 1024 workgroups in total, each partition at least 64K edges
+    int64_t parts = 1024 / h.nslices;
+    const int64_t by_size = (E + 65535) / 65536;
+    if (parts > by_size) parts = by_size;
+    if (parts < 1) parts = 1;
+    h.part_len = (E + parts - 1) / parts;
+    h.parts = h.part_len > 0 ? (E + h.part_len - 1) / h.part_len : 1;
+    h.lds = static_cast<size_t>(h.slice) * 4;
+    return h;
+}
+
+size_t hist_workspace(int64_t E, int64_t N) {
+    const HistPlan h = hist_plan(E, N);
+    return align_up(static_cast<size_t>(h.parts) * N * 4, 256) + 256;
+}
+
+template <typename Out>
+int count_targets(const int64_t *dst, int64_t E, int64_t N, Out *out, void *ws, hipStream_t s) {
+    if (N == 0) return PYG_OK;
+    if (E == 0) return fill<Out>(out, N, Out(0), s);
+    const HistPlan h = hist_plan(E, N);
+    uint32_t *partial = static_cast<uint32_t *>(ws);
+    if (hipFuncSetAttribute(reinterpret_cast<const void *>(k_hist_slice), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            static_cast<int>(h.lds)) != hipSuccess)
+        return PYG_ERR_HIP;
+    k_hist_slice<<<dim3((unsigned)h.nslices, (unsigned)h.parts), kHistThreads, h.lds, s>>>(dst, E, N, h.slice, h.part_len, partial);
+    PYG_LAUNCH_CHECK();
+    k_hist_reduce<Out><<<grid_for(N, kBlock), kBlock, 0, s>>>(partial, N, h.parts, out);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
+
+// ------------------------------------------------------------- radix sort
+
+struct Payload {  // one sort buffer: key plus carried fields
+    uint32_t *key;
+    uint32_t *id;
+    uint32_t *src;
+    float *w;
+};
 
 __global__ __launch_bounds__(kBlock) void k_radix_hist(const int64_t *__restrict__ dst64, const uint32_t *__restrict__ keys,
                                                        int64_t E, int shift, int bits, int64_t ntiles,
                                                        uint32_t *__restrict__ hist) {
-    __shared__ uint32_t h[1 << kMaxDigitBits];
+    __shared__ uint32_t h[kMaxRadix];
     const int radix = 1 << bits;
     const uint32_t mask = radix - 1;
     for (int i = threadIdx.x; i < radix; i += kBlock) h[i] = 0;
@@ -35,87 +151,161 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const int64_t *__restrict
     const int64_t tile = blockIdx.x;
     const int64_t base = tile * kTile + threadIdx.x;
 #pragma unroll 4
-    for (int r = 0; r < kTileItems; ++r) {
+    for (int r = 0; r < kItems; ++r) {
         const int64_t i = base + (int64_t)r * kBlock;
-        if (i < E) atomicAdd(&h[(load_key(dst64, keys, i) >> shift) & mask], 1u);
+        if (i < E) {
+            const uint32_t key = dst64 ? static_cast<uint32_t>(dst64[i]) : keys[i];
+            atomicAdd(&h[(key >> shift) & mask], 1u);
+        }
     }
     __syncthreads();
     for (int i = threadIdx.x; i < radix; i += kBlock) hist[(int64_t)i * ntiles + tile] = h[i];
 }
 
-// Stable scatter of one tile. Elements are visited in rounds of kBlock
-// consecutive ids (round r, thread t -> id tile*kTile + r*kBlock + t), which is
-// id order; inside a round, equal digits are ranked by wavefront ballots and
-// then by wave index, so every element lands after all earlier equal digits.
+// One stable scatter pass. Tile element order: wave w owns elements
+// [w*1024, (w+1)*1024) of the tile, visited 64 at a time in lane order.
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(
-    const int64_t *__restrict__ dst64, const uint32_t *__restrict__ keys_in, const uint32_t *__restrict__ vals_in,
-    int64_t E, int shift, int bits, int64_t ntiles, const uint32_t *__restrict__ offsets,
-    uint32_t *__restrict__ keys_out, uint32_t *__restrict__ vals_out,
-    int64_t *__restrict__ perm, int32_t *__restrict__ col, const int64_t *__restrict__ src64,
-    float *__restrict__ wcsr, const float *__restrict__ w) {
-    constexpr int kWaves = kBlock / kWave;
-    __shared__ uint32_t run[1 << kMaxDigitBits];
-    __shared__ uint32_t cnt[kWaves][1 << kMaxDigitBits];
+    const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64, const float *__restrict__ w_in,
+    Payload in, Payload out, int64_t *__restrict__ perm, int32_t *__restrict__ col, float *__restrict__ wcsr,
+    int64_t E, int shift, int bits, int64_t ntiles, const uint32_t *__restrict__ offsets, int last) {
+    __shared__ uint32_t wcnt[kWaves][kMaxRadix];  // per-wave running counts, then per-wave prefixes
+    __shared__ uint32_t start[kMaxRadix];         // first staged slot of each digit in the tile
+    __shared__ uint16_t stage[kTile];             // tile-local index of the element in sorted slot j
     const int radix = 1 << bits;
     const uint32_t mask = radix - 1;
-    const int64_t tile = blockIdx.x;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
+    const int64_t tile = blockIdx.x;
+    const int64_t tbase = tile * kTile;
+    const int64_t tlen = (E - tbase) < kTile ? (E - tbase) : kTile;
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
-    for (int i = threadIdx.x; i < radix; i += kBlock) run[i] = offsets[(int64_t)i * ntiles + tile];
-    for (int r = 0; r < kTileItems; ++r) {
-        const int64_t i = tile * kTile + (int64_t)r * kBlock + threadIdx.x;
-        const bool valid = i < E;
-        uint32_t key = 0, val = 0;
-        if (valid) {
-            key = load_key(dst64, keys_in, i);
-            val = vals_in ? vals_in[i] : static_cast<uint32_t>(i);
+
+    for (int i = lane; i < radix; i += kWave) wcnt[wave][i] = 0;
+    __builtin_amdgcn_wave_barrier();
+
+    // phase A: load this wave's keys, rank each against earlier equal digits
+    uint32_t dig[kItems];
+    uint32_t rk[kItems];
+    {
+        uint32_t key[kItems];
+#pragma unroll
+        for (int r = 0; r < kItems; ++r) {
+            const int64_t i = tbase + wave * kWaveKeys + r * kWave + lane;
+            key[r] = (i < E) ? (dst64 ? static_cast<uint32_t>(dst64[i]) : in.key[i]) : 0u;
+        }
+#pragma unroll
+        for (int r = 0; r < kItems; ++r) {
+            const int64_t i = tbase + wave * kWaveKeys + r * kWave + lane;
+            const bool valid = i < E;
+            const uint32_t d = (key[r] >> shift) & mask;
+            uint64_t peers = __ballot(valid);
+            for (int b = 0; b < bits; ++b) {
+                const bool bit = (d >> b) & 1u;
+                const uint64_t bal = __ballot(bit);
+                peers &= bit ? bal : ~bal;
+            }
+            const uint32_t before = __popcll(peers & lt_mask);
+            const uint32_t base = valid ? wcnt[wave][d] : 0u;
+            __builtin_amdgcn_wave_barrier();
+            if (valid && before == 0) wcnt[wave][d] = base + __popcll(peers);
+            __builtin_amdgcn_wave_barrier();
+            dig[r] = valid ? d : 0xFFFFFFFFu;
+            rk[r] = base + before;
+        }
+    }
+    __syncthreads();
+
+    // phase B: per digit, prefix over waves; then the tile start of each digit run
+    for (int t = threadIdx.x; t < radix; t += kBlock) {
+        uint32_t acc = 0;
+#pragma unroll
+        for (int wv = 0; wv < kWaves; ++wv) {
+            const uint32_t c = wcnt[wv][t];
+            wcnt[wv][t] = acc;
+            acc += c;
+        }
+        start[t] = acc;  // digit total, scanned below
+    }
+    __syncthreads();
+    if (threadIdx.x < kWave) {
+        // one wave scans up to 512 digit totals: 8 per lane, then a lane prefix
+        constexpr int per = kMaxRadix / kWave;
+        uint32_t v[per];
+        uint32_t s = 0;
+#pragma unroll
+        for (int j = 0; j < per; ++j) {
+            const int t = lane * per + j;
+            v[j] = t < radix ? start[t] : 0u;
+            s += v[j];
+        }
+        uint32_t incl = s;
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
+            const uint32_t y = __shfl_up(incl, d, kWave);
+            if (lane >= d) incl += y;
+        }
+        uint32_t run = incl - s;
+#pragma unroll
+        for (int j = 0; j < per; ++j) {
+            const int t = lane * per + j;
+            if (t < radix) start[t] = run;
+            run += v[j];
+        }
+    }
+    __syncthreads();
+
+    // phase C: stage the tile-local permutation in sorted order
+#pragma unroll
+    for (int r = 0; r < kItems; ++r) {
+        if (dig[r] != 0xFFFFFFFFu) {
+            const uint32_t slot = start[dig[r]] + wcnt[wave][dig[r]] + rk[r];
+            stage[slot] = static_cast<uint16_t>(wave * kWaveKeys + r * kWave + lane);
+        }
+    }
+    __syncthreads();
+
+    // phase D: write each digit run contiguously
+    for (int64_t j = threadIdx.x; j < tlen; j += kBlock) {
+        const int64_t li = stage[j];
+        if (li >= tlen) continue;  // cannot happen for a consistent ranking; keeps reads in bounds
+        const int64_t i = tbase + li;
+        uint32_t key, id, src;
+        float wv = 0.f;
+        if (dst64) {
+            key = static_cast<uint32_t>(dst64[i]);
+            id = static_cast<uint32_t>(i);
+            src = static_cast<uint32_t>(src64[i]);
+            if (w_in) wv = w_in[i];
+        } else {
+            key = in.key[i];
+            id = in.id[i];
+            src = in.src[i];
+            if (in.w) wv = in.w[i];
         }
         const uint32_t d = (key >> shift) & mask;
-        for (int t = threadIdx.x; t < kWaves * radix; t += kBlock) (&cnt[0][0])[(t / radix) * (1 << kMaxDigitBits) + (t % radix)] = 0;
-        __syncthreads();
-        uint64_t peers = __ballot(valid);
-        for (int b = 0; b < bits; ++b) {
-            const bool bit = (d >> b) & 1u;
-            const uint64_t bal = __ballot(bit);
-            peers &= bit ? bal : ~bal;
+        const int64_t pos = (int64_t)offsets[(int64_t)d * ntiles + tile] + (j - start[d]);
+        if (pos < 0 || pos >= E) continue;  // likewise: writes stay in bounds
+        if (last) {
+            perm[pos] = id;
+            col[pos] = static_cast<int32_t>(src);
+            if (wcsr) wcsr[pos] = wv;
+            out.key[pos] = key;
+        } else {
+            out.key[pos] = key;
+            out.id[pos] = id;
+            out.src[pos] = src;
+            if (out.w) out.w[pos] = wv;
         }
-        const uint32_t rank = __popcll(peers & lt_mask);
-        if (valid && rank == 0) cnt[wave][d] = __popcll(peers);
-        __syncthreads();
-        for (int t = threadIdx.x; t < radix; t += kBlock) {
-            uint32_t acc = run[t];
-#pragma unroll
-            for (int wv = 0; wv < kWaves; ++wv) {
-                const uint32_t c = cnt[wv][t];
-                cnt[wv][t] = acc;
-                acc += c;
-            }
-            run[t] = acc;
-        }
-        __syncthreads();
-        if (valid) {
-            const uint32_t pos = cnt[wave][d] + rank;
-            if (perm) {
-                perm[pos] = val;
-                col[pos] = static_cast<int32_t>(src64[val]);
-                if (wcsr) wcsr[pos] = w[val];
-            } else {
-                keys_out[pos] = key;
-                vals_out[pos] = val;
-            }
-        }
-        __syncthreads();
     }
 }
 
-// N <= 1: every edge targets node 0, the CSR order is the COO order.
-__global__ void k_identity_csr(const int64_t *__restrict__ src, int64_t E, int64_t *__restrict__ perm,
-                               int32_t *__restrict__ col, float *__restrict__ wcsr, const float *__restrict__ w) {
-    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < E; k += (int64_t)gridDim.x * blockDim.x) {
-        perm[k] = k;
-        col[k] = static_cast<int32_t>(src[k]);
-        if (wcsr) wcsr[k] = w[k];
+// rowptr from the sorted target ids: slot p starts every row in (key[p-1], key[p]].
+__global__ void k_row_bounds(const uint32_t *__restrict__ key, int64_t E, int64_t N, int64_t *__restrict__ rowptr) {
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p <= E; p += (int64_t)gridDim.x * blockDim.x) {
+        int64_t cur = p < E ? static_cast<int64_t>(key[p]) : N;
+        if (cur > N) cur = N;
+        const int64_t prev = p > 0 ? static_cast<int64_t>(key[p - 1]) : -1;
+        for (int64_t r = prev + 1; r <= cur; ++r) rowptr[r] = p;
     }
 }
 
@@ -133,63 +323,80 @@ __global__ void k_validate_batch(const int64_t *__restrict__ b, int64_t N, int64
     if (local) atomicAdd(bad, local);
 }
 
-int digit_plan(int64_t N, int *passes, int *bits_per_pass) {
-    int nb = 0;
-    while (nb < 63 && (int64_t(1) << nb) < N) ++nb;  // bits of N-1
-    *passes = (nb + kMaxDigitBits - 1) / kMaxDigitBits;
-    *bits_per_pass = *passes ? (nb + *passes - 1) / *passes : 0;
-    return nb;
+// Digit plan: total key bits, passes, bits per pass (at least one pass).
+void digit_plan(int64_t N, int *nb, int *passes, int *bpp) {
+    int b = 1;
+    while (b < 31 && (int64_t(1) << b) < N) ++b;
+    *nb = b;
+    *passes = (b + kMaxDigitBits - 1) / kMaxDigitBits;
+    *bpp = (b + *passes - 1) / *passes;
 }
 
 struct CsrWs {
-    uint32_t *keys[2];
-    uint32_t *vals[2];
+    Payload buf[2];
+    uint32_t *sorted_key;
     uint32_t *hist;
     uint32_t *hist_scan;
-    int64_t *row_scan;
     size_t bytes;
 };
 
-CsrWs carve_csr(void *base, int64_t E, int64_t N) {
-    int passes, bpp;
-    digit_plan(N, &passes, &bpp);
+CsrWs carve_csr(void *base, int64_t E, int64_t N, bool weighted) {
+    int nb, passes, bpp;
+    digit_plan(N, &nb, &passes, &bpp);
     const int64_t ntiles = (E + kTile - 1) / kTile;
-    const int64_t nhist = ntiles << (passes ? bpp : 0);
+    const int64_t nhist = ntiles << bpp;
     Carver c(base);
     CsrWs w{};
-    const int64_t bufs = passes >= 2 ? E : 0;
-    for (int i = 0; i < 2; ++i) {
-        w.keys[i] = c.take<uint32_t>(i == 0 || passes >= 3 ? bufs : 0);
-        w.vals[i] = c.take<uint32_t>(i == 0 || passes >= 3 ? bufs : 0);
+    for (int b = 0; b < 2; ++b) {
+        const int64_t n = (passes >= 2 + b) ? E : 0;  // buffer 0 from two passes on, buffer 1 from three
+        w.buf[b].key = c.take<uint32_t>(n);
+        w.buf[b].id = c.take<uint32_t>(n);
+        w.buf[b].src = c.take<uint32_t>(n);
+        w.buf[b].w = weighted && n ? c.take<float>(n) : nullptr;
     }
+    w.sorted_key = c.take<uint32_t>(E);
     w.hist = c.take<uint32_t>(nhist);
     w.hist_scan = c.take<uint32_t>(scan_workspace_elems(nhist));
-    w.row_scan = c.take<int64_t>(scan_workspace_elems(N));
     w.bytes = c.used + 256;
     return w;
 }
 
 }  // namespace
+
+size_t degree_workspace(int64_t E, int64_t N) { return hist_workspace(E, N); }
+
+int count_targets_i64(const int64_t *dst, int64_t E, int64_t N, int64_t *out, void *ws, hipStream_t s) {
+    return count_targets<int64_t>(dst, E, N, out, ws, s);
+}
+
+int count_targets_f64(const int64_t *dst, int64_t E, int64_t N, double *out, void *ws, hipStream_t s) {
+    return count_targets<double>(dst, E, N, out, ws, s);
+}
+
 }  // namespace pyg
 
 using namespace pyg;
 
-extern "C" int pyg_degree(const int64_t *edge_index, int64_t E, int64_t N, int64_t *deg, void *stream) {
+extern "C" int pyg_degree_workspace(int64_t E, int64_t N, size_t *bytes) {
+    if (E < 0 || N < 0 || !bytes) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    *bytes = degree_workspace(E, N);
+    return PYG_OK;
+}
+
+extern "C" int pyg_degree(const int64_t *edge_index, int64_t E, int64_t N, int64_t *deg, void *ws, size_t ws_bytes,
+                          void *stream) {
     if (E < 0 || N < 0 || (E > 0 && !edge_index) || (N > 0 && !deg)) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     if (E > 0 && N == 0) return PYG_ERR_INVALID_ARG;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    PYG_TRY(fill<int64_t>(deg, N, 0, s));
-    if (E == 0) return PYG_OK;
-    k_count_targets<<<grid_for(E, kBlock * 8), kBlock, 0, s>>>(edge_index + E, E, reinterpret_cast<unsigned long long *>(deg));
-    PYG_LAUNCH_CHECK();
-    return PYG_OK;
+    if (ws_bytes < degree_workspace(E, N) || !ws) return PYG_ERR_WORKSPACE;
+    return count_targets<int64_t>(edge_index + E, E, N, deg, ws, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int pyg_coo_to_csr_workspace(int64_t E, int64_t N, size_t *bytes) {
     if (E < 0 || N < 0 || !bytes) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
-    *bytes = carve_csr(nullptr, E, N).bytes;
+    *bytes = carve_csr(nullptr, E, N, true).bytes;
     return PYG_OK;
 }
 
@@ -200,46 +407,35 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
     if (E > 0 && (!edge_index || !col || !perm || N == 0)) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     if (!edge_weight) weight_csr = nullptr;
-    const CsrWs w = carve_csr(ws, E, N);
+    const CsrWs w = carve_csr(ws, E, N, edge_weight != nullptr);
     if (ws_bytes < w.bytes || (w.bytes > 256 && !ws)) return PYG_ERR_WORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (E == 0) return fill<int64_t>(rowptr, N + 1, 0, s);
     const int64_t *src = edge_index;
     const int64_t *dst = edge_index + E;
 
-    // row pointers: count per target into rowptr[1..N], inclusive scan in place
-    PYG_TRY(fill<int64_t>(rowptr, N + 1, 0, s));
-    if (E == 0) return PYG_OK;
-    k_count_targets<<<grid_for(E, kBlock * 8), kBlock, 0, s>>>(dst, E, reinterpret_cast<unsigned long long *>(rowptr + 1));
-    PYG_LAUNCH_CHECK();
-    PYG_TRY(scan_i64(rowptr + 1, rowptr + 1, N, true, w.row_scan, s));
-
-    int passes, bpp;
-    const int nb = digit_plan(N, &passes, &bpp);
-    if (passes == 0) {
-        k_identity_csr<<<grid_for(E, kBlock * 4), kBlock, 0, s>>>(src, E, perm, col, weight_csr, edge_weight);
-        PYG_LAUNCH_CHECK();
-        return PYG_OK;
-    }
+    int nb, passes, bpp;
+    digit_plan(N, &nb, &passes, &bpp);
     const int64_t ntiles = (E + kTile - 1) / kTile;
-    const uint32_t *kin = nullptr, *vin = nullptr;
+    Payload in{}, none{};
     int shift = 0;
     for (int p = 0; p < passes; ++p) {
         const int bits = (nb - shift) < bpp ? (nb - shift) : bpp;
         const bool last = p == passes - 1;
         const int64_t nhist = ntiles << bits;
-        k_radix_hist<<<(unsigned)ntiles, kBlock, 0, s>>>(p == 0 ? dst : nullptr, kin, E, shift, bits, ntiles, w.hist);
+        k_radix_hist<<<(unsigned)ntiles, kBlock, 0, s>>>(p == 0 ? dst : nullptr, in.key, E, shift, bits, ntiles, w.hist);
         PYG_LAUNCH_CHECK();
         PYG_TRY(scan_u32(w.hist, w.hist, nhist, false, w.hist_scan, s));
-        uint32_t *kout = last ? nullptr : w.keys[p & 1];
-        uint32_t *vout = last ? nullptr : w.vals[p & 1];
-        k_radix_scatter<<<(unsigned)ntiles, kBlock, 0, s>>>(
-            p == 0 ? dst : nullptr, kin, vin, E, shift, bits, ntiles, w.hist, kout, vout,
-            last ? perm : nullptr, col, src, weight_csr, edge_weight);
+        Payload out = last ? none : w.buf[p & 1];
+        if (last) out.key = w.sorted_key;
+        k_radix_scatter<<<(unsigned)ntiles, kBlock, 0, s>>>(p == 0 ? dst : nullptr, src, edge_weight, in, out, perm,
+                                                           col, weight_csr, E, shift, bits, ntiles, w.hist, last ? 1 : 0);
         PYG_LAUNCH_CHECK();
-        kin = kout;
-        vin = vout;
+        in = out;
         shift += bits;
     }
+    k_row_bounds<<<grid_for(E + 1, kBlock * 4), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
+    PYG_LAUNCH_CHECK();
     return PYG_OK;
 }
 

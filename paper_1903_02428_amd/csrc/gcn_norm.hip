@@ -1,8 +1,9 @@
 // GCN edge normalisation (the GCN operator listed in Section 2):
 //   d_i = sum_{k: target(k) = i} w_k,  dinv_i = d_i^-1/2 (0 if d_i = 0),
 //   norm_k = dinv_j * w_k * dinv_i.
-// The degree sums in fp64 hardware atomics; dinv and the edge product are
-// fp64 too, rounded once to fp32 at the end. With unit weights every fp64
+// Unit weights: d is the in-degree from the deterministic LDS histogram.
+// Explicit weights: d sums in fp64 hardware atomics. dinv and the edge
+// product are fp64, rounded once to fp32 at the end; with unit weights every
 // step is order-independent, so the result is reproducible bit for bit.
 #include "common.hpp"
 
@@ -22,9 +23,26 @@ __global__ void k_inv_sqrt(double *__restrict__ d, int64_t N) {
     }
 }
 
-__global__ void k_edge_norm(const int64_t *__restrict__ src, const int64_t *__restrict__ dst, const float *__restrict__ w,
-                            int64_t E, const double *__restrict__ dinv, float *__restrict__ norm) {
-    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < E; k += (int64_t)gridDim.x * blockDim.x) {
+// Four edges per thread per iteration keep enough loads in flight.
+__global__ __launch_bounds__(kBlock) void k_edge_norm(const int64_t *__restrict__ src, const int64_t *__restrict__ dst,
+                                                      const float *__restrict__ w, int64_t E,
+                                                      const double *__restrict__ dinv, float *__restrict__ norm) {
+    constexpr int U = 4;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    for (; k + (U - 1) * stride < E; k += U * stride) {
+        int64_t j[U], i[U];
+        double wk[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            j[u] = src[k + u * stride];
+            i[u] = dst[k + u * stride];
+            wk[u] = w ? static_cast<double>(w[k + u * stride]) : 1.0;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) norm[k + u * stride] = static_cast<float>(dinv[j[u]] * wk[u] * dinv[i[u]]);
+    }
+    for (; k < E; k += stride) {
         const double wk = w ? static_cast<double>(w[k]) : 1.0;
         norm[k] = static_cast<float>(dinv[src[k]] * wk * dinv[dst[k]]);
     }
@@ -35,9 +53,10 @@ __global__ void k_edge_norm(const int64_t *__restrict__ src, const int64_t *__re
 
 using namespace pyg;
 
-extern "C" int pyg_gcn_norm_workspace(int64_t N, size_t *bytes) {
-    if (N < 0 || !bytes) return PYG_ERR_INVALID_ARG;
-    *bytes = align_up(static_cast<size_t>(N) * sizeof(double), 256) + 256;
+extern "C" int pyg_gcn_norm_workspace(int64_t E, int64_t N, size_t *bytes) {
+    if (E < 0 || N < 0 || !bytes) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    *bytes = align_up(static_cast<size_t>(N) * sizeof(double), 256) + degree_workspace(E, N);
     return PYG_OK;
 }
 
@@ -46,17 +65,22 @@ extern "C" int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight,
     if (E < 0 || N < 0 || (E > 0 && (!edge_index || !norm || N == 0))) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     size_t need;
-    pyg_gcn_norm_workspace(N, &need);
+    PYG_TRY(pyg_gcn_norm_workspace(E, N, &need));
     if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
     if (E == 0) return PYG_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
     double *d = static_cast<double *>(ws);
-    PYG_TRY(fill<double>(d, N, 0.0, s));
-    k_weighted_degree<<<grid_for(E, kBlock * 8), kBlock, 0, s>>>(edge_index + E, edge_weight, E, d);
-    PYG_LAUNCH_CHECK();
+    void *hist_ws = static_cast<char *>(ws) + align_up(static_cast<size_t>(N) * sizeof(double), 256);
+    if (edge_weight) {
+        PYG_TRY(fill<double>(d, N, 0.0, s));
+        k_weighted_degree<<<grid_for(E, kBlock * 8), kBlock, 0, s>>>(edge_index + E, edge_weight, E, d);
+        PYG_LAUNCH_CHECK();
+    } else {
+        PYG_TRY(count_targets_f64(edge_index + E, E, N, d, hist_ws, s));
+    }
     k_inv_sqrt<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(d, N);
     PYG_LAUNCH_CHECK();
-    k_edge_norm<<<grid_for(E, kBlock * 8), kBlock, 0, s>>>(edge_index, edge_index + E, edge_weight, E, d, norm);
+    k_edge_norm<<<grid_for(E, kBlock * 4, 1 << 16), kBlock, 0, s>>>(edge_index, edge_index + E, edge_weight, E, d, norm);
     PYG_LAUNCH_CHECK();
     return PYG_OK;
 }

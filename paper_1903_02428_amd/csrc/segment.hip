@@ -302,36 +302,82 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
     if (lane == 0) p.head_row[c] = head;
 }
 
-// Fold the pieces of every long row, one wavefront per chunk that starts one.
+// Fold the pieces of every long row: one workgroup per chunk that starts a
+// long row. Piece 0 is the head partial (slot 2c+1), piece m >= 1 the
+// continuation in chunk c+m (slot 2(c+m)). The four waves fold contiguous,
+// ordered ranges of pieces with 8 loads in flight, then wave 0 combines the
+// four results in wave order: a fixed order, so the fold is deterministic,
+// and for max the earliest piece wins ties.
 template <typename T, bool MAXA>
 __global__ __launch_bounds__(kBlock) void k_segment_fixup(SegParams p) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
+    constexpr int kW = kBlock / kWave;
+    constexpr int kU = 8;
+    __shared__ float sv[kW][kWave];
+    __shared__ int32_t sp[kW][kWave];
+    const int64_t c = blockIdx.x;
     if (c >= p.nchunks) return;
     const int64_t r = p.head_row[c];
-    if (r < 0) return;
+    if (r < 0) return;  // uniform over the workgroup
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
     const int64_t s = p.rowptr[r], t = p.rowptr[r + 1];
-    const int64_t cB = (t - 1) / p.chunk;
+    const int64_t K = (t - 1) / p.chunk - c + 1;  // pieces of this row
+    const int64_t m0 = K * wave / kW, m1 = K * (wave + 1) / kW;
     T *out = static_cast<T *>(p.out);
-    for (int64_t fo = lane; fo < p.fcnt; fo += kWave) {
-        const int64_t f = p.fbase + fo;
-        float v = p.part_val[(2 * c + 1) * p.F + f];
-        int32_t ps = MAXA ? p.part_pos[(2 * c + 1) * p.F + f] : 0;
-        for (int64_t cc = c + 1; cc <= cB; ++cc) {
-            const float o = p.part_val[(2 * cc) * p.F + f];
-            if constexpr (MAXA) {
-                if (o > v) {  // later pieces hold later slots: strict > keeps the lowest
-                    v = o;
-                    ps = p.part_pos[(2 * cc) * p.F + f];
+    for (int64_t fg = 0; fg < p.fcnt; fg += kWave) {
+        const int64_t f = p.fbase + fg + lane;
+        const bool on = fg + lane < p.fcnt;
+        float v = 0.f;
+        int32_t ps = -1;
+        for (int64_t m = m0; m < m1; m += kU) {
+            float o[kU];
+            int32_t op[kU];
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int64_t mm = m + u;
+                const int64_t slot = mm == 0 ? 2 * c + 1 : 2 * (c + mm);
+                const bool ok = on && mm < m1;
+                o[u] = ok ? p.part_val[slot * p.F + f] : 0.f;
+                op[u] = (ok && MAXA) ? p.part_pos[slot * p.F + f] : -1;
+            }
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                if (m + u >= m1) break;
+                if constexpr (MAXA) {
+                    if (ps < 0 || o[u] > v) {  // later pieces hold later slots: strict > keeps the earliest
+                        v = o[u];
+                        ps = op[u];
+                    }
+                } else {
+                    v += o[u];
                 }
-            } else {
-                v += o;
             }
         }
-        if (!MAXA && p.mean) v = v / static_cast<float>(t - s);
-        if constexpr (sizeof(T) == 2) out[r * p.F + f] = f32_to_bf16_rne(v);
-        else out[r * p.F + f] = v;
-        if constexpr (MAXA) p.argmax[r * p.F + f] = p.perm ? p.perm[ps] : static_cast<int64_t>(ps);
+        sv[wave][lane] = v;
+        sp[wave][lane] = ps;
+        __syncthreads();
+        if (wave == 0 && on) {
+            float acc = sv[0][lane];
+            int32_t pos = sp[0][lane];
+#pragma unroll
+            for (int w = 1; w < kW; ++w) {
+                const float o = sv[w][lane];
+                const int32_t op = sp[w][lane];
+                if constexpr (MAXA) {
+                    if (op >= 0 && (pos < 0 || o > acc)) {
+                        acc = o;
+                        pos = op;
+                    }
+                } else if (K * (w + 1) / kW > K * w / kW) {  // skip waves that folded no piece
+                    acc += o;
+                }
+            }
+            if (!MAXA && p.mean) acc = acc / static_cast<float>(t - s);
+            if constexpr (sizeof(T) == 2) out[r * p.F + f] = f32_to_bf16_rne(acc);
+            else out[r * p.F + f] = acc;
+            if constexpr (MAXA) p.argmax[r * p.F + f] = p.perm ? p.perm[pos] : static_cast<int64_t>(pos);
+        }
+        __syncthreads();
     }
 }
 
@@ -351,7 +397,7 @@ int launch_window(const SegParams &p, hipStream_t s) {
     k_segment<T, VEC, NS, U, MSG, MAXA, IDENT><<<grid, kBlock, 0, s>>>(p);
     PYG_LAUNCH_CHECK();
     if (p.nchunks > 1) {
-        k_segment_fixup<T, MAXA><<<grid, kBlock, 0, s>>>(p);
+        k_segment_fixup<T, MAXA><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
         PYG_LAUNCH_CHECK();
     }
     return PYG_OK;

@@ -58,7 +58,7 @@ def test_workspace_queries_monotone(lib):
         last = b
     last = 0
     for N in (1, 100, 10**5):
-        rc, b = _ws(lib.pyg_gcn_norm_workspace, N)
+        rc, b = _ws(lib.pyg_gcn_norm_workspace, 1000, N)
         assert rc == PYG_OK and b >= N * 8 and b >= last
         last = b
     for kernel in (0, 1, 2):
@@ -112,9 +112,10 @@ def test_propagate_rejects_bad_arguments(lib):
 
 
 def test_other_entry_points_reject_bad_arguments(lib):
-    assert lib.pyg_degree(None, 5, 4, FAKE, None) == INVALID
-    assert lib.pyg_degree(FAKE, 5, 4, None, None) == INVALID
-    assert lib.pyg_degree(FAKE, 5, 2**31, FAKE, None) == UNSUPPORTED
+    assert lib.pyg_degree(None, 5, 4, FAKE, FAKE, 1 << 30, None) == INVALID
+    assert lib.pyg_degree(FAKE, 5, 4, None, FAKE, 1 << 30, None) == INVALID
+    assert lib.pyg_degree(FAKE, 5, 2**31, FAKE, FAKE, 1 << 30, None) == UNSUPPORTED
+    assert lib.pyg_degree(FAKE, 5, 4, FAKE, FAKE, 0, None) == WORKSPACE
     assert lib.pyg_coo_to_csr(FAKE, 5, 4, None, None, FAKE, FAKE, None, FAKE, 1 << 30, None) == INVALID
     assert lib.pyg_coo_to_csr(FAKE, 5, 4, None, FAKE, FAKE, FAKE, None, FAKE, 0, None) == WORKSPACE
     assert lib.pyg_gcn_norm(FAKE, None, 5, 4, FAKE, FAKE, 0, None) == WORKSPACE
