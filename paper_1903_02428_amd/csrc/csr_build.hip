@@ -26,10 +26,17 @@
 namespace pyg {
 namespace {
 
-constexpr int kItems = 16;                                  // keys per thread per tile
+#ifndef PYG_RADIX_ITEMS
+#define PYG_RADIX_ITEMS 16
+#endif
+#ifndef PYG_RADIX_BITS
+#define PYG_RADIX_BITS 9
+#endif
+constexpr int kItems = PYG_RADIX_ITEMS;                     // keys per thread per tile
 constexpr int kWaveKeys = kWave * kItems;                   // keys ranked by one wavefront
-constexpr int64_t kTile = (int64_t)kBlock * kItems;         // keys per tile (4096)
-constexpr int kMaxDigitBits = 9;
+constexpr int64_t kTile = (int64_t)kBlock * kItems;         // keys per tile
+constexpr int kMaxDigitBits = PYG_RADIX_BITS;               // widest digit of one pass
+static_assert(kTile <= 65536, "tile-local indices are staged as 16-bit");
 constexpr int kMaxRadix = 1 << kMaxDigitBits;
 constexpr int kWaves = kBlock / kWave;
 
@@ -164,13 +171,18 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist(const int64_t *__restrict
 
 // One stable scatter pass. Tile element order: wave w owns elements
 // [w*1024, (w+1)*1024) of the tile, visited 64 at a time in lane order.
+// Every global read is coalesced: each field (key, edge id, source, weight)
+// is loaded in tile order, scattered into LDS in sorted order, and written
+// out run by run, so no pass gathers from global memory.
 __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64, const float *__restrict__ w_in,
     Payload in, Payload out, int64_t *__restrict__ perm, int32_t *__restrict__ col, float *__restrict__ wcsr,
     int64_t E, int shift, int bits, int64_t ntiles, const uint32_t *__restrict__ offsets, int last) {
     __shared__ uint32_t wcnt[kWaves][kMaxRadix];  // per-wave running counts, then per-wave prefixes
     __shared__ uint32_t start[kMaxRadix];         // first staged slot of each digit in the tile
-    __shared__ uint16_t stage[kTile];             // tile-local index of the element in sorted slot j
+    __shared__ int64_t gbase[kMaxRadix];          // global slot of staged slot 0 of each digit run
+    __shared__ uint32_t stage[kTile];             // one field of the tile, in sorted order
+    __shared__ uint16_t sdig[kTile];              // digit of each sorted slot
     const int radix = 1 << bits;
     const uint32_t mask = radix - 1;
     const int lane = threadIdx.x & (kWave - 1);
@@ -179,39 +191,35 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     const int64_t tbase = tile * kTile;
     const int64_t tlen = (E - tbase) < kTile ? (E - tbase) : kTile;
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+    const int64_t ebase = tbase + wave * kWaveKeys + lane;  // element of round r: ebase + r * 64
 
     for (int i = lane; i < radix; i += kWave) wcnt[wave][i] = 0;
     __builtin_amdgcn_wave_barrier();
 
     // phase A: load this wave's keys, rank each against earlier equal digits
-    uint32_t dig[kItems];
-    uint32_t rk[kItems];
-    {
-        uint32_t key[kItems];
+    uint32_t key[kItems], dig[kItems], slot[kItems];
 #pragma unroll
-        for (int r = 0; r < kItems; ++r) {
-            const int64_t i = tbase + wave * kWaveKeys + r * kWave + lane;
-            key[r] = (i < E) ? (dst64 ? static_cast<uint32_t>(dst64[i]) : in.key[i]) : 0u;
-        }
+    for (int r = 0; r < kItems; ++r) {
+        const int64_t i = ebase + r * kWave;
+        key[r] = (i < E) ? (dst64 ? static_cast<uint32_t>(dst64[i]) : in.key[i]) : 0u;
+    }
 #pragma unroll
-        for (int r = 0; r < kItems; ++r) {
-            const int64_t i = tbase + wave * kWaveKeys + r * kWave + lane;
-            const bool valid = i < E;
-            const uint32_t d = (key[r] >> shift) & mask;
-            uint64_t peers = __ballot(valid);
-            for (int b = 0; b < bits; ++b) {
-                const bool bit = (d >> b) & 1u;
-                const uint64_t bal = __ballot(bit);
-                peers &= bit ? bal : ~bal;
-            }
-            const uint32_t before = __popcll(peers & lt_mask);
-            const uint32_t base = valid ? wcnt[wave][d] : 0u;
-            __builtin_amdgcn_wave_barrier();
-            if (valid && before == 0) wcnt[wave][d] = base + __popcll(peers);
-            __builtin_amdgcn_wave_barrier();
-            dig[r] = valid ? d : 0xFFFFFFFFu;
-            rk[r] = base + before;
+    for (int r = 0; r < kItems; ++r) {
+        const bool valid = ebase + r * kWave < E;
+        const uint32_t d = (key[r] >> shift) & mask;
+        uint64_t peers = __ballot(valid);
+        for (int b = 0; b < bits; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t bal = __ballot(bit);
+            peers &= bit ? bal : ~bal;
         }
+        const uint32_t before = __popcll(peers & lt_mask);
+        const uint32_t base = valid ? wcnt[wave][d] : 0u;
+        __builtin_amdgcn_wave_barrier();
+        if (valid && before == 0) wcnt[wave][d] = base + __popcll(peers);
+        __builtin_amdgcn_wave_barrier();
+        dig[r] = valid ? d : 0xFFFFFFFFu;
+        slot[r] = base + before;
     }
     __syncthreads();
 
@@ -228,23 +236,23 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     }
     __syncthreads();
     if (threadIdx.x < kWave) {
-        // one wave scans up to 512 digit totals: 8 per lane, then a lane prefix
-        constexpr int per = kMaxRadix / kWave;
+        // one wave scans up to 512 digit totals: a few per lane, then a lane prefix
+        constexpr int per = (kMaxRadix + kWave - 1) / kWave;
         uint32_t v[per];
-        uint32_t s = 0;
+        uint32_t sum = 0;
 #pragma unroll
         for (int j = 0; j < per; ++j) {
             const int t = lane * per + j;
             v[j] = t < radix ? start[t] : 0u;
-            s += v[j];
+            sum += v[j];
         }
-        uint32_t incl = s;
+        uint32_t incl = sum;
 #pragma unroll
         for (int d = 1; d < kWave; d <<= 1) {
             const uint32_t y = __shfl_up(incl, d, kWave);
             if (lane >= d) incl += y;
         }
-        uint32_t run = incl - s;
+        uint32_t run = incl - sum;
 #pragma unroll
         for (int j = 0; j < per; ++j) {
             const int t = lane * per + j;
@@ -253,48 +261,59 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
         }
     }
     __syncthreads();
-
-    // phase C: stage the tile-local permutation in sorted order
+    for (int t = threadIdx.x; t < radix; t += kBlock)
+        gbase[t] = (int64_t)offsets[(int64_t)t * ntiles + tile] - (int64_t)start[t];
 #pragma unroll
-    for (int r = 0; r < kItems; ++r) {
-        if (dig[r] != 0xFFFFFFFFu) {
-            const uint32_t slot = start[dig[r]] + wcnt[wave][dig[r]] + rk[r];
-            stage[slot] = static_cast<uint16_t>(wave * kWaveKeys + r * kWave + lane);
-        }
-    }
-    __syncthreads();
+    for (int r = 0; r < kItems; ++r)
+        if (dig[r] != 0xFFFFFFFFu) slot[r] += start[dig[r]] + wcnt[wave][dig[r]];
 
-    // phase D: write each digit run contiguously
-    for (int64_t j = threadIdx.x; j < tlen; j += kBlock) {
-        const int64_t li = stage[j];
-        if (li >= tlen) continue;  // cannot happen for a consistent ranking; keeps reads in bounds
-        const int64_t i = tbase + li;
-        uint32_t key, id, src;
-        float wv = 0.f;
-        if (dst64) {
-            key = static_cast<uint32_t>(dst64[i]);
-            id = static_cast<uint32_t>(i);
-            src = static_cast<uint32_t>(src64[i]);
-            if (w_in) wv = w_in[i];
-        } else {
-            key = in.key[i];
-            id = in.id[i];
-            src = in.src[i];
-            if (in.w) wv = in.w[i];
+    // field 0: the key (and the digit of every sorted slot)
+#pragma unroll
+    for (int r = 0; r < kItems; ++r)
+        if (dig[r] != 0xFFFFFFFFu && slot[r] < kTile) {
+            stage[slot[r]] = key[r];
+            sdig[slot[r]] = static_cast<uint16_t>(dig[r]);
         }
-        const uint32_t d = (key >> shift) & mask;
-        const int64_t pos = (int64_t)offsets[(int64_t)d * ntiles + tile] + (j - start[d]);
-        if (pos < 0 || pos >= E) continue;  // likewise: writes stay in bounds
-        if (last) {
-            perm[pos] = id;
-            col[pos] = static_cast<int32_t>(src);
-            if (wcsr) wcsr[pos] = wv;
-            out.key[pos] = key;
-        } else {
-            out.key[pos] = key;
-            out.id[pos] = id;
-            out.src[pos] = src;
-            if (out.w) out.w[pos] = wv;
+    __syncthreads();
+    uint32_t *key_out = out.key;
+    for (int64_t j = threadIdx.x; j < tlen; j += kBlock) {
+        const int64_t pos = gbase[sdig[j]] + j;
+        if (pos >= 0 && pos < E) key_out[pos] = stage[j];  // bounds hold for a consistent ranking
+    }
+
+    // fields 1..3: edge id, source, weight
+    for (int fld = 1; fld <= 3; ++fld) {
+        if (fld == 3 && !(dst64 ? w_in : in.w)) break;
+        __syncthreads();  // stage[] free again
+        uint32_t v[kItems];
+#pragma unroll
+        for (int r = 0; r < kItems; ++r) {
+            const int64_t i = ebase + r * kWave;
+            uint32_t x = 0;
+            if (i < E) {
+                if (fld == 1) x = dst64 ? static_cast<uint32_t>(i) : in.id[i];
+                else if (fld == 2) x = dst64 ? static_cast<uint32_t>(src64[i]) : in.src[i];
+                else x = dst64 ? __float_as_uint(w_in[i]) : __float_as_uint(in.w[i]);
+            }
+            v[r] = x;
+        }
+#pragma unroll
+        for (int r = 0; r < kItems; ++r)
+            if (dig[r] != 0xFFFFFFFFu && slot[r] < kTile) stage[slot[r]] = v[r];
+        __syncthreads();
+        for (int64_t j = threadIdx.x; j < tlen; j += kBlock) {
+            const int64_t pos = gbase[sdig[j]] + j;
+            if (pos < 0 || pos >= E) continue;
+            const uint32_t x = stage[j];
+            if (last) {
+                if (fld == 1) perm[pos] = x;
+                else if (fld == 2) col[pos] = static_cast<int32_t>(x);
+                else if (wcsr) wcsr[pos] = __uint_as_float(x);
+            } else {
+                if (fld == 1) out.id[pos] = x;
+                else if (fld == 2) out.src[pos] = x;
+                else out.w[pos] = __uint_as_float(x);
+            }
         }
     }
 }
