@@ -34,6 +34,35 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 
+# Byte counters of the CSR propagate kernel (k_segment, fp32 weighted sum on
+# the large power-law graph) from two rocprofv3 --pmc runs of this script
+# (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), with the same counters on a
+# plain 1024 MiB device copy for scale; see profiles/propagate_c5_counters.md.
+# They describe the kernel sources with the recorded hash only: after any
+# change to those sources the traffic field is reported as null.
+COUNTERS = {
+    "source_hash": "78065fa0009c458b",
+    "fetch_kib": 24477539.2, "write_kib": 120952.9,
+    "copy_mib": 1024, "copy_fetch_kib": 524311.4, "copy_write_kib": 1048576.0,
+}
+KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp"]
+
+
+def measured_traffic():
+    """HBM-side bytes per propagate launch from the recorded counters, scaled
+    by the copy calibration; None if the kernel sources changed since."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest()[:16] != COUNTERS["source_hash"]:
+        return None
+    ref_kib = COUNTERS["copy_mib"] * 1024.0
+    fetch = COUNTERS["fetch_kib"] * ref_kib / COUNTERS["copy_fetch_kib"]
+    write = COUNTERS["write_kib"] * ref_kib / COUNTERS["copy_write_kib"]
+    return (fetch + write) * 1024.0
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -45,6 +74,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-detail", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=float, default=0.08, help="fraction of target rows in the CPU sample")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one plain device copy of this size (for scaling rocprofv3 byte counters)")
     return ap.parse_args()
 
 
@@ -143,6 +174,14 @@ def main():
         step(False)
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} steps done")
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)  # reads and writes exactly copy_calibration_mib MiB
+        torch.cuda.synchronize()
+        del a, b
+        log(f"calibration copy of {args.copy_calibration_mib} MiB done")
 
     wall = 0.0
     for k in range(args.steps):
@@ -178,7 +217,7 @@ def main():
                    "N": N, "E": E, "F": F, "seed": args.seed, "chunk": args.chunk or "default",
                    "step": "degree+gcn_norm+coo_to_csr+propagate(sum,csr)+global_pool(mean)"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
                      "kernel": "pyg_propagate CSR segment (k_segment + k_segment_fixup), fp32 weighted sum",
                      "bytes_per_launch": balg, "avg_launch_ms": t_prop * 1e3},
         "detail": {"per_call_ms": {n: float(np.mean(times[n])) for n in names},

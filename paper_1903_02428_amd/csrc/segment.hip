@@ -155,13 +155,21 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
         for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(x + r * p.F + f0[sl]) : LN::zero();
     }
 
+    // column indices and weights stream once: read them 64 at a time,
+    // non-temporally, one batch ahead of the gathers that use them
+    int nxc = 0;
+    float nxw = 1.f;
+    if (s + lane < t) {
+        nxc = IDENT ? static_cast<int>(s + lane) : __builtin_nontemporal_load(p.col + s + lane);
+        if constexpr (MSG == kMsgWeighted) nxw = __builtin_nontemporal_load(p.w + s + lane);
+    }
     for (int64_t base = s; base < t; base += kWave) {
         const int n = static_cast<int>(uniform64((t - base) < kWave ? (t - base) : kWave));
-        int myc = 0;
-        float myw = 1.f;
-        if (lane < n) {
-            myc = IDENT ? static_cast<int>(base + lane) : p.col[base + lane];
-            if constexpr (MSG == kMsgWeighted) myw = p.w[base + lane];
+        const int myc = nxc;
+        const float myw = nxw;
+        if (base + kWave + lane < t) {
+            nxc = IDENT ? static_cast<int>(base + kWave + lane) : __builtin_nontemporal_load(p.col + base + kWave + lane);
+            if constexpr (MSG == kMsgWeighted) nxw = __builtin_nontemporal_load(p.w + base + kWave + lane);
         }
         for (int st = 0; st < n; st += S * U) {
             int jj[U];
