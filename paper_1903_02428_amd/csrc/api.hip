@@ -57,7 +57,7 @@ extern "C" int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t 
         return PYG_ERR_INVALID_ARG;
     if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
     const size_t coo = coo_workspace(dtype, N, F, aggr);
-    const size_t csr = segment_workspace(E, F, aggr, chunk);
+    const size_t csr = segment_workspace(E, F, aggr, chunk, N);
     *bytes = kernel == PYG_KERNEL_COO_ATOMIC ? coo : (kernel == PYG_KERNEL_CSR_SEGMENT ? csr : (coo > csr ? coo : csr));
     return PYG_OK;
 }
@@ -111,13 +111,14 @@ extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, con
     a.sentinel = E;
     a.out = out;
     a.argmax = argmax;
+    a.hint = true;
     return segment_reduce(a, ws, ws_bytes, s);
 }
 
 extern "C" int pyg_global_pool_workspace(int dtype, int64_t N, int64_t F, int64_t B, int aggr, size_t *bytes) {
     if (!bytes || !valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || B < 0) return PYG_ERR_INVALID_ARG;
     if (N >= kMax32 || B >= kMax32) return PYG_ERR_UNSUPPORTED;
-    *bytes = align_up(static_cast<size_t>(B + 1) * sizeof(int64_t), 256) + segment_workspace(N, F, aggr, 0);
+    *bytes = align_up(static_cast<size_t>(B + 1) * sizeof(int64_t), 256) + segment_workspace(N, F, aggr, 0, B);
     return PYG_OK;
 }
 
