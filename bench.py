@@ -158,7 +158,7 @@ def main():
         pyg.degree(ei, N, out=deg, workspace=ws_deg)
         mark("degree", 1)
         mark("gcn_norm", 0)
-        pyg.gcn_norm(ei, N, out=norm, workspace=ws_norm)
+        pyg.gcn_norm(ei, N, out=norm, workspace=ws_norm, deg=deg)  # reuses the in-degree of the step
         mark("gcn_norm", 1)
         mark("coo_to_csr", 0)
         pyg.coo_to_csr(ei, N, norm, chunk=args.chunk, out=csr, workspace=ws_csr)

@@ -128,9 +128,12 @@ int pyg_gcn_norm_workspace(int64_t E, int64_t N, size_t *bytes);
  *   d_i = sum of w_k over edges with target i (w = 1 when edge_weight is NULL),
  *   norm_k = d_j^-1/2 * w_k * d_i^-1/2 for edge k = (j -> i), 0 where d = 0.
  * Computed in fp64 and rounded once to fp32.
+ *   deg  int64 [N] or NULL: the in-degree of this edge list as returned by
+ *        pyg_degree, reused instead of counting again; read only when
+ *        edge_weight is NULL (weighted degrees are always summed here);
  *   norm fp32 [E] output in COO order. */
 int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight, int64_t E, int64_t N,
-                 float *norm, void *ws, size_t ws_bytes, void *stream);
+                 const int64_t *deg, float *norm, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_propagate for this shape, aggregation and
  * kernel (pass the same chunk as csr->chunk; 0 = default). */

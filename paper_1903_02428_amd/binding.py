@@ -64,7 +64,7 @@ def library() -> ctypes.CDLL:
             "pyg_coo_to_csr_workspace": [i64, i64, sz],
             "pyg_coo_to_csr": [p, i64, i64, p, p, p, p, p, p, ctypes.c_size_t, p],
             "pyg_gcn_norm_workspace": [i64, i64, sz],
-            "pyg_gcn_norm": [p, p, i64, i64, p, p, ctypes.c_size_t, p],
+            "pyg_gcn_norm": [p, p, i64, i64, p, p, p, ctypes.c_size_t, p],
             "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                               ctypes.c_size_t, p],
@@ -192,17 +192,23 @@ def coo_to_csr(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tens
 
 
 def gcn_norm(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None,
-             out: torch.Tensor | None = None, workspace: torch.Tensor | None = None) -> torch.Tensor:
+             out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+             deg: torch.Tensor | None = None) -> torch.Tensor:
+    """GCN edge norms; `deg` may pass the in-degree already computed by degree()."""
     lib = library()
     E = _edge_index(edge_index)
     dev = edge_index.device
     if edge_weight is not None:
         _need_cuda("edge_weight", edge_weight, torch.float32, 1)
+    if deg is not None:
+        _need_cuda("deg", deg, torch.int64, 1)
+        if deg.shape[0] != num_nodes:
+            raise ValueError("deg must be [N]")
     norm = torch.empty(E, dtype=torch.float32, device=dev) if out is None else out
     nbytes = _size(lib.pyg_gcn_norm_workspace, E, num_nodes)
     ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
-    _check(lib.pyg_gcn_norm(_ptr(edge_index), _ptr(edge_weight), E, num_nodes, _ptr(norm), _ptr(ws), nbytes,
-                            _stream(dev)), "pyg_gcn_norm")
+    _check(lib.pyg_gcn_norm(_ptr(edge_index), _ptr(edge_weight), E, num_nodes, _ptr(deg), _ptr(norm), _ptr(ws),
+                            nbytes, _stream(dev)), "pyg_gcn_norm")
     return norm
 
 

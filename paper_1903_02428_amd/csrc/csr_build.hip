@@ -30,7 +30,7 @@ namespace {
 #define PYG_RADIX_ITEMS 16
 #endif
 #ifndef PYG_RADIX_BITS
-#define PYG_RADIX_BITS 9
+#define PYG_RADIX_BITS 7  // 18-bit ids: three 6-bit passes, whose 64-key runs write whole lines
 #endif
 constexpr int kItems = PYG_RADIX_ITEMS;                     // keys per thread per tile
 constexpr int kWaveKeys = kWave * kItems;                   // keys ranked by one wavefront
@@ -318,13 +318,23 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     }
 }
 
-// rowptr from the sorted target ids: slot p starts every row in (key[p-1], key[p]].
+// rowptr from the sorted target ids: slot p starts every row in (key[p-1], key[p]]
+// (key[-1] = -1, key[E] = N). Each thread owns 4 consecutive slots.
 __global__ void k_row_bounds(const uint32_t *__restrict__ key, int64_t E, int64_t N, int64_t *__restrict__ rowptr) {
-    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p <= E; p += (int64_t)gridDim.x * blockDim.x) {
-        int64_t cur = p < E ? static_cast<int64_t>(key[p]) : N;
-        if (cur > N) cur = N;
-        const int64_t prev = p > 0 ? static_cast<int64_t>(key[p - 1]) : -1;
-        for (int64_t r = prev + 1; r <= cur; ++r) rowptr[r] = p;
+    const int64_t p0 = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+    if (p0 > E) return;
+    int64_t k[5];
+#pragma unroll
+    for (int i = 0; i < 5; ++i) {
+        const int64_t p = p0 - 1 + i;
+        int64_t v = p < 0 ? -1 : (p < E ? static_cast<int64_t>(key[p]) : N);
+        k[i] = v > N ? N : v;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t p = p0 + i;
+        if (p > E) break;
+        for (int64_t r = k[i] + 1; r <= k[i + 1]; ++r) rowptr[r] = p;
     }
 }
 
@@ -453,7 +463,7 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
         in = out;
         shift += bits;
     }
-    k_row_bounds<<<grid_for(E + 1, kBlock * 4), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
+    k_row_bounds<<<grid_for(E + 1, kBlock * 4, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
     PYG_LAUNCH_CHECK();
     return PYG_OK;
 }

@@ -60,8 +60,13 @@ extern "C" int pyg_gcn_norm_workspace(int64_t E, int64_t N, size_t *bytes) {
     return PYG_OK;
 }
 
+__global__ void k_count_to_f64(const int64_t *__restrict__ deg, int64_t N, double *__restrict__ d) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x)
+        d[i] = static_cast<double>(deg[i]);
+}
+
 extern "C" int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight, int64_t E, int64_t N,
-                            float *norm, void *ws, size_t ws_bytes, void *stream) {
+                            const int64_t *deg, float *norm, void *ws, size_t ws_bytes, void *stream) {
     if (E < 0 || N < 0 || (E > 0 && (!edge_index || !norm || N == 0))) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     size_t need;
@@ -74,6 +79,9 @@ extern "C" int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight,
     if (edge_weight) {
         PYG_TRY(fill<double>(d, N, 0.0, s));
         k_weighted_degree<<<grid_for(E, kBlock * 8), kBlock, 0, s>>>(edge_index + E, edge_weight, E, d);
+        PYG_LAUNCH_CHECK();
+    } else if (deg) {  // in-degree already counted (pyg_degree on the same edge list)
+        k_count_to_f64<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(deg, N, d);
         PYG_LAUNCH_CHECK();
     } else {
         PYG_TRY(count_targets_f64(edge_index + E, E, N, d, hist_ws, s));

@@ -118,8 +118,8 @@ def test_other_entry_points_reject_bad_arguments(lib):
     assert lib.pyg_degree(FAKE, 5, 4, FAKE, FAKE, 0, None) == WORKSPACE
     assert lib.pyg_coo_to_csr(FAKE, 5, 4, None, None, FAKE, FAKE, None, FAKE, 1 << 30, None) == INVALID
     assert lib.pyg_coo_to_csr(FAKE, 5, 4, None, FAKE, FAKE, FAKE, None, FAKE, 0, None) == WORKSPACE
-    assert lib.pyg_gcn_norm(FAKE, None, 5, 4, FAKE, FAKE, 0, None) == WORKSPACE
-    assert lib.pyg_gcn_norm(None, None, 5, 4, FAKE, FAKE, 1 << 20, None) == INVALID
+    assert lib.pyg_gcn_norm(FAKE, None, 5, 4, None, FAKE, FAKE, 0, None) == WORKSPACE
+    assert lib.pyg_gcn_norm(None, None, 5, 4, None, FAKE, FAKE, 1 << 20, None) == INVALID
     assert lib.pyg_global_pool(FAKE, 0, 10, 4, FAKE, 3, 2, ctypes.c_void_p(0x90000), None, FAKE, 1 << 30, None) == INVALID
     assert lib.pyg_global_pool(FAKE, 0, 10, 4, None, 3, 0, ctypes.c_void_p(0x90000), None, FAKE, 1 << 30, None) == INVALID
     assert lib.pyg_global_pool(FAKE, 0, 10, 4, FAKE, 3, 0, ctypes.c_void_p(0x90000), None, FAKE, 0, None) == WORKSPACE

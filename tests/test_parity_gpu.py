@@ -81,6 +81,10 @@ def test_gcn_norm(pyg, N, E, F, weighted):
         assert (np.abs(got.astype(np.float64) - ref) <= ulp).all()
     else:         # every fp64 step is exact-order: bit-identical to the rounded oracle
         assert np.array_equal(got, ref32)
+        # the same with the in-degree handed over from pyg_degree
+        d_ei = to_dev(ei_np)
+        got2 = pyg.gcn_norm(d_ei, N, deg=pyg.degree(d_ei, N)).cpu().numpy()
+        assert np.array_equal(got2, ref32)
 
 
 COMBOS = [(aggr, msg, kernel, dt) for aggr in ("sum", "mean", "max") for msg in ("src", "weighted", "diff")
