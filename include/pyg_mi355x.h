@@ -135,6 +135,19 @@ int pyg_gcn_norm_workspace(int64_t E, int64_t N, size_t *bytes);
 int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight, int64_t E, int64_t N,
                  const int64_t *deg, float *norm, void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes needed by pyg_gcn_norm_csr for N nodes. */
+int pyg_gcn_norm_csr_workspace(int64_t N, size_t *bytes);
+
+/* The same GCN normalisation computed on a CSR from pyg_coo_to_csr and
+ * written in CSR slot order, ready to serve as csr->weight of a propagate:
+ *   d_i = sum of the weights of row i's slots (csr->weight, or 1 when NULL),
+ *   norm_csr[p] = d_j^-1/2 * w_p * d_i^-1/2 for slot p of row i, j = col[p].
+ * Equal to pyg_gcn_norm's output gathered through csr->perm: bit for bit
+ * with unit weights; with weights the fp64 degree sums are ordered per row
+ * (deterministic) and may differ from another order by one fp32 ulp.
+ *   norm_csr fp32 [E] output (device). */
+int pyg_gcn_norm_csr(const pyg_csr *csr, float *norm_csr, void *ws, size_t ws_bytes, void *stream);
+
 /* Workspace bytes needed by pyg_propagate for this shape, aggregation and
  * kernel (pass the same chunk as csr->chunk; 0 = default). */
 int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int kernel,
@@ -146,9 +159,11 @@ int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr
  *   x           [N,F] fp32 or bf16 (dtype), 16-byte aligned rows give the
  *               vector path (F * sizeof(dtype) % 16 == 0), otherwise scalar;
  *   edge_index  [2,E] COO (required by the COO kernel; may be NULL for CSR);
- *   edge_weight fp32 [E] COO order or NULL. With the CSR kernel the weights
- *               are read from csr->weight, which must be non-NULL exactly
- *               when edge_weight is non-NULL. Not allowed with PYG_MSG_DIFF;
+ *   edge_weight fp32 [E] COO order or NULL, read by the COO kernel. The CSR
+ *               kernel reads the weights from csr->weight instead (the call
+ *               is weighted when csr->weight is set; edge_weight without
+ *               csr->weight is an error). Weights are not allowed with
+ *               PYG_MSG_DIFF;
  *   csr         CSR from pyg_coo_to_csr or NULL;
  *   out         [N,F] in x's dtype; fp32 accumulation, one rounding to bf16;
  *   argmax      int64 [N,F], required for PYG_MAX and NULL otherwise: the COO

@@ -20,6 +20,7 @@ from .binding import (  # noqa: F401
     coo_to_csr,
     degree,
     gcn_norm,
+    gcn_norm_csr,
     global_pool,
     library,
     library_path,

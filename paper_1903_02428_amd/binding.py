@@ -19,7 +19,8 @@ KERNEL = {"auto": 0, "coo": 1, "csr": 2}
 EXPORTED = [
     "pyg_strerror", "pyg_abi_version", "pyg_degree_workspace", "pyg_degree", "pyg_coo_to_csr_workspace",
     "pyg_coo_to_csr",
-    "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_propagate_workspace", "pyg_propagate",
+    "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_gcn_norm_csr_workspace", "pyg_gcn_norm_csr",
+    "pyg_propagate_workspace", "pyg_propagate",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
 ]
 
@@ -65,6 +66,8 @@ def library() -> ctypes.CDLL:
             "pyg_coo_to_csr": [p, i64, i64, p, p, p, p, p, p, ctypes.c_size_t, p],
             "pyg_gcn_norm_workspace": [i64, i64, sz],
             "pyg_gcn_norm": [p, p, i64, i64, p, p, p, ctypes.c_size_t, p],
+            "pyg_gcn_norm_csr_workspace": [i64, sz],
+            "pyg_gcn_norm_csr": [ctypes.POINTER(_Csr), p, p, ctypes.c_size_t, p],
             "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                               ctypes.c_size_t, p],
@@ -209,6 +212,19 @@ def gcn_norm(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor
     ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
     _check(lib.pyg_gcn_norm(_ptr(edge_index), _ptr(edge_weight), E, num_nodes, _ptr(deg), _ptr(norm), _ptr(ws),
                             nbytes, _stream(dev)), "pyg_gcn_norm")
+    return norm
+
+
+def gcn_norm_csr(csr: CSR, out: torch.Tensor | None = None, workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """GCN edge norms in CSR slot order (degrees from the CSR rows, weighted by
+    csr.weight when present); the result can serve as the weight of a CSR."""
+    lib = library()
+    dev = csr.rowptr.device
+    norm = torch.empty(csr.E, dtype=torch.float32, device=dev) if out is None else out
+    nbytes = _size(lib.pyg_gcn_norm_csr_workspace, csr.N)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
+    c = csr._c()
+    _check(lib.pyg_gcn_norm_csr(ctypes.byref(c), _ptr(norm), _ptr(ws), nbytes, _stream(dev)), "pyg_gcn_norm_csr")
     return norm
 
 

@@ -84,7 +84,8 @@ extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, con
     if (use_csr) {
         if (csr->N != N || csr->E != E || !csr->rowptr || csr->chunk < 0) return PYG_ERR_INVALID_ARG;
         if (E > 0 && (!csr->col || (aggr == PYG_MAX && !csr->perm))) return PYG_ERR_INVALID_ARG;
-        if ((edge_weight != nullptr) != (csr->weight != nullptr)) return PYG_ERR_INVALID_ARG;
+        if (edge_weight && !csr->weight) return PYG_ERR_INVALID_ARG;
+        if (msg == PYG_MSG_DIFF && csr->weight) return PYG_ERR_INVALID_ARG;
     } else if (E > 0 && !edge_index) {
         return PYG_ERR_INVALID_ARG;
     }
@@ -101,7 +102,7 @@ extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, con
     a.F = F;
     a.rowptr = csr->rowptr;
     a.col = csr->col;
-    a.weight = edge_weight ? csr->weight : nullptr;
+    a.weight = csr->weight;
     a.perm = csr->perm;
     a.n_rows = N;
     a.E = E;

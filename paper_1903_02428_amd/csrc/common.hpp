@@ -70,6 +70,36 @@ __device__ __forceinline__ float order_key_inv(uint32_t k) {
 // -0.0 -> +0.0 so that zeros tie when comparing for max.
 __device__ __forceinline__ float canon_zero(float m) { return m == 0.0f ? 0.0f : m; }
 
+// ---------------------------------------------------------- wave helpers
+
+// A wave-uniform 64-bit value in scalar registers.
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+    const uint64_t u = static_cast<uint64_t>(v);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32));
+    return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
+}
+
+// First index i in [0, len) with a[i] >= key; a is non-decreasing and
+// a[len - 1] >= key. 64-ary search: one coalesced probe per lane per level.
+__device__ inline int64_t wave_lower_bound(const int64_t *__restrict__ a, int64_t len, int64_t key, int lane) {
+    int64_t lo = 0, hi = len;
+    while (hi - lo > kWave) {
+        const int64_t step = (hi - lo + kWave - 1) / kWave;
+        int64_t idx = lo + (int64_t)(lane + 1) * step - 1;
+        if (idx > hi - 1) idx = hi - 1;
+        const uint64_t m = __ballot(a[idx] >= key);
+        if (m == 0) return len - 1;  // not monotone: malformed input, stay in bounds
+        const int lf = __ffsll(static_cast<unsigned long long>(m)) - 1;
+        const int64_t nhi = lo + (int64_t)(lf + 1) * step;
+        lo = lo + (int64_t)lf * step;
+        hi = nhi < hi ? nhi : hi;
+    }
+    const int64_t idx = lo + lane;
+    const uint64_t m = __ballot(idx >= hi || a[idx] >= key);
+    return m ? lo + (__ffsll(static_cast<unsigned long long>(m)) - 1) : len - 1;
+}
+
 // ------------------------------------------------------------ small kernels
 
 template <typename T>

@@ -48,10 +48,93 @@ __global__ __launch_bounds__(kBlock) void k_edge_norm(const int64_t *__restrict_
     }
 }
 
+// ----------------------------------------------------- CSR-ordered variant
+
+// dinv of every row from the row lengths (unit weights).
+__global__ void k_row_dinv_count(const int64_t *__restrict__ rowptr, int64_t N, double *__restrict__ dinv) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x) {
+        const double d = static_cast<double>(rowptr[i + 1] - rowptr[i]);
+        dinv[i] = d > 0.0 ? 1.0 / sqrt(d) : 0.0;
+    }
+}
+
+// dinv of every row from its CSR-ordered weights: one wavefront per row sums
+// in fp64 in a fixed order (lane-strided partial sums, then an xor butterfly).
+__global__ __launch_bounds__(kBlock) void k_row_dinv_weighted(const int64_t *__restrict__ rowptr,
+                                                              const float *__restrict__ w, int64_t N,
+                                                              double *__restrict__ dinv) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t r = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave); r < N; r += waves) {
+        const int64_t s = rowptr[r], t = rowptr[r + 1];
+        double acc = 0.0;
+        for (int64_t p = s + lane; p < t; p += kWave) acc += static_cast<double>(w[p]);
+        for (int off = kWave / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, kWave);
+        if (lane == 0) dinv[r] = acc > 0.0 ? 1.0 / sqrt(acc) : 0.0;
+    }
+}
+
+// norm_csr[p] = dinv[col[p]] * w[p] * dinv[row(p)]: one wavefront per chunk of
+// `chunk` slots; rows crossing chunk edges are simply split (slots are independent).
+__global__ __launch_bounds__(kBlock) void k_csr_edge_norm(const int64_t *__restrict__ rowptr, const int32_t *__restrict__ col,
+                                                          const float *__restrict__ w, int64_t N, int64_t E, int64_t chunk,
+                                                          const double *__restrict__ dinv, float *__restrict__ norm) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+    const int64_t e0 = c * chunk;
+    if (e0 >= E) return;
+    const int64_t e1 = (e0 + chunk) < E ? (e0 + chunk) : E;
+    // the row holding slot e0: last row with rowptr[r] <= e0
+    int64_t r = uniform64(wave_lower_bound(rowptr, N + 1, e0 + 1, lane)) - 1;
+    while (true) {
+        const int64_t s = uniform64(rowptr[r]), t = uniform64(rowptr[r + 1]);
+        const int64_t a = s > e0 ? s : e0, b = t < e1 ? t : e1;
+        const double di = dinv[r];
+        for (int64_t p = a + lane; p < b; p += kWave) {
+            const double wp = w ? static_cast<double>(w[p]) : 1.0;
+            norm[p] = static_cast<float>(dinv[col[p]] * wp * di);
+        }
+        if (t >= e1) break;
+        ++r;
+    }
+}
+
 }  // namespace
 }  // namespace pyg
 
 using namespace pyg;
+
+extern "C" int pyg_gcn_norm_csr_workspace(int64_t N, size_t *bytes) {
+    if (N < 0 || !bytes) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    *bytes = align_up(static_cast<size_t>(N) * sizeof(double), 256) + 256;
+    return PYG_OK;
+}
+
+extern "C" int pyg_gcn_norm_csr(const pyg_csr *csr, float *norm_csr, void *ws, size_t ws_bytes, void *stream) {
+    if (!csr || !csr->rowptr || csr->N < 0 || csr->E < 0) return PYG_ERR_INVALID_ARG;
+    const int64_t N = csr->N, E = csr->E;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    if (E > 0 && (!csr->col || !norm_csr || N == 0)) return PYG_ERR_INVALID_ARG;
+    size_t need;
+    PYG_TRY(pyg_gcn_norm_csr_workspace(N, &need));
+    if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
+    if (E == 0) return PYG_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    double *dinv = static_cast<double *>(ws);
+    if (csr->weight) {
+        k_row_dinv_weighted<<<grid_for(N, kBlock / kWave, 1 << 16), kBlock, 0, s>>>(csr->rowptr, csr->weight, N, dinv);
+    } else {
+        k_row_dinv_count<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(csr->rowptr, N, dinv);
+    }
+    PYG_LAUNCH_CHECK();
+    constexpr int64_t kChunk = 2048;
+    const int64_t nchunks = (E + kChunk - 1) / kChunk;
+    k_csr_edge_norm<<<static_cast<unsigned>((nchunks + 3) / 4), kBlock, 0, s>>>(csr->rowptr, csr->col, csr->weight, N, E,
+                                                                              kChunk, dinv, norm_csr);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
 
 extern "C" int pyg_gcn_norm_workspace(int64_t E, int64_t N, size_t *bytes) {
     if (E < 0 || N < 0 || !bytes) return PYG_ERR_INVALID_ARG;

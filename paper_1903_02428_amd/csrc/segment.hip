@@ -123,33 +123,6 @@ template <> struct Lane<uint16_t, false> {
     __device__ static void store(uint16_t *p, const float (&v)[N]) { *p = f32_to_bf16_rne(v[0]); }
 };
 
-__device__ __forceinline__ int64_t uniform64(int64_t v) {
-    const uint64_t u = static_cast<uint64_t>(v);
-    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
-    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32));
-    return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
-}
-
-// First index i in [0, len) with a[i] >= key; a is non-decreasing and
-// a[len - 1] >= key. 64-ary search: one coalesced probe per lane per level.
-__device__ int64_t wave_lower_bound(const int64_t *__restrict__ a, int64_t len, int64_t key, int lane) {
-    int64_t lo = 0, hi = len;
-    while (hi - lo > kWave) {
-        const int64_t step = (hi - lo + kWave - 1) / kWave;
-        int64_t idx = lo + (int64_t)(lane + 1) * step - 1;
-        if (idx > hi - 1) idx = hi - 1;
-        const uint64_t m = __ballot(a[idx] >= key);
-        if (m == 0) return len - 1;  // not monotone: malformed input, stay in bounds
-        const int lf = __ffsll(static_cast<unsigned long long>(m)) - 1;
-        const int64_t nhi = lo + (int64_t)(lf + 1) * step;
-        lo = lo + (int64_t)lf * step;
-        hi = nhi < hi ? nhi : hi;
-    }
-    const int64_t idx = lo + lane;
-    const uint64_t m = __ballot(idx >= hi || a[idx] >= key);
-    return m ? lo + (__ffsll(static_cast<unsigned long long>(m)) - 1) : len - 1;
-}
-
 // Degree class: 8 classes per octave, monotone in d, 0 for d <= 0.
 __device__ __forceinline__ int deg_class(int64_t d) {
     if (d <= 0) return 0;

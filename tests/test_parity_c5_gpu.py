@@ -51,6 +51,9 @@ def test_c5_degree_csr_norm_full(pyg, c5, dev_graph):
     assert np.array_equal(csr.weight.cpu().numpy(), w_ref[perm])
     # unit weights: every fp64 step is order-independent -> identical to the rounded oracle
     assert np.array_equal(pyg.gcn_norm(ei, N).cpu().numpy(), w_ref)
+    # the CSR-ordered normalisation the benchmark step uses
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E)
+    assert np.array_equal(pyg.gcn_norm_csr(plain).cpu().numpy(), w_ref[perm])
 
 
 def sample_rows(c5, n=1500):

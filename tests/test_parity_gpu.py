@@ -87,6 +87,22 @@ def test_gcn_norm(pyg, N, E, F, weighted):
         assert np.array_equal(got2, ref32)
 
 
+@pytest.mark.parametrize("N,E,F", SMALL)
+@pytest.mark.parametrize("weighted", [False, True])
+def test_gcn_norm_csr(pyg, N, E, F, weighted):
+    ei_np, _, w_np = graph(N, E, 3, F)
+    ei_np = synth.with_self_loops(ei_np, N)
+    w = np.concatenate([np.abs(w_np) + np.float32(0.5), np.ones(N, np.float32)]) if weighted else None
+    csr = pyg.coo_to_csr(to_dev(ei_np), N, to_dev(w) if weighted else None)
+    got = pyg.gcn_norm_csr(csr).cpu().numpy()
+    _, _, perm = oracle.coo_to_csr(ei_np, N)
+    ref = oracle.gcn_norm(ei_np, N, w)[perm]
+    if weighted:  # per-row fp64 sums in another order than the oracle's: at most one fp32 ulp
+        assert (np.abs(got.astype(np.float64) - ref) <= np.spacing(np.abs(ref.astype(np.float32)))).all()
+    else:
+        assert np.array_equal(got, ref.astype(np.float32))
+
+
 COMBOS = [(aggr, msg, kernel, dt) for aggr in ("sum", "mean", "max") for msg in ("src", "weighted", "diff")
           for kernel in ("coo", "csr") for dt in (F32, BF16)]
 
