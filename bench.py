@@ -74,6 +74,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-detail", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=float, default=0.08, help="fraction of target rows in the CPU sample")
+    ap.add_argument("--fig2", action="store_true",
+                    help="run the degree sweep of the paper's Fig. 2 (gather/scatter vs CSR, forward and backward) "
+                         "instead of the headline step; prints one JSON line per point")
+    ap.add_argument("--fig2-features", type=int, default=64)
+    ap.add_argument("--fig2-runs", type=int, default=1000)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for scaling rocprofv3 byte counters)")
     return ap.parse_args()
@@ -113,6 +118,9 @@ def main():
         build.build()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.fig2:
+        fig2_sweep(pyg, torch, synth, dev, args)
+        return
 
     t0 = time.time()
     c = synth.make_config(5, seed=args.seed)
@@ -234,6 +242,60 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(x_np, ei_np, w_ref, N, F, args.cpu_sample_rows, args.seed)
     print(json.dumps(result), flush=True)
+
+
+def fig2_sweep(pyg, torch, synth, dev, args):
+    """The paper's Fig. 2 on this GPU: Erdos-Renyi graphs with 10,000 nodes and
+    a swept average degree, edges in target order ("coalesced") or shuffled.
+    Forward = sum propagate; backward = its gradient with respect to x, the
+    propagate of grad_out over the transposed graph.
+      gs   : the COO atomic kernel, straight from the given edge order, both ways;
+      csr  : the CSR segment kernel; its forward uses a CSR built beforehand
+             (preprocessing, timed separately as csr_build); its backward must
+             first build the CSR of the transposed graph, which is timed inside.
+    Times are totals of `runs` back-to-back runs (HIP events), in ms."""
+    N, F, runs = 10_000, args.fig2_features, args.fig2_runs
+    rng = np.random.default_rng([args.seed, 2])
+    x = torch.randn(N, F, device=dev)
+    g = torch.randn(N, F, device=dev)
+    out = torch.empty_like(x)
+
+    def total_ms(fn):
+        fn()
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record()
+        for _ in range(runs):
+            fn()
+        e.record()
+        e.synchronize()
+        return s.elapsed_time(e)
+
+    for deg in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
+        for coalesced in (True, False):
+            ei_np = synth.erdos_renyi(N, deg, rng, coalesced)
+            E = ei_np.shape[1]
+            ei = torch.from_numpy(ei_np).to(dev)
+            eit = torch.from_numpy(np.ascontiguousarray(ei_np[::-1])).to(dev)  # transposed graph
+            csr = pyg.coo_to_csr(ei, N)
+            csr_t = pyg.coo_to_csr(eit, N)
+            ws_c = torch.empty(pyg.propagate_workspace_bytes(x, E, "sum", "coo"), dtype=torch.uint8, device=dev)
+            ws_s = torch.empty(pyg.propagate_workspace_bytes(x, E, "sum", "csr"), dtype=torch.uint8, device=dev)
+            import ctypes
+            sz = ctypes.c_size_t()
+            pyg.library().pyg_coo_to_csr_workspace(E, N, ctypes.byref(sz))
+            ws_b = torch.empty(sz.value, dtype=torch.uint8, device=dev)
+            rec = {
+                "metric": "fig2_gs_vs_csr", "n_nodes": N, "avg_degree": deg, "E": E, "F": F, "runs": runs,
+                "layout": "coalesced" if coalesced else "shuffled",
+                "gs_fwd_ms": total_ms(lambda: pyg.propagate(x, ei, kernel="coo", out=out, workspace=ws_c)),
+                "gs_bwd_ms": total_ms(lambda: pyg.propagate(g, eit, kernel="coo", out=out, workspace=ws_c)),
+                "csr_fwd_ms": total_ms(lambda: pyg.propagate(x, csr=csr, kernel="csr", out=out, workspace=ws_s)),
+                "csr_bwd_ms": total_ms(lambda: (pyg.coo_to_csr(eit, N, out=csr_t, workspace=ws_b),
+                                                pyg.propagate(g, csr=csr_t, kernel="csr", out=out, workspace=ws_s))),
+                "csr_build_ms": total_ms(lambda: pyg.coo_to_csr(ei, N, out=csr, workspace=ws_b)),
+            }
+            print(json.dumps(rec), flush=True)
 
 
 def timed(torch, fn, reps=10):

@@ -148,7 +148,7 @@ struct SegmentArgs {
     int64_t *argmax;    // [n_rows, F] or NULL
     bool hint;          // allow the cache-policy hint for hub source rows
 };
-int64_t segment_chunk(int64_t E, int64_t requested);
+int64_t segment_chunk(int64_t E, int64_t n_rows, int64_t requested);
 size_t segment_workspace(int64_t E, int64_t F, int aggr, int64_t chunk, int64_t n_rows);
 int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t s);
 

@@ -63,6 +63,7 @@ struct SegParams {
 // Measured on the large power-law graph (F = 128): fp32 rows (512 B) gain
 // 10 % with a 8-12 MB hot budget; bf16 rows (256 B) lose at every budget, so
 // the hint is used for rows of at least 512 B only.
+constexpr int64_t kLightMaxDegree = 8;           // mean row length up to which rows go to sub-groups
 constexpr int64_t kHintMinBytes = 8ll << 20;     // x larger than twice an XCD's L2
 constexpr int64_t kHintMinRowBytes = 512;
 constexpr int64_t kHotBudgetBytes = 12ll << 20;  // hot rows kept cacheable
@@ -296,7 +297,84 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
     }
 }
 
-template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT>
+// Light rows: one sub-group of L lanes reduces a whole short row alone, so a
+// wavefront works on S rows at once. `mine` is false for sub-groups without
+// a row; nothing below crosses sub-groups, so the branch may diverge.
+template <typename T, bool VEC, int U, int MSG, bool MAXA, bool IDENT>
+__device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t s, int64_t t, bool mine, int lane) {
+    using LN = Lane<T, VEC>;
+    using R = typename LN::R;
+    constexpr int EP = LN::N;
+    if (!mine) return;
+    const T *__restrict__ x = static_cast<const T *>(p.x);
+    const int q = lane & ((1 << p.lg_l) - 1);
+    const int64_t fo = (int64_t)q * EP;
+    const bool act = fo < p.fcnt;
+    const int64_t f0 = p.fbase + fo;
+    float acc[EP];
+    int32_t pos[EP];
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+        acc[e] = 0.f;
+        pos[e] = -1;
+    }
+    R xi = LN::zero();
+    if constexpr (MSG == kMsgDiff) xi = act ? LN::load(x + r * p.F + f0) : LN::zero();
+    for (int64_t base = s; base < t; base += U) {
+        int jj[U];
+        float ww[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {  // every lane of the sub-group reads the same slot
+            ok[u] = base + u < t;
+            jj[u] = ok[u] ? (IDENT ? static_cast<int>(base + u) : p.col[base + u]) : 0;
+            ww[u] = 1.f;
+            if constexpr (MSG == kMsgWeighted) ww[u] = ok[u] ? p.w[base + u] : 0.f;
+        }
+        R v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = (ok[u] && act) ? LN::load(x + (int64_t)jj[u] * p.F + f0) : LN::zero();
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (!ok[u]) continue;
+#pragma unroll
+            for (int e = 0; e < EP; ++e) {
+                const float xv = LN::get(v[u], e);
+                if constexpr (MAXA) {
+                    float m;
+                    if constexpr (MSG == kMsgDiff) m = xv - LN::get(xi, e);
+                    else if constexpr (MSG == kMsgWeighted) m = ww[u] * xv;
+                    else m = xv;
+                    m = canon_zero(m);
+                    if (pos[e] < 0 || m > acc[e]) {
+                        acc[e] = m;
+                        pos[e] = static_cast<int32_t>(base + u);
+                    }
+                } else {
+                    if constexpr (MSG == kMsgDiff) acc[e] += xv - LN::get(xi, e);
+                    else if constexpr (MSG == kMsgWeighted) acc[e] = fmaf(ww[u], xv, acc[e]);
+                    else acc[e] += xv;
+                }
+            }
+        }
+    }
+    if (!act) return;
+    float v[EP];
+    const int64_t deg = t - s;
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+        if constexpr (MAXA) v[e] = pos[e] >= 0 ? acc[e] : 0.f;
+        else v[e] = (p.mean && deg > 0) ? acc[e] / static_cast<float>(deg) : acc[e];
+    }
+    LN::store(static_cast<T *>(p.out) + r * p.F + f0, v);
+    if constexpr (MAXA) {
+        int64_t *ap = p.argmax + r * p.F + f0;
+#pragma unroll
+        for (int e = 0; e < EP; ++e) ap[e] = pos[e] < 0 ? p.sentinel : (p.perm ? p.perm[pos[e]] : static_cast<int64_t>(pos[e]));
+    }
+}
+
+template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool LIGHT>
 __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
@@ -317,6 +395,34 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
     }
     // rows whose first slot lies in [e0, e1) (the last chunk also takes the
     // empty rows that start at E)
+    if constexpr (LIGHT) {
+        const int S = kWave >> p.lg_l;
+        const int sg = lane >> p.lg_l;
+        int64_t rb = rA;
+        while (rb < p.n_rows) {
+            const int64_t rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
+            // rows rb .. rb+cnt-1 start in the chunk; lane i+1 holds the end of row rb+i
+            const bool in = lane < kWave - 1 && rb + lane < p.n_rows && (last || rp < e1);
+            const int cnt = __popcll(__ballot(in));
+            for (int i0 = 0; i0 < cnt; i0 += S) {
+                const int i = i0 + sg;
+                const int ii = i < cnt ? i : cnt - 1;
+                const int64_t s = __shfl(rp, ii, kWave), t = __shfl(rp, ii + 1, kWave);
+                const bool is_long = i < cnt && t - s > p.chunk;  // only the chunk's last row can be long
+                const uint64_t lm = __ballot(is_long);
+                if (lm) head = static_cast<int32_t>(rb + i0 + ((__ffsll(static_cast<unsigned long long>(lm)) - 1) >> p.lg_l));
+                light_row<T, VEC, U, MSG, MAXA, IDENT>(p, rb + i, s, t, i < cnt && !is_long, lane);
+            }
+            if (cnt < kWave - 1) break;  // the chunk's rows end in this batch
+            rb += cnt;
+        }
+        head = __builtin_amdgcn_readfirstlane(head);
+        if (head >= 0)
+            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT>(p, head, uniform64(p.rowptr[head]), e1, kPartial, 2 * c + 1,
+                                                          lane, 0);
+        if (lane == 0) p.head_row[c] = head;
+        return;
+    }
     int64_t rb = rA;
     int64_t rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
     for (int64_t r = rA; r < p.n_rows; ++r) {
@@ -452,10 +558,15 @@ __global__ void k_empty_rows(T *__restrict__ out, int64_t *__restrict__ argmax, 
 }
 
 template <typename T, bool VEC, int NS, int MSG, bool MAXA, bool IDENT>
-int launch_window(const SegParams &p, hipStream_t s) {
+int launch_window(const SegParams &p, bool light, hipStream_t s) {
     constexpr int U = NS == 1 ? 8 : (NS == 2 ? 4 : 2);
     const unsigned grid = static_cast<unsigned>((p.nchunks + (kBlock / kWave) - 1) / (kBlock / kWave));
-    k_segment<T, VEC, NS, U, MSG, MAXA, IDENT><<<grid, kBlock, 0, s>>>(p);
+    if constexpr (NS == 1) {
+        if (light) k_segment<T, VEC, NS, U, MSG, MAXA, IDENT, true><<<grid, kBlock, 0, s>>>(p);
+        else k_segment<T, VEC, NS, U, MSG, MAXA, IDENT, false><<<grid, kBlock, 0, s>>>(p);
+    } else {
+        k_segment<T, VEC, NS, U, MSG, MAXA, IDENT, false><<<grid, kBlock, 0, s>>>(p);
+    }
     PYG_LAUNCH_CHECK();
     if (p.nchunks > 1) {
         k_segment_fixup<T, MAXA><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
@@ -465,18 +576,18 @@ int launch_window(const SegParams &p, hipStream_t s) {
 }
 
 template <typename T, bool VEC, int MSG, bool MAXA, bool IDENT>
-int launch_ns(const SegParams &p, int ns, hipStream_t s) {
-    if (ns == 1) return launch_window<T, VEC, 1, MSG, MAXA, IDENT>(p, s);
-    if (ns == 2) return launch_window<T, VEC, 2, MSG, MAXA, IDENT>(p, s);
-    return launch_window<T, VEC, 4, MSG, MAXA, IDENT>(p, s);
+int launch_ns(const SegParams &p, int ns, bool light, hipStream_t s) {
+    if (ns == 1) return launch_window<T, VEC, 1, MSG, MAXA, IDENT>(p, light, s);
+    if (ns == 2) return launch_window<T, VEC, 2, MSG, MAXA, IDENT>(p, false, s);
+    return launch_window<T, VEC, 4, MSG, MAXA, IDENT>(p, false, s);
 }
 
 template <typename T, bool VEC, bool MAXA>
-int launch_msg(const SegParams &p, int msg, bool ident, int ns, hipStream_t s) {
-    if (ident) return launch_ns<T, VEC, kMsgSrc, MAXA, true>(p, ns, s);
-    if (msg == kMsgDiff) return launch_ns<T, VEC, kMsgDiff, MAXA, false>(p, ns, s);
-    if (msg == kMsgWeighted) return launch_ns<T, VEC, kMsgWeighted, MAXA, false>(p, ns, s);
-    return launch_ns<T, VEC, kMsgSrc, MAXA, false>(p, ns, s);
+int launch_msg(const SegParams &p, int msg, bool ident, int ns, bool light, hipStream_t s) {
+    if (ident) return launch_ns<T, VEC, kMsgSrc, MAXA, true>(p, ns, light, s);
+    if (msg == kMsgDiff) return launch_ns<T, VEC, kMsgDiff, MAXA, false>(p, ns, light, s);
+    if (msg == kMsgWeighted) return launch_ns<T, VEC, kMsgWeighted, MAXA, false>(p, ns, light, s);
+    return launch_ns<T, VEC, kMsgSrc, MAXA, false>(p, ns, light, s);
 }
 
 template <typename T>
@@ -515,9 +626,13 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
         const int ns = vn <= kWave ? 1 : (vn <= 2 * kWave ? 2 : 4);
         p.fbase = v0 * ep;
         p.fcnt = vn * ep;
+        // light rows: short rows on average and at least two sub-groups per wavefront
+        const bool light = ns == 1 && lg < 6 && a.E <= kLightMaxDegree * a.n_rows;
         int rc;
-        if (vec) rc = maxa ? launch_msg<T, true, true>(p, mk, ident, ns, s) : launch_msg<T, true, false>(p, mk, ident, ns, s);
-        else rc = maxa ? launch_msg<T, false, true>(p, mk, ident, ns, s) : launch_msg<T, false, false>(p, mk, ident, ns, s);
+        if (vec) rc = maxa ? launch_msg<T, true, true>(p, mk, ident, ns, light, s)
+                           : launch_msg<T, true, false>(p, mk, ident, ns, light, s);
+        else rc = maxa ? launch_msg<T, false, true>(p, mk, ident, ns, light, s)
+                       : launch_msg<T, false, false>(p, mk, ident, ns, light, s);
         if (rc != PYG_OK) return rc;
     }
     return PYG_OK;
@@ -549,20 +664,28 @@ SegWs carve_segment(void *base, int64_t E, int64_t F, int aggr, int64_t chunk, i
 
 }  // namespace
 
-int64_t segment_chunk(int64_t E, int64_t requested) {
+int64_t segment_chunk(int64_t E, int64_t n_rows, int64_t requested) {
     if (requested > 0) return requested;
-    int64_t c = 64;
-    while (c < 2048 && c * 32768 < E) c <<= 1;
+    int64_t c;
+    if (n_rows > 0 && E <= kLightMaxDegree * n_rows) {
+        // short rows: about 16 rows per wavefront
+        const int64_t avg = (E + n_rows - 1) / n_rows;
+        c = 16;
+        while (c < 16 * avg && c < 2048) c <<= 1;
+    } else {
+        c = 64;
+        while (c < 2048 && c * 32768 < E) c <<= 1;
+    }
     return c;
 }
 
 size_t segment_workspace(int64_t E, int64_t F, int aggr, int64_t chunk, int64_t n_rows) {
-    return carve_segment(nullptr, E, F, aggr, segment_chunk(E, chunk), n_rows).bytes;
+    return carve_segment(nullptr, E, F, aggr, segment_chunk(E, n_rows, chunk), n_rows).bytes;
 }
 
 int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t s) {
     if (a.n_rows == 0 || a.F == 0) return PYG_OK;
-    const int64_t chunk = segment_chunk(a.E, a.chunk);
+    const int64_t chunk = segment_chunk(a.E, a.n_rows, a.chunk);
     const SegWs w = carve_segment(ws, a.E, a.F, a.aggr, chunk, a.n_rows);
     if (ws_bytes < w.bytes || !ws) return PYG_ERR_WORKSPACE;
     SegParams p{};

@@ -12,6 +12,7 @@ from .graphs import (  # noqa: F401
     config3_minibatch,
     config4_knn_clouds,
     config5_large_power_law,
+    erdos_renyi,
     make_config,
     random_coo,
     rng_for,

@@ -188,6 +188,29 @@ def star_graph(N: int, hub: int = 0, rng: np.random.Generator | None = None) -> 
     return shuffle_edges(ei, rng) if rng is not None else ei
 
 
+def erdos_renyi(N: int, avg_degree: float, rng: np.random.Generator, coalesced: bool = False) -> np.ndarray:
+    """Directed Erdos-Renyi G(n, m) graph: m = round(N * avg_degree) distinct
+    pairs j -> i, j != i, uniform over all such pairs. `coalesced` orders the
+    edges by target (the CSR row), ascending source inside a target;
+    otherwise the order is random."""
+    M = int(round(N * avg_degree))
+    if M > N * (N - 1):
+        raise ValueError("too many edges")
+    keys = np.empty(0, np.int64)
+    while keys.size < M:
+        n = int((M - keys.size) * 1.1) + 16
+        j = rng.integers(0, N, n, dtype=np.int64)
+        i = rng.integers(0, N, n, dtype=np.int64)
+        ok = j != i
+        keys = _dedupe_keep_first(np.concatenate([keys, i[ok] * N + j[ok]]))
+    keys = keys[:M]
+    if coalesced:
+        keys = np.sort(keys)
+    else:
+        keys = keys[rng.permutation(M)]
+    return np.ascontiguousarray(np.stack([keys % N, keys // N]))
+
+
 # ----------------------------------------------------------------- configs
 
 def config1_sparse_uniform(seed: int = 0):

@@ -53,3 +53,13 @@ def test_config5_recipe_small():
     assert ei.shape == (2, 400_000 + 5000)
     assert _simple(ei[:, ~(ei[0] == ei[1])], 5000)
     assert (ei[0] == ei[1]).sum() == 5000
+
+
+def test_erdos_renyi_shapes():
+    rng = np.random.default_rng(0)
+    for coalesced in (False, True):
+        ei = synth.erdos_renyi(1000, 16, rng, coalesced)
+        assert ei.shape == (2, 16000) and not (ei[0] == ei[1]).any()
+        assert np.unique(ei[1] * 1000 + ei[0]).size == 16000
+        if coalesced:
+            assert (np.diff(ei[1] * 1000 + ei[0]) > 0).all()
