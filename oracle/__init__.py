@@ -57,8 +57,9 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_gcn_norm.argtypes = [p, p, i64, i64, p]
     lib.oracle_propagate.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p]
     lib.oracle_global_pool.argtypes = [p, i64, i64, p, i64, i32, p, p, p]
+    lib.oracle_propagate_backward.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p, p, p, p]
     for fn in (lib.oracle_degree, lib.oracle_coo_to_csr, lib.oracle_gcn_norm,
-               lib.oracle_propagate, lib.oracle_global_pool):
+               lib.oracle_propagate, lib.oracle_global_pool, lib.oracle_propagate_backward):
         fn.restype = ctypes.c_int
     return lib
 
@@ -145,3 +146,27 @@ def global_pool(x, batch, B: int, aggr: str = "sum", lib=None):
     _check(lib.oracle_global_pool(_ptr(x), N, F, _ptr(batch), B, AGGR[aggr], _ptr(out),
                                   _ptr(arg), _ptr(sabs)), "global_pool")
     return out, arg, sabs
+
+
+def propagate_backward(x, edge_index, grad_out, edge_weight=None, msg: str = "src", aggr: str = "sum",
+                       argmax=None, want_grad_w: bool = False, lib=None):
+    """Gradient of propagate for the upstream gradient grad_out. argmax is the
+    forward's (max only). Returns (grad_x fp64 [N,F], grad_w fp64 [E] or None,
+    sabs_x, sabs_w)."""
+    lib = lib or load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    N, F = x.shape
+    g = np.ascontiguousarray(grad_out, dtype=np.float32)
+    if g.shape != (N, F):
+        raise ValueError("grad_out must be [N, F]")
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    w = None if edge_weight is None else np.ascontiguousarray(edge_weight, dtype=np.float32)
+    arg = None if argmax is None else np.ascontiguousarray(argmax, dtype=np.int64)
+    gx = np.empty((N, F), np.float64)
+    sx = np.empty((N, F), np.float64)
+    gw = np.empty(E, np.float64) if want_grad_w else None
+    sw = np.empty(E, np.float64) if want_grad_w else None
+    _check(lib.oracle_propagate_backward(_ptr(x), N, F, _ptr(ei), E, _ptr(w), MSG[msg], AGGR[aggr], _ptr(g),
+                                         _ptr(arg), _ptr(gx), _ptr(gw), _ptr(sx), _ptr(sw)), "propagate_backward")
+    return gx, gw, sx, sw

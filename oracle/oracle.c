@@ -224,3 +224,95 @@ int oracle_global_pool(const float *x, int64_t N, int64_t F, const int64_t *batc
     free(node);
     return rc;
 }
+
+/* Gradient of oracle_propagate (Eq. (1), gamma = identity) for a given
+ * upstream gradient g = dL/d out [N,F]:
+ *   sum / mean: every edge k = (j -> i) passes s_i * g_i back, s_i = 1 (sum) or
+ *     1/deg_i (mean):  grad_x[j] += w_k s_i g_i,  grad_w[k] += s_i <g_i, x_j>;
+ *     for DIFF (phi = x_j - x_i):  grad_x[j] += s_i g_i,  grad_x[i] -= s_i g_i.
+ *   max: only the winning edge k = argmax[i,f] of each output element receives
+ *     it:  grad_x[j,f] += w_k g_{i,f},  grad_w[k] += g_{i,f} x_{j,f};
+ *     DIFF: grad_x[j,f] += g_{i,f}, grad_x[i,f] -= g_{i,f}. Empty rows pass nothing.
+ * argmax is the forward's (sentinel E for empty rows). grad_x fp64 [N,F];
+ * grad_w fp64 [E] (nullable; needs a weight and msg SRC); sabs_x / sabs_w
+ * (nullable) hold the sum of |terms| of each output. */
+int oracle_propagate_backward(const float *x, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                              const float *w, int msg, int aggr, const float *grad_out, const int64_t *argmax,
+                              double *grad_x, double *grad_w, double *sabs_x, double *sabs_w) {
+    if (N < 0 || F < 0 || E < 0) return ORACLE_ERR_ARG;
+    if (msg != ORACLE_MSG_SRC && msg != ORACLE_MSG_DIFF) return ORACLE_ERR_ARG;
+    if (aggr != ORACLE_SUM && aggr != ORACLE_MEAN && aggr != ORACLE_MAX) return ORACLE_ERR_ARG;
+    if (msg == ORACLE_MSG_DIFF && w) return ORACLE_ERR_ARG;
+    if (grad_w && (!w || msg != ORACLE_MSG_SRC)) return ORACLE_ERR_ARG;
+    if (N * F > 0 && (!x || !grad_out || !grad_x)) return ORACLE_ERR_ARG;
+    if (aggr == ORACLE_MAX && N * F > 0 && !argmax) return ORACLE_ERR_ARG;
+    if (E > 0 && !edge_index) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    if (!all_finite(x, N * F) || !all_finite(grad_out, N * F) || (w && !all_finite(w, E))) return ORACLE_ERR_NONFINITE;
+    for (int64_t t = 0; t < N * F; ++t) {
+        grad_x[t] = 0.0;
+        if (sabs_x) sabs_x[t] = 0.0;
+    }
+    for (int64_t k = 0; k < E && grad_w; ++k) {
+        grad_w[k] = 0.0;
+        if (sabs_w) sabs_w[k] = 0.0;
+    }
+    if (aggr == ORACLE_MAX) {
+        for (int64_t i = 0; i < N; ++i) {
+            for (int64_t f = 0; f < F; ++f) {
+                const int64_t k = argmax[i * F + f];
+                if (k == E) continue; /* empty row */
+                if (k < 0 || k > E || dst[k] != i) return ORACLE_ERR_INDEX;
+                const int64_t j = src[k];
+                const double g = grad_out[i * F + f];
+                if (msg == ORACLE_MSG_DIFF) {
+                    grad_x[j * F + f] += g;
+                    grad_x[i * F + f] -= g;
+                    if (sabs_x) {
+                        sabs_x[j * F + f] += fabs(g);
+                        sabs_x[i * F + f] += fabs(g);
+                    }
+                } else {
+                    const double wk = w ? (double)w[k] : 1.0;
+                    grad_x[j * F + f] += wk * g;
+                    if (sabs_x) sabs_x[j * F + f] += fabs(wk * g);
+                    if (grad_w) {
+                        grad_w[k] += g * (double)x[j * F + f];
+                        if (sabs_w) sabs_w[k] += fabs(g * (double)x[j * F + f]);
+                    }
+                }
+            }
+        }
+        return ORACLE_OK;
+    }
+    int64_t *deg = (int64_t *)calloc((size_t)(N > 0 ? N : 1), sizeof(int64_t));
+    if (!deg) return ORACLE_ERR_ARG;
+    for (int64_t k = 0; k < E; ++k) deg[dst[k]] += 1;
+    for (int64_t k = 0; k < E; ++k) {
+        const int64_t j = src[k], i = dst[k];
+        const double sc = aggr == ORACLE_MEAN ? 1.0 / (double)deg[i] : 1.0;
+        const double wk = w ? (double)w[k] : 1.0;
+        for (int64_t f = 0; f < F; ++f) {
+            const double g = sc * (double)grad_out[i * F + f];
+            if (msg == ORACLE_MSG_DIFF) {
+                grad_x[j * F + f] += g;
+                grad_x[i * F + f] -= g;
+                if (sabs_x) {
+                    sabs_x[j * F + f] += fabs(g);
+                    sabs_x[i * F + f] += fabs(g);
+                }
+            } else {
+                grad_x[j * F + f] += wk * g;
+                if (sabs_x) sabs_x[j * F + f] += fabs(wk * g);
+                if (grad_w) {
+                    grad_w[k] += g * (double)x[j * F + f];
+                    if (sabs_w) sabs_w[k] += fabs(g * (double)x[j * F + f]);
+                }
+            }
+        }
+    }
+    free(deg);
+    return ORACLE_OK;
+}

@@ -331,7 +331,82 @@ def pin_pool_relations(lib):
     assert np.array_equal(out[0], x.max(axis=0)) and np.array_equal(arg[0], x.argmax(axis=0))
 
 
+def pin_golden_backward(lib):
+    g = golden()
+    pr, b = g["propagate"], g["backward"]
+    x = np.array(pr["x"], np.float32)
+    ei = np.array(pr["edge_index"], np.int64)
+    w = np.array(pr["edge_weight"], np.float32)
+    go = np.array(b["grad_out"], np.float32)
+    gx, _, _, _ = oracle.propagate_backward(x, ei, go, aggr="sum", lib=lib)
+    assert np.array_equal(gx, np.array(b["sum_grad_x"]))
+    gx, gw, _, _ = oracle.propagate_backward(x, ei, go, w, aggr="sum", want_grad_w=True, lib=lib)
+    assert np.array_equal(gx, np.array(b["weighted_sum_grad_x"])) and np.array_equal(gw, np.array(b["weighted_sum_grad_w"]))
+    gx, _, _, _ = oracle.propagate_backward(x, ei, go, aggr="mean", lib=lib)
+    assert np.allclose(gx * 3.0, np.array(b["mean_grad_x_times_3"]), rtol=1e-15, atol=1e-15)
+    gx, _, _, _ = oracle.propagate_backward(x, ei, go, aggr="max", argmax=np.array(pr["src_argmax"]), lib=lib)
+    assert np.array_equal(gx, np.array(b["max_grad_x"]))
+    gx, _, _, _ = oracle.propagate_backward(x, ei, go, msg="diff", aggr="sum", lib=lib)
+    assert np.array_equal(gx, np.array(b["diff_sum_grad_x"]))
+
+
+def _torch_forward(x, ei, w, msg, aggr, N):
+    """An independent fp64 torch forward used only for its autograd."""
+    src, dst = torch.from_numpy(ei[0]), torch.from_numpy(ei[1])
+    if msg == "diff":
+        m = x[src] - x[dst]
+    else:
+        m = x[src] * (w[:, None] if w is not None else 1.0)
+    F = x.shape[1]
+    if aggr == "max":
+        base = torch.zeros(N, F, dtype=x.dtype)
+        return base.scatter_reduce(0, dst[:, None].expand(-1, F), m, "amax", include_self=False)
+    out = torch.zeros(N, F, dtype=x.dtype).index_add(0, dst, m)
+    if aggr == "mean":
+        deg = torch.bincount(dst, minlength=N).clamp(min=1).to(x.dtype)
+        out = out / deg[:, None]
+    return out
+
+
+def pin_backward_autograd(lib):
+    """torch autograd through an independent fp64 forward (tie-free data)."""
+    rng = np.random.default_rng(31)
+    for N, E in ((6, 14), (20, 90), (50, 300)):
+        ei = synth.random_coo(rng, N, E, duplicates=False)
+        F = 3
+        x = rng.standard_normal((N, F)).astype(np.float32)
+        w = rng.standard_normal(ei.shape[1]).astype(np.float32)
+        go = rng.standard_normal((N, F)).astype(np.float32)
+        for aggr in ("sum", "mean", "max"):
+            for msg, weighted in (("src", False), ("src", True), ("diff", False)):
+                xt = torch.tensor(x, dtype=torch.float64, requires_grad=True)
+                wt = torch.tensor(w, dtype=torch.float64, requires_grad=True) if weighted else None
+                out = _torch_forward(xt, ei, wt, msg, aggr, N)
+                out.backward(torch.tensor(go, dtype=torch.float64))
+                arg = None
+                if aggr == "max":
+                    _, arg, _ = oracle.propagate(x, ei, w if weighted else None, msg=msg, aggr="max", lib=lib)
+                gx, gw, _, _ = oracle.propagate_backward(x, ei, go, w if weighted else None, msg=msg, aggr=aggr,
+                                                         argmax=arg, want_grad_w=weighted, lib=lib)
+                assert np.allclose(gx, xt.grad.numpy(), rtol=1e-9, atol=1e-9), (aggr, msg, weighted)
+                if weighted:
+                    assert np.allclose(gw, wt.grad.numpy(), rtol=1e-9, atol=1e-9), (aggr, msg)
+
+
+def pin_backward_dense(lib):
+    """Sum backward = A^T g (dense fp64 matmul); grad w_k = <g_i, x_j>."""
+    for N, F, ei, x, w in small_cases():
+        rng = np.random.default_rng(N)
+        go = rng.standard_normal((N, F)).astype(np.float32)
+        A = dense_adjacency(ei, N, w)
+        gx, gw, sx, _ = oracle.propagate_backward(x, ei, go, w, aggr="sum", want_grad_w=True, lib=lib)
+        assert np.allclose(gx, A.T @ go.astype(np.float64), rtol=1e-12, atol=1e-12)
+        ref_w = (go.astype(np.float64)[ei[1]] * x.astype(np.float64)[ei[0]]).sum(axis=1)
+        assert np.allclose(gw, ref_w, rtol=1e-12, atol=1e-12)
+
+
 ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_golden_gcn_norm_directed,
             pin_golden_signed_zero,
             pin_degree_and_csr_library, pin_sum_mean_dense, pin_torch_scatter, pin_max_bruteforce,
-            pin_gcn_norm_closed_forms, pin_invariants, pin_pool_relations]
+            pin_gcn_norm_closed_forms, pin_invariants, pin_pool_relations, pin_golden_backward,
+            pin_backward_autograd, pin_backward_dense]

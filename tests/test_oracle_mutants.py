@@ -13,8 +13,8 @@ import oracle
 # (name, original text, mutated text); each original must occur in oracle.c
 MUTANTS = [
     ("propagate_swaps_src_dst",
-     "const int64_t *src = edge_index;\n    const int64_t *dst = edge_index + E;\n    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;\n    if (!all_finite",
-     "const int64_t *dst = edge_index;\n    const int64_t *src = edge_index + E;\n    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;\n    if (!all_finite"),
+     "return reduce_edges(x, N, F, src, dst, E, N, w, msg, aggr, out, argmax, sabs, E);",
+     "return reduce_edges(x, N, F, dst, src, E, N, w, msg, aggr, out, argmax, sabs, E);"),
     ("sum_overwrites", "out[o] += m;", "out[o] = m;"),
     ("diff_wrong_sign", "m = (double)xj - (double)x[i * F + f];", "m = (double)xj + (double)x[i * F + f];"),
     ("diff_max_wrong_operand", "if (msg == ORACLE_MSG_DIFF) m = xj - x[i * F + f];",
@@ -33,10 +33,18 @@ MUTANTS = [
     ("gcn_one_sided", "norm[k] = d[src[k]] * (w ? w[k] : 1.0) * d[dst[k]];", "norm[k] = d[dst[k]] * (w ? w[k] : 1.0) * d[dst[k]];"),
     ("csr_perm_is_source", "perm[p] = k;", "perm[p] = src[k];"),
     ("csr_col_is_target", "col[p] = src[k];", "col[p] = dst[k];"),
-    ("degree_counts_sources", "for (int64_t k = 0; k < E; ++k) deg[dst[k]] += 1;",
-     "for (int64_t k = 0; k < E; ++k) deg[edge_index[k]] += 1;"),
+    ("degree_counts_sources", "deg[i] = 0;\n    for (int64_t k = 0; k < E; ++k) deg[dst[k]] += 1;",
+     "deg[i] = 0;\n    for (int64_t k = 0; k < E; ++k) deg[edge_index[k]] += 1;"),
     ("pool_reads_first_node", "for (int64_t n = 0; n < N; ++n) node[n] = n;", "for (int64_t n = 0; n < N; ++n) node[n] = 0;"),
     ("pool_wrong_sentinel", "aggr, out, argmax, sabs, N);", "aggr, out, argmax, sabs, B);"),
+    ("bwd_grad_to_target", "                grad_x[j * F + f] += wk * g;\n                if (sabs_x) sabs_x[j * F + f] += fabs(wk * g);\n                if (grad_w) {\n                    grad_w[k] += g * (double)x[j * F + f];\n                    if (sabs_w) sabs_w[k] += fabs(g * (double)x[j * F + f]);\n                }\n            }\n        }\n    }\n    free(deg);",
+     "                grad_x[i * F + f] += wk * g;\n                if (sabs_x) sabs_x[j * F + f] += fabs(wk * g);\n                if (grad_w) {\n                    grad_w[k] += g * (double)x[j * F + f];\n                    if (sabs_w) sabs_w[k] += fabs(g * (double)x[j * F + f]);\n                }\n            }\n        }\n    }\n    free(deg);"),
+    ("bwd_mean_not_scaled", "const double sc = aggr == ORACLE_MEAN ? 1.0 / (double)deg[i] : 1.0;", "const double sc = 1.0;"),
+    ("bwd_grad_w_uses_target_x", "                    grad_w[k] += g * (double)x[j * F + f];\n                    if (sabs_w) sabs_w[k] += fabs(g * (double)x[j * F + f]);\n                }\n            }\n        }\n    }\n    free(deg);",
+     "                    grad_w[k] += g * (double)x[i * F + f];\n                    if (sabs_w) sabs_w[k] += fabs(g * (double)x[j * F + f]);\n                }\n            }\n        }\n    }\n    free(deg);"),
+    ("bwd_diff_drops_self_term", "                grad_x[j * F + f] += g;\n                grad_x[i * F + f] -= g;\n                if (sabs_x) {\n                    sabs_x[j * F + f] += fabs(g);\n                    sabs_x[i * F + f] += fabs(g);\n                }\n            } else {\n                grad_x[j * F + f] += wk * g;",
+     "                grad_x[j * F + f] += g;\n                if (sabs_x) {\n                    sabs_x[j * F + f] += fabs(g);\n                    sabs_x[i * F + f] += fabs(g);\n                }\n            } else {\n                grad_x[j * F + f] += wk * g;"),
+    ("bwd_max_ignores_weight", "                    const double wk = w ? (double)w[k] : 1.0;\n                    grad_x[j * F + f] += wk * g;", "                    const double wk = 1.0;\n                    grad_x[j * F + f] += wk * g;"),
 ]
 
 
