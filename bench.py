@@ -312,11 +312,9 @@ def timed(torch, fn, reps=10):
 
 
 def variants(pyg, torch, x, ei, csr, N, E, F, dev):
-    """Propagate-only times: CSR vs COO, fp32 vs bf16 storage, sum vs mean
-    (COO runs take the same norms, gathered back to COO order)."""
+    """Propagate-only times: CSR vs COO, fp32 vs bf16 storage, sum vs mean."""
     xb = x.to(torch.bfloat16)
-    norm = torch.empty_like(csr.weight)
-    norm[csr.perm] = csr.weight
+    norm = pyg.gcn_norm(ei, N)  # the same norms in COO order (equal bit for bit), for the COO kernel
     res = {}
     for dtname, xx, s in (("f32", x, 4), ("bf16", xb, 2)):
         o = torch.empty_like(xx)

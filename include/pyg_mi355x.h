@@ -120,6 +120,11 @@ int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, const float 
                    int64_t *rowptr, int32_t *col, int64_t *perm, float *weight_csr,
                    void *ws, size_t ws_bytes, void *stream);
 
+/* CSR-ordered copy of a COO-ordered edge array: out[p] = in[perm[p]] for
+ * p < E, with perm from pyg_coo_to_csr (e.g. fresh edge weights for an
+ * existing CSR). in and out are fp32 [E] device arrays and must differ. */
+int pyg_gather_edges(const int64_t *perm, int64_t E, const float *in, float *out, void *stream);
+
 /* Workspace bytes needed by pyg_gcn_norm for (E, N). */
 int pyg_gcn_norm_workspace(int64_t E, int64_t N, size_t *bytes);
 
@@ -178,6 +183,39 @@ int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F,
                   const int64_t *edge_index, int64_t E, const float *edge_weight,
                   const pyg_csr *csr, int msg, int aggr, int kernel,
                   void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_propagate_backward (chunk_t = csr_t->chunk). */
+int pyg_propagate_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int64_t chunk_t,
+                                     size_t *bytes);
+
+/* Gradient of pyg_propagate for an upstream gradient g = dL/d out (the
+ * backward pass that Appendix A compares for gather/scatter and SpMM):
+ *   sum / mean (s_i = 1 or 1/deg_i):
+ *     grad_x[j] = sum over edges k = (j -> i) of w_k s_i g_i, computed as a
+ *     propagate over the transposed graph; difference messages
+ *     (phi = x_j - x_i) add grad_x[i] -= deg_i s_i g_i;
+ *     grad_w[k] = s_i <g_i, x_j> (weighted source messages only).
+ *   max: each output element passes its gradient to its winning edge
+ *     k = argmax[i,f]: grad_x[j,f] += w_k g_{i,f}, grad_w[k] += g_{i,f} x_{j,f};
+ *     difference messages: grad_x[j,f] += g_{i,f}, grad_x[i,f] -= g_{i,f}.
+ * Arguments:
+ *   grad_out [N,F], x [N,F] (read only for grad_w), dtype of both;
+ *   edge_index [2,E] COO (max only), edge_weight fp32 [E] COO order or NULL:
+ *     the forward's weights; the call is weighted when it is non-NULL;
+ *   csr    the forward CSR (rows = targets): required for mean, difference
+ *          messages and grad_w (sum / mean);
+ *   csr_t  the CSR of the reversed edge list (rows = sources), built by
+ *          pyg_coo_to_csr from [edge_index[1]; edge_index[0]] with the same
+ *          weights: required for sum / mean;
+ *   argmax the forward's argmax [N,F] (max only);
+ *   grad_x [N,F] output in dtype (fp32 accumulation);
+ *   grad_w fp32 [E] output in COO order, or NULL to skip it.
+ * sum / mean results are deterministic; max scatters with float atomics, so
+ * colliding winners may sum in any order (last-bit differences). */
+int pyg_propagate_backward(const void *grad_out, const void *x, int dtype, int64_t N, int64_t F,
+                           const int64_t *edge_index, int64_t E, const float *edge_weight,
+                           const pyg_csr *csr, const pyg_csr *csr_t, int msg, int aggr, const int64_t *argmax,
+                           void *grad_x, float *grad_w, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_global_pool. */
 int pyg_global_pool_workspace(int dtype, int64_t N, int64_t F, int64_t B, int aggr, size_t *bytes);

@@ -14,18 +14,23 @@ from __future__ import annotations
 
 from .binding import (  # noqa: F401
     CSR,
+    Graph,
+    Propagate,
     LibraryMissing,
     PygError,
     abi_version,
     coo_to_csr,
     degree,
+    gather_edges,
     gcn_norm,
     gcn_norm_csr,
     global_pool,
     library,
     library_path,
     propagate,
+    propagate_backward,
     propagate_workspace_bytes,
+    reverse_edges,
     strerror,
     validate_batch,
     validate_coo,

@@ -18,9 +18,9 @@ KERNEL = {"auto": 0, "coo": 1, "csr": 2}
 
 EXPORTED = [
     "pyg_strerror", "pyg_abi_version", "pyg_degree_workspace", "pyg_degree", "pyg_coo_to_csr_workspace",
-    "pyg_coo_to_csr",
+    "pyg_coo_to_csr", "pyg_gather_edges",
     "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_gcn_norm_csr_workspace", "pyg_gcn_norm_csr",
-    "pyg_propagate_workspace", "pyg_propagate",
+    "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_backward_workspace", "pyg_propagate_backward",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
 ]
 
@@ -64,6 +64,7 @@ def library() -> ctypes.CDLL:
             "pyg_degree": [p, i64, i64, p, p, ctypes.c_size_t, p],
             "pyg_coo_to_csr_workspace": [i64, i64, sz],
             "pyg_coo_to_csr": [p, i64, i64, p, p, p, p, p, p, ctypes.c_size_t, p],
+            "pyg_gather_edges": [p, i64, p, p, p],
             "pyg_gcn_norm_workspace": [i64, i64, sz],
             "pyg_gcn_norm": [p, p, i64, i64, p, p, p, ctypes.c_size_t, p],
             "pyg_gcn_norm_csr_workspace": [i64, sz],
@@ -71,6 +72,9 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                               ctypes.c_size_t, p],
+            "pyg_propagate_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
+            "pyg_propagate_backward": [p, p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr),
+                                       i32, i32, p, p, p, p, ctypes.c_size_t, p],
             "pyg_global_pool_workspace": [i32, i64, i64, i64, i32, sz],
             "pyg_global_pool": [p, i32, i64, i64, p, i64, i32, p, p, p, ctypes.c_size_t, p],
             "pyg_validate_coo": [p, i64, i64, p, p],
@@ -194,6 +198,18 @@ def coo_to_csr(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tens
     return CSR(rowptr, col, perm, wcsr, num_nodes, E, chunk)
 
 
+def gather_edges(perm: torch.Tensor, values: torch.Tensor) -> torch.Tensor:
+    """values[perm] for a COO-ordered fp32 edge array (CSR slot order out)."""
+    _need_cuda("perm", perm, torch.int64, 1)
+    _need_cuda("values", values, torch.float32, 1)
+    if values.shape != perm.shape:
+        raise ValueError("perm and values must both be [E]")
+    out = torch.empty_like(values)
+    _check(library().pyg_gather_edges(_ptr(perm), perm.shape[0], _ptr(values), _ptr(out), _stream(perm.device)),
+           "pyg_gather_edges")
+    return out
+
+
 def gcn_norm(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None,
              out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
              deg: torch.Tensor | None = None) -> torch.Tensor:
@@ -275,6 +291,48 @@ def propagate(x: torch.Tensor, edge_index: torch.Tensor | None = None, edge_weig
     return out, argmax
 
 
+def reverse_edges(edge_index: torch.Tensor) -> torch.Tensor:
+    """[2,E] edge list with source and target swapped (the transposed graph)."""
+    return edge_index.flip(0).contiguous()
+
+
+def propagate_backward(grad_out: torch.Tensor, x: torch.Tensor | None = None, edge_index: torch.Tensor | None = None,
+                       edge_weight: torch.Tensor | None = None, csr: CSR | None = None, csr_t: CSR | None = None,
+                       aggr: str = "sum", msg: str = "src", argmax: torch.Tensor | None = None,
+                       need_grad_w: bool = False, workspace: torch.Tensor | None = None):
+    """Gradient of propagate. Returns (grad_x, grad_w or None). csr_t is the
+    CSR of reverse_edges(edge_index) built with the same weights (sum/mean)."""
+    lib = library()
+    _need_cuda("grad_out", grad_out, None, 2)
+    if grad_out.dtype not in DTYPE:
+        raise ValueError("grad_out must be float32 or bfloat16")
+    N, F = grad_out.shape
+    dev = grad_out.device
+    if edge_index is not None:
+        E = _edge_index(edge_index)
+    elif csr_t is not None:
+        E = csr_t.E
+    else:
+        raise ValueError("need edge_index or csr_t")
+    if x is not None:
+        _need_cuda("x", x, grad_out.dtype, 2)
+    if edge_weight is not None:
+        _need_cuda("edge_weight", edge_weight, torch.float32, 1)
+    grad_x = torch.empty_like(grad_out)
+    grad_w = torch.empty(E, dtype=torch.float32, device=dev) if need_grad_w else None
+    chunk_t = csr_t.chunk if csr_t is not None else 0
+    nbytes = _size(lib.pyg_propagate_backward_workspace, DTYPE[grad_out.dtype], N, F, E, AGGR[aggr], chunk_t)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
+    c = csr._c() if csr is not None else None
+    ct = csr_t._c() if csr_t is not None else None
+    rc = lib.pyg_propagate_backward(_ptr(grad_out), _ptr(x), DTYPE[grad_out.dtype], N, F, _ptr(edge_index), E,
+                                    _ptr(edge_weight), ctypes.byref(c) if c is not None else None,
+                                    ctypes.byref(ct) if ct is not None else None, MSG[msg], AGGR[aggr], _ptr(argmax),
+                                    _ptr(grad_x), _ptr(grad_w), _ptr(ws), ws.numel(), _stream(dev))
+    _check(rc, "pyg_propagate_backward")
+    return grad_x, grad_w
+
+
 def global_pool(x: torch.Tensor, batch: torch.Tensor, num_graphs: int, aggr: str = "sum",
                 out: torch.Tensor | None = None, argmax: torch.Tensor | None = None,
                 workspace: torch.Tensor | None = None):
@@ -315,3 +373,50 @@ def validate_batch(batch: torch.Tensor, num_graphs: int) -> int:
     _check(library().pyg_validate_batch(_ptr(batch), batch.shape[0], num_graphs, _ptr(bad), _stream(batch.device)),
            "pyg_validate_batch")
     return int(bad.item())
+
+
+class Graph:
+    """A graph prepared once for repeated propagates with gradients: the
+    forward CSR and the CSR of the transposed graph (both with the weights)."""
+
+    def __init__(self, edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None):
+        self.edge_index = edge_index
+        self.N = num_nodes
+        self.edge_weight = edge_weight
+        self.csr = coo_to_csr(edge_index, num_nodes, edge_weight)
+        self.csr_t = coo_to_csr(reverse_edges(edge_index), num_nodes, edge_weight)
+
+
+class Propagate(torch.autograd.Function):
+    """Differentiable propagate on the CSR segment kernel; the backward runs
+    pyg_propagate_backward (gradients for x and, when weighted, the weights).
+    Use as Propagate.apply(x, edge_weight_or_None, graph, aggr, msg)."""
+
+    @staticmethod
+    def forward(ctx, x, edge_weight, graph: Graph, aggr: str = "sum", msg: str = "src"):
+        csr = graph.csr
+        if edge_weight is not None:
+            # the CSR carries the weights in slot order: refresh them from the current tensor
+            csr = CSR(csr.rowptr, csr.col, csr.perm, gather_edges(csr.perm, edge_weight.detach().contiguous()),
+                      csr.N, csr.E, csr.chunk)
+        out, argmax = propagate(x.detach().contiguous(), graph.edge_index, None if edge_weight is None else
+                                edge_weight.detach(), csr=csr, aggr=aggr, msg=msg)
+        ctx.graph, ctx.aggr, ctx.msg = graph, aggr, msg
+        ctx.save_for_backward(x, edge_weight, argmax)
+        return out
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        x, edge_weight, argmax = ctx.saved_tensors
+        g = ctx.graph
+        csr, csr_t = g.csr, g.csr_t
+        if edge_weight is not None:
+            w = edge_weight.detach().contiguous()
+            csr = CSR(csr.rowptr, csr.col, csr.perm, gather_edges(csr.perm, w), csr.N, csr.E, csr.chunk)
+            csr_t = CSR(csr_t.rowptr, csr_t.col, csr_t.perm, gather_edges(csr_t.perm, w), csr_t.N, csr_t.E,
+                        csr_t.chunk)
+        need_w = edge_weight is not None and ctx.needs_input_grad[1]
+        gx, gw = propagate_backward(grad_out.contiguous(), x.detach().contiguous(), g.edge_index,
+                                    None if edge_weight is None else edge_weight.detach(), csr, csr_t,
+                                    ctx.aggr, ctx.msg, argmax, need_grad_w=need_w)
+        return gx, gw, None, None, None

@@ -338,6 +338,12 @@ __global__ void k_row_bounds(const uint32_t *__restrict__ key, int64_t E, int64_
     }
 }
 
+__global__ void k_gather_edges(const int64_t *__restrict__ perm, int64_t E, const float *__restrict__ in,
+                               float *__restrict__ out) {
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < E; p += (int64_t)gridDim.x * blockDim.x)
+        out[p] = in[perm[p]];
+}
+
 __global__ void k_validate_coo(const int64_t *__restrict__ ei, int64_t n, int64_t N, unsigned long long *__restrict__ bad) {
     unsigned long long local = 0;
     for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n; k += (int64_t)gridDim.x * blockDim.x)
@@ -485,6 +491,16 @@ extern "C" int pyg_validate_batch(const int64_t *batch, int64_t N, int64_t B, in
     PYG_TRY(fill<int64_t>(bad_count, 1, 0, s));
     if (N == 0) return PYG_OK;
     k_validate_batch<<<grid_for(N, kBlock * 8, 4096), kBlock, 0, s>>>(batch, N, B, reinterpret_cast<unsigned long long *>(bad_count));
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
+
+extern "C" int pyg_gather_edges(const int64_t *perm, int64_t E, const float *in, float *out, void *stream) {
+    if (E < 0 || (E > 0 && (!perm || !in || !out))) return PYG_ERR_INVALID_ARG;
+    if (E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    if (E > 0 && in == out) return PYG_ERR_INVALID_ARG;
+    if (E == 0) return PYG_OK;
+    k_gather_edges<<<grid_for(E, kBlock * 4), kBlock, 0, static_cast<hipStream_t>(stream)>>>(perm, E, in, out);
     PYG_LAUNCH_CHECK();
     return PYG_OK;
 }
