@@ -8,7 +8,9 @@ The arithmetic lives in ``oracle.c`` (plain C loops, fp64 accumulation),
 compiled with gcc into ``liboracle.so``. This module only marshals numpy
 arrays through ctypes. Every function follows Eq. (1) of the paper
 (Section 2, "Neighborhood Aggregation") with gamma = identity, or the
-"Global Pooling" / "Mini-batch Handling" paragraphs of Section 2.
+"Global Pooling" / "Mini-batch Handling" paragraphs of Section 2, or the
+attention operator GAT named there, whose sparse softmax Section 3 (runtime
+paragraph) singles out.
 """
 from __future__ import annotations
 
@@ -58,8 +60,15 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_propagate.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p]
     lib.oracle_global_pool.argtypes = [p, i64, i64, p, i64, i32, p, p, p]
     lib.oracle_propagate_backward.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p, p, p, p]
+    lib.oracle_gat_scores.argtypes = [p, p, i64, i64, p, i64, ctypes.c_float, p]
+    lib.oracle_segment_softmax.argtypes = [p, i64, i64, p, i64, p]
+    lib.oracle_segment_softmax_backward.argtypes = [p, p, i64, i64, p, i64, p, p]
+    lib.oracle_propagate_heads.argtypes = [p, i64, i64, i64, p, i64, p, p, p]
+    lib.oracle_propagate_heads_backward.argtypes = [p, i64, i64, i64, p, i64, p, p, p, p, p, p]
     for fn in (lib.oracle_degree, lib.oracle_coo_to_csr, lib.oracle_gcn_norm,
-               lib.oracle_propagate, lib.oracle_global_pool, lib.oracle_propagate_backward):
+               lib.oracle_propagate, lib.oracle_global_pool, lib.oracle_propagate_backward,
+               lib.oracle_gat_scores, lib.oracle_segment_softmax, lib.oracle_segment_softmax_backward,
+               lib.oracle_propagate_heads, lib.oracle_propagate_heads_backward):
         fn.restype = ctypes.c_int
     return lib
 
@@ -170,3 +179,103 @@ def propagate_backward(x, edge_index, grad_out, edge_weight=None, msg: str = "sr
     _check(lib.oracle_propagate_backward(_ptr(x), N, F, _ptr(ei), E, _ptr(w), MSG[msg], AGGR[aggr], _ptr(g),
                                          _ptr(arg), _ptr(gx), _ptr(gw), _ptr(sx), _ptr(sw)), "propagate_backward")
     return gx, gw, sx, sw
+
+
+def _scores2d(a, E: int, name: str, dtype=np.float32) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=dtype)
+    if a.ndim == 1:
+        a = a.reshape(E, 1)
+    if a.ndim != 2 or a.shape[0] != E:
+        raise ValueError(f"{name} must be [E, H]")
+    return a
+
+
+def gat_scores(a_src, a_dst, edge_index, slope: float = 0.2, lib=None) -> np.ndarray:
+    """GAT edge scores LeakyReLU(a_src[j] + a_dst[i]) per head, fp64 [E, H]."""
+    lib = lib or load()
+    a_src = np.ascontiguousarray(a_src, dtype=np.float32)
+    a_dst = np.ascontiguousarray(a_dst, dtype=np.float32)
+    if a_src.ndim != 2 or a_src.shape != a_dst.shape:
+        raise ValueError("a_src and a_dst must both be [N, H]")
+    N, H = a_src.shape
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    e = np.empty((E, H), np.float64)
+    _check(lib.oracle_gat_scores(_ptr(a_src), _ptr(a_dst), N, H, _ptr(ei), E, ctypes.c_float(slope), _ptr(e)),
+           "gat_scores")
+    return e
+
+
+def segment_softmax(scores, edge_index, N: int, lib=None) -> np.ndarray:
+    """Softmax of the scores [E, H] (or [E]) over the incoming edges of each
+    target, per head; fp64 [E, H]."""
+    lib = lib or load()
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    s = _scores2d(scores, E, "scores", np.float64)
+    H = s.shape[1]
+    alpha = np.empty((E, H), np.float64)
+    _check(lib.oracle_segment_softmax(_ptr(s), E, H, _ptr(ei), N, _ptr(alpha)), "segment_softmax")
+    return alpha
+
+
+def segment_softmax_backward(alpha, grad, edge_index, N: int, lib=None):
+    """Gradient of segment_softmax w.r.t. its scores. Returns (grad_s fp64 [E, H], sabs)."""
+    lib = lib or load()
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    a = _scores2d(alpha, E, "alpha")
+    g = _scores2d(grad, E, "grad")
+    if g.shape != a.shape:
+        raise ValueError("grad must match alpha")
+    H = a.shape[1]
+    gs = np.empty((E, H), np.float64)
+    sabs = np.empty((E, H), np.float64)
+    _check(lib.oracle_segment_softmax_backward(_ptr(a), _ptr(g), E, H, _ptr(ei), N, _ptr(gs), _ptr(sabs)),
+           "segment_softmax_backward")
+    return gs, sabs
+
+
+def propagate_heads(x, edge_index, alpha, H: int, lib=None):
+    """Sum over incoming edges of alpha[k, h] * x_j[h-th block of C columns];
+    x is [N, H*C]. Returns (out fp64 [N, H*C], sabs)."""
+    lib = lib or load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    N, F = x.shape
+    if H <= 0 or F % H:
+        raise ValueError("the feature width must be a multiple of H")
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    a = _scores2d(alpha, E, "alpha")
+    if a.shape[1] != H:
+        raise ValueError("alpha must be [E, H]")
+    out = np.empty((N, F), np.float64)
+    sabs = np.empty((N, F), np.float64)
+    _check(lib.oracle_propagate_heads(_ptr(x), N, H, F // H, _ptr(ei), E, _ptr(a), _ptr(out), _ptr(sabs)),
+           "propagate_heads")
+    return out, sabs
+
+
+def propagate_heads_backward(x, edge_index, alpha, grad_out, H: int, lib=None):
+    """Gradient of propagate_heads. Returns (grad_x fp64 [N, H*C], grad_alpha fp64 [E, H],
+    sabs_x, sabs_alpha)."""
+    lib = lib or load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    N, F = x.shape
+    if H <= 0 or F % H:
+        raise ValueError("the feature width must be a multiple of H")
+    g = np.ascontiguousarray(grad_out, dtype=np.float32)
+    if g.shape != (N, F):
+        raise ValueError("grad_out must be [N, F]")
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    a = _scores2d(alpha, E, "alpha")
+    if a.shape[1] != H:
+        raise ValueError("alpha must be [E, H]")
+    gx = np.empty((N, F), np.float64)
+    sx = np.empty((N, F), np.float64)
+    ga = np.empty((E, H), np.float64)
+    sa = np.empty((E, H), np.float64)
+    _check(lib.oracle_propagate_heads_backward(_ptr(x), N, H, F // H, _ptr(ei), E, _ptr(a), _ptr(g), _ptr(gx),
+                                               _ptr(ga), _ptr(sx), _ptr(sa)), "propagate_heads_backward")
+    return gx, ga, sx, sa

@@ -316,3 +316,174 @@ int oracle_propagate_backward(const float *x, int64_t N, int64_t F, const int64_
     free(deg);
     return ORACLE_OK;
 }
+
+/* ---------------------------------------------------------------------------
+ * Attention over incoming edges (Section 2 names GAT among the operators
+ * expressed by Eq. (1); Section 3, runtime paragraph, credits GAT's speed to
+ * a dedicated sparse softmax). With H attention heads every edge k carries
+ * H scores s[k,h] (row-major [E,H]).
+ * ------------------------------------------------------------------------- */
+
+/* GAT edge score for edge k = (j -> i) and head h:
+ *   e[k,h] = LeakyReLU(a_src[j,h] + a_dst[i,h]),  LeakyReLU(v) = v if v >= 0,
+ * slope * v otherwise. a_src / a_dst are the per-node halves of GAT's
+ * attention vector applied to the transformed features, fp32 [N,H]. The
+ * sum of two fp32 numbers and its product with an fp32 slope are exact in
+ * fp64. e is fp64 [E,H]. */
+int oracle_gat_scores(const float *a_src, const float *a_dst, int64_t N, int64_t H,
+                      const int64_t *edge_index, int64_t E, float slope, double *e) {
+    if (N < 0 || H < 0 || E < 0) return ORACLE_ERR_ARG;
+    if (E * H > 0 && (!a_src || !a_dst || !edge_index || !e)) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    if (!all_finite(a_src, N * H) || !all_finite(a_dst, N * H) || !isfinite(slope)) return ORACLE_ERR_NONFINITE;
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h) {
+            const double v = (double)a_src[src[k] * H + h] + (double)a_dst[dst[k] * H + h];
+            e[k * H + h] = v >= 0.0 ? v : (double)slope * v;
+        }
+    return ORACLE_OK;
+}
+
+/* Softmax over the incoming edges of every target, per head:
+ *   alpha[k,h] = exp(s[k,h] - m[i,h]) / sum_{k' : I[1,k'] = i} exp(s[k',h] - m[i,h]),
+ *   m[i,h] = max_{k' : I[1,k'] = i} s[k',h],  i = I[1,k].
+ * Subtracting the segment maximum leaves the value unchanged and keeps
+ * every exponential in (0, 1]. Targets without incoming edges own no
+ * entries. s fp64 [E,H]; alpha fp64 [E,H]. */
+int oracle_segment_softmax(const double *s, int64_t E, int64_t H, const int64_t *edge_index, int64_t N,
+                           double *alpha) {
+    if (N < 0 || H < 0 || E < 0) return ORACLE_ERR_ARG;
+    if (E * H > 0 && (!s || !edge_index || !alpha)) return ORACLE_ERR_ARG;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    for (int64_t t = 0; t < E * H; ++t)
+        if (!isfinite(s[t])) return ORACLE_ERR_NONFINITE;
+    double *m = (double *)malloc((size_t)(N * H > 0 ? N * H : 1) * sizeof(double));
+    double *den = (double *)malloc((size_t)(N * H > 0 ? N * H : 1) * sizeof(double));
+    if (!m || !den) {
+        free(m);
+        free(den);
+        return ORACLE_ERR_ARG;
+    }
+    for (int64_t t = 0; t < N * H; ++t) {
+        m[t] = -INFINITY;
+        den[t] = 0.0;
+    }
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h)
+            if (s[k * H + h] > m[dst[k] * H + h]) m[dst[k] * H + h] = s[k * H + h];
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h) den[dst[k] * H + h] += exp(s[k * H + h] - m[dst[k] * H + h]);
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h)
+            alpha[k * H + h] = exp(s[k * H + h] - m[dst[k] * H + h]) / den[dst[k] * H + h];
+    free(m);
+    free(den);
+    return ORACLE_OK;
+}
+
+/* Gradient of the segment softmax for an upstream gradient g = dL/d alpha:
+ *   grad_s[k,h] = alpha[k,h] * (g[k,h] - t[i,h]),  t[i,h] = sum_{k' in seg(i)} alpha[k',h] g[k',h].
+ * alpha and g fp32 [E,H] (alpha as the forward stored it); grad_s fp64;
+ * sabs (nullable) = |alpha g| + |alpha| sum_{k'} |alpha' g'|, the scale of
+ * the rounding error of any evaluation order. */
+int oracle_segment_softmax_backward(const float *alpha, const float *g, int64_t E, int64_t H,
+                                    const int64_t *edge_index, int64_t N, double *grad_s, double *sabs) {
+    if (N < 0 || H < 0 || E < 0) return ORACLE_ERR_ARG;
+    if (E * H > 0 && (!alpha || !g || !edge_index || !grad_s)) return ORACLE_ERR_ARG;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    if (!all_finite(alpha, E * H) || !all_finite(g, E * H)) return ORACLE_ERR_NONFINITE;
+    double *t = (double *)calloc((size_t)(N * H > 0 ? N * H : 1), sizeof(double));
+    double *ta = (double *)calloc((size_t)(N * H > 0 ? N * H : 1), sizeof(double));
+    if (!t || !ta) {
+        free(t);
+        free(ta);
+        return ORACLE_ERR_ARG;
+    }
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h) {
+            const double ag = (double)alpha[k * H + h] * (double)g[k * H + h];
+            t[dst[k] * H + h] += ag;
+            ta[dst[k] * H + h] += fabs(ag);
+        }
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h) {
+            const double a = alpha[k * H + h];
+            grad_s[k * H + h] = a * ((double)g[k * H + h] - t[dst[k] * H + h]);
+            if (sabs) sabs[k * H + h] = fabs(a * (double)g[k * H + h]) + fabs(a) * ta[dst[k] * H + h];
+        }
+    free(t);
+    free(ta);
+    return ORACLE_OK;
+}
+
+/* Attention-weighted aggregation with H heads (GAT's message alpha_{j,i} x_j
+ * under sum aggregation, Eq. (1), heads concatenated): x is [N, H*C] with
+ * head h owning columns h*C .. h*C+C-1, and
+ *   out[i, h*C + c] = sum_{k : I[1,k] = i} alpha[k,h] * x[I[0,k], h*C + c].
+ * alpha fp32 [E,H]; out fp64 [N, H*C]; sabs (nullable) = sum |term|. */
+int oracle_propagate_heads(const float *x, int64_t N, int64_t H, int64_t C, const int64_t *edge_index, int64_t E,
+                           const float *alpha, double *out, double *sabs) {
+    if (N < 0 || H < 0 || C < 0 || E < 0) return ORACLE_ERR_ARG;
+    const int64_t F = H * C;
+    if (N * F > 0 && (!x || !out)) return ORACLE_ERR_ARG;
+    if (E * H > 0 && (!alpha || !edge_index)) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    if (!all_finite(x, N * F) || !all_finite(alpha, E * H)) return ORACLE_ERR_NONFINITE;
+    for (int64_t t = 0; t < N * F; ++t) {
+        out[t] = 0.0;
+        if (sabs) sabs[t] = 0.0;
+    }
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h) {
+            const double a = alpha[k * H + h];
+            for (int64_t c = 0; c < C; ++c) {
+                const double term = a * (double)x[src[k] * F + h * C + c];
+                out[dst[k] * F + h * C + c] += term;
+                if (sabs) sabs[dst[k] * F + h * C + c] += fabs(term);
+            }
+        }
+    return ORACLE_OK;
+}
+
+/* Gradient of oracle_propagate_heads for g = dL/d out [N, H*C]:
+ *   grad_x[j, h*C + c] += alpha[k,h] g[i, h*C + c],
+ *   grad_alpha[k,h]     = sum_c g[i, h*C + c] x[j, h*C + c],   k = (j -> i).
+ * grad_x fp64 [N, H*C], grad_alpha fp64 [E,H] (nullable), sabs_* nullable. */
+int oracle_propagate_heads_backward(const float *x, int64_t N, int64_t H, int64_t C, const int64_t *edge_index,
+                                    int64_t E, const float *alpha, const float *g, double *grad_x,
+                                    double *grad_alpha, double *sabs_x, double *sabs_a) {
+    if (N < 0 || H < 0 || C < 0 || E < 0) return ORACLE_ERR_ARG;
+    const int64_t F = H * C;
+    if (N * F > 0 && (!x || !g || !grad_x)) return ORACLE_ERR_ARG;
+    if (E * H > 0 && (!alpha || !edge_index)) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    if (!all_finite(x, N * F) || !all_finite(g, N * F) || !all_finite(alpha, E * H)) return ORACLE_ERR_NONFINITE;
+    for (int64_t t = 0; t < N * F; ++t) {
+        grad_x[t] = 0.0;
+        if (sabs_x) sabs_x[t] = 0.0;
+    }
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h) {
+            const int64_t j = src[k], i = dst[k];
+            const double a = alpha[k * H + h];
+            double dot = 0.0, dabs = 0.0;
+            for (int64_t c = 0; c < C; ++c) {
+                const double gi = g[i * F + h * C + c];
+                grad_x[j * F + h * C + c] += a * gi;
+                if (sabs_x) sabs_x[j * F + h * C + c] += fabs(a * gi);
+                dot += gi * (double)x[j * F + h * C + c];
+                dabs += fabs(gi * (double)x[j * F + h * C + c]);
+            }
+            if (grad_alpha) grad_alpha[k * H + h] = dot;
+            if (sabs_a) sabs_a[k * H + h] = dabs;
+        }
+    return ORACLE_OK;
+}

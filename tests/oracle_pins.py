@@ -405,8 +405,154 @@ def pin_backward_dense(lib):
         assert np.allclose(gw, ref_w, rtol=1e-12, atol=1e-12)
 
 
+def _frac(a):
+    a = np.asarray(a, np.float64)
+    return a[..., 0] / a[..., 1]
+
+
+def pin_golden_attention(lib):
+    g = golden()["attention"]
+    ei = np.array(g["edge_index"], np.int64)
+    N, H = g["N"], g["H"]
+    s = np.log(np.array(g["scores_log_of"], np.float64))
+    s[:, 1] += g["head1_offset"]
+    alpha = oracle.segment_softmax(s, ei, N, lib=lib)
+    assert np.allclose(alpha, _frac(g["alpha_frac"]), rtol=1e-12, atol=0)
+    e = oracle.gat_scores(np.array(g["a_src"]), np.array(g["a_dst"]), ei, g["slope"], lib=lib)
+    assert np.array_equal(e, np.array(g["gat_scores"]))
+    a32 = _frac(g["alpha_frac"]).astype(np.float32)
+    gs, _ = oracle.segment_softmax_backward(a32, np.array(g["grad_alpha"]), ei, N, lib=lib)
+    assert np.allclose(gs, _frac(g["softmax_grad_frac"]), rtol=1e-6, atol=1e-7)
+    x = np.array(g["x"], np.float32)
+    out, _ = oracle.propagate_heads(x, ei, a32, H, lib=lib)
+    assert np.allclose(out, _frac(g["heads_out_frac"]), rtol=1e-6, atol=1e-7)
+    gx, ga, _, _ = oracle.propagate_heads_backward(x, ei, a32, np.array(g["grad_out"]), H, lib=lib)
+    assert np.allclose(gx, _frac(g["heads_grad_x_frac"]), rtol=1e-6, atol=1e-7)
+    assert np.array_equal(ga, np.array(g["heads_grad_alpha"]))
+
+
+def _attention_cases():
+    """Random multigraphs with isolated targets and H in 1..4 heads."""
+    rng = np.random.default_rng(4321)
+    out = []
+    for N, E, H in ((1, 3, 1), (5, 0, 2), (7, 20, 3), (16, 60, 1), (33, 200, 4), (64, 90, 2), (40, 300, 3)):
+        ei = synth.random_coo(rng, N, E)
+        s = (rng.standard_normal((E, H)) * 3.0).astype(np.float32)
+        out.append((N, H, ei, s, rng))
+    return out
+
+
+def pin_softmax_library(lib):
+    """Per-target softmax equals scipy.special.softmax of that target's scores."""
+    from scipy.special import softmax
+    for N, H, ei, s, _ in _attention_cases():
+        alpha = oracle.segment_softmax(s, ei, N, lib=lib)
+        for i in range(N):
+            k = np.flatnonzero(ei[1] == i)
+            if k.size:
+                assert np.allclose(alpha[k], softmax(s[k].astype(np.float64), axis=0), rtol=1e-13, atol=1e-15)
+
+
+def pin_softmax_invariants(lib):
+    """Sums to one per (target, head); shift by a per-target constant changes
+    nothing; one edge gives 1; two edges give the logistic function; edge
+    order only permutes the result; no overflow at large scores."""
+    from scipy.special import expit
+    for N, H, ei, s, rng in _attention_cases():
+        E = ei.shape[1]
+        alpha = oracle.segment_softmax(s, ei, N, lib=lib)
+        tot = np.zeros((N, H))
+        np.add.at(tot, ei[1], alpha)
+        has = np.bincount(ei[1], minlength=N) > 0
+        assert np.allclose(tot[has], 1.0, rtol=0, atol=1e-13) and np.all(tot[~has] == 0)
+        assert np.all(alpha > 0) and np.all(alpha <= 1)
+        shift = rng.integers(-500, 500, size=(N, H)).astype(np.float64)
+        shifted = oracle.segment_softmax(s.astype(np.float64) + shift[ei[1]], ei, N, lib=lib)
+        assert np.allclose(shifted, alpha, rtol=1e-12, atol=1e-15)
+        p = rng.permutation(E)
+        assert np.allclose(oracle.segment_softmax(s[p], ei[:, p], N, lib=lib), alpha[p], rtol=1e-14, atol=0)
+    ei = np.array([[0, 1, 2, 0], [1, 1, 2, 3]], np.int64)
+    s = np.array([[2.5, 700.0], [-1.0, 699.0], [40.0, -40.0], [-3.0, 0.0]])
+    alpha = oracle.segment_softmax(s, ei, 4, lib=lib)
+    assert np.allclose(alpha[0], expit(s[0] - s[1]), rtol=1e-14, atol=0)
+    assert np.allclose(alpha[1], expit(s[1] - s[0]), rtol=1e-14, atol=0)
+    assert np.array_equal(alpha[2:], np.ones((2, 2)))
+
+
+def _torch_softmax(s, dst, N):
+    """An independent fp64 segment softmax in torch, used for its autograd."""
+    H = s.shape[1]
+    idx = dst[:, None].expand(-1, H)
+    m = torch.full((N, H), -torch.inf, dtype=s.dtype).scatter_reduce(0, idx, s, "amax")
+    ex = torch.exp(s - m[dst])
+    den = torch.zeros(N, H, dtype=s.dtype).index_add(0, dst, ex)
+    return ex / den[dst]
+
+
+def pin_softmax_backward_autograd(lib):
+    """torch autograd through an independent forward; gradients sum to zero
+    over every segment (the softmax ignores a per-segment shift)."""
+    for N, H, ei, s, rng in _attention_cases():
+        E = ei.shape[1]
+        dst = torch.from_numpy(ei[1])
+        st = torch.tensor(s, dtype=torch.float64, requires_grad=True)
+        alpha = _torch_softmax(st, dst, N)
+        g = rng.standard_normal((E, H)).astype(np.float32)
+        alpha.backward(torch.tensor(g, dtype=torch.float64))
+        a32 = alpha.detach().numpy().astype(np.float32)
+        gs, sabs = oracle.segment_softmax_backward(a32, g, ei, N, lib=lib)
+        assert np.all(np.abs(gs - st.grad.numpy()) <= 1e-6 * sabs + 1e-12)
+        tot = np.zeros((N, H))
+        np.add.at(tot, ei[1], gs)
+        tabs = np.zeros((N, H))
+        np.add.at(tabs, ei[1], sabs)
+        assert np.all(np.abs(tot) <= 1e-6 * tabs + 1e-12)
+
+
+def pin_heads_dense(lib):
+    """Per head, the attention sum is a dense matmul with the alpha-weighted
+    adjacency; its backward is the transposed matmul and per-edge dots; one
+    head equals the weighted propagate."""
+    for N, H, ei, s, rng in _attention_cases():
+        E = ei.shape[1]
+        C = int(rng.integers(1, 4))
+        x = rng.standard_normal((N, H * C)).astype(np.float32)
+        a = rng.random((E, H)).astype(np.float32)
+        g = rng.standard_normal((N, H * C)).astype(np.float32)
+        out, _ = oracle.propagate_heads(x, ei, a, H, lib=lib)
+        gx, ga, _, _ = oracle.propagate_heads_backward(x, ei, a, g, H, lib=lib)
+        x64, g64 = x.astype(np.float64), g.astype(np.float64)
+        for h in range(H):
+            A = dense_adjacency(ei, N, a[:, h])
+            cols = slice(h * C, (h + 1) * C)
+            assert np.allclose(out[:, cols], A @ x64[:, cols], rtol=1e-12, atol=1e-12)
+            assert np.allclose(gx[:, cols], A.T @ g64[:, cols], rtol=1e-12, atol=1e-12)
+            ref = (g64[ei[1], cols] * x64[ei[0], cols]).sum(axis=1)
+            assert np.allclose(ga[:, h], ref, rtol=1e-12, atol=1e-12)
+        if H == 1:
+            ref, _, _ = oracle.propagate(x, ei, a[:, 0], aggr="sum", lib=lib)
+            assert np.array_equal(out, ref)
+
+
+def pin_uniform_attention_is_mean(lib):
+    """Equal scores give alpha = 1/deg, so the attention sum is the mean
+    aggregation of every head's block."""
+    for N, H, ei, _, rng in _attention_cases():
+        E = ei.shape[1]
+        a_node = np.zeros((N, H), np.float32)
+        e = oracle.gat_scores(a_node, a_node, ei, 0.2, lib=lib)
+        assert np.array_equal(e, np.zeros((E, H)))
+        alpha = oracle.segment_softmax(e, ei, N, lib=lib)
+        C = 2
+        x = rng.standard_normal((N, H * C)).astype(np.float32)
+        out, _ = oracle.propagate_heads(x, ei, alpha.astype(np.float32), H, lib=lib)
+        mean, _, _ = oracle.propagate(x, ei, aggr="mean", lib=lib)
+        assert np.allclose(out, mean, rtol=1e-6, atol=1e-6)
+
+
 ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_golden_gcn_norm_directed,
             pin_golden_signed_zero,
             pin_degree_and_csr_library, pin_sum_mean_dense, pin_torch_scatter, pin_max_bruteforce,
             pin_gcn_norm_closed_forms, pin_invariants, pin_pool_relations, pin_golden_backward,
-            pin_backward_autograd, pin_backward_dense]
+            pin_backward_autograd, pin_backward_dense, pin_golden_attention, pin_softmax_library,
+            pin_softmax_invariants, pin_softmax_backward_autograd, pin_heads_dense, pin_uniform_attention_is_mean]

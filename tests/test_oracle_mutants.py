@@ -45,6 +45,25 @@ MUTANTS = [
     ("bwd_diff_drops_self_term", "                grad_x[j * F + f] += g;\n                grad_x[i * F + f] -= g;\n                if (sabs_x) {\n                    sabs_x[j * F + f] += fabs(g);\n                    sabs_x[i * F + f] += fabs(g);\n                }\n            } else {\n                grad_x[j * F + f] += wk * g;",
      "                grad_x[j * F + f] += g;\n                if (sabs_x) {\n                    sabs_x[j * F + f] += fabs(g);\n                    sabs_x[i * F + f] += fabs(g);\n                }\n            } else {\n                grad_x[j * F + f] += wk * g;"),
     ("bwd_max_ignores_weight", "                    const double wk = w ? (double)w[k] : 1.0;\n                    grad_x[j * F + f] += wk * g;", "                    const double wk = 1.0;\n                    grad_x[j * F + f] += wk * g;"),
+    ("softmax_den_without_max", "den[dst[k] * H + h] += exp(s[k * H + h] - m[dst[k] * H + h]);",
+     "den[dst[k] * H + h] += exp(s[k * H + h]);"),
+    ("softmax_segment_by_source", "const int64_t *dst = edge_index + E;\n    if (check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;\n    for (int64_t t = 0; t < E * H; ++t)",
+     "const int64_t *dst = edge_index;\n    if (check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;\n    for (int64_t t = 0; t < E * H; ++t)"),
+    ("softmax_max_of_head0", "if (s[k * H + h] > m[dst[k] * H + h]) m[dst[k] * H + h] = s[k * H + h];",
+     "if (s[k * H] > m[dst[k] * H + h]) m[dst[k] * H + h] = s[k * H];"),
+    ("softmax_not_normalised", "alpha[k * H + h] = exp(s[k * H + h] - m[dst[k] * H + h]) / den[dst[k] * H + h];",
+     "alpha[k * H + h] = exp(s[k * H + h] - m[dst[k] * H + h]);"),
+    ("gat_slope_on_positive", "e[k * H + h] = v >= 0.0 ? v : (double)slope * v;", "e[k * H + h] = v >= 0.0 ? (double)slope * v : v;"),
+    ("gat_scores_swap_ends", "(double)a_src[src[k] * H + h] + (double)a_dst[dst[k] * H + h]",
+     "(double)a_src[dst[k] * H + h] + (double)a_dst[src[k] * H + h]"),
+    ("softmax_bwd_sign", "grad_s[k * H + h] = a * ((double)g[k * H + h] - t[dst[k] * H + h]);",
+     "grad_s[k * H + h] = a * ((double)g[k * H + h] + t[dst[k] * H + h]);"),
+    ("softmax_bwd_t_without_alpha", "const double ag = (double)alpha[k * H + h] * (double)g[k * H + h];",
+     "const double ag = (double)g[k * H + h];"),
+    ("heads_weight_of_head0", "const double a = alpha[k * H + h];\n            for (int64_t c = 0; c < C; ++c) {\n                const double term",
+     "const double a = alpha[k * H];\n            for (int64_t c = 0; c < C; ++c) {\n                const double term"),
+    ("heads_bwd_grad_to_target", "grad_x[j * F + h * C + c] += a * gi;", "grad_x[i * F + h * C + c] += a * gi;"),
+    ("heads_bwd_dot_uses_target_x", "dot += gi * (double)x[j * F + h * C + c];", "dot += gi * (double)x[i * F + h * C + c];"),
 ]
 
 
