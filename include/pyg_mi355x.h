@@ -70,6 +70,11 @@ typedef enum { PYG_MSG_SRC = 0, PYG_MSG_DIFF = 1 } pyg_msg;
  *   PYG_KERNEL_AUTO         CSR when a CSR is passed, else COO. */
 typedef enum { PYG_KERNEL_AUTO = 0, PYG_KERNEL_COO_ATOMIC = 1, PYG_KERNEL_CSR_SEGMENT = 2 } pyg_kernel;
 
+/* Order of per-edge arrays [E, H] of the attention calls:
+ *   PYG_ORDER_CSR  indexed by CSR slot (coalesced; what pyg_propagate_heads reads);
+ *   PYG_ORDER_COO  indexed by COO edge id, reached through csr->perm. */
+typedef enum { PYG_ORDER_CSR = 0, PYG_ORDER_COO = 1 } pyg_order;
+
 /* A target-sorted CSR built by pyg_coo_to_csr (device pointers).
  *   rowptr [N+1]  rowptr[i]..rowptr[i+1] are the CSR slots of target i;
  *   col    [E]    source node of each slot;
@@ -216,6 +221,58 @@ int pyg_propagate_backward(const void *grad_out, const void *x, int dtype, int64
                            const int64_t *edge_index, int64_t E, const float *edge_weight,
                            const pyg_csr *csr, const pyg_csr *csr_t, int msg, int aggr, const int64_t *argmax,
                            void *grad_x, float *grad_w, void *ws, size_t ws_bytes, void *stream);
+
+/* ---- Attention (GAT, an operator of Section 2; Section 3, runtime
+ * paragraph, credits its speed to a dedicated sparse softmax). Every edge
+ * carries H fp32 values per array, row-major [E, H], in the order `order`
+ * (pyg_order). The CSR fixes the segments: the incoming edges of each
+ * target. Targets without incoming edges own no entries. All results are
+ * bit-reproducible (fixed reduction orders). Sizes come from csr->N and
+ * csr->E (E < 2^31); errors: PYG_ERR_INVALID_ARG for a NULL pointer that is
+ * needed, H <= 0, an unknown order, or PYG_ORDER_COO without csr->perm. */
+
+/* Workspace bytes needed by the three softmax calls below (same for all;
+ * pass csr->chunk as chunk). */
+int pyg_segment_softmax_workspace(int64_t E, int64_t N, int64_t H, int64_t chunk, size_t *bytes);
+
+/* Softmax over the incoming edges of each target, per head h:
+ *   alpha[k,h] = exp(s[k,h] - m[i,h]) / sum_{k' -> i} exp(s[k',h] - m[i,h]),
+ *   m[i,h] = max_{k' -> i} s[k',h],  i = target of edge k.
+ * scores and alpha fp32 [E, H] (device), may not overlap. fp32 arithmetic:
+ * one online max/sum pass and one normalising pass. */
+int pyg_segment_softmax(const float *scores, int64_t H, const pyg_csr *csr, int order, float *alpha,
+                        void *ws, size_t ws_bytes, void *stream);
+
+/* GAT's attention coefficients in one call: the softmax above of the edge
+ * scores e[k,h] = LeakyReLU(a_src[j,h] + a_dst[i,h]) for edge k = (j -> i),
+ * LeakyReLU(v) = v for v >= 0 and negative_slope * v otherwise, computed on
+ * the fly (never stored). a_src, a_dst fp32 [N, H] (device): the per-node
+ * halves of GAT's attention vector applied to the transformed features. */
+int pyg_gat_softmax(const float *a_src, const float *a_dst, int64_t H, float negative_slope, const pyg_csr *csr,
+                    int order, float *alpha, void *ws, size_t ws_bytes, void *stream);
+
+/* Gradient of the softmax with respect to its scores, for the upstream
+ * gradient g = dL/d alpha:
+ *   grad_scores[k,h] = alpha[k,h] * (g[k,h] - sum_{k' -> i} alpha[k',h] g[k',h]).
+ * alpha, grad_alpha, grad_scores fp32 [E, H] (device); grad_scores may not
+ * overlap the inputs. */
+int pyg_segment_softmax_backward(const float *alpha, const float *grad_alpha, int64_t H, const pyg_csr *csr,
+                                 int order, float *grad_scores, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_propagate_heads (pass csr->chunk as chunk). */
+int pyg_propagate_heads_workspace(int dtype, int64_t N, int64_t H, int64_t C, int64_t E, int64_t chunk,
+                                  size_t *bytes);
+
+/* Attention-weighted sum with H heads (GAT's message alpha_{j,i} x_j under
+ * sum aggregation, Eq. (1), heads concatenated): x is [N, H*C] with head h
+ * owning columns h*C .. h*C+C-1, and
+ *   out[i, h*C + c] = sum over CSR slots p of row i of alpha[p,h] * x[col[p], h*C + c].
+ *   x, out  [N, H*C] fp32 or bf16 (dtype), fp32 accumulation; rows take the
+ *           16-byte vector path when C * sizeof(dtype) % 16 == 0;
+ *   alpha   fp32 [E, H] in CSR slot order (PYG_ORDER_CSR); csr->weight is ignored.
+ * Deterministic, same kernel and work split as pyg_propagate's CSR path. */
+int pyg_propagate_heads(const void *x, int dtype, int64_t N, int64_t H, int64_t C, const pyg_csr *csr,
+                        const float *alpha, void *out, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_global_pool. */
 int pyg_global_pool_workspace(int dtype, int64_t N, int64_t F, int64_t B, int aggr, size_t *bytes);

@@ -21,6 +21,7 @@ from .binding import (  # noqa: F401
     abi_version,
     coo_to_csr,
     degree,
+    gat_softmax,
     gather_edges,
     gcn_norm,
     gcn_norm_csr,
@@ -29,8 +30,11 @@ from .binding import (  # noqa: F401
     library_path,
     propagate,
     propagate_backward,
+    propagate_heads,
     propagate_workspace_bytes,
     reverse_edges,
+    segment_softmax,
+    segment_softmax_backward,
     strerror,
     validate_batch,
     validate_coo,

@@ -15,12 +15,15 @@ DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 AGGR = {"sum": 0, "mean": 1, "max": 2}
 MSG = {"src": 0, "diff": 1}
 KERNEL = {"auto": 0, "coo": 1, "csr": 2}
+ORDER = {"csr": 0, "coo": 1}
 
 EXPORTED = [
     "pyg_strerror", "pyg_abi_version", "pyg_degree_workspace", "pyg_degree", "pyg_coo_to_csr_workspace",
     "pyg_coo_to_csr", "pyg_gather_edges",
     "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_gcn_norm_csr_workspace", "pyg_gcn_norm_csr",
     "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_backward_workspace", "pyg_propagate_backward",
+    "pyg_segment_softmax_workspace", "pyg_segment_softmax", "pyg_gat_softmax", "pyg_segment_softmax_backward",
+    "pyg_propagate_heads_workspace", "pyg_propagate_heads",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
 ]
 
@@ -75,6 +78,12 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
             "pyg_propagate_backward": [p, p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr),
                                        i32, i32, p, p, p, p, ctypes.c_size_t, p],
+            "pyg_segment_softmax_workspace": [i64, i64, i64, i64, sz],
+            "pyg_segment_softmax": [p, i64, ctypes.POINTER(_Csr), i32, p, p, ctypes.c_size_t, p],
+            "pyg_gat_softmax": [p, p, i64, ctypes.c_float, ctypes.POINTER(_Csr), i32, p, p, ctypes.c_size_t, p],
+            "pyg_segment_softmax_backward": [p, p, i64, ctypes.POINTER(_Csr), i32, p, p, ctypes.c_size_t, p],
+            "pyg_propagate_heads_workspace": [i32, i64, i64, i64, i64, i64, sz],
+            "pyg_propagate_heads": [p, i32, i64, i64, i64, ctypes.POINTER(_Csr), p, p, p, ctypes.c_size_t, p],
             "pyg_global_pool_workspace": [i32, i64, i64, i64, i32, sz],
             "pyg_global_pool": [p, i32, i64, i64, p, i64, i32, p, p, p, ctypes.c_size_t, p],
             "pyg_validate_coo": [p, i64, i64, p, p],
@@ -331,6 +340,103 @@ def propagate_backward(grad_out: torch.Tensor, x: torch.Tensor | None = None, ed
                                     _ptr(grad_x), _ptr(grad_w), _ptr(ws), ws.numel(), _stream(dev))
     _check(rc, "pyg_propagate_backward")
     return grad_x, grad_w
+
+
+def _edge_values(name, t, E):
+    _need_cuda(name, t, torch.float32)
+    if t.dim() == 1:
+        t = t.view(E, 1) if E else t.view(0, 1)
+    if t.dim() != 2 or t.shape[0] != E:
+        raise ValueError(f"{name} must be [E, H] or [E]")
+    return t
+
+
+def _softmax_ws(csr: CSR, H: int, workspace):
+    nbytes = _size(library().pyg_segment_softmax_workspace, csr.E, csr.N, H, csr.chunk)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, csr.rowptr.device)
+    return workspace
+
+
+def segment_softmax(scores: torch.Tensor, csr: CSR, order: str = "coo", out: torch.Tensor | None = None,
+                    workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """Softmax of scores [E, H] (or [E]) over the incoming edges of every
+    target, per head; scores and the result are in `order` ("coo": edge id,
+    "csr": slot)."""
+    lib = library()
+    s2 = _edge_values("scores", scores, csr.E)
+    H = s2.shape[1]
+    out = torch.empty_like(scores) if out is None else out
+    ws = _softmax_ws(csr, H, workspace)
+    c = csr._c()
+    _check(lib.pyg_segment_softmax(_ptr(s2), H, ctypes.byref(c), ORDER[order], _ptr(out), _ptr(ws), ws.numel(),
+                                   _stream(csr.rowptr.device)), "pyg_segment_softmax")
+    return out
+
+
+def gat_softmax(a_src: torch.Tensor, a_dst: torch.Tensor, csr: CSR, negative_slope: float = 0.2,
+                order: str = "csr", out: torch.Tensor | None = None,
+                workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """GAT attention coefficients [E, H]: softmax over incoming edges of
+    LeakyReLU(a_src[j] + a_dst[i]), scores computed on the fly."""
+    lib = library()
+    _need_cuda("a_src", a_src, torch.float32, 2)
+    _need_cuda("a_dst", a_dst, torch.float32, 2)
+    if a_src.shape != a_dst.shape or a_src.shape[0] != csr.N:
+        raise ValueError("a_src and a_dst must both be [N, H]")
+    H = a_src.shape[1]
+    out = torch.empty((csr.E, H), dtype=torch.float32, device=a_src.device) if out is None else out
+    ws = _softmax_ws(csr, H, workspace)
+    c = csr._c()
+    _check(lib.pyg_gat_softmax(_ptr(a_src), _ptr(a_dst), H, ctypes.c_float(negative_slope), ctypes.byref(c),
+                               ORDER[order], _ptr(out), _ptr(ws), ws.numel(), _stream(a_src.device)),
+           "pyg_gat_softmax")
+    return out
+
+
+def segment_softmax_backward(alpha: torch.Tensor, grad_alpha: torch.Tensor, csr: CSR, order: str = "coo",
+                             out: torch.Tensor | None = None, workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """Gradient of segment_softmax w.r.t. its scores."""
+    lib = library()
+    a2 = _edge_values("alpha", alpha, csr.E)
+    g2 = _edge_values("grad_alpha", grad_alpha, csr.E)
+    if g2.shape != a2.shape:
+        raise ValueError("grad_alpha must match alpha")
+    H = a2.shape[1]
+    out = torch.empty_like(alpha) if out is None else out
+    ws = _softmax_ws(csr, H, workspace)
+    c = csr._c()
+    _check(lib.pyg_segment_softmax_backward(_ptr(a2), _ptr(g2), H, ctypes.byref(c), ORDER[order], _ptr(out),
+                                            _ptr(ws), ws.numel(), _stream(csr.rowptr.device)),
+           "pyg_segment_softmax_backward")
+    return out
+
+
+def propagate_heads(x: torch.Tensor, csr: CSR, alpha: torch.Tensor, heads: int, out: torch.Tensor | None = None,
+                    workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """out[i, h*C:(h+1)*C] = sum over CSR slots p of row i of alpha[p, h] * x[col[p], h*C:(h+1)*C];
+    alpha [E, H] in CSR slot order."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    if x.dtype not in DTYPE:
+        raise ValueError("x must be float32 or bfloat16")
+    N, F = x.shape
+    if heads <= 0 or F % heads:
+        raise ValueError("the feature width must be a multiple of heads")
+    if csr.N != N:
+        raise ValueError("csr does not match x")
+    a2 = _edge_values("alpha", alpha, csr.E)
+    if a2.shape[1] != heads:
+        raise ValueError("alpha must be [E, heads]")
+    C = F // heads
+    out = torch.empty_like(x) if out is None else out
+    nbytes = _size(lib.pyg_propagate_heads_workspace, DTYPE[x.dtype], N, heads, C, csr.E, csr.chunk)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, x.device)
+    c = csr._c()
+    _check(lib.pyg_propagate_heads(_ptr(x), DTYPE[x.dtype], N, heads, C, ctypes.byref(c), _ptr(a2), _ptr(out),
+                                   _ptr(workspace), workspace.numel(), _stream(x.device)), "pyg_propagate_heads")
+    return out
 
 
 def global_pool(x: torch.Tensor, batch: torch.Tensor, num_graphs: int, aggr: str = "sum",

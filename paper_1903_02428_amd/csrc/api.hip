@@ -116,6 +116,49 @@ extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, con
     return segment_reduce(a, ws, ws_bytes, s);
 }
 
+extern "C" int pyg_propagate_heads_workspace(int dtype, int64_t N, int64_t H, int64_t C, int64_t E, int64_t chunk,
+                                             size_t *bytes) {
+    if (!bytes || !valid_dtype(dtype) || N < 0 || H < 0 || C < 0 || E < 0 || chunk < 0) return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || E >= kMax32 || H * C >= kMax32) return PYG_ERR_UNSUPPORTED;
+    *bytes = segment_workspace(E, H * C, PYG_SUM, chunk, N);
+    return PYG_OK;
+}
+
+extern "C" int pyg_propagate_heads(const void *x, int dtype, int64_t N, int64_t H, int64_t C, const pyg_csr *csr,
+                                   const float *alpha, void *out, void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(dtype) || N < 0 || H <= 0 || C < 0 || !csr) return PYG_ERR_INVALID_ARG;
+    const int64_t E = csr->E, F = H * C;
+    if (N >= kMax32 || E >= kMax32 || F >= kMax32) return PYG_ERR_UNSUPPORTED;
+    if (csr->N != N || E < 0 || !csr->rowptr || csr->chunk < 0) return PYG_ERR_INVALID_ARG;
+    if (E > 0 && (N == 0 || !csr->col || !alpha)) return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && (!x || !out)) return PYG_ERR_INVALID_ARG;
+    const int64_t xbytes = N * F * dtype_size(dtype);
+    if (overlaps(x, xbytes, out, xbytes) || overlaps(alpha, E * H * 4, out, xbytes)) return PYG_ERR_INVALID_ARG;
+    size_t need;
+    PYG_TRY(pyg_propagate_heads_workspace(dtype, N, H, C, E, csr->chunk, &need));
+    if (ws_bytes < need || (need > 256 && !ws)) return PYG_ERR_WORKSPACE;
+    if (N * F == 0) return PYG_OK;
+    SegmentArgs a{};
+    a.x = x;
+    a.dtype = dtype;
+    a.F = F;
+    a.rowptr = csr->rowptr;
+    a.col = csr->col;
+    a.alpha = E > 0 ? alpha : nullptr;
+    a.H = H;
+    a.C = C;
+    a.perm = csr->perm;
+    a.n_rows = N;
+    a.E = E;
+    a.msg = PYG_MSG_SRC;
+    a.aggr = PYG_SUM;
+    a.chunk = csr->chunk;
+    a.sentinel = E;
+    a.out = out;
+    a.hint = true;
+    return segment_reduce(a, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
 extern "C" int pyg_global_pool_workspace(int dtype, int64_t N, int64_t F, int64_t B, int aggr, size_t *bytes) {
     if (!bytes || !valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || B < 0) return PYG_ERR_INVALID_ARG;
     if (N >= kMax32 || B >= kMax32) return PYG_ERR_UNSUPPORTED;

@@ -137,6 +137,9 @@ struct SegmentArgs {
     const int64_t *rowptr; // [n_rows + 1]
     const int32_t *col;    // [E] source row per slot; NULL = identity (slot id)
     const float *weight;   // [E] or NULL
+    const float *alpha;    // [E, H] per-head weights in slot order, or NULL (sum only)
+    int64_t H;             // heads; feature f belongs to head f / C
+    int64_t C;
     const int64_t *perm;   // [E] id reported by argmax; NULL = slot id
     int64_t n_rows;
     int64_t E;

@@ -41,6 +41,9 @@ struct SegParams {
     const int64_t *rowptr;
     const int32_t *col;
     const float *w;
+    const float *alpha;  // per-head weights [E, H] in slot order (kMsgHeads)
+    int64_t H;
+    int64_t C;           // columns per head: feature f belongs to head f / C
     const int64_t *perm;
     int64_t n_rows;
     int64_t E;
@@ -135,7 +138,7 @@ __device__ __forceinline__ int deg_class(int64_t d) {
 constexpr int kClasses = 256;
 
 constexpr int kFull = 0, kPartial = 1;
-constexpr int kMsgSrc = 0, kMsgWeighted = 1, kMsgDiff = 2;
+constexpr int kMsgSrc = 0, kMsgWeighted = 1, kMsgDiff = 2, kMsgHeads = 3;
 
 // Reduce slots [s, t) of row r; write the row (kFull) or a partial (kPartial).
 template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT>
@@ -172,6 +175,10 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
 #pragma unroll
         for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(x + r * p.F + f0[sl]) : LN::zero();
     }
+    // per-head weights: a lane vector never straddles two heads (C is a multiple of its width)
+    int64_t hd[NS];
+#pragma unroll
+    for (int sl = 0; sl < NS; ++sl) hd[sl] = MSG == kMsgHeads ? f0[sl] / p.C : 0;
 
     // column indices and weights stream once: read them 64 at a time,
     // non-temporally, one batch ahead of the gathers that use them; bit 31 of
@@ -203,6 +210,14 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                 ok[u] = idx < n;
                 jj[u] = __shfl(myc, idx & (kWave - 1), kWave);
                 if constexpr (MSG == kMsgWeighted) ww[u] = __shfl(myw, idx & (kWave - 1), kWave);
+            }
+            float wh[U][NS];
+            if constexpr (MSG == kMsgHeads) {
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int sl = 0; sl < NS; ++sl)
+                        wh[u][sl] = (ok[u] && act[sl]) ? p.alpha[(base + st + u * S + sg) * p.H + hd[sl]] : 0.f;
             }
             R v[U][NS];
 #pragma unroll
@@ -237,6 +252,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                         } else {
                             if constexpr (MSG == kMsgDiff) acc[sl][e] += xv - LN::get(xi[sl], e);
                             else if constexpr (MSG == kMsgWeighted) acc[sl][e] = fmaf(ww[u], xv, acc[sl][e]);
+                            else if constexpr (MSG == kMsgHeads) acc[sl][e] = fmaf(wh[u][sl], xv, acc[sl][e]);
                             else acc[sl][e] += xv;
                         }
                     }
@@ -320,6 +336,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
     }
     R xi = LN::zero();
     if constexpr (MSG == kMsgDiff) xi = act ? LN::load(x + r * p.F + f0) : LN::zero();
+    const int64_t hd = MSG == kMsgHeads ? f0 / p.C : 0;
     for (int64_t base = s; base < t; base += U) {
         int jj[U];
         float ww[U];
@@ -330,6 +347,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
             jj[u] = ok[u] ? (IDENT ? static_cast<int>(base + u) : p.col[base + u]) : 0;
             ww[u] = 1.f;
             if constexpr (MSG == kMsgWeighted) ww[u] = ok[u] ? p.w[base + u] : 0.f;
+            if constexpr (MSG == kMsgHeads) ww[u] = (ok[u] && act) ? p.alpha[(base + u) * p.H + hd] : 0.f;
         }
         R v[U];
 #pragma unroll
@@ -352,7 +370,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
                     }
                 } else {
                     if constexpr (MSG == kMsgDiff) acc[e] += xv - LN::get(xi, e);
-                    else if constexpr (MSG == kMsgWeighted) acc[e] = fmaf(ww[u], xv, acc[e]);
+                    else if constexpr (MSG == kMsgWeighted || MSG == kMsgHeads) acc[e] = fmaf(ww[u], xv, acc[e]);
                     else acc[e] += xv;
                 }
             }
@@ -585,6 +603,9 @@ int launch_ns(const SegParams &p, int ns, bool light, hipStream_t s) {
 template <typename T, bool VEC, bool MAXA>
 int launch_msg(const SegParams &p, int msg, bool ident, int ns, bool light, hipStream_t s) {
     if (ident) return launch_ns<T, VEC, kMsgSrc, MAXA, true>(p, ns, light, s);
+    if constexpr (!MAXA) {
+        if (msg == kMsgHeads) return launch_ns<T, VEC, kMsgHeads, false, false>(p, ns, light, s);
+    }
     if (msg == kMsgDiff) return launch_ns<T, VEC, kMsgDiff, MAXA, false>(p, ns, light, s);
     if (msg == kMsgWeighted) return launch_ns<T, VEC, kMsgWeighted, MAXA, false>(p, ns, light, s);
     return launch_ns<T, VEC, kMsgSrc, MAXA, false>(p, ns, light, s);
@@ -601,13 +622,14 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     }
     const int64_t row_bytes = a.F * (int64_t)sizeof(T);
     const bool vec = row_bytes % 16 == 0 && (reinterpret_cast<uintptr_t>(a.x) % 16) == 0 &&
-                     (reinterpret_cast<uintptr_t>(a.out) % 16) == 0;
+                     (reinterpret_cast<uintptr_t>(a.out) % 16) == 0 &&
+                     (!a.alpha || (a.C * (int64_t)sizeof(T)) % 16 == 0);
     const int ep = vec ? 16 / (int)sizeof(T) : 1;
     const int64_t nvec = a.F / ep;  // lane vectors per row
     int lg = 0;
     while ((1 << lg) < nvec && lg < 6) ++lg;
     p.lg_l = lg;
-    const int mk = a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc);
+    const int mk = a.alpha ? kMsgHeads : (a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc));
     const bool ident = a.col == nullptr;
     // cache hint: only when the source rows do not fit in L2 (row in-degree as the hotness proxy)
     p.hot_class = nullptr;
@@ -694,6 +716,9 @@ int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t 
     p.rowptr = a.rowptr;
     p.col = a.col;
     p.w = a.weight;
+    p.alpha = a.alpha;
+    p.H = a.H;
+    p.C = a.C;
     p.perm = a.perm;
     p.n_rows = a.n_rows;
     p.E = a.E;

@@ -7,6 +7,11 @@
   max        : values bit-exact (bf16: the RNE rounding of the oracle's fp32
                maximum), argmax bit-exact.
   integers   : bit-exact.
+  softmax    : |gpu - ref| <= ref * (1e-5 + 4 eps (|s| + |m| + 1)) + 1e-30,
+               eps = 2^-24, s the edge's score and m its segment's maximum:
+               the denominator is a sum of positive terms held to the 1e-5
+               sum rule, and rounding s - m (or forming s in fp32) moves
+               exp(s - m) by at most eps (|s| + |m|) relative.
 """
 from __future__ import annotations
 
@@ -76,3 +81,24 @@ def run_propagate_case(pyg, ei_np, x_np, w_np=None, msg="src", aggr="sum", kerne
         check_max(out, arg, ref, rarg, dtype == torch.bfloat16, tag)
         return 0.0
     return check_sum(out, ref, sabs, dtype == torch.bfloat16, tag)
+
+
+def segment_max(s: np.ndarray, dst: np.ndarray, N: int) -> np.ndarray:
+    """Per-target maximum of the scores [E, H] (used only for the tolerance)."""
+    m = np.full((N, s.shape[1]), -np.inf)
+    np.maximum.at(m, dst, s)
+    return m
+
+
+def check_softmax(gpu: torch.Tensor, ref: np.ndarray, s: np.ndarray, dst: np.ndarray, N: int, what: str = ""):
+    g = gpu.float().cpu().numpy().astype(np.float64).reshape(ref.shape)
+    s = np.asarray(s, np.float64).reshape(ref.shape)
+    m = segment_max(s, dst, N)[dst] if s.size else s
+    bound = ref * (1e-5 + 4 * 2.0**-24 * (np.abs(s) + np.abs(m) + 1)) + 1e-30
+    err = np.abs(g - ref)
+    bad = ~(err <= bound)
+    if bad.any():
+        i = tuple(np.argwhere(bad)[0])
+        raise AssertionError(f"{what}: {bad.sum()} alphas out of tolerance; first {i} gpu={g[i]!r} ref={ref[i]!r} "
+                             f"bound={bound[i]!r}")
+    return float((err / bound).max()) if err.size else 0.0

@@ -146,3 +146,46 @@ def test_binding_rejects_host_tensors():
         pyg.propagate(x, ei)
     with pytest.raises(ValueError):
         pyg.degree(ei, 4)
+
+
+def test_attention_entry_points_reject_bad_arguments(lib):
+    from paper_1903_02428_amd.binding import _Csr
+    good = _Csr(0x30000, 0x40000, 0x50000, None, 10, 20, 0)
+    no_perm = _Csr(0x30000, 0x40000, None, None, 10, 20, 0)
+    huge = _Csr(0x30000, 0x40000, 0x50000, None, 10, 2**31, 0)
+    A = ctypes.c_void_p(0x90000)
+    g = ctypes.byref(good)
+    sm = lib.pyg_segment_softmax
+    assert sm(FAKE, 2, None, 0, A, FAKE, 1 << 30, None) == INVALID            # no CSR
+    assert sm(FAKE, 0, g, 0, A, FAKE, 1 << 30, None) == INVALID               # H = 0
+    assert sm(FAKE, 2, g, 5, A, FAKE, 1 << 30, None) == INVALID               # unknown order
+    assert sm(FAKE, 2, ctypes.byref(no_perm), 1, A, FAKE, 1 << 30, None) == INVALID  # COO order needs perm
+    assert sm(None, 2, g, 0, A, FAKE, 1 << 30, None) == INVALID               # no scores
+    assert sm(FAKE, 2, g, 0, None, FAKE, 1 << 30, None) == INVALID            # no output
+    assert sm(FAKE, 2, ctypes.byref(huge), 0, A, FAKE, 1 << 30, None) == UNSUPPORTED
+    assert sm(FAKE, 2, g, 0, A, FAKE, 0, None) == WORKSPACE
+    assert sm(FAKE, 2, g, 0, A, None, 1 << 30, None) == WORKSPACE
+    gat = lib.pyg_gat_softmax
+    assert gat(FAKE, FAKE, 2, ctypes.c_float(float("nan")), g, 0, A, FAKE, 1 << 30, None) == INVALID
+    assert gat(None, FAKE, 2, ctypes.c_float(0.2), g, 0, A, FAKE, 1 << 30, None) == INVALID
+    assert gat(FAKE, FAKE, 2, ctypes.c_float(0.2), g, 0, A, FAKE, 0, None) == WORKSPACE
+    bwd = lib.pyg_segment_softmax_backward
+    assert bwd(FAKE, None, 2, g, 0, A, FAKE, 1 << 30, None) == INVALID
+    assert bwd(FAKE, FAKE, 2, g, 0, A, FAKE, 0, None) == WORKSPACE
+    ph = lib.pyg_propagate_heads
+    X, OUT = FAKE, ctypes.c_void_p(0x200000)
+    assert ph(X, 0, 10, 0, 4, g, A, OUT, FAKE, 1 << 30, None) == INVALID       # H = 0
+    assert ph(X, 0, 11, 2, 4, g, A, OUT, FAKE, 1 << 30, None) == INVALID       # CSR of another graph
+    assert ph(X, 0, 10, 2, 4, g, None, OUT, FAKE, 1 << 30, None) == INVALID    # no alpha
+    assert ph(X, 0, 10, 2, 4, None, A, OUT, FAKE, 1 << 30, None) == INVALID    # no CSR
+    assert ph(X, 3, 10, 2, 4, g, A, OUT, FAKE, 1 << 30, None) == INVALID       # bad dtype
+    assert ph(X, 0, 10, 2, 4, g, A, ctypes.c_void_p(0x10000 + 16), FAKE, 1 << 30, None) == INVALID  # out overlaps x
+    assert ph(X, 0, 10, 2, 4, g, A, OUT, FAKE, 0, None) == WORKSPACE
+    last = 0
+    for E in (0, 100, 10**5, 10**7):
+        rc, b = _ws(lib.pyg_segment_softmax_workspace, E, 1000, 4, 0)
+        assert rc == PYG_OK and b >= last
+        last = b
+    assert _ws(lib.pyg_segment_softmax_workspace, 10, 5, -1, 0)[0] == INVALID
+    assert _ws(lib.pyg_propagate_heads_workspace, 0, 10, 2, 4, 20, 0)[0] == PYG_OK
+    assert _ws(lib.pyg_propagate_heads_workspace, 0, 10, 2**20, 2**12, 20, 0)[0] == UNSUPPORTED
