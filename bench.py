@@ -77,6 +77,8 @@ def parse():
     ap.add_argument("--fig2", action="store_true",
                     help="run the degree sweep of the paper's Fig. 2 (gather/scatter vs CSR, forward and backward) "
                          "instead of the headline step; prints one JSON line per point")
+    ap.add_argument("--attention-only", action="store_true",
+                    help="time only the attention calls (GAT softmax, attention sum) on the large graph")
     ap.add_argument("--fig2-features", type=int, default=64)
     ap.add_argument("--fig2-runs", type=int, default=1000)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -153,6 +155,12 @@ def main():
     ws_prop = torch.empty(pyg.propagate_workspace_bytes(x, E, "sum", "csr", args.chunk), dtype=torch.uint8, device=dev)
     lib.pyg_global_pool_workspace(0, N, F, 1, 1, ctypes.byref(sz))
     ws_pool = torch.empty(sz.value, dtype=torch.uint8, device=dev)
+
+    if args.attention_only:
+        pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
+        print(json.dumps({"workload": "large power-law graph, GAT attention", "N": N, "E": E, "F": F,
+                          "attention": attention(pyg, torch, x, csr, N, E, F, dev)}), flush=True)
+        return
 
     names = ["degree", "coo_to_csr", "gcn_norm", "propagate", "global_pool"]
     ev = {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
@@ -234,6 +242,7 @@ def main():
 
     if not args.no_detail:
         result["detail"]["variants"] = variants(pyg, torch, x, ei, csr_w, N, E, F, dev)
+        result["detail"]["attention"] = attention(pyg, torch, x, csr, N, E, F, dev)
     if not (args.no_detail and args.no_cpu_baseline):
         import oracle
         w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)  # the oracle's own weights
@@ -328,6 +337,46 @@ def variants(pyg, torch, x, ei, csr, N, E, F, dev):
                 res[f"{kernel}-{aggr}-{dtname}"] = {"ms": ms, "edges_features_per_s": E * F / (ms * 1e-3),
                                                    "alg_GBps": b / (ms * 1e-3) / 1e9,
                                                    "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    return res
+
+
+def attention(pyg, torch, x, csr, N, E, F, dev, H=8):
+    """GAT-style attention on the same graph: H heads of C = F / H columns.
+    Times the fused score+softmax call, the attention-weighted sum (fp32 and
+    bf16 rows), and the softmax forward from stored scores and its backward,
+    each with its algorithmic bytes (unique bytes read and written once)."""
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7)
+    a_src = torch.randn(N, H, device=dev, generator=gen)
+    a_dst = torch.randn(N, H, device=dev, generator=gen)
+    alpha = torch.empty(E, H, device=dev)
+    scores = torch.randn(E, H, device=dev, generator=gen)
+    grad = torch.randn(E, H, device=dev, generator=gen)
+    gs = torch.empty(E, H, device=dev)
+    ws_sm = pyg.binding._softmax_ws(csr, H, None)
+    rp = 8 * (N + 1)
+
+    def rec(ms, b):
+        return {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9, "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "bytes": b}
+
+    res = {"heads": H, "channels_per_head": F // H}
+    ms = timed(torch, lambda: pyg.gat_softmax(a_src, a_dst, csr, 0.2, "csr", out=alpha, workspace=ws_sm))
+    res["gat_softmax"] = rec(ms, rp + 4 * E + 4 * E * H + 8 * N * H)
+    ms = timed(torch, lambda: pyg.segment_softmax(scores, csr, "csr", out=gs, workspace=ws_sm))
+    res["segment_softmax"] = rec(ms, rp + 8 * E * H)
+    ms = timed(torch, lambda: pyg.segment_softmax_backward(alpha, grad, csr, "csr", out=gs, workspace=ws_sm))
+    res["segment_softmax_backward"] = rec(ms, rp + 12 * E * H)
+    for dtname, xx, sz in (("f32", x, 4), ("bf16", x.to(torch.bfloat16), 2)):
+        o = torch.empty_like(xx)
+        ws = torch.empty(pyg.binding._size(pyg.library().pyg_propagate_heads_workspace, pyg.binding.DTYPE[xx.dtype],
+                                           N, H, F // H, E, csr.chunk), dtype=torch.uint8, device=dev)
+        ms = timed(torch, lambda: pyg.propagate_heads(xx, csr, alpha, H, out=o, workspace=ws))
+        r = rec(ms, rp + 4 * E + 4 * E * H + E * F * sz + N * F * sz)
+        r["edges_features_per_s"] = E * F / (ms * 1e-3)
+        res[f"propagate_heads_{dtname}"] = r
+    layer = res["gat_softmax"]["ms"] + res["propagate_heads_f32"]["ms"]
+    res["attention_layer_f32"] = {"ms": layer, "edges_features_per_s": E * F / (layer * 1e-3)}
     return res
 
 

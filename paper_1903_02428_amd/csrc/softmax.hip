@@ -9,13 +9,19 @@
 //
 // Work split, as in the propagate kernel: E slots cut into chunks, one
 // wavefront per chunk. A row of at most `chunk` slots belongs to the chunk
-// holding its first slot and is done there in two passes over its slots:
-// an online max/sum pass (one exp per element, rescaling when the running
-// maximum grows) and a normalising pass. Lanes are split into groups of G
-// lanes per row; inside a group Hq lanes (H rounded up to a power of two,
-// at most 64) cover the heads of one slot and G / Hq slots go side by side,
-// so consecutive lanes read consecutive addresses. Short rows share a
-// wavefront (G < 64) when the mean degree is small.
+// holding its first slot and is done there by a group of G lanes (short
+// rows share a wavefront when the mean degree is small).
+// Vector path (H a power of two, 16-byte aligned arrays): a row's values are
+// the flat range [s*H, t*H) of the [E,H] array and each lane takes 16-byte
+// blocks of it, so a lane's four elements always belong to the same four
+// heads (H >= 4) or repeat the heads (H = 1, 2). A row that fits the group's
+// registers (R blocks per lane) is read once: maximum, then exp and sum with
+// the exponentials kept in registers, then scaled stores. A larger row makes
+// an online pass (per-batch maximum, one exp per element, rescaling the sum)
+// and a second pass that recomputes and stores.
+// Scalar path (any H): Hq lanes (H rounded up to a power of two, at most 64)
+// cover the heads of one slot, G / Hq slots go side by side; online pass,
+// then normalising pass.
 // A longer row is cut at chunk boundaries: every piece's (max, sum) goes to
 // a partial, a fold kernel merges the partials of each long row in chunk
 // order, and a third kernel normalises the pieces. All orders are fixed, so
@@ -23,6 +29,15 @@
 #include "common.hpp"
 
 #include <math.h>
+
+// 16-byte blocks per lane held in registers by the vector path (forward,
+// backward); a row of up to G * R blocks is read once.
+#ifndef PYG_SOFTMAX_REGS
+#define PYG_SOFTMAX_REGS 8
+#endif
+#ifndef PYG_SOFTMAX_REGS_BWD
+#define PYG_SOFTMAX_REGS_BWD 8
+#endif
 
 namespace pyg {
 namespace {
@@ -43,14 +58,23 @@ struct SmParams {
     int64_t H;
     int64_t chunk;
     int64_t nchunks;
-    int lg_h;  // log2 of lanes per slot (Hq)
-    int lg_g;  // log2 of lanes per short row
+    int lg_h;   // scalar path: log2 of lanes per slot (Hq)
+    int lg_hh;  // vector path: log2 of H
+    int lg_g;   // log2 of lanes per short row
     float *out;
     float2 *part;       // [2 * nchunks, H]: piece states (continuing piece at 2c, head piece at 2c + 1)
     float2 *stat;       // [nchunks, H]: folded state of the long row that starts in chunk c
     int32_t *head_row;  // [nchunks]: long row starting in chunk c, or -1
     int32_t *cont_row;  // [nchunks]: long row continuing into chunk c, or -1
 };
+
+// exp(x) on the hardware exp2 unit as 2^(x log2 e): rounding the product
+// changes the result by at most |x| eps relative, the unit adds about one
+// ulp. It is only called on finite arguments: padding (-inf) and empty
+// states are mapped to 0 by explicit selects (pexp), which also keeps the
+// result independent of how the compiler treats exp2 of -inf.
+__device__ __forceinline__ float fexp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+__device__ __forceinline__ float pexp(float v, float m) { return v == -INFINITY ? 0.f : fexp(v - m); }
 
 // Running state of one (row, head): forward (m = max, d = sum exp(v - m)),
 // backward (m = sum alpha * g, d unused).
@@ -60,10 +84,10 @@ __device__ __forceinline__ void merge(float &m, float &d, float m2, float d2) {
         m += m2;
     } else {
         if (m2 > m) {
-            d = d * expf(m - m2) + d2;
+            d = pexp(m, m2) * d + d2;
             m = m2;
         } else if (m2 != -INFINITY) {
-            d += d2 * expf(m2 - m);
+            d += d2 * fexp(m2 - m);
         }
     }
 }
@@ -94,10 +118,10 @@ __device__ __forceinline__ void accumulate(float &m, float &d, float v, float gv
     if constexpr (SRC == kBackward) {
         m = fmaf(v, gv, m);
     } else if (v > m) {
-        d = d * expf(m - v) + 1.f;
+        d = pexp(m, v) * d + 1.f;
         m = v;
     } else {
-        d += expf(v - m);
+        d += fexp(v - m);
     }
 }
 
@@ -160,7 +184,7 @@ __device__ __forceinline__ void row_write(const SmParams &p, int64_t r, int64_t 
         for (int u = 0; u < U; ++u) {
             if (e[u] < 0) continue;
             if constexpr (SRC == kBackward) p.out[e[u]] = v[u] * (gv[u] - st.x);
-            else p.out[e[u]] = expf(v[u] - st.x) * inv;
+            else p.out[e[u]] = fexp(v[u] - st.x) * inv;
         }
     }
 }
@@ -175,7 +199,330 @@ __device__ __forceinline__ void piece_state(const SmParams &p, int64_t r, int64_
     }
 }
 
+// ------------------------------------------------------------ vector path
 template <int SRC>
+__device__ __forceinline__ float pad_value() { return SRC == kBackward ? 0.f : -INFINITY; }
+
+__device__ __forceinline__ float leaky(float v, float slope) { return v >= 0.f ? v : slope * v; }
+
+// Block b of the flat [E,H] range of a row (elements 4b .. 4b+3, those
+// outside [lo, hi) padded). H >= 4: one slot, heads (4b mod H) + i, the row
+// covers whole blocks. H < 4: slots (4b + i) / H, heads i mod H.
+template <int SRC, int VH>
+__device__ __forceinline__ void vload(const SmParams &p, int64_t b, int64_t lo, int64_t hi, const float (&adst)[4],
+                                      float (&v)[4], float (&gv)[4]) {
+    const int64_t f = 4 * b;
+    if constexpr (VH == 4) {
+        const int64_t slot = f >> p.lg_hh;
+        const int64_t j = f & (p.H - 1);
+        if constexpr (SRC == kGat) {
+            const float4 a = *reinterpret_cast<const float4 *>(p.a_src + (int64_t)p.col[slot] * p.H + j);
+            v[0] = leaky(a.x + adst[0], p.slope);
+            v[1] = leaky(a.y + adst[1], p.slope);
+            v[2] = leaky(a.z + adst[2], p.slope);
+            v[3] = leaky(a.w + adst[3], p.slope);
+        } else {
+            const int64_t e = p.perm ? p.perm[slot] * p.H + j : f;  // CSR order: slot * H + j = f
+            const float4 a = *reinterpret_cast<const float4 *>(p.s + e);
+            v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w;
+            if constexpr (SRC == kBackward) {
+                const float4 q = *reinterpret_cast<const float4 *>(p.g + e);
+                gv[0] = q.x, gv[1] = q.y, gv[2] = q.z, gv[3] = q.w;
+            }
+        }
+        return;
+    } else {
+    if (SRC != kGat && !p.perm && f >= lo && f + 4 <= hi) {
+        const float4 a = *reinterpret_cast<const float4 *>(p.s + f);
+        v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w;
+        if constexpr (SRC == kBackward) {
+            const float4 q = *reinterpret_cast<const float4 *>(p.g + f);
+            gv[0] = q.x, gv[1] = q.y, gv[2] = q.z, gv[3] = q.w;
+        }
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t fi = f + i;
+        v[i] = pad_value<SRC>();
+        gv[i] = 0.f;
+        if (fi < lo || fi >= hi) continue;
+        const int64_t slot = fi >> p.lg_hh;
+        const int64_t h = fi & (p.H - 1);
+        if constexpr (SRC == kGat) {
+            v[i] = leaky(p.a_src[(int64_t)p.col[slot] * p.H + h] + adst[i], p.slope);
+        } else {
+            const int64_t e = (p.perm ? p.perm[slot] : slot) * p.H + h;
+            v[i] = p.s[e];
+            if constexpr (SRC == kBackward) gv[i] = p.g[e];
+        }
+    }
+    }
+}
+
+// Store block b of the row's outputs (elements inside [lo, hi) only).
+template <int VH>
+__device__ __forceinline__ void vstore(const SmParams &p, int64_t b, int64_t lo, int64_t hi, const float (&o)[4]) {
+    const int64_t f = 4 * b;
+    if constexpr (VH == 4) {
+        const int64_t e = p.perm ? p.perm[f >> p.lg_hh] * p.H + (f & (p.H - 1)) : f;
+        *reinterpret_cast<float4 *>(p.out + e) = make_float4(o[0], o[1], o[2], o[3]);
+        return;
+    }
+    if (!p.perm && f >= lo && f + 4 <= hi) {
+        *reinterpret_cast<float4 *>(p.out + f) = make_float4(o[0], o[1], o[2], o[3]);
+        return;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t fi = f + i;
+        if (fi < lo || fi >= hi) continue;
+        const int64_t slot = fi >> p.lg_hh;
+        p.out[(p.perm ? p.perm[slot] : slot) * p.H + (fi & (p.H - 1))] = o[i];
+    }
+}
+
+// Combine per-element values over everything that shares a head: the other
+// elements of the lane (H = 1, 2), then lanes H/4 apart inside the group.
+template <int VH, typename OP>
+__device__ __forceinline__ void vcombine(const SmParams &p, int G, float (&x)[4], OP op) {
+    if constexpr (VH == 1) {
+        const float a = op(op(x[0], x[1]), op(x[2], x[3]));
+        x[0] = x[1] = x[2] = x[3] = a;
+    } else if constexpr (VH == 2) {
+        x[0] = x[2] = op(x[0], x[2]);
+        x[1] = x[3] = op(x[1], x[3]);
+    }
+    for (int off = VH == 4 ? static_cast<int>(p.H >> 2) : 1; off < G; off <<= 1)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[i] = op(x[i], __shfl_xor(x[i], off, kWave));
+}
+
+// Same for (max, sum) states of the forward.
+template <int VH>
+__device__ __forceinline__ void vcombine_state(const SmParams &p, int G, float (&m)[4], float (&d)[4]) {
+    if constexpr (VH == 1) {
+        merge<kScores>(m[0], d[0], m[1], d[1]);
+        merge<kScores>(m[2], d[2], m[3], d[3]);
+        merge<kScores>(m[0], d[0], m[2], d[2]);
+        m[1] = m[2] = m[3] = m[0];
+        d[1] = d[2] = d[3] = d[0];
+    } else if constexpr (VH == 2) {
+        merge<kScores>(m[0], d[0], m[2], d[2]);
+        merge<kScores>(m[1], d[1], m[3], d[3]);
+        m[2] = m[0], d[2] = d[0], m[3] = m[1], d[3] = d[1];
+    }
+    for (int off = VH == 4 ? static_cast<int>(p.H >> 2) : 1; off < G; off <<= 1)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float m2 = __shfl_xor(m[i], off, kWave);
+            const float d2 = __shfl_xor(d[i], off, kWave);
+            merge<kScores>(m[i], d[i], m2, d2);
+        }
+}
+
+template <int SRC, int VH>
+__device__ __forceinline__ void row_adst(const SmParams &p, int64_t r, int l, float (&adst)[4]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) adst[i] = 0.f;
+    if constexpr (SRC == kGat) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t h = VH == 4 ? ((4 * (int64_t)l) & (p.H - 1)) + i : (i & (p.H - 1));
+            adst[i] = p.a_dst[r * p.H + h];
+        }
+    }
+}
+
+// State of the flat range [lo, hi) of row r over a group of G lanes, one
+// online pass in batches of R blocks per lane: forward (m, d) per element
+// position, backward (t, -) with t = sum alpha * g.
+template <int SRC, int R, int VH>
+__device__ __forceinline__ void vstate(const SmParams &p, int64_t r, int64_t lo, int64_t hi, int G, int l,
+                                       float (&m)[4], float (&d)[4]) {
+    float adst[4];
+    row_adst<SRC, VH>(p, r, l, adst);
+    const int64_t b0 = lo >> 2, b1 = (hi + 3) >> 2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        m[i] = SRC == kBackward ? 0.f : -INFINITY;
+        d[i] = 0.f;
+    }
+    for (int64_t base = b0; base < b1; base += (int64_t)G * R) {
+        float v[R][4], gv[R][4];
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            const int64_t b = base + l + (int64_t)G * k;
+            if (b < b1) {
+                vload<SRC, VH>(p, b, lo, hi, adst, v[k], gv[k]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[k][i] = pad_value<SRC>(), gv[k][i] = 0.f;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (SRC == kBackward) {
+#pragma unroll
+                for (int k = 0; k < R; ++k) m[i] = fmaf(v[k][i], gv[k][i], m[i]);
+            } else {
+                float bm = v[0][i];
+#pragma unroll
+                for (int k = 1; k < R; ++k) bm = fmaxf(bm, v[k][i]);
+                const float mn = fmaxf(m[i], bm);
+                if (mn != -INFINITY) {
+                    float acc = pexp(m[i], mn) * d[i];
+#pragma unroll
+                    for (int k = 0; k < R; ++k) acc += pexp(v[k][i], mn);
+                    d[i] = acc;
+                    m[i] = mn;
+                }
+            }
+        }
+    }
+    if constexpr (SRC == kBackward) vcombine<VH>(p, G, m, [](float a, float b) { return a + b; });
+    else vcombine_state<VH>(p, G, m, d);
+}
+
+// Outputs of the flat range [lo, hi) of row r from the row's state.
+template <int SRC, int R, int VH>
+__device__ __forceinline__ void vwrite(const SmParams &p, int64_t r, int64_t lo, int64_t hi, int G, int l,
+                                       const float (&m)[4], const float (&d)[4]) {
+    float adst[4], inv[4];
+    row_adst<SRC, VH>(p, r, l, adst);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) inv[i] = SRC == kBackward ? 0.f : 1.f / d[i];
+    const int64_t b0 = lo >> 2, b1 = (hi + 3) >> 2;
+    for (int64_t base = b0; base < b1; base += (int64_t)G * R) {
+        float v[R][4], gv[R][4];
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            const int64_t b = base + l + (int64_t)G * k;
+            if (b < b1) vload<SRC, VH>(p, b, lo, hi, adst, v[k], gv[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < R; ++k) {
+            const int64_t b = base + l + (int64_t)G * k;
+            if (b >= b1) continue;
+            float o[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                o[i] = SRC == kBackward ? v[k][i] * (gv[k][i] - m[i]) : pexp(v[k][i], m[i]) * inv[i];
+            vstore<VH>(p, b, lo, hi, o);
+        }
+    }
+}
+
+// A whole row: read once when it fits R blocks per lane of the group.
+template <int SRC, int R, int VH>
+__device__ __forceinline__ void vrow(const SmParams &p, int64_t r, int64_t s, int64_t t, int G, int l) {
+    const int64_t lo = s * p.H, hi = t * p.H;
+    const int64_t b0 = lo >> 2, b1 = (hi + 3) >> 2;
+    float m[4], d[4];
+    if (b1 - b0 > (int64_t)G * R) {  // too large for registers: online pass, then a second read
+        vstate<SRC, 8, VH>(p, r, lo, hi, G, l, m, d);
+        vwrite<SRC, 8, VH>(p, r, lo, hi, G, l, m, d);
+        return;
+    }
+    float adst[4];
+    row_adst<SRC, VH>(p, r, l, adst);
+    const int K = static_cast<int>((b1 - b0 + G - 1) / G);  // blocks per lane, the same in the whole group
+    float v[R][4], gv[R][4];
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const int64_t b = b0 + l + (int64_t)G * k;
+        if (b < b1) {
+            vload<SRC, VH>(p, b, lo, hi, adst, v[k], gv[k]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) v[k][i] = pad_value<SRC>(), gv[k][i] = 0.f;
+        }
+    }
+    if constexpr (SRC == kBackward) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            m[i] = 0.f;
+#pragma unroll
+            for (int k = 0; k < R; ++k)
+                if (k < K) m[i] = fmaf(v[k][i], gv[k][i], m[i]);
+        }
+        vcombine<VH>(p, G, m, [](float a, float b) { return a + b; });
+#pragma unroll
+        for (int k = 0; k < R; ++k)
+            if (k < K)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) v[k][i] = v[k][i] * (gv[k][i] - m[i]);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            m[i] = v[0][i];
+#pragma unroll
+            for (int k = 1; k < R; ++k)
+                if (k < K) m[i] = fmaxf(m[i], v[k][i]);
+        }
+        vcombine<VH>(p, G, m, [](float a, float b) { return fmaxf(a, b); });
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            d[i] = 0.f;
+#pragma unroll
+            for (int k = 0; k < R; ++k)
+                if (k < K) {
+                    v[k][i] = pexp(v[k][i], m[i]);
+                    d[i] += v[k][i];
+                }
+        }
+        vcombine<VH>(p, G, d, [](float a, float b) { return a + b; });
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float inv = 1.f / d[i];
+#pragma unroll
+            for (int k = 0; k < R; ++k)
+                if (k < K) v[k][i] *= inv;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < R; ++k) {
+        const int64_t b = b0 + l + (int64_t)G * k;
+        if (b < b1) vstore<VH>(p, b, lo, hi, v[k]);
+    }
+}
+
+// Piece state of a long row over the whole wavefront, stored per head.
+template <int SRC, int R, int VH>
+__device__ __forceinline__ void vpiece_state(const SmParams &p, int64_t r, int64_t s, int64_t t, int64_t slot,
+                                             int lane) {
+    float m[4], d[4];
+    vstate<SRC, R, VH>(p, r, s * p.H, t * p.H, kWave, lane, m, d);
+    const int64_t nl = VH == 4 ? (p.H >> 2) : 1;  // lanes 0 .. nl-1 hold every head once
+    if (lane < nl) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t h = VH == 4 ? 4 * (int64_t)lane + i : i;
+            if (h < p.H) p.part[slot * p.H + h] = make_float2(m[i], d[i]);
+        }
+    }
+}
+
+template <int SRC, int VH>
+__device__ __forceinline__ void do_row(const SmParams &p, int64_t r, int64_t s, int64_t t, int lg_g, int l) {
+    if constexpr (VH > 0) {
+        vrow<SRC, SRC == kBackward ? PYG_SOFTMAX_REGS_BWD : PYG_SOFTMAX_REGS, VH>(p, r, s, t, 1 << lg_g, l);
+    } else {
+        for (int64_t hb = 0; hb < p.H; hb += (1 << p.lg_h)) {
+            const float2 st = row_state<SRC>(p, r, s, t, hb, lg_g, l);
+            row_write<SRC>(p, r, s, t, hb, lg_g, l, st);
+        }
+    }
+}
+
+template <int SRC, int VH>
+__device__ __forceinline__ void do_piece(const SmParams &p, int64_t r, int64_t s, int64_t t, int64_t slot, int lane) {
+    if constexpr (VH > 0) vpiece_state<SRC, 8, VH>(p, r, s, t, slot, lane);
+    else piece_state<SRC>(p, r, s, t, slot, lane);
+}
+
+// VH: 0 = scalar path; 1, 2 = vector path with H = 1, 2; 4 = vector path with H >= 4.
+template <int SRC, int VH>
 __global__ __launch_bounds__(kBlock) void k_softmax(SmParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
@@ -190,7 +537,7 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SmParams p) {
     if (rA > 0 && rpA > e0) {
         const int64_t s0 = uniform64(p.rowptr[rA - 1]);
         if (rpA - s0 > p.chunk) {
-            piece_state<SRC>(p, rA - 1, e0, rpA < e1 ? rpA : e1, 2 * c, lane);
+            do_piece<SRC, VH>(p, rA - 1, e0, rpA < e1 ? rpA : e1, 2 * c, lane);
             cont = static_cast<int32_t>(rA - 1);
         }
     }
@@ -212,18 +559,13 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SmParams p) {
             const bool is_long = i < cnt && t - s > p.chunk;  // only the chunk's last row can be long
             const uint64_t lm = __ballot(is_long);
             if (lm) head = static_cast<int32_t>(rb + i0 + ((__ffsll(static_cast<unsigned long long>(lm)) - 1) >> lg_g));
-            if (i < cnt && !is_long && t > s) {  // uniform within the group
-                for (int64_t hb = 0; hb < p.H; hb += (1 << p.lg_h)) {
-                    const float2 st = row_state<SRC>(p, rb + i, s, t, hb, lg_g, l);
-                    row_write<SRC>(p, rb + i, s, t, hb, lg_g, l, st);
-                }
-            }
+            if (i < cnt && !is_long && t > s) do_row<SRC, VH>(p, rb + i, s, t, lg_g, l);  // uniform within the group
         }
         if (cnt < kWave - 1) break;  // the chunk's rows end in this batch
         rb += cnt;
     }
     head = __builtin_amdgcn_readfirstlane(head);
-    if (head >= 0) piece_state<SRC>(p, head, uniform64(p.rowptr[head]), e1, 2 * c + 1, lane);
+    if (head >= 0) do_piece<SRC, VH>(p, head, uniform64(p.rowptr[head]), e1, 2 * c + 1, lane);
     if (lane == 0) {
         p.head_row[c] = head;
         p.cont_row[c] = cont;
@@ -252,7 +594,7 @@ __global__ __launch_bounds__(kBlock) void k_softmax_fold(SmParams p) {
 }
 
 // Normalise the long-row pieces of chunk c with their rows' folded states.
-template <int SRC>
+template <int SRC, int VH>
 __global__ __launch_bounds__(kBlock) void k_softmax_long(SmParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
@@ -267,6 +609,18 @@ __global__ __launch_bounds__(kBlock) void k_softmax_long(SmParams p) {
         const int64_t s = k == 0 ? e0 : rs;
         const int64_t t = k == 0 ? (rt < e1 ? rt : e1) : e1;
         const int64_t hc = k == 0 ? rs / p.chunk : c;  // chunk that owns the row's folded state
+        if constexpr (VH > 0) {
+            float m[4], d[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t h = VH == 4 ? ((4 * (int64_t)lane) & (p.H - 1)) + i : (i & (p.H - 1));
+                const float2 st = p.stat[hc * p.H + h];
+                m[i] = st.x;
+                d[i] = st.y;
+            }
+            vwrite<SRC, 8, VH>(p, r, s * p.H, t * p.H, kWave, lane, m, d);
+            continue;
+        }
         for (int64_t hb = 0; hb < p.H; hb += (1 << p.lg_h)) {
             const int64_t h = hb + (lane & ((1 << p.lg_h) - 1));
             const float2 st = h < p.H ? p.stat[hc * p.H + h] : identity_state<SRC>();
@@ -313,17 +667,35 @@ int run_softmax(SmParams p, const pyg_csr *csr, void *ws, size_t ws_bytes, hipSt
     p.head_row = w.head_row;
     p.cont_row = w.cont_row;
     p.lg_h = ceil_log2(p.H) < 6 ? ceil_log2(p.H) : 6;
-    // lanes per short row: about one lane per element of the mean row, at least Hq
+    p.lg_hh = ceil_log2(p.H);
     const int64_t avg = (p.E + p.n_rows - 1) / p.n_rows;
-    const int lg = p.lg_h + ceil_log2(avg);
+    auto al16 = [](const void *q) { return (reinterpret_cast<uintptr_t>(q) & 15) == 0; };
+    // vector path: H a power of two with at most 64 lanes per slot, 16-byte aligned arrays
+    const bool vec = (p.H & (p.H - 1)) == 0 && p.H <= 256 && al16(p.out) && al16(p.s) && al16(p.g) &&
+                     (SRC != kGat || p.H < 4 || al16(p.a_src));
+    int lg;
+    if (vec) {  // lanes per short row: about one 16-byte block per lane, at least H/4
+        const int lg_min = p.H >= 4 ? p.lg_hh - 2 : 0;
+        lg = ceil_log2((avg * p.H + 3) / 4);
+        lg = lg < lg_min ? lg_min : lg;
+    } else {    // about one lane per element of the mean row, at least Hq
+        lg = p.lg_h + ceil_log2(avg);
+    }
     p.lg_g = lg < 6 ? lg : 6;
     const unsigned grid = static_cast<unsigned>((p.nchunks + (kBlock / kWave) - 1) / (kBlock / kWave));
-    k_softmax<SRC><<<grid, kBlock, 0, s>>>(p);
+    const int vh = !vec ? 0 : (p.H >= 4 ? 4 : static_cast<int>(p.H));
+    if (vh == 4) k_softmax<SRC, 4><<<grid, kBlock, 0, s>>>(p);
+    else if (vh == 2) k_softmax<SRC, 2><<<grid, kBlock, 0, s>>>(p);
+    else if (vh == 1) k_softmax<SRC, 1><<<grid, kBlock, 0, s>>>(p);
+    else k_softmax<SRC, 0><<<grid, kBlock, 0, s>>>(p);
     PYG_LAUNCH_CHECK();
     if (p.nchunks > 1) {
         k_softmax_fold<SRC><<<grid, kBlock, 0, s>>>(p);
         PYG_LAUNCH_CHECK();
-        k_softmax_long<SRC><<<grid, kBlock, 0, s>>>(p);
+        if (vh == 4) k_softmax_long<SRC, 4><<<grid, kBlock, 0, s>>>(p);
+        else if (vh == 2) k_softmax_long<SRC, 2><<<grid, kBlock, 0, s>>>(p);
+        else if (vh == 1) k_softmax_long<SRC, 1><<<grid, kBlock, 0, s>>>(p);
+        else k_softmax_long<SRC, 0><<<grid, kBlock, 0, s>>>(p);
         PYG_LAUNCH_CHECK();
     }
     return PYG_OK;

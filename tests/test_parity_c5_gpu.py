@@ -97,3 +97,37 @@ def test_c5_propagate_sampled(pyg, c5, dev_graph, kernel):
         else:
             check_sum(got, ref[rows], sabs[rows], dt == torch.bfloat16, what)
         print(f"[c5] {what} ok", flush=True)
+
+
+def test_c5_attention_sampled(pyg, c5, dev_graph):
+    """GAT attention at the benchmark's shape (H = 8 heads of 16 columns) in
+    CSR slot order: the coefficients of every edge into the sampled rows and
+    the attention sum of those rows. A stable CSR keeps each row's edges in
+    ascending COO id, so the slots of row r are rowptr[r] + 0, 1, ... over
+    np.flatnonzero(target == r)."""
+    from tests.parity import check_softmax
+    ei_np, x_np, N = c5["edge_index_gcn"], c5["x"], c5["N"]
+    _, _, csr = dev_graph
+    H = 8
+    rng = np.random.default_rng(78)
+    a_src = rng.standard_normal((N, H)).astype(np.float32)
+    a_dst = rng.standard_normal((N, H)).astype(np.float32)
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E)
+    alpha = pyg.gat_softmax(to_dev(a_src), to_dev(a_dst), plain, 0.2, "csr")
+    out = pyg.propagate_heads(to_dev(x_np), plain, alpha, H)
+    torch.cuda.synchronize()
+    rows, keep = sample_rows(c5, n=400)
+    sub = np.ascontiguousarray(ei_np[:, keep])
+    rowptr = np.concatenate([[0], np.cumsum(np.bincount(ei_np[1], minlength=N))])
+    order = np.argsort(sub[1], kind="stable")  # sub edges grouped by row, ascending id inside a row
+    dst_sorted = sub[1][order]
+    first = np.searchsorted(dst_sorted, dst_sorted)  # first position of each row's run
+    slots = rowptr[dst_sorted] + (np.arange(order.size) - first)
+    got = alpha[to_dev(slots)].cpu()
+    e = oracle.gat_scores(a_src, a_dst, sub, 0.2)
+    ref = oracle.segment_softmax(e, sub, N)
+    check_softmax(got, ref[order], e[order], dst_sorted, N, "C5 gat_softmax")
+    ref_out, sabs = oracle.propagate_heads(x_np, sub, ref.astype(np.float32), H)
+    g = out[to_dev(rows)].cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(g - ref_out[rows]) <= 2e-5 * sabs[rows] + 1e-6), "C5 propagate_heads"
+    print("[c5] attention ok", flush=True)
