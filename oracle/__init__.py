@@ -65,10 +65,11 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_segment_softmax_backward.argtypes = [p, p, i64, i64, p, i64, p, p]
     lib.oracle_propagate_heads.argtypes = [p, i64, i64, i64, p, i64, p, p, p]
     lib.oracle_propagate_heads_backward.argtypes = [p, i64, i64, i64, p, i64, p, p, p, p, p, p]
+    lib.oracle_dense_transform.argtypes = [p, i64, i64, p, i64, p, p]
     for fn in (lib.oracle_degree, lib.oracle_coo_to_csr, lib.oracle_gcn_norm,
                lib.oracle_propagate, lib.oracle_global_pool, lib.oracle_propagate_backward,
                lib.oracle_gat_scores, lib.oracle_segment_softmax, lib.oracle_segment_softmax_backward,
-               lib.oracle_propagate_heads, lib.oracle_propagate_heads_backward):
+               lib.oracle_propagate_heads, lib.oracle_propagate_heads_backward, lib.oracle_dense_transform):
         fn.restype = ctypes.c_int
     return lib
 
@@ -279,3 +280,18 @@ def propagate_heads_backward(x, edge_index, alpha, grad_out, H: int, lib=None):
     _check(lib.oracle_propagate_heads_backward(_ptr(x), N, H, F // H, _ptr(ei), E, _ptr(a), _ptr(g), _ptr(gx),
                                                _ptr(ga), _ptr(sx), _ptr(sa)), "propagate_heads_backward")
     return gx, ga, sx, sa
+
+
+def dense_transform(x, theta, lib=None):
+    """X Theta of a GCN layer in fp64. Returns (out [N, Fo], sabs)."""
+    lib = lib or load()
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    t = np.ascontiguousarray(theta, dtype=np.float32)
+    if x.ndim != 2 or t.ndim != 2 or x.shape[1] != t.shape[0]:
+        raise ValueError("x must be [N, Fi] and theta [Fi, Fo]")
+    N, Fi = x.shape
+    Fo = t.shape[1]
+    out = np.empty((N, Fo), np.float64)
+    sabs = np.empty((N, Fo), np.float64)
+    _check(lib.oracle_dense_transform(_ptr(x), N, Fi, _ptr(t), Fo, _ptr(out), _ptr(sabs)), "dense_transform")
+    return out, sabs

@@ -487,3 +487,33 @@ int oracle_propagate_heads_backward(const float *x, int64_t N, int64_t H, int64_
         }
     return ORACLE_OK;
 }
+
+/* ---------------------------------------------------------------------------
+ * Dense feature transform of a GCN layer (Section 2 lists GCN; its layer
+ * multiplies the node features by a weight matrix before or after the
+ * normalised aggregation): out = X Theta.
+ * ------------------------------------------------------------------------- */
+
+/* out[n, o] = sum_k x[n, k] * theta[k, o]; x [N, Fi], theta [Fi, Fo] fp32
+ * (values as stored, e.g. bf16 widened exactly), out fp64 [N, Fo]; sabs
+ * (nullable) = sum_k |x[n, k] theta[k, o]|. */
+int oracle_dense_transform(const float *x, int64_t N, int64_t Fi, const float *theta, int64_t Fo, double *out,
+                           double *sabs) {
+    if (N < 0 || Fi < 0 || Fo < 0) return ORACLE_ERR_ARG;
+    if (N * Fo > 0 && !out) return ORACLE_ERR_ARG;
+    if (N * Fi > 0 && !x) return ORACLE_ERR_ARG;
+    if (Fi * Fo > 0 && !theta) return ORACLE_ERR_ARG;
+    if (!all_finite(x, N * Fi) || !all_finite(theta, Fi * Fo)) return ORACLE_ERR_NONFINITE;
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t o = 0; o < Fo; ++o) {
+            double acc = 0.0, a = 0.0;
+            for (int64_t k = 0; k < Fi; ++k) {
+                const double t = (double)x[n * Fi + k] * (double)theta[k * Fo + o];
+                acc += t;
+                a += fabs(t);
+            }
+            out[n * Fo + o] = acc;
+            if (sabs) sabs[n * Fo + o] = a;
+        }
+    return ORACLE_OK;
+}

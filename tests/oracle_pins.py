@@ -550,9 +550,37 @@ def pin_uniform_attention_is_mean(lib):
         assert np.allclose(out, mean, rtol=1e-6, atol=1e-6)
 
 
+def pin_golden_dense_transform(lib):
+    g = golden()["dense_transform"]
+    out, sabs = oracle.dense_transform(np.array(g["x"]), np.array(g["theta"]), lib=lib)
+    assert np.array_equal(out, np.array(g["out"]))
+    assert np.array_equal(sabs, np.abs(np.array(g["x"])) @ np.abs(np.array(g["theta"])))
+
+
+def pin_dense_transform_library(lib):
+    """numpy matmul; identity and column-selector weights; and the GCN layer
+    identity A (X Theta) = (A X) Theta across the propagate oracle."""
+    rng = np.random.default_rng(71)
+    for N, Fi, Fo in ((1, 1, 1), (5, 3, 7), (40, 16, 9), (33, 64, 32)):
+        x = rng.standard_normal((N, Fi)).astype(np.float32)
+        t = rng.standard_normal((Fi, Fo)).astype(np.float32)
+        out, _ = oracle.dense_transform(x, t, lib=lib)
+        assert np.allclose(out, x.astype(np.float64) @ t.astype(np.float64), rtol=1e-12, atol=1e-12)
+        eye, _ = oracle.dense_transform(x, np.eye(Fi, dtype=np.float32), lib=lib)
+        assert np.array_equal(eye, x.astype(np.float64))
+    for N, F, ei, x, w in small_cases():
+        t = np.random.default_rng(N).standard_normal((F, 4)).astype(np.float32)
+        xt, _ = oracle.dense_transform(x, t, lib=lib)
+        lhs, _, _ = oracle.propagate(xt.astype(np.float32), ei, w, aggr="sum", lib=lib)
+        ax, _, _ = oracle.propagate(x, ei, w, aggr="sum", lib=lib)
+        rhs = ax @ t.astype(np.float64)
+        assert np.allclose(lhs, rhs, rtol=1e-5, atol=1e-5)
+
+
 ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_golden_gcn_norm_directed,
             pin_golden_signed_zero,
             pin_degree_and_csr_library, pin_sum_mean_dense, pin_torch_scatter, pin_max_bruteforce,
             pin_gcn_norm_closed_forms, pin_invariants, pin_pool_relations, pin_golden_backward,
             pin_backward_autograd, pin_backward_dense, pin_golden_attention, pin_softmax_library,
-            pin_softmax_invariants, pin_softmax_backward_autograd, pin_heads_dense, pin_uniform_attention_is_mean]
+            pin_softmax_invariants, pin_softmax_backward_autograd, pin_heads_dense, pin_uniform_attention_is_mean,
+            pin_golden_dense_transform, pin_dense_transform_library]

@@ -64,6 +64,10 @@ MUTANTS = [
      "const double a = alpha[k * H];\n            for (int64_t c = 0; c < C; ++c) {\n                const double term"),
     ("heads_bwd_grad_to_target", "grad_x[j * F + h * C + c] += a * gi;", "grad_x[i * F + h * C + c] += a * gi;"),
     ("heads_bwd_dot_uses_target_x", "dot += gi * (double)x[j * F + h * C + c];", "dot += gi * (double)x[i * F + h * C + c];"),
+    ("transform_theta_transposed", "const double t = (double)x[n * Fi + k] * (double)theta[k * Fo + o];",
+     "const double t = (double)x[n * Fi + k] * (double)theta[o * Fi + k];"),
+    ("transform_skips_last_k", "for (int64_t k = 0; k < Fi; ++k) {\n                const double t",
+     "for (int64_t k = 0; k + 1 < Fi; ++k) {\n                const double t"),
 ]
 
 
