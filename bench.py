@@ -79,6 +79,8 @@ def parse():
                          "instead of the headline step; prints one JSON line per point")
     ap.add_argument("--attention-only", action="store_true",
                     help="time only the attention calls (GAT softmax, attention sum) on the large graph")
+    ap.add_argument("--gcn-layer-only", action="store_true",
+                    help="time only the GCN layer (matrix-core X Theta, then propagate) on the large graph")
     ap.add_argument("--fig2-features", type=int, default=64)
     ap.add_argument("--fig2-runs", type=int, default=1000)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -162,6 +164,13 @@ def main():
                           "attention": attention(pyg, torch, x, csr, N, E, F, dev)}), flush=True)
         return
 
+    if args.gcn_layer_only:
+        pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
+        pyg.gcn_norm_csr(csr, out=norm, workspace=ws_norm)
+        print(json.dumps({"workload": "large power-law graph, GCN layer", "N": N, "E": E, "F": F,
+                          "gcn_layer": gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)}), flush=True)
+        return
+
     names = ["degree", "coo_to_csr", "gcn_norm", "propagate", "global_pool"]
     ev = {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
     times = {n: [] for n in names}
@@ -243,6 +252,7 @@ def main():
     if not args.no_detail:
         result["detail"]["variants"] = variants(pyg, torch, x, ei, csr_w, N, E, F, dev)
         result["detail"]["attention"] = attention(pyg, torch, x, csr, N, E, F, dev)
+        result["detail"]["gcn_layer"] = gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)
     if not (args.no_detail and args.no_cpu_baseline):
         import oracle
         w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)  # the oracle's own weights
@@ -378,6 +388,37 @@ def attention(pyg, torch, x, csr, N, E, F, dev, H=8):
     layer = res["gat_softmax"]["ms"] + res["propagate_heads_f32"]["ms"]
     res["attention_layer_f32"] = {"ms": layer, "edges_features_per_s": E * F / (layer * 1e-3)}
     return res
+
+
+def gcn_layer(pyg, torch, x, csr_w, N, E, F, dev, Fo=128):
+    """One GCN layer on the same graph in bf16 storage: X Theta on the matrix
+    cores (bf16 operands, fp32 accumulation, bf16 out), then the
+    gcn_norm-weighted CSR propagate of the result. Theta ~ N(0, 1/F)."""
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(11)
+    xb = x.to(torch.bfloat16)
+    theta = (torch.randn(F, Fo, device=dev, generator=gen) / F ** 0.5).to(torch.bfloat16)
+    h = torch.empty(N, Fo, dtype=torch.bfloat16, device=dev)
+    o = torch.empty_like(h)
+    ws_d = torch.empty(pyg.binding._size(pyg.library().pyg_dense_transform_workspace, F, Fo), dtype=torch.uint8,
+                       device=dev)
+    ws_p = torch.empty(pyg.propagate_workspace_bytes(h, E, "sum", "csr", csr_w.chunk), dtype=torch.uint8, device=dev)
+    t_d = timed(torch, lambda: pyg.dense_transform(xb, theta, torch.bfloat16, out=h, workspace=ws_d))
+    t_p = timed(torch, lambda: pyg.propagate(h, csr=csr_w, aggr="sum", out=o, workspace=ws_p))
+
+    def layer():
+        pyg.dense_transform(xb, theta, torch.bfloat16, out=h, workspace=ws_d)
+        pyg.propagate(h, csr=csr_w, aggr="sum", out=o, workspace=ws_p)
+    t_l = timed(torch, layer)
+    bytes_d = N * F * 2 + F * Fo * 2 + N * Fo * 2
+    flops = 2.0 * N * F * Fo
+    return {"F_in": F, "F_out": Fo, "dtype": "bf16 storage, fp32 accumulation",
+            "dense_transform": {"ms": t_d, "alg_GBps": bytes_d / (t_d * 1e-3) / 1e9,
+                                "hbm_frac": bytes_d / (t_d * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                "TFLOPs": flops / (t_d * 1e-3) / 1e12, "mfma_bf16_frac": flops / (t_d * 1e-3) / 2.5e15,
+                                "bytes": bytes_d},
+            "propagate_bf16": {"ms": t_p, "alg_GBps": b_alg_csr(N, E, Fo, 2) / (t_p * 1e-3) / 1e9},
+            "layer": {"ms": t_l, "edges_features_per_s": E * Fo / (t_l * 1e-3)}}
 
 
 def sampled_parity(x_np, ei_np, w_ref, out, N, rows=200):

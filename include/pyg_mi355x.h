@@ -274,6 +274,26 @@ int pyg_propagate_heads_workspace(int dtype, int64_t N, int64_t H, int64_t C, in
 int pyg_propagate_heads(const void *x, int dtype, int64_t N, int64_t H, int64_t C, const pyg_csr *csr,
                         const float *alpha, void *out, void *ws, size_t ws_bytes, void *stream);
 
+/* ---- Dense feature transform of a GCN layer (Section 2 lists GCN; its
+ * layer multiplies the features by a weight matrix around the normalised
+ * aggregation, A (X Theta) = (A X) Theta). */
+
+/* Workspace bytes needed by pyg_dense_transform (Theta transposed and padded). */
+int pyg_dense_transform_workspace(int64_t Fi, int64_t Fo, size_t *bytes);
+
+/* out[n, o] = sum_k x[n, k] * theta[k, o] on the matrix cores (bf16
+ * operands, fp32 accumulation of exact bf16 products).
+ *   x      [N, Fi] bf16 (x_dtype must be PYG_BF16; PYG_F32 returns
+ *          PYG_ERR_UNSUPPORTED), 16-byte aligned rows (Fi % 8 == 0) take the
+ *          vector path;
+ *   theta  [Fi, Fo] bf16 row-major;
+ *   out    [N, Fo] in out_dtype (PYG_F32, or PYG_BF16 rounded once), may not
+ *          overlap x.
+ * Deterministic. Errors: PYG_ERR_INVALID_ARG (NULL pointers, negative sizes,
+ * overlap), PYG_ERR_UNSUPPORTED (fp32 x, N >= 2^31), PYG_ERR_WORKSPACE. */
+int pyg_dense_transform(const void *x, int x_dtype, int64_t N, int64_t Fi, const void *theta, int64_t Fo,
+                        void *out, int out_dtype, void *ws, size_t ws_bytes, void *stream);
+
 /* Workspace bytes needed by pyg_global_pool. */
 int pyg_global_pool_workspace(int dtype, int64_t N, int64_t F, int64_t B, int aggr, size_t *bytes);
 

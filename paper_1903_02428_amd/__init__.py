@@ -21,6 +21,7 @@ from .binding import (  # noqa: F401
     abi_version,
     coo_to_csr,
     degree,
+    dense_transform,
     gat_softmax,
     gather_edges,
     gcn_norm,

@@ -23,7 +23,7 @@ EXPORTED = [
     "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_gcn_norm_csr_workspace", "pyg_gcn_norm_csr",
     "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_backward_workspace", "pyg_propagate_backward",
     "pyg_segment_softmax_workspace", "pyg_segment_softmax", "pyg_gat_softmax", "pyg_segment_softmax_backward",
-    "pyg_propagate_heads_workspace", "pyg_propagate_heads",
+    "pyg_propagate_heads_workspace", "pyg_propagate_heads", "pyg_dense_transform_workspace", "pyg_dense_transform",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
 ]
 
@@ -84,6 +84,8 @@ def library() -> ctypes.CDLL:
             "pyg_segment_softmax_backward": [p, p, i64, ctypes.POINTER(_Csr), i32, p, p, ctypes.c_size_t, p],
             "pyg_propagate_heads_workspace": [i32, i64, i64, i64, i64, i64, sz],
             "pyg_propagate_heads": [p, i32, i64, i64, i64, ctypes.POINTER(_Csr), p, p, p, ctypes.c_size_t, p],
+            "pyg_dense_transform_workspace": [i64, i64, sz],
+            "pyg_dense_transform": [p, i32, i64, i64, p, i64, p, i32, p, ctypes.c_size_t, p],
             "pyg_global_pool_workspace": [i32, i64, i64, i64, i32, sz],
             "pyg_global_pool": [p, i32, i64, i64, p, i64, i32, p, p, p, ctypes.c_size_t, p],
             "pyg_validate_coo": [p, i64, i64, p, p],
@@ -436,6 +438,28 @@ def propagate_heads(x: torch.Tensor, csr: CSR, alpha: torch.Tensor, heads: int, 
     c = csr._c()
     _check(lib.pyg_propagate_heads(_ptr(x), DTYPE[x.dtype], N, heads, C, ctypes.byref(c), _ptr(a2), _ptr(out),
                                    _ptr(workspace), workspace.numel(), _stream(x.device)), "pyg_propagate_heads")
+    return out
+
+
+def dense_transform(x: torch.Tensor, theta: torch.Tensor, out_dtype=torch.float32, out: torch.Tensor | None = None,
+                    workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """x [N, Fi] (bf16) times theta [Fi, Fo] (bf16) on the matrix cores, fp32
+    accumulation; the result in out_dtype (float32 or bfloat16)."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    _need_cuda("theta", theta, torch.bfloat16, 2)
+    if x.dtype not in DTYPE or out_dtype not in DTYPE:
+        raise ValueError("x and out must be float32 or bfloat16")
+    N, Fi = x.shape
+    if theta.shape[0] != Fi:
+        raise ValueError("theta must be [Fi, Fo]")
+    Fo = theta.shape[1]
+    out = torch.empty((N, Fo), dtype=out_dtype, device=x.device) if out is None else out
+    nbytes = _size(lib.pyg_dense_transform_workspace, Fi, Fo)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, x.device)
+    _check(lib.pyg_dense_transform(_ptr(x), DTYPE[x.dtype], N, Fi, _ptr(theta), Fo, _ptr(out), DTYPE[out.dtype],
+                                   _ptr(workspace), workspace.numel(), _stream(x.device)), "pyg_dense_transform")
     return out
 
 

@@ -189,3 +189,20 @@ def test_attention_entry_points_reject_bad_arguments(lib):
     assert _ws(lib.pyg_segment_softmax_workspace, 10, 5, -1, 0)[0] == INVALID
     assert _ws(lib.pyg_propagate_heads_workspace, 0, 10, 2, 4, 20, 0)[0] == PYG_OK
     assert _ws(lib.pyg_propagate_heads_workspace, 0, 10, 2**20, 2**12, 20, 0)[0] == UNSUPPORTED
+
+
+def test_dense_transform_rejects_bad_arguments(lib):
+    X, T, OUT = FAKE, ctypes.c_void_p(0x300000), ctypes.c_void_p(0x900000)
+    dt = lib.pyg_dense_transform
+    assert dt(X, 0, 10, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == UNSUPPORTED   # fp32 operands
+    assert dt(X, 7, 10, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == INVALID       # bad dtype
+    assert dt(X, 1, 10, 8, T, 4, OUT, 9, FAKE, 1 << 30, None) == INVALID       # bad out dtype
+    assert dt(X, 1, -1, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == INVALID
+    assert dt(None, 1, 10, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == INVALID
+    assert dt(X, 1, 10, 8, None, 4, OUT, 0, FAKE, 1 << 30, None) == INVALID
+    assert dt(X, 1, 10, 8, T, 4, None, 0, FAKE, 1 << 30, None) == INVALID
+    assert dt(X, 1, 10, 8, T, 4, OUT, 0, FAKE, 0, None) == WORKSPACE
+    assert dt(X, 1, 10, 8, T, 4, ctypes.c_void_p(0x10000 + 32), 0, FAKE, 1 << 30, None) == INVALID  # overlap
+    assert dt(X, 1, 2**31, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == UNSUPPORTED
+    rc, b = _ws(lib.pyg_dense_transform_workspace, 602, 41)
+    assert rc == PYG_OK and b >= 48 * 608 * 2
