@@ -24,7 +24,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
-MSG = {"src": 0, "diff": 1}
+MSG = {"src": 0, "diff": 1, "edge_add": 2, "edge_relu": 3, "edge_mul": 4}
 AGGR = {"sum": 0, "mean": 1, "max": 2}
 _ERR = {-1: "invalid argument", -2: "index out of range", -3: "non-finite input"}
 
@@ -57,7 +57,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_degree.argtypes = [p, i64, i64, p]
     lib.oracle_coo_to_csr.argtypes = [p, i64, i64, p, p, p]
     lib.oracle_gcn_norm.argtypes = [p, p, i64, i64, p]
-    lib.oracle_propagate.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p]
+    lib.oracle_propagate.argtypes = [p, i64, i64, p, i64, p, p, i32, i32, p, p, p]
     lib.oracle_global_pool.argtypes = [p, i64, i64, p, i64, i32, p, p, p]
     lib.oracle_propagate_backward.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p, p, p, p]
     lib.oracle_gat_scores.argtypes = [p, p, i64, i64, p, i64, ctypes.c_float, p]
@@ -122,9 +122,10 @@ def gcn_norm(edge_index, N: int, edge_weight=None, lib=None) -> np.ndarray:
     return norm
 
 
-def propagate(x, edge_index, edge_weight=None, msg: str = "src", aggr: str = "sum", lib=None):
+def propagate(x, edge_index, edge_weight=None, msg: str = "src", aggr: str = "sum", lib=None, edge_attr=None):
     """Eq. (1) with gamma = identity. Returns (out fp64 [N,F], argmax int64 [N,F] or None,
-    sabs fp64 [N,F] = sum |message| (per degree for mean))."""
+    sabs fp64 [N,F] = sum |message| (per degree for mean)). edge_attr [E, F]
+    goes with the edge_* messages."""
     lib = lib or load()
     x = np.ascontiguousarray(x, dtype=np.float32)
     if x.ndim != 2:
@@ -133,10 +134,13 @@ def propagate(x, edge_index, edge_weight=None, msg: str = "src", aggr: str = "su
     ei = _ei(edge_index)
     E = ei.shape[1]
     w = None if edge_weight is None else np.ascontiguousarray(edge_weight, dtype=np.float32)
+    ea = None if edge_attr is None else np.ascontiguousarray(edge_attr, dtype=np.float32)
+    if ea is not None and ea.shape != (E, F):
+        raise ValueError("edge_attr must be [E, F]")
     out = np.empty((N, F), np.float64)
     sabs = np.empty((N, F), np.float64)
     arg = np.empty((N, F), np.int64) if aggr == "max" else None
-    _check(lib.oracle_propagate(_ptr(x), N, F, _ptr(ei), E, _ptr(w), MSG[msg], AGGR[aggr],
+    _check(lib.oracle_propagate(_ptr(x), N, F, _ptr(ei), E, _ptr(w), _ptr(ea), MSG[msg], AGGR[aggr],
                                 _ptr(out), _ptr(arg), _ptr(sabs)), "propagate")
     return out, arg, sabs
 

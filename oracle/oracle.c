@@ -42,8 +42,11 @@
 #define ORACLE_ERR_NONFINITE (-3)
 
 /* message kinds phi (Eq. 1) */
-#define ORACLE_MSG_SRC 0  /* x_j, times w_{j,i} when a weight is given */
-#define ORACLE_MSG_DIFF 1 /* x_j - x_i (EdgeConv-style) */
+#define ORACLE_MSG_SRC 0       /* x_j, times w_{j,i} when a weight is given */
+#define ORACLE_MSG_DIFF 1      /* x_j - x_i (EdgeConv-style) */
+#define ORACLE_MSG_EDGE_ADD 2  /* x_j + e_{j,i} (F-dimensional edge features) */
+#define ORACLE_MSG_EDGE_RELU 3 /* max(x_j + e_{j,i}, 0) */
+#define ORACLE_MSG_EDGE_MUL 4  /* x_j * e_{j,i}, elementwise */
 
 /* aggregations (the permutation-invariant operator of Eq. 1) */
 #define ORACLE_SUM 0
@@ -117,10 +120,11 @@ int oracle_gcn_norm(const int64_t *edge_index, const double *w, int64_t E, int64
 
 /* Shared by propagate and pooling: reduce messages m_k (k = 0..E-1, in
  * order) into rows tgt[k]. The message of element (k, f) is built by
- * the caller-supplied source row, weight and (for DIFF) target row. */
+ * the caller-supplied source row, weight, (for DIFF) target row and (for
+ * the EDGE kinds) edge feature row ea[k]. */
 static int reduce_edges(const float *x, int64_t N_src, int64_t F,
                         const int64_t *src, const int64_t *tgt, int64_t E, int64_t N_out,
-                        const float *w, int msg, int aggr,
+                        const float *w, const float *ea, int msg, int aggr,
                         double *out, int64_t *argmax, double *sabs, int64_t sentinel) {
     int64_t *cnt = (int64_t *)calloc((size_t)(N_out > 0 ? N_out : 1), sizeof(int64_t));
     float *best = (float *)malloc((size_t)((N_out * F) > 0 ? N_out * F : 1) * sizeof(float));
@@ -140,6 +144,9 @@ static int reduce_edges(const float *x, int64_t N_src, int64_t F,
             if (aggr == ORACLE_MAX) {
                 float m;
                 if (msg == ORACLE_MSG_DIFF) m = xj - x[i * F + f];
+                else if (msg == ORACLE_MSG_EDGE_ADD) m = xj + ea[k * F + f];
+                else if (msg == ORACLE_MSG_EDGE_RELU) m = xj + ea[k * F + f] > 0.0f ? xj + ea[k * F + f] : 0.0f;
+                else if (msg == ORACLE_MSG_EDGE_MUL) m = xj * ea[k * F + f];
                 else if (w) m = w[k] * xj;
                 else m = xj;
                 if (m == 0.0f) m = 0.0f; /* -0.0 -> +0.0 */
@@ -150,6 +157,9 @@ static int reduce_edges(const float *x, int64_t N_src, int64_t F,
             } else {
                 double m;
                 if (msg == ORACLE_MSG_DIFF) m = (double)xj - (double)x[i * F + f];
+                else if (msg == ORACLE_MSG_EDGE_ADD) m = (double)xj + (double)ea[k * F + f];
+                else if (msg == ORACLE_MSG_EDGE_RELU) m = fmax((double)xj + (double)ea[k * F + f], 0.0);
+                else if (msg == ORACLE_MSG_EDGE_MUL) m = (double)xj * (double)ea[k * F + f];
                 else if (w) m = (double)w[k] * (double)xj;
                 else m = (double)xj;
                 out[o] += m;
@@ -181,25 +191,30 @@ static int all_finite(const float *a, int64_t n) {
 
 /* Propagate, Eq. (1) with gamma = identity:
  *   out_i = AGG_{k : I[1,k] = i} phi_k,
- *   phi_k = x_j (SRC), w_k * x_j (SRC with weight), or x_j - x_i (DIFF),
+ *   phi_k = x_j (SRC), w_k * x_j (SRC with weight), x_j - x_i (DIFF), or,
+ *   with F-dimensional edge features e_k = ea[k] (the e_{j,i} of Eq. 1):
+ *   x_j + e_k (EDGE_ADD), max(x_j + e_k, 0) (EDGE_RELU), x_j * e_k (EDGE_MUL),
  * for every feature column. out is fp64 [N,F]; argmax (int64 [N,F], max
  * only, else may be NULL) holds the winning edge id; sabs (nullable) holds
- * sum |phi| (divided by the degree for mean). */
+ * sum |phi| (divided by the degree for mean). Max compares the messages
+ * formed in fp32 (one fp32 add or multiply). */
 int oracle_propagate(const float *x, int64_t N, int64_t F,
-                     const int64_t *edge_index, int64_t E, const float *w,
+                     const int64_t *edge_index, int64_t E, const float *w, const float *ea,
                      int msg, int aggr, double *out, int64_t *argmax, double *sabs) {
     if (N < 0 || F < 0 || E < 0) return ORACLE_ERR_ARG;
-    if (msg != ORACLE_MSG_SRC && msg != ORACLE_MSG_DIFF) return ORACLE_ERR_ARG;
+    if (msg < ORACLE_MSG_SRC || msg > ORACLE_MSG_EDGE_MUL) return ORACLE_ERR_ARG;
     if (aggr != ORACLE_SUM && aggr != ORACLE_MEAN && aggr != ORACLE_MAX) return ORACLE_ERR_ARG;
-    if (msg == ORACLE_MSG_DIFF && w) return ORACLE_ERR_ARG;
+    const int edge_msg = msg >= ORACLE_MSG_EDGE_ADD;
+    if (w && msg != ORACLE_MSG_SRC) return ORACLE_ERR_ARG;
+    if (edge_msg != (ea != NULL) && E * F > 0) return ORACLE_ERR_ARG;
     if (aggr == ORACLE_MAX && N * F > 0 && !argmax) return ORACLE_ERR_ARG;
     if (N * F > 0 && (!x || !out)) return ORACLE_ERR_ARG;
     if (E > 0 && !edge_index) return ORACLE_ERR_ARG;
     const int64_t *src = edge_index;
     const int64_t *dst = edge_index + E;
     if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
-    if (!all_finite(x, N * F) || (w && !all_finite(w, E))) return ORACLE_ERR_NONFINITE;
-    return reduce_edges(x, N, F, src, dst, E, N, w, msg, aggr, out, argmax, sabs, E);
+    if (!all_finite(x, N * F) || (w && !all_finite(w, E)) || (ea && !all_finite(ea, E * F))) return ORACLE_ERR_NONFINITE;
+    return reduce_edges(x, N, F, src, dst, E, N, w, ea, msg, aggr, out, argmax, sabs, E);
 }
 
 /* Global pooling (Section 2, "Global Pooling" and "Mini-batch Handling"):
@@ -220,7 +235,7 @@ int oracle_global_pool(const float *x, int64_t N, int64_t F, const int64_t *batc
     int64_t *node = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
     if (!node) return ORACLE_ERR_ARG;
     for (int64_t n = 0; n < N; ++n) node[n] = n;
-    int rc = reduce_edges(x, N, F, node, batch, N, B, NULL, ORACLE_MSG_SRC, aggr, out, argmax, sabs, N);
+    int rc = reduce_edges(x, N, F, node, batch, N, B, NULL, NULL, ORACLE_MSG_SRC, aggr, out, argmax, sabs, N);
     free(node);
     return rc;
 }

@@ -577,10 +577,59 @@ def pin_dense_transform_library(lib):
         assert np.allclose(lhs, rhs, rtol=1e-5, atol=1e-5)
 
 
+def pin_golden_edge_messages(lib):
+    g = golden()
+    pr, em = g["propagate"], g["edge_messages"]
+    x = np.array(pr["x"], np.float32)
+    ei = np.array(pr["edge_index"], np.int64)
+    ea = np.array(em["edge_attr"], np.float32)
+    for msg, key in (("edge_add", "add"), ("edge_relu", "relu"), ("edge_mul", "mul")):
+        out, _, _ = oracle.propagate(x, ei, msg=msg, aggr="sum", edge_attr=ea, lib=lib)
+        assert np.array_equal(out, np.array(em[f"{key}_sum"])), msg
+        mean, _, _ = oracle.propagate(x, ei, msg=msg, aggr="mean", edge_attr=ea, lib=lib)
+        assert np.allclose(mean * 3, np.array(em[f"{key}_sum"]), rtol=1e-15, atol=1e-15)
+        mx, arg, _ = oracle.propagate(x, ei, msg=msg, aggr="max", edge_attr=ea, lib=lib)
+        assert np.array_equal(mx, np.array(em[f"{key}_max"])) and np.array_equal(arg, np.array(em[f"{key}_argmax"])), msg
+
+
+def pin_edge_messages_library(lib):
+    """Sums against numpy scatter-adds of the formed messages, max against CPU
+    torch scatter_reduce(amax); e = 0 (add) and e = 1 (mul) reduce to the plain
+    propagate; large positive e makes relu the identity."""
+    for N, F, ei, x, w in small_cases():
+        rng = np.random.default_rng(N + 5)
+        E = ei.shape[1]
+        ea = rng.standard_normal((E, F)).astype(np.float32)
+        xs = x[ei[0]].astype(np.float64)
+        for msg, m in (("edge_add", xs + ea), ("edge_relu", np.maximum(xs + ea, 0.0)), ("edge_mul", xs * ea)):
+            ref = np.zeros((N, F))
+            np.add.at(ref, ei[1], m)
+            out, _, _ = oracle.propagate(x, ei, msg=msg, aggr="sum", edge_attr=ea, lib=lib)
+            assert np.allclose(out, ref, rtol=1e-12, atol=1e-12), msg
+            mx, _, _ = oracle.propagate(x, ei, msg=msg, aggr="max", edge_attr=ea, lib=lib)
+            m32 = torch.from_numpy(m.astype(np.float32))
+            tmax = torch.zeros(N, F).scatter_reduce(0, torch.from_numpy(ei[1])[:, None].expand(-1, F), m32, "amax",
+                                                    include_self=False)
+            assert np.array_equal(mx.astype(np.float32), tmax.numpy()), msg
+        for aggr in ("sum", "mean", "max"):
+            base = oracle.propagate(x, ei, aggr=aggr, lib=lib)
+            z = oracle.propagate(x, ei, msg="edge_add", aggr=aggr, edge_attr=np.zeros((E, F), np.float32), lib=lib)
+            one = oracle.propagate(x, ei, msg="edge_mul", aggr=aggr, edge_attr=np.ones((E, F), np.float32), lib=lib)
+            for got in (z, one):
+                assert np.array_equal(got[0], base[0])
+                if aggr == "max":
+                    assert np.array_equal(got[1], base[1])
+            big = np.full((E, F), 100.0, np.float32)
+            r = oracle.propagate(x, ei, msg="edge_relu", aggr=aggr, edge_attr=big, lib=lib)
+            a = oracle.propagate(x, ei, msg="edge_add", aggr=aggr, edge_attr=big, lib=lib)
+            assert np.array_equal(r[0], a[0])
+
+
 ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_golden_gcn_norm_directed,
             pin_golden_signed_zero,
             pin_degree_and_csr_library, pin_sum_mean_dense, pin_torch_scatter, pin_max_bruteforce,
             pin_gcn_norm_closed_forms, pin_invariants, pin_pool_relations, pin_golden_backward,
             pin_backward_autograd, pin_backward_dense, pin_golden_attention, pin_softmax_library,
             pin_softmax_invariants, pin_softmax_backward_autograd, pin_heads_dense, pin_uniform_attention_is_mean,
-            pin_golden_dense_transform, pin_dense_transform_library]
+            pin_golden_dense_transform, pin_dense_transform_library, pin_golden_edge_messages,
+            pin_edge_messages_library]

@@ -13,8 +13,8 @@ import oracle
 # (name, original text, mutated text); each original must occur in oracle.c
 MUTANTS = [
     ("propagate_swaps_src_dst",
-     "return reduce_edges(x, N, F, src, dst, E, N, w, msg, aggr, out, argmax, sabs, E);",
-     "return reduce_edges(x, N, F, dst, src, E, N, w, msg, aggr, out, argmax, sabs, E);"),
+     "return reduce_edges(x, N, F, src, dst, E, N, w, ea, msg, aggr, out, argmax, sabs, E);",
+     "return reduce_edges(x, N, F, dst, src, E, N, w, ea, msg, aggr, out, argmax, sabs, E);"),
     ("sum_overwrites", "out[o] += m;", "out[o] = m;"),
     ("diff_wrong_sign", "m = (double)xj - (double)x[i * F + f];", "m = (double)xj + (double)x[i * F + f];"),
     ("diff_max_wrong_operand", "if (msg == ORACLE_MSG_DIFF) m = xj - x[i * F + f];",
@@ -66,6 +66,14 @@ MUTANTS = [
     ("heads_bwd_dot_uses_target_x", "dot += gi * (double)x[j * F + h * C + c];", "dot += gi * (double)x[i * F + h * C + c];"),
     ("transform_theta_transposed", "const double t = (double)x[n * Fi + k] * (double)theta[k * Fo + o];",
      "const double t = (double)x[n * Fi + k] * (double)theta[o * Fi + k];"),
+    ("edge_add_ignores_edge", "else if (msg == ORACLE_MSG_EDGE_ADD) m = (double)xj + (double)ea[k * F + f];",
+     "else if (msg == ORACLE_MSG_EDGE_ADD) m = (double)xj;"),
+    ("edge_attr_by_source", "else if (msg == ORACLE_MSG_EDGE_MUL) m = (double)xj * (double)ea[k * F + f];",
+     "else if (msg == ORACLE_MSG_EDGE_MUL) m = (double)xj * (double)ea[(j % E) * F + f];"),
+    ("edge_relu_missing", "else if (msg == ORACLE_MSG_EDGE_RELU) m = fmax((double)xj + (double)ea[k * F + f], 0.0);",
+     "else if (msg == ORACLE_MSG_EDGE_RELU) m = (double)xj + (double)ea[k * F + f];"),
+    ("edge_max_relu_keeps_negative", "else if (msg == ORACLE_MSG_EDGE_RELU) m = xj + ea[k * F + f] > 0.0f ? xj + ea[k * F + f] : 0.0f;",
+     "else if (msg == ORACLE_MSG_EDGE_RELU) m = xj + ea[k * F + f];"),
     ("transform_skips_last_k", "for (int64_t k = 0; k < Fi; ++k) {\n                const double t",
      "for (int64_t k = 0; k + 1 < Fi; ++k) {\n                const double t"),
 ]
