@@ -58,9 +58,19 @@ typedef enum { PYG_F32 = 0, PYG_BF16 = 1 } pyg_dtype;
 typedef enum { PYG_SUM = 0, PYG_MEAN = 1, PYG_MAX = 2 } pyg_aggr;
 
 /* The message function phi of Eq. (1):
- *   PYG_MSG_SRC   phi = x_j, or w_k * x_j when a weight is given;
- *   PYG_MSG_DIFF  phi = x_j - x_i (the EdgeConv message, Section 2). */
-typedef enum { PYG_MSG_SRC = 0, PYG_MSG_DIFF = 1 } pyg_msg;
+ *   PYG_MSG_SRC        phi = x_j, or w_k * x_j when a weight is given;
+ *   PYG_MSG_DIFF       phi = x_j - x_i (the EdgeConv message, Section 2);
+ * and, with F-dimensional edge features e_{j,i} (pyg_propagate_edge only):
+ *   PYG_MSG_EDGE_ADD   phi = x_j + e_{j,i};
+ *   PYG_MSG_EDGE_RELU  phi = max(x_j + e_{j,i}, 0) (GINE-style);
+ *   PYG_MSG_EDGE_MUL   phi = x_j * e_{j,i}, elementwise. */
+typedef enum {
+    PYG_MSG_SRC = 0,
+    PYG_MSG_DIFF = 1,
+    PYG_MSG_EDGE_ADD = 2,
+    PYG_MSG_EDGE_RELU = 3,
+    PYG_MSG_EDGE_MUL = 4
+} pyg_msg;
 
 /* Kernel choice (Appendix A contrasts the two schemes):
  *   PYG_KERNEL_COO_ATOMIC   gather/scatter over the unsorted COO with
@@ -188,6 +198,25 @@ int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F,
                   const int64_t *edge_index, int64_t E, const float *edge_weight,
                   const pyg_csr *csr, int msg, int aggr, int kernel,
                   void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
+
+/* Propagate with F-dimensional edge features in the message (Eq. (1)'s
+ * e_{j,i}; Section 2 and Appendix A name the integration of
+ * multi-dimensional edge information as a property of the gather/scatter
+ * scheme):
+ *   out[i, f] = AGG over edges k = (j -> i) of phi(x_j[f], e_k[f]),
+ * phi from msg (PYG_MSG_EDGE_ADD / _RELU / _MUL), AGG from aggr.
+ *   edge_attr  [E, F] in x's dtype (device); attr_order PYG_ORDER_COO (row k
+ *              = edge k) or PYG_ORDER_CSR (row p = CSR slot p, the coalesced
+ *              layout; CSR kernel only, COO order is reached through
+ *              csr->perm);
+ *   kernel     as in pyg_propagate (COO atomics or CSR segments); the CSR
+ *              kernel ignores csr->weight here;
+ *   other arguments, the workspace (pyg_propagate_workspace), outputs,
+ *   argmax, tie and -0.0 rules as in pyg_propagate. Messages are formed in
+ *   fp32 (one add or multiply, then max(., 0) for _RELU); max compares them. */
+int pyg_propagate_edge(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                       const void *edge_attr, int attr_order, const pyg_csr *csr, int msg, int aggr, int kernel,
+                       void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_propagate_backward (chunk_t = csr_t->chunk). */
 int pyg_propagate_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int64_t chunk_t,

@@ -31,6 +31,7 @@ from .binding import (  # noqa: F401
     library_path,
     propagate,
     propagate_backward,
+    propagate_edge,
     propagate_heads,
     propagate_workspace_bytes,
     reverse_edges,

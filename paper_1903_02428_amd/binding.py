@@ -13,7 +13,7 @@ LIB_NAME = "libpyg_mi355x.so"
 PYG_OK = 0
 DTYPE = {torch.float32: 0, torch.bfloat16: 1}
 AGGR = {"sum": 0, "mean": 1, "max": 2}
-MSG = {"src": 0, "diff": 1}
+MSG = {"src": 0, "diff": 1, "edge_add": 2, "edge_relu": 3, "edge_mul": 4}
 KERNEL = {"auto": 0, "coo": 1, "csr": 2}
 ORDER = {"csr": 0, "coo": 1}
 
@@ -21,7 +21,8 @@ EXPORTED = [
     "pyg_strerror", "pyg_abi_version", "pyg_degree_workspace", "pyg_degree", "pyg_coo_to_csr_workspace",
     "pyg_coo_to_csr", "pyg_gather_edges",
     "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_gcn_norm_csr_workspace", "pyg_gcn_norm_csr",
-    "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_backward_workspace", "pyg_propagate_backward",
+    "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_edge", "pyg_propagate_backward_workspace",
+    "pyg_propagate_backward",
     "pyg_segment_softmax_workspace", "pyg_segment_softmax", "pyg_gat_softmax", "pyg_segment_softmax_backward",
     "pyg_propagate_heads_workspace", "pyg_propagate_heads", "pyg_dense_transform_workspace", "pyg_dense_transform",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
@@ -75,6 +76,8 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                               ctypes.c_size_t, p],
+            "pyg_propagate_edge": [p, i32, i64, i64, p, i64, p, i32, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
+                                   ctypes.c_size_t, p],
             "pyg_propagate_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
             "pyg_propagate_backward": [p, p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr),
                                        i32, i32, p, p, p, p, ctypes.c_size_t, p],
@@ -299,6 +302,45 @@ def propagate(x: torch.Tensor, edge_index: torch.Tensor | None = None, edge_weig
                            ctypes.byref(c) if c is not None else None, MSG[msg], AGGR[aggr], KERNEL[kernel],
                            _ptr(out), _ptr(argmax), _ptr(workspace), workspace.numel(), _stream(dev))
     _check(rc, "pyg_propagate")
+    return out, argmax
+
+
+def propagate_edge(x: torch.Tensor, edge_attr: torch.Tensor, edge_index: torch.Tensor | None = None,
+                   csr: CSR | None = None, msg: str = "edge_add", aggr: str = "sum", kernel: str = "auto",
+                   attr_order: str = "coo", out: torch.Tensor | None = None, argmax: torch.Tensor | None = None,
+                   workspace: torch.Tensor | None = None):
+    """Eq. (1) with F-dimensional edge features: phi = x_j + e, max(x_j + e, 0)
+    or x_j * e (msg "edge_add", "edge_relu", "edge_mul"). edge_attr [E, F] in
+    x's dtype, rows in `attr_order` ("coo": edge id, "csr": CSR slot).
+    Returns (out, argmax or None)."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    if x.dtype not in DTYPE:
+        raise ValueError("x must be float32 or bfloat16")
+    N, F = x.shape
+    dev = x.device
+    if edge_index is not None:
+        E = _edge_index(edge_index)
+    elif csr is not None:
+        E = csr.E
+    else:
+        raise ValueError("need edge_index or csr")
+    _need_cuda("edge_attr", edge_attr, x.dtype, 2)
+    if tuple(edge_attr.shape) != (E, F):
+        raise ValueError("edge_attr must be [E, F]")
+    if msg not in ("edge_add", "edge_relu", "edge_mul") or aggr not in AGGR or kernel not in KERNEL:
+        raise ValueError("bad msg / aggr / kernel")
+    out = torch.empty_like(x) if out is None else out
+    argmax = (torch.empty((N, F), dtype=torch.int64, device=dev) if argmax is None else argmax) if aggr == "max" else None
+    use = "coo" if kernel == "coo" or (kernel == "auto" and csr is None) else "csr"
+    nbytes = propagate_workspace_bytes(x, E, aggr, use, csr.chunk if (csr is not None and use == "csr") else 0)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, dev)
+    c = csr._c() if csr is not None else None
+    rc = lib.pyg_propagate_edge(_ptr(x), DTYPE[x.dtype], N, F, _ptr(edge_index), E, _ptr(edge_attr), ORDER[attr_order],
+                                ctypes.byref(c) if c is not None else None, MSG[msg], AGGR[aggr], KERNEL[kernel],
+                                _ptr(out), _ptr(argmax), _ptr(workspace), workspace.numel(), _stream(dev))
+    _check(rc, "pyg_propagate_edge")
     return out, argmax
 
 

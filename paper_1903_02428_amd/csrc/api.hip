@@ -116,6 +116,64 @@ extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, con
     return segment_reduce(a, ws, ws_bytes, s);
 }
 
+extern "C" int pyg_propagate_edge(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                                  const void *edge_attr, int attr_order, const pyg_csr *csr, int msg, int aggr,
+                                  int kernel, void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0) return PYG_ERR_INVALID_ARG;
+    if (msg != PYG_MSG_EDGE_ADD && msg != PYG_MSG_EDGE_RELU && msg != PYG_MSG_EDGE_MUL) return PYG_ERR_INVALID_ARG;
+    if (attr_order != PYG_ORDER_COO && attr_order != PYG_ORDER_CSR) return PYG_ERR_INVALID_ARG;
+    if (kernel != PYG_KERNEL_AUTO && kernel != PYG_KERNEL_COO_ATOMIC && kernel != PYG_KERNEL_CSR_SEGMENT)
+        return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
+    if ((aggr == PYG_MAX) != (argmax != nullptr) && N * F > 0) return PYG_ERR_INVALID_ARG;
+    if (aggr != PYG_MAX && argmax) return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && (!x || !out)) return PYG_ERR_INVALID_ARG;
+    if (E * F > 0 && !edge_attr) return PYG_ERR_INVALID_ARG;
+    if (E > 0 && N == 0) return PYG_ERR_INVALID_ARG;
+    const int64_t esz = dtype_size(dtype);
+    const int64_t xbytes = N * F * esz;
+    if (overlaps(x, xbytes, out, xbytes) || overlaps(edge_attr, E * F * esz, out, xbytes)) return PYG_ERR_INVALID_ARG;
+    if (argmax && (overlaps(argmax, N * F * 8, x, xbytes) || overlaps(argmax, N * F * 8, out, xbytes)))
+        return PYG_ERR_INVALID_ARG;
+    if (kernel == PYG_KERNEL_CSR_SEGMENT && !csr) return PYG_ERR_INVALID_ARG;
+    const bool use_csr = kernel == PYG_KERNEL_CSR_SEGMENT || (kernel == PYG_KERNEL_AUTO && csr);
+    if (use_csr) {
+        if (csr->N != N || csr->E != E || !csr->rowptr || csr->chunk < 0) return PYG_ERR_INVALID_ARG;
+        if (E > 0 && (!csr->col || ((aggr == PYG_MAX || attr_order == PYG_ORDER_COO) && !csr->perm)))
+            return PYG_ERR_INVALID_ARG;
+    } else {
+        if (E > 0 && !edge_index) return PYG_ERR_INVALID_ARG;
+        if (attr_order != PYG_ORDER_COO) return PYG_ERR_INVALID_ARG;  // the COO kernel reads edges in COO order
+    }
+    size_t need;
+    PYG_TRY(pyg_propagate_workspace(dtype, N, F, E, aggr, use_csr ? PYG_KERNEL_CSR_SEGMENT : PYG_KERNEL_COO_ATOMIC,
+                                    use_csr ? csr->chunk : 0, &need));
+    if (ws_bytes < need || (need > 256 && !ws)) return PYG_ERR_WORKSPACE;
+    if (N * F == 0) return PYG_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (!use_csr)
+        return coo_propagate(x, dtype, N, F, edge_index, E, nullptr, msg, aggr, out, argmax, ws, ws_bytes, s, edge_attr);
+    SegmentArgs a{};
+    a.x = x;
+    a.dtype = dtype;
+    a.F = F;
+    a.rowptr = csr->rowptr;
+    a.col = csr->col;
+    a.perm = csr->perm;
+    a.edge_attr = E > 0 ? edge_attr : nullptr;
+    a.attr_perm = attr_order == PYG_ORDER_COO ? csr->perm : nullptr;
+    a.n_rows = N;
+    a.E = E;
+    a.msg = msg;
+    a.aggr = aggr;
+    a.chunk = csr->chunk;
+    a.sentinel = E;
+    a.out = out;
+    a.argmax = argmax;
+    a.hint = true;
+    return segment_reduce(a, ws, ws_bytes, s);
+}
+
 extern "C" int pyg_propagate_heads_workspace(int dtype, int64_t N, int64_t H, int64_t C, int64_t E, int64_t chunk,
                                              size_t *bytes) {
     if (!bytes || !valid_dtype(dtype) || N < 0 || H < 0 || C < 0 || E < 0 || chunk < 0) return PYG_ERR_INVALID_ARG;

@@ -138,6 +138,8 @@ struct SegmentArgs {
     const int32_t *col;    // [E] source row per slot; NULL = identity (slot id)
     const float *weight;   // [E] or NULL
     const float *alpha;    // [E, H] per-head weights in slot order, or NULL (sum only)
+    const void *edge_attr;       // [E, F] edge features in x's dtype (edge messages), or NULL
+    const int64_t *attr_perm;    // non-NULL: edge_attr rows are COO edge ids, reached through perm
     int64_t H;             // heads; feature f belongs to head f / C
     int64_t C;
     const int64_t *perm;   // [E] id reported by argmax; NULL = slot id
@@ -157,7 +159,9 @@ int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t 
 
 // Unsorted-COO gather/scatter with hardware atomics.
 size_t coo_workspace(int dtype, int64_t N, int64_t F, int aggr);
+// ea: [E, F] edge features in x's dtype for the edge messages, else NULL.
 int coo_propagate(const void *x, int dtype, int64_t N, int64_t F, const int64_t *ei, int64_t E, const float *w, int msg,
-                  int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, hipStream_t s);
+                  int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, hipStream_t s,
+                  const void *ea = nullptr);
 
 }  // namespace pyg

@@ -31,33 +31,40 @@ __device__ __forceinline__ void store1(T *p, int64_t i, float v) {
     else p[i] = v;
 }
 
-template <typename T, int MSG>  // 0 src, 1 weighted, 2 diff
-__device__ __forceinline__ float message(const T *x, int64_t F, int64_t j, int64_t i, int64_t f, float wk) {
+// 0 src, 1 weighted, 2 diff; edge features e_k: 4 x_j + e, 5 max(x_j + e, 0), 6 x_j * e
+template <typename T, int MSG>
+__device__ __forceinline__ float message(const T *x, int64_t F, int64_t j, int64_t i, int64_t f, float wk,
+                                         const T *ea, int64_t k) {
     const float xj = load1(x, j * F + f);
     if constexpr (MSG == 2) return xj - load1(x, i * F + f);
     else if constexpr (MSG == 1) return wk * xj;
+    else if constexpr (MSG == 4) return xj + load1(ea, k * F + f);
+    else if constexpr (MSG == 5) return (xj + load1(ea, k * F + f)) > 0.f ? (xj + load1(ea, k * F + f)) : 0.f;
+    else if constexpr (MSG == 6) return xj * load1(ea, k * F + f);
     else return xj;
 }
 
 template <typename T, int MSG, bool COUNT>
 __global__ __launch_bounds__(kBlock) void k_coo_add(const T *__restrict__ x, int64_t F, const int64_t *__restrict__ src,
-                                                    const int64_t *__restrict__ dst, const float *__restrict__ w, int64_t E,
-                                                    int lg, float *__restrict__ acc, unsigned *__restrict__ cnt) {
+                                                    const int64_t *__restrict__ dst, const float *__restrict__ w,
+                                                    const T *__restrict__ ea, int64_t E, int lg,
+                                                    float *__restrict__ acc, unsigned *__restrict__ cnt) {
     const int G = 1 << lg;
     const int64_t per_grid = (int64_t)gridDim.x * (kBlock >> lg);
     const int q = threadIdx.x & (G - 1);
     for (int64_t k = (int64_t)blockIdx.x * (kBlock >> lg) + (threadIdx.x >> lg); k < E; k += per_grid) {
         const int64_t j = src[k], i = dst[k];
         const float wk = MSG == 1 ? w[k] : 1.f;
-        for (int64_t f = q; f < F; f += G) unsafeAtomicAdd(&acc[i * F + f], message<T, MSG>(x, F, j, i, f, wk));
+        for (int64_t f = q; f < F; f += G) unsafeAtomicAdd(&acc[i * F + f], message<T, MSG>(x, F, j, i, f, wk, ea, k));
         if (COUNT && q == 0) atomicAdd(&cnt[i], 1u);
     }
 }
 
 template <typename T, int MSG>
 __global__ __launch_bounds__(kBlock) void k_coo_max(const T *__restrict__ x, int64_t F, const int64_t *__restrict__ src,
-                                                    const int64_t *__restrict__ dst, const float *__restrict__ w, int64_t E,
-                                                    int lg, unsigned long long *__restrict__ keys) {
+                                                    const int64_t *__restrict__ dst, const float *__restrict__ w,
+                                                    const T *__restrict__ ea, int64_t E, int lg,
+                                                    unsigned long long *__restrict__ keys) {
     const int G = 1 << lg;
     const int64_t per_grid = (int64_t)gridDim.x * (kBlock >> lg);
     const int q = threadIdx.x & (G - 1);
@@ -66,7 +73,7 @@ __global__ __launch_bounds__(kBlock) void k_coo_max(const T *__restrict__ x, int
         const float wk = MSG == 1 ? w[k] : 1.f;
         const unsigned long long low = 0xFFFFFFFFull - static_cast<unsigned long long>(k);
         for (int64_t f = q; f < F; f += G) {
-            const float m = canon_zero(message<T, MSG>(x, F, j, i, f, wk));
+            const float m = canon_zero(message<T, MSG>(x, F, j, i, f, wk, ea, k));
             atomicMax(&keys[i * F + f], (static_cast<unsigned long long>(order_key(m)) << 32) | low);
         }
     }
@@ -101,8 +108,8 @@ __global__ void k_coo_max_decode(const unsigned long long *__restrict__ keys, in
 }
 
 template <typename T, int MSG>
-int coo_typed(const T *x, int64_t N, int64_t F, const int64_t *ei, int64_t E, const float *w, int aggr, T *out,
-              int64_t *argmax, float *acc_ws, unsigned *cnt_ws, unsigned long long *keys_ws, hipStream_t s) {
+int coo_typed(const T *x, int64_t N, int64_t F, const int64_t *ei, int64_t E, const float *w, const T *ea, int aggr,
+              T *out, int64_t *argmax, float *acc_ws, unsigned *cnt_ws, unsigned long long *keys_ws, hipStream_t s) {
     int lg = 0;
     while ((1 << lg) < F && lg < 6) ++lg;
     const unsigned grid = grid_for(E, kBlock >> lg, 1 << 18);
@@ -110,7 +117,7 @@ int coo_typed(const T *x, int64_t N, int64_t F, const int64_t *ei, int64_t E, co
     if (aggr == PYG_MAX) {
         PYG_TRY(fill<unsigned long long>(keys_ws, NF, 0ull, s));
         if (E > 0) {
-            k_coo_max<T, MSG><<<grid, kBlock, 0, s>>>(x, F, ei, ei + E, w, E, lg, keys_ws);
+            k_coo_max<T, MSG><<<grid, kBlock, 0, s>>>(x, F, ei, ei + E, w, ea, E, lg, keys_ws);
             PYG_LAUNCH_CHECK();
         }
         k_coo_max_decode<T><<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(keys_ws, NF, E, out, argmax);
@@ -123,8 +130,8 @@ int coo_typed(const T *x, int64_t N, int64_t F, const int64_t *ei, int64_t E, co
     PYG_TRY(fill<float>(acc, NF, 0.f, s));
     if (cnt) PYG_TRY(fill<unsigned>(cnt, N, 0u, s));
     if (E > 0) {
-        if (cnt) k_coo_add<T, MSG, true><<<grid, kBlock, 0, s>>>(x, F, ei, ei + E, w, E, lg, acc, cnt);
-        else k_coo_add<T, MSG, false><<<grid, kBlock, 0, s>>>(x, F, ei, ei + E, w, E, lg, acc, nullptr);
+        if (cnt) k_coo_add<T, MSG, true><<<grid, kBlock, 0, s>>>(x, F, ei, ei + E, w, ea, E, lg, acc, cnt);
+        else k_coo_add<T, MSG, false><<<grid, kBlock, 0, s>>>(x, F, ei, ei + E, w, ea, E, lg, acc, nullptr);
         PYG_LAUNCH_CHECK();
     }
     if (!direct) {
@@ -135,11 +142,17 @@ int coo_typed(const T *x, int64_t N, int64_t F, const int64_t *ei, int64_t E, co
 }
 
 template <typename T>
-int coo_msg(const T *x, int64_t N, int64_t F, const int64_t *ei, int64_t E, const float *w, int msg, int aggr, T *out,
-            int64_t *argmax, float *acc_ws, unsigned *cnt_ws, unsigned long long *keys_ws, hipStream_t s) {
-    if (msg == PYG_MSG_DIFF) return coo_typed<T, 2>(x, N, F, ei, E, w, aggr, out, argmax, acc_ws, cnt_ws, keys_ws, s);
-    if (w) return coo_typed<T, 1>(x, N, F, ei, E, w, aggr, out, argmax, acc_ws, cnt_ws, keys_ws, s);
-    return coo_typed<T, 0>(x, N, F, ei, E, w, aggr, out, argmax, acc_ws, cnt_ws, keys_ws, s);
+int coo_msg(const T *x, int64_t N, int64_t F, const int64_t *ei, int64_t E, const float *w, const T *ea, int msg,
+            int aggr, T *out, int64_t *argmax, float *acc_ws, unsigned *cnt_ws, unsigned long long *keys_ws,
+            hipStream_t s) {
+#define PYG_COO_CASE(K) return coo_typed<T, K>(x, N, F, ei, E, w, ea, aggr, out, argmax, acc_ws, cnt_ws, keys_ws, s)
+    if (msg == PYG_MSG_DIFF) PYG_COO_CASE(2);
+    if (msg == PYG_MSG_EDGE_ADD) PYG_COO_CASE(4);
+    if (msg == PYG_MSG_EDGE_RELU) PYG_COO_CASE(5);
+    if (msg == PYG_MSG_EDGE_MUL) PYG_COO_CASE(6);
+    if (w) PYG_COO_CASE(1);
+    PYG_COO_CASE(0);
+#undef PYG_COO_CASE
 }
 
 }  // namespace
@@ -165,14 +178,14 @@ static CooWs carve_coo(void *base, int dtype, int64_t N, int64_t F, int aggr) {
 size_t coo_workspace(int dtype, int64_t N, int64_t F, int aggr) { return carve_coo(nullptr, dtype, N, F, aggr).bytes; }
 
 int coo_propagate(const void *x, int dtype, int64_t N, int64_t F, const int64_t *ei, int64_t E, const float *w, int msg,
-                  int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, hipStream_t s) {
+                  int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, hipStream_t s, const void *ea) {
     const CooWs cw = carve_coo(ws, dtype, N, F, aggr);
     if (ws_bytes < cw.bytes || (cw.bytes > 256 && !ws)) return PYG_ERR_WORKSPACE;
     if (dtype == PYG_BF16)
-        return coo_msg<uint16_t>(static_cast<const uint16_t *>(x), N, F, ei, E, w, msg, aggr, static_cast<uint16_t *>(out),
-                                 argmax, cw.acc, cw.cnt, cw.keys, s);
-    return coo_msg<float>(static_cast<const float *>(x), N, F, ei, E, w, msg, aggr, static_cast<float *>(out), argmax,
-                          cw.acc, cw.cnt, cw.keys, s);
+        return coo_msg<uint16_t>(static_cast<const uint16_t *>(x), N, F, ei, E, w, static_cast<const uint16_t *>(ea),
+                                 msg, aggr, static_cast<uint16_t *>(out), argmax, cw.acc, cw.cnt, cw.keys, s);
+    return coo_msg<float>(static_cast<const float *>(x), N, F, ei, E, w, static_cast<const float *>(ea), msg, aggr,
+                          static_cast<float *>(out), argmax, cw.acc, cw.cnt, cw.keys, s);
 }
 
 }  // namespace pyg

@@ -42,6 +42,8 @@ struct SegParams {
     const int32_t *col;
     const float *w;
     const float *alpha;  // per-head weights [E, H] in slot order (kMsgHeads)
+    const void *ea;           // edge features [E, F] in x's dtype (edge messages)
+    const int64_t *ea_perm;   // non-NULL: ea is in COO order, row perm[slot]
     int64_t H;
     int64_t C;           // columns per head: feature f belongs to head f / C
     const int64_t *perm;
@@ -139,6 +141,15 @@ constexpr int kClasses = 256;
 
 constexpr int kFull = 0, kPartial = 1;
 constexpr int kMsgSrc = 0, kMsgWeighted = 1, kMsgDiff = 2, kMsgHeads = 3;
+constexpr int kMsgEdgeAdd = 4, kMsgEdgeRelu = 5, kMsgEdgeMul = 6;  // x_j + e, max(x_j + e, 0), x_j * e
+
+// Edge-feature message of one element (formed in fp32, as compared by max).
+template <int MSG>
+__device__ __forceinline__ float edge_msg(float xv, float ev) {
+    if constexpr (MSG == kMsgEdgeAdd) return xv + ev;
+    else if constexpr (MSG == kMsgEdgeRelu) return (xv + ev) > 0.f ? (xv + ev) : 0.f;
+    else return xv * ev;
+}
 
 // Reduce slots [s, t) of row r; write the row (kFull) or a partial (kPartial).
 template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT>
@@ -219,6 +230,21 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                     for (int sl = 0; sl < NS; ++sl)
                         wh[u][sl] = (ok[u] && act[sl]) ? p.alpha[(base + st + u * S + sg) * p.H + hd[sl]] : 0.f;
             }
+            constexpr bool EDGE = MSG >= kMsgEdgeAdd;
+            R ev[U][NS];
+            if constexpr (EDGE) {  // edge rows stream once: non-temporal
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int sl = 0; sl < NS; ++sl) {
+                        const int64_t slot = base + st + u * S + sg;
+                        ev[u][sl] = LN::zero();
+                        if (ok[u] && act[sl]) {
+                            const int64_t er = p.ea_perm ? p.ea_perm[slot] : slot;
+                            ev[u][sl] = LN::load_nt(static_cast<const T *>(p.ea) + er * p.F + f0[sl]);
+                        }
+                    }
+            }
             R v[U][NS];
 #pragma unroll
             for (int u = 0; u < U; ++u)
@@ -243,6 +269,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                             float m;
                             if constexpr (MSG == kMsgDiff) m = xv - LN::get(xi[sl], e);
                             else if constexpr (MSG == kMsgWeighted) m = ww[u] * xv;
+                            else if constexpr (EDGE) m = edge_msg<MSG>(xv, LN::get(ev[u][sl], e));
                             else m = xv;
                             m = canon_zero(m);
                             if (pos[sl][e] < 0 || m > acc[sl][e]) {
@@ -253,6 +280,8 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                             if constexpr (MSG == kMsgDiff) acc[sl][e] += xv - LN::get(xi[sl], e);
                             else if constexpr (MSG == kMsgWeighted) acc[sl][e] = fmaf(ww[u], xv, acc[sl][e]);
                             else if constexpr (MSG == kMsgHeads) acc[sl][e] = fmaf(wh[u][sl], xv, acc[sl][e]);
+                            else if constexpr (MSG == kMsgEdgeMul) acc[sl][e] = fmaf(xv, LN::get(ev[u][sl], e), acc[sl][e]);
+                            else if constexpr (EDGE) acc[sl][e] += edge_msg<MSG>(xv, LN::get(ev[u][sl], e));
                             else acc[sl][e] += xv;
                         }
                     }
@@ -349,6 +378,18 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
             if constexpr (MSG == kMsgWeighted) ww[u] = ok[u] ? p.w[base + u] : 0.f;
             if constexpr (MSG == kMsgHeads) ww[u] = (ok[u] && act) ? p.alpha[(base + u) * p.H + hd] : 0.f;
         }
+        constexpr bool EDGE = MSG >= kMsgEdgeAdd;
+        R ev[U];
+        if constexpr (EDGE) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                ev[u] = LN::zero();
+                if (ok[u] && act) {
+                    const int64_t er = p.ea_perm ? p.ea_perm[base + u] : base + u;
+                    ev[u] = LN::load_nt(static_cast<const T *>(p.ea) + er * p.F + f0);
+                }
+            }
+        }
         R v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) v[u] = (ok[u] && act) ? LN::load(x + (int64_t)jj[u] * p.F + f0) : LN::zero();
@@ -362,6 +403,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
                     float m;
                     if constexpr (MSG == kMsgDiff) m = xv - LN::get(xi, e);
                     else if constexpr (MSG == kMsgWeighted) m = ww[u] * xv;
+                    else if constexpr (EDGE) m = edge_msg<MSG>(xv, LN::get(ev[u], e));
                     else m = xv;
                     m = canon_zero(m);
                     if (pos[e] < 0 || m > acc[e]) {
@@ -371,6 +413,8 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
                 } else {
                     if constexpr (MSG == kMsgDiff) acc[e] += xv - LN::get(xi, e);
                     else if constexpr (MSG == kMsgWeighted || MSG == kMsgHeads) acc[e] = fmaf(ww[u], xv, acc[e]);
+                    else if constexpr (MSG == kMsgEdgeMul) acc[e] = fmaf(xv, LN::get(ev[u], e), acc[e]);
+                    else if constexpr (EDGE) acc[e] += edge_msg<MSG>(xv, LN::get(ev[u], e));
                     else acc[e] += xv;
                 }
             }
@@ -606,6 +650,9 @@ int launch_msg(const SegParams &p, int msg, bool ident, int ns, bool light, hipS
     if constexpr (!MAXA) {
         if (msg == kMsgHeads) return launch_ns<T, VEC, kMsgHeads, false, false>(p, ns, light, s);
     }
+    if (msg == kMsgEdgeAdd) return launch_ns<T, VEC, kMsgEdgeAdd, MAXA, false>(p, ns, light, s);
+    if (msg == kMsgEdgeRelu) return launch_ns<T, VEC, kMsgEdgeRelu, MAXA, false>(p, ns, light, s);
+    if (msg == kMsgEdgeMul) return launch_ns<T, VEC, kMsgEdgeMul, MAXA, false>(p, ns, light, s);
     if (msg == kMsgDiff) return launch_ns<T, VEC, kMsgDiff, MAXA, false>(p, ns, light, s);
     if (msg == kMsgWeighted) return launch_ns<T, VEC, kMsgWeighted, MAXA, false>(p, ns, light, s);
     return launch_ns<T, VEC, kMsgSrc, MAXA, false>(p, ns, light, s);
@@ -623,13 +670,17 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     const int64_t row_bytes = a.F * (int64_t)sizeof(T);
     const bool vec = row_bytes % 16 == 0 && (reinterpret_cast<uintptr_t>(a.x) % 16) == 0 &&
                      (reinterpret_cast<uintptr_t>(a.out) % 16) == 0 &&
-                     (!a.alpha || (a.C * (int64_t)sizeof(T)) % 16 == 0);
+                     (!a.alpha || (a.C * (int64_t)sizeof(T)) % 16 == 0) &&
+                     (reinterpret_cast<uintptr_t>(a.edge_attr) % 16) == 0;
     const int ep = vec ? 16 / (int)sizeof(T) : 1;
     const int64_t nvec = a.F / ep;  // lane vectors per row
     int lg = 0;
     while ((1 << lg) < nvec && lg < 6) ++lg;
     p.lg_l = lg;
-    const int mk = a.alpha ? kMsgHeads : (a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc));
+    int mk = a.alpha ? kMsgHeads : (a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc));
+    if (a.msg == PYG_MSG_EDGE_ADD) mk = kMsgEdgeAdd;
+    if (a.msg == PYG_MSG_EDGE_RELU) mk = kMsgEdgeRelu;
+    if (a.msg == PYG_MSG_EDGE_MUL) mk = kMsgEdgeMul;
     const bool ident = a.col == nullptr;
     // cache hint: only when the source rows do not fit in L2 (row in-degree as the hotness proxy)
     p.hot_class = nullptr;
@@ -717,6 +768,8 @@ int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t 
     p.col = a.col;
     p.w = a.weight;
     p.alpha = a.alpha;
+    p.ea = a.edge_attr;
+    p.ea_perm = a.attr_perm;
     p.H = a.H;
     p.C = a.C;
     p.perm = a.perm;

@@ -206,3 +206,29 @@ def test_dense_transform_rejects_bad_arguments(lib):
     assert dt(X, 1, 2**31, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == UNSUPPORTED
     rc, b = _ws(lib.pyg_dense_transform_workspace, 602, 41)
     assert rc == PYG_OK and b >= 48 * 608 * 2
+
+
+def test_propagate_edge_rejects_bad_arguments(lib):
+    from paper_1903_02428_amd.binding import _Csr
+    EA, OUT = ctypes.c_void_p(0x500000), ctypes.c_void_p(0x900000)
+    good = _Csr(0x30000, 0x40000, 0x50000, None, 10, 20, 0)
+    no_perm = _Csr(0x30000, 0x40000, None, None, 10, 20, 0)
+
+    def pe(x=FAKE, dtype=0, N=10, F=4, ei=FAKE, E=20, ea=EA, order=1, csr=None, msg=2, aggr=0, kernel=1, out=OUT,
+           argmax=None, ws=FAKE, ws_bytes=1 << 40):
+        return lib.pyg_propagate_edge(x, dtype, N, F, ei, E, ea, order, csr, msg, aggr, kernel, out, argmax, ws,
+                                      ws_bytes, None)
+    assert pe(msg=0) == INVALID                          # plain messages go through pyg_propagate
+    assert pe(msg=1) == INVALID
+    assert pe(msg=5) == INVALID
+    assert pe(order=3) == INVALID
+    assert pe(ea=None) == INVALID                        # edge messages need the features
+    assert pe(order=0) == INVALID                        # the COO kernel reads edges in COO order
+    assert pe(aggr=2) == INVALID                         # max needs argmax
+    assert pe(ei=None) == INVALID                        # COO kernel needs edges
+    assert pe(kernel=2, csr=ctypes.byref(no_perm), order=1) == INVALID  # COO-ordered features need perm
+    assert pe(kernel=2, csr=None) == INVALID
+    assert pe(out=ctypes.c_void_p(0x500000 + 64)) == INVALID  # out overlaps the edge features
+    assert pe(N=2**31) == UNSUPPORTED
+    assert pe(kernel=2, csr=ctypes.byref(good), order=0, ws_bytes=0) == WORKSPACE
+    assert pe(ws_bytes=0, aggr=1) == WORKSPACE
