@@ -81,6 +81,8 @@ def parse():
                     help="time only the attention calls (GAT softmax, attention sum) on the large graph")
     ap.add_argument("--gcn-layer-only", action="store_true",
                     help="time only the GCN layer (matrix-core X Theta, then propagate) on the large graph")
+    ap.add_argument("--edge-features-only", action="store_true",
+                    help="time only the edge-feature propagate (max(x_j + e, 0), F-dimensional e) on the large graph")
     ap.add_argument("--fig2-features", type=int, default=64)
     ap.add_argument("--fig2-runs", type=int, default=1000)
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -171,6 +173,12 @@ def main():
                           "gcn_layer": gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)}), flush=True)
         return
 
+    if args.edge_features_only:
+        pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
+        print(json.dumps({"workload": "large power-law graph, edge-feature messages", "N": N, "E": E, "F": F,
+                          "edge_features": edge_features(pyg, torch, x, ei, csr, N, E, F, dev)}), flush=True)
+        return
+
     names = ["degree", "coo_to_csr", "gcn_norm", "propagate", "global_pool"]
     ev = {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
     times = {n: [] for n in names}
@@ -253,6 +261,7 @@ def main():
         result["detail"]["variants"] = variants(pyg, torch, x, ei, csr_w, N, E, F, dev)
         result["detail"]["attention"] = attention(pyg, torch, x, csr, N, E, F, dev)
         result["detail"]["gcn_layer"] = gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)
+        result["detail"]["edge_features"] = edge_features(pyg, torch, x, ei, csr, N, E, F, dev)
     if not (args.no_detail and args.no_cpu_baseline):
         import oracle
         w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)  # the oracle's own weights
@@ -419,6 +428,34 @@ def gcn_layer(pyg, torch, x, csr_w, N, E, F, dev, Fo=128):
                                 "bytes": bytes_d},
             "propagate_bf16": {"ms": t_p, "alg_GBps": b_alg_csr(N, E, Fo, 2) / (t_p * 1e-3) / 1e9},
             "layer": {"ms": t_l, "edges_features_per_s": E * Fo / (t_l * 1e-3)}}
+
+
+def edge_features(pyg, torch, x, ei, csr, N, E, F, dev):
+    """Propagate with an F-dimensional feature on every edge (GINE-style
+    max(x_j + e, 0), sum): the CSR kernel with the features in CSR slot
+    order (streamed once, coalesced) and the COO atomic kernel with them in
+    COO order. Algorithmic bytes: the plain propagate's plus E*F*s."""
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(13)
+    res = {"msg": "max(x_j + e, 0)", "aggr": "sum"}
+    for dtname, dt, sz in (("f32", torch.float32, 4), ("bf16", torch.bfloat16, 2)):
+        xx = x.to(dt)
+        ea = torch.randn(E, F, device=dev, generator=gen).to(dt)
+        o = torch.empty_like(xx)
+        kernels = (("csr", "csr"), ("coo", "coo")) if dt == torch.float32 else (("csr", "csr"),)
+        for kernel, order in kernels:
+            ws = torch.empty(pyg.propagate_workspace_bytes(xx, E, "sum", kernel, csr.chunk), dtype=torch.uint8,
+                             device=dev)
+            ms = timed(torch, lambda: pyg.propagate_edge(xx, ea, ei, csr if kernel == "csr" else None, "edge_relu",
+                                                         "sum", kernel, order, out=o, workspace=ws), reps=5)
+            b = (b_alg_csr(N, E, F, sz, weighted=False) if kernel == "csr" else b_alg_coo(N, E, F, sz, weighted=False))
+            b += E * F * sz
+            res[f"{kernel}-{dtname}"] = {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9,
+                                         "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "bytes": b,
+                                         "edges_features_per_s": E * F / (ms * 1e-3)}
+        del ea
+        torch.cuda.empty_cache()
+    return res
 
 
 def sampled_parity(x_np, ei_np, w_ref, out, N, rows=200):
