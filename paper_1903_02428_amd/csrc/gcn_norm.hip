@@ -90,9 +90,25 @@ __global__ __launch_bounds__(kBlock) void k_csr_edge_norm(const int64_t *__restr
         const int64_t s = uniform64(rowptr[r]), t = uniform64(rowptr[r + 1]);
         const int64_t a = s > e0 ? s : e0, b = t < e1 ? t : e1;
         const double di = dinv[r];
-        for (int64_t p = a + lane; p < b; p += kWave) {
-            const double wp = w ? static_cast<double>(w[p]) : 1.0;
-            norm[p] = static_cast<float>(dinv[col[p]] * wp * di);
+        // U independent column loads, then U dinv gathers, per lane and batch
+        constexpr int U = 8;
+        for (int64_t p0 = a + lane; p0 < b; p0 += (int64_t)kWave * U) {
+            int32_t cj[U];
+            float wv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t p = p0 + (int64_t)u * kWave;
+                cj[u] = p < b ? col[p] : 0;
+                wv[u] = (w && p < b) ? w[p] : 1.f;
+            }
+            double dj[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) dj[u] = p0 + (int64_t)u * kWave < b ? dinv[cj[u]] : 0.0;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int64_t p = p0 + (int64_t)u * kWave;
+                if (p < b) norm[p] = static_cast<float>(dj[u] * static_cast<double>(wv[u]) * di);
+            }
         }
         if (t >= e1) break;
         ++r;

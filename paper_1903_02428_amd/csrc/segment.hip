@@ -511,10 +511,10 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
 // ordered ranges of pieces with 8 loads in flight, then wave 0 combines the
 // four results in wave order: a fixed order, so the fold is deterministic,
 // and for max the earliest piece wins ties.
-template <typename T, bool MAXA>
-__global__ __launch_bounds__(kBlock) void k_segment_fixup(SegParams p) {
-    constexpr int kW = kBlock / kWave;
-    constexpr int kU = 8;
+template <typename T, bool MAXA, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void k_segment_fixup(SegParams p) {
+    constexpr int kW = WAVES;
+    constexpr int kU = WAVES > 4 ? 16 : 8;
     __shared__ float sv[kW][kWave];
     __shared__ int32_t sp[kW][kWave];
     const int64_t c = blockIdx.x;
@@ -631,7 +631,11 @@ int launch_window(const SegParams &p, bool light, hipStream_t s) {
     }
     PYG_LAUNCH_CHECK();
     if (p.nchunks > 1) {
-        k_segment_fixup<T, MAXA><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
+        // few, very long rows (e.g. whole-graph pooling): 16 waves fold each row
+        if (p.E > 16 * p.chunk * (p.n_rows > 0 ? p.n_rows : 1))
+            k_segment_fixup<T, MAXA, 16><<<static_cast<unsigned>(p.nchunks), 16 * kWave, 0, s>>>(p);
+        else
+            k_segment_fixup<T, MAXA, 4><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
         PYG_LAUNCH_CHECK();
     }
     return PYG_OK;
