@@ -465,19 +465,26 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter64(
 }
 
 // rowptr from the sorted target ids: slot p starts every row in (key[p-1], key[p]]
-// (key[-1] = -1, key[E] = N). Each thread owns 4 consecutive slots.
+// (key[-1] = -1, key[E] = N; slot E closes the trailing rows, rowptr[N] = E).
+// Each thread owns 8 consecutive slots, read as two 16-byte loads.
 __global__ void k_row_bounds(const uint32_t *__restrict__ key, int64_t E, int64_t N, int64_t *__restrict__ rowptr) {
-    const int64_t p0 = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * 4;
+    constexpr int S = 8;  // slots per thread: two 16-byte loads
+    const int64_t p0 = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * S;
     if (p0 > E) return;
-    int64_t k[5];
+    int64_t k[S + 1];
+    k[0] = p0 == 0 ? -1 : static_cast<int64_t>(key[p0 - 1]);
+    if (p0 + S <= E) {
+        const uint4 a = *reinterpret_cast<const uint4 *>(key + p0);
+        const uint4 b = *reinterpret_cast<const uint4 *>(key + p0 + 4);
+        k[1] = a.x, k[2] = a.y, k[3] = a.z, k[4] = a.w, k[5] = b.x, k[6] = b.y, k[7] = b.z, k[8] = b.w;
+    } else {
 #pragma unroll
-    for (int i = 0; i < 5; ++i) {
-        const int64_t p = p0 - 1 + i;
-        int64_t v = p < 0 ? -1 : (p < E ? static_cast<int64_t>(key[p]) : N);
-        k[i] = v > N ? N : v;
+        for (int i = 0; i < S; ++i) k[i + 1] = p0 + i < E ? static_cast<int64_t>(key[p0 + i]) : N;
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i <= S; ++i) k[i] = k[i] > N ? N : k[i];
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
         const int64_t p = p0 + i;
         if (p > E) break;
         for (int64_t r = k[i] + 1; r <= k[i + 1]; ++r) rowptr[r] = p;
@@ -646,7 +653,7 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
             pin_w = pout_w;
             shift += bits;
         }
-        k_row_bounds<<<grid_for(E + 1, kBlock * 4, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
+        k_row_bounds<<<grid_for(E + 1, kBlock * 8, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
         PYG_LAUNCH_CHECK();
         return PYG_OK;
     }
@@ -669,7 +676,7 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
         in = out;
         shift += bits;
     }
-    k_row_bounds<<<grid_for(E + 1, kBlock * 4, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
+    k_row_bounds<<<grid_for(E + 1, kBlock * 8, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
     PYG_LAUNCH_CHECK();
     return PYG_OK;
 }
