@@ -131,3 +131,59 @@ def test_c5_attention_sampled(pyg, c5, dev_graph):
     g = out[to_dev(rows)].cpu().numpy().astype(np.float64)
     assert np.all(np.abs(g - ref_out[rows]) <= 2e-5 * sabs[rows] + 1e-6), "C5 propagate_heads"
     print("[c5] attention ok", flush=True)
+
+
+def test_c5_edge_features_sampled(pyg, c5, dev_graph):
+    """Edge-feature messages at the benchmark's shape: every edge of the large
+    graph carries a 128-dimensional feature (counter-based, regenerable for
+    any subset of edges); max(x_j + e, 0) with sum (the benchmark's call, fp32
+    and bf16, features in CSR slot order) plus the other two messages with
+    mean and max (features in COO order), checked on sampled target rows."""
+    from synth.hashed import hashed_matrix, hashed_values
+    ei_np, x_np, N = c5["edge_index_gcn"], c5["x"], c5["N"]
+    ei, _, csr = dev_graph
+    E, F = ei_np.shape[1], x_np.shape[1]
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E)
+    ea = hashed_matrix(E, F, seed=17, device="cuda")
+    ea_csr = ea[csr.perm]  # rows in CSR slot order, as the benchmark passes them
+    rows, keep = sample_rows(c5, n=300)
+    sub = np.ascontiguousarray(ei_np[:, keep])
+    kidx = np.nonzero(keep)[0]
+    ea_sub = hashed_values(torch.from_numpy(kidx), F, seed=17).numpy()
+    x32 = to_dev(x_np)
+    cases = [("edge_relu", "sum", torch.float32, "csr"), ("edge_relu", "sum", torch.bfloat16, "csr"),
+             ("edge_add", "mean", torch.float32, "coo"), ("edge_mul", "max", torch.float32, "coo")]
+    for msg, aggr, dt, order in cases:
+        feats = (ea_csr if order == "csr" else ea).to(dt)
+        out, arg = pyg.propagate_edge(x32.to(dt), feats, ei, plain, msg, aggr, "csr", order)
+        torch.cuda.synchronize()
+        bf = dt == torch.bfloat16
+        xin = bf16_round(x_np) if bf else x_np
+        ein = bf16_round(ea_sub) if bf else ea_sub
+        ref, rarg, sabs = oracle.propagate(xin, sub, msg=msg, aggr=aggr, edge_attr=ein)
+        what = f"C5 edge {msg} {aggr} {dt} {order}"
+        got = out[to_dev(rows)]
+        if aggr == "max":
+            rarg_full = np.where(rarg[rows] < sub.shape[1], kidx[np.minimum(rarg[rows], sub.shape[1] - 1)], E)
+            check_max(got, arg[to_dev(rows)], ref[rows], rarg_full, what=what)
+        else:
+            check_sum(got, ref[rows], sabs[rows], bf, what)
+        print(f"[c5] {what} ok", flush=True)
+        del feats
+    del ea, ea_csr
+    torch.cuda.empty_cache()
+
+
+def test_c5_dense_transform_sampled(pyg, c5):
+    """The matrix-core X Theta at the benchmark's shape (N=232,965, 128 -> 128,
+    bf16 operands, bf16 and fp32 out), sampled rows against the oracle."""
+    x_np = c5["x"]
+    rng = np.random.default_rng(79)
+    xb = bf16_round(x_np)
+    t = bf16_round((rng.standard_normal((128, 128)) / np.sqrt(128)).astype(np.float32))
+    rows = np.sort(rng.choice(x_np.shape[0], 2000, replace=False))
+    ref, sabs = oracle.dense_transform(xb[rows], t)
+    for odt in (torch.bfloat16, torch.float32):
+        out = pyg.dense_transform(to_dev(xb).to(torch.bfloat16), to_dev(t).to(torch.bfloat16), odt)
+        torch.cuda.synchronize()
+        check_sum(out[to_dev(rows)], ref, sabs, odt == torch.bfloat16, f"C5 dense {odt}")

@@ -63,3 +63,29 @@ def test_erdos_renyi_shapes():
         assert np.unique(ei[1] * 1000 + ei[0]).size == 16000
         if coalesced:
             assert (np.diff(ei[1] * 1000 + ei[0]) > 0).all()
+
+
+def test_hashed_values_match_a_plain_python_hash():
+    """The tensor generator equals a plain-integer rendering of its definition
+    on sample counters (including ones above 2^32), and stays in [-1, 1)."""
+    import torch
+
+    from synth.hashed import hashed_values
+
+    def lowbias32(x):
+        x ^= x >> 16
+        x = (x * 0x7FEB352D) & 0xFFFFFFFF
+        x ^= x >> 15
+        x = (x * 0x846CA68B) & 0xFFFFFFFF
+        return x ^ (x >> 16)
+
+    F, seed = 7, 5
+    rows = [0, 1, 12345, 2**29 + 3, 114_832_964]
+    got = hashed_values(torch.tensor(rows), F, seed).numpy()
+    for a, r in enumerate(rows):
+        for f in range(F):
+            c = r * F + f
+            lo, hi = c & 0xFFFFFFFF, (c >> 32) & 0xFFFFFFFF
+            x = lowbias32(lo ^ lowbias32((hi + seed * 0x9E37) & 0xFFFFFFFF))
+            assert got[a, f] == np.float32((x >> 8) * 2.0 ** -23 - 1.0)
+    assert got.min() >= -1.0 and got.max() < 1.0
