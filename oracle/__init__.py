@@ -66,10 +66,12 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_propagate_heads.argtypes = [p, i64, i64, i64, p, i64, p, p, p]
     lib.oracle_propagate_heads_backward.argtypes = [p, i64, i64, i64, p, i64, p, p, p, p, p, p]
     lib.oracle_dense_transform.argtypes = [p, i64, i64, p, i64, p, p]
+    lib.oracle_gat_scores_backward.argtypes = [p, p, i64, i64, p, i64, ctypes.c_float, p, p, p, p, p]
     for fn in (lib.oracle_degree, lib.oracle_coo_to_csr, lib.oracle_gcn_norm,
                lib.oracle_propagate, lib.oracle_global_pool, lib.oracle_propagate_backward,
                lib.oracle_gat_scores, lib.oracle_segment_softmax, lib.oracle_segment_softmax_backward,
-               lib.oracle_propagate_heads, lib.oracle_propagate_heads_backward, lib.oracle_dense_transform):
+               lib.oracle_propagate_heads, lib.oracle_propagate_heads_backward, lib.oracle_dense_transform,
+               lib.oracle_gat_scores_backward):
         fn.restype = ctypes.c_int
     return lib
 
@@ -299,3 +301,24 @@ def dense_transform(x, theta, lib=None):
     sabs = np.empty((N, Fo), np.float64)
     _check(lib.oracle_dense_transform(_ptr(x), N, Fi, _ptr(t), Fo, _ptr(out), _ptr(sabs)), "dense_transform")
     return out, sabs
+
+
+def gat_scores_backward(a_src, a_dst, edge_index, grad_e, slope: float = 0.2, lib=None):
+    """Gradient of gat_scores for dL/d e [E, H]. Returns (grad_a_src fp64 [N, H],
+    grad_a_dst fp64 [N, H], sabs_src, sabs_dst)."""
+    lib = lib or load()
+    a_src = np.ascontiguousarray(a_src, dtype=np.float32)
+    a_dst = np.ascontiguousarray(a_dst, dtype=np.float32)
+    if a_src.ndim != 2 or a_src.shape != a_dst.shape:
+        raise ValueError("a_src and a_dst must both be [N, H]")
+    N, H = a_src.shape
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    g = _scores2d(grad_e, E, "grad_e")
+    if g.shape[1] != H:
+        raise ValueError("grad_e must be [E, H]")
+    gs, gd = np.empty((N, H)), np.empty((N, H))
+    ss, sd = np.empty((N, H)), np.empty((N, H))
+    _check(lib.oracle_gat_scores_backward(_ptr(a_src), _ptr(a_dst), N, H, _ptr(ei), E, ctypes.c_float(slope), _ptr(g),
+                                          _ptr(gs), _ptr(gd), _ptr(ss), _ptr(sd)), "gat_scores_backward")
+    return gs, gd, ss, sd

@@ -532,3 +532,38 @@ int oracle_dense_transform(const float *x, int64_t N, int64_t Fi, const float *t
         }
     return ORACLE_OK;
 }
+
+/* Gradient of oracle_gat_scores for g = dL/d e [E,H] (fp32):
+ *   v = a_src[j,h] + a_dst[i,h],  de/dv = 1 if v >= 0 else slope,
+ *   grad_src[j,h] += g[k,h] de/dv,  grad_dst[i,h] += g[k,h] de/dv   for k = (j -> i).
+ * The branch is taken on the exact sum (its sign equals that of the
+ * correctly rounded fp32 sum). grad_src, grad_dst fp64 [N,H]; sabs_* (nullable)
+ * sum |terms|. */
+int oracle_gat_scores_backward(const float *a_src, const float *a_dst, int64_t N, int64_t H,
+                               const int64_t *edge_index, int64_t E, float slope, const float *g,
+                               double *grad_src, double *grad_dst, double *sabs_src, double *sabs_dst) {
+    if (N < 0 || H < 0 || E < 0) return ORACLE_ERR_ARG;
+    if (N * H > 0 && (!a_src || !a_dst || !grad_src || !grad_dst)) return ORACLE_ERR_ARG;
+    if (E * H > 0 && (!edge_index || !g)) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    if (!all_finite(a_src, N * H) || !all_finite(a_dst, N * H) || !all_finite(g, E * H) || !isfinite(slope))
+        return ORACLE_ERR_NONFINITE;
+    for (int64_t t = 0; t < N * H; ++t) {
+        grad_src[t] = 0.0;
+        grad_dst[t] = 0.0;
+        if (sabs_src) sabs_src[t] = 0.0;
+        if (sabs_dst) sabs_dst[t] = 0.0;
+    }
+    for (int64_t k = 0; k < E; ++k)
+        for (int64_t h = 0; h < H; ++h) {
+            const double v = (double)a_src[src[k] * H + h] + (double)a_dst[dst[k] * H + h];
+            const double gv = (double)g[k * H + h] * (v >= 0.0 ? 1.0 : (double)slope);
+            grad_src[src[k] * H + h] += gv;
+            grad_dst[dst[k] * H + h] += gv;
+            if (sabs_src) sabs_src[src[k] * H + h] += fabs(gv);
+            if (sabs_dst) sabs_dst[dst[k] * H + h] += fabs(gv);
+        }
+    return ORACLE_OK;
+}

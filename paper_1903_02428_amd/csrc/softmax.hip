@@ -38,6 +38,11 @@
 #ifndef PYG_SOFTMAX_REGS_BWD
 #define PYG_SOFTMAX_REGS_BWD 8
 #endif
+// 16-byte blocks per lane and batch of the two-pass path (rows too large for
+// registers, and long-row pieces)
+#ifndef PYG_SOFTMAX_STREAM
+#define PYG_SOFTMAX_STREAM 8
+#endif
 
 namespace pyg {
 namespace {
@@ -420,8 +425,8 @@ __device__ __forceinline__ void vrow(const SmParams &p, int64_t r, int64_t s, in
     const int64_t b0 = lo >> 2, b1 = (hi + 3) >> 2;
     float m[4], d[4];
     if (b1 - b0 > (int64_t)G * R) {  // too large for registers: online pass, then a second read
-        vstate<SRC, 8, VH>(p, r, lo, hi, G, l, m, d);
-        vwrite<SRC, 8, VH>(p, r, lo, hi, G, l, m, d);
+        vstate<SRC, PYG_SOFTMAX_STREAM, VH>(p, r, lo, hi, G, l, m, d);
+        vwrite<SRC, PYG_SOFTMAX_STREAM, VH>(p, r, lo, hi, G, l, m, d);
         return;
     }
     float adst[4];
@@ -517,7 +522,7 @@ __device__ __forceinline__ void do_row(const SmParams &p, int64_t r, int64_t s, 
 
 template <int SRC, int VH>
 __device__ __forceinline__ void do_piece(const SmParams &p, int64_t r, int64_t s, int64_t t, int64_t slot, int lane) {
-    if constexpr (VH > 0) vpiece_state<SRC, 8, VH>(p, r, s, t, slot, lane);
+    if constexpr (VH > 0) vpiece_state<SRC, PYG_SOFTMAX_STREAM, VH>(p, r, s, t, slot, lane);
     else piece_state<SRC>(p, r, s, t, slot, lane);
 }
 
@@ -618,7 +623,7 @@ __global__ __launch_bounds__(kBlock) void k_softmax_long(SmParams p) {
                 m[i] = st.x;
                 d[i] = st.y;
             }
-            vwrite<SRC, 8, VH>(p, r, s * p.H, t * p.H, kWave, lane, m, d);
+            vwrite<SRC, PYG_SOFTMAX_STREAM, VH>(p, r, s * p.H, t * p.H, kWave, lane, m, d);
             continue;
         }
         for (int64_t hb = 0; hb < p.H; hb += (1 << p.lg_h)) {

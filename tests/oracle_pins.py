@@ -625,6 +625,47 @@ def pin_edge_messages_library(lib):
             assert np.array_equal(r[0], a[0])
 
 
+def pin_golden_gat_backward(lib):
+    g = golden()["attention"]
+    ei = np.array(g["edge_index"], np.int64)
+    gs, gd, _, _ = oracle.gat_scores_backward(np.array(g["a_src"]), np.array(g["a_dst"]), ei,
+                                              np.array(g["grad_scores"]), g["slope"], lib=lib)
+    assert np.array_equal(gs, np.array(g["gat_grad_a_src"])) and np.array_equal(gd, np.array(g["gat_grad_a_dst"]))
+
+
+def pin_gat_layer_autograd(lib):
+    """A whole GAT attention layer (scores, softmax, attention sum) in CPU
+    torch fp64 autograd against the oracle's backward chain: attention-sum
+    backward -> softmax backward -> score backward."""
+    for N, H, ei, _, rng in _attention_cases():
+        E = ei.shape[1]
+        C = 3
+        x = rng.standard_normal((N, H * C)).astype(np.float32)
+        a_src = rng.standard_normal((N, H)).astype(np.float32)
+        a_dst = rng.standard_normal((N, H)).astype(np.float32)
+        g = rng.standard_normal((N, H * C)).astype(np.float32)
+        slope = 0.2
+        src, dst = torch.from_numpy(ei[0]), torch.from_numpy(ei[1])
+        xs = torch.tensor(x, dtype=torch.float64, requires_grad=True)
+        at_s = torch.tensor(a_src, dtype=torch.float64, requires_grad=True)
+        at_d = torch.tensor(a_dst, dtype=torch.float64, requires_grad=True)
+        v = at_s[src] + at_d[dst]
+        e = torch.where(v >= 0, v, slope * v)
+        alpha = _torch_softmax(e, dst, N)
+        msg = (alpha[:, :, None] * xs[src].view(E, H, C)).reshape(E, H * C)
+        out = torch.zeros(N, H * C, dtype=torch.float64).index_add(0, dst, msg)
+        out.backward(torch.tensor(g, dtype=torch.float64))
+        # oracle chain in fp64 values rounded to fp32 where the kernels store fp32
+        e_o = oracle.gat_scores(a_src, a_dst, ei, slope, lib=lib)
+        al = oracle.segment_softmax(e_o, ei, N, lib=lib).astype(np.float32)
+        gx, ga, _, sa = oracle.propagate_heads_backward(x, ei, al, g, H, lib=lib)
+        gsc, ss = oracle.segment_softmax_backward(al, ga.astype(np.float32), ei, N, lib=lib)
+        gs, gd, _, _ = oracle.gat_scores_backward(a_src, a_dst, ei, gsc.astype(np.float32), slope, lib=lib)
+        assert np.allclose(gx, xs.grad.numpy(), rtol=1e-5, atol=1e-6)
+        assert np.allclose(gs, at_s.grad.numpy(), rtol=1e-4, atol=1e-5)
+        assert np.allclose(gd, at_d.grad.numpy(), rtol=1e-4, atol=1e-5)
+
+
 ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_golden_gcn_norm_directed,
             pin_golden_signed_zero,
             pin_degree_and_csr_library, pin_sum_mean_dense, pin_torch_scatter, pin_max_bruteforce,
@@ -632,4 +673,4 @@ ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_gold
             pin_backward_autograd, pin_backward_dense, pin_golden_attention, pin_softmax_library,
             pin_softmax_invariants, pin_softmax_backward_autograd, pin_heads_dense, pin_uniform_attention_is_mean,
             pin_golden_dense_transform, pin_dense_transform_library, pin_golden_edge_messages,
-            pin_edge_messages_library]
+            pin_edge_messages_library, pin_golden_gat_backward, pin_gat_layer_autograd]

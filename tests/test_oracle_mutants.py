@@ -54,8 +54,8 @@ MUTANTS = [
     ("softmax_not_normalised", "alpha[k * H + h] = exp(s[k * H + h] - m[dst[k] * H + h]) / den[dst[k] * H + h];",
      "alpha[k * H + h] = exp(s[k * H + h] - m[dst[k] * H + h]);"),
     ("gat_slope_on_positive", "e[k * H + h] = v >= 0.0 ? v : (double)slope * v;", "e[k * H + h] = v >= 0.0 ? (double)slope * v : v;"),
-    ("gat_scores_swap_ends", "(double)a_src[src[k] * H + h] + (double)a_dst[dst[k] * H + h]",
-     "(double)a_src[dst[k] * H + h] + (double)a_dst[src[k] * H + h]"),
+    ("gat_scores_swap_ends", "(double)a_src[src[k] * H + h] + (double)a_dst[dst[k] * H + h];\n            e[k * H + h]",
+     "(double)a_src[dst[k] * H + h] + (double)a_dst[src[k] * H + h];\n            e[k * H + h]"),
     ("softmax_bwd_sign", "grad_s[k * H + h] = a * ((double)g[k * H + h] - t[dst[k] * H + h]);",
      "grad_s[k * H + h] = a * ((double)g[k * H + h] + t[dst[k] * H + h]);"),
     ("softmax_bwd_t_without_alpha", "const double ag = (double)alpha[k * H + h] * (double)g[k * H + h];",
@@ -74,6 +74,9 @@ MUTANTS = [
      "else if (msg == ORACLE_MSG_EDGE_RELU) m = (double)xj + (double)ea[k * F + f];"),
     ("edge_max_relu_keeps_negative", "else if (msg == ORACLE_MSG_EDGE_RELU) m = xj + ea[k * F + f] > 0.0f ? xj + ea[k * F + f] : 0.0f;",
      "else if (msg == ORACLE_MSG_EDGE_RELU) m = xj + ea[k * F + f];"),
+    ("gat_bwd_slope_on_positive", "const double gv = (double)g[k * H + h] * (v >= 0.0 ? 1.0 : (double)slope);",
+     "const double gv = (double)g[k * H + h] * (v >= 0.0 ? (double)slope : 1.0);"),
+    ("gat_bwd_dst_to_src", "            grad_dst[dst[k] * H + h] += gv;", "            grad_dst[src[k] * H + h] += gv;"),
     ("transform_skips_last_k", "for (int64_t k = 0; k < Fi; ++k) {\n                const double t",
      "for (int64_t k = 0; k + 1 < Fi; ++k) {\n                const double t"),
 ]
