@@ -303,6 +303,37 @@ int pyg_propagate_heads_workspace(int dtype, int64_t N, int64_t H, int64_t C, in
 int pyg_propagate_heads(const void *x, int dtype, int64_t N, int64_t H, int64_t C, const pyg_csr *csr,
                         const float *alpha, void *out, void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes needed by pyg_propagate_heads_backward (pass csr_t->chunk). */
+int pyg_propagate_heads_backward_workspace(int dtype, int64_t N, int64_t H, int64_t C, int64_t E, int64_t chunk_t,
+                                           size_t *bytes);
+
+/* Gradient of pyg_propagate_heads for g = dL/d out [N, H*C]:
+ *   grad_x[j, h*C + c]  = sum over edges k = (j -> i) of alpha[k,h] * g[i, h*C + c]
+ *                         (the attention sum over the reversed graph; csr_t is
+ *                         the CSR of the reversed edge list, built like csr);
+ *   grad_alpha[p, h]    = sum_c g[row(p), h*C + c] * x[col[p], h*C + c], CSR
+ *                         slot order of csr (the order of alpha).
+ * grad_out, x, grad_x in dtype (fp32 accumulation); alpha, grad_alpha fp32
+ * [E, H]. Either output may be NULL (not both); x is needed for grad_alpha.
+ * Deterministic. */
+int pyg_propagate_heads_backward(const void *grad_out, const void *x, int dtype, int64_t N, int64_t H, int64_t C,
+                                 const pyg_csr *csr, const pyg_csr *csr_t, const float *alpha, void *grad_x,
+                                 float *grad_alpha, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_gat_scores_backward (pass csr_t->chunk). */
+int pyg_gat_scores_backward_workspace(int64_t N, int64_t H, int64_t E, int64_t chunk_t, size_t *bytes);
+
+/* Gradient of GAT's edge scores e = LeakyReLU(a_src[j] + a_dst[i]) for
+ * g = dL/d e (fp32 [E, H], CSR slot order of csr, e.g. from
+ * pyg_segment_softmax_backward with PYG_ORDER_CSR):
+ *   dL/dv = g * (a_src[j,h] + a_dst[i,h] >= 0 ? 1 : negative_slope),
+ *   grad_a_dst[i, h] = sum of dL/dv over the incoming edges of i,
+ *   grad_a_src[j, h] = sum of dL/dv over the outgoing edges of j (rows of csr_t).
+ * a_src, a_dst, grad_a_src, grad_a_dst fp32 [N, H]. Deterministic. */
+int pyg_gat_scores_backward(const float *a_src, const float *a_dst, int64_t H, float negative_slope,
+                            const pyg_csr *csr, const pyg_csr *csr_t, const float *grad_scores, float *grad_a_src,
+                            float *grad_a_dst, void *ws, size_t ws_bytes, void *stream);
+
 /* ---- Dense feature transform of a GCN layer (Section 2 lists GCN; its
  * layer multiplies the features by a weight matrix around the normalised
  * aggregation, A (X Theta) = (A X) Theta). */

@@ -22,6 +22,7 @@ from .binding import (  # noqa: F401
     coo_to_csr,
     degree,
     dense_transform,
+    gat_scores_backward,
     gat_softmax,
     gather_edges,
     gcn_norm,
@@ -33,6 +34,7 @@ from .binding import (  # noqa: F401
     propagate_backward,
     propagate_edge,
     propagate_heads,
+    propagate_heads_backward,
     propagate_workspace_bytes,
     reverse_edges,
     segment_softmax,

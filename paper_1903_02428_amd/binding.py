@@ -25,6 +25,8 @@ EXPORTED = [
     "pyg_propagate_backward",
     "pyg_segment_softmax_workspace", "pyg_segment_softmax", "pyg_gat_softmax", "pyg_segment_softmax_backward",
     "pyg_propagate_heads_workspace", "pyg_propagate_heads", "pyg_dense_transform_workspace", "pyg_dense_transform",
+    "pyg_propagate_heads_backward_workspace", "pyg_propagate_heads_backward", "pyg_gat_scores_backward_workspace",
+    "pyg_gat_scores_backward",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
 ]
 
@@ -88,6 +90,12 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_heads_workspace": [i32, i64, i64, i64, i64, i64, sz],
             "pyg_propagate_heads": [p, i32, i64, i64, i64, ctypes.POINTER(_Csr), p, p, p, ctypes.c_size_t, p],
             "pyg_dense_transform_workspace": [i64, i64, sz],
+            "pyg_propagate_heads_backward_workspace": [i32, i64, i64, i64, i64, i64, sz],
+            "pyg_propagate_heads_backward": [p, p, i32, i64, i64, i64, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), p, p,
+                                             p, p, ctypes.c_size_t, p],
+            "pyg_gat_scores_backward_workspace": [i64, i64, i64, i64, sz],
+            "pyg_gat_scores_backward": [p, p, i64, ctypes.c_float, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), p, p, p,
+                                        p, ctypes.c_size_t, p],
             "pyg_dense_transform": [p, i32, i64, i64, p, i64, p, i32, p, ctypes.c_size_t, p],
             "pyg_global_pool_workspace": [i32, i64, i64, i64, i32, sz],
             "pyg_global_pool": [p, i32, i64, i64, p, i64, i32, p, p, p, ctypes.c_size_t, p],
@@ -481,6 +489,56 @@ def propagate_heads(x: torch.Tensor, csr: CSR, alpha: torch.Tensor, heads: int, 
     _check(lib.pyg_propagate_heads(_ptr(x), DTYPE[x.dtype], N, heads, C, ctypes.byref(c), _ptr(a2), _ptr(out),
                                    _ptr(workspace), workspace.numel(), _stream(x.device)), "pyg_propagate_heads")
     return out
+
+
+def propagate_heads_backward(grad_out: torch.Tensor, x: torch.Tensor | None, csr: CSR, csr_t: CSR,
+                             alpha: torch.Tensor, heads: int, need_grad_x: bool = True, need_grad_alpha: bool = True,
+                             workspace: torch.Tensor | None = None):
+    """Gradients of propagate_heads: (grad_x [N, H*C] in grad_out's dtype or
+    None, grad_alpha fp32 [E, H] in CSR slot order or None)."""
+    lib = library()
+    _need_cuda("grad_out", grad_out, None, 2)
+    if grad_out.dtype not in DTYPE:
+        raise ValueError("grad_out must be float32 or bfloat16")
+    N, F = grad_out.shape
+    if heads <= 0 or F % heads:
+        raise ValueError("the feature width must be a multiple of heads")
+    C = F // heads
+    a2 = _edge_values("alpha", alpha, csr.E)
+    if need_grad_alpha:
+        _need_cuda("x", x, grad_out.dtype, 2)
+    dev = grad_out.device
+    gx = torch.empty_like(grad_out) if need_grad_x else None
+    ga = torch.empty((csr.E, heads), dtype=torch.float32, device=dev) if need_grad_alpha else None
+    nbytes = _size(lib.pyg_propagate_heads_backward_workspace, DTYPE[grad_out.dtype], N, heads, C, csr.E, csr_t.chunk)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, dev)
+    c, ct = csr._c(), csr_t._c()
+    _check(lib.pyg_propagate_heads_backward(_ptr(grad_out), _ptr(x if need_grad_alpha else None), DTYPE[grad_out.dtype],
+                                            N, heads, C, ctypes.byref(c), ctypes.byref(ct), _ptr(a2), _ptr(gx),
+                                            _ptr(ga), _ptr(workspace), workspace.numel(), _stream(dev)),
+           "pyg_propagate_heads_backward")
+    return gx, ga
+
+
+def gat_scores_backward(a_src: torch.Tensor, a_dst: torch.Tensor, csr: CSR, csr_t: CSR, grad_scores: torch.Tensor,
+                        negative_slope: float = 0.2, workspace: torch.Tensor | None = None):
+    """Gradients of GAT's edge scores w.r.t. the node logits: (grad_a_src,
+    grad_a_dst), fp32 [N, H]; grad_scores [E, H] in CSR slot order."""
+    lib = library()
+    _need_cuda("a_src", a_src, torch.float32, 2)
+    _need_cuda("a_dst", a_dst, torch.float32, 2)
+    N, H = a_src.shape
+    g2 = _edge_values("grad_scores", grad_scores, csr.E)
+    gs, gd = torch.empty_like(a_src), torch.empty_like(a_dst)
+    nbytes = _size(lib.pyg_gat_scores_backward_workspace, N, H, csr.E, csr_t.chunk)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, a_src.device)
+    c, ct = csr._c(), csr_t._c()
+    _check(lib.pyg_gat_scores_backward(_ptr(a_src), _ptr(a_dst), H, ctypes.c_float(negative_slope), ctypes.byref(c),
+                                       ctypes.byref(ct), _ptr(g2), _ptr(gs), _ptr(gd), _ptr(workspace),
+                                       workspace.numel(), _stream(a_src.device)), "pyg_gat_scores_backward")
+    return gs, gd
 
 
 def dense_transform(x: torch.Tensor, theta: torch.Tensor, out_dtype=torch.float32, out: torch.Tensor | None = None,

@@ -232,3 +232,26 @@ def test_propagate_edge_rejects_bad_arguments(lib):
     assert pe(N=2**31) == UNSUPPORTED
     assert pe(kernel=2, csr=ctypes.byref(good), order=0, ws_bytes=0) == WORKSPACE
     assert pe(ws_bytes=0, aggr=1) == WORKSPACE
+
+
+def test_attention_backward_rejects_bad_arguments(lib):
+    from paper_1903_02428_amd.binding import _Csr
+    good = ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 10, 20, 0))
+    other = ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 11, 20, 0))
+    no_perm = ctypes.byref(_Csr(0x30000, 0x40000, None, None, 10, 20, 0))
+    G, X, A, GX, GA = FAKE, ctypes.c_void_p(0x200000), ctypes.c_void_p(0x300000), ctypes.c_void_p(0x400000), \
+        ctypes.c_void_p(0x500000)
+    hb = lib.pyg_propagate_heads_backward
+    assert hb(G, X, 0, 10, 2, 4, good, None, A, GX, GA, FAKE, 1 << 30, None) == INVALID   # no reversed CSR
+    assert hb(G, X, 0, 10, 2, 4, good, other, A, GX, GA, FAKE, 1 << 30, None) == INVALID  # CSRs of other graphs
+    assert hb(G, X, 0, 10, 2, 4, good, no_perm, A, GX, GA, FAKE, 1 << 30, None) == INVALID
+    assert hb(G, X, 0, 10, 0, 4, good, good, A, GX, GA, FAKE, 1 << 30, None) == INVALID    # H = 0
+    assert hb(G, X, 0, 10, 2, 4, good, good, None, GX, GA, FAKE, 1 << 30, None) == INVALID  # no alpha
+    assert hb(G, None, 0, 10, 2, 4, good, good, A, GX, GA, FAKE, 1 << 30, None) == INVALID  # grad_alpha needs x
+    assert hb(G, X, 0, 10, 2, 4, good, good, A, None, None, FAKE, 1 << 30, None) == INVALID  # nothing to compute
+    assert hb(G, X, 0, 10, 2, 4, good, good, A, GX, GA, FAKE, 0, None) == WORKSPACE
+    gb = lib.pyg_gat_scores_backward
+    assert gb(A, A, 2, ctypes.c_float(float("inf")), good, good, G, GX, GA, FAKE, 1 << 30, None) == INVALID
+    assert gb(A, A, 2, ctypes.c_float(0.2), good, None, G, GX, GA, FAKE, 1 << 30, None) == INVALID
+    assert gb(A, A, 2, ctypes.c_float(0.2), good, good, None, GX, GA, FAKE, 1 << 30, None) == INVALID
+    assert gb(A, A, 2, ctypes.c_float(0.2), good, good, G, GX, GA, FAKE, 0, None) == WORKSPACE
