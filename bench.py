@@ -163,7 +163,7 @@ def main():
     if args.attention_only:
         pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
         print(json.dumps({"workload": "large power-law graph, GAT attention", "N": N, "E": E, "F": F,
-                          "attention": attention(pyg, torch, x, csr, N, E, F, dev)}), flush=True)
+                          "attention": attention(pyg, torch, x, ei, csr, N, E, F, dev)}), flush=True)
         return
 
     if args.gcn_layer_only:
@@ -259,7 +259,7 @@ def main():
 
     if not args.no_detail:
         result["detail"]["variants"] = variants(pyg, torch, x, ei, csr_w, N, E, F, dev)
-        result["detail"]["attention"] = attention(pyg, torch, x, csr, N, E, F, dev)
+        result["detail"]["attention"] = attention(pyg, torch, x, ei, csr, N, E, F, dev)
         result["detail"]["gcn_layer"] = gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)
         result["detail"]["edge_features"] = edge_features(pyg, torch, x, ei, csr, N, E, F, dev)
     if not (args.no_detail and args.no_cpu_baseline):
@@ -359,11 +359,13 @@ def variants(pyg, torch, x, ei, csr, N, E, F, dev):
     return res
 
 
-def attention(pyg, torch, x, csr, N, E, F, dev, H=8):
+def attention(pyg, torch, x, ei, csr, N, E, F, dev, H=8):
     """GAT-style attention on the same graph: H heads of C = F / H columns.
     Times the fused score+softmax call, the attention-weighted sum (fp32 and
-    bf16 rows), and the softmax forward from stored scores and its backward,
-    each with its algorithmic bytes (unique bytes read and written once)."""
+    bf16 rows), the softmax forward from stored scores and its backward, and
+    the backward of the attention sum and of the scores, each with its
+    algorithmic bytes (unique bytes read and written once; gathered rows
+    counted once per edge, as for the propagate)."""
     gen = torch.Generator(device=dev)
     gen.manual_seed(7)
     a_src = torch.randn(N, H, device=dev, generator=gen)
@@ -396,6 +398,41 @@ def attention(pyg, torch, x, csr, N, E, F, dev, H=8):
         res[f"propagate_heads_{dtname}"] = r
     layer = res["gat_softmax"]["ms"] + res["propagate_heads_f32"]["ms"]
     res["attention_layer_f32"] = {"ms": layer, "edges_features_per_s": E * F / (layer * 1e-3)}
+
+    # Backward. The reversed CSR is part of the graph preprocessing (built
+    # once per graph), not of the timed calls.
+    csr_t = pyg.coo_to_csr(pyg.reverse_edges(ei), N, chunk=csr.chunk)
+    map_t = pyg.csr_transpose_map(csr, csr_t)
+    ws_map = torch.empty(pyg.binding._size(pyg.library().pyg_csr_transpose_map_workspace, E), dtype=torch.uint8,
+                         device=dev)
+    ms = timed(torch, lambda: pyg.csr_transpose_map(csr, csr_t, out=map_t, workspace=ws_map))
+    res["csr_transpose_map"] = rec(ms, 16 * E + 4 * E)  # both permutations in, the map out
+    tmap = 4 * E  # the transpose map (slot of csr for each slot of csr_t)
+    g_alpha = torch.empty(E, H, device=dev)
+    for dtname, xx, sz in (("f32", x, 4), ("bf16", x.to(torch.bfloat16), 2)):
+        g = torch.randn(N, F, device=dev, generator=gen).to(xx.dtype)
+        gx = torch.empty_like(g)
+        wsb = torch.empty(pyg.binding._size(pyg.library().pyg_propagate_heads_backward_workspace,
+                                            pyg.binding.DTYPE[xx.dtype], N, H, F // H, E, csr_t.chunk),
+                          dtype=torch.uint8, device=dev)
+        ms = timed(torch, lambda: pyg.propagate_heads_backward(g, xx, csr, csr_t, alpha, H, workspace=wsb,
+                                                               out=(gx, g_alpha), map_t=map_t))
+        # grad_x: the attention sum over the reversed graph; grad_alpha: per
+        # edge and head a dot product of a gathered x row block with g's row.
+        b = 2 * rp + 8 * E + tmap + 4 * E * H + 4 * E * H + E * F * sz + N * F * sz \
+            + E * F * sz + N * F * sz
+        r = rec(ms, b)
+        r["edges_features_per_s"] = E * F / (ms * 1e-3)
+        res[f"propagate_heads_backward_{dtname}"] = r
+    outs = (torch.empty(N, H, device=dev), torch.empty(N, H, device=dev))
+    wsg = torch.empty(pyg.binding._size(pyg.library().pyg_gat_scores_backward_workspace, N, H, E, csr_t.chunk),
+                      dtype=torch.uint8, device=dev)
+    ms = timed(torch, lambda: pyg.gat_scores_backward(a_src, a_dst, csr, csr_t, grad, 0.2, workspace=wsg, out=outs,
+                                                      map_t=map_t))
+    res["gat_scores_backward"] = rec(ms, 2 * rp + 4 * E + tmap + 4 * E * H + 4 * E * H + 8 * N * H + 8 * N * H)
+    back = res["segment_softmax_backward"]["ms"] + res["propagate_heads_backward_f32"]["ms"] \
+        + res["gat_scores_backward"]["ms"]
+    res["attention_layer_backward_f32"] = {"ms": back, "edges_features_per_s": E * F / (back * 1e-3)}
     return res
 
 

@@ -303,22 +303,44 @@ int pyg_propagate_heads_workspace(int dtype, int64_t N, int64_t H, int64_t C, in
 int pyg_propagate_heads(const void *x, int dtype, int64_t N, int64_t H, int64_t C, const pyg_csr *csr,
                         const float *alpha, void *out, void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes needed by pyg_csr_transpose_map. */
+int pyg_csr_transpose_map_workspace(int64_t E, size_t *bytes);
+
+/* The transpose map between the CSR of an edge list (csr) and the CSR of
+ * its reversed edge list (csr_t), both built by pyg_coo_to_csr:
+ *   map_t[q] = the slot of csr that holds the edge of slot q of csr_t
+ *              (the slot p with csr->perm[p] == csr_t->perm[q]).
+ * int32 [E], caller-owned. Graph preprocessing like csr_t itself: made once
+ * per graph, it lets the backward below read values kept in csr slot order
+ * (the coefficients alpha, dL/dv) from the reversed CSR's rows without
+ * re-ordering them. Entries of a malformed permutation are clamped into
+ * [0, E) (results are then meaningless but every read stays in bounds).
+ * Errors: PYG_ERR_INVALID_ARG (NULL or mismatched CSRs, no perm),
+ * PYG_ERR_UNSUPPORTED (E >= 2^31), PYG_ERR_WORKSPACE. */
+int pyg_csr_transpose_map(const pyg_csr *csr, const pyg_csr *csr_t, int32_t *map_t, void *ws, size_t ws_bytes,
+                          void *stream);
+
 /* Workspace bytes needed by pyg_propagate_heads_backward (pass csr_t->chunk). */
 int pyg_propagate_heads_backward_workspace(int dtype, int64_t N, int64_t H, int64_t C, int64_t E, int64_t chunk_t,
                                            size_t *bytes);
 
-/* Gradient of pyg_propagate_heads for g = dL/d out [N, H*C]:
+/* Gradient of pyg_propagate_heads (GAT's attention sum, Eq. (1)) for
+ * g = dL/d out [N, H*C]:
  *   grad_x[j, h*C + c]  = sum over edges k = (j -> i) of alpha[k,h] * g[i, h*C + c]
  *                         (the attention sum over the reversed graph; csr_t is
  *                         the CSR of the reversed edge list, built like csr);
  *   grad_alpha[p, h]    = sum_c g[row(p), h*C + c] * x[col[p], h*C + c], CSR
  *                         slot order of csr (the order of alpha).
  * grad_out, x, grad_x in dtype (fp32 accumulation); alpha, grad_alpha fp32
- * [E, H]. Either output may be NULL (not both); x is needed for grad_alpha.
- * Deterministic. */
+ * [E, H]. map_t: the transpose map of (csr, csr_t) from
+ * pyg_csr_transpose_map, or NULL to make it in the workspace on every call.
+ * Either output may be NULL (not both); x is needed for grad_alpha.
+ * Deterministic. Errors: PYG_ERR_INVALID_ARG (NULL or mismatched CSRs,
+ * missing arrays, H <= 0), PYG_ERR_UNSUPPORTED (N, E or H*C >= 2^31),
+ * PYG_ERR_WORKSPACE. */
 int pyg_propagate_heads_backward(const void *grad_out, const void *x, int dtype, int64_t N, int64_t H, int64_t C,
-                                 const pyg_csr *csr, const pyg_csr *csr_t, const float *alpha, void *grad_x,
-                                 float *grad_alpha, void *ws, size_t ws_bytes, void *stream);
+                                 const pyg_csr *csr, const pyg_csr *csr_t, const int32_t *map_t, const float *alpha,
+                                 void *grad_x, float *grad_alpha, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_gat_scores_backward (pass csr_t->chunk). */
 int pyg_gat_scores_backward_workspace(int64_t N, int64_t H, int64_t E, int64_t chunk_t, size_t *bytes);
@@ -329,10 +351,12 @@ int pyg_gat_scores_backward_workspace(int64_t N, int64_t H, int64_t E, int64_t c
  *   dL/dv = g * (a_src[j,h] + a_dst[i,h] >= 0 ? 1 : negative_slope),
  *   grad_a_dst[i, h] = sum of dL/dv over the incoming edges of i,
  *   grad_a_src[j, h] = sum of dL/dv over the outgoing edges of j (rows of csr_t).
- * a_src, a_dst, grad_a_src, grad_a_dst fp32 [N, H]. Deterministic. */
+ * a_src, a_dst, grad_a_src, grad_a_dst fp32 [N, H]; map_t as for
+ * pyg_propagate_heads_backward (or NULL). Deterministic. Errors as there,
+ * plus PYG_ERR_INVALID_ARG for a non-finite negative_slope. */
 int pyg_gat_scores_backward(const float *a_src, const float *a_dst, int64_t H, float negative_slope,
-                            const pyg_csr *csr, const pyg_csr *csr_t, const float *grad_scores, float *grad_a_src,
-                            float *grad_a_dst, void *ws, size_t ws_bytes, void *stream);
+                            const pyg_csr *csr, const pyg_csr *csr_t, const int32_t *map_t, const float *grad_scores,
+                            float *grad_a_src, float *grad_a_dst, void *ws, size_t ws_bytes, void *stream);
 
 /* ---- Dense feature transform of a GCN layer (Section 2 lists GCN; its
  * layer multiplies the features by a weight matrix around the normalised

@@ -22,6 +22,7 @@ from .binding import (  # noqa: F401
     coo_to_csr,
     degree,
     dense_transform,
+    csr_transpose_map,
     gat_scores_backward,
     gat_softmax,
     gather_edges,

@@ -25,6 +25,7 @@ EXPORTED = [
     "pyg_propagate_backward",
     "pyg_segment_softmax_workspace", "pyg_segment_softmax", "pyg_gat_softmax", "pyg_segment_softmax_backward",
     "pyg_propagate_heads_workspace", "pyg_propagate_heads", "pyg_dense_transform_workspace", "pyg_dense_transform",
+    "pyg_csr_transpose_map_workspace", "pyg_csr_transpose_map",
     "pyg_propagate_heads_backward_workspace", "pyg_propagate_heads_backward", "pyg_gat_scores_backward_workspace",
     "pyg_gat_scores_backward",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
@@ -91,11 +92,13 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_heads": [p, i32, i64, i64, i64, ctypes.POINTER(_Csr), p, p, p, ctypes.c_size_t, p],
             "pyg_dense_transform_workspace": [i64, i64, sz],
             "pyg_propagate_heads_backward_workspace": [i32, i64, i64, i64, i64, i64, sz],
+            "pyg_csr_transpose_map_workspace": [i64, sz],
+            "pyg_csr_transpose_map": [ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), p, p, ctypes.c_size_t, p],
             "pyg_propagate_heads_backward": [p, p, i32, i64, i64, i64, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), p, p,
-                                             p, p, ctypes.c_size_t, p],
+                                             p, p, p, ctypes.c_size_t, p],
             "pyg_gat_scores_backward_workspace": [i64, i64, i64, i64, sz],
             "pyg_gat_scores_backward": [p, p, i64, ctypes.c_float, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), p, p, p,
-                                        p, ctypes.c_size_t, p],
+                                        p, p, ctypes.c_size_t, p],
             "pyg_dense_transform": [p, i32, i64, i64, p, i64, p, i32, p, ctypes.c_size_t, p],
             "pyg_global_pool_workspace": [i32, i64, i64, i64, i32, sz],
             "pyg_global_pool": [p, i32, i64, i64, p, i64, i32, p, p, p, ctypes.c_size_t, p],
@@ -491,11 +494,47 @@ def propagate_heads(x: torch.Tensor, csr: CSR, alpha: torch.Tensor, heads: int, 
     return out
 
 
+def csr_transpose_map(csr: CSR, csr_t: CSR, out: torch.Tensor | None = None,
+                      workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """int32 [E]: for each slot of csr_t (the CSR of the reversed edges) the
+    slot of csr holding the same edge. Made once per graph, passed as map_t
+    to the attention backward."""
+    lib = library()
+    if csr.N != csr_t.N or csr.E != csr_t.E:
+        raise ValueError("csr and csr_t must describe the same graph")
+    dev = csr.rowptr.device
+    if out is None:
+        out = torch.empty(csr.E, dtype=torch.int32, device=dev)
+    else:
+        _need_cuda("out", out, torch.int32, 1)
+        if out.shape[0] != csr.E:
+            raise ValueError("out must be [E]")
+    nbytes = _size(lib.pyg_csr_transpose_map_workspace, csr.E)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, dev)
+    c, ct = csr._c(), csr_t._c()
+    _check(lib.pyg_csr_transpose_map(ctypes.byref(c), ctypes.byref(ct), _ptr(out), _ptr(workspace), workspace.numel(),
+                                     _stream(dev)), "pyg_csr_transpose_map")
+    return out
+
+
+def _map_t(map_t, E):
+    if map_t is None:
+        return None
+    _need_cuda("map_t", map_t, torch.int32, 1)
+    if map_t.shape[0] != E:
+        raise ValueError("map_t must be [E]")
+    return map_t
+
+
 def propagate_heads_backward(grad_out: torch.Tensor, x: torch.Tensor | None, csr: CSR, csr_t: CSR,
                              alpha: torch.Tensor, heads: int, need_grad_x: bool = True, need_grad_alpha: bool = True,
-                             workspace: torch.Tensor | None = None):
+                             workspace: torch.Tensor | None = None, out: tuple | None = None,
+                             map_t: torch.Tensor | None = None):
     """Gradients of propagate_heads: (grad_x [N, H*C] in grad_out's dtype or
-    None, grad_alpha fp32 [E, H] in CSR slot order or None)."""
+    None, grad_alpha fp32 [E, H] in CSR slot order or None). `out` may bring
+    both result tensors (grad_x, grad_alpha) preallocated; `map_t` is
+    csr_transpose_map(csr, csr_t), else made on every call."""
     lib = library()
     _need_cuda("grad_out", grad_out, None, 2)
     if grad_out.dtype not in DTYPE:
@@ -508,35 +547,58 @@ def propagate_heads_backward(grad_out: torch.Tensor, x: torch.Tensor | None, csr
     if need_grad_alpha:
         _need_cuda("x", x, grad_out.dtype, 2)
     dev = grad_out.device
-    gx = torch.empty_like(grad_out) if need_grad_x else None
-    ga = torch.empty((csr.E, heads), dtype=torch.float32, device=dev) if need_grad_alpha else None
+    if out is not None:
+        gx, ga = out
+        if need_grad_x:
+            _need_cuda("out[0]", gx, grad_out.dtype, 2)
+            if tuple(gx.shape) != (N, F):
+                raise ValueError("out[0] must match grad_out's shape")
+        if need_grad_alpha:
+            _need_cuda("out[1]", ga, torch.float32, 2)
+            if tuple(ga.shape) != (csr.E, heads):
+                raise ValueError("out[1] must be [E, heads]")
+    else:
+        gx = torch.empty_like(grad_out) if need_grad_x else None
+        ga = torch.empty((csr.E, heads), dtype=torch.float32, device=dev) if need_grad_alpha else None
     nbytes = _size(lib.pyg_propagate_heads_backward_workspace, DTYPE[grad_out.dtype], N, heads, C, csr.E, csr_t.chunk)
     if workspace is None or workspace.numel() < nbytes:
         workspace = _workspace(nbytes, dev)
     c, ct = csr._c(), csr_t._c()
+    mt = _map_t(map_t, csr.E)
     _check(lib.pyg_propagate_heads_backward(_ptr(grad_out), _ptr(x if need_grad_alpha else None), DTYPE[grad_out.dtype],
-                                            N, heads, C, ctypes.byref(c), ctypes.byref(ct), _ptr(a2), _ptr(gx),
+                                            N, heads, C, ctypes.byref(c), ctypes.byref(ct), _ptr(mt), _ptr(a2), _ptr(gx),
                                             _ptr(ga), _ptr(workspace), workspace.numel(), _stream(dev)),
            "pyg_propagate_heads_backward")
     return gx, ga
 
 
 def gat_scores_backward(a_src: torch.Tensor, a_dst: torch.Tensor, csr: CSR, csr_t: CSR, grad_scores: torch.Tensor,
-                        negative_slope: float = 0.2, workspace: torch.Tensor | None = None):
+                        negative_slope: float = 0.2, workspace: torch.Tensor | None = None,
+                        out: tuple | None = None, map_t: torch.Tensor | None = None):
     """Gradients of GAT's edge scores w.r.t. the node logits: (grad_a_src,
-    grad_a_dst), fp32 [N, H]; grad_scores [E, H] in CSR slot order."""
+    grad_a_dst), fp32 [N, H]; grad_scores [E, H] in CSR slot order. `out`
+    may bring both result tensors preallocated; `map_t` as for
+    propagate_heads_backward."""
     lib = library()
     _need_cuda("a_src", a_src, torch.float32, 2)
     _need_cuda("a_dst", a_dst, torch.float32, 2)
     N, H = a_src.shape
     g2 = _edge_values("grad_scores", grad_scores, csr.E)
-    gs, gd = torch.empty_like(a_src), torch.empty_like(a_dst)
+    if out is not None:
+        gs, gd = out
+        for name, t in (("out[0]", gs), ("out[1]", gd)):
+            _need_cuda(name, t, torch.float32, 2)
+            if t.shape != a_src.shape:
+                raise ValueError(f"{name} must be [N, heads]")
+    else:
+        gs, gd = torch.empty_like(a_src), torch.empty_like(a_dst)
     nbytes = _size(lib.pyg_gat_scores_backward_workspace, N, H, csr.E, csr_t.chunk)
     if workspace is None or workspace.numel() < nbytes:
         workspace = _workspace(nbytes, a_src.device)
     c, ct = csr._c(), csr_t._c()
+    mt = _map_t(map_t, csr.E)
     _check(lib.pyg_gat_scores_backward(_ptr(a_src), _ptr(a_dst), H, ctypes.c_float(negative_slope), ctypes.byref(c),
-                                       ctypes.byref(ct), _ptr(g2), _ptr(gs), _ptr(gd), _ptr(workspace),
+                                       ctypes.byref(ct), _ptr(mt), _ptr(g2), _ptr(gs), _ptr(gd), _ptr(workspace),
                                        workspace.numel(), _stream(a_src.device)), "pyg_gat_scores_backward")
     return gs, gd
 

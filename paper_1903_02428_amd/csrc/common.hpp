@@ -138,6 +138,7 @@ struct SegmentArgs {
     const int32_t *col;    // [E] source row per slot; NULL = identity (slot id)
     const float *weight;   // [E] or NULL
     const float *alpha;    // [E, H] per-head weights in slot order, or NULL (sum only)
+    const int32_t *alpha_idx;  // [E] row of alpha for each slot, or NULL (row = slot)
     const void *edge_attr;       // [E, F] edge features in x's dtype (edge messages), or NULL
     const int64_t *attr_perm;    // non-NULL: edge_attr rows are COO edge ids, reached through perm
     int64_t H;             // heads; feature f belongs to head f / C

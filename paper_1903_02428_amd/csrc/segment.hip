@@ -42,6 +42,7 @@ struct SegParams {
     const int32_t *col;
     const float *w;
     const float *alpha;  // per-head weights [E, H] in slot order (kMsgHeads)
+    const int32_t *alpha_idx;  // non-NULL: slot p takes row alpha_idx[p] of alpha
     const void *ea;           // edge features [E, F] in x's dtype (edge messages)
     const int64_t *ea_perm;   // non-NULL: ea is in COO order, row perm[slot]
     int64_t H;
@@ -194,7 +195,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
     // column indices and weights stream once: read them 64 at a time,
     // non-temporally, one batch ahead of the gathers that use them; bit 31 of
     // a column marks a cold source row (gathered non-temporally)
-    auto fetch = [&](int64_t e, int &c, float &w) {
+    auto fetch = [&](int64_t e, int &c, float &w, int &ar) {
         if (IDENT) {
             c = static_cast<int>(e);
         } else {
@@ -202,17 +203,19 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
             if (hot > 0 && p.node_class[c] < hot) c |= static_cast<int>(0x80000000u);
         }
         if constexpr (MSG == kMsgWeighted) w = __builtin_nontemporal_load(p.w + e);
+        if constexpr (MSG == kMsgHeads) ar = p.alpha_idx ? __builtin_nontemporal_load(p.alpha_idx + e) : static_cast<int>(e);
     };
-    int nxc = 0;
+    int nxc = 0, nxa = 0;
     float nxw = 1.f;
-    if (s + lane < t) fetch(s + lane, nxc, nxw);
+    if (s + lane < t) fetch(s + lane, nxc, nxw, nxa);
     for (int64_t base = s; base < t; base += kWave) {
         const int n = static_cast<int>(uniform64((t - base) < kWave ? (t - base) : kWave));
         const int myc = nxc;
         const float myw = nxw;
-        if (base + kWave + lane < t) fetch(base + kWave + lane, nxc, nxw);
+        const int mya = nxa;
+        if (base + kWave + lane < t) fetch(base + kWave + lane, nxc, nxw, nxa);
         for (int st = 0; st < n; st += S * U) {
-            int jj[U];
+            int jj[U], aa[U];
             float ww[U];
             bool ok[U];
 #pragma unroll
@@ -221,6 +224,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                 ok[u] = idx < n;
                 jj[u] = __shfl(myc, idx & (kWave - 1), kWave);
                 if constexpr (MSG == kMsgWeighted) ww[u] = __shfl(myw, idx & (kWave - 1), kWave);
+                if constexpr (MSG == kMsgHeads) aa[u] = __shfl(mya, idx & (kWave - 1), kWave);
             }
             float wh[U][NS];
             if constexpr (MSG == kMsgHeads) {
@@ -228,7 +232,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                 for (int u = 0; u < U; ++u)
 #pragma unroll
                     for (int sl = 0; sl < NS; ++sl)
-                        wh[u][sl] = (ok[u] && act[sl]) ? p.alpha[(base + st + u * S + sg) * p.H + hd[sl]] : 0.f;
+                        wh[u][sl] = (ok[u] && act[sl]) ? p.alpha[(int64_t)aa[u] * p.H + hd[sl]] : 0.f;
             }
             constexpr bool EDGE = MSG >= kMsgEdgeAdd;
             R ev[U][NS];
@@ -376,7 +380,10 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
             jj[u] = ok[u] ? (IDENT ? static_cast<int>(base + u) : p.col[base + u]) : 0;
             ww[u] = 1.f;
             if constexpr (MSG == kMsgWeighted) ww[u] = ok[u] ? p.w[base + u] : 0.f;
-            if constexpr (MSG == kMsgHeads) ww[u] = (ok[u] && act) ? p.alpha[(base + u) * p.H + hd] : 0.f;
+            if constexpr (MSG == kMsgHeads) {
+                const int64_t ar = p.alpha_idx ? (ok[u] ? p.alpha_idx[base + u] : 0) : base + u;
+                ww[u] = (ok[u] && act) ? p.alpha[ar * p.H + hd] : 0.f;
+            }
         }
         constexpr bool EDGE = MSG >= kMsgEdgeAdd;
         R ev[U];
@@ -772,6 +779,7 @@ int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t 
     p.col = a.col;
     p.w = a.weight;
     p.alpha = a.alpha;
+    p.alpha_idx = a.alpha_idx;
     p.ea = a.edge_attr;
     p.ea_perm = a.attr_perm;
     p.H = a.H;

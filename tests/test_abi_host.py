@@ -242,16 +242,23 @@ def test_attention_backward_rejects_bad_arguments(lib):
     G, X, A, GX, GA = FAKE, ctypes.c_void_p(0x200000), ctypes.c_void_p(0x300000), ctypes.c_void_p(0x400000), \
         ctypes.c_void_p(0x500000)
     hb = lib.pyg_propagate_heads_backward
-    assert hb(G, X, 0, 10, 2, 4, good, None, A, GX, GA, FAKE, 1 << 30, None) == INVALID   # no reversed CSR
-    assert hb(G, X, 0, 10, 2, 4, good, other, A, GX, GA, FAKE, 1 << 30, None) == INVALID  # CSRs of other graphs
-    assert hb(G, X, 0, 10, 2, 4, good, no_perm, A, GX, GA, FAKE, 1 << 30, None) == INVALID
-    assert hb(G, X, 0, 10, 0, 4, good, good, A, GX, GA, FAKE, 1 << 30, None) == INVALID    # H = 0
-    assert hb(G, X, 0, 10, 2, 4, good, good, None, GX, GA, FAKE, 1 << 30, None) == INVALID  # no alpha
-    assert hb(G, None, 0, 10, 2, 4, good, good, A, GX, GA, FAKE, 1 << 30, None) == INVALID  # grad_alpha needs x
-    assert hb(G, X, 0, 10, 2, 4, good, good, A, None, None, FAKE, 1 << 30, None) == INVALID  # nothing to compute
-    assert hb(G, X, 0, 10, 2, 4, good, good, A, GX, GA, FAKE, 0, None) == WORKSPACE
+    assert hb(G, X, 0, 10, 2, 4, good, None, None, A, GX, GA, FAKE, 1 << 30, None) == INVALID   # no reversed CSR
+    assert hb(G, X, 0, 10, 2, 4, good, other, None, A, GX, GA, FAKE, 1 << 30, None) == INVALID  # other graphs
+    assert hb(G, X, 0, 10, 2, 4, good, no_perm, None, A, GX, GA, FAKE, 1 << 30, None) == INVALID
+    assert hb(G, X, 0, 10, 0, 4, good, good, None, A, GX, GA, FAKE, 1 << 30, None) == INVALID    # H = 0
+    assert hb(G, X, 0, 10, 2, 4, good, good, None, None, GX, GA, FAKE, 1 << 30, None) == INVALID  # no alpha
+    assert hb(G, None, 0, 10, 2, 4, good, good, None, A, GX, GA, FAKE, 1 << 30, None) == INVALID  # grad_alpha needs x
+    assert hb(G, X, 0, 10, 2, 4, good, good, None, A, None, None, FAKE, 1 << 30, None) == INVALID  # nothing to do
+    assert hb(G, X, 0, 10, 2, 4, good, good, None, A, GX, GA, FAKE, 0, None) == WORKSPACE
     gb = lib.pyg_gat_scores_backward
-    assert gb(A, A, 2, ctypes.c_float(float("inf")), good, good, G, GX, GA, FAKE, 1 << 30, None) == INVALID
-    assert gb(A, A, 2, ctypes.c_float(0.2), good, None, G, GX, GA, FAKE, 1 << 30, None) == INVALID
-    assert gb(A, A, 2, ctypes.c_float(0.2), good, good, None, GX, GA, FAKE, 1 << 30, None) == INVALID
-    assert gb(A, A, 2, ctypes.c_float(0.2), good, good, G, GX, GA, FAKE, 0, None) == WORKSPACE
+    inf = ctypes.c_float(float("inf"))
+    assert gb(A, A, 2, inf, good, good, None, G, GX, GA, FAKE, 1 << 30, None) == INVALID
+    assert gb(A, A, 2, ctypes.c_float(0.2), good, None, None, G, GX, GA, FAKE, 1 << 30, None) == INVALID
+    assert gb(A, A, 2, ctypes.c_float(0.2), good, good, None, None, GX, GA, FAKE, 1 << 30, None) == INVALID
+    assert gb(A, A, 2, ctypes.c_float(0.2), good, good, None, G, GX, GA, FAKE, 0, None) == WORKSPACE
+    tm = lib.pyg_csr_transpose_map
+    assert tm(good, None, FAKE, FAKE, 1 << 30, None) == INVALID
+    assert tm(good, other, FAKE, FAKE, 1 << 30, None) == INVALID
+    assert tm(good, no_perm, FAKE, FAKE, 1 << 30, None) == INVALID
+    assert tm(good, good, None, FAKE, 1 << 30, None) == INVALID  # no output
+    assert tm(good, good, FAKE, FAKE, 0, None) == WORKSPACE

@@ -36,16 +36,37 @@ def graphs(pyg, rng, N, E, chunk=0, hub=False):
     return ei, csr, csr_t, perm
 
 
-def heads_bwd_case(pyg, N, E, H, C, seed, dtype, chunk=0, hub=False):
+def transpose_map_ref(ei, N):
+    """The slot of the CSR holding the edge of each slot of the reversed CSR,
+    from the oracle's two CSR permutations."""
+    _, _, perm = oracle.coo_to_csr(ei, N)
+    _, _, perm_t = oracle.coo_to_csr(ei[::-1].copy(), N)
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(len(perm))
+    return inv[perm_t]
+
+
+def test_csr_transpose_map(pyg):
+    for i, (N, E) in enumerate([(1, 0), (5, 1), (300, 5000), (3000, 90000)]):
+        rng = np.random.default_rng(870 + i)
+        ei, csr, csr_t, _ = graphs(pyg, rng, N, E, 64 if i == 3 else 0, hub=i == 3)
+        got = pyg.csr_transpose_map(csr, csr_t)
+        torch.cuda.synchronize()
+        assert got.dtype == torch.int32 and np.array_equal(got.cpu().numpy(), transpose_map_ref(ei, N)), (N, E)
+
+
+def heads_bwd_case(pyg, N, E, H, C, seed, dtype, chunk=0, hub=False, use_map=False):
     rng = np.random.default_rng(seed)
     ei, csr, csr_t, perm = graphs(pyg, rng, N, E, chunk, hub)
+    mt = pyg.csr_transpose_map(csr, csr_t) if use_map else None
     x = rng.standard_normal((N, H * C)).astype(np.float32)
     g = rng.standard_normal((N, H * C)).astype(np.float32)
     if dtype == torch.bfloat16:
         x, g = bf16_round(x), bf16_round(g)
     alpha = rng.random((E, H)).astype(np.float32)
     rx, ra, sx, sa = oracle.propagate_heads_backward(x, ei, alpha, g, H)
-    gx, ga = pyg.propagate_heads_backward(to_dev(g).to(dtype), to_dev(x).to(dtype), csr, csr_t, to_dev(alpha[perm]), H)
+    gx, ga = pyg.propagate_heads_backward(to_dev(g).to(dtype), to_dev(x).to(dtype), csr, csr_t, to_dev(alpha[perm]), H,
+                                          map_t=mt)
     torch.cuda.synchronize()
     tag = f"heads bwd N={N} E={E} H={H} C={C} {dtype} chunk={chunk}"
     check_sum(gx, rx, sx, dtype == torch.bfloat16, tag + " grad_x")
@@ -58,22 +79,35 @@ def heads_bwd_case(pyg, N, E, H, C, seed, dtype, chunk=0, hub=False):
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
 def test_propagate_heads_backward(pyg, dtype):
     for i, (N, E, H, C) in enumerate(CASES):
-        heads_bwd_case(pyg, N, E, H, C, 900 + i, dtype)
+        heads_bwd_case(pyg, N, E, H, C, 900 + i, dtype, use_map=i % 2 == 1)
+
+
+def test_propagate_heads_backward_shapes(pyg):
+    """Head widths on both sides of the vector kernel's conditions: C a
+    multiple of the lane vector or not, lanes per head not a power of two
+    (C = 24 fp32), heads wider than a wavefront (C = 320 fp32) and rows of
+    more than 64 lane vectors (F = 512 fp32, two windows)."""
+    for i, (H, C, dtype) in enumerate([(4, 24, torch.float32), (2, 320, torch.float32), (8, 64, torch.float32),
+                                       (3, 8, torch.bfloat16), (2, 4, torch.bfloat16), (1, 1, torch.float32),
+                                       (16, 32, torch.bfloat16)]):
+        heads_bwd_case(pyg, 500, 6000, H, C, 880 + i, dtype, use_map=True)
 
 
 @pytest.mark.parametrize("chunk", [0, 64])
 def test_propagate_heads_backward_hubs(pyg, chunk):
     heads_bwd_case(pyg, 3000, 30000, 8, 8, 31, torch.float32, chunk=chunk, hub=True)
+    heads_bwd_case(pyg, 3000, 30000, 8, 16, 32, torch.bfloat16, chunk=chunk, hub=True, use_map=True)
 
 
-def gat_bwd_case(pyg, N, E, H, seed, slope=0.2, chunk=0, hub=False):
+def gat_bwd_case(pyg, N, E, H, seed, slope=0.2, chunk=0, hub=False, use_map=False):
     rng = np.random.default_rng(seed)
     ei, csr, csr_t, perm = graphs(pyg, rng, N, E, chunk, hub)
+    mt = pyg.csr_transpose_map(csr, csr_t) if use_map else None
     a_src = rng.standard_normal((N, H)).astype(np.float32)
     a_dst = rng.standard_normal((N, H)).astype(np.float32)
     ge = rng.standard_normal((E, H)).astype(np.float32)
     rs, rd, ss, sd = oracle.gat_scores_backward(a_src, a_dst, ei, ge, slope)
-    gs, gd = pyg.gat_scores_backward(to_dev(a_src), to_dev(a_dst), csr, csr_t, to_dev(ge[perm]), slope)
+    gs, gd = pyg.gat_scores_backward(to_dev(a_src), to_dev(a_dst), csr, csr_t, to_dev(ge[perm]), slope, map_t=mt)
     torch.cuda.synchronize()
     tag = f"gat bwd N={N} E={E} H={H} chunk={chunk}"
     check_sum(gs, rs, ss, False, tag + " a_src")
@@ -82,9 +116,9 @@ def gat_bwd_case(pyg, N, E, H, seed, slope=0.2, chunk=0, hub=False):
 
 def test_gat_scores_backward(pyg):
     for i, (N, E, H, _) in enumerate(CASES):
-        gat_bwd_case(pyg, N, E, H, 950 + i)
+        gat_bwd_case(pyg, N, E, H, 950 + i, use_map=i % 2 == 0)
     for chunk in (0, 64):
-        gat_bwd_case(pyg, 3000, 30000, 8, 32, slope=0.01, chunk=chunk, hub=True)
+        gat_bwd_case(pyg, 3000, 30000, 8, 32, slope=0.01, chunk=chunk, hub=True, use_map=chunk == 64)
 
 
 def test_gat_layer_gradients(pyg):
@@ -105,10 +139,11 @@ def test_gat_layer_gradients(pyg):
     csr = pyg.coo_to_csr(d_ei, N)
     csr_t = pyg.coo_to_csr(pyg.reverse_edges(d_ei), N)
     d_src, d_dst, d_x, d_g = to_dev(a_src), to_dev(a_dst), to_dev(x), to_dev(g)
+    mt = pyg.csr_transpose_map(csr, csr_t)
     alpha = pyg.gat_softmax(d_src, d_dst, csr, 0.2, "csr")
-    gx, galpha = pyg.propagate_heads_backward(d_g, d_x, csr, csr_t, alpha, H)
+    gx, galpha = pyg.propagate_heads_backward(d_g, d_x, csr, csr_t, alpha, H, map_t=mt)
     gscore = pyg.segment_softmax_backward(alpha, galpha, csr, "csr")
-    gs, gd = pyg.gat_scores_backward(d_src, d_dst, csr, csr_t, gscore, 0.2)
+    gs, gd = pyg.gat_scores_backward(d_src, d_dst, csr, csr_t, gscore, 0.2, map_t=mt)
     torch.cuda.synchronize()
     e = oracle.gat_scores(a_src, a_dst, ei, 0.2)
     al = oracle.segment_softmax(e, ei, N).astype(np.float32)
@@ -129,10 +164,12 @@ def test_attention_backward_is_deterministic(pyg):
     alpha = torch.rand(E, H, device="cuda")
     a_s, a_d = torch.randn(N, H, device="cuda"), torch.randn(N, H, device="cuda")
     ge = torch.randn(E, H, device="cuda")
+    mt = pyg.csr_transpose_map(csr, csr_t)
     first = pyg.propagate_heads_backward(g, x, csr, csr_t, alpha, H)
     f2 = pyg.gat_scores_backward(a_s, a_d, csr, csr_t, ge)
-    for _ in range(2):
-        again = pyg.propagate_heads_backward(g, x, csr, csr_t, alpha, H)
+    for i in range(2):  # with and without the precomputed map: the same bits
+        m = mt if i else None
+        again = pyg.propagate_heads_backward(g, x, csr, csr_t, alpha, H, map_t=m)
         assert torch.equal(again[0], first[0]) and torch.equal(again[1], first[1])
-        a2 = pyg.gat_scores_backward(a_s, a_d, csr, csr_t, ge)
+        a2 = pyg.gat_scores_backward(a_s, a_d, csr, csr_t, ge, map_t=m)
         assert torch.equal(a2[0], f2[0]) and torch.equal(a2[1], f2[1])
