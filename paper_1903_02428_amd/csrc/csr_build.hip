@@ -46,23 +46,30 @@ constexpr int kWaves = kBlock / kWave;
 
 // ------------------------------------------------------------------ degree
 
-// Count targets of edge partition blockIdx.y that fall in node slice
-// blockIdx.x; write the slice's counters to partial[y][node]. One workgroup
-// of 1024 threads holds a whole slice in LDS, so each thread keeps 8 target
-// loads in flight.
+// Count targets of one edge partition that fall in one node slice; write
+// the slice's counters to partial[partition][node]. One workgroup of 1024
+// threads holds a whole slice in LDS, so each thread keeps 8 target loads in
+// flight. Every slice reads the whole partition: the workgroup -> (slice,
+// partition) map puts the slices of a partition on one XCD (workgroups are
+// dealt to the 8 XCDs in turn), so that one XCD's L2 serves the re-reads.
 constexpr int kHistThreads = 1024;
 constexpr int kHistUnroll = 8;
+constexpr int kXcds = 8;
 
 __global__ __launch_bounds__(kHistThreads) void k_hist_slice(const int64_t *__restrict__ dst, int64_t E, int64_t N,
-                                                             int64_t slice, int64_t part_len,
+                                                             int64_t slice, int64_t nslices, int64_t part_len,
                                                              uint32_t *__restrict__ partial) {
     extern __shared__ uint32_t cnt[];
-    const int64_t n0 = (int64_t)blockIdx.x * slice;
+    const int64_t T = gridDim.x, w = blockIdx.x;
+    const int64_t q = T / kXcds, rem = T % kXcds, xcd = w % kXcds, wi = w / kXcds;
+    const int64_t L = xcd < rem ? xcd * (q + 1) + wi : rem * (q + 1) + (xcd - rem) * q + wi;  // XCD-major order
+    const int64_t sl = L % nslices, part = L / nslices;
+    const int64_t n0 = sl * slice;
     const int64_t n1 = (n0 + slice) < N ? (n0 + slice) : N;
     const int64_t len = n1 - n0;
     for (int64_t i = threadIdx.x; i < len; i += kHistThreads) cnt[i] = 0;
     __syncthreads();
-    const int64_t e0 = (int64_t)blockIdx.y * part_len;
+    const int64_t e0 = part * part_len;
     const int64_t e1 = (e0 + part_len) < E ? (e0 + part_len) : E;
     int64_t k = e0 + threadIdx.x;
     for (; k + (kHistUnroll - 1) * kHistThreads < e1; k += kHistUnroll * kHistThreads) {
@@ -78,7 +85,7 @@ __global__ __launch_bounds__(kHistThreads) void k_hist_slice(const int64_t *__re
         if (static_cast<uint64_t>(d) < static_cast<uint64_t>(len)) atomicAdd(&cnt[d], 1u);
     }
     __syncthreads();
-    uint32_t *out = partial + (int64_t)blockIdx.y * N + n0;
+    uint32_t *out = partial + part * N + n0;
     for (int64_t i = threadIdx.x; i < len; i += kHistThreads) out[i] = cnt[i];
 }
 
@@ -135,7 +142,8 @@ int count_targets(const int64_t *dst, int64_t E, int64_t N, Out *out, void *ws, 
     if (hipFuncSetAttribute(reinterpret_cast<const void *>(k_hist_slice), hipFuncAttributeMaxDynamicSharedMemorySize,
                             static_cast<int>(h.lds)) != hipSuccess)
         return PYG_ERR_HIP;
-    k_hist_slice<<<dim3((unsigned)h.nslices, (unsigned)h.parts), kHistThreads, h.lds, s>>>(dst, E, N, h.slice, h.part_len, partial);
+    k_hist_slice<<<(unsigned)(h.nslices * h.parts), kHistThreads, h.lds, s>>>(dst, E, N, h.slice, h.nslices, h.part_len,
+                                                                              partial);
     PYG_LAUNCH_CHECK();
     k_hist_reduce<Out><<<grid_for(N, kBlock), kBlock, 0, s>>>(partial, N, h.parts, out);
     PYG_LAUNCH_CHECK();
