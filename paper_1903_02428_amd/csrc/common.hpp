@@ -100,6 +100,17 @@ __device__ inline int64_t wave_lower_bound(const int64_t *__restrict__ a, int64_
     return m ? lo + (__ffsll(static_cast<unsigned long long>(m)) - 1) : len - 1;
 }
 
+// Workgroups of a launch are dealt to the 8 XCDs in turn (workgroup w runs
+// on XCD w % 8). xcd_major(w, T) renumbers the T workgroups so that each XCD
+// takes one contiguous range of the new order: work items that are
+// neighbours in that order (and share data or cache lines) share one XCD's
+// L2. A bijection of [0, T) for every T; placement only, never results.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int64_t xcd_major(int64_t w, int64_t T) {
+    const int64_t q = T / kXcds, rem = T % kXcds, xcd = w % kXcds, wi = w / kXcds;
+    return xcd < rem ? xcd * (q + 1) + wi : rem * (q + 1) + (xcd - rem) * q + wi;
+}
+
 // ------------------------------------------------------------ small kernels
 
 template <typename T>

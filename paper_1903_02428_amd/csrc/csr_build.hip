@@ -54,15 +54,12 @@ constexpr int kWaves = kBlock / kWave;
 // dealt to the 8 XCDs in turn), so that one XCD's L2 serves the re-reads.
 constexpr int kHistThreads = 1024;
 constexpr int kHistUnroll = 8;
-constexpr int kXcds = 8;
 
 __global__ __launch_bounds__(kHistThreads) void k_hist_slice(const int64_t *__restrict__ dst, int64_t E, int64_t N,
                                                              int64_t slice, int64_t nslices, int64_t part_len,
                                                              uint32_t *__restrict__ partial) {
     extern __shared__ uint32_t cnt[];
-    const int64_t T = gridDim.x, w = blockIdx.x;
-    const int64_t q = T / kXcds, rem = T % kXcds, xcd = w % kXcds, wi = w / kXcds;
-    const int64_t L = xcd < rem ? xcd * (q + 1) + wi : rem * (q + 1) + (xcd - rem) * q + wi;  // XCD-major order
+    const int64_t L = xcd_major(blockIdx.x, gridDim.x);
     const int64_t sl = L % nslices, part = L / nslices;
     const int64_t n0 = sl * slice;
     const int64_t n1 = (n0 + slice) < N ? (n0 + slice) : N;
@@ -281,7 +278,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
     const uint32_t mask = (1u << bits) - 1;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    const int64_t tile = blockIdx.x;
+    const int64_t tile = xcd_major(blockIdx.x, gridDim.x);  // neighbouring tiles write neighbouring runs
     const int64_t tbase = tile * kTile;
     const int64_t tlen = (E - tbase) < kTile ? (E - tbase) : kTile;
     const int64_t ebase = tbase + wave * kWaveKeys + lane;  // element of round r: ebase + r * 64
@@ -414,7 +411,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter64(
     const uint64_t mask = (1ull << bits) - 1;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    const int64_t tile = blockIdx.x;
+    const int64_t tile = xcd_major(blockIdx.x, gridDim.x);  // neighbouring tiles write neighbouring runs
     const int64_t tbase = tile * kTile;
     const int64_t tlen = (E - tbase) < kTile ? (E - tbase) : kTile;
     const int64_t ebase = tbase + wave * kWaveKeys + lane;
