@@ -101,6 +101,13 @@ typedef struct {
     int64_t chunk;
 } pyg_csr;
 
+/* In-degree from a CSR built by pyg_coo_to_csr: deg[i] = rowptr[i+1] -
+ * rowptr[i], the same counts as pyg_degree on the edge list the CSR was
+ * built from (its rows are the targets), read off the row boundaries the
+ * sort produced instead of counting the edge list again. deg int64 [N]
+ * (device, output). Errors: PYG_ERR_INVALID_ARG (NULL csr/rowptr/deg). */
+int pyg_degree_csr(const pyg_csr *csr, int64_t *deg, void *stream);
+
 /* Human-readable text for a status code (static storage, never NULL). */
 const char *pyg_strerror(int status);
 

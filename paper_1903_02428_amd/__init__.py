@@ -20,9 +20,10 @@ from .binding import (  # noqa: F401
     PygError,
     abi_version,
     coo_to_csr,
-    degree,
-    dense_transform,
     csr_transpose_map,
+    degree,
+    degree_csr,
+    dense_transform,
     gat_scores_backward,
     gat_softmax,
     gather_edges,

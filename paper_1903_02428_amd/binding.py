@@ -18,7 +18,8 @@ KERNEL = {"auto": 0, "coo": 1, "csr": 2}
 ORDER = {"csr": 0, "coo": 1}
 
 EXPORTED = [
-    "pyg_strerror", "pyg_abi_version", "pyg_degree_workspace", "pyg_degree", "pyg_coo_to_csr_workspace",
+    "pyg_strerror", "pyg_abi_version", "pyg_degree_workspace", "pyg_degree", "pyg_degree_csr",
+    "pyg_coo_to_csr_workspace",
     "pyg_coo_to_csr", "pyg_gather_edges",
     "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_gcn_norm_csr_workspace", "pyg_gcn_norm_csr",
     "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_edge", "pyg_propagate_backward_workspace",
@@ -69,6 +70,7 @@ def library() -> ctypes.CDLL:
         sigs = {
             "pyg_degree_workspace": [i64, i64, sz],
             "pyg_degree": [p, i64, i64, p, p, ctypes.c_size_t, p],
+            "pyg_degree_csr": [ctypes.POINTER(_Csr), p, p],
             "pyg_coo_to_csr_workspace": [i64, i64, sz],
             "pyg_coo_to_csr": [p, i64, i64, p, p, p, p, p, p, ctypes.c_size_t, p],
             "pyg_gather_edges": [p, i64, p, p, p],
@@ -191,6 +193,22 @@ def degree(edge_index: torch.Tensor, num_nodes: int, out: torch.Tensor | None = 
     _check(lib.pyg_degree(_ptr(edge_index), E, num_nodes, _ptr(deg), _ptr(ws), ws.numel(), _stream(dev)),
            "pyg_degree")
     return deg
+
+
+def degree_csr(csr: "CSR", out: torch.Tensor | None = None) -> torch.Tensor:
+    """In-degree read off a CSR's row boundaries (the same counts as
+    degree() on the edge list the CSR was built from)."""
+    lib = library()
+    dev = csr.rowptr.device
+    if out is None:
+        out = torch.empty(csr.N, dtype=torch.int64, device=dev)
+    else:
+        _need_cuda("out", out, torch.int64, 1)
+        if out.shape[0] != csr.N:
+            raise ValueError("out must be [N]")
+    c = csr._c()
+    _check(lib.pyg_degree_csr(ctypes.byref(c), _ptr(out), _stream(dev)), "pyg_degree_csr")
+    return out
 
 
 def coo_to_csr(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tensor | None = None,

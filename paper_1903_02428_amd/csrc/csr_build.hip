@@ -31,7 +31,7 @@ namespace pyg {
 namespace {
 
 #ifndef PYG_RADIX_ITEMS
-#define PYG_RADIX_ITEMS 16
+#define PYG_RADIX_ITEMS 8  // 2048-key tiles: twice the workgroups of 16, measured faster with XCD-major tiles
 #endif
 #ifndef PYG_RADIX_BITS
 #define PYG_RADIX_BITS 7  // 18-bit ids: three 6-bit passes, whose 64-key runs write whole lines
@@ -610,6 +610,24 @@ extern "C" int pyg_degree(const int64_t *edge_index, int64_t E, int64_t N, int64
     if (E > 0 && N == 0) return PYG_ERR_INVALID_ARG;
     if (ws_bytes < degree_workspace(E, N) || !ws) return PYG_ERR_WORKSPACE;
     return count_targets<int64_t>(edge_index + E, E, N, deg, ws, static_cast<hipStream_t>(stream));
+}
+
+namespace pyg {
+namespace {
+__global__ void k_rowptr_degree(const int64_t *__restrict__ rowptr, int64_t N, int64_t *__restrict__ deg) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x)
+        deg[i] = rowptr[i + 1] - rowptr[i];
+}
+}  // namespace
+}  // namespace pyg
+
+extern "C" int pyg_degree_csr(const pyg_csr *csr, int64_t *deg, void *stream) {
+    if (!csr || csr->N < 0 || !csr->rowptr || (csr->N > 0 && !deg)) return PYG_ERR_INVALID_ARG;
+    if (csr->N == 0) return PYG_OK;
+    k_rowptr_degree<<<grid_for(csr->N, kBlock * 4), kBlock, 0, static_cast<hipStream_t>(stream)>>>(csr->rowptr, csr->N,
+                                                                                                    deg);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
 }
 
 extern "C" int pyg_coo_to_csr_workspace(int64_t E, int64_t N, size_t *bytes) {

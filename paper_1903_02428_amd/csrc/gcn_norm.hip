@@ -7,6 +7,13 @@
 // step is order-independent, so the result is reproducible bit for bit.
 #include "common.hpp"
 
+#ifndef PYG_NORM_UNROLL
+#define PYG_NORM_UNROLL 8  // column loads (then dinv gathers) in flight per lane
+#endif
+#ifndef PYG_NORM_CHUNK
+#define PYG_NORM_CHUNK 2048  // CSR slots per wavefront
+#endif
+
 namespace pyg {
 namespace {
 
@@ -91,7 +98,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_edge_norm(const int64_t *__restr
         const int64_t a = s > e0 ? s : e0, b = t < e1 ? t : e1;
         const double di = dinv[r];
         // U independent column loads, then U dinv gathers, per lane and batch
-        constexpr int U = 8;
+        constexpr int U = PYG_NORM_UNROLL;
         for (int64_t p0 = a + lane; p0 < b; p0 += (int64_t)kWave * U) {
             int32_t cj[U];
             float wv[U];
@@ -144,7 +151,7 @@ extern "C" int pyg_gcn_norm_csr(const pyg_csr *csr, float *norm_csr, void *ws, s
         k_row_dinv_count<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(csr->rowptr, N, dinv);
     }
     PYG_LAUNCH_CHECK();
-    constexpr int64_t kChunk = 2048;
+    constexpr int64_t kChunk = PYG_NORM_CHUNK;
     const int64_t nchunks = (E + kChunk - 1) / kChunk;
     k_csr_edge_norm<<<static_cast<unsigned>((nchunks + 3) / 4), kBlock, 0, s>>>(csr->rowptr, csr->col, csr->weight, N, E,
                                                                               kChunk, dinv, norm_csr);

@@ -262,3 +262,11 @@ def test_attention_backward_rejects_bad_arguments(lib):
     assert tm(good, no_perm, FAKE, FAKE, 1 << 30, None) == INVALID
     assert tm(good, good, None, FAKE, 1 << 30, None) == INVALID  # no output
     assert tm(good, good, FAKE, FAKE, 0, None) == WORKSPACE
+
+
+def test_degree_csr_rejects_bad_arguments(lib):
+    from paper_1903_02428_amd.binding import _Csr
+    assert lib.pyg_degree_csr(None, FAKE, None) == INVALID
+    assert lib.pyg_degree_csr(ctypes.byref(_Csr(None, 0x40000, 0x50000, None, 10, 20, 0)), FAKE, None) == INVALID
+    assert lib.pyg_degree_csr(ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 10, 20, 0)), None, None) == INVALID
+    assert lib.pyg_degree_csr(ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 0, 0, 0)), None, None) == 0  # N = 0

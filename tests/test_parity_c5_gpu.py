@@ -42,7 +42,9 @@ def dev_graph(pyg, c5):
 def test_c5_degree_csr_norm_full(pyg, c5, dev_graph):
     ei_np, N = c5["edge_index_gcn"], c5["N"]
     ei, w_ref, csr = dev_graph
-    assert np.array_equal(pyg.degree(ei, N).cpu().numpy(), oracle.degree(ei_np, N))
+    deg_ref = oracle.degree(ei_np, N)
+    assert np.array_equal(pyg.degree(ei, N).cpu().numpy(), deg_ref)
+    assert np.array_equal(pyg.degree_csr(csr).cpu().numpy(), deg_ref)  # what the benchmark step reports
     rp, col, perm = oracle.coo_to_csr(ei_np, N)
     assert np.array_equal(csr.rowptr.cpu().numpy(), rp)
     assert np.array_equal(csr.perm.cpu().numpy(), perm)

@@ -52,6 +52,7 @@ def test_degree_and_csr_bit_exact(pyg, N, E, F):
     assert np.array_equal(csr.col.cpu().numpy().astype(np.int64), col)
     assert np.array_equal(csr.perm.cpu().numpy(), perm)
     assert np.array_equal(csr.weight.cpu().numpy(), w_np[perm])
+    assert np.array_equal(pyg.degree_csr(csr).cpu().numpy(), oracle.degree(ei_np, N))
 
 
 def test_csr_many_digits(pyg):
