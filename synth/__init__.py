@@ -14,6 +14,7 @@ from .graphs import (  # noqa: F401
     config5_large_power_law,
     erdos_renyi,
     make_config,
+    graded_in_degree,
     random_coo,
     rng_for,
     star_graph,

@@ -181,6 +181,18 @@ def random_coo(rng: np.random.Generator, N: int, E: int, self_loops: bool = True
     return np.ascontiguousarray(ei)
 
 
+def graded_in_degree(rng: np.random.Generator, N: int, degrees) -> np.ndarray:
+    """Targets 0 .. len(degrees)-1 receive degrees[i] edges each from
+    uniform random sources in [0, N); edges in random order. Row lengths
+    spread over a chosen range (short rows, rows of a few hundred to a few
+    thousand slots, ...) without one hub taking the graph."""
+    deg = np.asarray(degrees, dtype=np.int64)
+    dst = np.repeat(np.arange(deg.size, dtype=np.int64), deg)
+    src = rng.integers(0, N, dst.size, dtype=np.int64)
+    order = rng.permutation(dst.size)
+    return np.ascontiguousarray(np.stack([src[order], dst[order]]))
+
+
 def star_graph(N: int, hub: int = 0, rng: np.random.Generator | None = None) -> np.ndarray:
     """Every other node points at ``hub`` (one in-degree N-1 row)."""
     leaves = np.array([i for i in range(N) if i != hub], np.int64)

@@ -179,6 +179,72 @@ def test_gat_layer_chain(pyg):
     assert np.all(np.abs(g - ref) <= 2e-5 * sabs + 1e-6)
 
 
+def graded_graph(pyg, rng, n_targets, dmax, chunk):
+    """Row lengths from 1 to dmax slots in geometric steps (rows that fit a
+    group's registers, rows just above, and rows up to a chunk that take the
+    two-pass path), a CSR built with the given chunk so that rows up to a
+    chunk stay whole."""
+    deg = np.unique(np.geomspace(1, dmax, n_targets).astype(np.int64))
+    N = max(int(deg.size), 64)
+    ei = synth.graded_in_degree(rng, N, deg)
+    d_ei = to_dev(ei)
+    csr = pyg.coo_to_csr(d_ei, N, chunk=chunk)
+    _, _, perm = oracle.coo_to_csr(ei, N)
+    assert np.array_equal(csr.perm.cpu().numpy(), perm)
+    return ei, csr, perm, N
+
+
+GRADED = [(4, 6000, 8192), (8, 4096, 4096), (16, 2048, 2048), (64, 300, 1024), (256, 80, 512)]
+
+
+@pytest.mark.parametrize("H,dmax,chunk", GRADED)
+def test_softmax_graded_rows(pyg, H, dmax, chunk):
+    """Row lengths across the register path and the two-pass path, whole
+    rows up to a chunk: forward from scores in both orders, the fused GAT
+    form and the backward, against the oracle."""
+    rng = np.random.default_rng(1000 + H)
+    ei, csr, perm, N = graded_graph(pyg, rng, 120, dmax, chunk)
+    E = ei.shape[1]
+    inv = np.argsort(perm)
+    s = (rng.standard_normal((E, H)) * 3).astype(np.float32)
+    ref = oracle.segment_softmax(s, ei, N)
+    for order in ("csr", "coo"):
+        got = pyg.segment_softmax(to_dev(s[perm] if order == "csr" else s), csr, order).cpu().numpy()
+        got = got[inv] if order == "csr" else got
+        check_softmax(torch.from_numpy(np.ascontiguousarray(got)), ref, s, ei[1], N, f"graded softmax H={H} {order}")
+    a_src = (rng.standard_normal((N, H)) * 2).astype(np.float32)
+    a_dst = (rng.standard_normal((N, H)) * 2).astype(np.float32)
+    e = oracle.gat_scores(a_src, a_dst, ei, 0.2)
+    got = pyg.gat_softmax(to_dev(a_src), to_dev(a_dst), csr, 0.2, "csr").cpu().numpy()[inv]
+    check_softmax(torch.from_numpy(np.ascontiguousarray(got)), oracle.segment_softmax(e, ei, N), e, ei[1], N,
+                  f"graded gat H={H}")
+    alpha = ref.astype(np.float32)
+    g = rng.standard_normal((E, H)).astype(np.float32)
+    rb, sabs = oracle.segment_softmax_backward(alpha, g, ei, N)
+    for order in ("csr", "coo"):
+        a_in, g_in = (alpha[perm], g[perm]) if order == "csr" else (alpha, g)
+        got = pyg.segment_softmax_backward(to_dev(a_in), to_dev(g_in), csr, order).cpu().numpy()
+        got = got[inv] if order == "csr" else got
+        err = np.abs(got.astype(np.float64) - rb)
+        bound = 1e-5 * sabs + 1e-12
+        assert np.all(err <= bound), f"graded softmax bwd H={H} {order}: max err/bound {np.max(err / bound)}"
+
+
+def test_softmax_graded_rows_deterministic(pyg):
+    rng = np.random.default_rng(1099)
+    ei, csr, perm, N = graded_graph(pyg, rng, 150, 4096, 4096)
+    E, H = ei.shape[1], 8
+    a_src, a_dst = torch.randn(N, H, device="cuda"), torch.randn(N, H, device="cuda")
+    s, g = torch.randn(E, H, device="cuda"), torch.randn(E, H, device="cuda")
+    first = (pyg.gat_softmax(a_src, a_dst, csr), pyg.segment_softmax(s, csr),
+             pyg.segment_softmax_backward(s.softmax(1).contiguous(), g, csr))
+    for _ in range(2):
+        again = (pyg.gat_softmax(a_src, a_dst, csr), pyg.segment_softmax(s, csr),
+                 pyg.segment_softmax_backward(s.softmax(1).contiguous(), g, csr))
+        for x, y in zip(first, again):
+            assert torch.equal(x, y)
+
+
 def test_attention_is_deterministic(pyg):
     rng = np.random.default_rng(17)
     N, E, H = 4000, 90000, 8
