@@ -77,6 +77,8 @@ def parse():
     ap.add_argument("--fig2", action="store_true",
                     help="run the degree sweep of the paper's Fig. 2 (gather/scatter vs CSR, forward and backward) "
                          "instead of the headline step; prints one JSON line per point")
+    ap.add_argument("--configs-only", action="store_true",
+                    help="only the throughput of the four smaller synthetic graphs (one JSON object)")
     ap.add_argument("--attention-only", action="store_true",
                     help="time only the attention calls (GAT softmax, attention sum) on the large graph")
     ap.add_argument("--gcn-layer-only", action="store_true",
@@ -126,6 +128,11 @@ def main():
     torch.cuda.set_device(dev)
     if args.fig2:
         fig2_sweep(pyg, torch, synth, dev, args)
+        return
+    if args.configs_only:
+        print(json.dumps({"workload": "the four smaller synthetic graphs", "configs": small_configs(pyg, torch, dev,
+                                                                                                  args.seed)}),
+              flush=True)
         return
 
     t0 = time.time()
@@ -263,6 +270,7 @@ def main():
         result["detail"]["attention"] = attention(pyg, torch, x, ei, csr, N, E, F, dev)
         result["detail"]["gcn_layer"] = gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)
         result["detail"]["edge_features"] = edge_features(pyg, torch, x, ei, csr, N, E, F, dev)
+        result["detail"]["configs"] = small_configs(pyg, torch, dev, args.seed)
     if not (args.no_detail and args.no_cpu_baseline):
         import oracle
         w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)  # the oracle's own weights
@@ -327,9 +335,10 @@ def fig2_sweep(pyg, torch, synth, dev, args):
             print(json.dumps(rec), flush=True)
 
 
-def timed(torch, fn, reps=10):
+def timed(torch, fn, reps=10, warm=1):
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    fn()
+    for _ in range(warm):
+        fn()
     ts = []
     for _ in range(reps):
         s.record()
@@ -338,6 +347,69 @@ def timed(torch, fn, reps=10):
         e.synchronize()
         ts.append(s.elapsed_time(e))
     return float(np.median(ts))
+
+
+def small_configs(pyg, torch, dev, seed):
+    """Throughput on the four smaller synthetic graphs, for the runs each one
+    names: the Cora-shaped and PubMed-shaped graphs (gcn_norm-weighted sum,
+    mean, max; F = 64 and 500 for the latter), the mini-batch (unweighted
+    sum, mean, max, then global sum/mean/max pooling of the sum), the kNN
+    clouds (x_j - x_i with max and mean). Both kernels, each call timed alone
+    (median of 10, after 50 warm-up calls that bring the clocks up) against its
+    algorithmic bytes. At these sizes (0.2 to
+    55 MB per call) launch latency and the chip's fill dominate."""
+    import synth
+    res = {}
+
+    def rec(ms, b, E, F):
+        return {"ms": ms, "edges_features_per_s": E * F / (ms * 1e-3), "alg_GBps": b / (ms * 1e-3) / 1e9,
+                "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
+    runs = [(1, {}), (2, {"F": 64}), (2, {"F": 500}), (3, {}), (4, {})]
+    for ci, kw in runs:
+        c = synth.make_config(ci, seed=seed, **kw)
+        N, F = c["N"], c["F"]
+        name = f"C{ci}" + (f"-F{F}" if ci == 2 else "")
+        ei_np = c["edge_index_gcn"] if ci in (1, 2) else c["edge_index"]
+        E = ei_np.shape[1]
+        ei = torch.from_numpy(ei_np).to(dev)
+        x = torch.from_numpy(c["x"]).to(dev)
+        weighted = ci in (1, 2)
+        w = pyg.gcn_norm(ei, N) if weighted else None
+        csr = pyg.coo_to_csr(ei, N, w)
+        msg = "diff" if ci == 4 else "src"
+        aggrs = ("max", "mean") if ci == 4 else ("sum", "mean", "max")
+        out = torch.empty_like(x)
+        am = torch.empty((N, F), dtype=torch.int64, device=dev)
+        entry = {"N": N, "E": E, "F": F, "msg": msg, "weighted": weighted}
+        for aggr in aggrs:
+            for kernel in ("csr", "coo"):
+                ws = torch.empty(pyg.propagate_workspace_bytes(x, E, aggr, kernel, csr.chunk), dtype=torch.uint8,
+                                 device=dev)
+                ms = timed(torch, lambda: pyg.propagate(x, ei, w, csr=csr if kernel == "csr" else None, aggr=aggr,
+                                                        msg=msg, kernel=kernel, out=out,
+                                                        argmax=am if aggr == "max" else None, workspace=ws),
+                           warm=50)
+                b = b_alg_csr(N, E, F, 4, weighted) if kernel == "csr" else b_alg_coo(N, E, F, 4, weighted)
+                if msg == "diff":  # x_i: once per row (CSR), once per edge (COO)
+                    b += N * F * 4 if kernel == "csr" else E * F * 4
+                if aggr == "max":
+                    b += N * F * 8  # argmax
+                entry[f"{kernel}-{aggr}"] = rec(ms, b, E, F)
+        if ci == 3:
+            B = c["B"]
+            batch = torch.from_numpy(c["batch"]).to(dev)
+            h = pyg.propagate(x, csr=csr, aggr="sum")[0]
+            pooled = torch.empty((B, F), device=dev)
+            pam = torch.empty((B, F), dtype=torch.int64, device=dev)
+            for aggr in ("sum", "mean", "max"):
+                ms = timed(torch, lambda: pyg.global_pool(h, batch, B, aggr, out=pooled,
+                                                          argmax=pam if aggr == "max" else None), warm=50)
+                b = 8 * N + N * F * 4 + B * F * 4 + (B * F * 8 if aggr == "max" else 0)
+                entry[f"pool-{aggr}"] = {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9,
+                                         "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        res[name] = entry
+    return res
 
 
 def variants(pyg, torch, x, ei, csr, N, E, F, dev):

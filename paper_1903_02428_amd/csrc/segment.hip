@@ -30,6 +30,10 @@
 // the hint changes only the cache policy, never the result.
 #include "common.hpp"
 
+#ifndef PYG_MIN_CHUNKS
+#define PYG_MIN_CHUNKS 4096  // chunk halved (down to 16 slots) while there are fewer chunks than this
+#endif
+
 namespace pyg {
 namespace {
 
@@ -69,7 +73,10 @@ struct SegParams {
 // Measured on the large power-law graph (F = 128): fp32 rows (512 B) gain
 // 10 % with a 8-12 MB hot budget; bf16 rows (256 B) lose at every budget, so
 // the hint is used for rows of at least 512 B only.
-constexpr int64_t kLightMaxDegree = 8;           // mean row length up to which rows go to sub-groups
+#ifndef PYG_LIGHT_MAX_DEGREE
+#define PYG_LIGHT_MAX_DEGREE 16  // kNN rows of 16 slots gain 25 % as light rows
+#endif
+constexpr int64_t kLightMaxDegree = PYG_LIGHT_MAX_DEGREE;  // mean row length up to which rows go to sub-groups
 constexpr int64_t kHintMinBytes = 8ll << 20;     // x larger than twice an XCD's L2
 constexpr int64_t kHintMinRowBytes = 512;
 constexpr int64_t kHotBudgetBytes = 12ll << 20;  // hot rows kept cacheable
@@ -756,6 +763,9 @@ int64_t segment_chunk(int64_t E, int64_t n_rows, int64_t requested) {
         const int64_t avg = (E + n_rows - 1) / n_rows;
         c = 16;
         while (c < 16 * avg && c < 2048) c <<= 1;
+        // small graphs: enough wavefronts to fill the chip (long rows are
+        // left alone: smaller chunks only add pieces to fold)
+        while (c > 16 && E < c * (int64_t)PYG_MIN_CHUNKS) c >>= 1;
     } else {
         c = 64;
         while (c < 2048 && c * 32768 < E) c <<= 1;
