@@ -135,6 +135,65 @@ def test_c5_attention_sampled(pyg, c5, dev_graph):
     print("[c5] attention ok", flush=True)
 
 
+def test_c5_attention_backward_sampled(pyg, c5, dev_graph):
+    """The attention backward at the benchmark's shape (H = 8 heads of 16
+    columns, fp32, coefficients and score gradients in CSR slot order, the
+    reversed CSR and the transpose map as the benchmark builds them). The
+    transpose map is compared in full with the one the oracle's two CSR
+    permutations define; the gradients on sampled nodes (their whole
+    neighbourhoods taken into the oracle's sub-graph) and on every edge of
+    that sub-graph. Coefficients and score gradients come from the
+    counter-based generator, so that the oracle can regenerate the rows of
+    its sub-graph."""
+    from synth.hashed import hashed_matrix, hashed_values
+    ei_np, x_np, N = c5["edge_index_gcn"], c5["x"], c5["N"]
+    ei, _, csr = dev_graph
+    E, F, H = ei_np.shape[1], x_np.shape[1], 8
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E)
+    csr_t = pyg.coo_to_csr(pyg.reverse_edges(ei), N, chunk=csr.chunk)
+    map_t = pyg.csr_transpose_map(plain, csr_t)
+    _, _, perm = oracle.coo_to_csr(ei_np, N)
+    _, _, perm_t = oracle.coo_to_csr(np.ascontiguousarray(ei_np[::-1]), N)
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(E)
+    assert np.array_equal(map_t.cpu().numpy().astype(np.int64), inv[perm_t]), "C5 transpose map"
+    del perm_t
+    print("[c5] transpose map ok", flush=True)
+
+    rng = np.random.default_rng(79)
+    g = rng.standard_normal((N, F)).astype(np.float32)
+    a_src = rng.standard_normal((N, H)).astype(np.float32)
+    a_dst = rng.standard_normal((N, H)).astype(np.float32)
+    d_perm = to_dev(perm)
+    alpha = hashed_matrix(E, H, seed=23, device="cuda")[d_perm]   # row k of the generator = COO edge k
+    gsc = hashed_matrix(E, H, seed=29, device="cuda")[d_perm]
+    gx, galpha = pyg.propagate_heads_backward(to_dev(g), to_dev(x_np), plain, csr_t, alpha, H, map_t=map_t)
+    gxb, galphab = pyg.propagate_heads_backward(to_dev(g).to(torch.bfloat16), to_dev(x_np).to(torch.bfloat16), plain,
+                                                csr_t, alpha, H, map_t=map_t)
+    gs, gd = pyg.gat_scores_backward(to_dev(a_src), to_dev(a_dst), plain, csr_t, gsc, 0.2, map_t=map_t)
+    torch.cuda.synchronize()
+    del alpha, gsc
+    nodes = sample_rows(c5, n=300)[0]
+    keep = np.isin(ei_np[0], nodes) | np.isin(ei_np[1], nodes)  # whole out- and in-neighbourhoods
+    kidx = np.nonzero(keep)[0]
+    sub = np.ascontiguousarray(ei_np[:, keep])
+    al_sub = hashed_values(torch.from_numpy(kidx), H, seed=23).numpy()
+    gs_sub = hashed_values(torch.from_numpy(kidx), H, seed=29).numpy()
+    rx, ra, sx, sa = oracle.propagate_heads_backward(x_np, sub, al_sub, g, H)
+    check_sum(gx[to_dev(nodes)].cpu(), rx[nodes], sx[nodes], False, "C5 attention backward grad_x")
+    slots = inv[kidx]
+    check_sum(galpha[to_dev(slots)].cpu(), ra, sa, False, "C5 attention backward grad_alpha")
+    rxb, rab, sxb, sab = oracle.propagate_heads_backward(bf16_round(x_np), sub, al_sub, bf16_round(g), H)
+    check_sum(gxb[to_dev(nodes)].cpu(), rxb[nodes], sxb[nodes], True, "C5 attention backward grad_x bf16")
+    check_sum(galphab[to_dev(slots)].cpu(), rab, sab, False, "C5 attention backward grad_alpha bf16 inputs")
+    rs, rd, ss, sd = oracle.gat_scores_backward(a_src, a_dst, sub, gs_sub, 0.2)
+    check_sum(gs[to_dev(nodes)].cpu(), rs[nodes], ss[nodes], False, "C5 score backward grad_a_src")
+    check_sum(gd[to_dev(nodes)].cpu(), rd[nodes], sd[nodes], False, "C5 score backward grad_a_dst")
+    print("[c5] attention backward ok", flush=True)
+    del csr_t, map_t, gx, galpha, gxb, galphab
+    torch.cuda.empty_cache()
+
+
 def test_c5_edge_features_sampled(pyg, c5, dev_graph):
     """Edge-feature messages at the benchmark's shape: every edge of the large
     graph carries a 128-dimensional feature (counter-based, regenerable for
