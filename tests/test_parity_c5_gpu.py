@@ -132,7 +132,70 @@ def test_c5_attention_sampled(pyg, c5, dev_graph):
     ref_out, sabs = oracle.propagate_heads(x_np, sub, ref.astype(np.float32), H)
     g = out[to_dev(rows)].cpu().numpy().astype(np.float64)
     assert np.all(np.abs(g - ref_out[rows]) <= 2e-5 * sabs[rows] + 1e-6), "C5 propagate_heads"
+    # the attention sum in bf16 storage with the GPU's coefficients' own oracle (alpha from the oracle, fp32)
+    alpha_ref = torch.zeros(csr.E, H)
+    alpha_ref[torch.from_numpy(slots)] = torch.from_numpy(ref[order].astype(np.float32))
+    outb = pyg.propagate_heads(to_dev(x_np).to(torch.bfloat16), plain, alpha_ref.to("cuda"), H)
+    torch.cuda.synchronize()
+    ref_b, sabs_b = oracle.propagate_heads(bf16_round(x_np), sub, ref.astype(np.float32), H)
+    check_sum(outb[to_dev(rows)].cpu(), ref_b[rows], sabs_b[rows], True, "C5 propagate_heads bf16")
     print("[c5] attention ok", flush=True)
+
+
+def test_c5_softmax_scores_sampled(pyg, c5, dev_graph):
+    """The softmax of given scores and its backward at the benchmark's shape
+    (H = 8, CSR slot order): every edge into the sampled rows. Scores,
+    coefficients and upstream gradients from the counter-based generator
+    (row k = COO edge k)."""
+    from synth.hashed import hashed_matrix, hashed_values
+    from tests.parity import check_softmax
+    ei_np, N = c5["edge_index_gcn"], c5["N"]
+    _, _, csr = dev_graph
+    E, H = ei_np.shape[1], 8
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E)
+    d_perm = csr.perm
+    sc = hashed_matrix(E, H, seed=31, device="cuda")[d_perm] * 4.0
+    al = hashed_matrix(E, H, seed=37, device="cuda")[d_perm] * 0.5 + 0.5
+    gg = hashed_matrix(E, H, seed=41, device="cuda")[d_perm]
+    alpha = pyg.segment_softmax(sc, plain, "csr")
+    gsc = pyg.segment_softmax_backward(al, gg, plain, "csr")
+    torch.cuda.synchronize()
+    del sc, al, gg
+    rows, keep = sample_rows(c5, n=400)
+    kidx = np.nonzero(keep)[0]
+    sub = np.ascontiguousarray(ei_np[:, keep])
+    rowptr = np.concatenate([[0], np.cumsum(np.bincount(ei_np[1], minlength=N))])
+    order = np.argsort(sub[1], kind="stable")
+    dst_sorted = sub[1][order]
+    first = np.searchsorted(dst_sorted, dst_sorted)
+    slots = rowptr[dst_sorted] + (np.arange(order.size) - first)
+    s_sub = hashed_values(torch.from_numpy(kidx), H, seed=31).numpy() * np.float32(4.0)
+    ref = oracle.segment_softmax(s_sub, sub, N)
+    check_softmax(alpha[to_dev(slots)].cpu(), ref[order], s_sub[order], dst_sorted, N, "C5 segment_softmax")
+    a_sub = hashed_values(torch.from_numpy(kidx), H, seed=37).numpy() * np.float32(0.5) + np.float32(0.5)
+    g_sub = hashed_values(torch.from_numpy(kidx), H, seed=41).numpy()
+    rb, sabs = oracle.segment_softmax_backward(a_sub, g_sub, sub, N)
+    err = np.abs(gsc[to_dev(slots)].cpu().numpy().astype(np.float64) - rb[order])
+    assert np.all(err <= 1e-5 * sabs[order] + 1e-12), f"C5 softmax backward: {np.max(err / (1e-5 * sabs[order] + 1e-12))}"
+    print("[c5] softmax of scores and backward ok", flush=True)
+    del alpha, gsc
+    torch.cuda.empty_cache()
+
+
+def test_c5_whole_graph_pool(pyg, c5):
+    """The benchmark's readout shape: one graph of all 232,965 nodes, F = 128,
+    mean (also sum and max), over the graph's features."""
+    x_np, N = c5["x"], c5["N"]
+    batch = np.zeros(N, dtype=np.int64)
+    for aggr in ("mean", "sum", "max"):
+        out, arg = pyg.global_pool(to_dev(x_np), to_dev(batch), 1, aggr)
+        torch.cuda.synchronize()
+        ref, rarg, sabs = oracle.global_pool(x_np, batch, 1, aggr)
+        if aggr == "max":
+            check_max(out, arg, ref, rarg, what="C5 pool max")
+        else:
+            check_sum(out, ref, sabs, False, f"C5 pool {aggr}")
+    print("[c5] whole-graph pool ok", flush=True)
 
 
 def test_c5_attention_backward_sampled(pyg, c5, dev_graph):
