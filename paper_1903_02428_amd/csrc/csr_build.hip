@@ -37,12 +37,16 @@ namespace {
 #define PYG_RADIX_BITS 7  // 18-bit ids: three 6-bit passes, whose 64-key runs write whole lines
 #endif
 constexpr int kItems = PYG_RADIX_ITEMS;                     // keys per thread per tile
+#ifndef PYG_SORT_THREADS
+#define PYG_SORT_THREADS 256
+#endif
+constexpr int kSortBlock = PYG_SORT_THREADS;                // threads per tile of the radix kernels
 constexpr int kWaveKeys = kWave * kItems;                   // keys ranked by one wavefront
-constexpr int64_t kTile = (int64_t)kBlock * kItems;         // keys per tile
+constexpr int64_t kTile = (int64_t)kSortBlock * kItems;     // keys per tile
 constexpr int kMaxDigitBits = PYG_RADIX_BITS;               // widest digit of one pass
 static_assert(kTile <= 65536, "tile-local indices are staged as 16-bit");
 constexpr int kMaxRadix = 1 << kMaxDigitBits;
-constexpr int kWaves = kBlock / kWave;
+constexpr int kWaves = kSortBlock / kWave;
 
 // ------------------------------------------------------------------ degree
 
@@ -156,26 +160,26 @@ struct Payload {  // one sort buffer: key plus carried fields
     float *w;
 };
 
-__global__ __launch_bounds__(kBlock) void k_radix_hist(const int64_t *__restrict__ dst64, const uint32_t *__restrict__ keys,
+__global__ __launch_bounds__(kSortBlock) void k_radix_hist(const int64_t *__restrict__ dst64, const uint32_t *__restrict__ keys,
                                                        int64_t E, int shift, int bits, int64_t ntiles,
                                                        uint32_t *__restrict__ hist) {
     __shared__ uint32_t h[kMaxRadix];
     const int radix = 1 << bits;
     const uint32_t mask = radix - 1;
-    for (int i = threadIdx.x; i < radix; i += kBlock) h[i] = 0;
+    for (int i = threadIdx.x; i < radix; i += kSortBlock) h[i] = 0;
     __syncthreads();
     const int64_t tile = blockIdx.x;
     const int64_t base = tile * kTile + threadIdx.x;
 #pragma unroll 4
     for (int r = 0; r < kItems; ++r) {
-        const int64_t i = base + (int64_t)r * kBlock;
+        const int64_t i = base + (int64_t)r * kSortBlock;
         if (i < E) {
             const uint32_t key = dst64 ? static_cast<uint32_t>(dst64[i]) : keys[i];
             atomicAdd(&h[(key >> shift) & mask], 1u);
         }
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < radix; i += kBlock) hist[(int64_t)i * ntiles + tile] = h[i];
+    for (int i = threadIdx.x; i < radix; i += kSortBlock) hist[(int64_t)i * ntiles + tile] = h[i];
 }
 
 // Stable rank of one tile's elements by digit. dig[r] is the digit of the
@@ -217,7 +221,7 @@ __device__ __forceinline__ void rank_tile(const uint32_t (&dig)[kItems], uint32_
     __syncthreads();
 
     // per digit, prefix over waves; then the tile start of each digit run
-    for (int t = threadIdx.x; t < radix; t += kBlock) {
+    for (int t = threadIdx.x; t < radix; t += kSortBlock) {
         uint32_t acc = 0;
 #pragma unroll
         for (int wv = 0; wv < kWaves; ++wv) {
@@ -254,7 +258,7 @@ __device__ __forceinline__ void rank_tile(const uint32_t (&dig)[kItems], uint32_
         }
     }
     __syncthreads();
-    for (int t = threadIdx.x; t < radix; t += kBlock)
+    for (int t = threadIdx.x; t < radix; t += kSortBlock)
         gbase[t] = (int64_t)offsets[(int64_t)t * ntiles + tile] - (int64_t)start[t];
 #pragma unroll
     for (int r = 0; r < kItems; ++r)
@@ -266,7 +270,7 @@ __device__ __forceinline__ void rank_tile(const uint32_t (&dig)[kItems], uint32_
 // Every global read is coalesced: each field (key, edge id, source, weight)
 // is loaded in tile order, scattered into LDS in sorted order, and written
 // out run by run, so no pass gathers from global memory.
-__global__ __launch_bounds__(kBlock) void k_radix_scatter(
+__global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64, const float *__restrict__ w_in,
     Payload in, Payload out, int64_t *__restrict__ perm, int32_t *__restrict__ col, float *__restrict__ wcsr,
     int64_t E, int shift, int bits, int64_t ntiles, const uint32_t *__restrict__ offsets, int last) {
@@ -302,7 +306,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
         }
     __syncthreads();
     uint32_t *key_out = out.key;
-    for (int64_t j = threadIdx.x; j < tlen; j += kBlock) {
+    for (int64_t j = threadIdx.x; j < tlen; j += kSortBlock) {
         const int64_t pos = gbase[sdig[j]] + j;
         if (pos >= 0 && pos < E) key_out[pos] = stage[j];  // bounds hold for a consistent ranking
     }
@@ -327,7 +331,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter(
         for (int r = 0; r < kItems; ++r)
             if (dig[r] != 0xFFFFFFFFu && slot[r] < kTile) stage[slot[r]] = v[r];
         __syncthreads();
-        for (int64_t j = threadIdx.x; j < tlen; j += kBlock) {
+        for (int64_t j = threadIdx.x; j < tlen; j += kSortBlock) {
             const int64_t pos = gbase[sdig[j]] + j;
             if (pos < 0 || pos >= E) continue;
             const uint32_t x = stage[j];
@@ -370,20 +374,20 @@ __device__ __forceinline__ uint64_t pack_edge(const int64_t *__restrict__ dst64,
 
 // Digit counts per tile (digit-major) of the packed elements; pass 0 packs
 // from the COO itself.
-__global__ __launch_bounds__(kBlock) void k_radix_hist64(const int64_t *__restrict__ dst64,
+__global__ __launch_bounds__(kSortBlock) void k_radix_hist64(const int64_t *__restrict__ dst64,
                                                          const uint64_t *__restrict__ keys, int64_t E, int shift,
                                                          int bits, int64_t ntiles, Packing pk,
                                                          uint32_t *__restrict__ hist) {
     __shared__ uint32_t h[kMaxRadixP];
     const int radix = 1 << bits;
     const uint64_t mask = radix - 1;
-    for (int i = threadIdx.x; i < radix; i += kBlock) h[i] = 0;
+    for (int i = threadIdx.x; i < radix; i += kSortBlock) h[i] = 0;
     __syncthreads();
     const int64_t tile = blockIdx.x;
     const int64_t base = tile * kTile + threadIdx.x;
 #pragma unroll 4
     for (int r = 0; r < kItems; ++r) {
-        const int64_t i = base + (int64_t)r * kBlock;
+        const int64_t i = base + (int64_t)r * kSortBlock;
         if (i < E) {
             const uint64_t d = dst64 ? (static_cast<uint64_t>(dst64[i]) >> shift)
                                      : (keys[i] >> (pk.nb + pk.ib + shift));
@@ -391,13 +395,13 @@ __global__ __launch_bounds__(kBlock) void k_radix_hist64(const int64_t *__restri
         }
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < radix; i += kBlock) hist[(int64_t)i * ntiles + tile] = h[i];
+    for (int i = threadIdx.x; i < radix; i += kSortBlock) hist[(int64_t)i * ntiles + tile] = h[i];
 }
 
 // One stable scatter pass over packed elements (same tile order and ranking
 // as k_radix_scatter). The last pass unpacks into perm, col and the sorted
 // target ids.
-__global__ __launch_bounds__(kBlock) void k_radix_scatter64(
+__global__ __launch_bounds__(kSortBlock) void k_radix_scatter64(
     const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64, const float *__restrict__ w_in,
     const uint64_t *__restrict__ in, const float *__restrict__ in_w, uint64_t *__restrict__ out,
     float *__restrict__ out_w, int64_t *__restrict__ perm, int32_t *__restrict__ col, float *__restrict__ wcsr,
@@ -434,7 +438,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter64(
         }
     __syncthreads();
     const uint64_t idmask = (1ull << pk.ib) - 1, nodemask = (1ull << pk.nb) - 1;
-    for (int64_t j = threadIdx.x; j < tlen; j += kBlock) {
+    for (int64_t j = threadIdx.x; j < tlen; j += kSortBlock) {
         const int64_t pos = gbase[sdig[j]] + j;
         if (pos < 0 || pos >= E) continue;  // bounds hold for a consistent ranking
         const uint64_t e = stage[j];
@@ -457,7 +461,7 @@ __global__ __launch_bounds__(kBlock) void k_radix_scatter64(
             stage32[slot[r]] = __float_as_uint(dst64 ? w_in[i] : in_w[i]);
     }
     __syncthreads();
-    for (int64_t j = threadIdx.x; j < tlen; j += kBlock) {
+    for (int64_t j = threadIdx.x; j < tlen; j += kSortBlock) {
         const int64_t pos = gbase[sdig[j]] + j;
         if (pos < 0 || pos >= E) continue;
         const float w = __uint_as_float(stage32[j]);
@@ -662,13 +666,13 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
             const int bits = (pk.nb - shift) < pbpp ? (pk.nb - shift) : pbpp;
             const bool last = p == ppasses - 1;
             const int64_t nhist = ntiles << bits;
-            k_radix_hist64<<<(unsigned)ntiles, kBlock, 0, s>>>(p == 0 ? dst : nullptr, pin, E, shift, bits, ntiles, pk,
+            k_radix_hist64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, pin, E, shift, bits, ntiles, pk,
                                                              w.hist);
             PYG_LAUNCH_CHECK();
             PYG_TRY(scan_u32(w.hist, w.hist, nhist, false, w.hist_scan, s));
             uint64_t *pout = last ? nullptr : w.pbuf[p & 1];
             float *pout_w = last ? nullptr : w.pw[p & 1];
-            k_radix_scatter64<<<(unsigned)ntiles, kBlock, 0, s>>>(p == 0 ? dst : nullptr, src, edge_weight, pin, pin_w,
+            k_radix_scatter64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, src, edge_weight, pin, pin_w,
                                                                 pout, pout_w, perm, col, weight_csr, w.sorted_key, E,
                                                                 shift, bits, ntiles, w.hist, last ? 1 : 0, pk);
             PYG_LAUNCH_CHECK();
@@ -688,12 +692,12 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
         const int bits = (nb - shift) < bpp ? (nb - shift) : bpp;
         const bool last = p == passes - 1;
         const int64_t nhist = ntiles << bits;
-        k_radix_hist<<<(unsigned)ntiles, kBlock, 0, s>>>(p == 0 ? dst : nullptr, in.key, E, shift, bits, ntiles, w.hist);
+        k_radix_hist<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, in.key, E, shift, bits, ntiles, w.hist);
         PYG_LAUNCH_CHECK();
         PYG_TRY(scan_u32(w.hist, w.hist, nhist, false, w.hist_scan, s));
         Payload out = last ? none : w.buf[p & 1];
         if (last) out.key = w.sorted_key;
-        k_radix_scatter<<<(unsigned)ntiles, kBlock, 0, s>>>(p == 0 ? dst : nullptr, src, edge_weight, in, out, perm,
+        k_radix_scatter<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, src, edge_weight, in, out, perm,
                                                            col, weight_csr, E, shift, bits, ntiles, w.hist, last ? 1 : 0);
         PYG_LAUNCH_CHECK();
         in = out;
