@@ -101,13 +101,6 @@ typedef struct {
     int64_t chunk;
 } pyg_csr;
 
-/* In-degree from a CSR built by pyg_coo_to_csr: deg[i] = rowptr[i+1] -
- * rowptr[i], the same counts as pyg_degree on the edge list the CSR was
- * built from (its rows are the targets), read off the row boundaries the
- * sort produced instead of counting the edge list again. deg int64 [N]
- * (device, output). Errors: PYG_ERR_INVALID_ARG (NULL csr/rowptr/deg). */
-int pyg_degree_csr(const pyg_csr *csr, int64_t *deg, void *stream);
-
 /* Human-readable text for a status code (static storage, never NULL). */
 const char *pyg_strerror(int status);
 
@@ -120,9 +113,20 @@ int pyg_degree_workspace(int64_t E, int64_t N, size_t *bytes);
 /* In-degree deg[i] = number of edges whose target is i, counted with
  * multiplicity (|N(i)| in Eq. (1); the denominator of mean).
  *   edge_index int64 [2,E] (device), deg int64 [N] (device, output).
- * Counted in on-chip histograms over slices of the node range; exact. */
+ * Counted in on-chip histograms over slices of the node range; exact.
+ * Errors: PYG_ERR_INVALID_ARG (negative sizes, NULL arrays, E > 0 with
+ * N = 0), PYG_ERR_UNSUPPORTED (N or E >= 2^31), PYG_ERR_WORKSPACE. */
 int pyg_degree(const int64_t *edge_index, int64_t E, int64_t N, int64_t *deg, void *ws, size_t ws_bytes,
                void *stream);
+
+/* In-degree (|N(i)| in Eq. (1)) from a CSR built by pyg_coo_to_csr:
+ * deg[i] = rowptr[i+1] - rowptr[i], the same counts as pyg_degree on the
+ * edge list the CSR was built from (its rows are the targets), read off the
+ * row boundaries the sort produced instead of counting the edge list again.
+ *   csr  read: rowptr and N only;  deg  int64 [N] (device, output).
+ * Errors: PYG_ERR_INVALID_ARG (NULL csr or rowptr, N < 0, NULL deg with
+ * N > 0). */
+int pyg_degree_csr(const pyg_csr *csr, int64_t *deg, void *stream);
 
 /* Workspace bytes needed by pyg_coo_to_csr for (E, N). */
 int pyg_coo_to_csr_workspace(int64_t E, int64_t N, size_t *bytes);
@@ -137,14 +141,19 @@ int pyg_coo_to_csr_workspace(int64_t E, int64_t N, size_t *bytes);
  *   col         int32 [E]          output;
  *   perm        int64 [E]          output;
  *   weight_csr  fp32 [E] or NULL   output, = edge_weight[perm] (requires
- *                                  edge_weight, ignored when it is NULL). */
+ *                                  edge_weight, ignored when it is NULL).
+ * Errors: PYG_ERR_INVALID_ARG (negative sizes, NULL rowptr, or NULL
+ * edge_index/col/perm or N = 0 when E > 0), PYG_ERR_UNSUPPORTED (N or
+ * E >= 2^31), PYG_ERR_WORKSPACE. */
 int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, const float *edge_weight,
                    int64_t *rowptr, int32_t *col, int64_t *perm, float *weight_csr,
                    void *ws, size_t ws_bytes, void *stream);
 
 /* CSR-ordered copy of a COO-ordered edge array: out[p] = in[perm[p]] for
  * p < E, with perm from pyg_coo_to_csr (e.g. fresh edge weights for an
- * existing CSR). in and out are fp32 [E] device arrays and must differ. */
+ * existing CSR). in and out are fp32 [E] device arrays and must differ.
+ * Errors: PYG_ERR_INVALID_ARG (E < 0, NULL arrays, in == out),
+ * PYG_ERR_UNSUPPORTED (E >= 2^31). */
 int pyg_gather_edges(const int64_t *perm, int64_t E, const float *in, float *out, void *stream);
 
 /* Workspace bytes needed by pyg_gcn_norm for (E, N). */
@@ -158,7 +167,10 @@ int pyg_gcn_norm_workspace(int64_t E, int64_t N, size_t *bytes);
  *   deg  int64 [N] or NULL: the in-degree of this edge list as returned by
  *        pyg_degree, reused instead of counting again; read only when
  *        edge_weight is NULL (weighted degrees are always summed here);
- *   norm fp32 [E] output in COO order. */
+ *   norm fp32 [E] output in COO order.
+ * Errors: PYG_ERR_INVALID_ARG (negative sizes, NULL edge_index/norm or
+ * N = 0 when E > 0), PYG_ERR_UNSUPPORTED (N or E >= 2^31),
+ * PYG_ERR_WORKSPACE. */
 int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight, int64_t E, int64_t N,
                  const int64_t *deg, float *norm, void *ws, size_t ws_bytes, void *stream);
 
@@ -172,7 +184,10 @@ int pyg_gcn_norm_csr_workspace(int64_t N, size_t *bytes);
  * Equal to pyg_gcn_norm's output gathered through csr->perm: bit for bit
  * with unit weights; with weights the fp64 degree sums are ordered per row
  * (deterministic) and may differ from another order by one fp32 ulp.
- *   norm_csr fp32 [E] output (device). */
+ *   norm_csr fp32 [E] output (device).
+ * Errors: PYG_ERR_INVALID_ARG (NULL csr/rowptr, negative sizes, NULL
+ * col/norm_csr or N = 0 when E > 0), PYG_ERR_UNSUPPORTED (N or E >= 2^31),
+ * PYG_ERR_WORKSPACE. */
 int pyg_gcn_norm_csr(const pyg_csr *csr, float *norm_csr, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_propagate for this shape, aggregation and
@@ -200,7 +215,12 @@ int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr
  * as +0.0; equal maxima resolve to the lowest edge id. Max, argmax and every
  * CSR result are bit-reproducible; COO sum/mean use float atomics and may
  * differ in the last bits between runs (Appendix A notes the same of GPU
- * scatter). `out` must not overlap `x`. */
+ * scatter). `out` must not overlap `x`.
+ * Errors: PYG_ERR_INVALID_ARG (bad dtype/msg/aggr/kernel, negative
+ * sizes, NULL arrays, argmax given without max or missing with it, a weight
+ * with difference messages, out overlapping x, a CSR that does not match
+ * N, E or the weights, CSR_SEGMENT without a CSR), PYG_ERR_UNSUPPORTED (N or
+ * E >= 2^31), PYG_ERR_WORKSPACE. */
 int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F,
                   const int64_t *edge_index, int64_t E, const float *edge_weight,
                   const pyg_csr *csr, int msg, int aggr, int kernel,
@@ -220,7 +240,9 @@ int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F,
  *              kernel ignores csr->weight here;
  *   other arguments, the workspace (pyg_propagate_workspace), outputs,
  *   argmax, tie and -0.0 rules as in pyg_propagate. Messages are formed in
- *   fp32 (one add or multiply, then max(., 0) for _RELU); max compares them. */
+ *   fp32 (one add or multiply, then max(., 0) for _RELU); max compares them.
+ * Errors: as pyg_propagate, plus PYG_ERR_INVALID_ARG for a message other
+ * than the three edge messages, a bad attr_order, or NULL edge_attr. */
 int pyg_propagate_edge(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
                        const void *edge_attr, int attr_order, const pyg_csr *csr, int msg, int aggr, int kernel,
                        void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
@@ -275,7 +297,10 @@ int pyg_segment_softmax_workspace(int64_t E, int64_t N, int64_t H, int64_t chunk
  *   alpha[k,h] = exp(s[k,h] - m[i,h]) / sum_{k' -> i} exp(s[k',h] - m[i,h]),
  *   m[i,h] = max_{k' -> i} s[k',h],  i = target of edge k.
  * scores and alpha fp32 [E, H] (device), may not overlap. fp32 arithmetic:
- * one online max/sum pass and one normalising pass. */
+ * one online max/sum pass and one normalising pass.
+ * Errors: PYG_ERR_INVALID_ARG (NULL or inconsistent csr, H <= 0, NULL
+ * arrays, bad order, COO order without csr->perm), PYG_ERR_UNSUPPORTED (N or
+ * E >= 2^31), PYG_ERR_WORKSPACE. */
 int pyg_segment_softmax(const float *scores, int64_t H, const pyg_csr *csr, int order, float *alpha,
                         void *ws, size_t ws_bytes, void *stream);
 
@@ -283,7 +308,9 @@ int pyg_segment_softmax(const float *scores, int64_t H, const pyg_csr *csr, int 
  * scores e[k,h] = LeakyReLU(a_src[j,h] + a_dst[i,h]) for edge k = (j -> i),
  * LeakyReLU(v) = v for v >= 0 and negative_slope * v otherwise, computed on
  * the fly (never stored). a_src, a_dst fp32 [N, H] (device): the per-node
- * halves of GAT's attention vector applied to the transformed features. */
+ * halves of GAT's attention vector applied to the transformed features.
+ * Errors: as pyg_segment_softmax, plus PYG_ERR_INVALID_ARG for a
+ * non-finite negative_slope. */
 int pyg_gat_softmax(const float *a_src, const float *a_dst, int64_t H, float negative_slope, const pyg_csr *csr,
                     int order, float *alpha, void *ws, size_t ws_bytes, void *stream);
 
@@ -291,7 +318,8 @@ int pyg_gat_softmax(const float *a_src, const float *a_dst, int64_t H, float neg
  * gradient g = dL/d alpha:
  *   grad_scores[k,h] = alpha[k,h] * (g[k,h] - sum_{k' -> i} alpha[k',h] g[k',h]).
  * alpha, grad_alpha, grad_scores fp32 [E, H] (device); grad_scores may not
- * overlap the inputs. */
+ * overlap the inputs.
+ * Errors: as pyg_segment_softmax. */
 int pyg_segment_softmax_backward(const float *alpha, const float *grad_alpha, int64_t H, const pyg_csr *csr,
                                  int order, float *grad_scores, void *ws, size_t ws_bytes, void *stream);
 
@@ -306,7 +334,10 @@ int pyg_propagate_heads_workspace(int dtype, int64_t N, int64_t H, int64_t C, in
  *   x, out  [N, H*C] fp32 or bf16 (dtype), fp32 accumulation; rows take the
  *           16-byte vector path when C * sizeof(dtype) % 16 == 0;
  *   alpha   fp32 [E, H] in CSR slot order (PYG_ORDER_CSR); csr->weight is ignored.
- * Deterministic, same kernel and work split as pyg_propagate's CSR path. */
+ * Deterministic, same kernel and work split as pyg_propagate's CSR path.
+ * Errors: PYG_ERR_INVALID_ARG (bad dtype, H <= 0, C < 0, NULL or
+ * mismatched csr, NULL arrays, out overlapping x or alpha),
+ * PYG_ERR_UNSUPPORTED (N, E or H*C >= 2^31), PYG_ERR_WORKSPACE. */
 int pyg_propagate_heads(const void *x, int dtype, int64_t N, int64_t H, int64_t C, const pyg_csr *csr,
                         const float *alpha, void *out, void *ws, size_t ws_bytes, void *stream);
 
@@ -393,15 +424,22 @@ int pyg_global_pool_workspace(int dtype, int64_t N, int64_t F, int64_t B, int ag
  * x[n, f], for B graphs.
  *   batch int64 [N], non-decreasing, values in [0, B);
  *   out   [B,F] in x's dtype; argmax int64 [B,F] (PYG_MAX only): node id,
- *         N for an empty graph. */
+ *         N for an empty graph.
+ * Errors: PYG_ERR_INVALID_ARG (bad dtype/aggr, negative sizes, NULL
+ * arrays, argmax given without max or missing with it, B = 0 with nodes,
+ * out overlapping x), PYG_ERR_UNSUPPORTED (N or B >= 2^31),
+ * PYG_ERR_WORKSPACE. */
 int pyg_global_pool(const void *x, int dtype, int64_t N, int64_t F, const int64_t *batch, int64_t B,
                     int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
 
-/* Count COO entries outside [0, N) into *bad_count (int64, device). */
+/* Count COO entries outside [0, N) into *bad_count (int64, device).
+ * Errors: PYG_ERR_INVALID_ARG (negative sizes, NULL bad_count or
+ * edge_index). */
 int pyg_validate_coo(const int64_t *edge_index, int64_t E, int64_t N, int64_t *bad_count, void *stream);
 
 /* Count batch entries outside [0, B) or smaller than their predecessor into
- * *bad_count (int64, device). */
+ * *bad_count (int64, device).
+ * Errors: PYG_ERR_INVALID_ARG (negative sizes, NULL bad_count or batch). */
 int pyg_validate_batch(const int64_t *batch, int64_t N, int64_t B, int64_t *bad_count, void *stream);
 
 #ifdef __cplusplus
