@@ -42,14 +42,19 @@ def test_dense_transform(pyg, out_dtype):
 def test_dense_transform_unaligned_rows(pyg):
     """A view whose rows start off a 16-byte boundary takes the scalar path."""
     rng = np.random.default_rng(9)
-    base = to_dev(bf16_round(rng.standard_normal((301, 65)).astype(np.float32))).to(torch.bfloat16)
+    base_np = bf16_round(rng.standard_normal((301, 65)).astype(np.float32))
+    t_np = bf16_round(rng.standard_normal((64, 32)).astype(np.float32) / 8)
+    base = to_dev(base_np).to(torch.bfloat16)
     x = base[:, 1:].contiguous()[:, :64]  # contiguous copy, aligned
     xo = base.view(-1)[1:1 + 300 * 64].view(300, 64)  # offset by 2 bytes
-    t = to_dev(bf16_round(rng.standard_normal((64, 32)).astype(np.float32) / 8)).to(torch.bfloat16)
-    for xx in (x[:300], xo):
+    t = to_dev(t_np).to(torch.bfloat16)
+    # the same values on the host, for the oracle
+    x_np = np.ascontiguousarray(base_np[:300, 1:65])
+    xo_np = base_np.reshape(-1)[1:1 + 300 * 64].reshape(300, 64)
+    for xx, xh in ((x[:300], x_np), (xo, xo_np)):
         got = pyg.dense_transform(xx, t)
         torch.cuda.synchronize()
-        ref, sabs = oracle.dense_transform(xx.float().cpu().numpy(), t.float().cpu().numpy())
+        ref, sabs = oracle.dense_transform(xh, t_np)
         check_sum(got, ref, sabs, False, "dense unaligned")
 
 
