@@ -60,6 +60,7 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
     lib.oracle_propagate.argtypes = [p, i64, i64, p, i64, p, p, i32, i32, p, p, p]
     lib.oracle_global_pool.argtypes = [p, i64, i64, p, i64, i32, p, p, p]
     lib.oracle_propagate_backward.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p, p, p, p]
+    lib.oracle_propagate_edge_backward.argtypes = [p, i64, i64, p, i64, p, i32, i32, p, p, p, p, p, p]
     lib.oracle_gat_scores.argtypes = [p, p, i64, i64, p, i64, ctypes.c_float, p]
     lib.oracle_segment_softmax.argtypes = [p, i64, i64, p, i64, p]
     lib.oracle_segment_softmax_backward.argtypes = [p, p, i64, i64, p, i64, p, p]
@@ -186,6 +187,36 @@ def propagate_backward(x, edge_index, grad_out, edge_weight=None, msg: str = "sr
     _check(lib.oracle_propagate_backward(_ptr(x), N, F, _ptr(ei), E, _ptr(w), MSG[msg], AGGR[aggr], _ptr(g),
                                          _ptr(arg), _ptr(gx), _ptr(gw), _ptr(sx), _ptr(sw)), "propagate_backward")
     return gx, gw, sx, sw
+
+
+def propagate_edge_backward(x, edge_index, edge_attr, grad_out, msg: str, aggr: str = "sum", argmax=None,
+                            want_grad_x: bool = True, want_grad_e: bool = True, lib=None):
+    """Gradient of propagate with an edge-feature message ("edge_add",
+    "edge_relu", "edge_mul") with respect to x and to the edge features
+    (COO edge order). argmax is the forward's (max only). Returns (grad_x fp64
+    [N,F] or None, grad_e fp64 [E,F] or None, sabs_x, sabs_e)."""
+    lib = lib or load()
+    if msg not in ("edge_add", "edge_relu", "edge_mul"):
+        raise ValueError("msg must be an edge-feature message")
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    N, F = x.shape
+    g = np.ascontiguousarray(grad_out, dtype=np.float32)
+    if g.shape != (N, F):
+        raise ValueError("grad_out must be [N, F]")
+    ei = _ei(edge_index)
+    E = ei.shape[1]
+    ea = np.ascontiguousarray(edge_attr, dtype=np.float32)
+    if ea.shape != (E, F):
+        raise ValueError("edge_attr must be [E, F]")
+    arg = None if argmax is None else np.ascontiguousarray(argmax, dtype=np.int64)
+    gx = np.empty((N, F), np.float64) if want_grad_x else None
+    sx = np.empty((N, F), np.float64) if want_grad_x else None
+    ge = np.empty((E, F), np.float64) if want_grad_e else None
+    se = np.empty((E, F), np.float64) if want_grad_e else None
+    _check(lib.oracle_propagate_edge_backward(_ptr(x), N, F, _ptr(ei), E, _ptr(ea), MSG[msg], AGGR[aggr], _ptr(g),
+                                              _ptr(arg), _ptr(gx), _ptr(ge), _ptr(sx), _ptr(se)),
+           "propagate_edge_backward")
+    return gx, ge, sx, se
 
 
 def _scores2d(a, E: int, name: str, dtype=np.float32) -> np.ndarray:

@@ -332,6 +332,84 @@ int oracle_propagate_backward(const float *x, int64_t N, int64_t F, const int64_
     return ORACLE_OK;
 }
 
+/* Gradient of oracle_propagate with the edge-feature messages (Eq. (1) with
+ * F-dimensional e_{j,i}; phi = x_j + e, max(x_j + e, 0) or x_j * e,
+ * elementwise) for g = dL/d out [N,F]. Each edge k = (j -> i) receives
+ * d_k = s_i g_i (sum: s_i = 1, mean: s_i = 1/deg_i), or, for max, g_{i,f}
+ * in the columns f where k is the forward's argmax[i,f] and 0 elsewhere;
+ * then by the chain rule through phi:
+ *   x_j + e:          grad_x[j] += d_k,             grad_e[k] = d_k;
+ *   max(x_j + e, 0):  both times [x_j + e_k > 0] (the sign of the exact sum;
+ *                     a message that is exactly 0 passes nothing);
+ *   x_j * e:          grad_x[j] += d_k * e_k,       grad_e[k] = d_k * x_j.
+ * grad_x fp64 [N,F], grad_e fp64 [E,F] in edge order (either may be NULL,
+ * not both); sabs_x / sabs_e (nullable) hold the sum of |terms|. */
+int oracle_propagate_edge_backward(const float *x, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                                   const float *ea, int msg, int aggr, const float *grad_out,
+                                   const int64_t *argmax, double *grad_x, double *grad_e, double *sabs_x,
+                                   double *sabs_e) {
+    if (N < 0 || F < 0 || E < 0) return ORACLE_ERR_ARG;
+    if (msg != ORACLE_MSG_EDGE_ADD && msg != ORACLE_MSG_EDGE_RELU && msg != ORACLE_MSG_EDGE_MUL) return ORACLE_ERR_ARG;
+    if (aggr != ORACLE_SUM && aggr != ORACLE_MEAN && aggr != ORACLE_MAX) return ORACLE_ERR_ARG;
+    if (!grad_x && !grad_e) return ORACLE_ERR_ARG;
+    if (N * F > 0 && (!x || !grad_out)) return ORACLE_ERR_ARG;
+    if (E * F > 0 && !ea) return ORACLE_ERR_ARG;
+    if (aggr == ORACLE_MAX && N * F > 0 && !argmax) return ORACLE_ERR_ARG;
+    if (E > 0 && !edge_index) return ORACLE_ERR_ARG;
+    const int64_t *src = edge_index;
+    const int64_t *dst = edge_index + E;
+    if (check_index_range(src, E, N) || check_index_range(dst, E, N)) return ORACLE_ERR_INDEX;
+    if (!all_finite(x, N * F) || !all_finite(grad_out, N * F) || !all_finite(ea, E * F)) return ORACLE_ERR_NONFINITE;
+    for (int64_t t = 0; grad_x && t < N * F; ++t) {
+        grad_x[t] = 0.0;
+        if (sabs_x) sabs_x[t] = 0.0;
+    }
+    for (int64_t t = 0; grad_e && t < E * F; ++t) {
+        grad_e[t] = 0.0;
+        if (sabs_e) sabs_e[t] = 0.0;
+    }
+    int64_t *deg = (int64_t *)calloc((size_t)(N > 0 ? N : 1), sizeof(int64_t));
+    if (!deg) return ORACLE_ERR_ARG;
+    for (int64_t k = 0; k < E; ++k) deg[dst[k]] += 1;
+    for (int64_t k = 0; k < E; ++k) {
+        const int64_t j = src[k], i = dst[k];
+        for (int64_t f = 0; f < F; ++f) {
+            double d;
+            if (aggr == ORACLE_MAX) {
+                const int64_t a = argmax[i * F + f];
+                if (a < 0 || a > E) { free(deg); return ORACLE_ERR_INDEX; }
+                d = a == k ? (double)grad_out[i * F + f] : 0.0;
+            } else {
+                d = (double)grad_out[i * F + f];
+                if (aggr == ORACLE_MEAN) d /= (double)deg[i];
+            }
+            const double xj = x[j * F + f], e = ea[k * F + f];
+            double dx, de;
+            if (msg == ORACLE_MSG_EDGE_ADD) {
+                dx = d;
+                de = d;
+            } else if (msg == ORACLE_MSG_EDGE_RELU) {
+                const double on = xj + e > 0.0 ? 1.0 : 0.0;
+                dx = d * on;
+                de = d * on;
+            } else {
+                dx = d * e;
+                de = d * xj;
+            }
+            if (grad_x) {
+                grad_x[j * F + f] += dx;
+                if (sabs_x) sabs_x[j * F + f] += fabs(dx);
+            }
+            if (grad_e) {
+                grad_e[k * F + f] = de;
+                if (sabs_e) sabs_e[k * F + f] = fabs(de);
+            }
+        }
+    }
+    free(deg);
+    return ORACLE_OK;
+}
+
 /* ---------------------------------------------------------------------------
  * Attention over incoming edges (Section 2 names GAT among the operators
  * expressed by Eq. (1); Section 3, runtime paragraph, credits GAT's speed to

@@ -666,6 +666,89 @@ def pin_gat_layer_autograd(lib):
         assert np.allclose(gd, at_d.grad.numpy(), rtol=1e-4, atol=1e-5)
 
 
+def pin_golden_edge_backward(lib):
+    g = golden()["edge_messages_backward"]
+    ei = np.array(g["edge_index"], np.int64)
+    x, ea, go = (np.array(g[k], np.float32) for k in ("x", "edge_attr", "grad_out"))
+    for msg, key in (("edge_add", "add"), ("edge_relu", "relu"), ("edge_mul", "mul")):
+        for aggr in ("sum", "mean", "max"):
+            name = f"{key}_{aggr}"
+            if name not in g:
+                continue
+            arg = None
+            if aggr == "max":
+                _, arg, _ = oracle.propagate(x, ei, msg=msg, aggr="max", edge_attr=ea, lib=lib)
+                assert np.array_equal(arg, np.array(g[name]["argmax"])), name
+            gx, ge, _, _ = oracle.propagate_edge_backward(x, ei, ea, go, msg, aggr, argmax=arg, lib=lib)
+            assert np.array_equal(gx, np.array(g[name]["grad_x"], np.float64)), name
+            assert np.array_equal(ge, np.array(g[name]["grad_e"], np.float64)), name
+
+
+def pin_edge_backward_autograd(lib):
+    """Every message and aggregation against CPU torch fp64 autograd of the
+    forward written with index_add / scatter_reduce (max with distinct
+    messages per row and column, so that autograd's split of tied maxima
+    does not arise)."""
+    for N, F, ei, x, _ in small_cases():
+        E = ei.shape[1]
+        rng = np.random.default_rng(N + 11)
+        ea = rng.standard_normal((E, F)).astype(np.float32)
+        g = rng.standard_normal((N, F)).astype(np.float32)
+        src, dst = torch.from_numpy(ei[0]), torch.from_numpy(ei[1])
+        deg = torch.bincount(dst, minlength=N).clamp(min=1).to(torch.float64)
+        for msg in ("edge_add", "edge_relu", "edge_mul"):
+            for aggr in ("sum", "mean", "max"):
+                xs = torch.tensor(x, dtype=torch.float64, requires_grad=True)
+                es = torch.tensor(ea, dtype=torch.float64, requires_grad=True)
+                v = xs[src] + es if msg != "edge_mul" else xs[src] * es
+                m = torch.relu(v) if msg == "edge_relu" else v
+                if aggr == "max":
+                    if msg == "edge_relu":  # zeros tie; keep the rows where every message is positive
+                        continue
+                    out = torch.zeros(N, F, dtype=torch.float64).scatter_reduce(
+                        0, dst[:, None].expand(-1, F), m, "amax", include_self=False)
+                else:
+                    out = torch.zeros(N, F, dtype=torch.float64).index_add(0, dst, m)
+                    if aggr == "mean":
+                        out = out / deg[:, None]
+                out.backward(torch.tensor(g, dtype=torch.float64))
+                arg = None
+                if aggr == "max":
+                    _, arg, _ = oracle.propagate(x, ei, msg=msg, aggr="max", edge_attr=ea, lib=lib)
+                gx, ge, _, _ = oracle.propagate_edge_backward(x, ei, ea, g, msg, aggr, argmax=arg, lib=lib)
+                assert np.allclose(gx, xs.grad.numpy(), rtol=1e-12, atol=1e-12), (msg, aggr, N)
+                assert np.allclose(ge, es.grad.numpy(), rtol=1e-12, atol=1e-12), (msg, aggr, N)
+
+
+def pin_edge_backward_reductions(lib):
+    """Special cases that reduce to the plain propagate backward: with e = 0
+    the x-gradient of x_j + e, and with e = 1 that of x_j * e, is the plain
+    sum/mean gradient; for x_j + e the feature gradient of every edge is
+    its target's (scaled) upstream gradient; with e large and positive the
+    relu gate is open everywhere."""
+    for N, F, ei, x, _ in small_cases():
+        E = ei.shape[1]
+        g = np.random.default_rng(N + 13).standard_normal((N, F)).astype(np.float32)
+        for aggr in ("sum", "mean"):
+            base, _, _, _ = oracle.propagate_backward(x, ei, g, aggr=aggr, lib=lib)
+            z = np.zeros((E, F), np.float32)
+            # mean: g / deg here, g * (1 / deg) there: equal up to one rounding
+            same = (lambda a, b: np.array_equal(a, b)) if aggr == "sum" else \
+                (lambda a, b: np.allclose(a, b, rtol=0, atol=1e-12))
+            gx, ge, _, _ = oracle.propagate_edge_backward(x, ei, z, g, "edge_add", aggr, lib=lib)
+            assert same(gx, base), aggr
+            deg = np.bincount(ei[1], minlength=N).astype(np.float64)
+            dg = g.astype(np.float64)[ei[1]] / (np.maximum(deg, 1.0)[ei[1], None] if aggr == "mean" else 1.0)
+            assert np.array_equal(ge, dg), aggr
+            gx1, _, _, _ = oracle.propagate_edge_backward(x, ei, np.ones((E, F), np.float32), g, "edge_mul", aggr,
+                                                         lib=lib)
+            assert same(gx1, base), aggr
+            big = np.full((E, F), 100.0, np.float32)
+            r = oracle.propagate_edge_backward(x, ei, big, g, "edge_relu", aggr, lib=lib)
+            a = oracle.propagate_edge_backward(x, ei, big, g, "edge_add", aggr, lib=lib)
+            assert np.array_equal(r[0], a[0]) and np.array_equal(r[1], a[1]), aggr
+
+
 ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_golden_gcn_norm_directed,
             pin_golden_signed_zero,
             pin_degree_and_csr_library, pin_sum_mean_dense, pin_torch_scatter, pin_max_bruteforce,
@@ -673,4 +756,5 @@ ALL_PINS = [pin_golden_propagate, pin_golden_pool, pin_golden_gcn_norm, pin_gold
             pin_backward_autograd, pin_backward_dense, pin_golden_attention, pin_softmax_library,
             pin_softmax_invariants, pin_softmax_backward_autograd, pin_heads_dense, pin_uniform_attention_is_mean,
             pin_golden_dense_transform, pin_dense_transform_library, pin_golden_edge_messages,
-            pin_edge_messages_library, pin_golden_gat_backward, pin_gat_layer_autograd]
+            pin_edge_messages_library, pin_golden_gat_backward, pin_gat_layer_autograd, pin_golden_edge_backward,
+            pin_edge_backward_autograd, pin_edge_backward_reductions]

@@ -79,6 +79,14 @@ MUTANTS = [
     ("gat_bwd_dst_to_src", "            grad_dst[dst[k] * H + h] += gv;", "            grad_dst[src[k] * H + h] += gv;"),
     ("transform_skips_last_k", "for (int64_t k = 0; k < Fi; ++k) {\n                const double t",
      "for (int64_t k = 0; k + 1 < Fi; ++k) {\n                const double t"),
+    ("edge_bwd_relu_gate_ignores_edge", "const double on = xj + e > 0.0 ? 1.0 : 0.0;",
+     "const double on = xj > 0.0 ? 1.0 : 0.0;"),
+    ("edge_bwd_mul_swaps_factors", "                dx = d * e;\n                de = d * xj;",
+     "                dx = d * xj;\n                de = d * e;"),
+    ("edge_bwd_mean_unscaled", "                if (aggr == ORACLE_MEAN) d /= (double)deg[i];", ""),
+    ("edge_bwd_max_routes_everywhere", "d = a == k ? (double)grad_out[i * F + f] : 0.0;",
+     "d = (double)grad_out[i * F + f];"),
+    ("edge_bwd_grad_to_target", "                grad_x[j * F + f] += dx;", "                grad_x[i * F + f] += dx;"),
 ]
 
 
