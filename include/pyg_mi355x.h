@@ -280,6 +280,36 @@ int pyg_propagate_backward(const void *grad_out, const void *x, int dtype, int64
                            const pyg_csr *csr, const pyg_csr *csr_t, int msg, int aggr, const int64_t *argmax,
                            void *grad_x, float *grad_w, void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes needed by pyg_propagate_edge_backward (chunk_t = csr_t->chunk
+ * when grad_x is wanted under sum / mean, else 0). */
+int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int64_t chunk_t,
+                                          size_t *bytes);
+
+/* Gradient of pyg_propagate_edge (Eq. (1) with F-dimensional edge features
+ * e_{j,i}) for g = dL/d out [N, F]. Edge k = (j -> i) receives d_k = s_i g_i
+ * (sum: s_i = 1, mean: 1/deg_i) or, for max, g_{i,f} in the columns f where
+ * k = argmax[i, f]; through phi:
+ *   x_j + e:          grad_x[j] += d_k,                 grad_e[k] = d_k;
+ *   max(x_j + e, 0):  both times [x_j + e_k > 0];
+ *   x_j * e:          grad_x[j] += d_k * e_k,           grad_e[k] = d_k * x_j.
+ *   grad_out, x, edge_attr, grad_x, grad_edge_attr fp32 (PYG_BF16 returns
+ *     PYG_ERR_UNSUPPORTED); edge_attr and grad_edge_attr [E, F] in
+ *     attr_order (PYG_ORDER_CSR: CSR slot order; PYG_ORDER_COO: edge id);
+ *     x and edge_attr are not read for x_j + e (may be NULL there);
+ *   csr     the forward's CSR (its E is the edge count); csr_t the CSR of
+ *           the reversed edge list (sum / mean with grad_x); map_t its
+ *           transpose map from pyg_csr_transpose_map (CSR order; NULL = made
+ *           in the workspace); edge_index and argmax (the forward's) for max.
+ *   Either output may be NULL, not both.
+ * sum / mean are deterministic; max adds into grad_x with float atomics.
+ * Errors: PYG_ERR_INVALID_ARG (bad msg/aggr/order, negative sizes, NULL or
+ * mismatched CSRs, missing arrays for the requested outputs),
+ * PYG_ERR_UNSUPPORTED (bf16, N or E >= 2^31), PYG_ERR_WORKSPACE. */
+int pyg_propagate_edge_backward(const void *grad_out, const void *x, const void *edge_attr, int dtype, int64_t N,
+                                int64_t F, const int64_t *edge_index, const pyg_csr *csr, const pyg_csr *csr_t,
+                                const int32_t *map_t, int attr_order, int msg, int aggr, const int64_t *argmax,
+                                void *grad_x, void *grad_edge_attr, void *ws, size_t ws_bytes, void *stream);
+
 /* ---- Attention (GAT, an operator of Section 2; Section 3, runtime
  * paragraph, credits its speed to a dedicated sparse softmax). Every edge
  * carries H fp32 values per array, row-major [E, H], in the order `order`

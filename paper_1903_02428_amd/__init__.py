@@ -35,6 +35,7 @@ from .binding import (  # noqa: F401
     propagate,
     propagate_backward,
     propagate_edge,
+    propagate_edge_backward,
     propagate_heads,
     propagate_heads_backward,
     propagate_workspace_bytes,

@@ -23,7 +23,7 @@ EXPORTED = [
     "pyg_coo_to_csr", "pyg_gather_edges",
     "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_gcn_norm_csr_workspace", "pyg_gcn_norm_csr",
     "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_edge", "pyg_propagate_backward_workspace",
-    "pyg_propagate_backward",
+    "pyg_propagate_backward", "pyg_propagate_edge_backward_workspace", "pyg_propagate_edge_backward",
     "pyg_segment_softmax_workspace", "pyg_segment_softmax", "pyg_gat_softmax", "pyg_segment_softmax_backward",
     "pyg_propagate_heads_workspace", "pyg_propagate_heads", "pyg_dense_transform_workspace", "pyg_dense_transform",
     "pyg_csr_transpose_map_workspace", "pyg_csr_transpose_map",
@@ -86,6 +86,9 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
             "pyg_propagate_backward": [p, p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr),
                                        i32, i32, p, p, p, p, ctypes.c_size_t, p],
+            "pyg_propagate_edge_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
+            "pyg_propagate_edge_backward": [p, p, p, i32, i64, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), p,
+                                            i32, i32, i32, p, p, p, p, ctypes.c_size_t, p],
             "pyg_segment_softmax_workspace": [i64, i64, i64, i64, sz],
             "pyg_segment_softmax": [p, i64, ctypes.POINTER(_Csr), i32, p, p, ctypes.c_size_t, p],
             "pyg_gat_softmax": [p, p, i64, ctypes.c_float, ctypes.POINTER(_Csr), i32, p, p, ctypes.c_size_t, p],
@@ -510,6 +513,49 @@ def propagate_heads(x: torch.Tensor, csr: CSR, alpha: torch.Tensor, heads: int, 
     _check(lib.pyg_propagate_heads(_ptr(x), DTYPE[x.dtype], N, heads, C, ctypes.byref(c), _ptr(a2), _ptr(out),
                                    _ptr(workspace), workspace.numel(), _stream(x.device)), "pyg_propagate_heads")
     return out
+
+
+def propagate_edge_backward(grad_out: torch.Tensor, x: torch.Tensor | None, edge_attr: torch.Tensor | None, csr: CSR,
+                            msg: str, aggr: str = "sum", order: str = "csr", csr_t: CSR | None = None,
+                            map_t: torch.Tensor | None = None, edge_index: torch.Tensor | None = None,
+                            argmax: torch.Tensor | None = None, need_grad_x: bool = True,
+                            need_grad_edge: bool = True, workspace: torch.Tensor | None = None):
+    """Gradients of propagate_edge (fp32): (grad_x [N, F] or None,
+    grad_edge_attr [E, F] in `order` or None). Sum / mean need csr_t for
+    grad_x (map_t optional); max needs edge_index and the forward's argmax."""
+    lib = library()
+    _need_cuda("grad_out", grad_out, torch.float32, 2)
+    N, F = grad_out.shape
+    E = csr.E
+    if msg not in ("edge_add", "edge_relu", "edge_mul") or aggr not in AGGR or order not in ORDER:
+        raise ValueError("bad msg / aggr / order")
+    if msg != "edge_add":
+        _need_cuda("x", x, torch.float32, 2)
+        _need_cuda("edge_attr", edge_attr, torch.float32, 2)
+        if tuple(edge_attr.shape) != (E, F):
+            raise ValueError("edge_attr must be [E, F]")
+    if aggr == "max":
+        _need_cuda("argmax", argmax, torch.int64, 2)
+        if edge_index is None:
+            raise ValueError("max needs edge_index")
+        _edge_index(edge_index)
+    elif need_grad_x and csr_t is None:
+        raise ValueError("sum / mean need csr_t for grad_x")
+    dev = grad_out.device
+    gx = torch.empty_like(grad_out) if need_grad_x else None
+    ge = torch.empty((E, F), dtype=torch.float32, device=dev) if need_grad_edge else None
+    chunk_t = csr_t.chunk if (csr_t is not None and aggr != "max" and need_grad_x) else 0
+    nbytes = _size(lib.pyg_propagate_edge_backward_workspace, DTYPE[torch.float32], N, F, E, AGGR[aggr], chunk_t)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, dev)
+    c = csr._c()
+    ct = csr_t._c() if csr_t is not None else None
+    _check(lib.pyg_propagate_edge_backward(_ptr(grad_out), _ptr(x), _ptr(edge_attr), DTYPE[torch.float32], N, F,
+                                           _ptr(edge_index), ctypes.byref(c), ctypes.byref(ct) if ct else None,
+                                           _ptr(_map_t(map_t, E)), ORDER[order], MSG[msg], AGGR[aggr], _ptr(argmax),
+                                           _ptr(gx), _ptr(ge), _ptr(workspace), workspace.numel(), _stream(dev)),
+           "pyg_propagate_edge_backward")
+    return gx, ge
 
 
 def csr_transpose_map(csr: CSR, csr_t: CSR, out: torch.Tensor | None = None,

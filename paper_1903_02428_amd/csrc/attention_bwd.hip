@@ -213,16 +213,6 @@ bool csr_ok(const pyg_csr *c, int64_t N, int64_t E) {
     return c && c->N == N && c->E == E && c->rowptr && c->chunk >= 0 && (E == 0 || (c->col && c->perm));
 }
 
-// Transpose map into map_t (inv: E int32 of scratch).
-int transpose_map(const pyg_csr *csr, const pyg_csr *csr_t, int32_t *inv, int32_t *map_t, hipStream_t s) {
-    const int64_t E = csr->E;
-    if (E == 0) return PYG_OK;
-    k_inverse_perm<<<grid_for(E, kBlock * 4), kBlock, 0, s>>>(csr->perm, E, inv);
-    PYG_LAUNCH_CHECK();
-    k_compose<<<grid_for(E, kBlock * 4), kBlock, 0, s>>>(csr_t->perm, inv, E, map_t);
-    PYG_LAUNCH_CHECK();
-    return PYG_OK;
-}
 
 struct BwdWs {
     int32_t *inv;
@@ -294,6 +284,23 @@ int head_dots(const T *g, const T *x, int64_t N, int64_t H, int64_t C, const pyg
 }
 
 }  // namespace
+
+int inverse_perm(const int64_t *perm, int64_t E, int32_t *inv, hipStream_t s) {
+    if (E == 0) return PYG_OK;
+    k_inverse_perm<<<grid_for(E, kBlock * 4), kBlock, 0, s>>>(perm, E, inv);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
+
+int transpose_map(const pyg_csr *csr, const pyg_csr *csr_t, int32_t *inv, int32_t *map_t, hipStream_t s) {
+    const int64_t E = csr->E;
+    if (E == 0) return PYG_OK;
+    PYG_TRY(inverse_perm(csr->perm, E, inv, s));
+    k_compose<<<grid_for(E, kBlock * 4), kBlock, 0, s>>>(csr_t->perm, inv, E, map_t);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
+
 }  // namespace pyg
 
 using namespace pyg;

@@ -152,6 +152,8 @@ struct SegmentArgs {
     const int32_t *alpha_idx;  // [E] row of alpha for each slot, or NULL (row = slot)
     const void *edge_attr;       // [E, F] edge features in x's dtype (edge messages), or NULL
     const int64_t *attr_perm;    // non-NULL: edge_attr rows are COO edge ids, reached through perm
+    const int32_t *attr_idx;     // non-NULL: edge_attr row attr_idx[slot] (precedence over attr_perm)
+    const void *x_self;          // kSegMsgEdgeReluGrad: the rows' own features [n_rows, F]
     int64_t H;             // heads; feature f belongs to head f / C
     int64_t C;
     const int64_t *perm;   // [E] id reported by argmax; NULL = slot id
@@ -165,9 +167,19 @@ struct SegmentArgs {
     int64_t *argmax;    // [n_rows, F] or NULL
     bool hint;          // allow the cache-policy hint for hub source rows
 };
+// Internal message kind beyond pyg_msg (sum only): the backward of
+// max(x_j + e, 0) over the reversed graph, x = the scaled upstream gradient,
+// gate x_self[row] + e > 0.
+constexpr int kSegMsgEdgeReluGrad = 100;
 int64_t segment_chunk(int64_t E, int64_t n_rows, int64_t requested);
 size_t segment_workspace(int64_t E, int64_t F, int aggr, int64_t chunk, int64_t n_rows);
 int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t s);
+
+// inv[perm[p]] = p for a CSR's slot -> edge-id permutation (ids outside
+// [0, E) skipped); transpose_map: map_t[q] = the csr slot of the edge in
+// slot q of csr_t (inv: E int32 of scratch).
+int inverse_perm(const int64_t *perm, int64_t E, int32_t *inv, hipStream_t s);
+int transpose_map(const pyg_csr *csr, const pyg_csr *csr_t, int32_t *inv, int32_t *map_t, hipStream_t s);
 
 // Unsorted-COO gather/scatter with hardware atomics.
 size_t coo_workspace(int dtype, int64_t N, int64_t F, int aggr);

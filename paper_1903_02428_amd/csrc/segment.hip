@@ -49,6 +49,8 @@ struct SegParams {
     const int32_t *alpha_idx;  // non-NULL: slot p takes row alpha_idx[p] of alpha
     const void *ea;           // edge features [E, F] in x's dtype (edge messages)
     const int64_t *ea_perm;   // non-NULL: ea is in COO order, row perm[slot]
+    const int32_t *ea_idx;    // non-NULL: ea row ea_idx[slot] (takes precedence over ea_perm)
+    const void *x_self;       // kMsgEdgeReluGrad: the rows' own x [n_rows, F]
     int64_t H;
     int64_t C;           // columns per head: feature f belongs to head f / C
     const int64_t *perm;
@@ -155,6 +157,9 @@ constexpr int kClasses = 256;
 constexpr int kFull = 0, kPartial = 1;
 constexpr int kMsgSrc = 0, kMsgWeighted = 1, kMsgDiff = 2, kMsgHeads = 3;
 constexpr int kMsgEdgeAdd = 4, kMsgEdgeRelu = 5, kMsgEdgeMul = 6;  // x_j + e, max(x_j + e, 0), x_j * e
+// Backward of max(x_r + e, 0) over the reversed graph: the gathered upstream
+// gradient where x_r + e > 0, x_r being the row's own features (x_self).
+constexpr int kMsgEdgeReluGrad = 7;
 
 // Edge-feature message of one element (formed in fp32, as compared by max).
 template <int MSG>
@@ -195,9 +200,10 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
             pos[sl][e] = -1;
         }
     R xi[NS];
-    if constexpr (MSG == kMsgDiff) {
+    if constexpr (MSG == kMsgDiff || MSG == kMsgEdgeReluGrad) {
+        const T *xr = MSG == kMsgDiff ? x : static_cast<const T *>(p.x_self);
 #pragma unroll
-        for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(x + r * p.F + f0[sl]) : LN::zero();
+        for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(xr + r * p.F + f0[sl]) : LN::zero();
     }
     // per-head weights: a lane vector never straddles two heads (C is a multiple of its width)
     int64_t hd[NS];
@@ -256,7 +262,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                         const int64_t slot = base + st + u * S + sg;
                         ev[u][sl] = LN::zero();
                         if (ok[u] && act[sl]) {
-                            const int64_t er = p.ea_perm ? p.ea_perm[slot] : slot;
+                            const int64_t er = p.ea_idx ? p.ea_idx[slot] : (p.ea_perm ? p.ea_perm[slot] : slot);
                             ev[u][sl] = LN::load_nt(static_cast<const T *>(p.ea) + er * p.F + f0[sl]);
                         }
                     }
@@ -297,6 +303,8 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                             else if constexpr (MSG == kMsgWeighted) acc[sl][e] = fmaf(ww[u], xv, acc[sl][e]);
                             else if constexpr (MSG == kMsgHeads) acc[sl][e] = fmaf(wh[u][sl], xv, acc[sl][e]);
                             else if constexpr (MSG == kMsgEdgeMul) acc[sl][e] = fmaf(xv, LN::get(ev[u][sl], e), acc[sl][e]);
+                            else if constexpr (MSG == kMsgEdgeReluGrad)
+                                acc[sl][e] += LN::get(xi[sl], e) + LN::get(ev[u][sl], e) > 0.f ? xv : 0.f;
                             else if constexpr (EDGE) acc[sl][e] += edge_msg<MSG>(xv, LN::get(ev[u][sl], e));
                             else acc[sl][e] += xv;
                         }
@@ -381,6 +389,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
     }
     R xi = LN::zero();
     if constexpr (MSG == kMsgDiff) xi = act ? LN::load(x + r * p.F + f0) : LN::zero();
+    if constexpr (MSG == kMsgEdgeReluGrad) xi = act ? LN::load(static_cast<const T *>(p.x_self) + r * p.F + f0) : LN::zero();
     const int64_t hd = MSG == kMsgHeads ? f0 / p.C : 0;
     for (int64_t base = s; base < t; base += U) {
         int jj[U];
@@ -404,7 +413,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
             for (int u = 0; u < U; ++u) {
                 ev[u] = LN::zero();
                 if (ok[u] && act) {
-                    const int64_t er = p.ea_perm ? p.ea_perm[base + u] : base + u;
+                    const int64_t er = p.ea_idx ? p.ea_idx[base + u] : (p.ea_perm ? p.ea_perm[base + u] : base + u);
                     ev[u] = LN::load_nt(static_cast<const T *>(p.ea) + er * p.F + f0);
                 }
             }
@@ -433,6 +442,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
                     if constexpr (MSG == kMsgDiff) acc[e] += xv - LN::get(xi, e);
                     else if constexpr (MSG == kMsgWeighted || MSG == kMsgHeads) acc[e] = fmaf(ww[u], xv, acc[e]);
                     else if constexpr (MSG == kMsgEdgeMul) acc[e] = fmaf(xv, LN::get(ev[u], e), acc[e]);
+                    else if constexpr (MSG == kMsgEdgeReluGrad) acc[e] += LN::get(xi, e) + LN::get(ev[u], e) > 0.f ? xv : 0.f;
                     else if constexpr (EDGE) acc[e] += edge_msg<MSG>(xv, LN::get(ev[u], e));
                     else acc[e] += xv;
                 }
@@ -694,6 +704,7 @@ int launch_msg(const SegParams &p, int msg, bool ident, int ns, bool light, hipS
     if (ident) return launch_ns<T, VEC, kMsgSrc, MAXA, true>(p, ns, light, s);
     if constexpr (!MAXA) {
         if (msg == kMsgHeads) return launch_ns<T, VEC, kMsgHeads, false, false>(p, ns, light, s);
+        if (msg == kMsgEdgeReluGrad) return launch_ns<T, VEC, kMsgEdgeReluGrad, false, false>(p, ns, light, s);
     }
     if (msg == kMsgEdgeAdd) return launch_ns<T, VEC, kMsgEdgeAdd, MAXA, false>(p, ns, light, s);
     if (msg == kMsgEdgeRelu) return launch_ns<T, VEC, kMsgEdgeRelu, MAXA, false>(p, ns, light, s);
@@ -716,7 +727,8 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     const bool vec = row_bytes % 16 == 0 && (reinterpret_cast<uintptr_t>(a.x) % 16) == 0 &&
                      (reinterpret_cast<uintptr_t>(a.out) % 16) == 0 &&
                      (!a.alpha || (a.C * (int64_t)sizeof(T)) % 16 == 0) &&
-                     (reinterpret_cast<uintptr_t>(a.edge_attr) % 16) == 0;
+                     (reinterpret_cast<uintptr_t>(a.edge_attr) % 16) == 0 &&
+                     (reinterpret_cast<uintptr_t>(a.x_self) % 16) == 0;
     const int ep = vec ? 16 / (int)sizeof(T) : 1;
     const int64_t nvec = a.F / ep;  // lane vectors per row
     int lg = 0;
@@ -726,6 +738,7 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     if (a.msg == PYG_MSG_EDGE_ADD) mk = kMsgEdgeAdd;
     if (a.msg == PYG_MSG_EDGE_RELU) mk = kMsgEdgeRelu;
     if (a.msg == PYG_MSG_EDGE_MUL) mk = kMsgEdgeMul;
+    if (a.msg == kSegMsgEdgeReluGrad) mk = kMsgEdgeReluGrad;
     const bool ident = a.col == nullptr;
     // cache hint: only when the source rows do not fit in L2 (row in-degree as the hotness proxy)
     p.hot_class = nullptr;
@@ -819,6 +832,8 @@ int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t 
     p.alpha_idx = a.alpha_idx;
     p.ea = a.edge_attr;
     p.ea_perm = a.attr_perm;
+    p.ea_idx = a.attr_idx;
+    p.x_self = a.x_self;
     p.H = a.H;
     p.C = a.C;
     p.perm = a.perm;

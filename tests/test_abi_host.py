@@ -270,3 +270,24 @@ def test_degree_csr_rejects_bad_arguments(lib):
     assert lib.pyg_degree_csr(ctypes.byref(_Csr(None, 0x40000, 0x50000, None, 10, 20, 0)), FAKE, None) == INVALID
     assert lib.pyg_degree_csr(ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 10, 20, 0)), None, None) == INVALID
     assert lib.pyg_degree_csr(ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 0, 0, 0)), None, None) == 0  # N = 0
+
+
+def test_edge_backward_rejects_bad_arguments(lib):
+    from paper_1903_02428_amd.binding import _Csr
+    good = ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 10, 20, 0))
+    other = ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 11, 20, 0))
+    G, X, EA, GX, GE = FAKE, ctypes.c_void_p(0x200000), ctypes.c_void_p(0x300000), ctypes.c_void_p(0x400000), \
+        ctypes.c_void_p(0x500000)
+    eb = lib.pyg_propagate_edge_backward
+    RELU, ADD, SUM, MAX = 3, 2, 0, 2
+    assert eb(G, X, EA, 1, 10, 4, FAKE, good, good, None, 0, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == -5  # bf16
+    assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 0, 0, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID  # msg
+    assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 2, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID
+    assert eb(G, X, EA, 0, 10, 4, FAKE, None, good, None, 0, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID
+    assert eb(G, X, EA, 0, 10, 4, FAKE, good, None, None, 0, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID
+    assert eb(G, X, EA, 0, 10, 4, FAKE, good, other, None, 0, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID
+    assert eb(G, None, EA, 0, 10, 4, FAKE, good, good, None, 0, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID
+    assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 0, RELU, SUM, None, None, None, FAKE, 1 << 30, None) == INVALID
+    assert eb(G, X, EA, 0, 10, 4, None, good, good, None, 0, RELU, MAX, FAKE, GX, GE, FAKE, 1 << 30, None) == INVALID
+    assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 0, RELU, MAX, None, GX, GE, FAKE, 1 << 30, None) == INVALID
+    assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 0, ADD, SUM, None, GX, GE, FAKE, 0, None) == WORKSPACE
