@@ -14,8 +14,10 @@ from __future__ import annotations
 
 from .binding import (  # noqa: F401
     CSR,
+    GATAttention,
     Graph,
     Propagate,
+    PropagateEdge,
     LibraryMissing,
     PygError,
     abi_version,

@@ -741,6 +741,20 @@ class Graph:
         self.edge_weight = edge_weight
         self.csr = coo_to_csr(edge_index, num_nodes, edge_weight)
         self.csr_t = coo_to_csr(reverse_edges(edge_index), num_nodes, edge_weight)
+        self._map_t = None
+
+    @property
+    def plain(self) -> CSR:
+        """The forward CSR without weights (attention and edge messages)."""
+        c = self.csr
+        return CSR(c.rowptr, c.col, c.perm, None, c.N, c.E, c.chunk)
+
+    @property
+    def map_t(self) -> torch.Tensor:
+        """Transpose map of (csr, csr_t), made on first use."""
+        if self._map_t is None:
+            self._map_t = csr_transpose_map(self.csr, self.csr_t)
+        return self._map_t
 
 
 class Propagate(torch.autograd.Function):
@@ -776,3 +790,66 @@ class Propagate(torch.autograd.Function):
                                     None if edge_weight is None else edge_weight.detach(), csr, csr_t,
                                     ctx.aggr, ctx.msg, argmax, need_grad_w=need_w)
         return gx, gw, None, None, None
+
+
+class GATAttention(torch.autograd.Function):
+    """GAT's attention aggregation (Section 2): coefficients alpha =
+    softmax over each target's incoming edges of LeakyReLU(a_src[j] +
+    a_dst[i]) per head, then out_i = sum_j alpha_{j,i} x_j per head block.
+    Forward: gat_softmax + propagate_heads; backward: propagate_heads_backward,
+    segment_softmax_backward, gat_scores_backward (all in CSR slot order).
+    Use as GATAttention.apply(x [N, H*C], a_src [N, H], a_dst [N, H], graph,
+    negative_slope); fp32 or bf16 x, fp32 logits."""
+
+    @staticmethod
+    def forward(ctx, x, a_src, a_dst, graph: Graph, negative_slope: float = 0.2):
+        H = a_src.shape[1]
+        csr = graph.plain
+        alpha = gat_softmax(a_src.detach().contiguous(), a_dst.detach().contiguous(), csr, negative_slope, "csr")
+        out = propagate_heads(x.detach().contiguous(), csr, alpha, H)
+        ctx.graph, ctx.slope = graph, negative_slope
+        ctx.save_for_backward(x, a_src, a_dst, alpha)
+        return out
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        x, a_src, a_dst, alpha = ctx.saved_tensors
+        g = ctx.graph
+        H = a_src.shape[1]
+        need_logits = ctx.needs_input_grad[1] or ctx.needs_input_grad[2]
+        gx, galpha = propagate_heads_backward(grad_out.contiguous().to(x.dtype), x.detach().contiguous(), g.plain,
+                                              g.csr_t, alpha, H, need_grad_x=ctx.needs_input_grad[0],
+                                              need_grad_alpha=need_logits, map_t=g.map_t)
+        ga_s = ga_d = None
+        if need_logits:
+            gscore = segment_softmax_backward(alpha, galpha, g.plain, "csr")
+            ga_s, ga_d = gat_scores_backward(a_src.detach().contiguous(), a_dst.detach().contiguous(), g.plain,
+                                             g.csr_t, gscore, ctx.slope, map_t=g.map_t)
+        return gx, ga_s, ga_d, None, None
+
+
+class PropagateEdge(torch.autograd.Function):
+    """Differentiable propagate with F-dimensional edge features (Eq. (1)):
+    phi = x_j + e, max(x_j + e, 0) or x_j * e on the CSR segment kernel;
+    gradients for x and the edge features (COO edge order) by
+    pyg_propagate_edge_backward (fp32). Use as
+    PropagateEdge.apply(x, edge_attr, graph, msg, aggr)."""
+
+    @staticmethod
+    def forward(ctx, x, edge_attr, graph: Graph, msg: str = "edge_add", aggr: str = "sum"):
+        out, argmax = propagate_edge(x.detach().contiguous(), edge_attr.detach().contiguous(), graph.edge_index,
+                                     graph.plain, msg, aggr, "csr", "coo")
+        ctx.graph, ctx.msg, ctx.aggr = graph, msg, aggr
+        ctx.save_for_backward(x, edge_attr, argmax)
+        return out
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        x, edge_attr, argmax = ctx.saved_tensors
+        g = ctx.graph
+        gx, ge = propagate_edge_backward(grad_out.contiguous(), x.detach().contiguous(),
+                                         edge_attr.detach().contiguous(), g.plain, ctx.msg, ctx.aggr, "coo",
+                                         csr_t=g.csr_t, edge_index=g.edge_index, argmax=argmax,
+                                         need_grad_x=ctx.needs_input_grad[0],
+                                         need_grad_edge=ctx.needs_input_grad[1])
+        return gx, ge, None, None, None
