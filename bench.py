@@ -77,6 +77,8 @@ def parse():
     ap.add_argument("--fig2", action="store_true",
                     help="run the degree sweep of the paper's Fig. 2 (gather/scatter vs CSR, forward and backward) "
                          "instead of the headline step; prints one JSON line per point")
+    ap.add_argument("--backward-only", action="store_true",
+                    help="only the gradient of the propagate on the large graph (one JSON object)")
     ap.add_argument("--configs-only", action="store_true",
                     help="only the throughput of the four smaller synthetic graphs (one JSON object)")
     ap.add_argument("--attention-only", action="store_true",
@@ -180,6 +182,13 @@ def main():
                           "gcn_layer": gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)}), flush=True)
         return
 
+    if args.backward_only:
+        pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
+        pyg.gcn_norm_csr(csr, out=norm, workspace=ws_norm)
+        print(json.dumps({"workload": "large power-law graph, gradient of the propagate", "N": N, "E": E, "F": F,
+                          "backward": backward_calls(pyg, torch, x, ei, csr_w, N, E, F, dev)}), flush=True)
+        return
+
     if args.edge_features_only:
         pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
         print(json.dumps({"workload": "large power-law graph, edge-feature messages", "N": N, "E": E, "F": F,
@@ -267,6 +276,7 @@ def main():
 
     if not args.no_detail:
         result["detail"]["variants"] = variants(pyg, torch, x, ei, csr_w, N, E, F, dev)
+        result["detail"]["backward"] = backward_calls(pyg, torch, x, ei, csr_w, N, E, F, dev)
         result["detail"]["attention"] = attention(pyg, torch, x, ei, csr, N, E, F, dev)
         result["detail"]["gcn_layer"] = gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)
         result["detail"]["edge_features"] = edge_features(pyg, torch, x, ei, csr, N, E, F, dev)
@@ -409,6 +419,44 @@ def small_configs(pyg, torch, dev, seed):
                 entry[f"pool-{aggr}"] = {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9,
                                          "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
         res[name] = entry
+    return res
+
+
+def backward_calls(pyg, torch, x, ei, csr_w, N, E, F, dev):
+    """The gradient of the propagate on the same graph (fp32): gcn-weighted
+    sum with the weight gradient, mean, and max routed through the
+    forward's argmax. The reversed CSR (with the weights) is preprocessing,
+    built once. Algorithmic bytes: grad_x as the propagate over the reversed
+    graph; grad_w one g row per target row, one x gather per edge, columns,
+    the slot -> edge permutation and the weight written; max: argmax, g and
+    one source id, x read and grad_x added per output element."""
+    w_coo = torch.empty_like(csr_w.weight)  # the weights in COO order
+    w_coo[csr_w.perm] = csr_w.weight
+    csr_t = pyg.coo_to_csr(pyg.reverse_edges(ei), N, w_coo, chunk=csr_w.chunk)
+    plain = pyg.CSR(csr_w.rowptr, csr_w.col, csr_w.perm, None, N, E, csr_w.chunk)
+    plain_t = pyg.CSR(csr_t.rowptr, csr_t.col, csr_t.perm, None, N, E, csr_t.chunk)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(17)
+    g = torch.randn(N, F, device=dev, generator=gen)
+    rp = 8 * (N + 1)
+    res = {}
+
+    def rec(ms, b):
+        return {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9, "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "bytes": b, "edges_features_per_s": E * F / (ms * 1e-3)}
+
+    ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, w_coo, csr=csr_w, csr_t=csr_t, aggr="sum",
+                                                     need_grad_w=True), reps=5)
+    res["sum-weighted-grad_x+grad_w"] = rec(ms, b_alg_csr(N, E, F, 4) + rp + 4 * E + 8 * E + N * F * 4 + E * F * 4
+                                           + 4 * E)
+    ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, None, csr=plain, csr_t=plain_t, aggr="mean"), reps=5)
+    res["mean-grad_x"] = rec(ms, b_alg_csr(N, E, F, 4, weighted=False) + rp + 2 * N * F * 4)
+    _, am = pyg.propagate(x, csr=plain, aggr="max")
+    ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, None, csr=plain, csr_t=plain_t, aggr="max",
+                                                     argmax=am), reps=5)
+    res["max-grad_x"] = rec(ms, N * F * (8 + 4 + 8 + 4) + N * F * 4)
+    del csr_t, plain_t, g, am, w_coo
+    torch.cuda.empty_cache()
     return res
 
 

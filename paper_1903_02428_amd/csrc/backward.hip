@@ -20,6 +20,10 @@
 // gradient is one pass over the CSR slots; max routes as above. fp32 only.
 #include "common.hpp"
 
+#ifndef PYG_SDDMM_U
+#define PYG_SDDMM_U 4  // slots per sub-group in flight in the weight-gradient dot products
+#endif
+
 namespace pyg {
 namespace {
 
@@ -91,6 +95,82 @@ __global__ __launch_bounds__(kBlock) void k_sddmm(const T *__restrict__ g, const
             }
             for (int off = L >> 1; off > 0; off >>= 1) acc += __shfl_xor(acc, off, kWave);
             if (p < b && q == 0) grad_w[perm[p]] = sc * acc;
+        }
+        if (t >= e1) break;
+        ++r;
+    }
+}
+
+// The same dot products with 16-byte lane vectors (F * sizeof(T) % 16 == 0,
+// aligned rows): a sub-group of L = 2^lg lanes covers a feature row (lanes
+// loop when it is longer than L vectors), U slots per sub-group in flight;
+// the target's gradient row is loaded once per row when one pass covers it.
+template <typename T, int U>
+__global__ __launch_bounds__(kBlock) void k_sddmm_vec(const T *__restrict__ g, const T *__restrict__ x, int64_t N,
+                                                      int64_t F, const int64_t *__restrict__ rowptr,
+                                                      const int32_t *__restrict__ col,
+                                                      const int64_t *__restrict__ perm, int64_t E, int64_t chunk,
+                                                      int lg, int mean, float *__restrict__ grad_w) {
+    constexpr int EP = 16 / sizeof(T);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int L = 1 << lg, S = kWave >> lg;
+    const int q = lane & (L - 1), sg = lane >> lg;
+    const bool one_pass = F <= (int64_t)L * EP;
+    const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+    const int64_t e0 = c * chunk;
+    if (e0 >= E) return;
+    const int64_t e1 = (e0 + chunk) < E ? (e0 + chunk) : E;
+    int64_t r = uniform64(wave_lower_bound(rowptr, N + 1, e0 + 1, lane)) - 1;
+    auto dot16 = [](const uint4 &a, const uint4 &b) {
+        const uint32_t wa[4] = {a.x, a.y, a.z, a.w}, wb[4] = {b.x, b.y, b.z, b.w};
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (sizeof(T) == 4) {
+                acc = fmaf(__uint_as_float(wa[i]), __uint_as_float(wb[i]), acc);
+            } else {
+                acc = fmaf(__uint_as_float(wa[i] << 16), __uint_as_float(wb[i] << 16), acc);
+                acc = fmaf(__uint_as_float(wa[i] & 0xFFFF0000u), __uint_as_float(wb[i] & 0xFFFF0000u), acc);
+            }
+        }
+        return acc;
+    };
+    while (true) {
+        const int64_t s = uniform64(rowptr[r]), t = uniform64(rowptr[r + 1]);
+        const int64_t a = s > e0 ? s : e0, b = t < e1 ? t : e1;
+        const float sc = mean ? 1.f / static_cast<float>(t - s) : 1.f;
+        const int64_t f0 = (int64_t)q * EP;
+        uint4 g1 = make_uint4(0, 0, 0, 0);
+        if (one_pass && f0 < F && a < b) g1 = *reinterpret_cast<const uint4 *>(g + r * F + f0);
+        for (int64_t k0 = a; k0 < b; k0 += (int64_t)S * U) {
+            int jj[U];
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int64_t p = k0 + (int64_t)k * S + sg;
+                jj[k] = p < b ? __builtin_nontemporal_load(col + p) : 0;
+            }
+            float acc[U];
+#pragma unroll
+            for (int k = 0; k < U; ++k) acc[k] = 0.f;
+            for (int64_t f = f0; f < F; f += (int64_t)L * EP) {
+                const uint4 gv = one_pass ? g1 : *reinterpret_cast<const uint4 *>(g + r * F + f);
+                uint4 xv[U];
+#pragma unroll
+                for (int k = 0; k < U; ++k) {
+                    const int64_t p = k0 + (int64_t)k * S + sg;
+                    xv[k] = p < b ? *reinterpret_cast<const uint4 *>(x + (int64_t)jj[k] * F + f) : make_uint4(0, 0, 0, 0);
+                }
+#pragma unroll
+                for (int k = 0; k < U; ++k) acc[k] += dot16(gv, xv[k]);
+            }
+            for (int off = 1; off < L; off <<= 1)
+#pragma unroll
+                for (int k = 0; k < U; ++k) acc[k] += __shfl_xor(acc[k], off, kWave);
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int64_t p = k0 + (int64_t)k * S + sg;
+                if (q == 0 && p < b) grad_w[perm[p]] = sc * acc[k];
+            }
         }
         if (t >= e1) break;
         ++r;
@@ -207,12 +287,23 @@ int backward_typed(const void *grad_out, const void *x, int dtype, int64_t N, in
         PYG_LAUNCH_CHECK();
     }
     if (grad_w && E > 0) {
-        int lg = 0;
-        while ((1 << lg) < F && lg < 6) ++lg;
         constexpr int64_t kChunk = 1024;
         const int64_t nchunks = (E + kChunk - 1) / kChunk;
-        k_sddmm<T><<<static_cast<unsigned>((nchunks + 3) / 4), kBlock, 0, s>>>(
-            g, static_cast<const T *>(x), N, F, csr->rowptr, csr->col, csr->perm, E, kChunk, lg, aggr == PYG_MEAN, grad_w);
+        const unsigned grid = static_cast<unsigned>((nchunks + 3) / 4);
+        constexpr int64_t EP = 16 / sizeof(T);
+        const bool vec = (F * (int64_t)sizeof(T)) % 16 == 0 && reinterpret_cast<uintptr_t>(g) % 16 == 0 &&
+                         reinterpret_cast<uintptr_t>(x) % 16 == 0;
+        if (vec && F > 0) {
+            int lg = 0;
+            while ((int64_t(1) << lg) < F / EP && lg < 6) ++lg;
+            k_sddmm_vec<T, PYG_SDDMM_U><<<grid, kBlock, 0, s>>>(g, static_cast<const T *>(x), N, F, csr->rowptr, csr->col,
+                                                      csr->perm, E, kChunk, lg, aggr == PYG_MEAN, grad_w);
+        } else {
+            int lg = 0;
+            while ((1 << lg) < F && lg < 6) ++lg;
+            k_sddmm<T><<<grid, kBlock, 0, s>>>(g, static_cast<const T *>(x), N, F, csr->rowptr, csr->col, csr->perm,
+                                               E, kChunk, lg, aggr == PYG_MEAN, grad_w);
+        }
         PYG_LAUNCH_CHECK();
     }
     return PYG_OK;

@@ -101,6 +101,53 @@ def test_c5_propagate_sampled(pyg, c5, dev_graph, kernel):
         print(f"[c5] {what} ok", flush=True)
 
 
+def test_c5_propagate_backward_sampled(pyg, c5, dev_graph):
+    """The gradient of the propagate as the benchmark times it (fp32):
+    gcn-weighted sum with the weight gradient, mean, and max through the
+    forward's argmax; grad_x on sampled nodes (their outgoing edges in the
+    oracle's sub-graph), grad_w on every edge of that sub-graph."""
+    ei_np, x_np, N = c5["edge_index_gcn"], c5["x"], c5["N"]
+    ei, w_ref, csr = dev_graph
+    E = ei_np.shape[1]
+    w = to_dev(w_ref)
+    csr_t = pyg.coo_to_csr(pyg.reverse_edges(ei), N, w, chunk=csr.chunk)
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, E, csr.chunk)
+    plain_t = pyg.CSR(csr_t.rowptr, csr_t.col, csr_t.perm, None, N, E, csr_t.chunk)
+    g = np.random.default_rng(81).standard_normal(x_np.shape).astype(np.float32)
+    x32, g32 = to_dev(x_np), to_dev(g)
+    gx_s, gw_s = pyg.propagate_backward(g32, x32, ei, w, csr=csr, csr_t=csr_t, aggr="sum", need_grad_w=True)
+    gx_m, _ = pyg.propagate_backward(g32, x32, ei, None, csr=plain, csr_t=plain_t, aggr="mean")
+    torch.cuda.synchronize()
+    nodes = sample_rows(c5, n=200)[0]
+    keep = np.isin(ei_np[0], nodes)
+    kidx = np.nonzero(keep)[0]
+    sub = np.ascontiguousarray(ei_np[:, keep])
+    # mean divides by the in-degree of each edge's target, taken over the whole graph: the
+    # oracle's sub-graph keeps only some of those edges, so mean is checked through s*g
+    deg = np.bincount(ei_np[1], minlength=N).astype(np.float64)
+    rx, rw, sx, sw = oracle.propagate_backward(x_np, sub, g, w_ref[keep], aggr="sum", want_grad_w=True)
+    check_sum(gx_s[to_dev(nodes)].cpu(), rx[nodes], sx[nodes], False, "C5 backward sum grad_x")
+    check_sum(gw_s[to_dev(kidx)].cpu(), rw, sw, False, "C5 backward sum grad_w")
+    gm = (g.astype(np.float64) / np.maximum(deg, 1.0)[:, None]).astype(np.float32)  # rounded like the kernel's s*g
+    rxm, _, sxm, _ = oracle.propagate_backward(x_np, sub, gm, aggr="sum")
+    check_sum(gx_m[to_dev(nodes)].cpu(), rxm[nodes], sxm[nodes], False, "C5 backward mean grad_x")
+    # max: every winner of the sampled target rows; the oracle's own argmax over those rows' edges
+    rows, keep_in = sample_rows(c5, n=200)
+    sub_in = np.ascontiguousarray(ei_np[:, keep_in])
+    kin = np.nonzero(keep_in)[0]
+    _, rarg, _ = oracle.propagate(x_np, sub_in, aggr="max")
+    arg_full = np.full((N, x_np.shape[1]), E, np.int64)
+    arg_full[rows] = np.where(rarg[rows] < sub_in.shape[1], kin[np.minimum(rarg[rows], sub_in.shape[1] - 1)], E)
+    gx_x, _ = pyg.propagate_backward(g32, x32, ei, None, csr=plain, csr_t=plain_t, aggr="max",
+                                     argmax=to_dev(arg_full))
+    torch.cuda.synchronize()
+    rxx, _, sxx, _ = oracle.propagate_backward(x_np, ei_np, g, aggr="max", argmax=arg_full)
+    check_sum(gx_x.cpu(), rxx, sxx, False, "C5 backward max grad_x")
+    print("[c5] propagate backward ok", flush=True)
+    del csr_t, gx_s, gw_s, gx_m, gx_x
+    torch.cuda.empty_cache()
+
+
 def test_c5_attention_sampled(pyg, c5, dev_graph):
     """GAT attention at the benchmark's shape (H = 8 heads of 16 columns) in
     CSR slot order: the coefficients of every edge into the sampled rows and
