@@ -300,7 +300,7 @@ int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64
  *           the reversed edge list (sum / mean with grad_x); map_t its
  *           transpose map from pyg_csr_transpose_map (CSR order; NULL = made
  *           in the workspace); edge_index and argmax (the forward's) for max.
- *   Either output may be NULL, not both.
+ *   Either output may be NULL, not both (unless both are empty).
  * sum / mean are deterministic; max adds into grad_x with float atomics.
  * Errors: PYG_ERR_INVALID_ARG (bad msg/aggr/order, negative sizes, NULL or
  * mismatched CSRs, missing arrays for the requested outputs),
@@ -402,7 +402,8 @@ int pyg_propagate_heads_backward_workspace(int dtype, int64_t N, int64_t H, int6
  * grad_out, x, grad_x in dtype (fp32 accumulation); alpha, grad_alpha fp32
  * [E, H]. map_t: the transpose map of (csr, csr_t) from
  * pyg_csr_transpose_map, or NULL to make it in the workspace on every call.
- * Either output may be NULL (not both); x is needed for grad_alpha.
+ * Either output may be NULL (not both, unless both are empty); x is needed
+ * for grad_alpha.
  * Deterministic. Errors: PYG_ERR_INVALID_ARG (NULL or mismatched CSRs,
  * missing arrays, H <= 0), PYG_ERR_UNSUPPORTED (N, E or H*C >= 2^31),
  * PYG_ERR_WORKSPACE. */

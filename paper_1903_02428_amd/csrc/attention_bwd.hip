@@ -344,7 +344,7 @@ extern "C" int pyg_propagate_heads_backward(const void *grad_out, const void *x,
     if (N * F > 0 && !grad_out) return PYG_ERR_INVALID_ARG;
     if (E > 0 && !alpha) return PYG_ERR_INVALID_ARG;
     if (grad_alpha && N * F > 0 && !x) return PYG_ERR_INVALID_ARG;
-    if (!grad_x && !grad_alpha) return PYG_ERR_INVALID_ARG;
+    if (!grad_x && !grad_alpha && (N * F > 0 || E * H > 0)) return PYG_ERR_INVALID_ARG;  // nothing asked for
     size_t need;
     PYG_TRY(pyg_propagate_heads_backward_workspace(dtype, N, H, C, E, csr_t->chunk, &need));
     if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;

@@ -519,7 +519,7 @@ extern "C" int pyg_propagate_edge_backward(const void *grad_out, const void *x, 
     const int64_t E = csr->E;
     if (E < 0 || csr->N != N) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
-    if (!grad_x && !grad_edge_attr) return PYG_ERR_INVALID_ARG;
+    if (!grad_x && !grad_edge_attr && (N * F > 0 || E * F > 0)) return PYG_ERR_INVALID_ARG;  // nothing asked for
     if (E > 0 && N == 0) return PYG_ERR_INVALID_ARG;
     if (N * F > 0 && !grad_out) return PYG_ERR_INVALID_ARG;
     if (msg != PYG_MSG_EDGE_ADD && N * F > 0 && (!x || (E * F > 0 && !edge_attr))) return PYG_ERR_INVALID_ARG;

@@ -1,0 +1,69 @@
+"""Degenerate sizes on the backward and attention entry points: no nodes,
+no edges, no feature columns. Every call must succeed and write zeros (or
+nothing) without touching memory it was not given."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from tests.parity import to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def pyg():
+    import paper_1903_02428_amd as m
+    assert torch.cuda.is_available()
+    m.library()
+    return m
+
+
+def graphs(pyg, N, E):
+    ei = synth.random_coo(np.random.default_rng(N + E), N, E) if N else np.zeros((2, 0), np.int64)
+    d = to_dev(ei)
+    csr = pyg.coo_to_csr(d, N)
+    csr_t = pyg.coo_to_csr(pyg.reverse_edges(d), N)
+    return d, csr, csr_t
+
+
+@pytest.mark.parametrize("N,E", [(0, 0), (7, 0), (7, 30)])
+def test_attention_backward_degenerate(pyg, N, E):
+    d, csr, csr_t = graphs(pyg, N, E)
+    H, C = 2, 4
+    g = torch.randn(N, H * C, device="cuda")
+    x = torch.randn(N, H * C, device="cuda")
+    alpha = torch.rand(E, H, device="cuda")
+    mt = pyg.csr_transpose_map(csr, csr_t)
+    assert mt.shape == (E,)
+    gx, ga = pyg.propagate_heads_backward(g, x, csr, csr_t, alpha, H, map_t=mt)
+    a_s, a_d = torch.randn(N, H, device="cuda"), torch.randn(N, H, device="cuda")
+    gs, gd = pyg.gat_scores_backward(a_s, a_d, csr, csr_t, torch.randn(E, H, device="cuda"), map_t=mt)
+    torch.cuda.synchronize()
+    assert gx.shape == (N, H * C) and ga.shape == (E, H) and gs.shape == (N, H) and gd.shape == (N, H)
+    if E == 0:
+        assert torch.count_nonzero(gx) == 0 and torch.count_nonzero(gs) == 0 and torch.count_nonzero(gd) == 0
+
+
+@pytest.mark.parametrize("N,E,F", [(0, 0, 4), (7, 0, 4), (7, 30, 0), (7, 30, 4)])
+@pytest.mark.parametrize("aggr", ["sum", "mean", "max"])
+def test_edge_backward_degenerate(pyg, N, E, F, aggr):
+    d, csr, csr_t = graphs(pyg, N, E)
+    g = torch.randn(N, F, device="cuda")
+    x = torch.randn(N, F, device="cuda")
+    ea = torch.randn(E, F, device="cuda")
+    arg = None
+    if aggr == "max":
+        _, arg = pyg.propagate_edge(x, ea, d, csr, "edge_relu", "max", "csr", "coo")
+    gx, ge = pyg.propagate_edge_backward(g, x, ea, csr, "edge_relu", aggr, "coo", csr_t=csr_t, edge_index=d,
+                                         argmax=arg)
+    torch.cuda.synchronize()
+    assert gx.shape == (N, F) and ge.shape == (E, F)
+    if E == 0:
+        assert torch.count_nonzero(gx) == 0
+
+
+def test_degree_csr_and_map_empty(pyg):
+    d, csr, csr_t = graphs(pyg, 5, 0)
+    assert torch.equal(pyg.degree_csr(csr).cpu(), torch.zeros(5, dtype=torch.int64))
+    assert pyg.csr_transpose_map(csr, csr_t).numel() == 0
