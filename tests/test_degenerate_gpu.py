@@ -67,3 +67,37 @@ def test_degree_csr_and_map_empty(pyg):
     d, csr, csr_t = graphs(pyg, 5, 0)
     assert torch.equal(pyg.degree_csr(csr).cpu(), torch.zeros(5, dtype=torch.int64))
     assert pyg.csr_transpose_map(csr, csr_t).numel() == 0
+
+
+@pytest.mark.parametrize("N,E,F", [(0, 0, 4), (7, 0, 4), (7, 30, 0)])
+def test_forward_calls_degenerate(pyg, N, E, F):
+    d, csr, csr_t = graphs(pyg, N, E)
+    x = torch.randn(N, F, device="cuda")
+    for kernel in ("csr", "coo"):
+        for aggr in ("sum", "mean", "max"):
+            for dt in (torch.float32, torch.bfloat16):
+                out, arg = pyg.propagate(x.to(dt), d, csr=csr if kernel == "csr" else None, aggr=aggr, kernel=kernel)
+                assert out.shape == (N, F)
+                if E == 0 and N * F:
+                    assert torch.count_nonzero(out) == 0
+                    if aggr == "max":
+                        assert torch.all(arg == E)
+    w = pyg.gcn_norm(d, N)
+    assert w.shape == (E,)
+    assert pyg.gcn_norm_csr(csr).shape == (E,)
+    assert torch.equal(pyg.degree(d, N).cpu(), pyg.degree_csr(csr).cpu())
+    H = 2
+    s = torch.randn(E, H, device="cuda")
+    assert pyg.segment_softmax(s, csr).shape == (E, H)
+    assert pyg.gat_softmax(torch.randn(N, H, device="cuda"), torch.randn(N, H, device="cuda"), csr).shape == (E, H)
+    assert pyg.segment_softmax_backward(s, s, csr).shape == (E, H)
+    batch = torch.zeros(N, dtype=torch.int64, device="cuda")
+    for aggr in ("sum", "mean", "max"):
+        pooled, _ = pyg.global_pool(x, batch, 1, aggr)
+        assert pooled.shape == (1, F)
+        if N == 0 and F:
+            assert torch.count_nonzero(pooled) == 0
+    if F % 8 == 0:
+        t = torch.randn(F, 16, device="cuda").to(torch.bfloat16)
+        assert pyg.dense_transform(x.to(torch.bfloat16), t).shape == (N, 16)
+    torch.cuda.synchronize()
