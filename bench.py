@@ -592,10 +592,13 @@ def edge_features(pyg, torch, x, ei, csr, N, E, F, dev):
     """Propagate with an F-dimensional feature on every edge (GINE-style
     max(x_j + e, 0), sum): the CSR kernel with the features in CSR slot
     order (streamed once, coalesced) and the COO atomic kernel with them in
-    COO order. Algorithmic bytes: the plain propagate's plus E*F*s."""
+    COO order, and the backward of the CSR call in both dtypes. Algorithmic
+    bytes: the plain propagate's plus E*F*s."""
     gen = torch.Generator(device=dev)
     gen.manual_seed(13)
     res = {"msg": "max(x_j + e, 0)", "aggr": "sum"}
+    csr_t = pyg.coo_to_csr(pyg.reverse_edges(ei), N, chunk=csr.chunk)
+    map_t = pyg.csr_transpose_map(csr, csr_t)
     for dtname, dt, sz in (("f32", torch.float32, 4), ("bf16", torch.bfloat16, 2)):
         xx = x.to(dt)
         ea = torch.randn(E, F, device=dev, generator=gen).to(dt)
@@ -611,27 +614,26 @@ def edge_features(pyg, torch, x, ei, csr, N, E, F, dev):
             res[f"{kernel}-{dtname}"] = {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9,
                                          "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "bytes": b,
                                          "edges_features_per_s": E * F / (ms * 1e-3)}
-        if dt == torch.float32:
-            # the backward of the same call (fp32): grad_x over the reversed
-            # graph, edge rows reached through the transpose map, and grad_e
-            csr_t = pyg.coo_to_csr(pyg.reverse_edges(ei), N, chunk=csr.chunk)
-            map_t = pyg.csr_transpose_map(csr, csr_t)
-            g = torch.randn(N, F, device=dev, generator=gen)
-            ws = torch.empty(pyg.binding._size(pyg.library().pyg_propagate_edge_backward_workspace, 0, N, F, E, 0,
-                                               csr_t.chunk), dtype=torch.uint8, device=dev)
-            ms = timed(torch, lambda: pyg.propagate_edge_backward(g, xx, ea, csr, "edge_relu", "sum", "csr",
-                                                                  csr_t=csr_t, map_t=map_t, workspace=ws), reps=5)
-            rp = 8 * (N + 1)
-            # grad_x: columns and map, one gathered g row, one edge row per
-            # edge, the row's own x and the output; grad_e: columns, g per
-            # row, one x gather, one edge row in and one out per edge
-            b = (rp + 8 * E + 2 * E * F * 4 + 2 * N * F * 4) + (rp + 4 * E + N * F * 4 + 3 * E * F * 4)
-            res["backward-csr-f32"] = {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9,
-                                       "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "bytes": b,
-                                       "edges_features_per_s": E * F / (ms * 1e-3)}
-            del csr_t, map_t, g, ws
+        # the backward of the same call: grad_x over the reversed graph, edge
+        # rows reached through the transpose map, and grad_e
+        g = torch.randn(N, F, device=dev, generator=gen).to(dt)
+        ws = torch.empty(pyg.binding._size(pyg.library().pyg_propagate_edge_backward_workspace,
+                                           pyg.binding.DTYPE[dt], N, F, E, pyg.binding.MSG["edge_relu"],
+                                           pyg.binding.AGGR["sum"], csr_t.chunk), dtype=torch.uint8, device=dev)
+        ms = timed(torch, lambda: pyg.propagate_edge_backward(g, xx, ea, csr, "edge_relu", "sum", "csr",
+                                                              csr_t=csr_t, map_t=map_t, workspace=ws), reps=5)
+        rp = 8 * (N + 1)
+        # grad_x: columns and map, one gathered g row, one edge row per
+        # edge, the row's own x and the output; grad_e: columns, g per
+        # row, one x gather, one edge row in and one out per edge
+        b = (rp + 8 * E + 2 * E * F * sz + 2 * N * F * sz) + (rp + 4 * E + N * F * sz + 3 * E * F * sz)
+        res[f"backward-csr-{dtname}"] = {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9,
+                                         "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, "bytes": b,
+                                         "edges_features_per_s": E * F / (ms * 1e-3)}
+        del g, ws
         del ea
         torch.cuda.empty_cache()
+    del csr_t, map_t
     return res
 
 

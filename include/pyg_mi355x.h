@@ -281,9 +281,13 @@ int pyg_propagate_backward(const void *grad_out, const void *x, int dtype, int64
                            void *grad_x, float *grad_w, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_propagate_edge_backward (chunk_t = csr_t->chunk
- * when grad_x is wanted under sum / mean, else 0). */
-int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int64_t chunk_t,
-                                          size_t *bytes);
+ * when grad_x is wanted under sum / mean, else 0). bf16 adds fp32 scratch:
+ * N*F*4 bytes for grad_x under mean or max, and under mean with
+ * max(x_j + e, 0) or x_j * e another N*F*4 + E*F*4 bytes (x and the edge
+ * rows widened to fp32). Errors: PYG_ERR_INVALID_ARG (NULL bytes, negative
+ * sizes, bad dtype/msg/aggr), PYG_ERR_UNSUPPORTED (N or E >= 2^31). */
+int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int msg, int aggr,
+                                          int64_t chunk_t, size_t *bytes);
 
 /* Gradient of pyg_propagate_edge (Eq. (1) with F-dimensional edge features
  * e_{j,i}) for g = dL/d out [N, F]. Edge k = (j -> i) receives d_k = s_i g_i
@@ -292,8 +296,10 @@ int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64
  *   x_j + e:          grad_x[j] += d_k,                 grad_e[k] = d_k;
  *   max(x_j + e, 0):  both times [x_j + e_k > 0];
  *   x_j * e:          grad_x[j] += d_k * e_k,           grad_e[k] = d_k * x_j.
- *   grad_out, x, edge_attr, grad_x, grad_edge_attr fp32 (PYG_BF16 returns
- *     PYG_ERR_UNSUPPORTED); edge_attr and grad_edge_attr [E, F] in
+ *   grad_out, x, edge_attr, grad_x, grad_edge_attr all in dtype (PYG_F32
+ *     or PYG_BF16; bf16 is widened as it is loaded, every sum and product
+ *     is fp32 and each gradient is rounded once); edge_attr and
+ *     grad_edge_attr [E, F] in
  *     attr_order (PYG_ORDER_CSR: CSR slot order; PYG_ORDER_COO: edge id);
  *     x and edge_attr are not read for x_j + e (may be NULL there);
  *   csr     the forward's CSR (its E is the edge count); csr_t the CSR of
@@ -302,9 +308,9 @@ int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64
  *           in the workspace); edge_index and argmax (the forward's) for max.
  *   Either output may be NULL, not both (unless both are empty).
  * sum / mean are deterministic; max adds into grad_x with float atomics.
- * Errors: PYG_ERR_INVALID_ARG (bad msg/aggr/order, negative sizes, NULL or
- * mismatched CSRs, missing arrays for the requested outputs),
- * PYG_ERR_UNSUPPORTED (bf16, N or E >= 2^31), PYG_ERR_WORKSPACE. */
+ * Errors: PYG_ERR_INVALID_ARG (bad dtype/msg/aggr/order, negative sizes, NULL
+ * or mismatched CSRs, missing arrays for the requested outputs),
+ * PYG_ERR_UNSUPPORTED (N or E >= 2^31), PYG_ERR_WORKSPACE. */
 int pyg_propagate_edge_backward(const void *grad_out, const void *x, const void *edge_attr, int dtype, int64_t N,
                                 int64_t F, const int64_t *edge_index, const pyg_csr *csr, const pyg_csr *csr_t,
                                 const int32_t *map_t, int attr_order, int msg, int aggr, const int64_t *argmax,

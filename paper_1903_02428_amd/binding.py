@@ -86,7 +86,7 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
             "pyg_propagate_backward": [p, p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr),
                                        i32, i32, p, p, p, p, ctypes.c_size_t, p],
-            "pyg_propagate_edge_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
+            "pyg_propagate_edge_backward_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate_edge_backward": [p, p, p, i32, i64, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), p,
                                             i32, i32, i32, p, p, p, p, ctypes.c_size_t, p],
             "pyg_segment_softmax_workspace": [i64, i64, i64, i64, sz],
@@ -520,18 +520,22 @@ def propagate_edge_backward(grad_out: torch.Tensor, x: torch.Tensor | None, edge
                             map_t: torch.Tensor | None = None, edge_index: torch.Tensor | None = None,
                             argmax: torch.Tensor | None = None, need_grad_x: bool = True,
                             need_grad_edge: bool = True, workspace: torch.Tensor | None = None):
-    """Gradients of propagate_edge (fp32): (grad_x [N, F] or None,
-    grad_edge_attr [E, F] in `order` or None). Sum / mean need csr_t for
-    grad_x (map_t optional); max needs edge_index and the forward's argmax."""
+    """Gradients of propagate_edge (fp32 or bf16, the dtype of grad_out):
+    (grad_x [N, F] or None, grad_edge_attr [E, F] in `order` or None). Sum /
+    mean need csr_t for grad_x (map_t optional); max needs edge_index and the
+    forward's argmax."""
     lib = library()
-    _need_cuda("grad_out", grad_out, torch.float32, 2)
+    _need_cuda("grad_out", grad_out, None, 2)
+    if grad_out.dtype not in DTYPE:
+        raise ValueError("grad_out must be float32 or bfloat16")
+    dt = grad_out.dtype
     N, F = grad_out.shape
     E = csr.E
     if msg not in ("edge_add", "edge_relu", "edge_mul") or aggr not in AGGR or order not in ORDER:
         raise ValueError("bad msg / aggr / order")
     if msg != "edge_add":
-        _need_cuda("x", x, torch.float32, 2)
-        _need_cuda("edge_attr", edge_attr, torch.float32, 2)
+        _need_cuda("x", x, dt, 2)
+        _need_cuda("edge_attr", edge_attr, dt, 2)
         if tuple(edge_attr.shape) != (E, F):
             raise ValueError("edge_attr must be [E, F]")
     if aggr == "max":
@@ -543,14 +547,14 @@ def propagate_edge_backward(grad_out: torch.Tensor, x: torch.Tensor | None, edge
         raise ValueError("sum / mean need csr_t for grad_x")
     dev = grad_out.device
     gx = torch.empty_like(grad_out) if need_grad_x else None
-    ge = torch.empty((E, F), dtype=torch.float32, device=dev) if need_grad_edge else None
+    ge = torch.empty((E, F), dtype=dt, device=dev) if need_grad_edge else None
     chunk_t = csr_t.chunk if (csr_t is not None and aggr != "max" and need_grad_x) else 0
-    nbytes = _size(lib.pyg_propagate_edge_backward_workspace, DTYPE[torch.float32], N, F, E, AGGR[aggr], chunk_t)
+    nbytes = _size(lib.pyg_propagate_edge_backward_workspace, DTYPE[dt], N, F, E, MSG[msg], AGGR[aggr], chunk_t)
     if workspace is None or workspace.numel() < nbytes:
         workspace = _workspace(nbytes, dev)
     c = csr._c()
     ct = csr_t._c() if csr_t is not None else None
-    _check(lib.pyg_propagate_edge_backward(_ptr(grad_out), _ptr(x), _ptr(edge_attr), DTYPE[torch.float32], N, F,
+    _check(lib.pyg_propagate_edge_backward(_ptr(grad_out), _ptr(x), _ptr(edge_attr), DTYPE[dt], N, F,
                                            _ptr(edge_index), ctypes.byref(c), ctypes.byref(ct) if ct else None,
                                            _ptr(_map_t(map_t, E)), ORDER[order], MSG[msg], AGGR[aggr], _ptr(argmax),
                                            _ptr(gx), _ptr(ge), _ptr(workspace), workspace.numel(), _stream(dev)),
@@ -832,7 +836,7 @@ class PropagateEdge(torch.autograd.Function):
     """Differentiable propagate with F-dimensional edge features (Eq. (1)):
     phi = x_j + e, max(x_j + e, 0) or x_j * e on the CSR segment kernel;
     gradients for x and the edge features (COO edge order) by
-    pyg_propagate_edge_backward (fp32). Use as
+    pyg_propagate_edge_backward (fp32 or bf16). Use as
     PropagateEdge.apply(x, edge_attr, graph, msg, aggr)."""
 
     @staticmethod

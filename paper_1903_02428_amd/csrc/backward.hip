@@ -17,7 +17,8 @@
 // gradient with respect to the edge features and gate or scale the one with
 // respect to x; sum / mean run the segment kernel over the reversed graph
 // (edge rows reached through the transpose map or the edge ids), the edge
-// gradient is one pass over the CSR slots; max routes as above. fp32 only.
+// gradient is one pass over the CSR slots; max routes as above. fp32 or bf16
+// operands; bf16 gradients keep fp32 intermediates and are rounded once.
 #include "common.hpp"
 
 #ifndef PYG_SDDMM_U
@@ -309,17 +310,64 @@ int backward_typed(const void *grad_out, const void *x, int dtype, int64_t N, in
     return PYG_OK;
 }
 
+// V consecutive elements of p as floats / stored from floats: V = 4 is one
+// 16-byte fp32 or 8-byte bf16 vector, V = 8 one 16-byte bf16 vector or two
+// fp32 ones (the caller checks alignment).
+template <typename T, int V>
+__device__ __forceinline__ void ldv(const T *p, float (&o)[V]) {
+    if constexpr (V == 1) {
+        o[0] = ld(p, 0);
+    } else if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int h = 0; h < V / 4; ++h) {
+            const float4 v = reinterpret_cast<const float4 *>(p)[h];
+            o[4 * h] = v.x, o[4 * h + 1] = v.y, o[4 * h + 2] = v.z, o[4 * h + 3] = v.w;
+        }
+    } else if constexpr (V == 4) {
+        const uint2 v = *reinterpret_cast<const uint2 *>(p);
+        o[0] = bf16_bits_to_f32(v.x & 0xFFFFu), o[1] = bf16_bits_to_f32(v.x >> 16);
+        o[2] = bf16_bits_to_f32(v.y & 0xFFFFu), o[3] = bf16_bits_to_f32(v.y >> 16);
+    } else {
+        const uint4 v = *reinterpret_cast<const uint4 *>(p);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int h = 0; h < 4; ++h)
+            o[2 * h] = bf16_bits_to_f32(w[h] & 0xFFFFu), o[2 * h + 1] = bf16_bits_to_f32(w[h] >> 16);
+    }
+}
+
+template <typename T, int V>
+__device__ __forceinline__ void stv(T *p, const float (&o)[V]) {
+    if constexpr (V == 1) {
+        st(p, 0, o[0]);
+    } else if constexpr (sizeof(T) == 4) {
+#pragma unroll
+        for (int h = 0; h < V / 4; ++h)
+            reinterpret_cast<float4 *>(p)[h] = make_float4(o[4 * h], o[4 * h + 1], o[4 * h + 2], o[4 * h + 3]);
+    } else {
+        uint32_t w[V / 2];
+#pragma unroll
+        for (int h = 0; h < V / 2; ++h)
+            w[h] = uint32_t(f32_to_bf16_rne(o[2 * h])) | (uint32_t(f32_to_bf16_rne(o[2 * h + 1])) << 16);
+        if constexpr (V == 4)
+            *reinterpret_cast<uint2 *>(p) = make_uint2(w[0], w[1]);
+        else
+            *reinterpret_cast<uint4 *>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+}
+
 // grad_e[row(p)] for every CSR slot p = (j -> i): d = gs[i] (the scaled
-// upstream gradient), times [x_j + e > 0] (relu) or x_j (mul); the edge row
-// is p (CSR order) or perm[p] (COO order). One wavefront per chunk of slots;
-// sub-groups of L lanes take one slot each, V floats per lane (V = 4: 16-byte
-// vectors when F % 4 == 0 and the arrays are aligned).
-template <int V>
-__global__ __launch_bounds__(kBlock) void k_edge_grad(const float *__restrict__ gs, const float *__restrict__ x,
-                                                      const float *__restrict__ ea, int64_t N, int64_t F,
+// upstream gradient, fp32 or the bf16 gradient itself under sum), times
+// [x_j + e > 0] (relu) or x_j (mul), in fp32, rounded once into T; the edge
+// row is p (CSR order) or perm[p] (COO order). One wavefront per chunk of
+// slots; sub-groups of L lanes take one slot each, V elements per lane
+// (V = 4 or 8: vectors when V divides F and the arrays are aligned).
+template <typename TG, typename T, int V>
+__global__ __launch_bounds__(kBlock) void k_edge_grad(const TG *__restrict__ gs, const T *__restrict__ x,
+                                                      const T *__restrict__ ea, int64_t N, int64_t F,
                                                       const int64_t *__restrict__ rowptr, const int32_t *__restrict__ col,
                                                       const int64_t *__restrict__ perm, int64_t E, int64_t chunk, int lg,
-                                                      int msg, float *__restrict__ ge) {
+                                                      int msg, T *__restrict__ ge) {
     const int lane = threadIdx.x & (kWave - 1);
     const int L = 1 << lg, S = kWave >> lg;
     const int q = lane & (L - 1), sg = lane >> lg;
@@ -336,30 +384,16 @@ __global__ __launch_bounds__(kBlock) void k_edge_grad(const float *__restrict__ 
             const int64_t er = perm ? perm[p] : p;
             for (int64_t f = (int64_t)q * V; f < F; f += (int64_t)L * V) {
                 float d[V], o[V];
-                if constexpr (V == 4) {
-                    const float4 g4 = *reinterpret_cast<const float4 *>(gs + r * F + f);
-                    d[0] = g4.x, d[1] = g4.y, d[2] = g4.z, d[3] = g4.w;
-                } else {
-                    d[0] = gs[r * F + f];
-                }
+                ldv<TG, V>(gs + r * F + f, d);
                 if (msg == PYG_MSG_EDGE_ADD) {
 #pragma unroll
                     for (int v = 0; v < V; ++v) o[v] = d[v];
                 } else {
-                    float xv[V], ev[V];
-                    if constexpr (V == 4) {
-                        const float4 x4 = *reinterpret_cast<const float4 *>(x + j * F + f);
-                        xv[0] = x4.x, xv[1] = x4.y, xv[2] = x4.z, xv[3] = x4.w;
-                    } else {
-                        xv[0] = x[j * F + f];
-                    }
+                    float xv[V];
+                    ldv<T, V>(x + j * F + f, xv);
                     if (msg == PYG_MSG_EDGE_RELU) {
-                        if constexpr (V == 4) {
-                            const float4 e4 = *reinterpret_cast<const float4 *>(ea + er * F + f);
-                            ev[0] = e4.x, ev[1] = e4.y, ev[2] = e4.z, ev[3] = e4.w;
-                        } else {
-                            ev[0] = ea[er * F + f];
-                        }
+                        float ev[V];
+                        ldv<T, V>(ea + er * F + f, ev);
 #pragma unroll
                         for (int v = 0; v < V; ++v) o[v] = xv[v] + ev[v] > 0.f ? d[v] : 0.f;
                     } else {
@@ -367,10 +401,7 @@ __global__ __launch_bounds__(kBlock) void k_edge_grad(const float *__restrict__ 
                         for (int v = 0; v < V; ++v) o[v] = d[v] * xv[v];
                     }
                 }
-                if constexpr (V == 4)
-                    *reinterpret_cast<float4 *>(ge + er * F + f) = make_float4(o[0], o[1], o[2], o[3]);
-                else
-                    ge[er * F + f] = o[0];
+                stv<T, V>(ge + er * F + f, o);
             }
         }
         if (t >= e1) break;
@@ -379,13 +410,14 @@ __global__ __launch_bounds__(kBlock) void k_edge_grad(const float *__restrict__ 
 }
 
 // Max: the winning edge k of each output element (i, f) receives g[i, f]:
-// grad_x[j, f] += g * dphi/dx (atomics), grad_e[row(k), f] = g * dphi/de (one
-// writer per element). Edge rows: k (COO order) or inv[k] (CSR order).
-__global__ void k_edge_max_backward(const float *__restrict__ g, const float *__restrict__ x,
-                                    const float *__restrict__ ea, int64_t N, int64_t F,
-                                    const int64_t *__restrict__ src, int64_t E, const int32_t *__restrict__ inv,
-                                    const int64_t *__restrict__ argmax, int msg, float *__restrict__ gx,
-                                    float *__restrict__ ge) {
+// grad_x[j, f] += g * dphi/dx (fp32 atomics into gx), grad_e[row(k), f] =
+// g * dphi/de (one writer per element, rounded once into T). Edge rows: k
+// (COO order) or inv[k] (CSR order).
+template <typename T>
+__global__ void k_edge_max_backward(const T *__restrict__ g, const T *__restrict__ x, const T *__restrict__ ea,
+                                    int64_t N, int64_t F, const int64_t *__restrict__ src, int64_t E,
+                                    const int32_t *__restrict__ inv, const int64_t *__restrict__ argmax, int msg,
+                                    float *__restrict__ gx, T *__restrict__ ge) {
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < N * F; t += (int64_t)gridDim.x * blockDim.x) {
         const int64_t k = argmax[t];
         if (k < 0 || k >= E) continue;  // empty row (sentinel E)
@@ -393,10 +425,10 @@ __global__ void k_edge_max_backward(const float *__restrict__ g, const float *__
         const int64_t j = src[k];
         const int64_t er = inv ? inv[k] : k;
         if (er < 0 || er >= E) continue;  // a malformed permutation: stay in bounds
-        const float d = g[t];
+        const float d = ld(g, t);
         float dx = d, de = d;
         if (msg != PYG_MSG_EDGE_ADD) {
-            const float xv = x[j * F + f], ev = ea[er * F + f];
+            const float xv = ld(x, j * F + f), ev = ld(ea, er * F + f);
             if (msg == PYG_MSG_EDGE_RELU) {
                 const float on = xv + ev > 0.f ? 1.f : 0.f;
                 dx = d * on;
@@ -407,12 +439,21 @@ __global__ void k_edge_max_backward(const float *__restrict__ g, const float *__
             }
         }
         if (gx) unsafeAtomicAdd(&gx[j * F + f], dx);
-        if (ge) ge[er * F + f] = de;
+        if (ge) st(ge, er * F + f, de);
     }
 }
 
+// fp32 scratch of the edge-message backward. bf16 keeps every intermediate
+// in fp32 and rounds each gradient once: max and mean accumulate grad_x in
+// gx32; mean also widens x and the edge rows (relu / mul) so that the
+// reversed-graph reduction reads the fp32 scaled gradient beside fp32
+// operands. bf16 sum needs none of these: its reduction reads the bf16
+// gradient directly and rounds once itself.
 struct EdgeBwdWs {
     float *gs;
+    float *gx32;
+    float *x32;
+    float *ea32;
     int32_t *inv;
     int32_t *map;
     void *seg;
@@ -420,16 +461,139 @@ struct EdgeBwdWs {
     size_t bytes;
 };
 
-EdgeBwdWs carve_edge_bwd(void *base, int64_t N, int64_t F, int64_t E, int aggr, int64_t chunk_t) {
+EdgeBwdWs carve_edge_bwd(void *base, int dtype, int64_t N, int64_t F, int64_t E, int msg, int aggr, int64_t chunk_t) {
+    const bool bf16 = dtype == PYG_BF16;
+    const bool widen = bf16 && aggr == PYG_MEAN && msg != PYG_MSG_EDGE_ADD;
     Carver c(base);
     EdgeBwdWs w{};
     w.gs = c.take<float>(aggr == PYG_MEAN ? N * F : 0);
+    w.gx32 = c.take<float>(bf16 && aggr != PYG_SUM ? N * F : 0);
+    w.x32 = c.take<float>(widen ? N * F : 0);
+    w.ea32 = c.take<float>(widen ? E * F : 0);
     w.inv = c.take<int32_t>(E);
     w.map = c.take<int32_t>(aggr == PYG_MAX ? 0 : E);
     w.seg_bytes = aggr == PYG_MAX ? 0 : segment_workspace(E, F, PYG_SUM, chunk_t, N);
     w.seg = c.take<char>(static_cast<int64_t>(w.seg_bytes));
     w.bytes = c.used + 256;
     return w;
+}
+
+template <typename TG, typename T>
+int launch_edge_grad(const TG *gs, const T *x, const T *ea, int64_t N, int64_t F, const pyg_csr *csr,
+                     const int64_t *perm, int64_t E, int msg, T *ge, hipStream_t s) {
+    // widest vector: 16 bytes of T per lane (4 fp32, 8 bf16)
+    const auto fits = [&](int v) {
+        const auto al = [](const void *p, size_t b) { return reinterpret_cast<uintptr_t>(p) % b == 0; };
+        return F % v == 0 && al(gs, v * sizeof(TG)) && (msg == PYG_MSG_EDGE_ADD || al(x, v * sizeof(T))) &&
+               (msg != PYG_MSG_EDGE_RELU || al(ea, v * sizeof(T))) && al(ge, v * sizeof(T));
+    };
+    const int V = sizeof(T) == 2 && fits(8) ? 8 : fits(4) ? 4 : 1;
+    const int64_t nv = F / V;
+    int lg = 0;
+    while ((int64_t(1) << lg) < nv && lg < 6) ++lg;
+    constexpr int64_t kChunk = 1024;
+    const unsigned grid = static_cast<unsigned>(((E + kChunk - 1) / kChunk + 3) / 4);
+    if (V == 8)
+        k_edge_grad<TG, T, 8><<<grid, kBlock, 0, s>>>(gs, x, ea, N, F, csr->rowptr, csr->col, perm, E, kChunk, lg,
+                                                      msg, ge);
+    else if (V == 4)
+        k_edge_grad<TG, T, 4><<<grid, kBlock, 0, s>>>(gs, x, ea, N, F, csr->rowptr, csr->col, perm, E, kChunk, lg,
+                                                      msg, ge);
+    else
+        k_edge_grad<TG, T, 1><<<grid, kBlock, 0, s>>>(gs, x, ea, N, F, csr->rowptr, csr->col, perm, E, kChunk, lg,
+                                                      msg, ge);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
+
+// Sum / mean / max edge-message backward for T = float or bf16 bits; the
+// arguments are checked by the entry point.
+template <typename T>
+int edge_backward_typed(const T *g, const T *xf, const T *ea, int64_t N, int64_t F, const int64_t *edge_index,
+                        const pyg_csr *csr, const pyg_csr *csr_t, const int32_t *map_t, bool coo, int msg, int aggr,
+                        const int64_t *argmax, T *gx, T *ge, const EdgeBwdWs &w, hipStream_t s) {
+    constexpr bool bf16 = sizeof(T) == 2;
+    const int64_t E = csr->E, NF = N * F;
+    auto cast_gx = [&](const float *acc) -> int {
+        if (!bf16 || !gx || NF == 0) return PYG_OK;
+        k_cast_out<T><<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(acc, NF, gx);
+        PYG_LAUNCH_CHECK();
+        return PYG_OK;
+    };
+    if (aggr == PYG_MAX) {
+        float *acc = gx ? (bf16 ? w.gx32 : reinterpret_cast<float *>(gx)) : nullptr;
+        if (acc) PYG_TRY(fill<float>(acc, NF, 0.f, s));
+        if (ge) PYG_TRY(fill<T>(ge, E * F, T(0), s));  // +0 in fp32 and in bf16 bits
+        if (E > 0 && NF > 0) {
+            const int32_t *inv = nullptr;
+            if (!coo) {
+                PYG_TRY(inverse_perm(csr->perm, E, w.inv, s));
+                inv = w.inv;
+            }
+            k_edge_max_backward<T><<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(g, xf, ea, N, F, edge_index, E, inv,
+                                                                              argmax, msg, acc, ge);
+            PYG_LAUNCH_CHECK();
+        }
+        return cast_gx(acc);
+    }
+    if (NF == 0) return PYG_OK;
+    // d = s g in fp32 (mean: s_i = 1 / deg_i); sum reads grad_out directly
+    // in its own type (the reductions widen each element as they load it)
+    if (aggr == PYG_MEAN) {
+        k_scale_rows<T><<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(g, csr->rowptr, N, F, 1, w.gs);
+        PYG_LAUNCH_CHECK();
+    }
+    const bool widen = bf16 && aggr == PYG_MEAN && msg != PYG_MSG_EDGE_ADD;
+    if (gx) {
+        SegmentArgs a{};
+        a.x = aggr == PYG_MEAN ? static_cast<const void *>(w.gs) : static_cast<const void *>(g);
+        a.dtype = aggr == PYG_MEAN || !bf16 ? PYG_F32 : PYG_BF16;
+        a.F = F;
+        a.rowptr = csr_t->rowptr;
+        a.col = csr_t->col;
+        a.n_rows = N;
+        a.E = E;
+        a.aggr = PYG_SUM;
+        a.chunk = csr_t->chunk;
+        a.sentinel = E;
+        a.out = bf16 && aggr == PYG_MEAN ? static_cast<void *>(w.gx32) : static_cast<void *>(gx);
+        a.hint = true;
+        a.msg = PYG_MSG_SRC;  // x_j + e: the scaled gradient of every outgoing edge
+        if (msg != PYG_MSG_EDGE_ADD && E > 0) {
+            a.msg = msg == PYG_MSG_EDGE_MUL ? PYG_MSG_EDGE_MUL : kSegMsgEdgeReluGrad;
+            a.edge_attr = ea;
+            a.x_self = xf;
+            if (widen) {  // fp32 operands beside the fp32 scaled gradient
+                k_scale_rows<T><<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(xf, nullptr, N, F, 0, w.x32);
+                PYG_LAUNCH_CHECK();
+                k_scale_rows<T><<<grid_for(E * F, kBlock * 4), kBlock, 0, s>>>(ea, nullptr, E, F, 0, w.ea32);
+                PYG_LAUNCH_CHECK();
+                a.edge_attr = w.ea32;
+                a.x_self = w.x32;
+            }
+            if (coo) {
+                a.attr_perm = csr_t->perm;  // slot q of csr_t is COO edge perm_t[q]
+            } else {
+                const int32_t *map = map_t;
+                if (!map) {
+                    PYG_TRY(transpose_map(csr, csr_t, w.inv, w.map, s));
+                    map = w.map;
+                }
+                a.attr_idx = map;
+            }
+        }
+        PYG_TRY(segment_reduce(a, w.seg, w.seg_bytes, s));
+        if (aggr == PYG_MEAN) PYG_TRY(cast_gx(w.gx32));
+    }
+    if (ge && E > 0 && F > 0) {
+        const int64_t *perm = coo ? csr->perm : nullptr;
+        if (aggr == PYG_MEAN || !bf16)
+            PYG_TRY((launch_edge_grad<float, T>(aggr == PYG_MEAN ? w.gs : reinterpret_cast<const float *>(g), xf, ea, N,
+                                                F, csr, perm, E, msg, ge, s)));
+        else
+            PYG_TRY((launch_edge_grad<T, T>(g, xf, ea, N, F, csr, perm, E, msg, ge, s)));
+    }
+    return PYG_OK;
 }
 
 bool csr_matches(const pyg_csr *c, int64_t N, int64_t E) {
@@ -495,14 +659,14 @@ extern "C" int pyg_propagate_backward(const void *grad_out, const void *x, int d
                                  grad_x, grad_w, w, s);
 }
 
-extern "C" int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr,
+extern "C" int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int msg, int aggr,
                                                      int64_t chunk_t, size_t *bytes) {
     if (!bytes || N < 0 || F < 0 || E < 0 || chunk_t < 0) return PYG_ERR_INVALID_ARG;
+    if (dtype != PYG_F32 && dtype != PYG_BF16) return PYG_ERR_INVALID_ARG;
+    if (msg != PYG_MSG_EDGE_ADD && msg != PYG_MSG_EDGE_RELU && msg != PYG_MSG_EDGE_MUL) return PYG_ERR_INVALID_ARG;
     if (aggr != PYG_SUM && aggr != PYG_MEAN && aggr != PYG_MAX) return PYG_ERR_INVALID_ARG;
-    if (dtype == PYG_BF16) return PYG_ERR_UNSUPPORTED;
-    if (dtype != PYG_F32) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
-    *bytes = carve_edge_bwd(nullptr, N, F, E, aggr, chunk_t).bytes;
+    *bytes = carve_edge_bwd(nullptr, dtype, N, F, E, msg, aggr, chunk_t).bytes;
     return PYG_OK;
 }
 
@@ -511,8 +675,7 @@ extern "C" int pyg_propagate_edge_backward(const void *grad_out, const void *x, 
                                            const pyg_csr *csr_t, const int32_t *map_t, int attr_order, int msg,
                                            int aggr, const int64_t *argmax, void *grad_x, void *grad_edge_attr,
                                            void *ws, size_t ws_bytes, void *stream) {
-    if (dtype == PYG_BF16) return PYG_ERR_UNSUPPORTED;
-    if (dtype != PYG_F32 || N < 0 || F < 0 || !csr) return PYG_ERR_INVALID_ARG;
+    if ((dtype != PYG_F32 && dtype != PYG_BF16) || N < 0 || F < 0 || !csr) return PYG_ERR_INVALID_ARG;
     if (msg != PYG_MSG_EDGE_ADD && msg != PYG_MSG_EDGE_RELU && msg != PYG_MSG_EDGE_MUL) return PYG_ERR_INVALID_ARG;
     if (aggr != PYG_SUM && aggr != PYG_MEAN && aggr != PYG_MAX) return PYG_ERR_INVALID_ARG;
     if (attr_order != PYG_ORDER_CSR && attr_order != PYG_ORDER_COO) return PYG_ERR_INVALID_ARG;
@@ -525,11 +688,6 @@ extern "C" int pyg_propagate_edge_backward(const void *grad_out, const void *x, 
     if (msg != PYG_MSG_EDGE_ADD && N * F > 0 && (!x || (E * F > 0 && !edge_attr))) return PYG_ERR_INVALID_ARG;
     const bool coo = attr_order == PYG_ORDER_COO;
     const int64_t NF = N * F;
-    const float *g = static_cast<const float *>(grad_out);
-    const float *xf = static_cast<const float *>(x);
-    const float *ea = static_cast<const float *>(edge_attr);
-    float *gx = static_cast<float *>(grad_x);
-    float *ge = static_cast<float *>(grad_edge_attr);
     int64_t chunk_t = 0;
     if (aggr == PYG_MAX) {
         if (NF > 0 && !argmax) return PYG_ERR_INVALID_ARG;
@@ -537,8 +695,8 @@ extern "C" int pyg_propagate_edge_backward(const void *grad_out, const void *x, 
         if (E > 0 && !coo && !csr->perm) return PYG_ERR_INVALID_ARG;  // edge id -> CSR slot
     } else {
         if (!csr->rowptr || (E > 0 && !csr->col)) return PYG_ERR_INVALID_ARG;
-        if (ge && coo && E > 0 && !csr->perm) return PYG_ERR_INVALID_ARG;
-        if (gx) {
+        if (grad_edge_attr && coo && E > 0 && !csr->perm) return PYG_ERR_INVALID_ARG;
+        if (grad_x) {
             if (!csr_t || csr_t->N != N || csr_t->E != E || !csr_t->rowptr || csr_t->chunk < 0 ||
                 (E > 0 && !csr_t->col))
                 return PYG_ERR_INVALID_ARG;
@@ -550,80 +708,17 @@ extern "C" int pyg_propagate_edge_backward(const void *grad_out, const void *x, 
         }
     }
     size_t need;
-    PYG_TRY(pyg_propagate_edge_backward_workspace(dtype, N, F, E, aggr, chunk_t, &need));
+    PYG_TRY(pyg_propagate_edge_backward_workspace(dtype, N, F, E, msg, aggr, chunk_t, &need));
     if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const EdgeBwdWs w = carve_edge_bwd(ws, N, F, E, aggr, chunk_t);
-    if (aggr == PYG_MAX) {
-        if (gx) PYG_TRY(fill<float>(gx, NF, 0.f, s));
-        if (ge) PYG_TRY(fill<float>(ge, E * F, 0.f, s));
-        if (E == 0 || NF == 0) return PYG_OK;
-        const int32_t *inv = nullptr;
-        if (!coo) {
-            PYG_TRY(inverse_perm(csr->perm, E, w.inv, s));
-            inv = w.inv;
-        }
-        k_edge_max_backward<<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(g, xf, ea, N, F, edge_index, E, inv, argmax,
-                                                                       msg, gx, ge);
-        PYG_LAUNCH_CHECK();
-        return PYG_OK;
-    }
-    if (NF == 0) return PYG_OK;
-    // d = s g in fp32 (mean: s_i = 1 / deg_i; sum reads grad_out directly)
-    const float *gs = g;
-    if (aggr == PYG_MEAN) {
-        k_scale_rows<float><<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(g, csr->rowptr, N, F, 1, w.gs);
-        PYG_LAUNCH_CHECK();
-        gs = w.gs;
-    }
-    if (gx) {
-        SegmentArgs a{};
-        a.x = gs;
-        a.dtype = PYG_F32;
-        a.F = F;
-        a.rowptr = csr_t->rowptr;
-        a.col = csr_t->col;
-        a.n_rows = N;
-        a.E = E;
-        a.aggr = PYG_SUM;
-        a.chunk = csr_t->chunk;
-        a.sentinel = E;
-        a.out = gx;
-        a.hint = true;
-        a.msg = PYG_MSG_SRC;  // x_j + e: the scaled gradient of every outgoing edge
-        if (msg != PYG_MSG_EDGE_ADD && E > 0) {
-            a.msg = msg == PYG_MSG_EDGE_MUL ? PYG_MSG_EDGE_MUL : kSegMsgEdgeReluGrad;
-            a.edge_attr = ea;
-            a.x_self = xf;
-            if (coo) {
-                a.attr_perm = csr_t->perm;  // slot q of csr_t is COO edge perm_t[q]
-            } else {
-                const int32_t *map = map_t;
-                if (!map) {
-                    PYG_TRY(transpose_map(csr, csr_t, w.inv, w.map, s));
-                    map = w.map;
-                }
-                a.attr_idx = map;
-            }
-        }
-        PYG_TRY(segment_reduce(a, w.seg, w.seg_bytes, s));
-    }
-    if (ge && E > 0 && F > 0) {
-        const bool vec = F % 4 == 0 && reinterpret_cast<uintptr_t>(gs) % 16 == 0 &&
-                         (msg == PYG_MSG_EDGE_ADD || reinterpret_cast<uintptr_t>(xf) % 16 == 0) &&
-                         (msg != PYG_MSG_EDGE_RELU || reinterpret_cast<uintptr_t>(ea) % 16 == 0) &&
-                         reinterpret_cast<uintptr_t>(ge) % 16 == 0;
-        const int64_t nv = vec ? F / 4 : F;
-        int lg = 0;
-        while ((int64_t(1) << lg) < nv && lg < 6) ++lg;
-        constexpr int64_t kChunk = 1024;
-        const unsigned grid = static_cast<unsigned>(((E + kChunk - 1) / kChunk + 3) / 4);
-        const int64_t *perm = coo ? csr->perm : nullptr;
-        if (vec)
-            k_edge_grad<4><<<grid, kBlock, 0, s>>>(gs, xf, ea, N, F, csr->rowptr, csr->col, perm, E, kChunk, lg, msg, ge);
-        else
-            k_edge_grad<1><<<grid, kBlock, 0, s>>>(gs, xf, ea, N, F, csr->rowptr, csr->col, perm, E, kChunk, lg, msg, ge);
-        PYG_LAUNCH_CHECK();
-    }
-    return PYG_OK;
+    const EdgeBwdWs w = carve_edge_bwd(ws, dtype, N, F, E, msg, aggr, chunk_t);
+    if (dtype == PYG_BF16)
+        return edge_backward_typed<uint16_t>(static_cast<const uint16_t *>(grad_out), static_cast<const uint16_t *>(x),
+                                             static_cast<const uint16_t *>(edge_attr), N, F, edge_index, csr, csr_t,
+                                             map_t, coo, msg, aggr, argmax, static_cast<uint16_t *>(grad_x),
+                                             static_cast<uint16_t *>(grad_edge_attr), w, s);
+    return edge_backward_typed<float>(static_cast<const float *>(grad_out), static_cast<const float *>(x),
+                                      static_cast<const float *>(edge_attr), N, F, edge_index, csr, csr_t, map_t, coo,
+                                      msg, aggr, argmax, static_cast<float *>(grad_x),
+                                      static_cast<float *>(grad_edge_attr), w, s);
 }

@@ -280,7 +280,7 @@ def test_edge_backward_rejects_bad_arguments(lib):
         ctypes.c_void_p(0x500000)
     eb = lib.pyg_propagate_edge_backward
     RELU, ADD, SUM, MAX = 3, 2, 0, 2
-    assert eb(G, X, EA, 1, 10, 4, FAKE, good, good, None, 0, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == -5  # bf16
+    assert eb(G, X, EA, 2, 10, 4, FAKE, good, good, None, 0, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID
     assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 0, 0, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID  # msg
     assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 2, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID
     assert eb(G, X, EA, 0, 10, 4, FAKE, None, good, None, 0, RELU, SUM, None, GX, GE, FAKE, 1 << 30, None) == INVALID
@@ -291,3 +291,31 @@ def test_edge_backward_rejects_bad_arguments(lib):
     assert eb(G, X, EA, 0, 10, 4, None, good, good, None, 0, RELU, MAX, FAKE, GX, GE, FAKE, 1 << 30, None) == INVALID
     assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 0, RELU, MAX, None, GX, GE, FAKE, 1 << 30, None) == INVALID
     assert eb(G, X, EA, 0, 10, 4, FAKE, good, good, None, 0, ADD, SUM, None, GX, GE, FAKE, 0, None) == WORKSPACE
+
+
+def test_edge_backward_workspace_sizes(lib):
+    """bf16 adds only fp32 scratch: none under sum, grad_x's N*F*4 under
+    max and mean, and under mean with relu / mul also x and the edge rows
+    widened (N*F*4 + E*F*4). Sizes here are multiples of the 256-byte carve
+    alignment, so the differences are exact."""
+    ws = lib.pyg_propagate_edge_backward_workspace
+    N, F, E = 1000, 16, 5000
+    ADD, RELU, MUL, SUM, MEAN, MAX = 2, 3, 4, 0, 1, 2
+
+    def q(dt, msg, aggr, chunk=0):
+        sz = ctypes.c_size_t()
+        assert ws(dt, N, F, E, msg, aggr, chunk, ctypes.byref(sz)) == 0
+        return sz.value
+
+    for msg in (ADD, RELU, MUL):
+        assert q(1, msg, SUM) == q(0, msg, SUM)
+        assert q(1, msg, MAX) == q(0, msg, MAX) + N * F * 4
+    assert q(1, ADD, MEAN) == q(0, ADD, MEAN) + N * F * 4
+    for msg in (RELU, MUL):
+        assert q(1, msg, MEAN) == q(0, msg, MEAN) + 2 * N * F * 4 + E * F * 4
+    sz = ctypes.c_size_t()
+    assert ws(2, N, F, E, RELU, SUM, 0, ctypes.byref(sz)) == INVALID  # dtype
+    assert ws(0, N, F, E, 0, SUM, 0, ctypes.byref(sz)) == INVALID  # not an edge-feature message
+    assert ws(0, N, F, E, RELU, 3, 0, ctypes.byref(sz)) == INVALID
+    assert ws(0, N, F, E, RELU, SUM, 0, None) == INVALID
+    assert ws(0, N, F, 1 << 31, RELU, SUM, 0, ctypes.byref(sz)) == -5

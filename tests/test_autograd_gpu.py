@@ -65,3 +65,31 @@ def test_propagate_edge_autograd(pyg, msg, aggr):
     rx, re, sx, se = oracle.propagate_edge_backward(x, ei, ea, g, msg, aggr, argmax=arg)
     check_sum(xt.grad, rx, sx, False, f"PropagateEdge {msg} {aggr} grad_x")
     check_sum(et.grad, re, se, False, f"PropagateEdge {msg} {aggr} grad_e")
+
+
+@pytest.mark.parametrize("aggr", ["sum", "mean", "max"])
+def test_propagate_edge_autograd_bf16(pyg, aggr):
+    """bf16 leaves: the gradients come back in bf16, against the oracle on
+    the bf16-rounded values."""
+    from tests.parity import bf16_round
+    rng = np.random.default_rng(91)
+    N, E, F = 600, 8000, 32
+    ei = synth.random_coo(rng, N, E)
+    x = bf16_round(rng.standard_normal((N, F)).astype(np.float32))
+    ea = bf16_round(rng.standard_normal((E, F)).astype(np.float32))
+    g = bf16_round(rng.standard_normal((N, F)).astype(np.float32))
+    graph = pyg.Graph(to_dev(ei), N)
+    for msg in ("edge_add", "edge_relu", "edge_mul"):
+        xt = to_dev(x).bfloat16().requires_grad_()
+        et = to_dev(ea).bfloat16().requires_grad_()
+        out = pyg.PropagateEdge.apply(xt, et, graph, msg, aggr)
+        assert out.dtype == torch.bfloat16
+        out.backward(to_dev(g).bfloat16())
+        torch.cuda.synchronize()
+        assert xt.grad.dtype == torch.bfloat16 and et.grad.dtype == torch.bfloat16
+        arg = None
+        if aggr == "max":
+            _, arg, _ = oracle.propagate(x, ei, msg=msg, aggr="max", edge_attr=ea)
+        rx, re, sx, se = oracle.propagate_edge_backward(x, ei, ea, g, msg, aggr, argmax=arg)
+        check_sum(xt.grad, rx, sx, True, f"PropagateEdge bf16 {msg} {aggr} grad_x")
+        check_sum(et.grad, re, se, True, f"PropagateEdge bf16 {msg} {aggr} grad_e")

@@ -345,22 +345,27 @@ def test_c5_edge_features_sampled(pyg, c5, dev_graph):
     torch.cuda.empty_cache()
 
 
-def test_c5_edge_backward_sampled(pyg, c5, dev_graph):
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_c5_edge_backward_sampled(pyg, c5, dev_graph, dtype):
     """The backward of the benchmark's edge-feature call (max(x_j + e, 0),
-    sum, features in CSR slot order, fp32): grad_x on sampled nodes (all
-    their outgoing edges in the oracle's sub-graph) and grad_e on every
-    edge of that sub-graph."""
+    sum, features in CSR slot order, fp32 and bf16): grad_x on sampled nodes
+    (all their outgoing edges in the oracle's sub-graph) and grad_e on every
+    edge of that sub-graph. bf16: the oracle sees the bf16-rounded values."""
     from synth.hashed import hashed_matrix, hashed_values
+    bf16 = dtype == torch.bfloat16
     ei_np, x_np, N = c5["edge_index_gcn"], c5["x"], c5["N"]
     ei, _, csr = dev_graph
     E, F = ei_np.shape[1], x_np.shape[1]
     plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E)
     csr_t = pyg.coo_to_csr(pyg.reverse_edges(ei), N, chunk=csr.chunk)
     map_t = pyg.csr_transpose_map(plain, csr_t)
-    ea_csr = hashed_matrix(E, F, seed=43, device="cuda")[csr.perm]  # row k of the generator = COO edge k
+    ea_csr = hashed_matrix(E, F, seed=43, device="cuda")[csr.perm].to(dtype)  # row k of the generator = COO edge k
     g = np.random.default_rng(80).standard_normal((N, F)).astype(np.float32)
-    gx, ge = pyg.propagate_edge_backward(to_dev(g), to_dev(x_np), ea_csr, plain, "edge_relu", "sum", "csr",
-                                         csr_t=csr_t, map_t=map_t)
+    xs = x_np
+    if bf16:
+        g, xs = bf16_round(g), bf16_round(x_np)
+    gx, ge = pyg.propagate_edge_backward(to_dev(g).to(dtype), to_dev(xs).to(dtype), ea_csr, plain, "edge_relu", "sum",
+                                         "csr", csr_t=csr_t, map_t=map_t)
     torch.cuda.synchronize()
     del ea_csr
     nodes = sample_rows(c5, n=200)[0]
@@ -368,13 +373,15 @@ def test_c5_edge_backward_sampled(pyg, c5, dev_graph):
     kidx = np.nonzero(keep)[0]
     sub = np.ascontiguousarray(ei_np[:, keep])
     ea_sub = hashed_values(torch.from_numpy(kidx), F, seed=43).numpy()
-    rx, re, sx, se = oracle.propagate_edge_backward(x_np, sub, ea_sub, g, "edge_relu", "sum")
-    check_sum(gx[to_dev(nodes)].cpu(), rx[nodes], sx[nodes], False, "C5 edge backward grad_x")
+    if bf16:
+        ea_sub = bf16_round(ea_sub)
+    rx, re, sx, se = oracle.propagate_edge_backward(xs, sub, ea_sub, g, "edge_relu", "sum")
+    check_sum(gx[to_dev(nodes)].cpu(), rx[nodes], sx[nodes], bf16, f"C5 edge backward {dtype} grad_x")
     _, _, perm = oracle.coo_to_csr(ei_np, N)
     inv = np.empty_like(perm)
     inv[perm] = np.arange(E)
-    check_sum(ge[to_dev(inv[kidx])].cpu(), re, se, False, "C5 edge backward grad_e")
-    print("[c5] edge backward ok", flush=True)
+    check_sum(ge[to_dev(inv[kidx])].cpu(), re, se, bf16, f"C5 edge backward {dtype} grad_e")
+    print(f"[c5] edge backward {dtype} ok", flush=True)
     del gx, ge, csr_t, map_t
     torch.cuda.empty_cache()
 
