@@ -11,7 +11,8 @@ already resident in HBM:
 
 `value` is E*F of the step's propagate divided by the step time
 (edges*features/s). The `roofline` object covers the dominant call, the CSR
-propagate, timed with HIP events on the launch stream inside the timed steps.
+propagate (its feature-window launches together), timed with HIP events on
+the launch stream inside the timed steps.
 `cpu_baseline` times the oracle (single-threaded plain C loop) on a bounded
 sample of the same workload. `detail` adds per-call times and the COO-vs-CSR,
 fp32-vs-bf16 and sum-vs-mean comparison.
@@ -36,14 +37,15 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 
 # Byte counters of the CSR propagate kernel (k_segment, fp32 weighted sum on
 # the large power-law graph) from two rocprofv3 --pmc runs of this script
-# (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), with the same counters on a
+# (FETCH_SIZE, then WRITE_SIZE, KiB per propagate call: the sum over its
+# feature-window dispatches), with the same counters on a
 # plain 1024 MiB device copy for scale; see profiles/propagate_c5_counters.md.
 # They describe the kernel sources with the recorded hash only: after any
 # change to those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "ba08e129b788c024",
-    "fetch_kib": 22248112.1, "write_kib": 128824.4,
-    "copy_mib": 1024, "copy_fetch_kib": 524312.6, "copy_write_kib": 1048576.0,
+    "source_hash": "14252b9a1e5c00ae",
+    "fetch_kib": 18501630.5, "write_kib": 133369.5,
+    "copy_mib": 1024, "copy_fetch_kib": 524307.9, "copy_write_kib": 1048576.0,
 }
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp"]
 
@@ -267,8 +269,11 @@ def main():
                    "step": "coo_to_csr+degree(csr row bounds)+gcn_norm(csr order)+propagate(sum,csr)+global_pool(mean)"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
-                     "kernel": "pyg_propagate CSR segment (k_segment + k_segment_fixup), fp32 weighted sum",
-                     "bytes_per_launch": balg, "avg_launch_ms": t_prop * 1e3},
+                     "kernel": "pyg_propagate CSR segment, fp32 weighted sum: one k_segment launch per "
+                               "128-byte feature window (F*4/128 = %d) and one k_segment_fixup" % (F * 4 // 128),
+                     "unit_of_work": "one propagate call (all its window launches): every edge gathers its "
+                                     "source row once in total",
+                     "bytes_per_call": balg, "avg_call_ms": t_prop * 1e3},
         "detail": {"per_call_ms": {n: float(np.mean(times[n])) for n in names},
                    "propagate_edges_features_per_s": E * F / t_prop,
                    "degree_from_coo_ms": timed(torch, lambda: pyg.degree(ei, N, out=deg, workspace=ws_deg))},
