@@ -429,8 +429,8 @@ def small_configs(pyg, torch, dev, seed):
 
 def backward_calls(pyg, torch, x, ei, csr_w, N, E, F, dev):
     """The gradient of the propagate on the same graph (fp32): gcn-weighted
-    sum with the weight gradient, mean, and max routed through the
-    forward's argmax. The reversed CSR (with the weights) is preprocessing,
+    sum with the weight gradient (in COO edge order, and in CSR slot order),
+    mean, and max routed through the forward's argmax. The reversed CSR (with the weights) is preprocessing,
     built once. Algorithmic bytes: grad_x as the propagate over the reversed
     graph; grad_w one g row per target row, one x gather per edge, columns,
     the slot -> edge permutation and the weight written; max: argmax, g and
@@ -454,6 +454,11 @@ def backward_calls(pyg, torch, x, ei, csr_w, N, E, F, dev):
                                                      need_grad_w=True), reps=5)
     res["sum-weighted-grad_x+grad_w"] = rec(ms, b_alg_csr(N, E, F, 4) + rp + 4 * E + 8 * E + N * F * 4 + E * F * 4
                                            + 4 * E)
+    # grad_w in CSR slot order (the order of the CSR's weights): no scatter through perm
+    ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, w_coo, csr=csr_w, csr_t=csr_t, aggr="sum",
+                                                     need_grad_w=True, w_order="csr"), reps=5)
+    res["sum-weighted-grad_x+grad_w-csr-order"] = rec(ms, b_alg_csr(N, E, F, 4) + rp + 4 * E + N * F * 4
+                                                     + E * F * 4 + 4 * E)
     ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, None, csr=plain, csr_t=plain_t, aggr="mean"), reps=5)
     res["mean-grad_x"] = rec(ms, b_alg_csr(N, E, F, 4, weighted=False) + rp + 2 * N * F * 4)
     _, am = pyg.propagate(x, csr=plain, aggr="max")

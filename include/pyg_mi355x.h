@@ -272,13 +272,20 @@ int pyg_propagate_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E,
  *          weights: required for sum / mean;
  *   argmax the forward's argmax [N,F] (max only);
  *   grad_x [N,F] output in dtype (fp32 accumulation);
- *   grad_w fp32 [E] output in COO order, or NULL to skip it.
+ *   grad_w fp32 [E] output, or NULL to skip it, in w_order: PYG_ORDER_COO
+ *          (edge ids, the order of edge_weight) or PYG_ORDER_CSR (the slots
+ *          of csr, the order of csr->weight: coalesced stores, no scatter
+ *          through perm); max in CSR order needs csr (with perm) too.
  * sum / mean results are deterministic; max scatters with float atomics, so
- * colliding winners may sum in any order (last-bit differences). */
+ * colliding winners may sum in any order (last-bit differences).
+ * Errors: PYG_ERR_INVALID_ARG (bad dtype/msg/aggr/w_order, negative sizes,
+ * NULL or mismatched CSRs or arrays that the call needs, grad_w without
+ * weights, overlapping grad_x and inputs), PYG_ERR_UNSUPPORTED (N or
+ * E >= 2^31), PYG_ERR_WORKSPACE. */
 int pyg_propagate_backward(const void *grad_out, const void *x, int dtype, int64_t N, int64_t F,
                            const int64_t *edge_index, int64_t E, const float *edge_weight,
                            const pyg_csr *csr, const pyg_csr *csr_t, int msg, int aggr, const int64_t *argmax,
-                           void *grad_x, float *grad_w, void *ws, size_t ws_bytes, void *stream);
+                           void *grad_x, float *grad_w, int w_order, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_propagate_edge_backward (chunk_t = csr_t->chunk
  * when grad_x is wanted under sum / mean, else 0). bf16 adds fp32 scratch:

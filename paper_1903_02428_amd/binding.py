@@ -85,7 +85,7 @@ def library() -> ctypes.CDLL:
                                    ctypes.c_size_t, p],
             "pyg_propagate_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
             "pyg_propagate_backward": [p, p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr),
-                                       i32, i32, p, p, p, p, ctypes.c_size_t, p],
+                                       i32, i32, p, p, p, i32, p, ctypes.c_size_t, p],
             "pyg_propagate_edge_backward_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate_edge_backward": [p, p, p, i32, i64, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr), p,
                                             i32, i32, i32, p, p, p, p, ctypes.c_size_t, p],
@@ -384,9 +384,11 @@ def reverse_edges(edge_index: torch.Tensor) -> torch.Tensor:
 def propagate_backward(grad_out: torch.Tensor, x: torch.Tensor | None = None, edge_index: torch.Tensor | None = None,
                        edge_weight: torch.Tensor | None = None, csr: CSR | None = None, csr_t: CSR | None = None,
                        aggr: str = "sum", msg: str = "src", argmax: torch.Tensor | None = None,
-                       need_grad_w: bool = False, workspace: torch.Tensor | None = None):
+                       need_grad_w: bool = False, workspace: torch.Tensor | None = None, w_order: str = "coo"):
     """Gradient of propagate. Returns (grad_x, grad_w or None). csr_t is the
-    CSR of reverse_edges(edge_index) built with the same weights (sum/mean)."""
+    CSR of reverse_edges(edge_index) built with the same weights (sum/mean).
+    grad_w comes in `w_order`: "coo" (edge ids, like edge_weight) or "csr"
+    (the slots of csr, like csr.weight)."""
     lib = library()
     _need_cuda("grad_out", grad_out, None, 2)
     if grad_out.dtype not in DTYPE:
@@ -403,6 +405,8 @@ def propagate_backward(grad_out: torch.Tensor, x: torch.Tensor | None = None, ed
         _need_cuda("x", x, grad_out.dtype, 2)
     if edge_weight is not None:
         _need_cuda("edge_weight", edge_weight, torch.float32, 1)
+    if w_order not in ORDER:
+        raise ValueError("w_order must be 'coo' or 'csr'")
     grad_x = torch.empty_like(grad_out)
     grad_w = torch.empty(E, dtype=torch.float32, device=dev) if need_grad_w else None
     chunk_t = csr_t.chunk if csr_t is not None else 0
@@ -413,7 +417,7 @@ def propagate_backward(grad_out: torch.Tensor, x: torch.Tensor | None = None, ed
     rc = lib.pyg_propagate_backward(_ptr(grad_out), _ptr(x), DTYPE[grad_out.dtype], N, F, _ptr(edge_index), E,
                                     _ptr(edge_weight), ctypes.byref(c) if c is not None else None,
                                     ctypes.byref(ct) if ct is not None else None, MSG[msg], AGGR[aggr], _ptr(argmax),
-                                    _ptr(grad_x), _ptr(grad_w), _ptr(ws), ws.numel(), _stream(dev))
+                                    _ptr(grad_x), _ptr(grad_w), ORDER[w_order], _ptr(ws), ws.numel(), _stream(dev))
     _check(rc, "pyg_propagate_backward")
     return grad_x, grad_w
 

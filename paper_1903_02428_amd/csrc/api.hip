@@ -48,7 +48,7 @@ extern "C" const char *pyg_strerror(int status) {
     }
 }
 
-extern "C" int pyg_abi_version(void) { return 1; }
+extern "C" int pyg_abi_version(void) { return 2; }
 
 extern "C" int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int kernel, int64_t chunk,
                                        size_t *bytes) {

@@ -6,7 +6,9 @@
 //               difference messages add the self term -deg_i s_i g_i;
 //               grad_w[k] = s_i <g_i, x_j> by a CSR-ordered per-slot dot
 //               product (one g row per target row, one x gather per slot),
-//               written to COO order through perm - deterministic.
+//               written in CSR slot order (coalesced) or to COO order
+//               through perm (one scattered 4-byte store per edge, about a
+//               fifth of the call on the large graph) - deterministic.
 //   max         only the winning edge of each output element receives its
 //               gradient: hardware float atomics scatter w_k g into grad_x
 //               (and g x_j into grad_w), so sums of colliding winners may
@@ -67,7 +69,8 @@ __global__ void k_diff_self(float *__restrict__ gx, const T *__restrict__ g, con
     }
 }
 
-// grad_w[perm[p]] = s_i <g_i, x_{col[p]}> for every slot p of row i: one
+// grad_w[perm[p]] (or grad_w[p] when perm is NULL: CSR order) =
+// s_i <g_i, x_{col[p]}> for every slot p of row i: one
 // wavefront per chunk of slots; sub-groups of L lanes take one slot each and
 // reduce their partial dot products with an xor butterfly.
 template <typename T>
@@ -95,7 +98,7 @@ __global__ __launch_bounds__(kBlock) void k_sddmm(const T *__restrict__ g, const
                 for (int64_t f = q; f < F; f += L) acc = fmaf(ld(g, r * F + f), ld(x, j * F + f), acc);
             }
             for (int off = L >> 1; off > 0; off >>= 1) acc += __shfl_xor(acc, off, kWave);
-            if (p < b && q == 0) grad_w[perm[p]] = sc * acc;
+            if (p < b && q == 0) grad_w[perm ? perm[p] : p] = sc * acc;
         }
         if (t >= e1) break;
         ++r;
@@ -170,7 +173,7 @@ __global__ __launch_bounds__(kBlock) void k_sddmm_vec(const T *__restrict__ g, c
 #pragma unroll
             for (int k = 0; k < U; ++k) {
                 const int64_t p = k0 + (int64_t)k * S + sg;
-                if (q == 0 && p < b) grad_w[perm[p]] = sc * acc[k];
+                if (q == 0 && p < b) grad_w[perm ? perm[p] : p] = sc * acc[k];
             }
         }
         if (t >= e1) break;
@@ -178,11 +181,13 @@ __global__ __launch_bounds__(kBlock) void k_sddmm_vec(const T *__restrict__ g, c
     }
 }
 
-// Max: route every output element's gradient to its winning edge.
+// Max: route every output element's gradient to its winning edge; grad_w
+// entries at the edge id k, or at its CSR slot inv[k] (CSR order).
 template <typename T, bool DIFF>
 __global__ void k_max_backward(const T *__restrict__ g, const T *__restrict__ x, int64_t N, int64_t F,
                                const int64_t *__restrict__ ei, int64_t E, const float *__restrict__ w,
-                               const int64_t *__restrict__ argmax, float *__restrict__ acc, float *__restrict__ grad_w) {
+                               const int64_t *__restrict__ argmax, const int32_t *__restrict__ inv,
+                               float *__restrict__ acc, float *__restrict__ grad_w) {
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < N * F; t += (int64_t)gridDim.x * blockDim.x) {
         const int64_t k = argmax[t];
         if (k < 0 || k >= E) continue;  // empty row (sentinel E)
@@ -194,7 +199,10 @@ __global__ void k_max_backward(const T *__restrict__ g, const T *__restrict__ x,
             unsafeAtomicAdd(&acc[i * F + f], -gv);
         } else {
             unsafeAtomicAdd(&acc[j * F + f], w ? w[k] * gv : gv);
-            if (grad_w) unsafeAtomicAdd(&grad_w[k], gv * ld(x, j * F + f));
+            if (grad_w) {
+                const int64_t wk = inv ? inv[k] : k;
+                if (wk >= 0 && wk < E) unsafeAtomicAdd(&grad_w[wk], gv * ld(x, j * F + f));
+            }
         }
     }
 }
@@ -208,6 +216,7 @@ __global__ void k_cast_out(const float *__restrict__ acc, int64_t n, T *__restri
 struct BwdWs {
     void *gscaled;
     float *acc;
+    int32_t *inv;  // max: slot of every edge id (grad_w in CSR order)
     void *seg;
     size_t seg_bytes;
     size_t bytes;
@@ -220,6 +229,7 @@ BwdWs carve_bwd(void *base, int dtype, int64_t N, int64_t F, int64_t E, int aggr
     BwdWs w{};
     w.gscaled = c.take<float>(aggr != PYG_MAX && (aggr == PYG_MEAN || bf16) ? N * F : 0);
     w.acc = c.take<float>(bf16 ? N * F : 0);
+    w.inv = c.take<int32_t>(aggr == PYG_MAX ? E : 0);
     w.seg_bytes = aggr == PYG_MAX ? 0 : segment_workspace(E, F, PYG_SUM, chunk_t, N);
     w.seg = c.take<char>(w.seg_bytes);
     w.bytes = c.used + 256;
@@ -229,7 +239,8 @@ BwdWs carve_bwd(void *base, int dtype, int64_t N, int64_t F, int64_t E, int aggr
 template <typename T>
 int backward_typed(const void *grad_out, const void *x, int dtype, int64_t N, int64_t F, const int64_t *ei, int64_t E,
                    const float *ew, const pyg_csr *csr, const pyg_csr *csr_t, int msg, int aggr, const int64_t *argmax,
-                   void *grad_x, float *grad_w, const BwdWs &w, hipStream_t s) {
+                   void *grad_x, float *grad_w, int w_order, const BwdWs &w, hipStream_t s) {
+    const bool w_csr = w_order == PYG_ORDER_CSR;
     const T *g = static_cast<const T *>(grad_out);
     const int64_t NF = N * F;
     if (grad_w) PYG_TRY(fill<float>(grad_w, E, 0.f, s));
@@ -237,12 +248,17 @@ int backward_typed(const void *grad_out, const void *x, int dtype, int64_t N, in
         float *acc = sizeof(T) == 4 ? static_cast<float *>(grad_x) : w.acc;
         PYG_TRY(fill<float>(acc, NF, 0.f, s));
         if (E > 0) {
+            const int32_t *inv = nullptr;
+            if (grad_w && w_csr) {
+                PYG_TRY(inverse_perm(csr->perm, E, w.inv, s));
+                inv = w.inv;
+            }
             if (msg == PYG_MSG_DIFF)
                 k_max_backward<T, true><<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(g, static_cast<const T *>(x), N, F, ei, E,
-                                                                                     ew, argmax, acc, nullptr);
+                                                                                     ew, argmax, nullptr, acc, nullptr);
             else
                 k_max_backward<T, false><<<grid_for(NF, kBlock * 4), kBlock, 0, s>>>(g, static_cast<const T *>(x), N, F, ei, E,
-                                                                                      ew, argmax, acc, grad_w);
+                                                                                      ew, argmax, inv, acc, grad_w);
             PYG_LAUNCH_CHECK();
         }
         if (sizeof(T) == 2) {
@@ -298,12 +314,13 @@ int backward_typed(const void *grad_out, const void *x, int dtype, int64_t N, in
             int lg = 0;
             while ((int64_t(1) << lg) < F / EP && lg < 6) ++lg;
             k_sddmm_vec<T, PYG_SDDMM_U><<<grid, kBlock, 0, s>>>(g, static_cast<const T *>(x), N, F, csr->rowptr, csr->col,
-                                                      csr->perm, E, kChunk, lg, aggr == PYG_MEAN, grad_w);
+                                                      w_csr ? nullptr : csr->perm, E, kChunk, lg, aggr == PYG_MEAN,
+                                                      grad_w);
         } else {
             int lg = 0;
             while ((1 << lg) < F && lg < 6) ++lg;
-            k_sddmm<T><<<grid, kBlock, 0, s>>>(g, static_cast<const T *>(x), N, F, csr->rowptr, csr->col, csr->perm,
-                                               E, kChunk, lg, aggr == PYG_MEAN, grad_w);
+            k_sddmm<T><<<grid, kBlock, 0, s>>>(g, static_cast<const T *>(x), N, F, csr->rowptr, csr->col,
+                                               w_csr ? nullptr : csr->perm, E, kChunk, lg, aggr == PYG_MEAN, grad_w);
         }
         PYG_LAUNCH_CHECK();
     }
@@ -618,9 +635,10 @@ extern "C" int pyg_propagate_backward_workspace(int dtype, int64_t N, int64_t F,
 extern "C" int pyg_propagate_backward(const void *grad_out, const void *x, int dtype, int64_t N, int64_t F,
                                       const int64_t *edge_index, int64_t E, const float *edge_weight,
                                       const pyg_csr *csr, const pyg_csr *csr_t, int msg, int aggr,
-                                      const int64_t *argmax, void *grad_x, float *grad_w, void *ws, size_t ws_bytes,
-                                      void *stream) {
+                                      const int64_t *argmax, void *grad_x, float *grad_w, int w_order, void *ws,
+                                      size_t ws_bytes, void *stream) {
     if ((dtype != PYG_F32 && dtype != PYG_BF16) || N < 0 || F < 0 || E < 0) return PYG_ERR_INVALID_ARG;
+    if (w_order != PYG_ORDER_CSR && w_order != PYG_ORDER_COO) return PYG_ERR_INVALID_ARG;
     if (aggr != PYG_SUM && aggr != PYG_MEAN && aggr != PYG_MAX) return PYG_ERR_INVALID_ARG;
     if (msg != PYG_MSG_SRC && msg != PYG_MSG_DIFF) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
@@ -641,11 +659,14 @@ extern "C" int pyg_propagate_backward(const void *grad_out, const void *x, int d
     if (aggr == PYG_MAX) {
         if (N * F > 0 && !argmax) return PYG_ERR_INVALID_ARG;
         if (E > 0 && !edge_index) return PYG_ERR_INVALID_ARG;
+        // grad_w in CSR order: the edge id -> slot map comes from csr->perm
+        if (grad_w && w_order == PYG_ORDER_CSR && E > 0 && (!csr_matches(csr, N, E) || !csr->perm))
+            return PYG_ERR_INVALID_ARG;
     } else {
         if (!csr_matches(csr_t, N, E)) return PYG_ERR_INVALID_ARG;
         if (weighted != (csr_t->weight != nullptr)) return PYG_ERR_INVALID_ARG;
         if ((aggr == PYG_MEAN || msg == PYG_MSG_DIFF || grad_w) && !csr_matches(csr, N, E)) return PYG_ERR_INVALID_ARG;
-        if (grad_w && E > 0 && !csr->perm) return PYG_ERR_INVALID_ARG;
+        if (grad_w && w_order == PYG_ORDER_COO && E > 0 && !csr->perm) return PYG_ERR_INVALID_ARG;
         chunk_t = csr_t->chunk;
     }
     const BwdWs w = carve_bwd(ws, dtype, N, F, E, aggr, chunk_t);
@@ -654,9 +675,9 @@ extern "C" int pyg_propagate_backward(const void *grad_out, const void *x, int d
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (dtype == PYG_BF16)
         return backward_typed<uint16_t>(grad_out, x, dtype, N, F, edge_index, E, edge_weight, csr, csr_t, msg, aggr,
-                                        argmax, grad_x, grad_w, w, s);
+                                        argmax, grad_x, grad_w, w_order, w, s);
     return backward_typed<float>(grad_out, x, dtype, N, F, edge_index, E, edge_weight, csr, csr_t, msg, aggr, argmax,
-                                 grad_x, grad_w, w, s);
+                                 grad_x, grad_w, w_order, w, s);
 }
 
 extern "C" int pyg_propagate_edge_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int msg, int aggr,

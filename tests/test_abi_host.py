@@ -38,7 +38,7 @@ def test_exports_every_declared_symbol(lib):
 
 def test_version_and_strerror(lib):
     import paper_1903_02428_amd as pyg
-    assert pyg.abi_version() == 1
+    assert pyg.abi_version() == 2
     for code, text in ((0, "success"), (-1, "invalid argument"), (-3, "workspace too small"),
                        (-4, "HIP runtime or launch error"), (-5, "unsupported size or combination"), (7, "unknown status")):
         assert pyg.strerror(code) == text
@@ -319,3 +319,15 @@ def test_edge_backward_workspace_sizes(lib):
     assert ws(0, N, F, E, RELU, 3, 0, ctypes.byref(sz)) == INVALID
     assert ws(0, N, F, E, RELU, SUM, 0, None) == INVALID
     assert ws(0, N, F, 1 << 31, RELU, SUM, 0, ctypes.byref(sz)) == -5
+
+
+def test_backward_rejects_bad_grad_w_order(lib):
+    from paper_1903_02428_amd.binding import _Csr
+    good = ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, 0x60000, 10, 20, 0))
+    G, X, GX, GW = FAKE, ctypes.c_void_p(0x200000), ctypes.c_void_p(0x400000), ctypes.c_void_p(0x500000)
+    bw = lib.pyg_propagate_backward
+    SUM, MAX, CSR, COO = 0, 2, 0, 1
+    assert bw(G, X, 0, 10, 4, FAKE, 20, FAKE, good, good, 0, SUM, None, GX, GW, 7, FAKE, 1 << 30, None) == INVALID
+    # max with grad_w in CSR order needs the forward CSR (its perm maps edge ids to slots)
+    assert bw(G, X, 0, 10, 4, FAKE, 20, FAKE, None, None, 0, MAX, FAKE, GX, GW, CSR, FAKE, 1 << 30, None) == INVALID
+    assert bw(G, X, 0, 10, 4, FAKE, 20, FAKE, None, None, 0, MAX, FAKE, GX, GW, COO, FAKE, 0, None) == WORKSPACE

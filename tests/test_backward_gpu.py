@@ -129,3 +129,38 @@ def test_autograd_function(pyg):
         rx, rw, sx, sw = oracle.propagate_backward(x, ei, g, w, aggr=aggr, argmax=arg, want_grad_w=True)
         check_sum(xt.grad, rx, sx, what=f"autograd grad_x {aggr}")
         check_sum(wt.grad, rw, sw, what=f"autograd grad_w {aggr}")
+
+
+@pytest.mark.parametrize("aggr", ["sum", "mean", "max"])
+@pytest.mark.parametrize("dtype", [F32, BF16], ids=["f32", "bf16"])
+def test_backward_grad_w_csr_order(pyg, aggr, dtype):
+    """grad_w in CSR slot order: under sum / mean the same dot products as the
+    COO order, stored at the slot instead of the edge id (bit for bit); under
+    max the atomically summed entries against the oracle, re-ordered by the
+    CSR permutation."""
+    for i, (N, E, F) in enumerate([(300, 5000, 16), (2000, 30000, 64), (700, 9000, 128), (257, 4000, 260)]):
+        rng = np.random.default_rng(300 + i)
+        ei = synth.random_coo(rng, N, E)
+        x = rng.standard_normal((N, F)).astype(np.float32)
+        g = rng.standard_normal((N, F)).astype(np.float32)
+        w = rng.standard_normal(E).astype(np.float32)
+        if dtype == BF16:
+            x, g = bf16_round(x), bf16_round(g)
+        d_ei, d_w = to_dev(ei), to_dev(w)
+        csr = pyg.coo_to_csr(d_ei, N, d_w)
+        csr_t = pyg.coo_to_csr(pyg.reverse_edges(d_ei), N, d_w)
+        _, _, perm = oracle.coo_to_csr(ei, N)
+        argmax = None
+        if aggr == "max":
+            _, argmax, _ = oracle.propagate(x, ei, w, aggr="max")
+        args = dict(argmax=to_dev(argmax) if argmax is not None else None, need_grad_w=True)
+        gd, xd = to_dev(g).to(dtype), to_dev(x).to(dtype)
+        gx_coo, gw_coo = pyg.propagate_backward(gd, xd, d_ei, d_w, csr, csr_t, aggr, **args)
+        gx_csr, gw_csr = pyg.propagate_backward(gd, xd, d_ei, d_w, csr, csr_t, aggr, w_order="csr", **args)
+        torch.cuda.synchronize()
+        tag = f"grad_w csr order N={N} E={E} F={F} {aggr} {dtype}"
+        if aggr != "max":
+            assert torch.equal(gx_csr, gx_coo), tag
+            assert torch.equal(gw_csr, gw_coo[torch.from_numpy(perm).cuda()]), tag
+        _, ref_w, _, sw = oracle.propagate_backward(x, ei, g, w, aggr=aggr, argmax=argmax, want_grad_w=True)
+        check_sum(gw_csr, ref_w[perm], sw[perm], False, tag)

@@ -128,6 +128,11 @@ def test_c5_propagate_backward_sampled(pyg, c5, dev_graph):
     rx, rw, sx, sw = oracle.propagate_backward(x_np, sub, g, w_ref[keep], aggr="sum", want_grad_w=True)
     check_sum(gx_s[to_dev(nodes)].cpu(), rx[nodes], sx[nodes], False, "C5 backward sum grad_x")
     check_sum(gw_s[to_dev(kidx)].cpu(), rw, sw, False, "C5 backward sum grad_w")
+    # grad_w in CSR slot order (as the benchmark also times it): the same values at the slots
+    _, gw_c = pyg.propagate_backward(g32, x32, ei, w, csr=csr, csr_t=csr_t, aggr="sum", need_grad_w=True,
+                                     w_order="csr")
+    assert torch.equal(gw_c, gw_s[csr.perm]), "C5 backward sum grad_w in CSR order"
+    del gw_c
     gm = (g.astype(np.float64) / np.maximum(deg, 1.0)[:, None]).astype(np.float32)  # rounded like the kernel's s*g
     rxm, _, sxm, _ = oracle.propagate_backward(x_np, sub, gm, aggr="sum")
     check_sum(gx_m[to_dev(nodes)].cpu(), rxm[nodes], sxm[nodes], False, "C5 backward mean grad_x")
