@@ -570,7 +570,8 @@ def attention(pyg, torch, x, ei, csr, N, E, F, dev, H=8):
 def gcn_layer(pyg, torch, x, csr_w, N, E, F, dev, Fo=128):
     """One GCN layer on the same graph in bf16 storage: X Theta on the matrix
     cores (bf16 operands, fp32 accumulation, bf16 out), then the
-    gcn_norm-weighted CSR propagate of the result. Theta ~ N(0, 1/F)."""
+    gcn_norm-weighted CSR propagate of the result. Theta ~ N(0, 1/F). The
+    same layer in fp32 (fp32 operands and output) beside it."""
     gen = torch.Generator(device=dev)
     gen.manual_seed(11)
     xb = x.to(torch.bfloat16)
@@ -589,13 +590,31 @@ def gcn_layer(pyg, torch, x, csr_w, N, E, F, dev, Fo=128):
     t_l = timed(torch, layer)
     bytes_d = N * F * 2 + F * Fo * 2 + N * Fo * 2
     flops = 2.0 * N * F * Fo
+    # the same layer in fp32 (fp32 operands on the fp32 matrix-core path, the same Theta values)
+    theta32 = theta.float()
+    h32 = torch.empty(N, Fo, dtype=torch.float32, device=dev)
+    o32 = torch.empty_like(h32)
+    ws_p32 = torch.empty(pyg.propagate_workspace_bytes(h32, E, "sum", "csr", csr_w.chunk), dtype=torch.uint8,
+                         device=dev)
+    t_d32 = timed(torch, lambda: pyg.dense_transform(x, theta32, torch.float32, out=h32, workspace=ws_d))
+
+    def layer32():
+        pyg.dense_transform(x, theta32, torch.float32, out=h32, workspace=ws_d)
+        pyg.propagate(h32, csr=csr_w, aggr="sum", out=o32, workspace=ws_p32)
+    t_l32 = timed(torch, layer32)
+    bytes_d32 = N * F * 4 + F * Fo * 4 + N * Fo * 4
     return {"F_in": F, "F_out": Fo, "dtype": "bf16 storage, fp32 accumulation",
             "dense_transform": {"ms": t_d, "alg_GBps": bytes_d / (t_d * 1e-3) / 1e9,
                                 "hbm_frac": bytes_d / (t_d * 1e-3) / 1e9 / HBM_PEAK_GBS,
                                 "TFLOPs": flops / (t_d * 1e-3) / 1e12, "mfma_bf16_frac": flops / (t_d * 1e-3) / 2.5e15,
                                 "bytes": bytes_d},
             "propagate_bf16": {"ms": t_p, "alg_GBps": b_alg_csr(N, E, Fo, 2) / (t_p * 1e-3) / 1e9},
-            "layer": {"ms": t_l, "edges_features_per_s": E * Fo / (t_l * 1e-3)}}
+            "layer": {"ms": t_l, "edges_features_per_s": E * Fo / (t_l * 1e-3)},
+            "dense_transform_f32": {"ms": t_d32, "alg_GBps": bytes_d32 / (t_d32 * 1e-3) / 1e9,
+                                    "hbm_frac": bytes_d32 / (t_d32 * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                                    "TFLOPs": flops / (t_d32 * 1e-3) / 1e12,
+                                    "mfma_f32_frac": flops / (t_d32 * 1e-3) / 157.3e12, "bytes": bytes_d32},
+            "layer_f32": {"ms": t_l32, "edges_features_per_s": E * Fo / (t_l32 * 1e-3)}}
 
 
 def edge_features(pyg, torch, x, ei, csr, N, E, F, dev):

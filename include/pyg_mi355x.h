@@ -444,19 +444,21 @@ int pyg_gat_scores_backward(const float *a_src, const float *a_dst, int64_t H, f
  * layer multiplies the features by a weight matrix around the normalised
  * aggregation, A (X Theta) = (A X) Theta). */
 
-/* Workspace bytes needed by pyg_dense_transform (Theta transposed and padded). */
+/* Workspace bytes needed by pyg_dense_transform (Theta transposed and padded,
+ * enough for either operand type). */
 int pyg_dense_transform_workspace(int64_t Fi, int64_t Fo, size_t *bytes);
 
-/* out[n, o] = sum_k x[n, k] * theta[k, o] on the matrix cores (bf16
- * operands, fp32 accumulation of exact bf16 products).
- *   x      [N, Fi] bf16 (x_dtype must be PYG_BF16; PYG_F32 returns
- *          PYG_ERR_UNSUPPORTED), 16-byte aligned rows (Fi % 8 == 0) take the
- *          vector path;
- *   theta  [Fi, Fo] bf16 row-major;
+/* out[n, o] = sum_k x[n, k] * theta[k, o] on the matrix cores, fp32
+ * accumulation: bf16 operands (exact products, v_mfma_f32_16x16x32_bf16) or
+ * fp32 operands (v_mfma_f32_16x16x4_f32).
+ *   x      [N, Fi] in x_dtype (PYG_BF16 or PYG_F32); 16-byte aligned rows
+ *          (Fi % 8 == 0 for bf16, Fi % 4 == 0 for fp32) take the vector path;
+ *   theta  [Fi, Fo] row-major, in x_dtype;
  *   out    [N, Fo] in out_dtype (PYG_F32, or PYG_BF16 rounded once), may not
  *          overlap x.
- * Deterministic. Errors: PYG_ERR_INVALID_ARG (NULL pointers, negative sizes,
- * overlap), PYG_ERR_UNSUPPORTED (fp32 x, N >= 2^31), PYG_ERR_WORKSPACE. */
+ * Deterministic. Errors: PYG_ERR_INVALID_ARG (bad dtypes, NULL pointers,
+ * negative sizes, overlap), PYG_ERR_UNSUPPORTED (N >= 2^31, Fi or Fo >=
+ * 2^24), PYG_ERR_WORKSPACE. */
 int pyg_dense_transform(const void *x, int x_dtype, int64_t N, int64_t Fi, const void *theta, int64_t Fo,
                         void *out, int out_dtype, void *ws, size_t ws_bytes, void *stream);
 

@@ -677,13 +677,14 @@ def gat_scores_backward(a_src: torch.Tensor, a_dst: torch.Tensor, csr: CSR, csr_
 
 def dense_transform(x: torch.Tensor, theta: torch.Tensor, out_dtype=torch.float32, out: torch.Tensor | None = None,
                     workspace: torch.Tensor | None = None) -> torch.Tensor:
-    """x [N, Fi] (bf16) times theta [Fi, Fo] (bf16) on the matrix cores, fp32
-    accumulation; the result in out_dtype (float32 or bfloat16)."""
+    """x [N, Fi] times theta [Fi, Fo] (both bf16 or both float32) on the
+    matrix cores, fp32 accumulation; the result in out_dtype (float32 or
+    bfloat16)."""
     lib = library()
     _need_cuda("x", x, None, 2)
-    _need_cuda("theta", theta, torch.bfloat16, 2)
     if x.dtype not in DTYPE or out_dtype not in DTYPE:
         raise ValueError("x and out must be float32 or bfloat16")
+    _need_cuda("theta", theta, x.dtype, 2)
     N, Fi = x.shape
     if theta.shape[0] != Fi:
         raise ValueError("theta must be [Fi, Fo]")

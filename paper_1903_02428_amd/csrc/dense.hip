@@ -1,5 +1,6 @@
 // Dense feature transform of a GCN layer, out = X Theta, on the matrix cores
-// of gfx950 (v_mfma_f32_16x16x32_bf16: bf16 operands, fp32 accumulation).
+// of gfx950 (v_mfma_f32_16x16x32_bf16: bf16 operands, fp32 accumulation;
+// fp32 operands on v_mfma_f32_16x16x4_f32, below).
 //
 // Shapes on this path are tall and thin (N ~ 10^5 rows, Fi and Fo ~ 10^2),
 // so the transform is bound by reading X and writing out, not by the matrix
@@ -221,7 +222,96 @@ __global__ __launch_bounds__(kBlock) void k_dense(const uint16_t *__restrict__ x
     store_tile(out, N, Fo, r0, c0, li, lg, acc);
 }
 
+// ------------------------------------------------------------- fp32 operands
+// The same tiling with fp32 X and Theta on v_mfma_f32_16x16x4_f32 (16 x 16 x
+// 4, one k per lane group). A lane loads 16 bytes (4 consecutive k) of its X
+// row and of its Theta^T row and feeds them to four MFMA steps: at step e,
+// lane group lg holds k = 16 s + 4 lg + e in both operands, so the four
+// steps cover the 16 k of the block with A and B paired on the same k (the
+// order of the k inside a block is a relabelling of the sum, which the
+// matrix unit adds in fp32 either way). K is staged 64 at a time.
+constexpr int kChunkF = 64;
+constexpr int kLdsStrideF = kChunkF + 4;  // floats per LDS row; +16 B skews the banks
+
+__global__ void k_theta_t_f32(const float *__restrict__ theta, int64_t Fi, int64_t Fo, int64_t Kp, int64_t Fo_pad,
+                              float *__restrict__ tt) {
+    const int64_t n = Fo_pad * Kp;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t o = i / Kp, k = i % Kp;
+        tt[i] = (o < Fo && k < Fi) ? theta[k * Fo + o] : 0.f;
+    }
+}
+
+// X[row, k0 .. k0+3] (zeros outside the matrix); VEC: Fi % 4 == 0 and
+// 16-byte aligned rows, so the 4 values are one load.
+template <bool VEC>
+__device__ __forceinline__ f32x4 load_af(const float *__restrict__ x, int64_t N, int64_t Fi, int64_t row, int64_t k0) {
+    if (row >= N || k0 >= Fi) return f32x4{0.f, 0.f, 0.f, 0.f};
+    const float *p = x + row * Fi + k0;
+    if constexpr (VEC) {
+        return *reinterpret_cast<const f32x4 *>(p);
+    } else {
+        f32x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = (k0 + i < Fi) ? p[i] : 0.f;
+        return v;
+    }
+}
+
+template <typename TO, bool VEC>
+__global__ __launch_bounds__(kBlock) void k_dense_f32(const float *__restrict__ x, int64_t N, int64_t Fi, int64_t Kp,
+                                                      const float *__restrict__ tt, int64_t Fo, TO *__restrict__ out) {
+    __shared__ __align__(16) float lds[kCols * kLdsStrideF];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t r0 = (int64_t)blockIdx.x * (kRowsWave * (kBlock / kWave)) + wave * kRowsWave;
+    const int64_t c0 = (int64_t)blockIdx.y * kCols;
+    const int li = lane & 15, lg = lane >> 4;
+
+    f32x4 acc[2][8];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc[t][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    for (int64_t kc = 0; kc < Kp; kc += kChunkF) {
+        const int kn = static_cast<int>((Kp - kc) < kChunkF ? (Kp - kc) : kChunkF);  // multiple of 16
+        f32x4 a[2][kChunkF / 16];
+#pragma unroll
+        for (int st = 0; st < kChunkF / 16; ++st)
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+                a[t][st] = (st * 16 < kn) ? load_af<VEC>(x, N, Fi, r0 + 16 * t + li, kc + 16 * st + 4 * lg)
+                                          : f32x4{0.f, 0.f, 0.f, 0.f};
+        __syncthreads();
+        // stage Theta^T[c0 .. c0+127][kc .. kc+kn) (zeros past Fo), 16 B per thread and step
+        const int per_row = kn / 4;
+        for (int i = threadIdx.x; i < kCols * per_row; i += kBlock) {
+            const int n = i / per_row, q = i % per_row;
+            f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (c0 + n < Fo) v = *reinterpret_cast<const f32x4 *>(tt + (c0 + n) * Kp + kc + 4 * q);
+            *reinterpret_cast<f32x4 *>(lds + n * kLdsStrideF + 4 * q) = v;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int st = 0; st < kChunkF / 16; ++st) {
+            if (st * 16 >= kn) break;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const f32x4 b = *reinterpret_cast<const f32x4 *>(lds + (16 * u + li) * kLdsStrideF + 16 * st + 4 * lg);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[0][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[e], a[0][st][e], acc[0][u], 0, 0, 0);
+                    acc[1][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[e], a[1][st][e], acc[1][u], 0, 0, 0);
+                }
+            }
+        }
+    }
+    store_tile(out, N, Fo, r0, c0, li, lg, acc);
+}
+
 int64_t kpad(int64_t Fi) { return (Fi + 31) / 32 * 32; }
+int64_t kpadf(int64_t Fi) { return (Fi + 15) / 16 * 16; }
 int64_t fopad(int64_t Fo) { return (Fo + 15) / 16 * 16; }
 
 }  // namespace
@@ -232,7 +322,9 @@ using namespace pyg;
 extern "C" int pyg_dense_transform_workspace(int64_t Fi, int64_t Fo, size_t *bytes) {
     if (!bytes || Fi < 0 || Fo < 0) return PYG_ERR_INVALID_ARG;
     if (Fi >= (int64_t(1) << 24) || Fo >= (int64_t(1) << 24)) return PYG_ERR_UNSUPPORTED;
-    *bytes = align_up(static_cast<size_t>(fopad(Fo) * kpad(Fi)) * 2, 256);
+    // Theta^T padded: bf16 (K to 32) or fp32 (K to 16), whichever is larger
+    const size_t b16 = static_cast<size_t>(fopad(Fo) * kpad(Fi)) * 2, b32 = static_cast<size_t>(fopad(Fo) * kpadf(Fi)) * 4;
+    *bytes = align_up(b16 > b32 ? b16 : b32, 256);
     return PYG_OK;
 }
 
@@ -241,7 +333,6 @@ extern "C" int pyg_dense_transform(const void *x, int x_dtype, int64_t N, int64_
     if (N < 0 || Fi < 0 || Fo < 0) return PYG_ERR_INVALID_ARG;
     if (x_dtype != PYG_BF16 && x_dtype != PYG_F32) return PYG_ERR_INVALID_ARG;
     if (out_dtype != PYG_BF16 && out_dtype != PYG_F32) return PYG_ERR_INVALID_ARG;
-    if (x_dtype != PYG_BF16) return PYG_ERR_UNSUPPORTED;  // the matrix-core path takes bf16 operands
     if (N >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     if (N * Fo > 0 && !out) return PYG_ERR_INVALID_ARG;
     if (N * Fi > 0 && !x) return PYG_ERR_INVALID_ARG;
@@ -250,11 +341,31 @@ extern "C" int pyg_dense_transform(const void *x, int x_dtype, int64_t N, int64_
     PYG_TRY(pyg_dense_transform_workspace(Fi, Fo, &need));
     if (N * Fo == 0) return PYG_OK;
     if (!ws || ws_bytes < need) return PYG_ERR_WORKSPACE;
-    const int64_t osz = out_dtype == PYG_F32 ? 4 : 2;
+    const int64_t osz = out_dtype == PYG_F32 ? 4 : 2, xsz = x_dtype == PYG_F32 ? 4 : 2;
     const char *xb = static_cast<const char *>(x);
     const char *ob = static_cast<const char *>(out);
-    if (ob < xb + N * Fi * 2 && xb < ob + N * Fo * osz) return PYG_ERR_INVALID_ARG;  // out overlaps x
+    if (ob < xb + N * Fi * xsz && xb < ob + N * Fo * osz) return PYG_ERR_INVALID_ARG;  // out overlaps x
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (x_dtype == PYG_F32) {
+        const int64_t Kp = kpadf(Fi), Fp = fopad(Fo);
+        float *tt = static_cast<float *>(ws);
+        k_theta_t_f32<<<grid_for(Fp * Kp, kBlock * 4), kBlock, 0, s>>>(static_cast<const float *>(theta), Fi, Fo, Kp, Fp,
+                                                                       tt);
+        PYG_LAUNCH_CHECK();
+        const bool vec = Fi % 4 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
+        const dim3 grid(static_cast<unsigned>((N + kRowsWave * (kBlock / kWave) - 1) / (kRowsWave * (kBlock / kWave))),
+                        static_cast<unsigned>((Fo + kCols - 1) / kCols));
+        const float *xf = static_cast<const float *>(x);
+        if (out_dtype == PYG_F32) {
+            if (vec) k_dense_f32<float, true><<<grid, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<float *>(out));
+            else k_dense_f32<float, false><<<grid, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<float *>(out));
+        } else {
+            if (vec) k_dense_f32<uint16_t, true><<<grid, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<uint16_t *>(out));
+            else k_dense_f32<uint16_t, false><<<grid, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<uint16_t *>(out));
+        }
+        PYG_LAUNCH_CHECK();
+        return PYG_OK;
+    }
     const int64_t Kp = kpad(Fi), Fp = fopad(Fo);
     uint16_t *tt = static_cast<uint16_t *>(ws);
     k_theta_t<<<grid_for(Fp * Kp, kBlock * 4), kBlock, 0, s>>>(static_cast<const uint16_t *>(theta), Fi, Fo, Kp, Fp, tt);

@@ -194,7 +194,8 @@ def test_attention_entry_points_reject_bad_arguments(lib):
 def test_dense_transform_rejects_bad_arguments(lib):
     X, T, OUT = FAKE, ctypes.c_void_p(0x300000), ctypes.c_void_p(0x900000)
     dt = lib.pyg_dense_transform
-    assert dt(X, 0, 10, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == UNSUPPORTED   # fp32 operands
+    assert dt(X, 0, 10, 8, T, 4, OUT, 0, FAKE, 0, None) == WORKSPACE   # fp32 operands: accepted, checked further
+    assert dt(X, 0, 10, 8, T, 4, ctypes.c_void_p(0x10000 + 64), 0, FAKE, 1 << 30, None) == INVALID  # overlap (4-byte x)
     assert dt(X, 7, 10, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == INVALID       # bad dtype
     assert dt(X, 1, 10, 8, T, 4, OUT, 9, FAKE, 1 << 30, None) == INVALID       # bad out dtype
     assert dt(X, 1, -1, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == INVALID
@@ -205,7 +206,7 @@ def test_dense_transform_rejects_bad_arguments(lib):
     assert dt(X, 1, 10, 8, T, 4, ctypes.c_void_p(0x10000 + 32), 0, FAKE, 1 << 30, None) == INVALID  # overlap
     assert dt(X, 1, 2**31, 8, T, 4, OUT, 0, FAKE, 1 << 30, None) == UNSUPPORTED
     rc, b = _ws(lib.pyg_dense_transform_workspace, 602, 41)
-    assert rc == PYG_OK and b >= 48 * 608 * 2
+    assert rc == PYG_OK and b >= 48 * 608 * 2 and b >= 48 * 608 * 4  # bf16 or fp32 Theta^T
 
 
 def test_propagate_edge_rejects_bad_arguments(lib):

@@ -100,4 +100,5 @@ def test_forward_calls_degenerate(pyg, N, E, F):
     if F % 8 == 0:
         t = torch.randn(F, 16, device="cuda").to(torch.bfloat16)
         assert pyg.dense_transform(x.to(torch.bfloat16), t).shape == (N, 16)
+        assert pyg.dense_transform(x.float(), t.float()).shape == (N, 16)
     torch.cuda.synchronize()

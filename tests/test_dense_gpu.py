@@ -39,6 +39,43 @@ def test_dense_transform(pyg, out_dtype):
         check_sum(got, ref, sabs, out_dtype == torch.bfloat16, f"dense N={N} Fi={Fi} Fo={Fo} {out_dtype}")
 
 
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
+def test_dense_transform_f32_operands(pyg, out_dtype):
+    """fp32 X and Theta on the fp32 matrix-core path, against the fp64 oracle
+    on the same fp32 values (ragged shapes, Fi not a multiple of 4, several K
+    chunks of 64 and column passes of 128)."""
+    for i, (N, Fi, Fo) in enumerate(SHAPES + [(500, 66, 130), (64, 3, 200)]):
+        rng = np.random.default_rng(650 + i)
+        x = rng.standard_normal((N, Fi)).astype(np.float32)
+        t = (rng.standard_normal((Fi, Fo)) / np.sqrt(max(Fi, 1))).astype(np.float32)
+        got = pyg.dense_transform(to_dev(x), to_dev(t), out_dtype)
+        torch.cuda.synchronize()
+        assert got.dtype == out_dtype
+        ref, sabs = oracle.dense_transform(x, t)
+        check_sum(got, ref, sabs, out_dtype == torch.bfloat16, f"dense f32 N={N} Fi={Fi} Fo={Fo} {out_dtype}")
+
+
+def test_dense_transform_f32_unaligned_and_deterministic(pyg):
+    """An fp32 view whose rows start 4 bytes off a 16-byte boundary takes the
+    scalar loads; repeated calls give identical bits."""
+    rng = np.random.default_rng(19)
+    base_np = rng.standard_normal(301 * 64 + 1).astype(np.float32)
+    t_np = (rng.standard_normal((64, 48)) / 8).astype(np.float32)
+    base, t = to_dev(base_np), to_dev(t_np)
+    xo = base[1:].view(301, 64)
+    got = pyg.dense_transform(xo, t)
+    torch.cuda.synchronize()
+    ref, sabs = oracle.dense_transform(base_np[1:].reshape(301, 64), t_np)
+    check_sum(got, ref, sabs, False, "dense f32 unaligned")
+    x = torch.randn(5000, 128, device="cuda")
+    tt = torch.randn(128, 96, device="cuda") / 11
+    first = pyg.dense_transform(x, tt)
+    for _ in range(3):
+        assert torch.equal(pyg.dense_transform(x, tt), first)
+    with pytest.raises(ValueError):
+        pyg.dense_transform(x, tt.to(torch.bfloat16))  # operands of two types
+
+
 def test_dense_transform_unaligned_rows(pyg):
     """A view whose rows start off a 16-byte boundary takes the scalar path."""
     rng = np.random.default_rng(9)

@@ -404,3 +404,9 @@ def test_c5_dense_transform_sampled(pyg, c5):
         out = pyg.dense_transform(to_dev(xb).to(torch.bfloat16), to_dev(t).to(torch.bfloat16), odt)
         torch.cuda.synchronize()
         check_sum(out[to_dev(rows)], ref, sabs, odt == torch.bfloat16, f"C5 dense {odt}")
+    # fp32 operands (the fp32 matrix-core path) on the benchmark's fp32 features
+    t32 = (rng.standard_normal((128, 128)) / np.sqrt(128)).astype(np.float32)
+    ref32, sabs32 = oracle.dense_transform(x_np[rows], t32)
+    out = pyg.dense_transform(to_dev(x_np), to_dev(t32), torch.float32)
+    torch.cuda.synchronize()
+    check_sum(out[to_dev(rows)], ref32, sabs32, False, "C5 dense fp32 operands")
