@@ -231,6 +231,9 @@ __global__ __launch_bounds__(kBlock) void k_dense(const uint16_t *__restrict__ x
 // order of the k inside a block is a relabelling of the sum, which the
 // matrix unit adds in fp32 either way). K is staged 64 at a time.
 constexpr int kChunkF = 64;
+#ifndef PYG_DENSE_F32_PERSIST
+#define PYG_DENSE_F32_PERSIST 1
+#endif
 constexpr int kLdsStrideF = kChunkF + 4;  // floats per LDS row; +16 B skews the banks
 
 __global__ void k_theta_t_f32(const float *__restrict__ theta, int64_t Fi, int64_t Fo, int64_t Kp, int64_t Fo_pad,
@@ -296,18 +299,87 @@ __global__ __launch_bounds__(kBlock) void k_dense_f32(const float *__restrict__ 
 #pragma unroll
         for (int st = 0; st < kChunkF / 16; ++st) {
             if (st * 16 >= kn) break;
+            // all eight Theta^T operands first, then the steps e outermost: the 16
+            // accumulators are updated in turn, so no MFMA waits on the one before
+            f32x4 b[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const f32x4 b = *reinterpret_cast<const f32x4 *>(lds + (16 * u + li) * kLdsStrideF + 16 * st + 4 * lg);
+            for (int u = 0; u < 8; ++u)
+                b[u] = *reinterpret_cast<const f32x4 *>(lds + (16 * u + li) * kLdsStrideF + 16 * st + 4 * lg);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    acc[0][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[e], a[0][st][e], acc[0][u], 0, 0, 0);
-                    acc[1][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[e], a[1][st][e], acc[1][u], 0, 0, 0);
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    acc[0][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[u][e], a[0][st][e], acc[0][u], 0, 0, 0);
+                    acc[1][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(b[u][e], a[1][st][e], acc[1][u], 0, 0, 0);
                 }
-            }
         }
     }
     store_tile(out, N, Fo, r0, c0, li, lg, acc);
+}
+
+// Fi <= 128: persistent workgroups that stage the whole Theta^T (128 columns
+// x Kp <= 128 fp32, 66 KB) once and walk over row blocks, loading the next
+// block's X operands before multiplying the current ones, as the bf16 form.
+constexpr int kLdsStrideFS = 128 + 4;
+constexpr int64_t kPersistBlocksF = 512;  // 2 workgroups per CU (LDS)
+
+template <typename TO, bool VEC>
+__global__ __launch_bounds__(kBlock) void k_dense_small_f32(const float *__restrict__ x, int64_t N, int64_t Fi,
+                                                            int64_t Kp, const float *__restrict__ tt, int64_t Fo,
+                                                            TO *__restrict__ out, int64_t nblocks) {
+    __shared__ __align__(16) float lds[kCols * kLdsStrideFS];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int64_t c0 = (int64_t)blockIdx.y * kCols;
+    const int li = lane & 15, lg = lane >> 4;
+    const int kn = static_cast<int>(Kp);  // multiple of 16, at most 128
+    const int per_row = kn / 4;
+    for (int i = threadIdx.x; i < kCols * per_row; i += kBlock) {
+        const int n = i / per_row, q = i % per_row;
+        f32x4 v = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (c0 + n < Fo) v = *reinterpret_cast<const f32x4 *>(tt + (c0 + n) * Kp + 4 * q);
+        *reinterpret_cast<f32x4 *>(lds + n * kLdsStrideFS + 4 * q) = v;
+    }
+    __syncthreads();
+    constexpr int S = 128 / 16;
+    f32x4 a[2][S], an[2][S];
+    auto load_block = [&](int64_t b, f32x4 (&dst)[2][S]) {
+        const int64_t r0 = b * (kRowsWave * (kBlock / kWave)) + wave * kRowsWave;
+#pragma unroll
+        for (int st = 0; st < S; ++st)
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+                dst[t][st] = (st * 16 < kn) ? load_af<VEC>(x, N, Fi, r0 + 16 * t + li, 16 * st + 4 * lg)
+                                            : f32x4{0.f, 0.f, 0.f, 0.f};
+    };
+    int64_t b = blockIdx.x;
+    if (b < nblocks) load_block(b, a);
+    for (; b < nblocks; b += gridDim.x) {
+        if (b + gridDim.x < nblocks) load_block(b + gridDim.x, an);
+        f32x4 acc[2][8];
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc[t][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int st = 0; st < S; ++st) {
+            if (st * 16 >= kn) break;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const f32x4 bv = *reinterpret_cast<const f32x4 *>(lds + (16 * u + li) * kLdsStrideFS + 16 * st + 4 * lg);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[0][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv[e], a[0][st][e], acc[0][u], 0, 0, 0);
+                    acc[1][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(bv[e], a[1][st][e], acc[1][u], 0, 0, 0);
+                }
+            }
+        }
+        store_tile(out, N, Fo, b * (kRowsWave * (kBlock / kWave)) + wave * kRowsWave, c0, li, lg, acc);
+#pragma unroll
+        for (int st = 0; st < S; ++st)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) a[t][st] = an[t][st];
+    }
 }
 
 int64_t kpad(int64_t Fi) { return (Fi + 31) / 32 * 32; }
@@ -353,9 +425,23 @@ extern "C" int pyg_dense_transform(const void *x, int x_dtype, int64_t N, int64_
                                                                        tt);
         PYG_LAUNCH_CHECK();
         const bool vec = Fi % 4 == 0 && (reinterpret_cast<uintptr_t>(x) & 15) == 0;
-        const dim3 grid(static_cast<unsigned>((N + kRowsWave * (kBlock / kWave) - 1) / (kRowsWave * (kBlock / kWave))),
-                        static_cast<unsigned>((Fo + kCols - 1) / kCols));
+        const int64_t nblocks = (N + kRowsWave * (kBlock / kWave) - 1) / (kRowsWave * (kBlock / kWave));
+        const unsigned gy = static_cast<unsigned>((Fo + kCols - 1) / kCols);
+        const dim3 grid(static_cast<unsigned>(nblocks), gy);
         const float *xf = static_cast<const float *>(x);
+        if (Kp <= 128 && PYG_DENSE_F32_PERSIST) {  // persistent workgroups, Theta staged once
+            const int64_t iters = (nblocks + kPersistBlocksF - 1) / kPersistBlocksF;
+            const dim3 g(static_cast<unsigned>((nblocks + iters - 1) / iters), gy);
+            if (out_dtype == PYG_F32) {
+                if (vec) k_dense_small_f32<float, true><<<g, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<float *>(out), nblocks);
+                else k_dense_small_f32<float, false><<<g, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<float *>(out), nblocks);
+            } else {
+                if (vec) k_dense_small_f32<uint16_t, true><<<g, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<uint16_t *>(out), nblocks);
+                else k_dense_small_f32<uint16_t, false><<<g, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<uint16_t *>(out), nblocks);
+            }
+            PYG_LAUNCH_CHECK();
+            return PYG_OK;
+        }
         if (out_dtype == PYG_F32) {
             if (vec) k_dense_f32<float, true><<<grid, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<float *>(out));
             else k_dense_f32<float, false><<<grid, kBlock, 0, s>>>(xf, N, Fi, Kp, tt, Fo, static_cast<float *>(out));
