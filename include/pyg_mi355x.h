@@ -247,6 +247,27 @@ int pyg_propagate_edge(const void *x, int dtype, int64_t N, int64_t F, const int
                        const void *edge_attr, int attr_order, const pyg_csr *csr, int msg, int aggr, int kernel,
                        void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes needed by pyg_propagate_edge_encoded (kernel as passed to
+ * the call; chunk = csr->chunk for the CSR kernel, else 0). */
+int pyg_propagate_edge_encoded_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t D, int aggr, int kernel,
+                                         int64_t chunk, size_t *bytes);
+
+/* pyg_propagate_edge with edge features of another width D (Eq. (1)'s
+ * e_{j,i} in R^D): the features are first projected to F,
+ * e = edge_attr Theta_e, by the dense transform (matrix cores, fp32
+ * accumulation, e stored in dtype: rounded once for bf16), then propagated
+ * as pyg_propagate_edge does with that e.
+ *   edge_attr [E, D] in dtype and attr_order; theta_e [D, F] in dtype;
+ *   everything else as pyg_propagate_edge. The projected features live in
+ *   the workspace (E*F elements of dtype, then the two calls' workspaces).
+ * Errors: as pyg_propagate_edge and pyg_dense_transform, plus
+ * PYG_ERR_INVALID_ARG for NULL edge_attr or theta_e with E*D or D*F > 0 and
+ * for out or edge_attr overlapping the workspace. */
+int pyg_propagate_edge_encoded(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                               const void *edge_attr, int64_t D, const void *theta_e, int attr_order,
+                               const pyg_csr *csr, int msg, int aggr, int kernel, void *out, int64_t *argmax,
+                               void *ws, size_t ws_bytes, void *stream);
+
 /* Workspace bytes needed by pyg_propagate_backward (chunk_t = csr_t->chunk). */
 int pyg_propagate_backward_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int64_t chunk_t,
                                      size_t *bytes);

@@ -38,6 +38,7 @@ from .binding import (  # noqa: F401
     propagate_backward,
     propagate_edge,
     propagate_edge_backward,
+    propagate_edge_encoded,
     propagate_heads,
     propagate_heads_backward,
     propagate_workspace_bytes,

@@ -22,7 +22,8 @@ EXPORTED = [
     "pyg_coo_to_csr_workspace",
     "pyg_coo_to_csr", "pyg_gather_edges",
     "pyg_gcn_norm_workspace", "pyg_gcn_norm", "pyg_gcn_norm_csr_workspace", "pyg_gcn_norm_csr",
-    "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_edge", "pyg_propagate_backward_workspace",
+    "pyg_propagate_workspace", "pyg_propagate", "pyg_propagate_edge", "pyg_propagate_edge_encoded_workspace",
+    "pyg_propagate_edge_encoded", "pyg_propagate_backward_workspace",
     "pyg_propagate_backward", "pyg_propagate_edge_backward_workspace", "pyg_propagate_edge_backward",
     "pyg_segment_softmax_workspace", "pyg_segment_softmax", "pyg_gat_softmax", "pyg_segment_softmax_backward",
     "pyg_propagate_heads_workspace", "pyg_propagate_heads", "pyg_dense_transform_workspace", "pyg_dense_transform",
@@ -83,6 +84,9 @@ def library() -> ctypes.CDLL:
                               ctypes.c_size_t, p],
             "pyg_propagate_edge": [p, i32, i64, i64, p, i64, p, i32, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                                    ctypes.c_size_t, p],
+            "pyg_propagate_edge_encoded_workspace": [i32, i64, i64, i64, i64, i32, i32, i64, sz],
+            "pyg_propagate_edge_encoded": [p, i32, i64, i64, p, i64, p, i64, p, i32, ctypes.POINTER(_Csr), i32, i32,
+                                           i32, p, p, p, ctypes.c_size_t, p],
             "pyg_propagate_backward_workspace": [i32, i64, i64, i64, i32, i64, sz],
             "pyg_propagate_backward": [p, p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), ctypes.POINTER(_Csr),
                                        i32, i32, p, p, p, i32, p, ctypes.c_size_t, p],
@@ -373,6 +377,49 @@ def propagate_edge(x: torch.Tensor, edge_attr: torch.Tensor, edge_index: torch.T
                                 ctypes.byref(c) if c is not None else None, MSG[msg], AGGR[aggr], KERNEL[kernel],
                                 _ptr(out), _ptr(argmax), _ptr(workspace), workspace.numel(), _stream(dev))
     _check(rc, "pyg_propagate_edge")
+    return out, argmax
+
+
+def propagate_edge_encoded(x: torch.Tensor, edge_attr: torch.Tensor, theta_e: torch.Tensor,
+                           edge_index: torch.Tensor | None = None, csr: CSR | None = None, msg: str = "edge_add",
+                           aggr: str = "sum", kernel: str = "auto", attr_order: str = "coo",
+                           out: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+    """propagate_edge with D-dimensional edge features projected to F first:
+    e = edge_attr [E, D] @ theta_e [D, F] (the matrix-core transform, e in
+    x's dtype), then the edge-feature message with e. Returns (out, argmax
+    or None)."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    if x.dtype not in DTYPE:
+        raise ValueError("x must be float32 or bfloat16")
+    N, F = x.shape
+    dev = x.device
+    if edge_index is not None:
+        E = _edge_index(edge_index)
+    elif csr is not None:
+        E = csr.E
+    else:
+        raise ValueError("need edge_index or csr")
+    _need_cuda("edge_attr", edge_attr, x.dtype, 2)
+    _need_cuda("theta_e", theta_e, x.dtype, 2)
+    D = edge_attr.shape[1]
+    if edge_attr.shape[0] != E or tuple(theta_e.shape) != (D, F):
+        raise ValueError("edge_attr must be [E, D] and theta_e [D, F]")
+    if msg not in ("edge_add", "edge_relu", "edge_mul") or aggr not in AGGR or kernel not in KERNEL:
+        raise ValueError("bad msg / aggr / kernel")
+    out = torch.empty_like(x) if out is None else out
+    argmax = torch.empty((N, F), dtype=torch.int64, device=dev) if aggr == "max" else None
+    use_csr = kernel == "csr" or (kernel == "auto" and csr is not None)
+    nbytes = _size(lib.pyg_propagate_edge_encoded_workspace, DTYPE[x.dtype], N, F, E, D, AGGR[aggr],
+                   KERNEL["csr" if use_csr else "coo"], csr.chunk if (csr is not None and use_csr) else 0)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, dev)
+    c = csr._c() if csr is not None else None
+    rc = lib.pyg_propagate_edge_encoded(_ptr(x), DTYPE[x.dtype], N, F, _ptr(edge_index), E, _ptr(edge_attr), D,
+                                        _ptr(theta_e), ORDER[attr_order], ctypes.byref(c) if c is not None else None,
+                                        MSG[msg], AGGR[aggr], KERNEL[kernel], _ptr(out), _ptr(argmax),
+                                        _ptr(workspace), workspace.numel(), _stream(dev))
+    _check(rc, "pyg_propagate_edge_encoded")
     return out, argmax
 
 

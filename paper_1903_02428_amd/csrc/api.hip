@@ -262,3 +262,68 @@ extern "C" int pyg_global_pool(const void *x, int dtype, int64_t N, int64_t F, c
     a.argmax = argmax;
     return segment_reduce(a, static_cast<char *>(ws) + ptr_bytes, ws_bytes - ptr_bytes, s);
 }
+
+// Edge features of another width D: e = edge_attr Theta_e ([E, D] x [D, F]
+// by the dense transform, stored in x's dtype in the workspace), then the
+// edge-feature propagate with e. Workspace: e, then the transform's, then the
+// propagate's, each 256-byte aligned.
+namespace {
+struct EncWs {
+    size_t e_off, d_off, p_off, bytes;
+};
+int enc_layout(int dtype, int64_t N, int64_t F, int64_t E, int64_t D, int aggr, int kernel, int64_t chunk, EncWs *w) {
+    size_t d = 0, p = 0;
+    PYG_TRY(pyg_dense_transform_workspace(D, F, &d));
+    PYG_TRY(pyg_propagate_workspace(dtype, N, F, E, aggr, kernel, chunk, &p));
+    w->e_off = 0;
+    w->d_off = align_up(static_cast<size_t>(E * F * dtype_size(dtype)), 256);
+    w->p_off = w->d_off + align_up(d, 256);
+    w->bytes = w->p_off + p + 256;
+    return PYG_OK;
+}
+}  // namespace
+
+extern "C" int pyg_propagate_edge_encoded_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t D, int aggr,
+                                                    int kernel, int64_t chunk, size_t *bytes) {
+    if (!bytes || !valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0 || D < 0 || chunk < 0)
+        return PYG_ERR_INVALID_ARG;
+    EncWs w;
+    PYG_TRY(enc_layout(dtype, N, F, E, D, aggr, kernel, chunk, &w));
+    *bytes = w.bytes;
+    return PYG_OK;
+}
+
+extern "C" int pyg_propagate_edge_encoded(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index,
+                                          int64_t E, const void *edge_attr, int64_t D, const void *theta_e,
+                                          int attr_order, const pyg_csr *csr, int msg, int aggr, int kernel, void *out,
+                                          int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
+    if (!valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0 || D < 0) return PYG_ERR_INVALID_ARG;
+    if (msg != PYG_MSG_EDGE_ADD && msg != PYG_MSG_EDGE_RELU && msg != PYG_MSG_EDGE_MUL) return PYG_ERR_INVALID_ARG;
+    if (kernel != PYG_KERNEL_AUTO && kernel != PYG_KERNEL_COO_ATOMIC && kernel != PYG_KERNEL_CSR_SEGMENT)
+        return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
+    if (E * D > 0 && !edge_attr) return PYG_ERR_INVALID_ARG;
+    if (D * F > 0 && !theta_e) return PYG_ERR_INVALID_ARG;
+    const bool use_csr = kernel == PYG_KERNEL_CSR_SEGMENT || (kernel == PYG_KERNEL_AUTO && csr);
+    if (use_csr && (!csr || csr->chunk < 0)) return PYG_ERR_INVALID_ARG;
+    const int kused = use_csr ? PYG_KERNEL_CSR_SEGMENT : PYG_KERNEL_COO_ATOMIC;
+    EncWs w;
+    PYG_TRY(enc_layout(dtype, N, F, E, D, aggr, kused, use_csr ? csr->chunk : 0, &w));
+    if (!ws || ws_bytes < w.bytes) return PYG_ERR_WORKSPACE;
+    char *base = static_cast<char *>(ws);
+    void *e = base + w.e_off;
+    const int64_t esz = dtype_size(dtype);
+    if (overlaps(out, N * F * esz, ws, static_cast<int64_t>(ws_bytes)) ||
+        overlaps(edge_attr, E * D * esz, ws, static_cast<int64_t>(ws_bytes)))
+        return PYG_ERR_INVALID_ARG;
+    if (E * F > 0) {
+        if (D == 0) {  // no edge features: e = 0
+            PYG_TRY(fill<uint8_t>(static_cast<uint8_t *>(e), E * F * esz, uint8_t(0), static_cast<hipStream_t>(stream)));
+        } else {
+            PYG_TRY(pyg_dense_transform(edge_attr, dtype, E, D, theta_e, F, e, dtype, base + w.d_off, w.p_off - w.d_off,
+                                        stream));
+        }
+    }
+    return pyg_propagate_edge(x, dtype, N, F, edge_index, E, E * F > 0 ? e : nullptr, attr_order, csr, msg, aggr,
+                              kernel, out, argmax, base + w.p_off, ws_bytes - w.p_off, stream);
+}

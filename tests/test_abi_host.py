@@ -332,3 +332,19 @@ def test_backward_rejects_bad_grad_w_order(lib):
     # max with grad_w in CSR order needs the forward CSR (its perm maps edge ids to slots)
     assert bw(G, X, 0, 10, 4, FAKE, 20, FAKE, None, None, 0, MAX, FAKE, GX, GW, CSR, FAKE, 1 << 30, None) == INVALID
     assert bw(G, X, 0, 10, 4, FAKE, 20, FAKE, None, None, 0, MAX, FAKE, GX, GW, COO, FAKE, 0, None) == WORKSPACE
+
+
+def test_edge_encoded_rejects_bad_arguments(lib):
+    from paper_1903_02428_amd.binding import _Csr
+    good = ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 10, 20, 0))
+    X, EA, TH, OUT = FAKE, ctypes.c_void_p(0x300000), ctypes.c_void_p(0x400000), ctypes.c_void_p(0x900000)
+    en = lib.pyg_propagate_edge_encoded
+    ADD, SUM, CSRK = 2, 0, 2
+    assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 0, good, 0, SUM, CSRK, OUT, None, FAKE, 1 << 30, None) == INVALID  # msg
+    assert en(X, 0, 10, 4, FAKE, 20, None, 3, TH, 0, good, ADD, SUM, CSRK, OUT, None, FAKE, 1 << 30, None) == INVALID
+    assert en(X, 0, 10, 4, FAKE, 20, EA, 3, None, 0, good, ADD, SUM, CSRK, OUT, None, FAKE, 1 << 30, None) == INVALID
+    assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 0, None, ADD, SUM, CSRK, OUT, None, FAKE, 1 << 30, None) == INVALID
+    assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 0, good, ADD, SUM, CSRK, OUT, None, FAKE, 0, None) == WORKSPACE
+    assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 0, good, ADD, SUM, CSRK, FAKE, None, FAKE, 1 << 30, None) == INVALID
+    rc, b = _ws(lib.pyg_propagate_edge_encoded_workspace, 0, 10, 4, 20, 3, SUM, CSRK, 0)
+    assert rc == PYG_OK and b >= 20 * 4 * 4
