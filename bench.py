@@ -135,8 +135,8 @@ def main():
         return
     if args.configs_only:
         print(json.dumps({"workload": "the four smaller synthetic graphs", "configs": small_configs(pyg, torch, dev,
-                                                                                                  args.seed)}),
-              flush=True)
+                                                                                                  args.seed),
+                          "step_graph_small": step_graph_small(pyg, torch, dev, args.seed)}), flush=True)
         return
 
     t0 = time.time()
@@ -286,6 +286,7 @@ def main():
         result["detail"]["gcn_layer"] = gcn_layer(pyg, torch, x, csr_w, N, E, F, dev)
         result["detail"]["edge_features"] = edge_features(pyg, torch, x, ei, csr, N, E, F, dev)
         result["detail"]["configs"] = small_configs(pyg, torch, dev, args.seed)
+        result["detail"]["step_graph_small"] = step_graph_small(pyg, torch, dev, args.seed)
     if not (args.no_detail and args.no_cpu_baseline):
         import oracle
         w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)  # the oracle's own weights
@@ -362,6 +363,63 @@ def timed(torch, fn, reps=10, warm=1):
         e.synchronize()
         ts.append(s.elapsed_time(e))
     return float(np.median(ts))
+
+
+def step_graph_small(pyg, torch, dev, seed):
+    """The whole step (coo_to_csr, degree, gcn_norm, propagate, mean pool) on
+    the Cora-shaped graph and the mini-batch, run eagerly (one Python call
+    per entry point) and as one captured HIP graph replayed: at these sizes
+    the step is launch-bound, and the graph removes the host side of every
+    call. Median of 20 after warm-up."""
+    import ctypes
+    import synth
+    res = {}
+    c1, c3 = synth.make_config(1, seed=seed), synth.make_config(3, seed=seed)
+    for name, ei_np, N, x_np, batch_np, B in (("C1", c1["edge_index_gcn"], c1["N"], c1["x"],
+                                               np.zeros(c1["N"], np.int64), 1),
+                                              ("C3", c3["edge_index"], c3["N"], c3["x"], c3["batch"], c3["B"])):
+        lib = pyg.library()
+        E = ei_np.shape[1]
+        ei, x, batch = (torch.from_numpy(np.ascontiguousarray(a)).to(dev) for a in (ei_np, x_np, batch_np))
+        F = x.shape[1]
+        csr = pyg.CSR(torch.empty(N + 1, dtype=torch.int64, device=dev), torch.empty(E, dtype=torch.int32, device=dev),
+                      torch.empty(E, dtype=torch.int64, device=dev), None, N, E, 0)
+        norm = torch.empty(E, dtype=torch.float32, device=dev)
+        csr_w = pyg.CSR(csr.rowptr, csr.col, csr.perm, norm, N, E, 0)
+        deg = torch.empty(N, dtype=torch.int64, device=dev)
+        out = torch.empty_like(x)
+        pooled = torch.empty(B, F, dtype=torch.float32, device=dev)
+        sz = ctypes.c_size_t()
+
+        def ws(fn, *a):
+            fn(*a, ctypes.byref(sz))
+            return torch.empty(max(sz.value, 1), dtype=torch.uint8, device=dev)
+        ws_csr, ws_norm = ws(lib.pyg_coo_to_csr_workspace, E, N), ws(lib.pyg_gcn_norm_csr_workspace, N)
+        ws_pool = ws(lib.pyg_global_pool_workspace, 0, N, F, B, 1)
+        ws_prop = torch.empty(pyg.propagate_workspace_bytes(x, E, "sum", "csr", 0), dtype=torch.uint8, device=dev)
+
+        def step():
+            pyg.coo_to_csr(ei, N, None, out=csr, workspace=ws_csr)
+            pyg.degree_csr(csr, out=deg)
+            pyg.gcn_norm_csr(csr, out=norm, workspace=ws_norm)
+            pyg.propagate(x, csr=csr_w, aggr="sum", out=out, workspace=ws_prop)
+            pyg.global_pool(out, batch, B, "mean", out=pooled, workspace=ws_pool)
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        torch.cuda.synchronize()
+        eager = timed(torch, step, reps=20, warm=50)
+        replay = timed(torch, graph.replay, reps=20, warm=50)
+        res[name] = {"N": N, "E": E, "F": F, "graphs": B, "eager_ms": eager, "graph_replay_ms": replay,
+                     "speedup": eager / replay}
+        del graph
+    return res
 
 
 def small_configs(pyg, torch, dev, seed):

@@ -122,6 +122,40 @@ __global__ __launch_bounds__(kBlock) void k_csr_edge_norm(const int64_t *__restr
     }
 }
 
+// Short rows (mean degree at most 16): the kernel above walks a chunk's rows
+// one after another, a chain of dependent loads per row, which left a
+// 13k-edge graph at 360 us. Here the chunks are kNormLightChunk slots and
+// lane k of the wavefront takes row r0 + k (the rows that meet the chunk, 64
+// at a time) with its slots inside the chunk, so a lane never handles more
+// than one chunk of slots, hub rows included. The same expression per slot.
+constexpr int64_t kNormLightChunk = 64;
+__global__ __launch_bounds__(kBlock) void k_csr_edge_norm_light(const int64_t *__restrict__ rowptr,
+                                                                const int32_t *__restrict__ col,
+                                                                const float *__restrict__ w, int64_t N, int64_t E,
+                                                                const double *__restrict__ dinv,
+                                                                float *__restrict__ norm) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave);
+    const int64_t e0 = c * kNormLightChunk;
+    if (e0 >= E) return;
+    const int64_t e1 = (e0 + kNormLightChunk) < E ? (e0 + kNormLightChunk) : E;
+    const int64_t r0 = uniform64(wave_lower_bound(rowptr, N + 1, e0 + 1, lane)) - 1;  // row holding slot e0
+    for (int64_t rb = r0;; rb += kWave) {
+        const int64_t r = rb + lane;
+        if (r < N) {
+            const int64_t s = rowptr[r], t = rowptr[r + 1];
+            const int64_t a = s > e0 ? s : e0, b = t < e1 ? t : e1;
+            if (a < b) {
+                const double di = dinv[r];
+                for (int64_t p = a; p < b; ++p)
+                    norm[p] = static_cast<float>(dinv[col[p]] * static_cast<double>(w ? w[p] : 1.f) * di);
+            }
+        }
+        const int64_t nxt = rb + kWave;  // the next batch of rows, if one still starts inside the chunk
+        if (nxt >= N || uniform64(rowptr[nxt]) >= e1) break;
+    }
+}
+
 }  // namespace
 }  // namespace pyg
 
@@ -151,6 +185,14 @@ extern "C" int pyg_gcn_norm_csr(const pyg_csr *csr, float *norm_csr, void *ws, s
         k_row_dinv_count<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(csr->rowptr, N, dinv);
     }
     PYG_LAUNCH_CHECK();
+    if (E <= 16 * N) {  // short rows: a lane per row
+        const int64_t nchunks = (E + kNormLightChunk - 1) / kNormLightChunk;
+        k_csr_edge_norm_light<<<static_cast<unsigned>((nchunks + 3) / 4), kBlock, 0, s>>>(csr->rowptr, csr->col,
+                                                                                        csr->weight, N, E, dinv,
+                                                                                        norm_csr);
+        PYG_LAUNCH_CHECK();
+        return PYG_OK;
+    }
     constexpr int64_t kChunk = PYG_NORM_CHUNK;
     const int64_t nchunks = (E + kChunk - 1) / kChunk;
     k_csr_edge_norm<<<static_cast<unsigned>((nchunks + 3) / 4), kBlock, 0, s>>>(csr->rowptr, csr->col, csr->weight, N, E,
