@@ -262,7 +262,7 @@ int pyg_propagate_edge_encoded_workspace(int dtype, int64_t N, int64_t F, int64_
  *   the workspace (E*F elements of dtype, then the two calls' workspaces).
  * Errors: as pyg_propagate_edge and pyg_dense_transform, plus
  * PYG_ERR_INVALID_ARG for NULL edge_attr or theta_e with E*D or D*F > 0 and
- * for out or edge_attr overlapping the workspace. */
+ * for x, edge_attr, theta_e or out overlapping the workspace. */
 int pyg_propagate_edge_encoded(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
                                const void *edge_attr, int64_t D, const void *theta_e, int attr_order,
                                const pyg_csr *csr, int msg, int aggr, int kernel, void *out, int64_t *argmax,

@@ -313,9 +313,10 @@ extern "C" int pyg_propagate_edge_encoded(const void *x, int dtype, int64_t N, i
     char *base = static_cast<char *>(ws);
     void *e = base + w.e_off;
     const int64_t esz = dtype_size(dtype);
-    if (overlaps(out, N * F * esz, ws, static_cast<int64_t>(ws_bytes)) ||
-        overlaps(edge_attr, E * D * esz, ws, static_cast<int64_t>(ws_bytes)))
-        return PYG_ERR_INVALID_ARG;
+    const int64_t wsb = static_cast<int64_t>(ws_bytes);
+    if (overlaps(out, N * F * esz, ws, wsb) || overlaps(edge_attr, E * D * esz, ws, wsb) ||
+        overlaps(x, N * F * esz, ws, wsb) || overlaps(theta_e, D * F * esz, ws, wsb))
+        return PYG_ERR_INVALID_ARG;  // the workspace is written before the inputs are read
     if (E * F > 0) {
         if (D == 0) {  // no edge features: e = 0
             PYG_TRY(fill<uint8_t>(static_cast<uint8_t *>(e), E * F * esz, uint8_t(0), static_cast<hipStream_t>(stream)));

@@ -346,5 +346,10 @@ def test_edge_encoded_rejects_bad_arguments(lib):
     assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 0, None, ADD, SUM, CSRK, OUT, None, FAKE, 1 << 30, None) == INVALID
     assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 0, good, ADD, SUM, CSRK, OUT, None, FAKE, 0, None) == WORKSPACE
     assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 0, good, ADD, SUM, CSRK, FAKE, None, FAKE, 1 << 30, None) == INVALID
+    WS = ctypes.c_void_p(0x1000000)
+    assert en(ctypes.c_void_p(0x1000040), 0, 10, 4, FAKE, 20, EA, 3, TH, 0, good, ADD, SUM, CSRK, OUT, None, WS,
+              1 << 20, None) == INVALID  # x inside the workspace
+    assert en(X, 0, 10, 4, FAKE, 20, EA, 3, ctypes.c_void_p(0x1000040), 0, good, ADD, SUM, CSRK, OUT, None, WS,
+              1 << 20, None) == INVALID  # theta_e inside the workspace
     rc, b = _ws(lib.pyg_propagate_edge_encoded_workspace, 0, 10, 4, 20, 3, SUM, CSRK, 0)
     assert rc == PYG_OK and b >= 20 * 4 * 4
