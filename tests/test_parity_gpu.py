@@ -104,6 +104,29 @@ def test_gcn_norm_csr(pyg, N, E, F, weighted):
         assert np.array_equal(got, ref.astype(np.float32))
 
 
+@pytest.mark.parametrize("weighted", [False, True])
+def test_gcn_norm_csr_light_rows_with_hubs(pyg, weighted):
+    """Short rows on average (the lane-per-row path) with two hub targets of
+    5,000 and 700 edges spanning many 64-slot chunks, and empty rows."""
+    rng = np.random.default_rng(31)
+    N, E = 4000, 20000
+    ei_np = synth.random_coo(rng, N, E)
+    ei_np[1, :5000] = 7
+    ei_np[1, 5000:5700] = N - 1
+    ei_np[1, ei_np[1] % 97 == 3] = 8  # some targets lose all their edges (no self-loops: empty rows, d = 0)
+    E2 = ei_np.shape[1]
+    assert E2 <= 16 * N
+    w = (rng.random(E2) + 0.5).astype(np.float32) if weighted else None
+    csr = pyg.coo_to_csr(to_dev(ei_np), N, to_dev(w) if weighted else None)
+    got = pyg.gcn_norm_csr(csr).cpu().numpy()
+    _, _, perm = oracle.coo_to_csr(ei_np, N)
+    ref = oracle.gcn_norm(ei_np, N, w)[perm]
+    if weighted:
+        assert (np.abs(got.astype(np.float64) - ref) <= np.spacing(np.abs(ref.astype(np.float32)))).all()
+    else:
+        assert np.array_equal(got, ref.astype(np.float32))
+
+
 COMBOS = [(aggr, msg, kernel, dt) for aggr in ("sum", "mean", "max") for msg in ("src", "weighted", "diff")
           for kernel in ("coo", "csr") for dt in (F32, BF16)]
 
