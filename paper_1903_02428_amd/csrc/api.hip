@@ -116,9 +116,13 @@ extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, con
     return segment_reduce(a, ws, ws_bytes, s);
 }
 
-extern "C" int pyg_propagate_edge(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
-                                  const void *edge_attr, int attr_order, const pyg_csr *csr, int msg, int aggr,
-                                  int kernel, void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
+namespace {
+// Argument checks of the edge-feature propagate, shared with the encoded
+// variant (which must reject its arguments before any device work):
+// edge_attr and attr_bytes are the features the caller passes.
+int check_edge_args(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                    const void *edge_attr, int64_t attr_bytes, int attr_order, const pyg_csr *csr, int msg, int aggr,
+                    int kernel, const void *out, const int64_t *argmax, bool *use_csr) {
     if (!valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0) return PYG_ERR_INVALID_ARG;
     if (msg != PYG_MSG_EDGE_ADD && msg != PYG_MSG_EDGE_RELU && msg != PYG_MSG_EDGE_MUL) return PYG_ERR_INVALID_ARG;
     if (attr_order != PYG_ORDER_COO && attr_order != PYG_ORDER_CSR) return PYG_ERR_INVALID_ARG;
@@ -128,16 +132,15 @@ extern "C" int pyg_propagate_edge(const void *x, int dtype, int64_t N, int64_t F
     if ((aggr == PYG_MAX) != (argmax != nullptr) && N * F > 0) return PYG_ERR_INVALID_ARG;
     if (aggr != PYG_MAX && argmax) return PYG_ERR_INVALID_ARG;
     if (N * F > 0 && (!x || !out)) return PYG_ERR_INVALID_ARG;
-    if (E * F > 0 && !edge_attr) return PYG_ERR_INVALID_ARG;
+    if (attr_bytes > 0 && !edge_attr) return PYG_ERR_INVALID_ARG;
     if (E > 0 && N == 0) return PYG_ERR_INVALID_ARG;
-    const int64_t esz = dtype_size(dtype);
-    const int64_t xbytes = N * F * esz;
-    if (overlaps(x, xbytes, out, xbytes) || overlaps(edge_attr, E * F * esz, out, xbytes)) return PYG_ERR_INVALID_ARG;
+    const int64_t xbytes = N * F * dtype_size(dtype);
+    if (overlaps(x, xbytes, out, xbytes) || overlaps(edge_attr, attr_bytes, out, xbytes)) return PYG_ERR_INVALID_ARG;
     if (argmax && (overlaps(argmax, N * F * 8, x, xbytes) || overlaps(argmax, N * F * 8, out, xbytes)))
         return PYG_ERR_INVALID_ARG;
     if (kernel == PYG_KERNEL_CSR_SEGMENT && !csr) return PYG_ERR_INVALID_ARG;
-    const bool use_csr = kernel == PYG_KERNEL_CSR_SEGMENT || (kernel == PYG_KERNEL_AUTO && csr);
-    if (use_csr) {
+    *use_csr = kernel == PYG_KERNEL_CSR_SEGMENT || (kernel == PYG_KERNEL_AUTO && csr);
+    if (*use_csr) {
         if (csr->N != N || csr->E != E || !csr->rowptr || csr->chunk < 0) return PYG_ERR_INVALID_ARG;
         if (E > 0 && (!csr->col || ((aggr == PYG_MAX || attr_order == PYG_ORDER_COO) && !csr->perm)))
             return PYG_ERR_INVALID_ARG;
@@ -145,6 +148,16 @@ extern "C" int pyg_propagate_edge(const void *x, int dtype, int64_t N, int64_t F
         if (E > 0 && !edge_index) return PYG_ERR_INVALID_ARG;
         if (attr_order != PYG_ORDER_COO) return PYG_ERR_INVALID_ARG;  // the COO kernel reads edges in COO order
     }
+    return PYG_OK;
+}
+}  // namespace
+
+extern "C" int pyg_propagate_edge(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                                  const void *edge_attr, int attr_order, const pyg_csr *csr, int msg, int aggr,
+                                  int kernel, void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
+    bool use_csr = false;
+    PYG_TRY(check_edge_args(x, dtype, N, F, edge_index, E, edge_attr, E * F * dtype_size(dtype), attr_order, csr,
+                            msg, aggr, kernel, out, argmax, &use_csr));
     size_t need;
     PYG_TRY(pyg_propagate_workspace(dtype, N, F, E, aggr, use_csr ? PYG_KERNEL_CSR_SEGMENT : PYG_KERNEL_COO_ATOMIC,
                                     use_csr ? csr->chunk : 0, &need));
@@ -297,15 +310,11 @@ extern "C" int pyg_propagate_edge_encoded(const void *x, int dtype, int64_t N, i
                                           int64_t E, const void *edge_attr, int64_t D, const void *theta_e,
                                           int attr_order, const pyg_csr *csr, int msg, int aggr, int kernel, void *out,
                                           int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
-    if (!valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0 || D < 0) return PYG_ERR_INVALID_ARG;
-    if (msg != PYG_MSG_EDGE_ADD && msg != PYG_MSG_EDGE_RELU && msg != PYG_MSG_EDGE_MUL) return PYG_ERR_INVALID_ARG;
-    if (kernel != PYG_KERNEL_AUTO && kernel != PYG_KERNEL_COO_ATOMIC && kernel != PYG_KERNEL_CSR_SEGMENT)
-        return PYG_ERR_INVALID_ARG;
-    if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
-    if (E * D > 0 && !edge_attr) return PYG_ERR_INVALID_ARG;
+    if (D < 0) return PYG_ERR_INVALID_ARG;
+    bool use_csr = false;  // every check of the edge propagate first: nothing runs before an argument error
+    PYG_TRY(check_edge_args(x, dtype, N, F, edge_index, E, edge_attr, E * D * dtype_size(dtype), attr_order, csr,
+                            msg, aggr, kernel, out, argmax, &use_csr));
     if (D * F > 0 && !theta_e) return PYG_ERR_INVALID_ARG;
-    const bool use_csr = kernel == PYG_KERNEL_CSR_SEGMENT || (kernel == PYG_KERNEL_AUTO && csr);
-    if (use_csr && (!csr || csr->chunk < 0)) return PYG_ERR_INVALID_ARG;
     const int kused = use_csr ? PYG_KERNEL_CSR_SEGMENT : PYG_KERNEL_COO_ATOMIC;
     EncWs w;
     PYG_TRY(enc_layout(dtype, N, F, E, D, aggr, kused, use_csr ? csr->chunk : 0, &w));

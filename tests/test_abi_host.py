@@ -351,5 +351,10 @@ def test_edge_encoded_rejects_bad_arguments(lib):
               1 << 20, None) == INVALID  # x inside the workspace
     assert en(X, 0, 10, 4, FAKE, 20, EA, 3, ctypes.c_void_p(0x1000040), 0, good, ADD, SUM, CSRK, OUT, None, WS,
               1 << 20, None) == INVALID  # theta_e inside the workspace
+    # every check of the edge propagate comes before the projection runs
+    other = ctypes.byref(_Csr(0x30000, 0x40000, 0x50000, None, 11, 20, 0))
+    assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 0, other, ADD, SUM, CSRK, OUT, None, FAKE, 1 << 30, None) == INVALID
+    assert en(X, 0, 0, 4, FAKE, 20, EA, 3, TH, 0, None, ADD, SUM, 1, OUT, None, FAKE, 1 << 30, None) == INVALID
+    assert en(X, 0, 10, 4, FAKE, 20, EA, 3, TH, 1, good, ADD, 2, CSRK, OUT, None, FAKE, 1 << 30, None) == INVALID
     rc, b = _ws(lib.pyg_propagate_edge_encoded_workspace, 0, 10, 4, 20, 3, SUM, CSRK, 0)
     assert rc == PYG_OK and b >= 20 * 4 * 4
