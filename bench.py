@@ -44,8 +44,8 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 # change to those sources the traffic field is reported as null.
 COUNTERS = {
     "source_hash": "14252b9a1e5c00ae",
-    "fetch_kib": 18501630.5, "write_kib": 133369.5,
-    "copy_mib": 1024, "copy_fetch_kib": 524307.9, "copy_write_kib": 1048576.0,
+    "fetch_kib": 18503227.6, "write_kib": 133373.8,
+    "copy_mib": 1024, "copy_fetch_kib": 524307.1, "copy_write_kib": 1048576.0,
 }
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp"]
 
