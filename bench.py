@@ -37,15 +37,14 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 
 # Byte counters of the CSR propagate kernel (k_segment, fp32 weighted sum on
 # the large power-law graph) from two rocprofv3 --pmc runs of this script
-# (FETCH_SIZE, then WRITE_SIZE, KiB per propagate call: the sum over its
-# feature-window dispatches), with the same counters on a
+# (FETCH_SIZE, then WRITE_SIZE, KiB per propagate call), with the same counters on a
 # plain 1024 MiB device copy for scale; see profiles/propagate_c5_counters.md.
 # They describe the kernel sources with the recorded hash only: after any
 # change to those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "14252b9a1e5c00ae",
-    "fetch_kib": 18503227.6, "write_kib": 133373.8,
-    "copy_mib": 1024, "copy_fetch_kib": 524307.1, "copy_write_kib": 1048576.0,
+    "source_hash": "aa0fb0cd3a1c63f2",
+    "fetch_kib": 18709799.8, "write_kib": 133726.8,
+    "copy_mib": 1024, "copy_fetch_kib": 524307.2, "copy_write_kib": 1048576.0,
 }
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp"]
 
@@ -269,10 +268,10 @@ def main():
                    "step": "coo_to_csr+degree(csr row bounds)+gcn_norm(csr order)+propagate(sum,csr)+global_pool(mean)"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
-                     "kernel": "pyg_propagate CSR segment, fp32 weighted sum: one k_segment launch per "
-                               "128-byte feature window (F*4/128 = %d) and one k_segment_fixup" % (F * 4 // 128),
-                     "unit_of_work": "one propagate call (all its window launches): every edge gathers its "
-                                     "source row once in total",
+                     "kernel": "pyg_propagate CSR segment, fp32 weighted sum: one k_segment launch over the "
+                               "%d 128-byte feature windows (window-major) and one k_segment_fixup" % (F * 4 // 128),
+                     "unit_of_work": "one propagate call: every edge gathers its source row once in total, a "
+                                     "128-byte window at a time",
                      "bytes_per_call": balg, "avg_call_ms": t_prop * 1e3},
         "detail": {"per_call_ms": {n: float(np.mean(times[n])) for n in names},
                    "propagate_edges_features_per_s": E * F / t_prop,

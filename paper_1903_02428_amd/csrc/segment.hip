@@ -30,9 +30,9 @@
 // the hint changes only the cache policy, never the result.
 //
 // Narrow windows: for large inputs with rows wider than a cache line, the
-// plain messages run one launch per 128-byte feature window (one line
-// gathered per slot, 8 lanes per sub-group), and long rows are folded once
-// after the last window; the hint is then off. Each window's reduction order
+// plain messages run over 128-byte feature windows (one line gathered per
+// slot, 8 lanes per sub-group), all windows in one launch, window-major, and
+// long rows are folded once after it; the hint is then off. Each window's reduction order
 // is fixed, so results stay bit-reproducible.
 #include "common.hpp"
 
@@ -48,6 +48,7 @@ struct SegParams {
     int64_t F;      // row stride of x, out and partials (elements)
     int64_t fbase;  // first feature of this launch's window
     int64_t fcnt;   // features in the window
+    int64_t nwin;   // > 1: this launch covers nwin windows of fcnt features, window-major
     const int64_t *rowptr;
     const int32_t *col;
     const float *w;
@@ -95,11 +96,13 @@ constexpr int64_t kHintMinRowBytes = 512;
 constexpr int64_t kHotBudgetBytes = 12ll << 20;  // hot rows kept cacheable
 // Narrow windows: when the source rows are large in total and wider than one
 // cache line, the row is reduced one 128-byte window (32 fp32 / 64 bf16
-// features) at a time, one launch per window. Each launch then gathers a
-// single line per slot, a sub-group needs only 8 lanes (8 slots in flight
-// per wavefront instead of 2 for 512-byte rows), and the lines that one
-// launch reuses are a quarter of the rows' bytes, so far more of them stay in
-// L2. The index stream is read once per window (8 B per slot). Measured on
+// features) at a time. Every wavefront then gathers a single line per slot,
+// a sub-group needs only 8 lanes (8 slots in flight per wavefront instead of
+// 2 for 512-byte rows), and the wavefronts in flight work on one window at a
+// time (the launch is window-major), so the lines they reuse are a quarter
+// of the rows' bytes and far more of them stay in L2. The index stream is
+// read once per window (8 B per slot). One launch for all windows instead of
+// one per window leaves a single drain tail: 5.44 -> 5.35 ms. Measured on
 // the large power-law graph (F = 128): fp32 6.52 -> 5.43 ms, bf16 3.12 ->
 // 2.69 ms; 256-byte windows 6.77 ms. Graphs whose rows total under 16 MB
 // lose (more launches for rows that fit in L2 anyway), so they keep whole
@@ -115,6 +118,9 @@ constexpr int64_t kHotBudgetBytes = 12ll << 20;  // hot rows kept cacheable
 #endif
 #ifndef PYG_NARROW_ALL
 #define PYG_NARROW_ALL 0  // 1: narrow windows for every message kind
+#endif
+#ifndef PYG_WINDOWS_ONE_LAUNCH
+#define PYG_WINDOWS_ONE_LAUNCH 1  // 0: one launch per narrow window
 #endif
 #ifndef PYG_HINT_NARROW
 #define PYG_HINT_NARROW 0  // 0: no hint with narrow windows; 1: hot budget counted in window bytes; 2: in row bytes
@@ -502,7 +508,13 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
 template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool LIGHT>
 __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
+    int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
+    if (p.nwin > 1) {  // all chunks of window 0, then of window 1, ...: one tail for all windows
+        const int64_t w = c / p.nchunks;
+        if (w >= p.nwin) return;
+        c -= w * p.nchunks;
+        p.fbase += w * p.fcnt;
+    }
     if (c >= p.nchunks) return;
     const int64_t e0 = c * p.chunk;
     const int64_t e1 = (e0 + p.chunk) < p.E ? (e0 + p.chunk) : p.E;
@@ -719,7 +731,8 @@ int launch_fixup(const SegParams &p, hipStream_t s) {
 template <typename T, bool VEC, int NS, int MSG, bool MAXA, bool IDENT>
 int launch_window(const SegParams &p, bool light, bool fixup, hipStream_t s) {
     constexpr int U = NS == 1 ? 8 : (NS == 2 ? 4 : 2);
-    const unsigned grid = static_cast<unsigned>((p.nchunks + (kBlock / kWave) - 1) / (kBlock / kWave));
+    const int64_t nc = p.nchunks * (p.nwin > 1 ? p.nwin : 1);
+    const unsigned grid = static_cast<unsigned>((nc + (kBlock / kWave) - 1) / (kBlock / kWave));
     if constexpr (NS == 1) {
         if (light) k_segment<T, VEC, NS, U, MSG, MAXA, IDENT, true><<<grid, kBlock, 0, s>>>(p);
         else k_segment<T, VEC, NS, U, MSG, MAXA, IDENT, false><<<grid, kBlock, 0, s>>>(p);
@@ -796,6 +809,25 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     }
     // lane vectors covered by one launch (NS = 4, or one narrow window)
     const int64_t per_window = narrow ? kWindowBytes / 16 : 4 * kWave;
+    if (narrow && PYG_WINDOWS_ONE_LAUNCH) {
+        // every window is the same width (rows are a multiple of a window): one
+        // launch, window-major, then the fold of the long rows over all features
+        int lg = 0;
+        while ((1 << lg) < per_window && lg < 6) ++lg;
+        p.lg_l = lg;
+        p.fbase = 0;
+        p.fcnt = per_window * ep;
+        p.nwin = nvec / per_window;
+        const bool light = lg < 6 && a.E <= kLightMaxDegree * a.n_rows;
+        int rc;
+        if (maxa) rc = launch_msg<T, true, true>(p, mk, ident, 1, light, false, s);
+        else rc = launch_msg<T, true, false>(p, mk, ident, 1, light, false, s);
+        if (rc != PYG_OK) return rc;
+        p.nwin = 1;
+        p.fbase = 0;
+        p.fcnt = a.F;
+        return maxa ? launch_fixup<T, true>(p, s) : launch_fixup<T, false>(p, s);
+    }
     for (int64_t v0 = 0; v0 < nvec; v0 += per_window) {
         const int64_t vn = (nvec - v0) < per_window ? (nvec - v0) : per_window;
         const int ns = vn <= kWave ? 1 : (vn <= 2 * kWave ? 2 : 4);
