@@ -42,9 +42,9 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 # They describe the kernel sources with the recorded hash only: after any
 # change to those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "aa0fb0cd3a1c63f2",
-    "fetch_kib": 18709799.8, "write_kib": 133726.8,
-    "copy_mib": 1024, "copy_fetch_kib": 524307.2, "copy_write_kib": 1048576.0,
+    "source_hash": "723d8cb8c5a866dd",
+    "fetch_kib": 18517199.5, "write_kib": 156942.8,
+    "copy_mib": 1024, "copy_fetch_kib": 524307.7, "copy_write_kib": 1048576.0,
 }
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp"]
 

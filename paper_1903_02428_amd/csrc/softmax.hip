@@ -642,6 +642,16 @@ struct SmWs {
     size_t bytes;
 };
 
+// Default chunk of the softmax: the segment kernel's, but long-row graphs
+// keep 2048 slots per wavefront (1024 or 512 measured slower here, e.g. the
+// scores-given softmax 1.95 -> 2.09 ms at 512 on the large power-law graph).
+int64_t softmax_chunk(int64_t E, int64_t n_rows, int64_t requested) {
+    if (requested > 0 || (n_rows > 0 && E <= 16 * n_rows)) return segment_chunk(E, n_rows, requested);
+    int64_t c = 64;
+    while (c < 2048 && c * 32768 < E) c <<= 1;
+    return c;
+}
+
 SmWs carve_softmax(void *base, int64_t E, int64_t H, int64_t chunk) {
     const int64_t nchunks = E > 0 ? (E + chunk - 1) / chunk : 0;
     Carver c(base);
@@ -663,7 +673,7 @@ int ceil_log2(int64_t v) {
 template <int SRC>
 int run_softmax(SmParams p, const pyg_csr *csr, void *ws, size_t ws_bytes, hipStream_t s) {
     if (p.E == 0 || p.H == 0) return PYG_OK;
-    p.chunk = segment_chunk(p.E, p.n_rows, csr->chunk);
+    p.chunk = softmax_chunk(p.E, p.n_rows, csr->chunk);
     p.nchunks = (p.E + p.chunk - 1) / p.chunk;
     const SmWs w = carve_softmax(ws, p.E, p.H, p.chunk);
     if (!ws || ws_bytes < w.bytes) return PYG_ERR_WORKSPACE;
@@ -736,7 +746,7 @@ using namespace pyg;
 
 extern "C" int pyg_segment_softmax_workspace(int64_t E, int64_t N, int64_t H, int64_t chunk, size_t *bytes) {
     if (!bytes || E < 0 || N < 0 || H < 0 || chunk < 0) return PYG_ERR_INVALID_ARG;
-    *bytes = E > 0 ? carve_softmax(nullptr, E, H, segment_chunk(E, N, chunk)).bytes : 0;
+    *bytes = E > 0 ? carve_softmax(nullptr, E, H, softmax_chunk(E, N, chunk)).bytes : 0;
     return PYG_OK;
 }
 
