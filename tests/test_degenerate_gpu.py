@@ -45,22 +45,46 @@ def test_attention_backward_degenerate(pyg, N, E):
         assert torch.count_nonzero(gx) == 0 and torch.count_nonzero(gs) == 0 and torch.count_nonzero(gd) == 0
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16], ids=["f32", "bf16"])
 @pytest.mark.parametrize("N,E,F", [(0, 0, 4), (7, 0, 4), (7, 30, 0), (7, 30, 4)])
 @pytest.mark.parametrize("aggr", ["sum", "mean", "max"])
-def test_edge_backward_degenerate(pyg, N, E, F, aggr):
+def test_edge_backward_degenerate(pyg, N, E, F, aggr, dtype):
     d, csr, csr_t = graphs(pyg, N, E)
-    g = torch.randn(N, F, device="cuda")
-    x = torch.randn(N, F, device="cuda")
-    ea = torch.randn(E, F, device="cuda")
+    g = torch.randn(N, F, device="cuda").to(dtype)
+    x = torch.randn(N, F, device="cuda").to(dtype)
+    ea = torch.randn(E, F, device="cuda").to(dtype)
     arg = None
     if aggr == "max":
         _, arg = pyg.propagate_edge(x, ea, d, csr, "edge_relu", "max", "csr", "coo")
     gx, ge = pyg.propagate_edge_backward(g, x, ea, csr, "edge_relu", aggr, "coo", csr_t=csr_t, edge_index=d,
                                          argmax=arg)
     torch.cuda.synchronize()
-    assert gx.shape == (N, F) and ge.shape == (E, F)
+    assert gx.shape == (N, F) and ge.shape == (E, F) and gx.dtype == dtype and ge.dtype == dtype
     if E == 0:
         assert torch.count_nonzero(gx) == 0
+
+
+@pytest.mark.parametrize("N,E,F,D", [(0, 0, 4, 3), (7, 0, 4, 3), (7, 30, 0, 3), (7, 30, 4, 0), (7, 30, 4, 3)])
+def test_edge_encoded_and_grad_w_order_degenerate(pyg, N, E, F, D):
+    """The encoded edge propagate and grad_w in CSR order at empty sizes."""
+    d, csr, csr_t = graphs(pyg, N, E)
+    x = torch.randn(N, F, device="cuda")
+    out, _ = pyg.propagate_edge_encoded(x, torch.randn(E, D, device="cuda"), torch.randn(D, F, device="cuda"), d, csr,
+                                        "edge_relu", "sum", "csr", "coo")
+    w = torch.rand(E, device="cuda")
+    cw = pyg.coo_to_csr(d, N, w)
+    cwt = pyg.coo_to_csr(pyg.reverse_edges(d), N, w)
+    gx, gw = pyg.propagate_backward(torch.randn(N, F, device="cuda"), x, d, w, csr=cw, csr_t=cwt, aggr="sum",
+                                    need_grad_w=True, w_order="csr")
+    torch.cuda.synchronize()
+    assert out.shape == (N, F) and gx.shape == (N, F) and gw.shape == (E,)
+    if E == 0:
+        assert torch.count_nonzero(out) == 0
+    elif D == 0:  # no edge features: the message sees e = 0
+        ref, _ = pyg.propagate_edge(x, torch.zeros(E, F, device="cuda"), d, csr, "edge_relu", "sum", "csr", "coo")
+        assert torch.equal(out, ref)
+    if F == 0:
+        assert torch.count_nonzero(gw) == 0
 
 
 def test_degree_csr_and_map_empty(pyg):
