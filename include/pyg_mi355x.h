@@ -226,6 +226,28 @@ int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F,
                   const pyg_csr *csr, int msg, int aggr, int kernel,
                   void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
 
+/* Size of the static scratch array of pyg_propagate_noalloc, per GPU. */
+#define PYG_NOALLOC_SCRATCH_MIB 128
+
+/* pyg_propagate without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc). Same arguments, kernels, results
+ * and errors as pyg_propagate, minus (ws, ws_bytes): the scratch comes from
+ * a static device array of PYG_NOALLOC_SCRATCH_MIB MiB that every GPU the
+ * library runs on holds until the process ends. The call allocates nothing.
+ *   stream  must belong to the current device (else PYG_ERR_INVALID_ARG);
+ *           the current device's array is used.
+ * A call that needs more scratch than the array holds (pyg_propagate_workspace
+ * above PYG_NOALLOC_SCRATCH_MIB MiB, e.g. max on graphs of ~10^8 edges)
+ * returns PYG_ERR_UNSUPPORTED before any device work. Every call on one GPU
+ * shares that GPU's array: calls that overlap in time on one GPU (two
+ * streams, two host threads) race and give wrong results; calls ordered on
+ * one stream are safe, whatever an earlier call left in the array.
+ * PYG_ERR_HIP if the device or the array's address cannot be queried. */
+int pyg_propagate_noalloc(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                          const float *edge_weight, const pyg_csr *csr, int msg, int aggr, int kernel, void *out,
+                          int64_t *argmax, void *stream);
+
 /* Propagate with F-dimensional edge features in the message (Eq. (1)'s
  * e_{j,i}; Section 2 and Appendix A name the integration of
  * multi-dimensional edge information as a property of the gather/scatter

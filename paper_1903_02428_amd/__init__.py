@@ -41,6 +41,7 @@ from .binding import (  # noqa: F401
     propagate_edge_encoded,
     propagate_heads,
     propagate_heads_backward,
+    propagate_noalloc,
     propagate_workspace_bytes,
     reverse_edges,
     segment_softmax,

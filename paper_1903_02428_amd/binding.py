@@ -31,6 +31,7 @@ EXPORTED = [
     "pyg_propagate_heads_backward_workspace", "pyg_propagate_heads_backward", "pyg_gat_scores_backward_workspace",
     "pyg_gat_scores_backward",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
+    "pyg_propagate_noalloc",
 ]
 
 
@@ -82,6 +83,7 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                               ctypes.c_size_t, p],
+            "pyg_propagate_noalloc": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p],
             "pyg_propagate_edge": [p, i32, i64, i64, p, i64, p, i32, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                                    ctypes.c_size_t, p],
             "pyg_propagate_edge_encoded_workspace": [i32, i64, i64, i64, i64, i32, i32, i64, sz],
@@ -338,6 +340,37 @@ def propagate(x: torch.Tensor, edge_index: torch.Tensor | None = None, edge_weig
                            ctypes.byref(c) if c is not None else None, MSG[msg], AGGR[aggr], KERNEL[kernel],
                            _ptr(out), _ptr(argmax), _ptr(workspace), workspace.numel(), _stream(dev))
     _check(rc, "pyg_propagate")
+    return out, argmax
+
+
+def propagate_noalloc(x: torch.Tensor, edge_index: torch.Tensor | None = None,
+                      edge_weight: torch.Tensor | None = None, csr: CSR | None = None, aggr: str = "sum",
+                      msg: str = "src", kernel: str = "auto", out: torch.Tensor | None = None,
+                      argmax: torch.Tensor | None = None):
+    """propagate() through pyg_propagate_noalloc: no workspace, the library's
+    static per-GPU scratch instead. Allocates nothing when out (and argmax for
+    max) are given. Returns (out, argmax or None)."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    if x.dtype not in DTYPE:
+        raise ValueError("x must be float32 or bfloat16")
+    N, F = x.shape
+    E = _edge_index(edge_index) if edge_index is not None else (csr.E if csr is not None else None)
+    if E is None:
+        raise ValueError("need edge_index or csr")
+    if aggr not in AGGR or msg not in MSG or kernel not in KERNEL:
+        raise ValueError("bad aggr / msg / kernel")
+    if out is None:
+        out = torch.empty_like(x)
+    if aggr == "max" and argmax is None:
+        argmax = torch.empty((N, F), dtype=torch.int64, device=x.device)
+    if aggr != "max":
+        argmax = None
+    c = csr._c() if csr is not None else None
+    rc = lib.pyg_propagate_noalloc(_ptr(x), DTYPE[x.dtype], N, F, _ptr(edge_index), E, _ptr(edge_weight),
+                                   ctypes.byref(c) if c is not None else None, MSG[msg], AGGR[aggr], KERNEL[kernel],
+                                   _ptr(out), _ptr(argmax), _stream(x.device))
+    _check(rc, "pyg_propagate_noalloc")
     return out, argmax
 
 

@@ -62,9 +62,10 @@ extern "C" int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t 
     return PYG_OK;
 }
 
-extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
-                             const float *edge_weight, const pyg_csr *csr, int msg, int aggr, int kernel, void *out,
-                             int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
+namespace pyg {
+int propagate_check(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                    const float *edge_weight, const pyg_csr *csr, int msg, int aggr, int kernel, const void *out,
+                    const int64_t *argmax, size_t *need) {
     if (!valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0) return PYG_ERR_INVALID_ARG;
     if (msg != PYG_MSG_SRC && msg != PYG_MSG_DIFF) return PYG_ERR_INVALID_ARG;
     if (kernel != PYG_KERNEL_AUTO && kernel != PYG_KERNEL_COO_ATOMIC && kernel != PYG_KERNEL_CSR_SEGMENT)
@@ -89,11 +90,19 @@ extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, con
     } else if (E > 0 && !edge_index) {
         return PYG_ERR_INVALID_ARG;
     }
-    size_t need;
-    PYG_TRY(pyg_propagate_workspace(dtype, N, F, E, aggr, use_csr ? PYG_KERNEL_CSR_SEGMENT : PYG_KERNEL_COO_ATOMIC,
-                                    use_csr ? csr->chunk : 0, &need));
+    return pyg_propagate_workspace(dtype, N, F, E, aggr, use_csr ? PYG_KERNEL_CSR_SEGMENT : PYG_KERNEL_COO_ATOMIC,
+                                   use_csr ? csr->chunk : 0, need);
+}
+}  // namespace pyg
+
+extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                             const float *edge_weight, const pyg_csr *csr, int msg, int aggr, int kernel, void *out,
+                             int64_t *argmax, void *ws, size_t ws_bytes, void *stream) {
+    size_t need = 0;
+    PYG_TRY(propagate_check(x, dtype, N, F, edge_index, E, edge_weight, csr, msg, aggr, kernel, out, argmax, &need));
     if (ws_bytes < need || (need > 256 && !ws)) return PYG_ERR_WORKSPACE;
     if (N * F == 0) return PYG_OK;
+    const bool use_csr = kernel == PYG_KERNEL_CSR_SEGMENT || (kernel == PYG_KERNEL_AUTO && csr);
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (!use_csr) return coo_propagate(x, dtype, N, F, edge_index, E, edge_weight, msg, aggr, out, argmax, ws, ws_bytes, s);
     SegmentArgs a{};

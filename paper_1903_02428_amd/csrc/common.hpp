@@ -181,6 +181,12 @@ int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t 
 int inverse_perm(const int64_t *perm, int64_t E, int32_t *inv, hipStream_t s);
 int transpose_map(const pyg_csr *csr, const pyg_csr *csr_t, int32_t *inv, int32_t *map_t, hipStream_t s);
 
+// Every argument check of pyg_propagate (nothing is launched); on success
+// *need is the workspace the call takes.
+int propagate_check(const void *x, int dtype, int64_t N, int64_t F, const int64_t *edge_index, int64_t E,
+                    const float *edge_weight, const pyg_csr *csr, int msg, int aggr, int kernel, const void *out,
+                    const int64_t *argmax, size_t *need);
+
 // Unsorted-COO gather/scatter with hardware atomics.
 size_t coo_workspace(int dtype, int64_t N, int64_t F, int aggr);
 // ea: [E, F] edge features in x's dtype for the edge messages, else NULL.

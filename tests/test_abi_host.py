@@ -111,6 +111,23 @@ def test_propagate_rejects_bad_arguments(lib):
     assert prop(lib, ws=None, aggr=1) == WORKSPACE
 
 
+def test_noalloc_rejects_on_the_host(lib):
+    # every argument check of pyg_propagate, then the static scratch limit,
+    # all before the device is touched (this runs without a GPU)
+    def na(x=FAKE, dtype=0, N=10, F=4, ei=FAKE, E=20, w=None, csr=None, msg=0, aggr=0, kernel=1,
+           out=ctypes.c_void_p(0x20000), argmax=None):
+        return lib.pyg_propagate_noalloc(x, dtype, N, F, ei, E, w, csr, msg, aggr, kernel, out, argmax, None)
+    assert na(dtype=3) == INVALID
+    assert na(aggr=2) == INVALID                          # max needs argmax
+    assert na(out=ctypes.c_void_p(0x10000 + 8)) == INVALID  # out overlaps x
+    assert na(kernel=2) == INVALID                        # CSR kernel needs a CSR
+    assert na(N=2**31) == UNSUPPORTED
+    # COO max keeps N*F 8-byte keys: 2^20 x 128 needs 1 GiB > the 128 MiB array
+    big = 1 << 20
+    assert na(N=big, F=128, aggr=2, argmax=ctypes.c_void_p(0x10000000000),
+              out=ctypes.c_void_p(0x20000000000), x=ctypes.c_void_p(0x30000000000)) == UNSUPPORTED
+
+
 def test_other_entry_points_reject_bad_arguments(lib):
     assert lib.pyg_degree(None, 5, 4, FAKE, FAKE, 1 << 30, None) == INVALID
     assert lib.pyg_degree(FAKE, 5, 4, None, FAKE, 1 << 30, None) == INVALID
