@@ -35,34 +35,148 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 
-# Byte counters of the CSR propagate kernel (k_segment, fp32 weighted sum on
-# the large power-law graph) from two rocprofv3 --pmc runs of this script
-# (FETCH_SIZE, then WRITE_SIZE, KiB per propagate call), with the same counters on a
+# Byte counters of the CSR propagate call (fp32 gcn-weighted sum on the large
+# power-law graph) from rocprofv3 --pmc runs of this script (FETCH_SIZE, then
+# WRITE_SIZE, then TCC_HIT_sum + TCC_MISS_sum; KiB / counts per propagate
+# call, summed over the call's launches), with FETCH_SIZE and WRITE_SIZE on a
 # plain 1024 MiB device copy for scale; see profiles/propagate_c5_counters.md.
-# They describe the kernel sources with the recorded hash only: after any
-# change to those sources the traffic field is reported as null.
+# They describe the sources with the recorded hash only: after any change to
+# those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "723d8cb8c5a866dd",
-    "fetch_kib": 18517199.5, "write_kib": 156942.8,
-    "copy_mib": 1024, "copy_fetch_kib": 524307.7, "copy_write_kib": 1048576.0,
+    "source_hash": None,
+    "fetch_kib": None, "write_kib": None, "tcc_hit": None, "tcc_miss": None,
+    "copy_mib": 1024, "copy_fetch_kib": None, "copy_write_kib": None,
 }
-KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp"]
+# everything that decides which kernels a propagate call launches and how
+KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp",
+                  "paper_1903_02428_amd/csrc/api.hip", "paper_1903_02428_amd/binding.py"]
 
 
-def measured_traffic():
-    """HBM-side bytes per propagate launch from the recorded counters, scaled
-    by the copy calibration; None if the kernel sources changed since."""
+def source_hash():
     import hashlib
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
-    if h.hexdigest()[:16] != COUNTERS["source_hash"]:
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """Bytes past L2 (fetched plus written) per propagate call from the
+    recorded counters, scaled by the copy calibration; None if the sources
+    changed since they were taken."""
+    if COUNTERS["source_hash"] is None or source_hash() != COUNTERS["source_hash"]:
         return None
     ref_kib = COUNTERS["copy_mib"] * 1024.0
     fetch = COUNTERS["fetch_kib"] * ref_kib / COUNTERS["copy_fetch_kib"]
     write = COUNTERS["write_kib"] * ref_kib / COUNTERS["copy_write_kib"]
     return (fetch + write) * 1024.0
+
+
+def measured_l2_hit():
+    if COUNTERS["source_hash"] is None or source_hash() != COUNTERS["source_hash"] or not COUNTERS["tcc_hit"]:
+        return None
+    return COUNTERS["tcc_hit"] / (COUNTERS["tcc_hit"] + COUNTERS["tcc_miss"])
+
+
+class Probe:
+    """The bandwidth probes (libpyg_probe.so): a >= 1 GiB flush that evicts
+    every L2 and the Infinity Cache, random 128-byte-line gathers with exactly
+    known byte counts, and a streaming read."""
+
+    def __init__(self, torch, dev, flush_bytes=1 << 30):
+        import ctypes
+        from paper_1903_02428_amd import build
+        if not os.path.exists(build.PROBE_PATH):
+            build.build_probe()
+        lib = ctypes.CDLL(build.PROBE_PATH)
+        u64, i32, u32, p = ctypes.c_uint64, ctypes.c_int, ctypes.c_uint32, ctypes.c_void_p
+        lib.pyg_probe_sink_elems.argtypes, lib.pyg_probe_sink_elems.restype = [], ctypes.c_int64
+        lib.pyg_probe_flush.argtypes, lib.pyg_probe_flush.restype = [p, u64, u32, p], i32
+        lib.pyg_probe_gather.argtypes, lib.pyg_probe_gather.restype = [p, u64, i32, i32, i32, u64, u32, i32, i32, p,
+                                                                        p], i32
+        lib.pyg_probe_stream_read.argtypes, lib.pyg_probe_stream_read.restype = [p, u64, p, p], i32
+        self.lib, self.torch, self.dev = lib, torch, dev
+        self.flush_buf = torch.empty(flush_bytes, dtype=torch.uint8, device=dev)
+        self.sink = torch.empty(int(lib.pyg_probe_sink_elems()), dtype=torch.int32, device=dev)
+        self.salt = 0
+
+    def _stream(self):
+        import ctypes
+        return ctypes.c_void_p(self.torch.cuda.current_stream(self.dev).cuda_stream)
+
+    def flush(self):
+        import ctypes
+        self.salt += 1
+        rc = self.lib.pyg_probe_flush(ctypes.c_void_p(self.flush_buf.data_ptr()), self.flush_buf.numel(),
+                                      self.salt, self._stream())
+        assert rc == 0, f"pyg_probe_flush: {rc}"
+
+    def gather(self, buf, nbytes, line, parts, n, seed=1, in_flight=8, groups=2048, stride=1):
+        import ctypes
+        rc = self.lib.pyg_probe_gather(ctypes.c_void_p(buf.data_ptr()), nbytes, line, parts, stride, n, seed,
+                                       in_flight, groups, ctypes.c_void_p(self.sink.data_ptr()), self._stream())
+        assert rc == 0, f"pyg_probe_gather: {rc}"
+
+    def stream_read(self, buf, nbytes):
+        import ctypes
+        rc = self.lib.pyg_probe_stream_read(ctypes.c_void_p(buf.data_ptr()), nbytes,
+                                            ctypes.c_void_p(self.sink.data_ptr()), self._stream())
+        assert rc == 0, f"pyg_probe_stream_read: {rc}"
+
+
+def probe_ladder(probe, torch, dev, x_bytes):
+    """Gather and stream rates of this GPU (GB/s of requested bytes, median
+    of 5 launches). Random 128-byte lines from buffers of growing size, warm
+    (each buffer touched once before timing): a buffer of x's size stays in
+    the 256 MB Infinity Cache, so nearly every gather misses L2 and is served
+    over the fabric from there; that rate is the ceiling of the propagate's
+    traffic past L2. With parts = 8 each XCD draws from its own eighth (a 32
+    MiB buffer then fits the eight 4 MB L2s). Streams: a cold 4 GiB read
+    (HBM)."""
+    res = {"unit": "GB/s", "line_bytes": 128, "gathers_per_launch": 1 << 26}
+    n = 1 << 26
+    sizes = [("16MiB", 16 << 20), ("32MiB", 32 << 20), ("64MiB", 64 << 20), ("x", x_bytes),
+             ("256MiB", 256 << 20), ("1GiB", 1 << 30), ("4GiB", 4 << 30)]
+    for name, nbytes in sizes:
+        nbytes = nbytes // 128 * 128
+        buf = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        buf.zero_()
+        if name == "64MiB":  # 4 MiB of distinct lines per XCD: every 2nd / 4th line of an 8 / 16 MiB part
+            for stride, big in ((2, 64 << 20), (4, 128 << 20)):
+                b2 = torch.zeros(big, dtype=torch.uint8, device=dev)
+                ms = timed(torch, lambda: probe.gather(b2, big, 128, 8, n, stride=stride), reps=5, warm=1)
+                res[f"gather_4MiB_per_xcd_stride{stride}"] = n * 128 / (ms * 1e-3) / 1e9
+                del b2
+        for parts in ((1, 8) if nbytes <= (64 << 20) else (1,)):
+            ms = timed(torch, lambda: probe.gather(buf, nbytes, 128, parts, n), reps=5, warm=1)
+            res[f"gather_{name}" + ("_xcd_local" if parts == 8 else "")] = n * 128 / (ms * 1e-3) / 1e9
+        if name == "x":
+            ms = timed(torch, lambda: probe.gather(buf, nbytes, 64, 1, n), reps=5, warm=1)
+            res["gather64_x"] = n * 64 / (ms * 1e-3) / 1e9
+            # launch shapes: gathers in flight per lane x workgroups; the
+            # best of them is the ceiling
+            best = res["gather_x"]
+            for u in (4, 8, 16):
+                for groups in (1024, 2048, 4096, 8192):
+                    ms = timed(torch, lambda: probe.gather(buf, nbytes, 128, 1, n, in_flight=u, groups=groups),
+                               reps=5, warm=1)
+                    r = n * 128 / (ms * 1e-3) / 1e9
+                    res[f"gather_x_u{u}_g{groups}"] = r
+                    best = max(best, r)
+            res["gather_x_best"] = best
+            # one 128-byte window of 512-byte rows: every 4th line; per XCD
+            # an eighth of the rows (the pattern of an XCD-affine propagate)
+            for parts in (1, 8):
+                ms = timed(torch, lambda: probe.gather(buf, nbytes, 128, parts, n, stride=4), reps=5, warm=1)
+                res["gather_x_stride4" + ("_xcd_local" if parts == 8 else "")] = n * 128 / (ms * 1e-3) / 1e9
+        if name == "4GiB":
+            ms = timed(torch, lambda: probe.stream_read(buf, nbytes), reps=5, warm=1, flush=probe.flush)
+            res["stream_read_4GiB_cold"] = nbytes / (ms * 1e-3) / 1e9
+        del buf
+        torch.cuda.empty_cache()
+    res["x_bytes"] = x_bytes
+    return res
 
 
 def parse():
@@ -90,6 +204,10 @@ def parse():
                     help="time only the edge-feature propagate (max(x_j + e, 0), F-dimensional e) on the large graph")
     ap.add_argument("--fig2-features", type=int, default=64)
     ap.add_argument("--fig2-runs", type=int, default=1000)
+    ap.add_argument("--probe-only", action="store_true",
+                    help="only the bandwidth probes (gather ladder, stream read; one JSON object)")
+    ap.add_argument("--warm-detail", action="store_true",
+                    help="time the large-graph detail calls back to back instead of after a 1 GiB flush each")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for scaling rocprofv3 byte counters)")
     return ap.parse_args()
@@ -104,6 +222,13 @@ def b_alg_csr(N, E, F, s_x, weighted=True, s_out=None):
     weights, one source-row gather per edge, one output write."""
     s_out = s_x if s_out is None else s_out
     return 8 * (N + 1) + 4 * E + (4 * E if weighted else 0) + E * F * s_x + N * F * s_out
+
+
+def b_uniq_csr(N, E, F, s_x, weighted=True, s_out=None):
+    """Compulsory bytes of one CSR propagate: every distinct byte once (x read
+    once however often its rows are gathered)."""
+    s_out = s_x if s_out is None else s_out
+    return 8 * (N + 1) + 4 * E + (4 * E if weighted else 0) + N * F * s_x + N * F * s_out
 
 
 def b_alg_coo(N, E, F, s_x, weighted=True):
@@ -129,6 +254,11 @@ def main():
         build.build()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.probe_only:
+        probe = Probe(torch, dev)
+        print(json.dumps({"workload": "bandwidth probes", "probe": probe_ladder(probe, torch, dev, 232965 * 128 * 4)}),
+              flush=True)
+        return
     if args.fig2:
         fig2_sweep(pyg, torch, synth, dev, args)
         return
@@ -145,6 +275,10 @@ def main():
     E = ei_np.shape[1]
     log(f"generated {c['name']}: N={N} E={E} F={F} in {time.time() - t0:.1f}s")
 
+    global FLUSH
+    probe = Probe(torch, dev)  # allocated first: the 1 GiB flush buffer
+    if not args.warm_detail:
+        FLUSH = probe.flush
     ei = torch.from_numpy(ei_np).to(dev)
     x = torch.from_numpy(x_np).to(dev)
     batch = torch.zeros(N, dtype=torch.int64, device=dev)  # one graph: whole-graph readout
@@ -247,8 +381,13 @@ def main():
 
     t_prop = float(np.mean(times["propagate"])) * 1e-3
     balg = b_alg_csr(N, E, F, 4)
-    achieved = balg / t_prop / 1e9
+    buniq = b_uniq_csr(N, E, F, 4)
     value = E * F / (ms_per_step * 1e-3)
+    ladder = probe_ladder(probe, torch, dev, N * F * 4)
+    log("probe ladder done")
+    traffic = measured_traffic()
+    peak = ladder["gather_x_best"]
+    achieved = traffic / t_prop / 1e9 if traffic is not None else None
 
     result = {
         "metric": "propagate throughput: edges·features/s and achieved HBM GB/s (% of peak)",
@@ -266,16 +405,31 @@ def main():
         "config": {"workload": "large power-law graph (Chung-Lu gamma=2.1), gcn_norm-weighted sum, CSR segment kernel",
                    "N": N, "E": E, "F": F, "seed": args.seed, "chunk": args.chunk or "default",
                    "step": "coo_to_csr+degree(csr row bounds)+gcn_norm(csr order)+propagate(sum,csr)+global_pool(mean)"},
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
-                     "kernel": "pyg_propagate CSR segment, fp32 weighted sum: one k_segment launch over the "
-                               "%d 128-byte feature windows (window-major) and one k_segment_fixup" % (F * 4 // 128),
-                     "unit_of_work": "one propagate call: every edge gathers its source row once in total, a "
-                                     "128-byte window at a time",
-                     "bytes_per_call": balg, "avg_call_ms": t_prop * 1e3},
+        "roofline": {"bound": "fabric", "achieved": achieved, "peak": peak, "unit": "GB/s",
+                     "frac": achieved / peak if achieved is not None else None, "traffic": traffic,
+                     "peak_source": "measured in this run: random 128-byte lines gathered from a buffer the size "
+                                    "of x (%.1f MB), resident in the Infinity Cache (pyg_probe_gather)" %
+                                    (N * F * 4 / 1e6),
+                     "achieved_source": "bytes past L2 per call (FETCH_SIZE + WRITE_SIZE counters, copy-calibrated) "
+                                        "/ the call's event time in the timed steps",
+                     "l2_hit": measured_l2_hit(),
+                     "kernel": "pyg_propagate CSR segment, fp32 weighted sum (k_segment + k_segment_fixup)",
+                     "unit_of_work": "one propagate call over the whole graph",
+                     "avg_call_ms": t_prop * 1e3,
+                     "algorithmic": {"bytes_per_call": balg, "GBps": balg / t_prop / 1e9, "hbm_peak": HBM_PEAK_GBS,
+                                     "frac_of_hbm": balg / t_prop / 1e9 / HBM_PEAK_GBS,
+                                     "convention": "every edge gathers its source row once (cache reuse counted as "
+                                                   "traffic), plus rowptr, columns, weights and one output write"},
+                     "compulsory": {"bytes_per_call": buniq, "GBps": buniq / t_prop / 1e9,
+                                    "frac_of_hbm": buniq / t_prop / 1e9 / HBM_PEAK_GBS,
+                                    "convention": "every distinct byte once: rowptr, columns, weights, x, output"}},
+        "probe": ladder,
         "detail": {"per_call_ms": {n: float(np.mean(times[n])) for n in names},
+                   "per_call_cache": "in-step: each call follows the previous call of the same step",
+                   "detail_cache": "warm (back to back)" if args.warm_detail else
+                                   "cold: a 1 GiB write before every timed call evicts L2 and the Infinity Cache",
                    "propagate_edges_features_per_s": E * F / t_prop,
-                   "degree_from_coo_ms": timed(torch, lambda: pyg.degree(ei, N, out=deg, workspace=ws_deg))},
+                   "degree_from_coo_ms": cold(torch, lambda: pyg.degree(ei, N, out=deg, workspace=ws_deg))},
     }
 
     if not args.no_detail:
@@ -350,18 +504,31 @@ def fig2_sweep(pyg, torch, synth, dev, args):
             print(json.dumps(rec), flush=True)
 
 
-def timed(torch, fn, reps=10, warm=1):
+FLUSH = None  # set to a Probe's flush: the large-graph detail calls are then timed cold
+
+
+def timed(torch, fn, reps=10, warm=1, flush=None):
+    """Median of `reps` calls, each bracketed by HIP events on the current
+    stream. With `flush`, every timed call starts cold: the flush runs before
+    it, outside the events."""
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     for _ in range(warm):
         fn()
     ts = []
     for _ in range(reps):
+        if flush is not None:
+            flush()
         s.record()
         fn()
         e.record()
         e.synchronize()
         ts.append(s.elapsed_time(e))
     return float(np.median(ts))
+
+
+def cold(torch, fn, reps=10, warm=1):
+    """timed() with the 1 GiB flush before every call when a probe is loaded."""
+    return timed(torch, fn, reps=reps, warm=warm, flush=FLUSH)
 
 
 def step_graph_small(pyg, torch, dev, seed):
@@ -507,19 +674,19 @@ def backward_calls(pyg, torch, x, ei, csr_w, N, E, F, dev):
         return {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9, "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                 "bytes": b, "edges_features_per_s": E * F / (ms * 1e-3)}
 
-    ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, w_coo, csr=csr_w, csr_t=csr_t, aggr="sum",
+    ms = cold(torch, lambda: pyg.propagate_backward(g, x, ei, w_coo, csr=csr_w, csr_t=csr_t, aggr="sum",
                                                      need_grad_w=True), reps=5)
     res["sum-weighted-grad_x+grad_w"] = rec(ms, b_alg_csr(N, E, F, 4) + rp + 4 * E + 8 * E + N * F * 4 + E * F * 4
                                            + 4 * E)
     # grad_w in CSR slot order (the order of the CSR's weights): no scatter through perm
-    ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, w_coo, csr=csr_w, csr_t=csr_t, aggr="sum",
+    ms = cold(torch, lambda: pyg.propagate_backward(g, x, ei, w_coo, csr=csr_w, csr_t=csr_t, aggr="sum",
                                                      need_grad_w=True, w_order="csr"), reps=5)
     res["sum-weighted-grad_x+grad_w-csr-order"] = rec(ms, b_alg_csr(N, E, F, 4) + rp + 4 * E + N * F * 4
                                                      + E * F * 4 + 4 * E)
-    ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, None, csr=plain, csr_t=plain_t, aggr="mean"), reps=5)
+    ms = cold(torch, lambda: pyg.propagate_backward(g, x, ei, None, csr=plain, csr_t=plain_t, aggr="mean"), reps=5)
     res["mean-grad_x"] = rec(ms, b_alg_csr(N, E, F, 4, weighted=False) + rp + 2 * N * F * 4)
     _, am = pyg.propagate(x, csr=plain, aggr="max")
-    ms = timed(torch, lambda: pyg.propagate_backward(g, x, ei, None, csr=plain, csr_t=plain_t, aggr="max",
+    ms = cold(torch, lambda: pyg.propagate_backward(g, x, ei, None, csr=plain, csr_t=plain_t, aggr="max",
                                                      argmax=am), reps=5)
     res["max-grad_x"] = rec(ms, N * F * (8 + 4 + 8 + 4) + N * F * 4)
     del csr_t, plain_t, g, am, w_coo
@@ -538,7 +705,7 @@ def variants(pyg, torch, x, ei, csr, N, E, F, dev):
             for kernel in ("csr", "coo"):
                 ws = torch.empty(pyg.propagate_workspace_bytes(xx, E, aggr, kernel, csr.chunk), dtype=torch.uint8,
                                  device=dev)
-                ms = timed(torch, lambda: pyg.propagate(xx, ei, norm, csr=csr if kernel == "csr" else None, aggr=aggr,
+                ms = cold(torch, lambda: pyg.propagate(xx, ei, norm, csr=csr if kernel == "csr" else None, aggr=aggr,
                                                         kernel=kernel, out=o, workspace=ws))
                 b = b_alg_csr(N, E, F, s) if kernel == "csr" else b_alg_coo(N, E, F, s)
                 res[f"{kernel}-{aggr}-{dtname}"] = {"ms": ms, "edges_features_per_s": E * F / (ms * 1e-3),
@@ -570,17 +737,17 @@ def attention(pyg, torch, x, ei, csr, N, E, F, dev, H=8):
                 "bytes": b}
 
     res = {"heads": H, "channels_per_head": F // H}
-    ms = timed(torch, lambda: pyg.gat_softmax(a_src, a_dst, csr, 0.2, "csr", out=alpha, workspace=ws_sm))
+    ms = cold(torch, lambda: pyg.gat_softmax(a_src, a_dst, csr, 0.2, "csr", out=alpha, workspace=ws_sm))
     res["gat_softmax"] = rec(ms, rp + 4 * E + 4 * E * H + 8 * N * H)
-    ms = timed(torch, lambda: pyg.segment_softmax(scores, csr, "csr", out=gs, workspace=ws_sm))
+    ms = cold(torch, lambda: pyg.segment_softmax(scores, csr, "csr", out=gs, workspace=ws_sm))
     res["segment_softmax"] = rec(ms, rp + 8 * E * H)
-    ms = timed(torch, lambda: pyg.segment_softmax_backward(alpha, grad, csr, "csr", out=gs, workspace=ws_sm))
+    ms = cold(torch, lambda: pyg.segment_softmax_backward(alpha, grad, csr, "csr", out=gs, workspace=ws_sm))
     res["segment_softmax_backward"] = rec(ms, rp + 12 * E * H)
     for dtname, xx, sz in (("f32", x, 4), ("bf16", x.to(torch.bfloat16), 2)):
         o = torch.empty_like(xx)
         ws = torch.empty(pyg.binding._size(pyg.library().pyg_propagate_heads_workspace, pyg.binding.DTYPE[xx.dtype],
                                            N, H, F // H, E, csr.chunk), dtype=torch.uint8, device=dev)
-        ms = timed(torch, lambda: pyg.propagate_heads(xx, csr, alpha, H, out=o, workspace=ws))
+        ms = cold(torch, lambda: pyg.propagate_heads(xx, csr, alpha, H, out=o, workspace=ws))
         r = rec(ms, rp + 4 * E + 4 * E * H + E * F * sz + N * F * sz)
         r["edges_features_per_s"] = E * F / (ms * 1e-3)
         res[f"propagate_heads_{dtname}"] = r
@@ -593,7 +760,7 @@ def attention(pyg, torch, x, ei, csr, N, E, F, dev, H=8):
     map_t = pyg.csr_transpose_map(csr, csr_t)
     ws_map = torch.empty(pyg.binding._size(pyg.library().pyg_csr_transpose_map_workspace, E), dtype=torch.uint8,
                          device=dev)
-    ms = timed(torch, lambda: pyg.csr_transpose_map(csr, csr_t, out=map_t, workspace=ws_map))
+    ms = cold(torch, lambda: pyg.csr_transpose_map(csr, csr_t, out=map_t, workspace=ws_map))
     res["csr_transpose_map"] = rec(ms, 16 * E + 4 * E)  # both permutations in, the map out
     tmap = 4 * E  # the transpose map (slot of csr for each slot of csr_t)
     g_alpha = torch.empty(E, H, device=dev)
@@ -603,7 +770,7 @@ def attention(pyg, torch, x, ei, csr, N, E, F, dev, H=8):
         wsb = torch.empty(pyg.binding._size(pyg.library().pyg_propagate_heads_backward_workspace,
                                             pyg.binding.DTYPE[xx.dtype], N, H, F // H, E, csr_t.chunk),
                           dtype=torch.uint8, device=dev)
-        ms = timed(torch, lambda: pyg.propagate_heads_backward(g, xx, csr, csr_t, alpha, H, workspace=wsb,
+        ms = cold(torch, lambda: pyg.propagate_heads_backward(g, xx, csr, csr_t, alpha, H, workspace=wsb,
                                                                out=(gx, g_alpha), map_t=map_t))
         # grad_x: the attention sum over the reversed graph; grad_alpha: per
         # edge and head a dot product of a gathered x row block with g's row.
@@ -615,7 +782,7 @@ def attention(pyg, torch, x, ei, csr, N, E, F, dev, H=8):
     outs = (torch.empty(N, H, device=dev), torch.empty(N, H, device=dev))
     wsg = torch.empty(pyg.binding._size(pyg.library().pyg_gat_scores_backward_workspace, N, H, E, csr_t.chunk),
                       dtype=torch.uint8, device=dev)
-    ms = timed(torch, lambda: pyg.gat_scores_backward(a_src, a_dst, csr, csr_t, grad, 0.2, workspace=wsg, out=outs,
+    ms = cold(torch, lambda: pyg.gat_scores_backward(a_src, a_dst, csr, csr_t, grad, 0.2, workspace=wsg, out=outs,
                                                       map_t=map_t))
     res["gat_scores_backward"] = rec(ms, 2 * rp + 4 * E + tmap + 4 * E * H + 4 * E * H + 8 * N * H + 8 * N * H)
     back = res["segment_softmax_backward"]["ms"] + res["propagate_heads_backward_f32"]["ms"] \
@@ -638,13 +805,13 @@ def gcn_layer(pyg, torch, x, csr_w, N, E, F, dev, Fo=128):
     ws_d = torch.empty(pyg.binding._size(pyg.library().pyg_dense_transform_workspace, F, Fo), dtype=torch.uint8,
                        device=dev)
     ws_p = torch.empty(pyg.propagate_workspace_bytes(h, E, "sum", "csr", csr_w.chunk), dtype=torch.uint8, device=dev)
-    t_d = timed(torch, lambda: pyg.dense_transform(xb, theta, torch.bfloat16, out=h, workspace=ws_d))
-    t_p = timed(torch, lambda: pyg.propagate(h, csr=csr_w, aggr="sum", out=o, workspace=ws_p))
+    t_d = cold(torch, lambda: pyg.dense_transform(xb, theta, torch.bfloat16, out=h, workspace=ws_d))
+    t_p = cold(torch, lambda: pyg.propagate(h, csr=csr_w, aggr="sum", out=o, workspace=ws_p))
 
     def layer():
         pyg.dense_transform(xb, theta, torch.bfloat16, out=h, workspace=ws_d)
         pyg.propagate(h, csr=csr_w, aggr="sum", out=o, workspace=ws_p)
-    t_l = timed(torch, layer)
+    t_l = cold(torch, layer)
     bytes_d = N * F * 2 + F * Fo * 2 + N * Fo * 2
     flops = 2.0 * N * F * Fo
     # the same layer in fp32 (fp32 operands on the fp32 matrix-core path, the same Theta values)
@@ -653,12 +820,12 @@ def gcn_layer(pyg, torch, x, csr_w, N, E, F, dev, Fo=128):
     o32 = torch.empty_like(h32)
     ws_p32 = torch.empty(pyg.propagate_workspace_bytes(h32, E, "sum", "csr", csr_w.chunk), dtype=torch.uint8,
                          device=dev)
-    t_d32 = timed(torch, lambda: pyg.dense_transform(x, theta32, torch.float32, out=h32, workspace=ws_d))
+    t_d32 = cold(torch, lambda: pyg.dense_transform(x, theta32, torch.float32, out=h32, workspace=ws_d))
 
     def layer32():
         pyg.dense_transform(x, theta32, torch.float32, out=h32, workspace=ws_d)
         pyg.propagate(h32, csr=csr_w, aggr="sum", out=o32, workspace=ws_p32)
-    t_l32 = timed(torch, layer32)
+    t_l32 = cold(torch, layer32)
     bytes_d32 = N * F * 4 + F * Fo * 4 + N * Fo * 4
     return {"F_in": F, "F_out": Fo, "dtype": "bf16 storage, fp32 accumulation",
             "dense_transform": {"ms": t_d, "alg_GBps": bytes_d / (t_d * 1e-3) / 1e9,
@@ -693,7 +860,7 @@ def edge_features(pyg, torch, x, ei, csr, N, E, F, dev):
         for kernel, order in kernels:
             ws = torch.empty(pyg.propagate_workspace_bytes(xx, E, "sum", kernel, csr.chunk), dtype=torch.uint8,
                              device=dev)
-            ms = timed(torch, lambda: pyg.propagate_edge(xx, ea, ei, csr if kernel == "csr" else None, "edge_relu",
+            ms = cold(torch, lambda: pyg.propagate_edge(xx, ea, ei, csr if kernel == "csr" else None, "edge_relu",
                                                          "sum", kernel, order, out=o, workspace=ws), reps=5)
             b = (b_alg_csr(N, E, F, sz, weighted=False) if kernel == "csr" else b_alg_coo(N, E, F, sz, weighted=False))
             b += E * F * sz
@@ -706,7 +873,7 @@ def edge_features(pyg, torch, x, ei, csr, N, E, F, dev):
         ws = torch.empty(pyg.binding._size(pyg.library().pyg_propagate_edge_backward_workspace,
                                            pyg.binding.DTYPE[dt], N, F, E, pyg.binding.MSG["edge_relu"],
                                            pyg.binding.AGGR["sum"], csr_t.chunk), dtype=torch.uint8, device=dev)
-        ms = timed(torch, lambda: pyg.propagate_edge_backward(g, xx, ea, csr, "edge_relu", "sum", "csr",
+        ms = cold(torch, lambda: pyg.propagate_edge_backward(g, xx, ea, csr, "edge_relu", "sum", "csr",
                                                               csr_t=csr_t, map_t=map_t, workspace=ws), reps=5)
         rp = 8 * (N + 1)
         # grad_x: columns and map, one gathered g row, one edge row per

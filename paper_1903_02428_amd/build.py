@@ -18,6 +18,9 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_NAME = "libpyg_mi355x.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
+# bandwidth probes of the benchmark's roofline (not part of the library's ABI)
+PROBE_SRC = os.path.join(HERE, "probe", "probe.hip")
+PROBE_PATH = os.path.join(HERE, "libpyg_probe.so")
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -49,13 +52,27 @@ def _filter_warnings(text: str) -> str:
     return "".join(keep)
 
 
+def build_probe() -> str:
+    """Compile the bandwidth-probe library (one source) next to this file."""
+    tmp = PROBE_PATH + ".tmp"
+    cmd = [HIPCC, *CFLAGS, "-shared", PROBE_SRC, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {PROBE_SRC}:\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, PROBE_PATH)
+    return PROBE_PATH
+
+
 def build(jobs: int | None = None) -> str:
-    """Compile all HIP sources and link the shared library; returns its path."""
+    """Compile all HIP sources and link the shared library (and the probe
+    library); returns the library's path."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     srcs = sources()
     jobs = jobs or min(len(srcs), os.cpu_count() or 4, 8)
-    with cf.ThreadPoolExecutor(jobs) as ex:
+    with cf.ThreadPoolExecutor(jobs + 1) as ex:
+        probe = ex.submit(build_probe)
         objs = list(ex.map(_compile, srcs))
+        probe.result()
     tmp = LIB_PATH + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
