@@ -711,6 +711,22 @@ def variants(pyg, torch, x, ei, csr, N, E, F, dev):
                 res[f"{kernel}-{aggr}-{dtname}"] = {"ms": ms, "edges_features_per_s": E * F / (ms * 1e-3),
                                                    "alg_GBps": b / (ms * 1e-3) / 1e9,
                                                    "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+    # the source-blocked form (XCD-affine, partial rows folded): the blocking
+    # pass (preprocessing, per graph) and the gcn-weighted sum
+    for B in (2, 8):
+        bc = pyg.csr_blocks(csr, B)
+        res[f"csr_blocks_build-B{B}"] = {"ms": cold(torch, lambda: pyg.csr_blocks(csr, B, out=bc))}
+        for dtname, xx, s in (("f32", x, 4), ("bf16", xb, 2)):
+            o = torch.empty_like(xx)
+            ws = torch.empty(pyg.propagate_blocked_workspace_bytes(xx, bc, "sum"), dtype=torch.uint8, device=dev)
+            ms = cold(torch, lambda: pyg.propagate_blocked(xx, bc, "sum", out=o, workspace=ws))
+            b = b_alg_csr(N, E, F, s) + 8 * B * N
+            res[f"blocked-B{B}-sum-{dtname}"] = {"ms": ms, "edges_features_per_s": E * F / (ms * 1e-3),
+                                                 "alg_GBps": b / (ms * 1e-3) / 1e9,
+                                                 "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+            del ws
+        del bc
+        torch.cuda.empty_cache()
     return res
 
 

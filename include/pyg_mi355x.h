@@ -101,6 +101,28 @@ typedef struct {
     int64_t chunk;
 } pyg_csr;
 
+/* A CSR whose slots are regrouped by source block (built by
+ * pyg_csr_blocks_build from a pyg_csr): the source ids are cut into B blocks
+ * of ceil(N / B) consecutive ids, and virtual row b * N + i holds the slots
+ * of target i whose source lies in block b, in ascending edge id. It is a
+ * CSR over B * N rows:
+ *   rowptr [B*N + 1]  rowptr[b*N + i] .. rowptr[b*N + i + 1];
+ *   col    [E]        source node of each slot;
+ *   perm   [E]        COO edge id of each slot, or NULL (needed for max);
+ *   weight [E]        edge weight in this slot order, or NULL;
+ *   B                 2 or 4 (blocks shared by 4 or 2 XCDs), or 8, 16, 24 or 32 (one to four blocks per XCD);
+ *   chunk             slots per work unit of the propagate, 0 = default. */
+typedef struct {
+    const int64_t *rowptr;
+    const int32_t *col;
+    const int64_t *perm;
+    const float *weight;
+    int64_t N;
+    int64_t E;
+    int64_t B;
+    int64_t chunk;
+} pyg_csr_blocks;
+
 /* Human-readable text for a status code (static storage, never NULL). */
 const char *pyg_strerror(int status);
 
@@ -225,6 +247,50 @@ int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F,
                   const int64_t *edge_index, int64_t E, const float *edge_weight,
                   const pyg_csr *csr, int msg, int aggr, int kernel,
                   void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_csr_blocks_build. */
+int pyg_csr_blocks_workspace(int64_t N, int64_t E, int64_t B, size_t *bytes);
+
+/* Regroups the slots of a CSR (pyg_coo_to_csr) by source block, for
+ * pyg_propagate_blocked: the preprocessing of the same row-ordered layout
+ * Appendix A builds once per graph, cut by source as well so that a
+ * propagate reads an eighth of x per XCD. Stable: inside a virtual row the
+ * slots keep the CSR's order (ascending edge id), so the result is unique.
+ *   csr     input CSR (rowptr, col; perm when perm is wanted, weight when
+ *           weight is wanted);
+ *   B       source blocks: 2, 4, 8, 16, 24 or 32;
+ *   rowptr  int64 [B*N + 1] output;  col  int32 [E] output;
+ *   perm    int64 [E] output or NULL (COO edge id of every slot);
+ *   weight  fp32 [E] output or NULL (csr->weight in the new slot order).
+ * Errors: PYG_ERR_INVALID_ARG (NULL csr/rowptr/col, a bad B, perm or weight
+ * wanted but absent from csr), PYG_ERR_UNSUPPORTED (N or E >= 2^31),
+ * PYG_ERR_WORKSPACE. */
+int pyg_csr_blocks_build(const pyg_csr *csr, int64_t B, int64_t *rowptr, int32_t *col, int64_t *perm,
+                         float *weight, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_propagate_blocked (chunk as in the blocked
+ * CSR). Holds B fp32 partial rows per target (B*N*F*4 bytes, plus B*N*F*8
+ * for max). */
+int pyg_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t B, int aggr, int64_t chunk,
+                                    size_t *bytes);
+
+/* Propagate (Eq. (1) of Section 2, the same results as pyg_propagate with
+ * the CSR kernel) over a source-blocked CSR: every XCD reduces the virtual
+ * rows of its own source blocks (its L2 holds the rows of x it gathers, one
+ * 128-byte feature window at a time) into fp32 partial rows, which are then
+ * folded in block order. Sum and mean differ from pyg_propagate only in the
+ * order of the additions (deterministic, the same tolerance); max and argmax
+ * are the same bits (ties to the lowest edge id across blocks too).
+ *   x    [N,F] fp32 or bf16 with 16-byte rows (F * sizeof(dtype) % 16 == 0)
+ *        and 16-byte aligned x and out;
+ *   bcsr from pyg_csr_blocks_build (weighted when bcsr->weight is set; perm
+ *        required for max);
+ *   msg  PYG_MSG_SRC or PYG_MSG_DIFF (no weight with DIFF); aggr, out,
+ *        argmax as pyg_propagate.
+ * Errors: as pyg_propagate, plus PYG_ERR_UNSUPPORTED for rows that are not
+ * 16-byte vectors or a bad B. */
+int pyg_propagate_blocked(const void *x, int dtype, int64_t N, int64_t F, const pyg_csr_blocks *bcsr, int msg,
+                          int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
 
 /* Size of the static scratch array of pyg_propagate_noalloc, per GPU. */
 #define PYG_NOALLOC_SCRATCH_MIB 128

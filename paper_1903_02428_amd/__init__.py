@@ -14,6 +14,7 @@ from __future__ import annotations
 
 from .binding import (  # noqa: F401
     CSR,
+    CSRBlocks,
     GATAttention,
     Graph,
     Propagate,
@@ -22,6 +23,7 @@ from .binding import (  # noqa: F401
     PygError,
     abi_version,
     coo_to_csr,
+    csr_blocks,
     csr_transpose_map,
     degree,
     degree_csr,
@@ -36,6 +38,8 @@ from .binding import (  # noqa: F401
     library_path,
     propagate,
     propagate_backward,
+    propagate_blocked,
+    propagate_blocked_workspace_bytes,
     propagate_edge,
     propagate_edge_backward,
     propagate_edge_encoded,

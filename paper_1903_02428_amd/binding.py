@@ -31,7 +31,8 @@ EXPORTED = [
     "pyg_propagate_heads_backward_workspace", "pyg_propagate_heads_backward", "pyg_gat_scores_backward_workspace",
     "pyg_gat_scores_backward",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
-    "pyg_propagate_noalloc",
+    "pyg_propagate_noalloc", "pyg_csr_blocks_workspace", "pyg_csr_blocks_build", "pyg_propagate_blocked_workspace",
+    "pyg_propagate_blocked",
 ]
 
 
@@ -48,6 +49,12 @@ class PygError(RuntimeError):
 class _Csr(ctypes.Structure):
     _fields_ = [("rowptr", ctypes.c_void_p), ("col", ctypes.c_void_p), ("perm", ctypes.c_void_p),
                 ("weight", ctypes.c_void_p), ("N", ctypes.c_int64), ("E", ctypes.c_int64),
+                ("chunk", ctypes.c_int64)]
+
+
+class _CsrBlocks(ctypes.Structure):
+    _fields_ = [("rowptr", ctypes.c_void_p), ("col", ctypes.c_void_p), ("perm", ctypes.c_void_p),
+                ("weight", ctypes.c_void_p), ("N", ctypes.c_int64), ("E", ctypes.c_int64), ("B", ctypes.c_int64),
                 ("chunk", ctypes.c_int64)]
 
 
@@ -83,6 +90,11 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                               ctypes.c_size_t, p],
+            "pyg_csr_blocks_workspace": [i64, i64, i64, sz],
+            "pyg_csr_blocks_build": [ctypes.POINTER(_Csr), i64, p, p, p, p, p, ctypes.c_size_t, p],
+            "pyg_propagate_blocked_workspace": [i32, i64, i64, i64, i64, i32, i64, sz],
+            "pyg_propagate_blocked": [p, i32, i64, i64, ctypes.POINTER(_CsrBlocks), i32, i32, p, p, p, ctypes.c_size_t,
+                                      p],
             "pyg_propagate_noalloc": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p],
             "pyg_propagate_edge": [p, i32, i64, i64, p, i64, p, i32, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                                    ctypes.c_size_t, p],
@@ -189,6 +201,92 @@ class CSR:
         return _Csr(self.rowptr.data_ptr(), self.col.data_ptr() if self.E else None,
                     self.perm.data_ptr() if self.E else None,
                     None if self.weight is None else self.weight.data_ptr(), self.N, self.E, self.chunk)
+
+
+@dataclass
+class CSRBlocks:
+    """A CSR regrouped by source block (pyg_csr_blocks_build): virtual row
+    b * N + i holds the slots of target i whose source lies in block b."""
+    rowptr: torch.Tensor         # int64 [B*N+1]
+    col: torch.Tensor            # int32 [E]
+    perm: torch.Tensor | None    # int64 [E] COO edge ids, or None
+    weight: torch.Tensor | None  # fp32 [E] in this slot order, or None
+    N: int
+    E: int
+    B: int
+    chunk: int = 0
+
+    def _c(self) -> _CsrBlocks:
+        return _CsrBlocks(self.rowptr.data_ptr(), self.col.data_ptr() if self.E else None,
+                          None if self.perm is None or not self.E else self.perm.data_ptr(),
+                          None if self.weight is None or not self.E else self.weight.data_ptr(),
+                          self.N, self.E, self.B, self.chunk)
+
+
+def csr_blocks(csr: CSR, B: int = 8, with_perm: bool = False, with_weight: bool | None = None,
+               out: CSRBlocks | None = None, workspace: torch.Tensor | None = None) -> CSRBlocks:
+    """Regroup a CSR's slots by source block (B = 2, 4, 8, 16, 24 or 32). The
+    weights come along when the CSR has them (unless with_weight is False);
+    the edge ids (needed for max) when with_perm."""
+    lib = library()
+    dev = csr.rowptr.device
+    with_weight = csr.weight is not None if with_weight is None else with_weight
+    if with_weight and csr.weight is None:
+        raise ValueError("the CSR has no weights")
+    if out is not None:
+        if out.N != csr.N or out.E != csr.E or out.B != B or (out.perm is None) == with_perm or \
+                (out.weight is None) == with_weight:
+            raise ValueError("out CSRBlocks has another shape")
+        rowptr, col, perm, w = out.rowptr, out.col, out.perm, out.weight
+    else:
+        rowptr = torch.empty(B * csr.N + 1, dtype=torch.int64, device=dev)
+        col = torch.empty(csr.E, dtype=torch.int32, device=dev)
+        perm = torch.empty(csr.E, dtype=torch.int64, device=dev) if with_perm else None
+        w = torch.empty(csr.E, dtype=torch.float32, device=dev) if with_weight else None
+    nbytes = _size(lib.pyg_csr_blocks_workspace, csr.N, csr.E, B)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
+    c = csr._c()
+    _check(lib.pyg_csr_blocks_build(ctypes.byref(c), B, _ptr(rowptr), _ptr(col), _ptr(perm), _ptr(w), _ptr(ws), nbytes,
+                                    _stream(dev)), "pyg_csr_blocks_build")
+    if out is not None:
+        out.chunk = csr.chunk
+        return out
+    return CSRBlocks(rowptr, col, perm, w, csr.N, csr.E, B, csr.chunk)
+
+
+def propagate_blocked_workspace_bytes(x: torch.Tensor, bcsr: CSRBlocks, aggr: str) -> int:
+    return _size(library().pyg_propagate_blocked_workspace, DTYPE[x.dtype], x.shape[0], x.shape[1], bcsr.E, bcsr.B,
+                 AGGR[aggr], bcsr.chunk)
+
+
+def propagate_blocked(x: torch.Tensor, bcsr: CSRBlocks, aggr: str = "sum", msg: str = "src",
+                      out: torch.Tensor | None = None, argmax: torch.Tensor | None = None,
+                      workspace: torch.Tensor | None = None):
+    """Eq. (1) over a source-blocked CSR (pyg_propagate_blocked): the same
+    results as propagate() with the CSR kernel. Returns (out, argmax or None)."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    if x.dtype not in DTYPE:
+        raise ValueError("x must be float32 or bfloat16")
+    N, F = x.shape
+    if bcsr.N != N:
+        raise ValueError("bcsr does not match x")
+    if aggr not in AGGR or msg not in ("src", "diff"):
+        raise ValueError("bad aggr / msg")
+    if out is None:
+        out = torch.empty_like(x)
+    if aggr == "max" and argmax is None:
+        argmax = torch.empty((N, F), dtype=torch.int64, device=x.device)
+    if aggr != "max":
+        argmax = None
+    nbytes = propagate_blocked_workspace_bytes(x, bcsr, aggr)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, x.device)
+    c = bcsr._c()
+    rc = lib.pyg_propagate_blocked(_ptr(x), DTYPE[x.dtype], N, F, ctypes.byref(c), MSG[msg], AGGR[aggr], _ptr(out),
+                                   _ptr(argmax), _ptr(workspace), workspace.numel(), _stream(x.device))
+    _check(rc, "pyg_propagate_blocked")
+    return out, argmax
 
 
 def degree(edge_index: torch.Tensor, num_nodes: int, out: torch.Tensor | None = None,

@@ -125,6 +125,60 @@ extern "C" int pyg_propagate(const void *x, int dtype, int64_t N, int64_t F, con
     return segment_reduce(a, ws, ws_bytes, s);
 }
 
+extern "C" int pyg_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t B, int aggr,
+                                               int64_t chunk, size_t *bytes) {
+    if (!bytes || !valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0 || chunk < 0)
+        return PYG_ERR_INVALID_ARG;
+    if (!(B == 2 || B == 4 || (B >= 8 && B % 8 == 0 && B <= 32))) return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
+    *bytes = segment_blocked_workspace(E, N, F, B, aggr, chunk);
+    return PYG_OK;
+}
+
+extern "C" int pyg_propagate_blocked(const void *x, int dtype, int64_t N, int64_t F, const pyg_csr_blocks *bcsr,
+                                     int msg, int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes,
+                                     void *stream) {
+    if (!valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || !bcsr) return PYG_ERR_INVALID_ARG;
+    if (msg != PYG_MSG_SRC && msg != PYG_MSG_DIFF) return PYG_ERR_INVALID_ARG;
+    const int64_t E = bcsr->E, B = bcsr->B;
+    if (bcsr->N != N || E < 0 || !bcsr->rowptr || bcsr->chunk < 0) return PYG_ERR_INVALID_ARG;
+    if (!(B == 2 || B == 4 || (B >= 8 && B % 8 == 0 && B <= 32))) return PYG_ERR_INVALID_ARG;
+    if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
+    if ((aggr == PYG_MAX) != (argmax != nullptr) && N * F > 0) return PYG_ERR_INVALID_ARG;
+    if (aggr != PYG_MAX && argmax) return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && (!x || !out)) return PYG_ERR_INVALID_ARG;
+    if (E > 0 && (N == 0 || !bcsr->col || (aggr == PYG_MAX && !bcsr->perm))) return PYG_ERR_INVALID_ARG;
+    if (msg == PYG_MSG_DIFF && bcsr->weight) return PYG_ERR_INVALID_ARG;
+    const int64_t xbytes = N * F * dtype_size(dtype);
+    if (overlaps(x, xbytes, out, xbytes)) return PYG_ERR_INVALID_ARG;
+    if (argmax && (overlaps(argmax, N * F * 8, x, xbytes) || overlaps(argmax, N * F * 8, out, xbytes)))
+        return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && ((F * dtype_size(dtype)) % 16 != 0 || reinterpret_cast<uintptr_t>(x) % 16 != 0 ||
+                      reinterpret_cast<uintptr_t>(out) % 16 != 0))
+        return PYG_ERR_UNSUPPORTED;
+    size_t need = 0;
+    PYG_TRY(pyg_propagate_blocked_workspace(dtype, N, F, E, B, aggr, bcsr->chunk, &need));
+    if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
+    if (N * F == 0) return PYG_OK;
+    SegmentArgs a{};
+    a.x = x;
+    a.dtype = dtype;
+    a.F = F;
+    a.rowptr = bcsr->rowptr;
+    a.col = bcsr->col;
+    a.weight = bcsr->weight;
+    a.perm = bcsr->perm;
+    a.n_rows = N;
+    a.E = E;
+    a.msg = msg;
+    a.aggr = aggr;
+    a.chunk = bcsr->chunk;
+    a.sentinel = E;
+    a.out = out;
+    a.argmax = argmax;
+    return segment_reduce_blocked(a, B, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
 namespace {
 // Argument checks of the edge-feature propagate, shared with the encoded
 // variant (which must reject its arguments before any device work):

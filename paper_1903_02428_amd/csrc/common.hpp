@@ -172,6 +172,12 @@ struct SegmentArgs {
 // gate x_self[row] + e > 0.
 constexpr int kSegMsgEdgeReluGrad = 100;
 int64_t segment_chunk(int64_t E, int64_t n_rows, int64_t requested);
+// Source-blocked form: a.rowptr has B * n_rows + 1 entries (virtual row
+// b * n_rows + i = the slots of target i whose source lies in block b), a.col,
+// a.weight and a.perm are in that slot order; B a multiple of 8 (at most 32),
+// 16-byte rows. Plain, weighted and difference messages, any aggregation.
+size_t segment_blocked_workspace(int64_t E, int64_t n_rows, int64_t F, int64_t B, int aggr, int64_t chunk);
+int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_bytes, hipStream_t s);
 size_t segment_workspace(int64_t E, int64_t F, int aggr, int64_t chunk, int64_t n_rows);
 int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t s);
 

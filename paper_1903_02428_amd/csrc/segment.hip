@@ -80,6 +80,10 @@ struct SegParams {
     int32_t *class_hist;       // workspace for the hint pre-pass
     int32_t *hot_slot;
     uint8_t *node_class;       // degree class of every row [n_rows]
+    // source-blocked rows (XCD-affine launch): the rows are `blocks` runs of
+    // `rpb` virtual rows, virtual row r = (source block r / rpb, target r % rpb)
+    int64_t blocks;
+    int64_t rpb;
 };
 
 // Measured on the large power-law graph (F = 128): fp32 rows (512 B) gain
@@ -187,6 +191,25 @@ template <> struct Lane<uint16_t, false> {
     __device__ static void store(uint16_t *p, const float (&v)[N]) { *p = f32_to_bf16_rne(v[0]); }
 };
 
+// Stores one lane's EP results of a row: in the row dtype T, or as fp32
+// (OF32: partial rows of source blocks, folded later).
+template <typename T, bool VEC, bool OF32>
+__device__ __forceinline__ void store_out(void *out, int64_t idx, const float (&v)[Lane<T, VEC>::N]) {
+    constexpr int EP = Lane<T, VEC>::N;
+    if constexpr (OF32) {
+        float *o = static_cast<float *>(out) + idx;
+        if constexpr (VEC) {
+#pragma unroll
+            for (int k = 0; k < EP / 4; ++k)
+                reinterpret_cast<float4 *>(o)[k] = make_float4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
+        } else {
+            o[0] = v[0];
+        }
+    } else {
+        Lane<T, VEC>::store(static_cast<T *>(out) + idx, v);
+    }
+}
+
 // Degree class: 8 classes per octave, monotone in d, 0 for d <= 0.
 __device__ __forceinline__ int deg_class(int64_t d) {
     if (d <= 0) return 0;
@@ -213,7 +236,7 @@ __device__ __forceinline__ float edge_msg(float xv, float ev) {
 }
 
 // Reduce slots [s, t) of row r; write the row (kFull) or a partial (kPartial).
-template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT>
+template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool OF32 = false>
 __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int64_t s, int64_t t, int kind,
                                              int64_t slot, int lane, int hot) {
     using LN = Lane<T, VEC>;
@@ -230,7 +253,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
 #pragma unroll
     for (int sl = 0; sl < NS; ++sl) {
         const int64_t fo = ((int64_t)sl * L + q) * EP;
-        act[sl] = fo < p.fcnt;
+        act[sl] = fo < p.fcnt && p.fbase + fo < p.F;  // the last window of a row may be narrower
         f0[sl] = p.fbase + fo;
     }
     float acc[NS][EP];
@@ -245,8 +268,9 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
     R xi[NS];
     if constexpr (MSG == kMsgDiff || MSG == kMsgEdgeReluGrad) {
         const T *xr = MSG == kMsgDiff ? x : static_cast<const T *>(p.x_self);
+        const int64_t rr = p.blocks > 1 ? r % p.rpb : r;  // the target of a source-blocked virtual row
 #pragma unroll
-        for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(xr + r * p.F + f0[sl]) : LN::zero();
+        for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(xr + rr * p.F + f0[sl]) : LN::zero();
     }
     // per-head weights: a lane vector never straddles two heads (C is a multiple of its width)
     int64_t hd[NS];
@@ -397,7 +421,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
             if constexpr (MAXA) v[e] = pos[sl][e] >= 0 ? acc[sl][e] : 0.f;
             else v[e] = (p.mean && deg > 0) ? acc[sl][e] / static_cast<float>(deg) : acc[sl][e];
         }
-        LN::store(static_cast<T *>(p.out) + r * p.F + f0[sl], v);
+        store_out<T, VEC, OF32>(p.out, r * p.F + f0[sl], v);
         if constexpr (MAXA) {
             int64_t *ap = p.argmax + r * p.F + f0[sl];
 #pragma unroll
@@ -412,7 +436,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
 // Light rows: one sub-group of L lanes reduces a whole short row alone, so a
 // wavefront works on S rows at once. `mine` is false for sub-groups without
 // a row; nothing below crosses sub-groups, so the branch may diverge.
-template <typename T, bool VEC, int U, int MSG, bool MAXA, bool IDENT>
+template <typename T, bool VEC, int U, int MSG, bool MAXA, bool IDENT, bool OF32>
 __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t s, int64_t t, bool mine, int lane) {
     using LN = Lane<T, VEC>;
     using R = typename LN::R;
@@ -500,7 +524,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
         if constexpr (MAXA) v[e] = pos[e] >= 0 ? acc[e] : 0.f;
         else v[e] = (p.mean && deg > 0) ? acc[e] / static_cast<float>(deg) : acc[e];
     }
-    LN::store(static_cast<T *>(p.out) + r * p.F + f0, v);
+    store_out<T, VEC, OF32>(p.out, r * p.F + f0, v);
     if constexpr (MAXA) {
         int64_t *ap = p.argmax + r * p.F + f0;
 #pragma unroll
@@ -508,17 +532,9 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
     }
 }
 
-template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool LIGHT>
-__global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
-    const int lane = threadIdx.x & (kWave - 1);
-    int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
-    if (p.nwin > 1) {  // all chunks of window 0, then of window 1, ...: one tail for all windows
-        const int64_t w = c / p.nchunks;
-        if (w >= p.nwin) return;
-        c -= w * p.nchunks;
-        p.fbase += w * p.fcnt;
-    }
-    if (c >= p.nchunks) return;
+// One wavefront's work on chunk c (features p.fbase .. p.fbase + p.fcnt).
+template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool LIGHT, bool OF32>
+__device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c, int lane) {
     const int64_t e0 = c * p.chunk;
     const int64_t e1 = (e0 + p.chunk) < p.E ? (e0 + p.chunk) : p.E;
     const bool last = c == p.nchunks - 1;
@@ -531,7 +547,7 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
     if (rA > 0 && rpA > e0) {
         const int64_t s0 = uniform64(p.rowptr[rA - 1]);
         if (rpA - s0 > p.chunk)
-            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT>(p, rA - 1, e0, rpA < e1 ? rpA : e1, kPartial, 2 * c, lane, hot);
+            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT, OF32>(p, rA - 1, e0, rpA < e1 ? rpA : e1, kPartial, 2 * c, lane, hot);
     }
     // rows whose first slot lies in [e0, e1) (the last chunk also takes the
     // empty rows that start at E)
@@ -551,16 +567,16 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
                 const bool is_long = i < cnt && t - s > p.chunk;  // only the chunk's last row can be long
                 const uint64_t lm = __ballot(is_long);
                 if (lm) head = static_cast<int32_t>(rb + i0 + ((__ffsll(static_cast<unsigned long long>(lm)) - 1) >> p.lg_l));
-                light_row<T, VEC, U, MSG, MAXA, IDENT>(p, rb + i, s, t, i < cnt && !is_long, lane);
+                light_row<T, VEC, U, MSG, MAXA, IDENT, OF32>(p, rb + i, s, t, i < cnt && !is_long, lane);
             }
             if (cnt < kWave - 1) break;  // the chunk's rows end in this batch
             rb += cnt;
         }
         head = __builtin_amdgcn_readfirstlane(head);
         if (head >= 0)
-            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT>(p, head, uniform64(p.rowptr[head]), e1, kPartial, 2 * c + 1,
+            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT, OF32>(p, head, uniform64(p.rowptr[head]), e1, kPartial, 2 * c + 1,
                                                           lane, 0);
-        if (lane == 0) p.head_row[c] = head;
+        p.head_row[c] = head;  // uniform: every lane stores the same value (no lane-0 branch)
         return;
     }
     int64_t rb = rA;
@@ -574,13 +590,76 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
         const int64_t t = uniform64(__shfl(rp, (int)(r + 1 - rb), kWave));
         if (!last && s >= e1) break;
         if (t - s > p.chunk) {
-            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT>(p, r, s, e1, kPartial, 2 * c + 1, lane, hot);
+            reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT, OF32>(p, r, s, e1, kPartial, 2 * c + 1, lane, hot);
             head = static_cast<int32_t>(r);
             break;
         }
-        reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT>(p, r, s, t, kFull, 0, lane, hot);
+        reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT, OF32>(p, r, s, t, kFull, 0, lane, hot);
     }
-    if (lane == 0) p.head_row[c] = head;
+    p.head_row[c] = head;  // uniform: every lane stores the same value (no lane-0 branch)
+}
+
+template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool LIGHT>
+__global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
+    const int lane = threadIdx.x & (kWave - 1);
+    int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
+    if (p.nwin > 1) {  // all chunks of window 0, then of window 1, ...: one tail for all windows
+        const int64_t w = c / p.nchunks;
+        if (w >= p.nwin) return;
+        c -= w * p.nchunks;
+        p.fbase += w * p.fcnt;
+    }
+    if (c >= p.nchunks) return;
+    segment_chunk_work<T, VEC, NS, U, MSG, MAXA, IDENT, LIGHT, false>(p, c, lane);
+}
+
+// Source-blocked rows, XCD-affine (workgroup w runs on XCD w % 8). With
+// B >= 8 blocks, XCD x reduces the virtual rows of blocks x*S .. x*S+S-1
+// (S = B / 8); with B < 8, the G = 8 / B XCDs x = b*G .. b*G+G-1 share
+// block b. Either way the source rows an XCD gathers are a 1/B part of x
+// (one feature window at a time), a working set that fits its L2 (B = 8) or
+// lets it hold a larger share of the hot rows (B = 2, 4). Persistent,
+// statically scheduled: the items of the XCD's blocks (sub-block-major, then
+// window, then chunk) are dealt to its wavefronts in turn, so the wavefronts
+// in flight work on neighbouring chunks of one window; XCDs that share a
+// block take every G-th item. The loop is wave-uniform (no lane-dependent
+// branch around its back edge, no atomics). Chunks belong to the block in
+// which they start. Partial rows are written in fp32 (OF32) and folded
+// afterwards.
+constexpr int kMaxSubBlocks = 4;  // source blocks per XCD: B in {2, 4, 8, 16, 24, 32}
+template <typename T, int U, int MSG, bool MAXA>
+__global__ __launch_bounds__(kBlock) void k_segment_xcd(SegParams p) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int x = static_cast<int>(blockIdx.x % kXcds);
+    const int G = p.blocks < kXcds ? static_cast<int>(kXcds / p.blocks) : 1;  // XCDs per block
+    const int S = p.blocks < kXcds ? 1 : static_cast<int>(p.blocks / kXcds);  // blocks per XCD
+    const int64_t b0 = p.blocks < kXcds ? x / G : (int64_t)x * S;
+    const int g = x % G;  // rank among the XCDs of the block
+    // first chunk of each of this XCD's sub-blocks, and the end
+    int64_t cb[kMaxSubBlocks + 1];
+#pragma unroll
+    for (int k = 0; k <= kMaxSubBlocks; ++k) {
+        const int64_t b = b0 + (k < S ? k : S);
+        cb[k] = b >= p.blocks ? p.nchunks : (uniform64(p.rowptr[b * p.rpb]) + p.chunk - 1) / p.chunk;
+    }
+    const int64_t items = (cb[S] - cb[0]) * p.nwin;
+    const int64_t waves = uniform64((int64_t)(gridDim.x / kXcds) * (kBlock / kWave));  // gridDim.x % 8 == 0
+    const int64_t first = uniform64((int64_t)(blockIdx.x / kXcds) * (kBlock / kWave) + threadIdx.x / kWave);
+    const int64_t fbase0 = p.fbase;
+    for (int64_t it = first * G + g; it < items; it += waves * G) {
+        int64_t rem = it, c = cb[0], w = 0;
+        for (int k = 0; k < S; ++k) {
+            const int64_t nk = cb[k + 1] - cb[k];
+            if (rem < nk * p.nwin) {
+                w = rem / nk;
+                c = cb[k] + (rem - w * nk);
+                break;
+            }
+            rem -= nk * p.nwin;
+        }
+        p.fbase = fbase0 + w * p.fcnt;
+        segment_chunk_work<T, true, 1, U, MSG, MAXA, false, false, true>(p, c, lane);
+    }
 }
 
 // Fold the pieces of every long row: one workgroup per chunk that starts a
@@ -589,7 +668,7 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
 // ordered ranges of pieces with 8 loads in flight, then wave 0 combines the
 // four results in wave order: a fixed order, so the fold is deterministic,
 // and for max the earliest piece wins ties.
-template <typename T, bool MAXA, int WAVES>
+template <typename T, bool MAXA, int WAVES, bool OF32>
 __global__ __launch_bounds__(WAVES * kWave) void k_segment_fixup(SegParams p) {
     constexpr int kW = WAVES;
     constexpr int kU = WAVES > 4 ? 16 : 8;
@@ -654,7 +733,8 @@ __global__ __launch_bounds__(WAVES * kWave) void k_segment_fixup(SegParams p) {
                 }
             }
             if (!MAXA && p.mean) acc = acc / static_cast<float>(t - s);
-            if constexpr (sizeof(T) == 2) out[r * p.F + f] = f32_to_bf16_rne(acc);
+            if constexpr (OF32) static_cast<float *>(p.out)[r * p.F + f] = acc;
+            else if constexpr (sizeof(T) == 2) out[r * p.F + f] = f32_to_bf16_rne(acc);
             else out[r * p.F + f] = acc;
             if constexpr (MAXA) p.argmax[r * p.F + f] = p.perm ? p.perm[pos] : static_cast<int64_t>(pos);
         }
@@ -719,14 +799,14 @@ __global__ void k_empty_rows(T *__restrict__ out, int64_t *__restrict__ argmax, 
     }
 }
 
-template <typename T, bool MAXA>
+template <typename T, bool MAXA, bool OF32 = false>
 int launch_fixup(const SegParams &p, hipStream_t s) {
     if (p.nchunks <= 1) return PYG_OK;
     // few, very long rows (e.g. whole-graph pooling): 16 waves fold each row
     if (p.E > 16 * p.chunk * (p.n_rows > 0 ? p.n_rows : 1))
-        k_segment_fixup<T, MAXA, 16><<<static_cast<unsigned>(p.nchunks), 16 * kWave, 0, s>>>(p);
+        k_segment_fixup<T, MAXA, 16, OF32><<<static_cast<unsigned>(p.nchunks), 16 * kWave, 0, s>>>(p);
     else
-        k_segment_fixup<T, MAXA, 4><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
+        k_segment_fixup<T, MAXA, 4, OF32><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
     PYG_LAUNCH_CHECK();
     return PYG_OK;
 }
@@ -858,6 +938,90 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     return PYG_OK;
 }
 
+// Folds the fp32 partial rows of the source blocks in block order:
+// out[i] = sum over b of P[b*N + i] (mean: divided by deg_i, the row's slots
+// over all blocks, as the unblocked kernel divides); max: the largest
+// partial, equal values to the lower edge id, blocks without slots (argmax =
+// sentinel) skipped. A fixed order: deterministic. F % 4 == 0.
+template <typename T, bool MAXA>
+__global__ __launch_bounds__(kBlock) void k_block_fold(const float *__restrict__ P, const int64_t *__restrict__ Parg,
+                                                       const int64_t *__restrict__ rowptr, int64_t N, int64_t F,
+                                                       int64_t B, int mean, int64_t sentinel, T *__restrict__ out,
+                                                       int64_t *__restrict__ argmax) {
+    const int64_t nq = N * F / 4;
+    const int64_t NF = N * F;
+    for (int64_t q = blockIdx.x * (int64_t)kBlock + threadIdx.x; q < nq; q += (int64_t)gridDim.x * kBlock) {
+        const int64_t e = q * 4;  // element i * F + f of four consecutive features
+        float v[4] = {0.f, 0.f, 0.f, 0.f};
+        int64_t a[4] = {sentinel, sentinel, sentinel, sentinel};
+        for (int64_t b = 0; b < B; ++b) {
+            const float4 pv = *reinterpret_cast<const float4 *>(P + b * NF + e);
+            const float pw[4] = {pv.x, pv.y, pv.z, pv.w};
+            if constexpr (MAXA) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int64_t pa = Parg[b * NF + e + k];
+                    if (pa != sentinel && (a[k] == sentinel || pw[k] > v[k] || (pw[k] == v[k] && pa < a[k]))) {
+                        v[k] = pw[k];
+                        a[k] = pa;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) v[k] += pw[k];
+            }
+        }
+        if (!MAXA && mean) {
+            const int64_t i = e / F;
+            int64_t deg = 0;
+            for (int64_t b = 0; b < B; ++b) deg += rowptr[b * N + i + 1] - rowptr[b * N + i];
+            if (deg > 0) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) v[k] = v[k] / static_cast<float>(deg);
+            }
+        }
+        if constexpr (sizeof(T) == 2) {
+            const uint32_t lo = uint32_t(f32_to_bf16_rne(v[0])) | (uint32_t(f32_to_bf16_rne(v[1])) << 16);
+            const uint32_t hi = uint32_t(f32_to_bf16_rne(v[2])) | (uint32_t(f32_to_bf16_rne(v[3])) << 16);
+            *reinterpret_cast<uint2 *>(out + e) = make_uint2(lo, hi);
+        } else {
+            *reinterpret_cast<float4 *>(out + e) = make_float4(v[0], v[1], v[2], v[3]);
+        }
+        if constexpr (MAXA) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) argmax[e + k] = a[k];
+        }
+    }
+}
+
+// Workgroups of a statically scheduled (persistent) launch: as many as are
+// resident at once (a later workgroup would start its equal share late),
+// a multiple of the 8 XCDs. Queried once per kernel.
+template <typename K>
+unsigned resident_grid(K kernel) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kBlock, 0) != hipSuccess || per_cu < 1 ||
+        cus < kXcds)
+        return kXcds * 32 * 4;  // 256 compute units, 4 workgroups each
+    return static_cast<unsigned>(cus / kXcds * kXcds * per_cu);
+}
+
+template <typename T, int MSG>
+int launch_blocked(const SegParams &p, bool maxa, hipStream_t s) {
+    constexpr int U = 8;  // gathers in flight per lane, as in the unblocked kernel
+    if (maxa) {
+        static const unsigned grid = resident_grid(k_segment_xcd<T, U, MSG, true>);
+        k_segment_xcd<T, U, MSG, true><<<grid, kBlock, 0, s>>>(p);
+    } else {
+        static const unsigned grid = resident_grid(k_segment_xcd<T, U, MSG, false>);
+        k_segment_xcd<T, U, MSG, false><<<grid, kBlock, 0, s>>>(p);
+    }
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
+
 struct SegWs {
     float *part_val;
     int32_t *part_pos;
@@ -882,7 +1046,121 @@ SegWs carve_segment(void *base, int64_t E, int64_t F, int aggr, int64_t chunk, i
     return w;
 }
 
+struct BlockedWs {
+    float *P;        // [B * N, F] fp32 partial rows
+    int64_t *Parg;   // [B * N, F] their argmax (max only)
+    void *seg;       // the segment reduction's workspace over the B * N virtual rows
+    size_t seg_bytes;
+    size_t bytes;
+};
+
+BlockedWs carve_blocked(void *base, int64_t E, int64_t N, int64_t F, int64_t B, int aggr, int64_t chunk) {
+    Carver c(base);
+    BlockedWs w{};
+    w.P = c.take<float>(B * N * F);
+    w.Parg = c.take<int64_t>(aggr == PYG_MAX ? B * N * F : 0);
+    w.seg_bytes = carve_segment(nullptr, E, F, aggr, chunk, B * N).bytes;
+    w.seg = c.take<char>(w.seg_bytes);
+    w.bytes = c.used + 256;
+    return w;
+}
+
 }  // namespace
+
+size_t segment_blocked_workspace(int64_t E, int64_t N, int64_t F, int64_t B, int aggr, int64_t chunk) {
+    return carve_blocked(nullptr, E, N, F, B, aggr, segment_chunk(E, B * N, chunk)).bytes;
+}
+
+int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_bytes, hipStream_t s) {
+    const int64_t N = a.n_rows, F = a.F, E = a.E;
+    if (N == 0 || F == 0) return PYG_OK;
+    const bool maxa = a.aggr == PYG_MAX;
+    const int64_t sz = a.dtype == PYG_BF16 ? 2 : 4;
+    if ((F * sz) % 16 != 0 || reinterpret_cast<uintptr_t>(a.x) % 16 != 0 || reinterpret_cast<uintptr_t>(a.out) % 16 != 0)
+        return PYG_ERR_UNSUPPORTED;  // 16-byte lane vectors only
+    if (!(B == 2 || B == 4 || (B % kXcds == 0 && B / kXcds <= kMaxSubBlocks))) return PYG_ERR_UNSUPPORTED;
+    const int64_t chunk = segment_chunk(E, B * N, a.chunk);
+    const BlockedWs w = carve_blocked(ws, E, N, F, B, a.aggr, chunk);
+    if (!ws || ws_bytes < w.bytes) return PYG_ERR_WORKSPACE;
+    if (E == 0) {
+        if (a.dtype == PYG_BF16)
+            k_empty_rows<uint16_t><<<grid_for(N * F, kBlock * 4), kBlock, 0, s>>>(static_cast<uint16_t *>(a.out),
+                                                                                 maxa ? a.argmax : nullptr, N * F, E);
+        else
+            k_empty_rows<float><<<grid_for(N * F, kBlock * 4), kBlock, 0, s>>>(static_cast<float *>(a.out),
+                                                                              maxa ? a.argmax : nullptr, N * F, E);
+        PYG_LAUNCH_CHECK();
+        return PYG_OK;
+    }
+    const SegWs sw = carve_segment(w.seg, E, F, a.aggr, chunk, B * N);
+    SegParams p{};
+    p.x = a.x;
+    p.F = F;
+    p.rowptr = a.rowptr;
+    p.col = a.col;
+    p.w = a.weight;
+    p.perm = a.perm;
+    p.n_rows = B * N;
+    p.E = E;
+    p.chunk = chunk;
+    p.nchunks = (E + chunk - 1) / chunk;
+    p.mean = 0;  // partial sums; the fold divides
+    p.sentinel = E;
+    p.out = w.P;
+    p.argmax = maxa ? w.Parg : nullptr;
+    p.part_val = sw.part_val;
+    p.part_pos = sw.part_pos;
+    p.head_row = sw.head_row;
+    p.class_hist = sw.class_hist;
+    p.hot_slot = sw.hot_slot;
+    p.node_class = sw.node_class;
+    p.hot_class = nullptr;
+    p.blocks = B;
+    p.rpb = N;
+    // windows of up to 128 bytes: 8 lanes of 16 bytes (fewer for narrower rows)
+    const int64_t ep = 16 / sz, nvec = F / ep;
+    int lg = 0;
+    while ((1 << lg) < nvec && lg < 3) ++lg;
+    p.lg_l = lg;
+    p.fbase = 0;
+    p.fcnt = (int64_t(1) << lg) * ep;
+    p.nwin = (F + p.fcnt - 1) / p.fcnt;
+    if (p.nchunks * p.nwin >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    const int mk = a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc);
+    int rc;
+    if (a.dtype == PYG_BF16) {
+        rc = mk == kMsgDiff ? launch_blocked<uint16_t, kMsgDiff>(p, maxa, s)
+                            : (mk == kMsgWeighted ? launch_blocked<uint16_t, kMsgWeighted>(p, maxa, s)
+                                                  : launch_blocked<uint16_t, kMsgSrc>(p, maxa, s));
+    } else {
+        rc = mk == kMsgDiff ? launch_blocked<float, kMsgDiff>(p, maxa, s)
+                            : (mk == kMsgWeighted ? launch_blocked<float, kMsgWeighted>(p, maxa, s)
+                                                  : launch_blocked<float, kMsgSrc>(p, maxa, s));
+    }
+    if (rc != PYG_OK) return rc;
+    // long virtual rows: fold their pieces (all features) into P
+    p.nwin = 1;
+    p.fbase = 0;
+    p.fcnt = F;
+    if (a.dtype == PYG_BF16) rc = maxa ? launch_fixup<uint16_t, true, true>(p, s) : launch_fixup<uint16_t, false, true>(p, s);
+    else rc = maxa ? launch_fixup<float, true, true>(p, s) : launch_fixup<float, false, true>(p, s);
+    if (rc != PYG_OK) return rc;
+    const unsigned g = grid_for(N * F / 4, kBlock, 1 << 16);
+    const int mean = a.aggr == PYG_MEAN;
+    if (a.dtype == PYG_BF16) {
+        if (maxa) k_block_fold<uint16_t, true><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
+                                                                      static_cast<uint16_t *>(a.out), a.argmax);
+        else k_block_fold<uint16_t, false><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
+                                                                  static_cast<uint16_t *>(a.out), a.argmax);
+    } else {
+        if (maxa) k_block_fold<float, true><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
+                                                                   static_cast<float *>(a.out), a.argmax);
+        else k_block_fold<float, false><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
+                                                               static_cast<float *>(a.out), a.argmax);
+    }
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
 
 int64_t segment_chunk(int64_t E, int64_t n_rows, int64_t requested) {
     if (requested > 0) return requested;
