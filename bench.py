@@ -43,9 +43,9 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 # They describe the sources with the recorded hash only: after any change to
 # those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": None,
-    "fetch_kib": None, "write_kib": None, "tcc_hit": None, "tcc_miss": None,
-    "copy_mib": 1024, "copy_fetch_kib": None, "copy_write_kib": None,
+    "source_hash": "d9618da60b8bb337",
+    "fetch_kib": 18542300.7, "write_kib": 166694.0, "tcc_hit": 219795172.7, "tcc_miss": 298164150.0,
+    "copy_mib": 1024, "copy_fetch_kib": 524314.2, "copy_write_kib": 1048576.0,
 }
 # everything that decides which kernels a propagate call launches and how
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp",
@@ -96,6 +96,7 @@ class Probe:
         lib.pyg_probe_gather.argtypes, lib.pyg_probe_gather.restype = [p, u64, i32, i32, i32, u64, u32, i32, i32, p,
                                                                         p], i32
         lib.pyg_probe_stream_read.argtypes, lib.pyg_probe_stream_read.restype = [p, u64, p, p], i32
+        lib.pyg_probe_atomic.argtypes, lib.pyg_probe_atomic.restype = [p, u64, u64, u32, p], i32
         self.lib, self.torch, self.dev = lib, torch, dev
         self.flush_buf = torch.empty(flush_bytes, dtype=torch.uint8, device=dev)
         self.sink = torch.empty(int(lib.pyg_probe_sink_elems()), dtype=torch.int32, device=dev)
@@ -117,6 +118,11 @@ class Probe:
         rc = self.lib.pyg_probe_gather(ctypes.c_void_p(buf.data_ptr()), nbytes, line, parts, stride, n, seed,
                                        in_flight, groups, ctypes.c_void_p(self.sink.data_ptr()), self._stream())
         assert rc == 0, f"pyg_probe_gather: {rc}"
+
+    def atomic(self, buf, nbytes, n_ops, seed=1):
+        import ctypes
+        rc = self.lib.pyg_probe_atomic(ctypes.c_void_p(buf.data_ptr()), nbytes, n_ops, seed, self._stream())
+        assert rc == 0, f"pyg_probe_atomic: {rc}"
 
     def stream_read(self, buf, nbytes):
         import ctypes
@@ -170,6 +176,11 @@ def probe_ladder(probe, torch, dev, x_bytes):
             for parts in (1, 8):
                 ms = timed(torch, lambda: probe.gather(buf, nbytes, 128, parts, n, stride=4), reps=5, warm=1)
                 res["gather_x_stride4" + ("_xcd_local" if parts == 8 else "")] = n * 128 / (ms * 1e-3) / 1e9
+            # float atomics (the COO kernel's scatter): 64-byte atomic requests per second
+            ops = 1 << 24
+            ms = timed(torch, lambda: probe.atomic(buf, nbytes, ops), reps=5, warm=1)
+            res["atomic_x_requests_per_s"] = ops * 4 / (ms * 1e-3)
+            res["atomic_x_float_adds_per_s"] = ops * 64 / (ms * 1e-3)
         if name == "4GiB":
             ms = timed(torch, lambda: probe.stream_read(buf, nbytes), reps=5, warm=1, flush=probe.flush)
             res["stream_read_4GiB_cold"] = nbytes / (ms * 1e-3) / 1e9
@@ -202,6 +213,11 @@ def parse():
                     help="time only the GCN layer (matrix-core X Theta, then propagate) on the large graph")
     ap.add_argument("--edge-features-only", action="store_true",
                     help="time only the edge-feature propagate (max(x_j + e, 0), F-dimensional e) on the large graph")
+    ap.add_argument("--coo-only", action="store_true",
+                    help="only the COO atomic kernel on the large graph (gcn-weighted sum and mean, fp32; one JSON "
+                         "object), e.g. under rocprofv3 counters")
+    ap.add_argument("--fig2-degrees", type=str, default="1,2,4,8,16,32,64,128,256,512",
+                    help="average degrees of the Fig. 2 sweep (comma-separated)")
     ap.add_argument("--fig2-features", type=int, default=64)
     ap.add_argument("--fig2-runs", type=int, default=1000)
     ap.add_argument("--probe-only", action="store_true",
@@ -322,6 +338,20 @@ def main():
         pyg.gcn_norm_csr(csr, out=norm, workspace=ws_norm)
         print(json.dumps({"workload": "large power-law graph, gradient of the propagate", "N": N, "E": E, "F": F,
                           "backward": backward_calls(pyg, torch, x, ei, csr_w, N, E, F, dev)}), flush=True)
+        return
+
+    if args.coo_only:
+        w_coo = pyg.gcn_norm(ei, N)
+        res = {}
+        for aggr in ("sum", "mean"):
+            ws = torch.empty(pyg.propagate_workspace_bytes(x, E, aggr, "coo"), dtype=torch.uint8, device=dev)
+            ms = cold(torch, lambda: pyg.propagate(x, ei, w_coo, aggr=aggr, kernel="coo", out=out, workspace=ws),
+                      reps=3)
+            b = b_alg_coo(N, E, F, 4)
+            res[f"coo-{aggr}-f32"] = {"ms": ms, "alg_GBps": b / (ms * 1e-3) / 1e9, "bytes": b,
+                                      "atomics": E * F, "atomics_per_s": E * F / (ms * 1e-3)}
+        print(json.dumps({"workload": "large power-law graph, COO atomic kernel", "N": N, "E": E, "F": F,
+                          "coo": res}), flush=True)
         return
 
     if args.edge_features_only:
@@ -477,7 +507,7 @@ def fig2_sweep(pyg, torch, synth, dev, args):
         e.synchronize()
         return s.elapsed_time(e)
 
-    for deg in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512):
+    for deg in [int(d) for d in args.fig2_degrees.split(",")]:
         for coalesced in (True, False):
             ei_np = synth.erdos_renyi(N, deg, rng, coalesced)
             E = ei_np.shape[1]

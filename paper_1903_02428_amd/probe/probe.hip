@@ -11,7 +11,9 @@
 //                          draw only from the x-th eighth of the buffer, the
 //                          pattern of an XCD-affine gather (groups should
 //                          then be a multiple of 8);
-//   pyg_probe_stream_read  reads a buffer once, front to back.
+//   pyg_probe_stream_read  reads a buffer once, front to back;
+//   pyg_probe_atomic       n random 256-byte blocks of a float buffer each
+//                          get a float atomic add per element (no return).
 //
 // Every kernel writes one 4-byte word per thread into `sink` (the xor of what
 // it loaded), so no load can be dropped; the sink holds
@@ -94,6 +96,21 @@ __global__ __launch_bounds__(kThreads) void k_stream(const uint4 *__restrict__ b
     sink[tid] = acc;
 }
 
+// Float atomic adds with no return: wavefront op k adds 1 to the 64
+// consecutive floats (256 bytes, four 64-byte atomic requests) of a random
+// 256-byte block of the buffer; ops are independent, so many are in flight.
+// Exactly n_ops * 64 float adds.
+__global__ __launch_bounds__(kThreads) void k_atomic(float *__restrict__ buf, uint32_t blocks, uint64_t n_ops,
+                                                     uint32_t seed) {
+    const int lane = threadIdx.x & 63;
+    const uint64_t wave = (blockIdx.x * (uint64_t)kThreads + threadIdx.x) / 64;
+    const uint64_t nw = (uint64_t)gridDim.x * (kThreads / 64);
+    for (uint64_t k = wave; k < n_ops; k += nw) {
+        const uint64_t b = ((uint64_t)mix32(static_cast<uint32_t>(k) ^ seed) * blocks) >> 32;
+        unsafeAtomicAdd(buf + b * 64 + lane, 1.0f);
+    }
+}
+
 int launched() { return hipGetLastError() == hipSuccess ? 0 : -4; }
 
 }  // namespace
@@ -144,5 +161,14 @@ extern "C" int pyg_probe_stream_read(const void *buf, uint64_t bytes, uint32_t *
     if (!buf || !sink || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(buf) % 16 != 0) return -1;
     k_stream<<<kGroups, kThreads, 0, static_cast<hipStream_t>(stream)>>>(static_cast<const uint4 *>(buf), bytes / 16,
                                                                         sink);
+    return launched();
+}
+
+extern "C" int pyg_probe_atomic(float *buf, uint64_t buf_bytes, uint64_t n_ops, uint32_t seed, void *stream) {
+    if (!buf || reinterpret_cast<uintptr_t>(buf) % 256 != 0 || n_ops >= (uint64_t(1) << 32)) return -1;
+    const uint64_t blocks = buf_bytes / 256;  // block b covers floats [64 b, 64 b + 64): inside the buffer
+    if (blocks == 0 || blocks >= (uint64_t(1) << 32)) return -1;
+    k_atomic<<<kGroups, kThreads, 0, static_cast<hipStream_t>(stream)>>>(buf, static_cast<uint32_t>(blocks), n_ops,
+                                                                        seed);
     return launched();
 }

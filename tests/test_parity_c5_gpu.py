@@ -410,3 +410,72 @@ def test_c5_dense_transform_sampled(pyg, c5):
     out = pyg.dense_transform(to_dev(x_np), to_dev(t32), torch.float32)
     torch.cuda.synchronize()
     check_sum(out[to_dev(rows)], ref32, sabs32, False, "C5 dense fp32 operands")
+
+
+@pytest.fixture(scope="module")
+def c5_oracle_full(c5):
+    """The oracle over the whole large graph (every row): the gcn-weighted sum
+    and mean of fp32 x, the sum of the bf16-rounded x, and the unweighted max
+    with argmax. Four independent single-threaded oracle calls, run side by
+    side (each releases the interpreter while it loops)."""
+    import concurrent.futures as cf
+    ei_np, x_np, N = c5["edge_index_gcn"], c5["x"], c5["N"]
+    w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)
+    xb = bf16_round(x_np)
+    jobs = {"sum": (x_np, w_ref, "sum"), "mean": (x_np, w_ref, "mean"), "sum_bf16": (xb, w_ref, "sum"),
+            "max": (x_np, None, "max")}
+    with cf.ThreadPoolExecutor(len(jobs)) as ex:
+        futs = {k: ex.submit(oracle.propagate, xx, ei_np, ww, aggr=a) for k, (xx, ww, a) in jobs.items()}
+        res = {k: f.result() for k, f in futs.items()}
+    print("[c5] full-graph oracle done", flush=True)
+    return res
+
+
+def test_c5_propagate_every_row(pyg, c5, dev_graph, c5_oracle_full):
+    """The benchmark's propagate (gcn-weighted sum, CSR kernel, the launch
+    configuration it times) on every row of the large graph, and the same
+    CSR with mean, bf16 rows and max / argmax (bit for bit), against the
+    oracle's whole-graph results."""
+    x_np, N = c5["x"], c5["N"]
+    ei, w_ref, csr = dev_graph
+    x32 = to_dev(x_np)
+    ref = c5_oracle_full
+    out, _ = pyg.propagate(x32, csr=csr, aggr="sum")
+    torch.cuda.synchronize()
+    r = check_sum(out, ref["sum"][0], ref["sum"][2], False, "C5 every row: fp32 gcn-weighted sum (CSR)")
+    print(f"[c5] every row fp32 sum ok (worst error / bound {r:.3f})", flush=True)
+    out, _ = pyg.propagate(x32, csr=csr, aggr="mean")
+    torch.cuda.synchronize()
+    check_sum(out, ref["mean"][0], ref["mean"][2], False, "C5 every row: fp32 gcn-weighted mean (CSR)")
+    out, _ = pyg.propagate(x32.to(torch.bfloat16), csr=csr, aggr="sum")
+    torch.cuda.synchronize()
+    check_sum(out, ref["sum_bf16"][0], ref["sum_bf16"][2], True, "C5 every row: bf16 gcn-weighted sum (CSR)")
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E, csr.chunk)
+    out, arg = pyg.propagate(x32, csr=plain, aggr="max")
+    torch.cuda.synchronize()
+    check_max(out, arg, ref["max"][0], ref["max"][1], what="C5 every row: fp32 max / argmax (CSR)")
+    print("[c5] every row: sum, mean, bf16 sum, max ok", flush=True)
+
+
+@pytest.mark.parametrize("B", [2, 8])
+def test_c5_propagate_blocked_every_row(pyg, c5, dev_graph, c5_oracle_full, B):
+    """The source-blocked propagate on every row of the large graph: the
+    gcn-weighted sum in fp32 and bf16, and max / argmax bit for bit."""
+    x_np, N = c5["x"], c5["N"]
+    ei, w_ref, csr = dev_graph
+    ref = c5_oracle_full
+    x32 = to_dev(x_np)
+    bc = pyg.csr_blocks(csr, B)
+    out, _ = pyg.propagate_blocked(x32, bc, "sum")
+    torch.cuda.synchronize()
+    check_sum(out, ref["sum"][0], ref["sum"][2], False, f"C5 every row: blocked B={B} fp32 sum")
+    out, _ = pyg.propagate_blocked(x32.to(torch.bfloat16), bc, "sum")
+    torch.cuda.synchronize()
+    check_sum(out, ref["sum_bf16"][0], ref["sum_bf16"][2], True, f"C5 every row: blocked B={B} bf16 sum")
+    del bc
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E, csr.chunk)
+    bp = pyg.csr_blocks(plain, B, with_perm=True)
+    out, arg = pyg.propagate_blocked(x32, bp, "max")
+    torch.cuda.synchronize()
+    check_max(out, arg, ref["max"][0], ref["max"][1], what=f"C5 every row: blocked B={B} max / argmax")
+    print(f"[c5] every row: blocked B={B} ok", flush=True)
