@@ -937,6 +937,12 @@ class Graph:
         return CSR(c.rowptr, c.col, c.perm, None, c.N, c.E, c.chunk)
 
     @property
+    def plain_t(self) -> CSR:
+        """The CSR of the transposed graph without weights."""
+        c = self.csr_t
+        return CSR(c.rowptr, c.col, c.perm, None, c.N, c.E, c.chunk)
+
+    @property
     def map_t(self) -> torch.Tensor:
         """Transpose map of (csr, csr_t), made on first use."""
         if self._map_t is None:
@@ -951,7 +957,8 @@ class Propagate(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, x, edge_weight, graph: Graph, aggr: str = "sum", msg: str = "src"):
-        csr = graph.csr
+        # without a weight the message is x_j (or x_j - x_i), whatever weights the Graph was built with
+        csr = graph.plain
         if edge_weight is not None:
             # the CSR carries the weights in slot order: refresh them from the current tensor
             csr = CSR(csr.rowptr, csr.col, csr.perm, gather_edges(csr.perm, edge_weight.detach().contiguous()),
@@ -966,7 +973,7 @@ class Propagate(torch.autograd.Function):
     def backward(ctx, grad_out):
         x, edge_weight, argmax = ctx.saved_tensors
         g = ctx.graph
-        csr, csr_t = g.csr, g.csr_t
+        csr, csr_t = g.plain, g.plain_t
         if edge_weight is not None:
             w = edge_weight.detach().contiguous()
             csr = CSR(csr.rowptr, csr.col, csr.perm, gather_edges(csr.perm, w), csr.N, csr.E, csr.chunk)

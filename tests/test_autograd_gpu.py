@@ -93,3 +93,29 @@ def test_propagate_edge_autograd_bf16(pyg, aggr):
         rx, re, sx, se = oracle.propagate_edge_backward(x, ei, ea, g, msg, aggr, argmax=arg)
         check_sum(xt.grad, rx, sx, True, f"PropagateEdge bf16 {msg} {aggr} grad_x")
         check_sum(et.grad, re, se, True, f"PropagateEdge bf16 {msg} {aggr} grad_e")
+
+
+@pytest.mark.parametrize("aggr,msg", [("sum", "src"), ("mean", "src"), ("max", "src"), ("sum", "diff"),
+                                      ("max", "diff")])
+def test_propagate_autograd_unweighted_on_weighted_graph(pyg, aggr, msg):
+    """A Graph built with weights, used without them: Eq. (1) with phi = x_j
+    (or x_j - x_i) and its gradient, not the weighted propagate."""
+    rng = np.random.default_rng(37)
+    N, E, F = 600, 8000, 16
+    ei = synth.random_coo(rng, N, E)
+    x = rng.standard_normal((N, F)).astype(np.float32)
+    w = rng.standard_normal(E).astype(np.float32)
+    g = rng.standard_normal((N, F)).astype(np.float32)
+    graph = pyg.Graph(to_dev(ei), N, to_dev(w))
+    xt = to_dev(x).requires_grad_()
+    out = pyg.Propagate.apply(xt, None, graph, aggr, msg)
+    out.backward(to_dev(g))
+    torch.cuda.synchronize()
+    ref, rarg, sabs = oracle.propagate(x, ei, None, msg=msg, aggr=aggr)
+    if aggr == "max":
+        assert np.array_equal(out.detach().cpu().numpy(), ref.astype(np.float32)), "forward max"
+    else:
+        check_sum(out.detach(), ref, sabs, False, f"forward {aggr} {msg}")
+    rx, _, sx, _ = oracle.propagate_backward(x, ei, g, None, msg=msg, aggr=aggr,
+                                             argmax=rarg if aggr == "max" else None)
+    check_sum(xt.grad, rx, sx, False, f"grad_x {aggr} {msg}")
