@@ -6,13 +6,16 @@ Workload: the large power-law graph (Chung-Lu degree exponent 2.1, N=232,965,
 features. One step is one pass of the whole path on that graph, inputs
 already resident in HBM:
 
-    degree -> coo_to_csr -> gcn_norm (in CSR slot order) -> propagate
+    coo_to_csr -> degree (from the CSR row bounds) -> gcn_norm (CSR slot
+    order, formed and written inside the propagate) + propagate
     (gcn_norm-weighted sum, CSR segment kernel) -> global mean pool
 
 `value` is E*F of the step's propagate divided by the step time
-(edges*features/s). The `roofline` object covers the dominant call, the CSR
-propagate (its feature-window launches together), timed with HIP events on
-the launch stream inside the timed steps.
+(edges*features/s). The `roofline` object covers the dominant call, the
+fused gcn_norm + propagate (its launches together), timed with HIP events on
+the launch stream inside the timed steps: its bytes past L2 (rocprofv3
+counters recorded below) against the gather ceiling the bandwidth probes
+measure in the same run.
 `cpu_baseline` times the oracle (single-threaded plain C loop) on a bounded
 sample of the same workload. `detail` adds per-call times and the COO-vs-CSR,
 fp32-vs-bf16 and sum-vs-mean comparison.
@@ -360,7 +363,8 @@ def main():
                           "edge_features": edge_features(pyg, torch, x, ei, csr, N, E, F, dev)}), flush=True)
         return
 
-    names = ["coo_to_csr", "degree", "gcn_norm", "propagate", "global_pool"]
+    ws_gcn = torch.empty(pyg.gcn_propagate_workspace_bytes(x, csr), dtype=torch.uint8, device=dev)
+    names = ["coo_to_csr", "degree", "gcn_norm+propagate", "global_pool"]
     ev = {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
     times = {n: [] for n in names}
 
@@ -374,12 +378,11 @@ def main():
         mark("degree", 0)  # the in-degree, read off the row boundaries the sort produced
         pyg.degree_csr(csr, out=deg)
         mark("degree", 1)
-        mark("gcn_norm", 0)
-        pyg.gcn_norm_csr(csr, out=norm, workspace=ws_norm)
-        mark("gcn_norm", 1)
-        mark("propagate", 0)
-        pyg.propagate(x, csr=csr_w, aggr="sum", out=out, workspace=ws_prop)
-        mark("propagate", 1)
+        # gcn_norm formed inside the propagate (pyg_gcn_propagate): the norms are
+        # written to `norm` (CSR slot order) and summed with the gathered rows
+        mark("gcn_norm+propagate", 0)
+        pyg.gcn_propagate(x, csr, norm_out=norm, out=out, workspace=ws_gcn)
+        mark("gcn_norm+propagate", 1)
         mark("global_pool", 0)
         pyg.global_pool(out, batch, 1, "mean", out=pooled, workspace=ws_pool)
         mark("global_pool", 1)
@@ -408,10 +411,13 @@ def main():
             times[n].append(ev[n][0].elapsed_time(ev[n][1]))
     ms_per_step = wall / args.steps * 1e3
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+    out_step = out.clone()  # the step's output, for the sampled parity check after the detail calls
 
-    t_prop = float(np.mean(times["propagate"])) * 1e-3
-    balg = b_alg_csr(N, E, F, 4)
-    buniq = b_uniq_csr(N, E, F, 4)
+    t_prop = float(np.mean(times["gcn_norm+propagate"])) * 1e-3
+    # the fused call: columns once per window, x rows gathered, the norms
+    # formed (rowptr, dinv per node and per slot) and written, the output
+    balg = b_alg_csr(N, E, F, 4, weighted=False) + 8 * N + 8 * E + 4 * E
+    buniq = b_uniq_csr(N, E, F, 4, weighted=False) + 8 * N + 4 * E
     value = E * F / (ms_per_step * 1e-3)
     ladder = probe_ladder(probe, torch, dev, N * F * 4)
     log("probe ladder done")
@@ -434,7 +440,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": "large power-law graph (Chung-Lu gamma=2.1), gcn_norm-weighted sum, CSR segment kernel",
                    "N": N, "E": E, "F": F, "seed": args.seed, "chunk": args.chunk or "default",
-                   "step": "coo_to_csr+degree(csr row bounds)+gcn_norm(csr order)+propagate(sum,csr)+global_pool(mean)"},
+                   "step": "coo_to_csr+degree(csr row bounds)+[gcn_norm(csr order) formed and written inside the "
+                           "propagate (sum, csr)]+global_pool(mean)"},
         "roofline": {"bound": "fabric", "achieved": achieved, "peak": peak, "unit": "GB/s",
                      "frac": achieved / peak if achieved is not None else None, "traffic": traffic,
                      "peak_source": "measured in this run: random 128-byte lines gathered from a buffer the size "
@@ -443,23 +450,30 @@ def main():
                      "achieved_source": "bytes past L2 per call (FETCH_SIZE + WRITE_SIZE counters, copy-calibrated) "
                                         "/ the call's event time in the timed steps",
                      "l2_hit": measured_l2_hit(),
-                     "kernel": "pyg_propagate CSR segment, fp32 weighted sum (k_segment + k_segment_fixup)",
-                     "unit_of_work": "one propagate call over the whole graph",
+                     "kernel": "pyg_gcn_propagate, fp32: k_segment over feature window 0 forming and writing the "
+                               "gcn norms, k_segment over windows 1-3 reading them, k_segment_fixup",
+                     "unit_of_work": "one gcn_norm+propagate call over the whole graph",
                      "avg_call_ms": t_prop * 1e3,
                      "algorithmic": {"bytes_per_call": balg, "GBps": balg / t_prop / 1e9, "hbm_peak": HBM_PEAK_GBS,
                                      "frac_of_hbm": balg / t_prop / 1e9 / HBM_PEAK_GBS,
-                                     "convention": "every edge gathers its source row once (cache reuse counted as "
-                                                   "traffic), plus rowptr, columns, weights and one output write"},
+                                     "convention": "every edge gathers its source row and its source's d^-1/2 once "
+                                                   "(cache reuse counted as traffic), plus rowptr, columns, d^-1/2 "
+                                                   "per node, the norms written and one output write"},
                      "compulsory": {"bytes_per_call": buniq, "GBps": buniq / t_prop / 1e9,
                                     "frac_of_hbm": buniq / t_prop / 1e9 / HBM_PEAK_GBS,
-                                    "convention": "every distinct byte once: rowptr, columns, weights, x, output"}},
+                                    "convention": "every distinct byte once: rowptr, columns, d^-1/2, x, norms "
+                                                  "written, output"}},
         "probe": ladder,
         "detail": {"per_call_ms": {n: float(np.mean(times[n])) for n in names},
                    "per_call_cache": "in-step: each call follows the previous call of the same step",
                    "detail_cache": "warm (back to back)" if args.warm_detail else
                                    "cold: a 1 GiB write before every timed call evicts L2 and the Infinity Cache",
                    "propagate_edges_features_per_s": E * F / t_prop,
-                   "degree_from_coo_ms": cold(torch, lambda: pyg.degree(ei, N, out=deg, workspace=ws_deg))},
+                   "degree_from_coo_ms": cold(torch, lambda: pyg.degree(ei, N, out=deg, workspace=ws_deg)),
+                   # the same two rows as separate calls (gcn_norm pass, then the weighted propagate)
+                   "gcn_norm_csr_ms": cold(torch, lambda: pyg.gcn_norm_csr(csr, out=norm, workspace=ws_norm)),
+                   "propagate_weighted_ms": cold(torch, lambda: pyg.propagate(x, csr=csr_w, aggr="sum", out=out,
+                                                                              workspace=ws_prop))},
     }
 
     if not args.no_detail:
@@ -474,7 +488,7 @@ def main():
         import oracle
         w_ref = oracle.gcn_norm(ei_np, N).astype(np.float32)  # the oracle's own weights
     if not args.no_detail:
-        result["detail"]["parity_sampled"] = sampled_parity(x_np, ei_np, w_ref, out, N)
+        result["detail"]["parity_sampled"] = sampled_parity(x_np, ei_np, w_ref, out_step, N)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(x_np, ei_np, w_ref, N, F, args.cpu_sample_rows, args.seed)
     print(json.dumps(result), flush=True)

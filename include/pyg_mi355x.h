@@ -212,6 +212,26 @@ int pyg_gcn_norm_csr_workspace(int64_t N, size_t *bytes);
  * PYG_ERR_WORKSPACE. */
 int pyg_gcn_norm_csr(const pyg_csr *csr, float *norm_csr, void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes needed by pyg_gcn_propagate (chunk = csr->chunk). */
+int pyg_gcn_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t chunk, size_t *bytes);
+
+/* The GCN propagate with its normalisation fused in (the GCN operator of
+ * Section 2; Eq. (1) with phi = norm_p * x_j and a sum):
+ *   out[i] = sum over the slots p of row i of norm_p * x[col[p]],
+ *   norm_p = d_j^-1/2 * w_p * d_i^-1/2, d and w as pyg_gcn_norm_csr (the CSR's
+ * weights, or 1), formed in fp64 and rounded once to fp32 per slot inside
+ * the propagate (by its first 128-byte feature window, which writes them;
+ * the later windows read them back), instead of a separate pass.
+ *   csr       CSR from pyg_coo_to_csr; csr->weight optional (the w_p);
+ *   norm_out  fp32 [E] in CSR slot order, or NULL: receives every norm_p,
+ *             equal bit for bit to pyg_gcn_norm_csr's output;
+ *   x, out    as pyg_propagate (out fully overwritten, fp32 accumulation).
+ * Deterministic. Errors: PYG_ERR_INVALID_ARG (bad dtype, NULL/inconsistent
+ * csr, NULL x/out, norm_out or out overlapping another array),
+ * PYG_ERR_UNSUPPORTED (N or E >= 2^31), PYG_ERR_WORKSPACE. */
+int pyg_gcn_propagate(const void *x, int dtype, int64_t N, int64_t F, const pyg_csr *csr, float *norm_out,
+                      void *out, void *ws, size_t ws_bytes, void *stream);
+
 /* Workspace bytes needed by pyg_propagate for this shape, aggregation and
  * kernel (pass the same chunk as csr->chunk; 0 = default). */
 int pyg_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int aggr, int kernel,

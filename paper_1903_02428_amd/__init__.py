@@ -33,6 +33,8 @@ from .binding import (  # noqa: F401
     gather_edges,
     gcn_norm,
     gcn_norm_csr,
+    gcn_propagate,
+    gcn_propagate_workspace_bytes,
     global_pool,
     library,
     library_path,

@@ -31,7 +31,7 @@ EXPORTED = [
     "pyg_propagate_heads_backward_workspace", "pyg_propagate_heads_backward", "pyg_gat_scores_backward_workspace",
     "pyg_gat_scores_backward",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
-    "pyg_propagate_noalloc", "pyg_csr_blocks_workspace", "pyg_csr_blocks_build", "pyg_propagate_blocked_workspace",
+    "pyg_propagate_noalloc", "pyg_gcn_propagate_workspace", "pyg_gcn_propagate", "pyg_csr_blocks_workspace", "pyg_csr_blocks_build", "pyg_propagate_blocked_workspace",
     "pyg_propagate_blocked",
 ]
 
@@ -90,6 +90,8 @@ def library() -> ctypes.CDLL:
             "pyg_propagate_workspace": [i32, i64, i64, i64, i32, i32, i64, sz],
             "pyg_propagate": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p,
                               ctypes.c_size_t, p],
+            "pyg_gcn_propagate_workspace": [i32, i64, i64, i64, i64, sz],
+            "pyg_gcn_propagate": [p, i32, i64, i64, ctypes.POINTER(_Csr), p, p, p, ctypes.c_size_t, p],
             "pyg_csr_blocks_workspace": [i64, i64, i64, sz],
             "pyg_csr_blocks_build": [ctypes.POINTER(_Csr), i64, p, p, p, p, p, ctypes.c_size_t, p],
             "pyg_propagate_blocked_workspace": [i32, i64, i64, i64, i64, i32, i64, sz],
@@ -392,6 +394,37 @@ def gcn_norm_csr(csr: CSR, out: torch.Tensor | None = None, workspace: torch.Ten
     c = csr._c()
     _check(lib.pyg_gcn_norm_csr(ctypes.byref(c), _ptr(norm), _ptr(ws), nbytes, _stream(dev)), "pyg_gcn_norm_csr")
     return norm
+
+
+def gcn_propagate(x: torch.Tensor, csr: CSR, norm_out: torch.Tensor | None = None, out: torch.Tensor | None = None,
+                  workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """GCN propagate with the normalisation fused in (pyg_gcn_propagate):
+    out_i = sum_p norm_p x_col[p], norm_p = d_j^-1/2 w_p d_i^-1/2 formed per slot;
+    the norms go to norm_out (CSR slot order) when given."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    if x.dtype not in DTYPE:
+        raise ValueError("x must be float32 or bfloat16")
+    N, F = x.shape
+    if csr.N != N:
+        raise ValueError("csr does not match x")
+    if norm_out is not None:
+        _need_cuda("norm_out", norm_out, torch.float32, 1)
+        if norm_out.shape[0] != csr.E:
+            raise ValueError("norm_out must be [E]")
+    if out is None:
+        out = torch.empty_like(x)
+    nbytes = _size(lib.pyg_gcn_propagate_workspace, DTYPE[x.dtype], N, F, csr.E, csr.chunk)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, x.device)
+    c = csr._c()
+    _check(lib.pyg_gcn_propagate(_ptr(x), DTYPE[x.dtype], N, F, ctypes.byref(c), _ptr(norm_out), _ptr(out),
+                                 _ptr(workspace), workspace.numel(), _stream(x.device)), "pyg_gcn_propagate")
+    return out
+
+
+def gcn_propagate_workspace_bytes(x: torch.Tensor, csr: CSR) -> int:
+    return _size(library().pyg_gcn_propagate_workspace, DTYPE[x.dtype], x.shape[0], x.shape[1], csr.E, csr.chunk)
 
 
 def propagate_workspace_bytes(x: torch.Tensor, E: int, aggr: str, kernel: str, chunk: int = 0) -> int:

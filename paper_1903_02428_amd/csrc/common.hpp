@@ -166,11 +166,16 @@ struct SegmentArgs {
     void *out;          // [n_rows, F]
     int64_t *argmax;    // [n_rows, F] or NULL
     bool hint;          // allow the cache-policy hint for hub source rows
+    const double *dinv; // kSegMsgGcn: d^-1/2 of every row [n_rows]
+    float *norm_out;    // kSegMsgGcn: the slots' weights written here [E], or NULL
 };
 // Internal message kind beyond pyg_msg (sum only): the backward of
 // max(x_j + e, 0) over the reversed graph, x = the scaled upstream gradient,
 // gate x_self[row] + e > 0.
 constexpr int kSegMsgEdgeReluGrad = 100;
+// Internal message kind (sum only): GCN, slot weight dinv[col] * w * dinv[row]
+// formed in fp64 and rounded once (w = csr weight, or 1), optionally written out.
+constexpr int kSegMsgGcn = 101;
 int64_t segment_chunk(int64_t E, int64_t n_rows, int64_t requested);
 // Source-blocked form: a.rowptr has B * n_rows + 1 entries (virtual row
 // b * n_rows + i = the slots of target i whose source lies in block b), a.col,

@@ -240,3 +240,67 @@ extern "C" int pyg_gcn_norm(const int64_t *edge_index, const float *edge_weight,
     PYG_LAUNCH_CHECK();
     return PYG_OK;
 }
+
+// ---------------------------------------------- normalisation fused into the propagate
+
+extern "C" int pyg_gcn_propagate_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t chunk, size_t *bytes) {
+    if (!bytes || (dtype != PYG_F32 && dtype != PYG_BF16) || N < 0 || F < 0 || E < 0 || chunk < 0)
+        return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    // dinv, the slots' weights (when the caller keeps none), the segment reduction
+    *bytes = align_up(static_cast<size_t>(N) * sizeof(double), 256) + align_up(static_cast<size_t>(E) * 4, 256) +
+             segment_workspace(E, F, PYG_SUM, chunk, N);
+    return PYG_OK;
+}
+
+extern "C" int pyg_gcn_propagate(const void *x, int dtype, int64_t N, int64_t F, const pyg_csr *csr, float *norm_out,
+                                 void *out, void *ws, size_t ws_bytes, void *stream) {
+    if ((dtype != PYG_F32 && dtype != PYG_BF16) || N < 0 || F < 0 || !csr || !csr->rowptr) return PYG_ERR_INVALID_ARG;
+    const int64_t E = csr->E;
+    if (csr->N != N || E < 0 || csr->chunk < 0) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    if (E > 0 && (!csr->col || N == 0)) return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && (!x || !out)) return PYG_ERR_INVALID_ARG;
+    const int64_t xbytes = N * F * (dtype == PYG_BF16 ? 2 : 4);
+    const uintptr_t xa = reinterpret_cast<uintptr_t>(x), oa = reinterpret_cast<uintptr_t>(out),
+                    na = reinterpret_cast<uintptr_t>(norm_out);
+    auto overlap = [](uintptr_t a, int64_t an, uintptr_t b, int64_t bn) {
+        return a && b && an > 0 && bn > 0 && a < b + static_cast<uintptr_t>(bn) && b < a + static_cast<uintptr_t>(an);
+    };
+    if (overlap(xa, xbytes, oa, xbytes) || overlap(na, E * 4, xa, xbytes) || overlap(na, E * 4, oa, xbytes))
+        return PYG_ERR_INVALID_ARG;
+    size_t need;
+    PYG_TRY(pyg_gcn_propagate_workspace(dtype, N, F, E, csr->chunk, &need));
+    if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
+    if (N == 0) return PYG_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (F == 0)  // nothing to propagate: the norms alone
+        return norm_out ? pyg_gcn_norm_csr(csr, norm_out, ws, ws_bytes, stream) : PYG_OK;
+    double *dinv = static_cast<double *>(ws);
+    float *norm_ws = reinterpret_cast<float *>(static_cast<char *>(ws) + align_up(static_cast<size_t>(N) * sizeof(double), 256));
+    void *seg_ws = reinterpret_cast<char *>(norm_ws) + align_up(static_cast<size_t>(E) * 4, 256);
+    if (csr->weight)
+        k_row_dinv_weighted<<<grid_for(N, kBlock / kWave, 1 << 16), kBlock, 0, s>>>(csr->rowptr, csr->weight, N, dinv);
+    else
+        k_row_dinv_count<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(csr->rowptr, N, dinv);
+    PYG_LAUNCH_CHECK();
+    SegmentArgs a{};
+    a.x = x;
+    a.dtype = dtype;
+    a.F = F;
+    a.rowptr = csr->rowptr;
+    a.col = csr->col;
+    a.weight = csr->weight;
+    a.perm = csr->perm;
+    a.n_rows = N;
+    a.E = E;
+    a.msg = kSegMsgGcn;
+    a.aggr = PYG_SUM;
+    a.chunk = csr->chunk;
+    a.sentinel = E;
+    a.out = out;
+    a.hint = true;
+    a.dinv = dinv;
+    a.norm_out = norm_out ? norm_out : norm_ws;  // the later feature windows read the weights back
+    return segment_reduce(a, seg_ws, ws_bytes - (static_cast<char *>(seg_ws) - static_cast<char *>(ws)), s);
+}

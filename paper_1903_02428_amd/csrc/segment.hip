@@ -84,6 +84,11 @@ struct SegParams {
     // `rpb` virtual rows, virtual row r = (source block r / rpb, target r % rpb)
     int64_t blocks;
     int64_t rpb;
+    // GCN messages (kMsgGcn): dinv [n_rows] fp64 (d^-1/2 of every row), the
+    // slot weight w_p = dinv[col] * w_p * dinv[row] formed in fp64 and rounded
+    // once; norm_out [E] (or NULL) receives it from the window at feature 0
+    const double *dinv;
+    float *norm_out;
 };
 
 // Measured on the large power-law graph (F = 128): fp32 rows (512 B) gain
@@ -226,6 +231,10 @@ constexpr int kMsgEdgeAdd = 4, kMsgEdgeRelu = 5, kMsgEdgeMul = 6;  // x_j + e, m
 // Backward of max(x_r + e, 0) over the reversed graph: the gathered upstream
 // gradient where x_r + e > 0, x_r being the row's own features (x_self).
 constexpr int kMsgEdgeReluGrad = 7;
+// GCN: the weight of slot p is dinv[col[p]] * w_p * dinv[row] (w_p = 1 without weights)
+constexpr int kMsgGcn = 8;
+// messages whose slot carries a scalar weight (read or formed)
+template <int MSG> constexpr bool kWeightedMsg = MSG == 1 || MSG == 8;
 
 // Edge-feature message of one element (formed in fp32, as compared by max).
 template <int MSG>
@@ -272,6 +281,9 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
 #pragma unroll
         for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(xr + rr * p.F + f0[sl]) : LN::zero();
     }
+    // GCN: the row's own d^-1/2
+    double dr = 0.0;
+    if constexpr (MSG == kMsgGcn) dr = p.dinv[r];
     // per-head weights: a lane vector never straddles two heads (C is a multiple of its width)
     int64_t hd[NS];
 #pragma unroll
@@ -285,6 +297,11 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
             c = static_cast<int>(e);
         } else {
             c = __builtin_nontemporal_load(p.col + e);
+            if constexpr (MSG == kMsgGcn) {
+                const double wv = p.w ? static_cast<double>(__builtin_nontemporal_load(p.w + e)) : 1.0;
+                w = static_cast<float>(p.dinv[c] * wv * dr);
+                if (p.norm_out && p.fbase == 0) p.norm_out[e] = w;  // every slot once, by the first window
+            }
             if (hot > 0 && p.node_class[c] < hot) c |= static_cast<int>(0x80000000u);
         }
         if constexpr (MSG == kMsgWeighted) w = __builtin_nontemporal_load(p.w + e);
@@ -308,7 +325,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                 const int idx = st + u * S + sg;
                 ok[u] = idx < n;
                 jj[u] = __shfl(myc, idx & (kWave - 1), kWave);
-                if constexpr (MSG == kMsgWeighted) ww[u] = __shfl(myw, idx & (kWave - 1), kWave);
+                if constexpr (kWeightedMsg<MSG>) ww[u] = __shfl(myw, idx & (kWave - 1), kWave);
                 if constexpr (MSG == kMsgHeads) aa[u] = __shfl(mya, idx & (kWave - 1), kWave);
             }
             float wh[U][NS];
@@ -357,7 +374,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                         if constexpr (MAXA) {
                             float m;
                             if constexpr (MSG == kMsgDiff) m = xv - LN::get(xi[sl], e);
-                            else if constexpr (MSG == kMsgWeighted) m = ww[u] * xv;
+                            else if constexpr (kWeightedMsg<MSG>) m = ww[u] * xv;
                             else if constexpr (EDGE) m = edge_msg<MSG>(xv, LN::get(ev[u][sl], e));
                             else m = xv;
                             m = canon_zero(m);
@@ -367,7 +384,7 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
                             }
                         } else {
                             if constexpr (MSG == kMsgDiff) acc[sl][e] += xv - LN::get(xi[sl], e);
-                            else if constexpr (MSG == kMsgWeighted) acc[sl][e] = fmaf(ww[u], xv, acc[sl][e]);
+                            else if constexpr (kWeightedMsg<MSG>) acc[sl][e] = fmaf(ww[u], xv, acc[sl][e]);
                             else if constexpr (MSG == kMsgHeads) acc[sl][e] = fmaf(wh[u][sl], xv, acc[sl][e]);
                             else if constexpr (MSG == kMsgEdgeMul) acc[sl][e] = fmaf(xv, LN::get(ev[u][sl], e), acc[sl][e]);
                             else if constexpr (MSG == kMsgEdgeReluGrad)
@@ -468,6 +485,15 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
             jj[u] = ok[u] ? (IDENT ? static_cast<int>(base + u) : p.col[base + u]) : 0;
             ww[u] = 1.f;
             if constexpr (MSG == kMsgWeighted) ww[u] = ok[u] ? p.w[base + u] : 0.f;
+            if constexpr (MSG == kMsgGcn) {
+                if (ok[u]) {
+                    const double wv = p.w ? static_cast<double>(p.w[base + u]) : 1.0;
+                    ww[u] = static_cast<float>(p.dinv[jj[u]] * wv * p.dinv[r]);
+                    if (p.norm_out && p.fbase == 0 && q == 0) p.norm_out[base + u] = ww[u];
+                } else {
+                    ww[u] = 0.f;
+                }
+            }
             if constexpr (MSG == kMsgHeads) {
                 const int64_t ar = p.alpha_idx ? (ok[u] ? p.alpha_idx[base + u] : 0) : base + u;
                 ww[u] = (ok[u] && act) ? p.alpha[ar * p.H + hd] : 0.f;
@@ -497,7 +523,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
                 if constexpr (MAXA) {
                     float m;
                     if constexpr (MSG == kMsgDiff) m = xv - LN::get(xi, e);
-                    else if constexpr (MSG == kMsgWeighted) m = ww[u] * xv;
+                    else if constexpr (kWeightedMsg<MSG>) m = ww[u] * xv;
                     else if constexpr (EDGE) m = edge_msg<MSG>(xv, LN::get(ev[u], e));
                     else m = xv;
                     m = canon_zero(m);
@@ -507,7 +533,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
                     }
                 } else {
                     if constexpr (MSG == kMsgDiff) acc[e] += xv - LN::get(xi, e);
-                    else if constexpr (MSG == kMsgWeighted || MSG == kMsgHeads) acc[e] = fmaf(ww[u], xv, acc[e]);
+                    else if constexpr (kWeightedMsg<MSG> || MSG == kMsgHeads) acc[e] = fmaf(ww[u], xv, acc[e]);
                     else if constexpr (MSG == kMsgEdgeMul) acc[e] = fmaf(xv, LN::get(ev[u], e), acc[e]);
                     else if constexpr (MSG == kMsgEdgeReluGrad) acc[e] += LN::get(xi, e) + LN::get(ev[u], e) > 0.f ? xv : 0.f;
                     else if constexpr (EDGE) acc[e] += edge_msg<MSG>(xv, LN::get(ev[u], e));
@@ -845,6 +871,9 @@ int launch_msg(const SegParams &p, int msg, bool ident, int ns, bool light, bool
     if (msg == kMsgEdgeMul) return launch_ns<T, VEC, kMsgEdgeMul, MAXA, false>(p, ns, light, fixup, s);
     if (msg == kMsgDiff) return launch_ns<T, VEC, kMsgDiff, MAXA, false>(p, ns, light, fixup, s);
     if (msg == kMsgWeighted) return launch_ns<T, VEC, kMsgWeighted, MAXA, false>(p, ns, light, fixup, s);
+    if constexpr (!MAXA) {
+        if (msg == kMsgGcn) return launch_ns<T, VEC, kMsgGcn, false, false>(p, ns, light, fixup, s);
+    }
     return launch_ns<T, VEC, kMsgSrc, MAXA, false>(p, ns, light, fixup, s);
 }
 
@@ -866,6 +895,7 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     const int ep = vec ? 16 / (int)sizeof(T) : 1;
     const int64_t nvec = a.F / ep;  // lane vectors per row
     int mk = a.alpha ? kMsgHeads : (a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc));
+    if (a.msg == kSegMsgGcn) mk = kMsgGcn;
     if (a.msg == PYG_MSG_EDGE_ADD) mk = kMsgEdgeAdd;
     if (a.msg == PYG_MSG_EDGE_RELU) mk = kMsgEdgeRelu;
     if (a.msg == PYG_MSG_EDGE_MUL) mk = kMsgEdgeMul;
@@ -874,7 +904,7 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     // narrow windows: gathered (not identity) source rows of one of the
     // plain messages, vector lanes, rows wider than a window, large in total
     const bool narrow = kWindowBytes > 0 && vec && !ident &&
-                        (PYG_NARROW_ALL || mk == kMsgSrc || mk == kMsgWeighted || mk == kMsgDiff) &&
+                        (PYG_NARROW_ALL || mk == kMsgSrc || mk == kMsgWeighted || mk == kMsgDiff || mk == kMsgGcn) &&
                         row_bytes > kWindowBytes &&
                         row_bytes % kWindowBytes == 0 && a.n_rows * row_bytes >= kWindowMinBytes;
     // cache hint: only when the source rows do not fit in L2 (row in-degree as the hotness proxy)
@@ -903,8 +933,24 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
         p.nwin = nvec / per_window;
         const bool light = lg < 6 && a.E <= kLightMaxDegree * a.n_rows;
         int rc;
-        if (maxa) rc = launch_msg<T, true, true>(p, mk, ident, 1, light, false, s);
-        else rc = launch_msg<T, true, false>(p, mk, ident, 1, light, false, s);
+        if (mk == kMsgGcn && p.nwin > 1) {
+            // GCN: window 0 forms every slot's weight and writes it (norm_out is
+            // set); the later windows read those weights (stream order) instead
+            // of forming them again
+            SegParams q = p;
+            q.nwin = 1;
+            rc = launch_msg<T, true, false>(q, kMsgGcn, ident, 1, light, false, s);
+            if (rc != PYG_OK) return rc;
+            q = p;
+            q.fbase = p.fcnt;
+            q.nwin = p.nwin - 1;
+            q.w = p.norm_out;
+            rc = launch_msg<T, true, false>(q, kMsgWeighted, ident, 1, light, false, s);
+        } else if (maxa) {
+            rc = launch_msg<T, true, true>(p, mk, ident, 1, light, false, s);
+        } else {
+            rc = launch_msg<T, true, false>(p, mk, ident, 1, light, false, s);
+        }
         if (rc != PYG_OK) return rc;
         p.nwin = 1;
         p.fbase = 0;
@@ -1221,6 +1267,8 @@ int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t 
     p.class_hist = w.class_hist;
     p.hot_slot = w.hot_slot;
     p.node_class = w.node_class;
+    p.dinv = a.dinv;
+    p.norm_out = a.norm_out;
     return a.dtype == PYG_BF16 ? run_typed<uint16_t>(a, p, s) : run_typed<float>(a, p, s);
 }
 

@@ -479,3 +479,18 @@ def test_c5_propagate_blocked_every_row(pyg, c5, dev_graph, c5_oracle_full, B):
     torch.cuda.synchronize()
     check_max(out, arg, ref["max"][0], ref["max"][1], what=f"C5 every row: blocked B={B} max / argmax")
     print(f"[c5] every row: blocked B={B} ok", flush=True)
+
+
+def test_c5_gcn_propagate_every_row(pyg, c5, dev_graph, c5_oracle_full):
+    """The fused GCN propagate (the benchmark step's call) on the large graph:
+    norms bit for bit against the oracle's, every output row against the
+    oracle's gcn-weighted sum."""
+    x_np, N = c5["x"], c5["N"]
+    ei, w_ref, csr = dev_graph
+    plain = pyg.CSR(csr.rowptr, csr.col, csr.perm, None, N, csr.E, csr.chunk)
+    norm = torch.empty(csr.E, device="cuda")
+    out = pyg.gcn_propagate(to_dev(x_np), plain, norm_out=norm)
+    torch.cuda.synchronize()
+    assert torch.equal(norm, csr.weight), "C5 fused norms differ from the oracle's (in CSR order)"
+    r = check_sum(out, c5_oracle_full["sum"][0], c5_oracle_full["sum"][2], False, "C5 every row: fused GCN propagate")
+    print(f"[c5] every row: fused GCN propagate ok (worst error / bound {r:.3f})", flush=True)
