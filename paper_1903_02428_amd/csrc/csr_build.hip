@@ -375,7 +375,8 @@ __device__ __forceinline__ uint64_t pack_edge(const int64_t *__restrict__ dst64,
 // Digit counts per tile (digit-major) of the packed elements; pass 0 packs
 // from the COO itself.
 __global__ __launch_bounds__(kSortBlock) void k_radix_hist64(const int64_t *__restrict__ dst64,
-                                                         const uint64_t *__restrict__ keys, int64_t E, int shift,
+                                                         const uint64_t *__restrict__ keys,
+                                                         const uint8_t *__restrict__ dig8, int64_t E, int shift,
                                                          int bits, int64_t ntiles, Packing pk,
                                                          uint32_t *__restrict__ hist) {
     __shared__ uint32_t h[kMaxRadixP];
@@ -389,8 +390,9 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist64(const int64_t *__re
     for (int r = 0; r < kItems; ++r) {
         const int64_t i = base + (int64_t)r * kSortBlock;
         if (i < E) {
-            const uint64_t d = dst64 ? (static_cast<uint64_t>(dst64[i]) >> shift)
-                                     : (keys[i] >> (pk.nb + pk.ib + shift));
+            const uint64_t d = dig8 ? dig8[i]
+                                    : (dst64 ? (static_cast<uint64_t>(dst64[i]) >> shift)
+                                             : (keys[i] >> (pk.nb + pk.ib + shift)));
             atomicAdd(&h[d & mask], 1u);
         }
     }
@@ -406,7 +408,8 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter64(
     const uint64_t *__restrict__ in, const float *__restrict__ in_w, uint64_t *__restrict__ out,
     float *__restrict__ out_w, int64_t *__restrict__ perm, int32_t *__restrict__ col, float *__restrict__ wcsr,
     uint32_t *__restrict__ sorted_key, int64_t E, int shift, int bits, int64_t ntiles,
-    const uint32_t *__restrict__ offsets, int last, Packing pk) {
+    const uint32_t *__restrict__ offsets, int last, Packing pk, uint8_t *__restrict__ next_dig, int next_shift,
+    int next_bits) {
     __shared__ uint32_t wcnt[kWaves][kMaxRadixP];
     __shared__ uint32_t start[kMaxRadixP];
     __shared__ int64_t gbase[kMaxRadixP];
@@ -448,6 +451,8 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter64(
             sorted_key[pos] = static_cast<uint32_t>(e >> koff);
         } else {
             out[pos] = e;
+            // the next pass's digit, one byte: its histogram reads these instead of the 8-byte words
+            if (next_dig) next_dig[pos] = static_cast<uint8_t>((e >> (koff + next_shift)) & ((1u << next_bits) - 1));
         }
     }
     // the weight, if any, as a second staged field
@@ -546,6 +551,7 @@ struct CsrWs {
     uint64_t *pbuf[2];  // packed elements
     float *pw[2];       // packed path: weights
     uint32_t *sorted_key;
+    uint8_t *next_dig;  // packed path: the next pass's digit of every element
     uint32_t *hist;
     uint32_t *hist_scan;
     size_t bytes;
@@ -578,6 +584,7 @@ CsrWs carve_csr(void *base, int64_t E, int64_t N, bool weighted) {
         w.buf[b].w = weighted && n ? c.take<float>(n) : nullptr;
     }
     w.sorted_key = c.take<uint32_t>(E);
+    w.next_dig = c.take<uint8_t>(packed && passes >= 2 ? E : 0);
     w.hist = c.take<uint32_t>(nhist);
     w.hist_scan = c.take<uint32_t>(scan_workspace_elems(nhist));
     w.bytes = c.used + 256;
@@ -666,15 +673,19 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
             const int bits = (pk.nb - shift) < pbpp ? (pk.nb - shift) : pbpp;
             const bool last = p == ppasses - 1;
             const int64_t nhist = ntiles << bits;
-            k_radix_hist64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, pin, E, shift, bits, ntiles, pk,
-                                                             w.hist);
+            k_radix_hist64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, pin,
+                                                                   p == 0 ? nullptr : w.next_dig, E, shift, bits,
+                                                                   ntiles, pk, w.hist);
             PYG_LAUNCH_CHECK();
             PYG_TRY(scan_u32(w.hist, w.hist, nhist, false, w.hist_scan, s));
             uint64_t *pout = last ? nullptr : w.pbuf[p & 1];
             float *pout_w = last ? nullptr : w.pw[p & 1];
+            const int nshift = shift + bits;
+            const int nbits = last ? 0 : ((pk.nb - nshift) < pbpp ? (pk.nb - nshift) : pbpp);
             k_radix_scatter64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, src, edge_weight, pin, pin_w,
                                                                 pout, pout_w, perm, col, weight_csr, w.sorted_key, E,
-                                                                shift, bits, ntiles, w.hist, last ? 1 : 0, pk);
+                                                                shift, bits, ntiles, w.hist, last ? 1 : 0, pk,
+                                                                last ? nullptr : w.next_dig, nshift, nbits);
             PYG_LAUNCH_CHECK();
             pin = pout;
             pin_w = pout_w;
