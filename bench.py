@@ -38,8 +38,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 
-# Byte counters of the CSR propagate call (fp32 gcn-weighted sum on the large
-# power-law graph) from rocprofv3 --pmc runs of this script (FETCH_SIZE, then
+# Byte counters of the step's propagate call (fp32 gcn-weighted sum on the
+# large power-law graph) from rocprofv3 --pmc runs of this script (FETCH_SIZE, then
 # WRITE_SIZE, then TCC_HIT_sum + TCC_MISS_sum; KiB / counts per propagate
 # call, summed over the call's launches), with FETCH_SIZE and WRITE_SIZE on a
 # plain 1024 MiB device copy for scale; see profiles/propagate_c5_counters.md.
@@ -52,7 +52,8 @@ COUNTERS = {
 }
 # everything that decides which kernels a propagate call launches and how
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp",
-                  "paper_1903_02428_amd/csrc/api.hip", "paper_1903_02428_amd/binding.py"]
+                  "paper_1903_02428_amd/csrc/api.hip", "paper_1903_02428_amd/csrc/gcn_norm.hip",
+                  "paper_1903_02428_amd/binding.py"]
 
 
 def source_hash():
@@ -227,6 +228,9 @@ def parse():
                     help="only the bandwidth probes (gather ladder, stream read; one JSON object)")
     ap.add_argument("--warm-detail", action="store_true",
                     help="time the large-graph detail calls back to back instead of after a 1 GiB flush each")
+    ap.add_argument("--blocks", type=int, default=2,
+                    help="source blocks of the step's propagate (pyg_csr_blocks_build + pyg_gcn_propagate_blocked); "
+                         "0 = the unblocked CSR propagate (pyg_gcn_propagate)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for scaling rocprofv3 byte counters)")
     return ap.parse_args()
@@ -364,6 +368,16 @@ def main():
         return
 
     ws_gcn = torch.empty(pyg.gcn_propagate_workspace_bytes(x, csr), dtype=torch.uint8, device=dev)
+    B = args.blocks
+    if B:
+        # the source-blocked CSR (virtual row b*N + i: the slots of target i
+        # whose source lies in block b), built straight from the COO every step
+        bcsr = pyg.CSRBlocks(torch.empty(B * N + 1, dtype=torch.int64, device=dev),
+                             torch.empty(E, dtype=torch.int32, device=dev), None, None, N, E, B, args.chunk)
+        ws_blk = torch.empty(pyg.coo_to_csr_blocked_workspace_bytes(E, N, B), dtype=torch.uint8, device=dev)
+        ws_gcnb = torch.empty(pyg.gcn_propagate_blocked_workspace_bytes(x, bcsr), dtype=torch.uint8, device=dev)
+        # the plain CSR of the detail calls, built once
+        pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
     names = ["coo_to_csr", "degree", "gcn_norm+propagate", "global_pool"]
     ev = {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for n in names}
     times = {n: [] for n in names}
@@ -372,17 +386,32 @@ def main():
         def mark(n, i):
             if record:
                 ev[n][i].record()
-        mark("coo_to_csr", 0)
-        pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
-        mark("coo_to_csr", 1)
-        mark("degree", 0)  # the in-degree, read off the row boundaries the sort produced
-        pyg.degree_csr(csr, out=deg)
-        mark("degree", 1)
-        # gcn_norm formed inside the propagate (pyg_gcn_propagate): the norms are
-        # written to `norm` (CSR slot order) and summed with the gathered rows
-        mark("gcn_norm+propagate", 0)
-        pyg.gcn_propagate(x, csr, norm_out=norm, out=out, workspace=ws_gcn)
-        mark("gcn_norm+propagate", 1)
+        if B:
+            mark("coo_to_csr", 0)  # stable sort by (source block, target, edge id)
+            pyg.coo_to_csr_blocked(ei, N, B, None, chunk=args.chunk, out=bcsr, workspace=ws_blk)
+            mark("coo_to_csr", 1)
+            mark("degree", 0)  # the in-degree, read off the virtual rows' boundaries
+            pyg.degree_csr_blocks(bcsr, out=deg)
+            mark("degree", 1)
+            # gcn_norm formed inside the propagate (pyg_gcn_propagate_blocked): d
+            # from the blocked CSR, the norms written to `norm` (blocked slot
+            # order) and summed with the gathered rows, one source block after
+            # another
+            mark("gcn_norm+propagate", 0)
+            pyg.gcn_propagate_blocked(x, None, bcsr, norm_out=norm, out=out, workspace=ws_gcnb)
+            mark("gcn_norm+propagate", 1)
+        else:
+            mark("coo_to_csr", 0)
+            pyg.coo_to_csr(ei, N, None, chunk=args.chunk, out=csr, workspace=ws_csr)
+            mark("coo_to_csr", 1)
+            mark("degree", 0)  # the in-degree, read off the row boundaries the sort produced
+            pyg.degree_csr(csr, out=deg)
+            mark("degree", 1)
+            # gcn_norm formed inside the propagate (pyg_gcn_propagate): the norms are
+            # written to `norm` (CSR slot order) and summed with the gathered rows
+            mark("gcn_norm+propagate", 0)
+            pyg.gcn_propagate(x, csr, norm_out=norm, out=out, workspace=ws_gcn)
+            mark("gcn_norm+propagate", 1)
         mark("global_pool", 0)
         pyg.global_pool(out, batch, 1, "mean", out=pooled, workspace=ws_pool)
         mark("global_pool", 1)
@@ -418,6 +447,9 @@ def main():
     # formed (rowptr, dinv per node and per slot) and written, the output
     balg = b_alg_csr(N, E, F, 4, weighted=False) + 8 * N + 8 * E + 4 * E
     buniq = b_uniq_csr(N, E, F, 4, weighted=False) + 8 * N + 4 * E
+    if B:  # B row pointers per target, and the fp32 partial rows written and folded
+        balg += 8 * (B - 1) * N + 2 * B * N * F * 4
+        buniq += 8 * (B - 1) * N
     value = E * F / (ms_per_step * 1e-3)
     ladder = probe_ladder(probe, torch, dev, N * F * 4)
     log("probe ladder done")
@@ -438,9 +470,15 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "large power-law graph (Chung-Lu gamma=2.1), gcn_norm-weighted sum, CSR segment kernel",
+        "config": {"workload": "large power-law graph (Chung-Lu gamma=2.1), gcn_norm-weighted sum, CSR segment kernel"
+                               + (f" over {B} source blocks" if B else ""),
                    "N": N, "E": E, "F": F, "seed": args.seed, "chunk": args.chunk or "default",
-                   "step": "coo_to_csr+degree(csr row bounds)+[gcn_norm(csr order) formed and written inside the "
+                   "source_blocks": B or None,
+                   "step": ("coo_to_csr_blocked(B=%d: stable sort by source block, target, edge id)+degree(blocked "
+                            "row bounds)+[gcn_norm formed and written inside the propagate (sum, blocked csr, "
+                            "partials folded)]+global_pool(mean)" % B)
+                           if B else
+                           "coo_to_csr+degree(csr row bounds)+[gcn_norm(csr order) formed and written inside the "
                            "propagate (sum, csr)]+global_pool(mean)"},
         "roofline": {"bound": "fabric", "achieved": achieved, "peak": peak, "unit": "GB/s",
                      "frac": achieved / peak if achieved is not None else None, "traffic": traffic,
@@ -450,7 +488,10 @@ def main():
                      "achieved_source": "bytes past L2 per call (FETCH_SIZE + WRITE_SIZE counters, copy-calibrated) "
                                         "/ the call's event time in the timed steps",
                      "l2_hit": measured_l2_hit(),
-                     "kernel": "pyg_gcn_propagate, fp32: k_segment over feature window 0 forming and writing the "
+                     "kernel": ("pyg_gcn_propagate_blocked, fp32, B=%d: k_segment over feature window 0 forming "
+                                "and writing the gcn norms, k_segment over windows 1-3 reading them (virtual rows "
+                                "b*N+i, fp32 partial rows), k_segment_fixup, k_block_fold" % B) if B else
+                               "pyg_gcn_propagate, fp32: k_segment over feature window 0 forming and writing the "
                                "gcn norms, k_segment over windows 1-3 reading them, k_segment_fixup",
                      "unit_of_work": "one gcn_norm+propagate call over the whole graph",
                      "avg_call_ms": t_prop * 1e3,
@@ -458,7 +499,9 @@ def main():
                                      "frac_of_hbm": balg / t_prop / 1e9 / HBM_PEAK_GBS,
                                      "convention": "every edge gathers its source row and its source's d^-1/2 once "
                                                    "(cache reuse counted as traffic), plus rowptr, columns, d^-1/2 "
-                                                   "per node, the norms written and one output write"},
+                                                   "per node, the norms written and one output write"
+                                                   + (", and the fp32 partial rows written and read by the fold"
+                                                      if B else "")},
                      "compulsory": {"bytes_per_call": buniq, "GBps": buniq / t_prop / 1e9,
                                     "frac_of_hbm": buniq / t_prop / 1e9 / HBM_PEAK_GBS,
                                     "convention": "every distinct byte once: rowptr, columns, d^-1/2, x, norms "
@@ -473,7 +516,13 @@ def main():
                    # the same two rows as separate calls (gcn_norm pass, then the weighted propagate)
                    "gcn_norm_csr_ms": cold(torch, lambda: pyg.gcn_norm_csr(csr, out=norm, workspace=ws_norm)),
                    "propagate_weighted_ms": cold(torch, lambda: pyg.propagate(x, csr=csr_w, aggr="sum", out=out,
-                                                                              workspace=ws_prop))},
+                                                                              workspace=ws_prop)),
+                   # the step's calls without source blocks: the plain CSR build and
+                   # pyg_gcn_propagate over it
+                   "coo_to_csr_unblocked_ms": cold(torch, lambda: pyg.coo_to_csr(ei, N, None, chunk=args.chunk,
+                                                                                 out=csr, workspace=ws_csr)),
+                   "gcn_propagate_unblocked_ms": cold(torch, lambda: pyg.gcn_propagate(x, csr, norm_out=norm, out=out,
+                                                                                       workspace=ws_gcn))},
     }
 
     if not args.no_detail:

@@ -110,7 +110,7 @@ typedef struct {
  *   col    [E]        source node of each slot;
  *   perm   [E]        COO edge id of each slot, or NULL (needed for max);
  *   weight [E]        edge weight in this slot order, or NULL;
- *   B                 2 or 4 (blocks shared by 4 or 2 XCDs), or 8, 16, 24 or 32 (one to four blocks per XCD);
+ *   B                 2 .. 32;
  *   chunk             slots per work unit of the propagate, 0 = default. */
 typedef struct {
     const int64_t *rowptr;
@@ -273,12 +273,13 @@ int pyg_csr_blocks_workspace(int64_t N, int64_t E, int64_t B, size_t *bytes);
 
 /* Regroups the slots of a CSR (pyg_coo_to_csr) by source block, for
  * pyg_propagate_blocked: the preprocessing of the same row-ordered layout
- * Appendix A builds once per graph, cut by source as well so that a
- * propagate reads an eighth of x per XCD. Stable: inside a virtual row the
+ * Appendix A builds once per graph, cut by source as well so that the
+ * propagate's wavefronts in flight gather from one source block (a 1/B part
+ * of x) at a time. Stable: inside a virtual row the
  * slots keep the CSR's order (ascending edge id), so the result is unique.
  *   csr     input CSR (rowptr, col; perm when perm is wanted, weight when
  *           weight is wanted);
- *   B       source blocks: 2, 4, 8, 16, 24 or 32;
+ *   B       source blocks, 2 .. 32;
  *   rowptr  int64 [B*N + 1] output;  col  int32 [E] output;
  *   perm    int64 [E] output or NULL (COO edge id of every slot);
  *   weight  fp32 [E] output or NULL (csr->weight in the new slot order).
@@ -288,6 +289,35 @@ int pyg_csr_blocks_workspace(int64_t N, int64_t E, int64_t B, size_t *bytes);
 int pyg_csr_blocks_build(const pyg_csr *csr, int64_t B, int64_t *rowptr, int32_t *col, int64_t *perm,
                          float *weight, void *ws, size_t ws_bytes, void *stream);
 
+/* Workspace bytes needed by pyg_coo_to_csr_blocked. */
+int pyg_coo_to_csr_blocked_workspace(int64_t E, int64_t N, int64_t B, size_t *bytes);
+
+/* The source-blocked CSR straight from the COO (the same arrays as
+ * pyg_csr_blocks_build(pyg_coo_to_csr(...)), bit for bit, in one sort):
+ * the stable radix sort of pyg_coo_to_csr keyed by the virtual row
+ * (source / ceil(N / B)) * N + target instead of the target, so that slots
+ * are ordered by source block, then target, then edge id. The
+ * preprocessing of Appendix A's row-ordered layout in the form that the
+ * blocked propagate reads; with B * N below 2^31.
+ *   edge_index, E, N, edge_weight  as pyg_coo_to_csr;
+ *   B       source blocks, 2 .. 32;
+ *   rowptr  int64 [B*N + 1] output; col int32 [E] output;
+ *   perm    int64 [E] output or NULL (the COO edge id of every slot; needed
+ *           by max);
+ *   weight_csr fp32 [E] output or NULL (edge_weight in the blocked order).
+ * Errors: PYG_ERR_INVALID_ARG (negative sizes, a bad B, NULL rowptr, NULL
+ * edge_index/col or N = 0 when E > 0), PYG_ERR_UNSUPPORTED (N, E or B*N >=
+ * 2^31), PYG_ERR_WORKSPACE. */
+int pyg_coo_to_csr_blocked(const int64_t *edge_index, int64_t E, int64_t N, int64_t B, const float *edge_weight,
+                           int64_t *rowptr, int32_t *col, int64_t *perm, float *weight_csr, void *ws,
+                           size_t ws_bytes, void *stream);
+
+/* In-degree from a source-blocked CSR: deg[i] = the slots of target i over
+ * all blocks (bit-exact; equal to pyg_degree).
+ *   deg int64 [N] output. Errors: PYG_ERR_INVALID_ARG (NULL bcsr/rowptr/deg,
+ * a bad B). */
+int pyg_degree_csr_blocks(const pyg_csr_blocks *bcsr, int64_t *deg, void *stream);
+
 /* Workspace bytes needed by pyg_propagate_blocked (chunk as in the blocked
  * CSR). Holds B fp32 partial rows per target (B*N*F*4 bytes, plus B*N*F*8
  * for max). */
@@ -295,10 +325,12 @@ int pyg_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t E, 
                                     size_t *bytes);
 
 /* Propagate (Eq. (1) of Section 2, the same results as pyg_propagate with
- * the CSR kernel) over a source-blocked CSR: every XCD reduces the virtual
- * rows of its own source blocks (its L2 holds the rows of x it gathers, one
- * 128-byte feature window at a time) into fp32 partial rows, which are then
- * folded in block order. Sum and mean differ from pyg_propagate only in the
+ * the CSR kernel) over a source-blocked CSR: the virtual rows are reduced
+ * into fp32 partial rows one 128-byte feature window at a time, block after
+ * block inside a window (so the rows of x gathered at any moment are one
+ * window of one source block, which the L2s hold far better than a window
+ * of all of x), and the partials of each target are then folded in block
+ * order. Sum and mean differ from pyg_propagate only in the
  * order of the additions (deterministic, the same tolerance); max and argmax
  * are the same bits (ties to the lowest edge id across blocks too).
  *   x    [N,F] fp32 or bf16 with 16-byte rows (F * sizeof(dtype) % 16 == 0)
@@ -311,6 +343,36 @@ int pyg_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t E, 
  * 16-byte vectors or a bad B. */
 int pyg_propagate_blocked(const void *x, int dtype, int64_t N, int64_t F, const pyg_csr_blocks *bcsr, int msg,
                           int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by pyg_gcn_propagate_blocked (chunk as in the
+ * blocked CSR): d^-1/2, the norms when norm_out is NULL, and the blocked
+ * propagate's partial rows. */
+int pyg_gcn_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t B, int64_t chunk,
+                                        size_t *bytes);
+
+/* pyg_gcn_propagate over a source-blocked CSR (the GCN operator of Section
+ * 2 with the normalisation fused in, on the blocked schedule of
+ * pyg_propagate_blocked):
+ *   out[i] = sum over the edges (j -> i) of norm * x[j],
+ *   norm = d_j^-1/2 * w * d_i^-1/2, d from `csr` exactly as
+ * pyg_gcn_norm_csr takes it (row lengths, or csr->weight summed in fp64 in
+ * CSR slot order) when csr is given, else from bcsr (the row lengths summed
+ * over the blocks, or the weights summed in fp64 in blocked slot order),
+ * formed in fp64 and rounded once per slot.
+ *   csr       the graph's CSR (pyg_coo_to_csr), for d, or NULL;
+ *   bcsr      pyg_csr_blocks_build(csr, ...) or pyg_coo_to_csr_blocked,
+ *             weighted iff csr is weighted;
+ *   norm_out  fp32 [E] in bcsr's slot order, or NULL: every norm, equal bit
+ *             for bit to pyg_gcn_norm_csr's norm of the same edge (with
+ *             weights and csr NULL: up to the order of the fp64 degree sum);
+ *   x, out    as pyg_propagate_blocked (16-byte rows; out overwritten).
+ * Sum differs from pyg_gcn_propagate only in the order of the additions
+ * (deterministic). Errors: PYG_ERR_INVALID_ARG (bad dtype, NULL bcsr,
+ * mismatched csr/bcsr, NULL x/out, overlapping arrays), PYG_ERR_UNSUPPORTED
+ * (N or E >= 2^31, rows that are not 16-byte vectors), PYG_ERR_WORKSPACE. */
+int pyg_gcn_propagate_blocked(const void *x, int dtype, int64_t N, int64_t F, const pyg_csr *csr,
+                              const pyg_csr_blocks *bcsr, float *norm_out, void *out, void *ws, size_t ws_bytes,
+                              void *stream);
 
 /* Size of the static scratch array of pyg_propagate_noalloc, per GPU. */
 #define PYG_NOALLOC_SCRATCH_MIB 128

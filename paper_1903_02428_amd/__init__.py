@@ -23,10 +23,13 @@ from .binding import (  # noqa: F401
     PygError,
     abi_version,
     coo_to_csr,
+    coo_to_csr_blocked,
+    coo_to_csr_blocked_workspace_bytes,
     csr_blocks,
     csr_transpose_map,
     degree,
     degree_csr,
+    degree_csr_blocks,
     dense_transform,
     gat_scores_backward,
     gat_softmax,
@@ -34,6 +37,8 @@ from .binding import (  # noqa: F401
     gcn_norm,
     gcn_norm_csr,
     gcn_propagate,
+    gcn_propagate_blocked,
+    gcn_propagate_blocked_workspace_bytes,
     gcn_propagate_workspace_bytes,
     global_pool,
     library,

@@ -32,7 +32,8 @@ EXPORTED = [
     "pyg_gat_scores_backward",
     "pyg_global_pool_workspace", "pyg_global_pool", "pyg_validate_coo", "pyg_validate_batch",
     "pyg_propagate_noalloc", "pyg_gcn_propagate_workspace", "pyg_gcn_propagate", "pyg_csr_blocks_workspace", "pyg_csr_blocks_build", "pyg_propagate_blocked_workspace",
-    "pyg_propagate_blocked",
+    "pyg_propagate_blocked", "pyg_gcn_propagate_blocked_workspace", "pyg_gcn_propagate_blocked",
+    "pyg_coo_to_csr_blocked_workspace", "pyg_coo_to_csr_blocked", "pyg_degree_csr_blocks",
 ]
 
 
@@ -95,6 +96,12 @@ def library() -> ctypes.CDLL:
             "pyg_csr_blocks_workspace": [i64, i64, i64, sz],
             "pyg_csr_blocks_build": [ctypes.POINTER(_Csr), i64, p, p, p, p, p, ctypes.c_size_t, p],
             "pyg_propagate_blocked_workspace": [i32, i64, i64, i64, i64, i32, i64, sz],
+            "pyg_gcn_propagate_blocked_workspace": [i32, i64, i64, i64, i64, i64, sz],
+            "pyg_coo_to_csr_blocked_workspace": [i64, i64, i64, sz],
+            "pyg_coo_to_csr_blocked": [p, i64, i64, i64, p, p, p, p, p, p, ctypes.c_size_t, p],
+            "pyg_degree_csr_blocks": [ctypes.POINTER(_CsrBlocks), p, p],
+            "pyg_gcn_propagate_blocked": [p, i32, i64, i64, ctypes.POINTER(_Csr), ctypes.POINTER(_CsrBlocks), p, p, p,
+                                          ctypes.c_size_t, p],
             "pyg_propagate_blocked": [p, i32, i64, i64, ctypes.POINTER(_CsrBlocks), i32, i32, p, p, p, ctypes.c_size_t,
                                       p],
             "pyg_propagate_noalloc": [p, i32, i64, i64, p, i64, p, ctypes.POINTER(_Csr), i32, i32, i32, p, p, p],
@@ -227,7 +234,7 @@ class CSRBlocks:
 
 def csr_blocks(csr: CSR, B: int = 8, with_perm: bool = False, with_weight: bool | None = None,
                out: CSRBlocks | None = None, workspace: torch.Tensor | None = None) -> CSRBlocks:
-    """Regroup a CSR's slots by source block (B = 2, 4, 8, 16, 24 or 32). The
+    """Regroup a CSR's slots by source block (2 <= B <= 32). The
     weights come along when the CSR has them (unless with_weight is False);
     the edge ids (needed for max) when with_perm."""
     lib = library()
@@ -350,6 +357,61 @@ def coo_to_csr(edge_index: torch.Tensor, num_nodes: int, edge_weight: torch.Tens
     return CSR(rowptr, col, perm, wcsr, num_nodes, E, chunk)
 
 
+def coo_to_csr_blocked(edge_index: torch.Tensor, num_nodes: int, B: int, edge_weight: torch.Tensor | None = None,
+                       with_perm: bool = False, chunk: int = 0, out: "CSRBlocks | None" = None,
+                       workspace: torch.Tensor | None = None) -> "CSRBlocks":
+    """The source-blocked CSR straight from the COO (pyg_coo_to_csr_blocked):
+    the same arrays as csr_blocks(coo_to_csr(...), B), in one sort. The edge
+    ids (needed for max) when with_perm; `out` and `workspace` may be passed
+    to reuse device buffers."""
+    lib = library()
+    E = _edge_index(edge_index)
+    dev = edge_index.device
+    if edge_weight is not None:
+        _need_cuda("edge_weight", edge_weight, torch.float32, 1)
+        if edge_weight.shape[0] != E:
+            raise ValueError("edge_weight must be [E]")
+    if out is not None:
+        if out.N != num_nodes or out.E != E or out.B != B or (out.perm is None) == with_perm or \
+                ((out.weight is None) != (edge_weight is None)):
+            raise ValueError("out CSRBlocks has another shape")
+        rowptr, col, perm, wcsr = out.rowptr, out.col, out.perm, out.weight
+    else:
+        rowptr = torch.empty(B * num_nodes + 1, dtype=torch.int64, device=dev)
+        col = torch.empty(E, dtype=torch.int32, device=dev)
+        perm = torch.empty(E, dtype=torch.int64, device=dev) if with_perm else None
+        wcsr = torch.empty(E, dtype=torch.float32, device=dev) if edge_weight is not None else None
+    nbytes = _size(lib.pyg_coo_to_csr_blocked_workspace, E, num_nodes, B)
+    ws = workspace if workspace is not None and workspace.numel() >= nbytes else _workspace(nbytes, dev)
+    _check(lib.pyg_coo_to_csr_blocked(_ptr(edge_index), E, num_nodes, B, _ptr(edge_weight), _ptr(rowptr), _ptr(col),
+                                      _ptr(perm), _ptr(wcsr), _ptr(ws), nbytes, _stream(dev)),
+           "pyg_coo_to_csr_blocked")
+    if out is not None:
+        out.chunk = chunk
+        return out
+    return CSRBlocks(rowptr, col, perm, wcsr, num_nodes, E, B, chunk)
+
+
+def coo_to_csr_blocked_workspace_bytes(E: int, num_nodes: int, B: int) -> int:
+    return _size(library().pyg_coo_to_csr_blocked_workspace, E, num_nodes, B)
+
+
+def degree_csr_blocks(bcsr: "CSRBlocks", out: torch.Tensor | None = None) -> torch.Tensor:
+    """In-degree from a source-blocked CSR (the slots of each target over all
+    blocks; the same counts as degree())."""
+    lib = library()
+    dev = bcsr.rowptr.device
+    if out is None:
+        out = torch.empty(bcsr.N, dtype=torch.int64, device=dev)
+    else:
+        _need_cuda("out", out, torch.int64, 1)
+        if out.shape[0] != bcsr.N:
+            raise ValueError("out must be [N]")
+    c = bcsr._c()
+    _check(lib.pyg_degree_csr_blocks(ctypes.byref(c), _ptr(out), _stream(dev)), "pyg_degree_csr_blocks")
+    return out
+
+
 def gather_edges(perm: torch.Tensor, values: torch.Tensor) -> torch.Tensor:
     """values[perm] for a COO-ordered fp32 edge array (CSR slot order out)."""
     _need_cuda("perm", perm, torch.int64, 1)
@@ -425,6 +487,40 @@ def gcn_propagate(x: torch.Tensor, csr: CSR, norm_out: torch.Tensor | None = Non
 
 def gcn_propagate_workspace_bytes(x: torch.Tensor, csr: CSR) -> int:
     return _size(library().pyg_gcn_propagate_workspace, DTYPE[x.dtype], x.shape[0], x.shape[1], csr.E, csr.chunk)
+
+
+def gcn_propagate_blocked(x: torch.Tensor, csr: CSR | None, bcsr: CSRBlocks, norm_out: torch.Tensor | None = None,
+                          out: torch.Tensor | None = None, workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """gcn_propagate over a source-blocked CSR (pyg_gcn_propagate_blocked):
+    d from `csr` when given, else from bcsr; the propagate over `bcsr`; the
+    norms go to norm_out in bcsr's slot order when given."""
+    lib = library()
+    _need_cuda("x", x, None, 2)
+    if x.dtype not in DTYPE:
+        raise ValueError("x must be float32 or bfloat16")
+    N, F = x.shape
+    if bcsr.N != N or (csr is not None and (csr.N != N or csr.E != bcsr.E)):
+        raise ValueError("csr / bcsr do not match x")
+    if norm_out is not None:
+        _need_cuda("norm_out", norm_out, torch.float32, 1)
+        if norm_out.shape[0] != bcsr.E:
+            raise ValueError("norm_out must be [E]")
+    if out is None:
+        out = torch.empty_like(x)
+    nbytes = gcn_propagate_blocked_workspace_bytes(x, bcsr)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = _workspace(nbytes, x.device)
+    c, b = (csr._c() if csr is not None else None), bcsr._c()
+    _check(lib.pyg_gcn_propagate_blocked(_ptr(x), DTYPE[x.dtype], N, F, ctypes.byref(c) if c is not None else None,
+                                         ctypes.byref(b),
+                                         _ptr(norm_out), _ptr(out), _ptr(workspace), workspace.numel(),
+                                         _stream(x.device)), "pyg_gcn_propagate_blocked")
+    return out
+
+
+def gcn_propagate_blocked_workspace_bytes(x: torch.Tensor, bcsr: CSRBlocks) -> int:
+    return _size(library().pyg_gcn_propagate_blocked_workspace, DTYPE[x.dtype], x.shape[0], x.shape[1], bcsr.E,
+                 bcsr.B, bcsr.chunk)
 
 
 def propagate_workspace_bytes(x: torch.Tensor, E: int, aggr: str, kernel: str, chunk: int = 0) -> int:

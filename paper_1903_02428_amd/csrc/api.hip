@@ -129,7 +129,7 @@ extern "C" int pyg_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, 
                                                int64_t chunk, size_t *bytes) {
     if (!bytes || !valid_dtype(dtype) || !valid_aggr(aggr) || N < 0 || F < 0 || E < 0 || chunk < 0)
         return PYG_ERR_INVALID_ARG;
-    if (!(B == 2 || B == 4 || (B >= 8 && B % 8 == 0 && B <= 32))) return PYG_ERR_INVALID_ARG;
+    if (B < 2 || B > 32) return PYG_ERR_INVALID_ARG;
     if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
     *bytes = segment_blocked_workspace(E, N, F, B, aggr, chunk);
     return PYG_OK;
@@ -142,7 +142,7 @@ extern "C" int pyg_propagate_blocked(const void *x, int dtype, int64_t N, int64_
     if (msg != PYG_MSG_SRC && msg != PYG_MSG_DIFF) return PYG_ERR_INVALID_ARG;
     const int64_t E = bcsr->E, B = bcsr->B;
     if (bcsr->N != N || E < 0 || !bcsr->rowptr || bcsr->chunk < 0) return PYG_ERR_INVALID_ARG;
-    if (!(B == 2 || B == 4 || (B >= 8 && B % 8 == 0 && B <= 32))) return PYG_ERR_INVALID_ARG;
+    if (B < 2 || B > 32) return PYG_ERR_INVALID_ARG;
     if (N >= kMax32 || E >= kMax32) return PYG_ERR_UNSUPPORTED;
     if ((aggr == PYG_MAX) != (argmax != nullptr) && N * F > 0) return PYG_ERR_INVALID_ARG;
     if (aggr != PYG_MAX && argmax) return PYG_ERR_INVALID_ARG;

@@ -96,7 +96,7 @@ BlocksWs carve_blocks(void *base, int64_t N, int64_t B) {
 using namespace pyg;
 
 extern "C" int pyg_csr_blocks_workspace(int64_t N, int64_t E, int64_t B, size_t *bytes) {
-    if (!bytes || N < 0 || E < 0 || !(B == 2 || B == 4 || (B >= 8 && B % 8 == 0 && B <= 32)))
+    if (!bytes || N < 0 || E < 0 || B < 2 || B > 32)
         return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     *bytes = carve_blocks(nullptr, N, B).bytes;

@@ -153,6 +153,22 @@ int count_targets(const int64_t *dst, int64_t E, int64_t N, Out *out, void *ws, 
 
 // ------------------------------------------------------------- radix sort
 
+// The sort key of an edge: its target, or for a source-blocked CSR
+// (bsize > 0) the virtual row (source / bsize) * N + target, so that the
+// sorted order is by source block, then target, then edge id.
+struct SortKey {
+    int64_t bsize;  // 0: plain CSR
+    int64_t N;
+};
+
+__device__ __forceinline__ uint32_t first_key(const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64,
+                                              int64_t i, SortKey sk) {
+    const uint32_t t = static_cast<uint32_t>(dst64[i]);
+    if (sk.bsize == 0) return t;
+    const uint32_t b = static_cast<uint32_t>(src64[i]) / static_cast<uint32_t>(sk.bsize);
+    return b * static_cast<uint32_t>(sk.N) + t;
+}
+
 struct Payload {  // one sort buffer: key plus carried fields
     uint32_t *key;
     uint32_t *id;
@@ -160,7 +176,8 @@ struct Payload {  // one sort buffer: key plus carried fields
     float *w;
 };
 
-__global__ __launch_bounds__(kSortBlock) void k_radix_hist(const int64_t *__restrict__ dst64, const uint32_t *__restrict__ keys,
+__global__ __launch_bounds__(kSortBlock) void k_radix_hist(const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64,
+                                                       const uint32_t *__restrict__ keys, SortKey sk,
                                                        int64_t E, int shift, int bits, int64_t ntiles,
                                                        uint32_t *__restrict__ hist) {
     __shared__ uint32_t h[kMaxRadix];
@@ -174,7 +191,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const int64_t *__rest
     for (int r = 0; r < kItems; ++r) {
         const int64_t i = base + (int64_t)r * kSortBlock;
         if (i < E) {
-            const uint32_t key = dst64 ? static_cast<uint32_t>(dst64[i]) : keys[i];
+            const uint32_t key = dst64 ? first_key(dst64, src64, i, sk) : keys[i];
             atomicAdd(&h[(key >> shift) & mask], 1u);
         }
     }
@@ -273,7 +290,7 @@ __device__ __forceinline__ void rank_tile(const uint32_t (&dig)[kItems], uint32_
 __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64, const float *__restrict__ w_in,
     Payload in, Payload out, int64_t *__restrict__ perm, int32_t *__restrict__ col, float *__restrict__ wcsr,
-    int64_t E, int shift, int bits, int64_t ntiles, const uint32_t *__restrict__ offsets, int last) {
+    int64_t E, int shift, int bits, int64_t ntiles, const uint32_t *__restrict__ offsets, int last, SortKey sk) {
     __shared__ uint32_t wcnt[kWaves][kMaxRadix];  // per-wave running counts, then per-wave prefixes
     __shared__ uint32_t start[kMaxRadix];         // first staged slot of each digit in the tile
     __shared__ int64_t gbase[kMaxRadix];          // global slot of staged slot 0 of each digit run
@@ -292,7 +309,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
 #pragma unroll
     for (int r = 0; r < kItems; ++r) {
         const int64_t i = ebase + r * kWave;
-        key[r] = (i < E) ? (dst64 ? static_cast<uint32_t>(dst64[i]) : in.key[i]) : 0u;
+        key[r] = (i < E) ? (dst64 ? first_key(dst64, src64, i, sk) : in.key[i]) : 0u;
         dig[r] = (i < E) ? (key[r] >> shift) & mask : 0xFFFFFFFFu;
     }
     rank_tile<kMaxRadix>(dig, slot, wcnt, start, gbase, offsets, ntiles, tile, bits);
@@ -336,7 +353,9 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
             if (pos < 0 || pos >= E) continue;
             const uint32_t x = stage[j];
             if (last) {
-                if (fld == 1) perm[pos] = x;
+                if (fld == 1) {
+                    if (perm) perm[pos] = x;
+                }
                 else if (fld == 2) col[pos] = static_cast<int32_t>(x);
                 else if (wcsr) wcsr[pos] = __uint_as_float(x);
             } else {
@@ -349,8 +368,8 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
 }
 
 // ------------------------------------------------------------ packed sort
-// When 2 nb + ib <= 64 (nb bits of a node id, ib bits of an edge id), an
-// element travels as one 64-bit word  target << (nb + ib) | source << ib | id:
+// When kb + nb + ib <= 64 (kb bits of the sort key, nb of a node id, ib of an
+// edge id), an element travels as one 64-bit word  key << (nb + ib) | source << ib | id:
 // 8 bytes per element and pass instead of 12 (the large power-law graph:
 // 3.63 -> 3.00 ms). Digits stay at most 7 bits (three 6-bit passes for 18-bit
 // ids): two 9-bit passes measured slower (3.71 ms), their 8-element runs per
@@ -362,19 +381,22 @@ constexpr int kMaxDigitBitsP = PYG_RADIX_BITS_PACKED;
 constexpr int kMaxRadixP = 1 << kMaxDigitBitsP;
 
 struct Packing {
+    int kb;  // bits of the sort key (the target, or the virtual row of a blocked CSR)
     int nb;  // bits of a node id
     int ib;  // bits of an edge id
+    SortKey sk;
 };
 
 __device__ __forceinline__ uint64_t pack_edge(const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64,
                                               int64_t i, Packing pk) {
-    return (static_cast<uint64_t>(dst64[i]) << (pk.nb + pk.ib)) | (static_cast<uint64_t>(src64[i]) << pk.ib) |
-           static_cast<uint64_t>(i);
+    return (static_cast<uint64_t>(first_key(dst64, src64, i, pk.sk)) << (pk.nb + pk.ib)) |
+           (static_cast<uint64_t>(src64[i]) << pk.ib) | static_cast<uint64_t>(i);
 }
 
 // Digit counts per tile (digit-major) of the packed elements; pass 0 packs
 // from the COO itself.
 __global__ __launch_bounds__(kSortBlock) void k_radix_hist64(const int64_t *__restrict__ dst64,
+                                                         const int64_t *__restrict__ src64,
                                                          const uint64_t *__restrict__ keys,
                                                          const uint8_t *__restrict__ dig8, int64_t E, int shift,
                                                          int bits, int64_t ntiles, Packing pk,
@@ -391,7 +413,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist64(const int64_t *__re
         const int64_t i = base + (int64_t)r * kSortBlock;
         if (i < E) {
             const uint64_t d = dig8 ? dig8[i]
-                                    : (dst64 ? (static_cast<uint64_t>(dst64[i]) >> shift)
+                                    : (dst64 ? (static_cast<uint64_t>(first_key(dst64, src64, i, pk.sk)) >> shift)
                                              : (keys[i] >> (pk.nb + pk.ib + shift)));
             atomicAdd(&h[d & mask], 1u);
         }
@@ -446,7 +468,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter64(
         if (pos < 0 || pos >= E) continue;  // bounds hold for a consistent ranking
         const uint64_t e = stage[j];
         if (last) {
-            perm[pos] = static_cast<int64_t>(e & idmask);
+            if (perm) perm[pos] = static_cast<int64_t>(e & idmask);
             col[pos] = static_cast<int32_t>((e >> pk.ib) & nodemask);
             sorted_key[pos] = static_cast<uint32_t>(e >> koff);
         } else {
@@ -482,6 +504,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter64(
 // (key[-1] = -1, key[E] = N; slot E closes the trailing rows, rowptr[N] = E).
 // Each thread owns 8 consecutive slots, read as two 16-byte loads.
 __global__ void k_row_bounds(const uint32_t *__restrict__ key, int64_t E, int64_t N, int64_t *__restrict__ rowptr) {
+    // N: the number of rows (target ids, or virtual rows of a blocked CSR)
     constexpr int S = 8;  // slots per thread: two 16-byte loads
     const int64_t p0 = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) * S;
     if (p0 > E) return;
@@ -525,25 +548,38 @@ __global__ void k_validate_batch(const int64_t *__restrict__ b, int64_t N, int64
     if (local) atomicAdd(bad, local);
 }
 
-// Digit plan: total key bits, passes, bits per pass (at least one pass).
-void digit_plan(int64_t N, int *nb, int *passes, int *bpp) {
+// Digit plan for keys in [0, nkeys): total key bits, passes, bits per pass
+// (at least one pass).
+void digit_plan(int64_t nkeys, int *nb, int *passes, int *bpp) {
     int b = 1;
-    while (b < 31 && (int64_t(1) << b) < N) ++b;
+    while (b < 31 && (int64_t(1) << b) < nkeys) ++b;
     *nb = b;
     *passes = (b + kMaxDigitBits - 1) / kMaxDigitBits;
     *bpp = (b + *passes - 1) / *passes;
 }
 
-// Packed layout when a node id, a node id and an edge id fit 64 bits.
-bool packed_plan(int64_t E, int64_t N, Packing *pk, int *passes, int *bpp) {
-    int nb = 1, ib = 1;
+// Source blocks: B blocks of ceil(N / B) consecutive source ids (B = 1: the
+// plain CSR, keyed by target alone).
+SortKey sort_key(int64_t N, int64_t B) {
+    SortKey sk{};
+    sk.bsize = B > 1 ? (N + B - 1) / B : 0;
+    sk.N = N;
+    return sk;
+}
+
+// Packed layout when a sort key, a node id and an edge id fit 64 bits.
+bool packed_plan(int64_t E, int64_t N, int64_t B, Packing *pk, int *passes, int *bpp) {
+    int kb = 1, nb = 1, ib = 1;
+    while (kb < 31 && (int64_t(1) << kb) < B * N) ++kb;
     while (nb < 31 && (int64_t(1) << nb) < N) ++nb;
     while (ib < 62 && (int64_t(1) << ib) < E) ++ib;
+    pk->kb = kb;
     pk->nb = nb;
     pk->ib = ib;
-    *passes = (nb + kMaxDigitBitsP - 1) / kMaxDigitBitsP;
-    *bpp = (nb + *passes - 1) / *passes;
-    return 2 * nb + ib <= 64;
+    pk->sk = sort_key(N, B);
+    *passes = (kb + kMaxDigitBitsP - 1) / kMaxDigitBitsP;
+    *bpp = (kb + *passes - 1) / *passes;
+    return kb + nb + ib <= 64;
 }
 
 struct CsrWs {
@@ -557,12 +593,12 @@ struct CsrWs {
     size_t bytes;
 };
 
-CsrWs carve_csr(void *base, int64_t E, int64_t N, bool weighted) {
+CsrWs carve_csr(void *base, int64_t E, int64_t N, int64_t B, bool weighted) {
     int nb, passes, bpp;
-    digit_plan(N, &nb, &passes, &bpp);
+    digit_plan(B * N, &nb, &passes, &bpp);
     Packing pk;
     int ppasses, pbpp;
-    const bool packed = packed_plan(E, N, &pk, &ppasses, &pbpp);
+    const bool packed = packed_plan(E, N, B, &pk, &ppasses, &pbpp);
     if (packed) {
         passes = ppasses;
         bpp = pbpp;
@@ -644,36 +680,38 @@ extern "C" int pyg_degree_csr(const pyg_csr *csr, int64_t *deg, void *stream) {
 extern "C" int pyg_coo_to_csr_workspace(int64_t E, int64_t N, size_t *bytes) {
     if (E < 0 || N < 0 || !bytes) return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
-    *bytes = carve_csr(nullptr, E, N, true).bytes;
+    *bytes = carve_csr(nullptr, E, N, 1, true).bytes;
     return PYG_OK;
 }
 
-extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, const float *edge_weight,
-                              int64_t *rowptr, int32_t *col, int64_t *perm, float *weight_csr,
-                              void *ws, size_t ws_bytes, void *stream) {
-    if (E < 0 || N < 0 || !rowptr) return PYG_ERR_INVALID_ARG;
-    if (E > 0 && (!edge_index || !col || !perm || N == 0)) return PYG_ERR_INVALID_ARG;
-    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+namespace {
+
+// The stable sort of the edges by sort key (target, or source block then
+// target), carrying edge id, source and weight; rowptr over the B * N rows
+// from the key changes of the sorted keys.
+int coo_to_csr_impl(const int64_t *edge_index, int64_t E, int64_t N, int64_t B, const float *edge_weight,
+                    int64_t *rowptr, int32_t *col, int64_t *perm, float *weight_csr, void *ws, size_t ws_bytes,
+                    hipStream_t s) {
     if (!edge_weight) weight_csr = nullptr;
-    const CsrWs w = carve_csr(ws, E, N, edge_weight != nullptr);
+    const CsrWs w = carve_csr(ws, E, N, B, edge_weight != nullptr);
     if (ws_bytes < w.bytes || (w.bytes > 256 && !ws)) return PYG_ERR_WORKSPACE;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    if (E == 0) return fill<int64_t>(rowptr, N + 1, 0, s);
+    const int64_t rows = B * N;
+    if (E == 0) return fill<int64_t>(rowptr, rows + 1, 0, s);
     const int64_t *src = edge_index;
     const int64_t *dst = edge_index + E;
 
     const int64_t ntiles = (E + kTile - 1) / kTile;
     Packing pk;
     int ppasses, pbpp;
-    if (packed_plan(E, N, &pk, &ppasses, &pbpp)) {
+    if (packed_plan(E, N, B, &pk, &ppasses, &pbpp)) {
         const uint64_t *pin = nullptr;
         const float *pin_w = nullptr;
         int shift = 0;
         for (int p = 0; p < ppasses; ++p) {
-            const int bits = (pk.nb - shift) < pbpp ? (pk.nb - shift) : pbpp;
+            const int bits = (pk.kb - shift) < pbpp ? (pk.kb - shift) : pbpp;
             const bool last = p == ppasses - 1;
             const int64_t nhist = ntiles << bits;
-            k_radix_hist64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, pin,
+            k_radix_hist64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, src, pin,
                                                                    p == 0 ? nullptr : w.next_dig, E, shift, bits,
                                                                    ntiles, pk, w.hist);
             PYG_LAUNCH_CHECK();
@@ -681,7 +719,7 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
             uint64_t *pout = last ? nullptr : w.pbuf[p & 1];
             float *pout_w = last ? nullptr : w.pw[p & 1];
             const int nshift = shift + bits;
-            const int nbits = last ? 0 : ((pk.nb - nshift) < pbpp ? (pk.nb - nshift) : pbpp);
+            const int nbits = last ? 0 : ((pk.kb - nshift) < pbpp ? (pk.kb - nshift) : pbpp);
             k_radix_scatter64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, src, edge_weight, pin, pin_w,
                                                                 pout, pout_w, perm, col, weight_csr, w.sorted_key, E,
                                                                 shift, bits, ntiles, w.hist, last ? 1 : 0, pk,
@@ -691,30 +729,81 @@ extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, c
             pin_w = pout_w;
             shift += bits;
         }
-        k_row_bounds<<<grid_for(E + 1, kBlock * 8, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
+        k_row_bounds<<<grid_for(E + 1, kBlock * 8, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, rows, rowptr);
         PYG_LAUNCH_CHECK();
         return PYG_OK;
     }
     int nb, passes, bpp;
-    digit_plan(N, &nb, &passes, &bpp);
+    digit_plan(rows, &nb, &passes, &bpp);
+    const SortKey sk = sort_key(N, B);
     Payload in{}, none{};
     int shift = 0;
     for (int p = 0; p < passes; ++p) {
         const int bits = (nb - shift) < bpp ? (nb - shift) : bpp;
         const bool last = p == passes - 1;
         const int64_t nhist = ntiles << bits;
-        k_radix_hist<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, in.key, E, shift, bits, ntiles, w.hist);
+        k_radix_hist<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, src, in.key, sk, E, shift, bits,
+                                                             ntiles, w.hist);
         PYG_LAUNCH_CHECK();
         PYG_TRY(scan_u32(w.hist, w.hist, nhist, false, w.hist_scan, s));
         Payload out = last ? none : w.buf[p & 1];
         if (last) out.key = w.sorted_key;
         k_radix_scatter<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, src, edge_weight, in, out, perm,
-                                                           col, weight_csr, E, shift, bits, ntiles, w.hist, last ? 1 : 0);
+                                                           col, weight_csr, E, shift, bits, ntiles, w.hist, last ? 1 : 0,
+                                                           sk);
         PYG_LAUNCH_CHECK();
         in = out;
         shift += bits;
     }
-    k_row_bounds<<<grid_for(E + 1, kBlock * 8, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, N, rowptr);
+    k_row_bounds<<<grid_for(E + 1, kBlock * 8, int64_t(1) << 30), kBlock, 0, s>>>(w.sorted_key, E, rows, rowptr);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
+}
+
+// deg[i] = the slots of target i over all source blocks.
+__global__ void k_blocks_degree(const int64_t *__restrict__ rowptr, int64_t N, int64_t B, int64_t *__restrict__ deg) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t d = 0;
+        for (int64_t b = 0; b < B; ++b) d += rowptr[b * N + i + 1] - rowptr[b * N + i];
+        deg[i] = d;
+    }
+}
+
+}  // namespace
+
+extern "C" int pyg_coo_to_csr(const int64_t *edge_index, int64_t E, int64_t N, const float *edge_weight,
+                              int64_t *rowptr, int32_t *col, int64_t *perm, float *weight_csr,
+                              void *ws, size_t ws_bytes, void *stream) {
+    if (E < 0 || N < 0 || !rowptr) return PYG_ERR_INVALID_ARG;
+    if (E > 0 && (!edge_index || !col || !perm || N == 0)) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    return coo_to_csr_impl(edge_index, E, N, 1, edge_weight, rowptr, col, perm, weight_csr, ws, ws_bytes,
+                           static_cast<hipStream_t>(stream));
+}
+
+extern "C" int pyg_coo_to_csr_blocked_workspace(int64_t E, int64_t N, int64_t B, size_t *bytes) {
+    if (E < 0 || N < 0 || !bytes || B < 2 || B > 32) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31) || B * N >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    *bytes = carve_csr(nullptr, E, N, B, true).bytes;
+    return PYG_OK;
+}
+
+extern "C" int pyg_coo_to_csr_blocked(const int64_t *edge_index, int64_t E, int64_t N, int64_t B,
+                                      const float *edge_weight, int64_t *rowptr, int32_t *col, int64_t *perm,
+                                      float *weight_csr, void *ws, size_t ws_bytes, void *stream) {
+    if (E < 0 || N < 0 || !rowptr || B < 2 || B > 32) return PYG_ERR_INVALID_ARG;
+    if (E > 0 && (!edge_index || !col || N == 0)) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31) || B * N >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    return coo_to_csr_impl(edge_index, E, N, B, edge_weight, rowptr, col, perm, weight_csr, ws, ws_bytes,
+                           static_cast<hipStream_t>(stream));
+}
+
+extern "C" int pyg_degree_csr_blocks(const pyg_csr_blocks *bcsr, int64_t *deg, void *stream) {
+    if (!bcsr || !bcsr->rowptr || bcsr->N < 0 || bcsr->B < 2 || bcsr->B > 32 || (bcsr->N > 0 && !deg))
+        return PYG_ERR_INVALID_ARG;
+    if (bcsr->N == 0) return PYG_OK;
+    k_blocks_degree<<<grid_for(bcsr->N, kBlock * 4), kBlock, 0, static_cast<hipStream_t>(stream)>>>(
+        bcsr->rowptr, bcsr->N, bcsr->B, deg);
     PYG_LAUNCH_CHECK();
     return PYG_OK;
 }

@@ -304,3 +304,133 @@ extern "C" int pyg_gcn_propagate(const void *x, int dtype, int64_t N, int64_t F,
     a.norm_out = norm_out ? norm_out : norm_ws;  // the later feature windows read the weights back
     return segment_reduce(a, seg_ws, ws_bytes - (static_cast<char *>(seg_ws) - static_cast<char *>(ws)), s);
 }
+
+// The norms alone over a source-blocked CSR: one wavefront per virtual row
+// b * N + i, d^-1/2 of target i uniform, the same expression per slot.
+__global__ __launch_bounds__(kBlock) void k_blocked_slot_norm(const int64_t *__restrict__ brow,
+                                                              const int32_t *__restrict__ col,
+                                                              const float *__restrict__ w, int64_t N, int64_t B,
+                                                              const double *__restrict__ dinv,
+                                                              float *__restrict__ norm) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t r = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave); r < B * N; r += waves) {
+        const int64_t s = brow[r], t = brow[r + 1];
+        const double di = dinv[r % N];
+        for (int64_t p = s + lane; p < t; p += kWave) {
+            const double wv = w ? static_cast<double>(w[p]) : 1.0;
+            norm[p] = static_cast<float>(dinv[col[p]] * wv * di);
+        }
+    }
+}
+
+// dinv of every target from a source-blocked CSR: the slots of its B virtual
+// rows (unit weights).
+__global__ void k_blocked_dinv_count(const int64_t *__restrict__ brow, int64_t N, int64_t B, double *__restrict__ dinv) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < N; i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t c = 0;
+        for (int64_t b = 0; b < B; ++b) c += brow[b * N + i + 1] - brow[b * N + i];
+        const double d = static_cast<double>(c);
+        dinv[i] = d > 0.0 ? 1.0 / sqrt(d) : 0.0;
+    }
+}
+
+// ... from its weights: one wavefront per target sums in fp64 over the
+// virtual rows in block order (lane-strided partial sums, then an xor
+// butterfly): a fixed order.
+__global__ __launch_bounds__(kBlock) void k_blocked_dinv_weighted(const int64_t *__restrict__ brow,
+                                                                  const float *__restrict__ w, int64_t N, int64_t B,
+                                                                  double *__restrict__ dinv) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t waves = (int64_t)gridDim.x * (kBlock / kWave);
+    for (int64_t i = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave); i < N; i += waves) {
+        double acc = 0.0;
+        for (int64_t b = 0; b < B; ++b) {
+            const int64_t s = brow[b * N + i], t = brow[b * N + i + 1];
+            for (int64_t p = s + lane; p < t; p += kWave) acc += static_cast<double>(w[p]);
+        }
+        for (int off = kWave / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, kWave);
+        if (lane == 0) dinv[i] = acc > 0.0 ? 1.0 / sqrt(acc) : 0.0;
+    }
+}
+
+// The same over a source-blocked CSR: d and d^-1/2 from the graph's CSR when
+// given (its row lengths, or its weights in CSR slot order, exactly as
+// above), else from the blocked CSR itself; the propagate over the blocked
+// virtual rows, the norms written in the blocked slot order.
+extern "C" int pyg_gcn_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t B, int64_t chunk,
+                                                   size_t *bytes) {
+    if (!bytes || (dtype != PYG_F32 && dtype != PYG_BF16) || N < 0 || F < 0 || E < 0 || chunk < 0 || B < 2 || B > 32)
+        return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    *bytes = align_up(static_cast<size_t>(N) * sizeof(double), 256) + align_up(static_cast<size_t>(E) * 4, 256) +
+             segment_blocked_workspace(E, N, F, B, PYG_SUM, chunk);
+    return PYG_OK;
+}
+
+extern "C" int pyg_gcn_propagate_blocked(const void *x, int dtype, int64_t N, int64_t F, const pyg_csr *csr,
+                                         const pyg_csr_blocks *bcsr, float *norm_out, void *out, void *ws,
+                                         size_t ws_bytes, void *stream) {
+    if ((dtype != PYG_F32 && dtype != PYG_BF16) || N < 0 || F < 0 || !bcsr || !bcsr->rowptr || (csr && !csr->rowptr))
+        return PYG_ERR_INVALID_ARG;
+    const int64_t E = bcsr->E, B = bcsr->B;
+    if (bcsr->N != N || E < 0 || bcsr->chunk < 0 || B < 2 || B > 32) return PYG_ERR_INVALID_ARG;
+    if (csr && (csr->N != N || csr->E != E)) return PYG_ERR_INVALID_ARG;
+    if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    if (E > 0 && (!bcsr->col || N == 0)) return PYG_ERR_INVALID_ARG;
+    if (csr && (csr->weight != nullptr) != (bcsr->weight != nullptr) && E > 0) return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && (!x || !out)) return PYG_ERR_INVALID_ARG;
+    const int64_t sz = dtype == PYG_BF16 ? 2 : 4;
+    const int64_t xbytes = N * F * sz;
+    const uintptr_t xa = reinterpret_cast<uintptr_t>(x), oa = reinterpret_cast<uintptr_t>(out),
+                    na = reinterpret_cast<uintptr_t>(norm_out);
+    auto overlap = [](uintptr_t a, int64_t an, uintptr_t b, int64_t bn) {
+        return a && b && an > 0 && bn > 0 && a < b + static_cast<uintptr_t>(bn) && b < a + static_cast<uintptr_t>(an);
+    };
+    if (overlap(xa, xbytes, oa, xbytes) || overlap(na, E * 4, xa, xbytes) || overlap(na, E * 4, oa, xbytes))
+        return PYG_ERR_INVALID_ARG;
+    if (N * F > 0 && ((F * sz) % 16 != 0 || xa % 16 != 0 || oa % 16 != 0)) return PYG_ERR_UNSUPPORTED;
+    size_t need;
+    PYG_TRY(pyg_gcn_propagate_blocked_workspace(dtype, N, F, E, B, bcsr->chunk, &need));
+    if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
+    if (N == 0) return PYG_OK;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    double *dinv = static_cast<double *>(ws);
+    float *norm_ws = reinterpret_cast<float *>(static_cast<char *>(ws) + align_up(static_cast<size_t>(N) * sizeof(double), 256));
+    void *seg_ws = reinterpret_cast<char *>(norm_ws) + align_up(static_cast<size_t>(E) * 4, 256);
+    if (csr && csr->weight)
+        k_row_dinv_weighted<<<grid_for(N, kBlock / kWave, 1 << 16), kBlock, 0, s>>>(csr->rowptr, csr->weight, N, dinv);
+    else if (csr)
+        k_row_dinv_count<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(csr->rowptr, N, dinv);
+    else if (bcsr->weight)
+        k_blocked_dinv_weighted<<<grid_for(N, kBlock / kWave, 1 << 16), kBlock, 0, s>>>(bcsr->rowptr, bcsr->weight, N,
+                                                                                      B, dinv);
+    else
+        k_blocked_dinv_count<<<grid_for(N, kBlock * 4), kBlock, 0, s>>>(bcsr->rowptr, N, B, dinv);
+    PYG_LAUNCH_CHECK();
+    if (F == 0) {  // nothing to propagate: the norms alone, one slot per lane
+        if (!norm_out || E == 0) return PYG_OK;
+        k_blocked_slot_norm<<<grid_for(B * N, kBlock / kWave, 1 << 16), kBlock, 0, s>>>(bcsr->rowptr, bcsr->col,
+                                                                                      bcsr->weight, N, B, dinv, norm_out);
+        PYG_LAUNCH_CHECK();
+        return PYG_OK;
+    }
+    SegmentArgs a{};
+    a.x = x;
+    a.dtype = dtype;
+    a.F = F;
+    a.rowptr = bcsr->rowptr;
+    a.col = bcsr->col;
+    a.weight = bcsr->weight;
+    a.perm = bcsr->perm;
+    a.n_rows = N;
+    a.E = E;
+    a.msg = kSegMsgGcn;
+    a.aggr = PYG_SUM;
+    a.chunk = bcsr->chunk;
+    a.sentinel = E;
+    a.out = out;
+    a.dinv = dinv;
+    a.norm_out = norm_out ? norm_out : norm_ws;  // the later feature windows read the weights back
+    return segment_reduce_blocked(a, B, seg_ws, ws_bytes - (static_cast<char *>(seg_ws) - static_cast<char *>(ws)), s);
+}

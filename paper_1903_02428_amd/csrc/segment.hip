@@ -80,8 +80,8 @@ struct SegParams {
     int32_t *class_hist;       // workspace for the hint pre-pass
     int32_t *hot_slot;
     uint8_t *node_class;       // degree class of every row [n_rows]
-    // source-blocked rows (XCD-affine launch): the rows are `blocks` runs of
-    // `rpb` virtual rows, virtual row r = (source block r / rpb, target r % rpb)
+    // source-blocked rows: the rows are `blocks` runs of `rpb` virtual rows,
+    // virtual row r = (source block r / rpb, target r % rpb)
     int64_t blocks;
     int64_t rpb;
     // GCN messages (kMsgGcn): dinv [n_rows] fp64 (d^-1/2 of every row), the
@@ -236,6 +236,12 @@ constexpr int kMsgGcn = 8;
 // messages whose slot carries a scalar weight (read or formed)
 template <int MSG> constexpr bool kWeightedMsg = MSG == 1 || MSG == 8;
 
+// The target of row r: r itself, or for a source-blocked virtual row the
+// target it belongs to.
+__device__ __forceinline__ int64_t target_row(const SegParams &p, int64_t r) {
+    return p.blocks > 1 ? r % p.rpb : r;
+}
+
 // Edge-feature message of one element (formed in fp32, as compared by max).
 template <int MSG>
 __device__ __forceinline__ float edge_msg(float xv, float ev) {
@@ -277,13 +283,13 @@ __device__ __forceinline__ void reduce_piece(const SegParams &p, int64_t r, int6
     R xi[NS];
     if constexpr (MSG == kMsgDiff || MSG == kMsgEdgeReluGrad) {
         const T *xr = MSG == kMsgDiff ? x : static_cast<const T *>(p.x_self);
-        const int64_t rr = p.blocks > 1 ? r % p.rpb : r;  // the target of a source-blocked virtual row
+        const int64_t rr = target_row(p, r);
 #pragma unroll
         for (int sl = 0; sl < NS; ++sl) xi[sl] = act[sl] ? LN::load(xr + rr * p.F + f0[sl]) : LN::zero();
     }
     // GCN: the row's own d^-1/2
     double dr = 0.0;
-    if constexpr (MSG == kMsgGcn) dr = p.dinv[r];
+    if constexpr (MSG == kMsgGcn) dr = p.dinv[target_row(p, r)];
     // per-head weights: a lane vector never straddles two heads (C is a multiple of its width)
     int64_t hd[NS];
 #pragma unroll
@@ -462,7 +468,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
     const T *__restrict__ x = static_cast<const T *>(p.x);
     const int q = lane & ((1 << p.lg_l) - 1);
     const int64_t fo = (int64_t)q * EP;
-    const bool act = fo < p.fcnt;
+    const bool act = fo < p.fcnt && p.fbase + fo < p.F;  // the last window of a row may be narrower
     const int64_t f0 = p.fbase + fo;
     float acc[EP];
     int32_t pos[EP];
@@ -472,8 +478,9 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
         pos[e] = -1;
     }
     R xi = LN::zero();
-    if constexpr (MSG == kMsgDiff) xi = act ? LN::load(x + r * p.F + f0) : LN::zero();
-    if constexpr (MSG == kMsgEdgeReluGrad) xi = act ? LN::load(static_cast<const T *>(p.x_self) + r * p.F + f0) : LN::zero();
+    const int64_t rr = target_row(p, r);
+    if constexpr (MSG == kMsgDiff) xi = act ? LN::load(x + rr * p.F + f0) : LN::zero();
+    if constexpr (MSG == kMsgEdgeReluGrad) xi = act ? LN::load(static_cast<const T *>(p.x_self) + rr * p.F + f0) : LN::zero();
     const int64_t hd = MSG == kMsgHeads ? f0 / p.C : 0;
     for (int64_t base = s; base < t; base += U) {
         int jj[U];
@@ -488,7 +495,7 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
             if constexpr (MSG == kMsgGcn) {
                 if (ok[u]) {
                     const double wv = p.w ? static_cast<double>(p.w[base + u]) : 1.0;
-                    ww[u] = static_cast<float>(p.dinv[jj[u]] * wv * p.dinv[r]);
+                    ww[u] = static_cast<float>(p.dinv[jj[u]] * wv * p.dinv[rr]);
                     if (p.norm_out && p.fbase == 0 && q == 0) p.norm_out[base + u] = ww[u];
                 } else {
                     ww[u] = 0.f;
@@ -625,7 +632,7 @@ __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c
     p.head_row[c] = head;  // uniform: every lane stores the same value (no lane-0 branch)
 }
 
-template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool LIGHT>
+template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool LIGHT, bool OF32 = false>
 __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
@@ -636,56 +643,7 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
         p.fbase += w * p.fcnt;
     }
     if (c >= p.nchunks) return;
-    segment_chunk_work<T, VEC, NS, U, MSG, MAXA, IDENT, LIGHT, false>(p, c, lane);
-}
-
-// Source-blocked rows, XCD-affine (workgroup w runs on XCD w % 8). With
-// B >= 8 blocks, XCD x reduces the virtual rows of blocks x*S .. x*S+S-1
-// (S = B / 8); with B < 8, the G = 8 / B XCDs x = b*G .. b*G+G-1 share
-// block b. Either way the source rows an XCD gathers are a 1/B part of x
-// (one feature window at a time), a working set that fits its L2 (B = 8) or
-// lets it hold a larger share of the hot rows (B = 2, 4). Persistent,
-// statically scheduled: the items of the XCD's blocks (sub-block-major, then
-// window, then chunk) are dealt to its wavefronts in turn, so the wavefronts
-// in flight work on neighbouring chunks of one window; XCDs that share a
-// block take every G-th item. The loop is wave-uniform (no lane-dependent
-// branch around its back edge, no atomics). Chunks belong to the block in
-// which they start. Partial rows are written in fp32 (OF32) and folded
-// afterwards.
-constexpr int kMaxSubBlocks = 4;  // source blocks per XCD: B in {2, 4, 8, 16, 24, 32}
-template <typename T, int U, int MSG, bool MAXA>
-__global__ __launch_bounds__(kBlock) void k_segment_xcd(SegParams p) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int x = static_cast<int>(blockIdx.x % kXcds);
-    const int G = p.blocks < kXcds ? static_cast<int>(kXcds / p.blocks) : 1;  // XCDs per block
-    const int S = p.blocks < kXcds ? 1 : static_cast<int>(p.blocks / kXcds);  // blocks per XCD
-    const int64_t b0 = p.blocks < kXcds ? x / G : (int64_t)x * S;
-    const int g = x % G;  // rank among the XCDs of the block
-    // first chunk of each of this XCD's sub-blocks, and the end
-    int64_t cb[kMaxSubBlocks + 1];
-#pragma unroll
-    for (int k = 0; k <= kMaxSubBlocks; ++k) {
-        const int64_t b = b0 + (k < S ? k : S);
-        cb[k] = b >= p.blocks ? p.nchunks : (uniform64(p.rowptr[b * p.rpb]) + p.chunk - 1) / p.chunk;
-    }
-    const int64_t items = (cb[S] - cb[0]) * p.nwin;
-    const int64_t waves = uniform64((int64_t)(gridDim.x / kXcds) * (kBlock / kWave));  // gridDim.x % 8 == 0
-    const int64_t first = uniform64((int64_t)(blockIdx.x / kXcds) * (kBlock / kWave) + threadIdx.x / kWave);
-    const int64_t fbase0 = p.fbase;
-    for (int64_t it = first * G + g; it < items; it += waves * G) {
-        int64_t rem = it, c = cb[0], w = 0;
-        for (int k = 0; k < S; ++k) {
-            const int64_t nk = cb[k + 1] - cb[k];
-            if (rem < nk * p.nwin) {
-                w = rem / nk;
-                c = cb[k] + (rem - w * nk);
-                break;
-            }
-            rem -= nk * p.nwin;
-        }
-        p.fbase = fbase0 + w * p.fcnt;
-        segment_chunk_work<T, true, 1, U, MSG, MAXA, false, false, true>(p, c, lane);
-    }
+    segment_chunk_work<T, VEC, NS, U, MSG, MAXA, IDENT, LIGHT, OF32>(p, c, lane);
 }
 
 // Fold the pieces of every long row: one workgroup per chunk that starts a
@@ -1040,32 +998,35 @@ __global__ __launch_bounds__(kBlock) void k_block_fold(const float *__restrict__
     }
 }
 
-// Workgroups of a statically scheduled (persistent) launch: as many as are
-// resident at once (a later workgroup would start its equal share late),
-// a multiple of the 8 XCDs. Queried once per kernel.
-template <typename K>
-unsigned resident_grid(K kernel) {
-    int dev = 0, cus = 0, per_cu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kBlock, 0) != hipSuccess || per_cu < 1 ||
-        cus < kXcds)
-        return kXcds * 32 * 4;  // 256 compute units, 4 workgroups each
-    return static_cast<unsigned>(cus / kXcds * kXcds * per_cu);
-}
+// Source-blocked virtual rows: the ordinary chunked launch over the B * N
+// virtual rows (window-major, and inside a window block-major, since the
+// virtual rows of block b precede those of block b + 1), writing fp32
+// partial rows. At any moment the wavefronts in flight gather from one
+// source block of one feature window, a 1/B part of x's bytes per window.
+constexpr int64_t kMaxBlocks = 32;  // source blocks of a blocked CSR, at most
 
-template <typename T, int MSG>
-int launch_blocked(const SegParams &p, bool maxa, hipStream_t s) {
+template <typename T, int MSG, bool MAXA>
+int launch_blocked(const SegParams &p, bool light, hipStream_t s) {
     constexpr int U = 8;  // gathers in flight per lane, as in the unblocked kernel
-    if (maxa) {
-        static const unsigned grid = resident_grid(k_segment_xcd<T, U, MSG, true>);
-        k_segment_xcd<T, U, MSG, true><<<grid, kBlock, 0, s>>>(p);
-    } else {
-        static const unsigned grid = resident_grid(k_segment_xcd<T, U, MSG, false>);
-        k_segment_xcd<T, U, MSG, false><<<grid, kBlock, 0, s>>>(p);
-    }
+    const int64_t nc = p.nchunks * (p.nwin > 1 ? p.nwin : 1);
+    const unsigned grid = static_cast<unsigned>((nc + (kBlock / kWave) - 1) / (kBlock / kWave));
+    if (light) k_segment<T, true, 1, U, MSG, MAXA, false, true, true><<<grid, kBlock, 0, s>>>(p);
+    else k_segment<T, true, 1, U, MSG, MAXA, false, false, true><<<grid, kBlock, 0, s>>>(p);
     PYG_LAUNCH_CHECK();
     return PYG_OK;
+}
+
+template <typename T>
+int launch_blocked_msg(const SegParams &p, int mk, bool maxa, bool light, hipStream_t s) {
+    if (maxa) {
+        if (mk == kMsgDiff) return launch_blocked<T, kMsgDiff, true>(p, light, s);
+        if (mk == kMsgWeighted) return launch_blocked<T, kMsgWeighted, true>(p, light, s);
+        return launch_blocked<T, kMsgSrc, true>(p, light, s);
+    }
+    if (mk == kMsgDiff) return launch_blocked<T, kMsgDiff, false>(p, light, s);
+    if (mk == kMsgWeighted) return launch_blocked<T, kMsgWeighted, false>(p, light, s);
+    if (mk == kMsgGcn) return launch_blocked<T, kMsgGcn, false>(p, light, s);
+    return launch_blocked<T, kMsgSrc, false>(p, light, s);
 }
 
 struct SegWs {
@@ -1124,7 +1085,7 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     const int64_t sz = a.dtype == PYG_BF16 ? 2 : 4;
     if ((F * sz) % 16 != 0 || reinterpret_cast<uintptr_t>(a.x) % 16 != 0 || reinterpret_cast<uintptr_t>(a.out) % 16 != 0)
         return PYG_ERR_UNSUPPORTED;  // 16-byte lane vectors only
-    if (!(B == 2 || B == 4 || (B % kXcds == 0 && B / kXcds <= kMaxSubBlocks))) return PYG_ERR_UNSUPPORTED;
+    if (B < 2 || B > kMaxBlocks) return PYG_ERR_UNSUPPORTED;
     const int64_t chunk = segment_chunk(E, B * N, a.chunk);
     const BlockedWs w = carve_blocked(ws, E, N, F, B, a.aggr, chunk);
     if (!ws || ws_bytes < w.bytes) return PYG_ERR_WORKSPACE;
@@ -1163,6 +1124,8 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     p.hot_class = nullptr;
     p.blocks = B;
     p.rpb = N;
+    p.dinv = a.dinv;
+    p.norm_out = a.norm_out;
     // windows of up to 128 bytes: 8 lanes of 16 bytes (fewer for narrower rows)
     const int64_t ep = 16 / sz, nvec = F / ep;
     int lg = 0;
@@ -1172,16 +1135,30 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     p.fcnt = (int64_t(1) << lg) * ep;
     p.nwin = (F + p.fcnt - 1) / p.fcnt;
     if (p.nchunks * p.nwin >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
-    const int mk = a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc);
+    int mk = a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc);
+    if (a.msg == kSegMsgGcn) mk = kMsgGcn;
+    if (mk == kMsgGcn && (maxa || !a.dinv || !a.norm_out)) return PYG_ERR_INVALID_ARG;
+    // short virtual rows on average: one sub-group per row
+    const bool light = lg < 6 && E <= kLightMaxDegree * B * N;
     int rc;
-    if (a.dtype == PYG_BF16) {
-        rc = mk == kMsgDiff ? launch_blocked<uint16_t, kMsgDiff>(p, maxa, s)
-                            : (mk == kMsgWeighted ? launch_blocked<uint16_t, kMsgWeighted>(p, maxa, s)
-                                                  : launch_blocked<uint16_t, kMsgSrc>(p, maxa, s));
+    auto launch = [&](const SegParams &q, int kind) {
+        return a.dtype == PYG_BF16 ? launch_blocked_msg<uint16_t>(q, kind, maxa, light, s)
+                                   : launch_blocked_msg<float>(q, kind, maxa, light, s);
+    };
+    if (mk == kMsgGcn && p.nwin > 1) {
+        // window 0 forms every slot's weight and writes it; the later windows
+        // read those weights back (stream order)
+        SegParams q = p;
+        q.nwin = 1;
+        rc = launch(q, kMsgGcn);
+        if (rc != PYG_OK) return rc;
+        q = p;
+        q.fbase = p.fcnt;
+        q.nwin = p.nwin - 1;
+        q.w = p.norm_out;
+        rc = launch(q, kMsgWeighted);
     } else {
-        rc = mk == kMsgDiff ? launch_blocked<float, kMsgDiff>(p, maxa, s)
-                            : (mk == kMsgWeighted ? launch_blocked<float, kMsgWeighted>(p, maxa, s)
-                                                  : launch_blocked<float, kMsgSrc>(p, maxa, s));
+        rc = launch(p, mk);
     }
     if (rc != PYG_OK) return rc;
     // long virtual rows: fold their pieces (all features) into P

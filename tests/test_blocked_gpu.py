@@ -1,7 +1,9 @@
-"""GPU parity of the source-blocked propagate path: pyg_csr_blocks_build
-(bit-exact against a stable sort of the oracle's CSR by source block) and
-pyg_propagate_blocked against the oracle (sum / mean within the parity rule,
-max / argmax bit for bit, ties across blocks to the lowest edge id)."""
+"""GPU parity of the source-blocked propagate path: pyg_csr_blocks_build and
+pyg_coo_to_csr_blocked (bit-exact against a stable sort of the oracle's CSR
+by source block), pyg_degree_csr_blocks (bit-exact against the oracle's
+degree) and pyg_propagate_blocked against the oracle (sum / mean within the
+parity rule, max / argmax bit for bit, ties across blocks to the lowest edge
+id)."""
 import numpy as np
 import pytest
 import torch
@@ -48,7 +50,7 @@ GRAPHS = [(1, 0), (5, 40), (300, 5000), (2000, 40000), (7001, 90000)]
 
 
 @pytest.mark.parametrize("N,E", GRAPHS)
-@pytest.mark.parametrize("B", [2, 4, 8, 16, 32])
+@pytest.mark.parametrize("B", [2, 3, 4, 8, 16, 32])
 def test_csr_blocks_bit_exact(pyg, N, E, B):
     rng = np.random.default_rng(N + E + B)
     ei_np = synth.random_coo(rng, N, E)
@@ -60,6 +62,41 @@ def test_csr_blocks_bit_exact(pyg, N, E, B):
     assert np.array_equal(bc.col.cpu().numpy().astype(np.int64), col)
     assert np.array_equal(bc.perm.cpu().numpy(), perm)
     assert np.array_equal(bc.weight.cpu().numpy(), w)
+
+
+# the packed sort (key, source and edge id in one 64-bit word) and, for the
+# last graph (2 * 21 + 22 + 1 bits), the sort with separate fields
+DIRECT = [(1, 0), (5, 40), (300, 5000), (7001, 90000), (2_100_000, 4_200_000)]
+
+
+@pytest.mark.parametrize("N,E", DIRECT)
+@pytest.mark.parametrize("B", [2, 3, 8, 32])
+def test_coo_to_csr_blocked_bit_exact(pyg, N, E, B):
+    if N > 100_000 and B not in (2, 32):
+        pytest.skip("one small and one large block count on the large graph")
+    rng = np.random.default_rng(N + E + 7 * B)
+    ei_np = synth.random_coo(rng, N, E)
+    w_np = rng.standard_normal(E).astype(np.float32)
+    ei = to_dev(ei_np)
+    brp, col, perm, w, _ = expected_blocks(ei_np, N, B, w_np)
+    bc = pyg.coo_to_csr_blocked(ei, N, B, to_dev(w_np), with_perm=True)
+    deg = pyg.degree_csr_blocks(bc)
+    torch.cuda.synchronize()
+    assert np.array_equal(bc.rowptr.cpu().numpy(), brp)
+    assert np.array_equal(bc.col.cpu().numpy().astype(np.int64), col)
+    assert np.array_equal(bc.perm.cpu().numpy(), perm)
+    assert np.array_equal(bc.weight.cpu().numpy(), w)
+    assert np.array_equal(deg.cpu().numpy(), oracle.degree(ei_np, N))
+    # without weights and edge ids: the same rowptr and columns
+    bp = pyg.coo_to_csr_blocked(ei, N, B)
+    torch.cuda.synchronize()
+    assert bp.perm is None and bp.weight is None
+    assert torch.equal(bp.rowptr, bc.rowptr) and torch.equal(bp.col, bc.col)
+    # equal to the blocks regrouped from the plain CSR
+    if E:
+        rg = pyg.csr_blocks(pyg.coo_to_csr(ei, N, to_dev(w_np)), B, with_perm=True)
+        torch.cuda.synchronize()
+        assert torch.equal(rg.rowptr, bc.rowptr) and torch.equal(rg.col, bc.col) and torch.equal(rg.perm, bc.perm)
 
 
 def run_case(pyg, ei_np, x_np, B, w_np=None, msg="src", aggr="sum", dtype=F32, chunk=0, what=""):
@@ -97,7 +134,7 @@ def test_propagate_blocked_weighted(pyg, N, E, F, aggr, dtype):
     run_case(pyg, ei_np, x_np, 8, w_np, aggr=aggr, dtype=dtype, what=f"N={N} E={E} F={F}")
 
 
-@pytest.mark.parametrize("B", [2, 4, 8, 16, 24, 32])
+@pytest.mark.parametrize("B", [2, 3, 4, 5, 8, 16, 24, 32])
 @pytest.mark.parametrize("msg,aggr", [("src", "sum"), ("src", "max"), ("diff", "mean"), ("diff", "max")])
 def test_propagate_blocked_messages_and_blocks(pyg, B, msg, aggr):
     rng = np.random.default_rng(B)

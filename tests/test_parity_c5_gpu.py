@@ -494,3 +494,33 @@ def test_c5_gcn_propagate_every_row(pyg, c5, dev_graph, c5_oracle_full):
     assert torch.equal(norm, csr.weight), "C5 fused norms differ from the oracle's (in CSR order)"
     r = check_sum(out, c5_oracle_full["sum"][0], c5_oracle_full["sum"][2], False, "C5 every row: fused GCN propagate")
     print(f"[c5] every row: fused GCN propagate ok (worst error / bound {r:.3f})", flush=True)
+
+
+def test_c5_gcn_propagate_blocked_every_row(pyg, c5, dev_graph, c5_oracle_full):
+    """The fused GCN propagate over the two-block source-blocked CSR (the
+    benchmark step's call): norms bit for bit against the oracle's (carried
+    into the blocked slot order), every output row against the oracle's
+    gcn-weighted sum, fp32 and bf16."""
+    x_np, N = c5["x"], c5["N"]
+    ei, w_ref, csr = dev_graph
+    # the step's calls: the blocked CSR straight from the COO, d from it
+    bplain = pyg.coo_to_csr_blocked(ei, N, 2)
+    deg = pyg.degree_csr_blocks(bplain)
+    norm = torch.empty(csr.E, device="cuda")
+    out = pyg.gcn_propagate_blocked(to_dev(x_np), None, bplain, norm_out=norm)
+    ref_b = pyg.csr_blocks(csr, 2)  # the oracle's norms in the blocked slot order
+    torch.cuda.synchronize()
+    assert torch.equal(bplain.rowptr, ref_b.rowptr) and torch.equal(bplain.col, ref_b.col), \
+        "C5 blocked CSR from the COO differs from the regrouped CSR"
+    assert np.array_equal(deg.cpu().numpy(), oracle.degree(c5["edge_index_gcn"], N))
+    ref_norm = ref_b.weight
+    del ref_b
+    assert torch.equal(norm, ref_norm), "C5 blocked fused norms differ from the oracle's"
+    r = check_sum(out, c5_oracle_full["sum"][0], c5_oracle_full["sum"][2], False,
+                  "C5 every row: blocked fused GCN propagate")
+    del ref_norm
+    outb = pyg.gcn_propagate_blocked(to_dev(x_np).to(torch.bfloat16), None, bplain)
+    torch.cuda.synchronize()
+    check_sum(outb, c5_oracle_full["sum_bf16"][0], c5_oracle_full["sum_bf16"][2], True,
+              "C5 every row: blocked fused GCN propagate bf16")
+    print(f"[c5] every row: blocked fused GCN propagate ok (worst error / bound {r:.3f})", flush=True)
