@@ -345,8 +345,8 @@ int pyg_propagate_blocked(const void *x, int dtype, int64_t N, int64_t F, const 
                           int aggr, void *out, int64_t *argmax, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes needed by pyg_gcn_propagate_blocked (chunk as in the
- * blocked CSR): d^-1/2, the norms when norm_out is NULL, and the blocked
- * propagate's partial rows. */
+ * blocked CSR): d^-1/2, the norms when norm_out is NULL, fp32 rows of
+ * d^-1/2 x (fp32 only), and the blocked propagate's partial rows. */
 int pyg_gcn_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t E, int64_t B, int64_t chunk,
                                         size_t *bytes);
 
@@ -358,7 +358,11 @@ int pyg_gcn_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t
  * pyg_gcn_norm_csr takes it (row lengths, or csr->weight summed in fp64 in
  * CSR slot order) when csr is given, else from bcsr (the row lengths summed
  * over the blocks, or the weights summed in fp64 in blocked slot order),
- * formed in fp64 and rounded once per slot.
+ * formed in fp64 and rounded once per slot. The first 128-byte feature
+ * window uses these norms (and writes them); for fp32 rows without edge
+ * weights the later windows sum the rows d_j^-1/2 x_j (an fp64 product
+ * rounded once, formed in the workspace) and the fold multiplies by
+ * d_i^-1/2 (the same sum up to rounding), otherwise they read the norms.
  *   csr       the graph's CSR (pyg_coo_to_csr), for d, or NULL;
  *   bcsr      pyg_csr_blocks_build(csr, ...) or pyg_coo_to_csr_blocked,
  *             weighted iff csr is weighted;

@@ -168,6 +168,7 @@ struct SegmentArgs {
     bool hint;          // allow the cache-policy hint for hub source rows
     const double *dinv; // kSegMsgGcn: d^-1/2 of every row [n_rows]
     float *norm_out;    // kSegMsgGcn: the slots' weights written here [E], or NULL
+    float *x_scaled;    // kSegMsgGcn, blocked, fp32 x, no weights: room for d^-1/2 x [n_rows, F], or NULL
 };
 // Internal message kind beyond pyg_msg (sum only): the backward of
 // max(x_j + e, 0) over the reversed graph, x = the scaled upstream gradient,
@@ -179,8 +180,9 @@ constexpr int kSegMsgGcn = 101;
 int64_t segment_chunk(int64_t E, int64_t n_rows, int64_t requested);
 // Source-blocked form: a.rowptr has B * n_rows + 1 entries (virtual row
 // b * n_rows + i = the slots of target i whose source lies in block b), a.col,
-// a.weight and a.perm are in that slot order; B a multiple of 8 (at most 32),
-// 16-byte rows. Plain, weighted and difference messages, any aggregation.
+// a.weight and a.perm are in that slot order; 2 <= B <= 32, 16-byte rows.
+// Plain, weighted and difference messages, any aggregation; GCN messages
+// (sum).
 size_t segment_blocked_workspace(int64_t E, int64_t n_rows, int64_t F, int64_t B, int aggr, int64_t chunk);
 int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_bytes, hipStream_t s);
 size_t segment_workspace(int64_t E, int64_t F, int aggr, int64_t chunk, int64_t n_rows);

@@ -324,6 +324,12 @@ __global__ __launch_bounds__(kBlock) void k_blocked_slot_norm(const int64_t *__r
     }
 }
 
+// Room for the pre-scaled rows d^-1/2 x of the blocked GCN propagate (fp32
+// rows: its feature windows after the first gather those, unweighted).
+size_t blocked_scaled_bytes(int dtype, int64_t N, int64_t F) {
+    return dtype == PYG_F32 ? align_up(static_cast<size_t>(N) * F * 4, 256) : 0;
+}
+
 // dinv of every target from a source-blocked CSR: the slots of its B virtual
 // rows (unit weights).
 __global__ void k_blocked_dinv_count(const int64_t *__restrict__ brow, int64_t N, int64_t B, double *__restrict__ dinv) {
@@ -364,7 +370,7 @@ extern "C" int pyg_gcn_propagate_blocked_workspace(int dtype, int64_t N, int64_t
         return PYG_ERR_INVALID_ARG;
     if (N >= (int64_t(1) << 31) || E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     *bytes = align_up(static_cast<size_t>(N) * sizeof(double), 256) + align_up(static_cast<size_t>(E) * 4, 256) +
-             segment_blocked_workspace(E, N, F, B, PYG_SUM, chunk);
+             blocked_scaled_bytes(dtype, N, F) + segment_blocked_workspace(E, N, F, B, PYG_SUM, chunk);
     return PYG_OK;
 }
 
@@ -397,7 +403,8 @@ extern "C" int pyg_gcn_propagate_blocked(const void *x, int dtype, int64_t N, in
     hipStream_t s = static_cast<hipStream_t>(stream);
     double *dinv = static_cast<double *>(ws);
     float *norm_ws = reinterpret_cast<float *>(static_cast<char *>(ws) + align_up(static_cast<size_t>(N) * sizeof(double), 256));
-    void *seg_ws = reinterpret_cast<char *>(norm_ws) + align_up(static_cast<size_t>(E) * 4, 256);
+    float *xs = reinterpret_cast<float *>(reinterpret_cast<char *>(norm_ws) + align_up(static_cast<size_t>(E) * 4, 256));
+    void *seg_ws = reinterpret_cast<char *>(xs) + blocked_scaled_bytes(dtype, N, F);
     if (csr && csr->weight)
         k_row_dinv_weighted<<<grid_for(N, kBlock / kWave, 1 << 16), kBlock, 0, s>>>(csr->rowptr, csr->weight, N, dinv);
     else if (csr)
@@ -432,5 +439,6 @@ extern "C" int pyg_gcn_propagate_blocked(const void *x, int dtype, int64_t N, in
     a.out = out;
     a.dinv = dinv;
     a.norm_out = norm_out ? norm_out : norm_ws;  // the later feature windows read the weights back
+    a.x_scaled = dtype == PYG_F32 ? xs : nullptr;
     return segment_reduce_blocked(a, B, seg_ws, ws_bytes - (static_cast<char *>(seg_ws) - static_cast<char *>(ws)), s);
 }

@@ -946,12 +946,15 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
 // out[i] = sum over b of P[b*N + i] (mean: divided by deg_i, the row's slots
 // over all blocks, as the unblocked kernel divides); max: the largest
 // partial, equal values to the lower edge id, blocks without slots (argmax =
-// sentinel) skipped. A fixed order: deterministic. F % 4 == 0.
+// sentinel) skipped. A fixed order: deterministic. F % 4 == 0. With `scale`,
+// features from `scale_from` on (a multiple of 4) are multiplied by
+// scale[i] in fp64 and rounded once.
 template <typename T, bool MAXA>
 __global__ __launch_bounds__(kBlock) void k_block_fold(const float *__restrict__ P, const int64_t *__restrict__ Parg,
                                                        const int64_t *__restrict__ rowptr, int64_t N, int64_t F,
                                                        int64_t B, int mean, int64_t sentinel, T *__restrict__ out,
-                                                       int64_t *__restrict__ argmax) {
+                                                       int64_t *__restrict__ argmax, const double *__restrict__ scale,
+                                                       int64_t scale_from) {
     const int64_t nq = N * F / 4;
     const int64_t NF = N * F;
     for (int64_t q = blockIdx.x * (int64_t)kBlock + threadIdx.x; q < nq; q += (int64_t)gridDim.x * kBlock) {
@@ -974,6 +977,11 @@ __global__ __launch_bounds__(kBlock) void k_block_fold(const float *__restrict__
 #pragma unroll
                 for (int k = 0; k < 4; ++k) v[k] += pw[k];
             }
+        }
+        if (!MAXA && scale && e % F >= scale_from) {
+            const double si = scale[e / F];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = static_cast<float>(static_cast<double>(v[k]) * si);
         }
         if (!MAXA && mean) {
             const int64_t i = e / F;
@@ -1004,6 +1012,23 @@ __global__ __launch_bounds__(kBlock) void k_block_fold(const float *__restrict__
 // partial rows. At any moment the wavefronts in flight gather from one
 // source block of one feature window, a 1/B part of x's bytes per window.
 constexpr int64_t kMaxBlocks = 32;  // source blocks of a blocked CSR, at most
+
+// xs[i, f] = d_i^-1/2 * x[i, f] for the features f >= f0 (fp64 product,
+// rounded once), four features per thread; F and f0 multiples of 4.
+__global__ __launch_bounds__(kBlock) void k_prescale_rows(const float *__restrict__ x, const double *__restrict__ dinv,
+                                                          int64_t N, int64_t F, int64_t f0, float *__restrict__ xs) {
+    const int64_t per_row = (F - f0) / 4;
+    const int64_t n = N * per_row;
+    for (int64_t q = blockIdx.x * (int64_t)kBlock + threadIdx.x; q < n; q += (int64_t)gridDim.x * kBlock) {
+        const int64_t i = q / per_row;
+        const int64_t e = i * F + f0 + (q - i * per_row) * 4;
+        const float4 v = *reinterpret_cast<const float4 *>(x + e);
+        const double d = dinv[i];
+        *reinterpret_cast<float4 *>(xs + e) =
+            make_float4(static_cast<float>(v.x * d), static_cast<float>(v.y * d), static_cast<float>(v.z * d),
+                        static_cast<float>(v.w * d));
+    }
+}
 
 template <typename T, int MSG, bool MAXA>
 int launch_blocked(const SegParams &p, bool light, hipStream_t s) {
@@ -1134,6 +1159,7 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     p.fbase = 0;
     p.fcnt = (int64_t(1) << lg) * ep;
     p.nwin = (F + p.fcnt - 1) / p.fcnt;
+    const int64_t win_feats = p.fcnt;  // features per window
     if (p.nchunks * p.nwin >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     int mk = a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc);
     if (a.msg == kSegMsgGcn) mk = kMsgGcn;
@@ -1145,9 +1171,13 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
         return a.dtype == PYG_BF16 ? launch_blocked_msg<uint16_t>(q, kind, maxa, light, s)
                                    : launch_blocked_msg<float>(q, kind, maxa, light, s);
     };
+    // GCN without edge weights on fp32 rows: the later windows propagate
+    // d^-1/2 x unweighted and the fold multiplies their features by d_i^-1/2
+    // (no weight stream; the norms are still formed and written by window 0)
+    const bool prescale = mk == kMsgGcn && p.nwin > 1 && !a.weight && a.dtype == PYG_F32 && a.x_scaled;
     if (mk == kMsgGcn && p.nwin > 1) {
         // window 0 forms every slot's weight and writes it; the later windows
-        // read those weights back (stream order)
+        // read those weights back (stream order), or gather pre-scaled rows
         SegParams q = p;
         q.nwin = 1;
         rc = launch(q, kMsgGcn);
@@ -1155,8 +1185,17 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
         q = p;
         q.fbase = p.fcnt;
         q.nwin = p.nwin - 1;
-        q.w = p.norm_out;
-        rc = launch(q, kMsgWeighted);
+        if (prescale) {
+            k_prescale_rows<<<grid_for(N * (F - p.fcnt) / 4, kBlock, 1 << 16), kBlock, 0, s>>>(
+                static_cast<const float *>(a.x), a.dinv, N, F, p.fcnt, a.x_scaled);
+            PYG_LAUNCH_CHECK();
+            q.x = a.x_scaled;
+            q.w = nullptr;
+            rc = launch(q, kMsgSrc);
+        } else {
+            q.w = p.norm_out;
+            rc = launch(q, kMsgWeighted);
+        }
     } else {
         rc = launch(p, mk);
     }
@@ -1170,16 +1209,20 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     if (rc != PYG_OK) return rc;
     const unsigned g = grid_for(N * F / 4, kBlock, 1 << 16);
     const int mean = a.aggr == PYG_MEAN;
+    const double *scale = prescale ? a.dinv : nullptr;
+    const int64_t scale_from = win_feats;  // the pre-scaled windows: all but the first
     if (a.dtype == PYG_BF16) {
         if (maxa) k_block_fold<uint16_t, true><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
-                                                                      static_cast<uint16_t *>(a.out), a.argmax);
+                                                                      static_cast<uint16_t *>(a.out), a.argmax,
+                                                                      nullptr, 0);
         else k_block_fold<uint16_t, false><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
-                                                                  static_cast<uint16_t *>(a.out), a.argmax);
+                                                                  static_cast<uint16_t *>(a.out), a.argmax, nullptr, 0);
     } else {
         if (maxa) k_block_fold<float, true><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
-                                                                   static_cast<float *>(a.out), a.argmax);
+                                                                   static_cast<float *>(a.out), a.argmax, nullptr, 0);
         else k_block_fold<float, false><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
-                                                               static_cast<float *>(a.out), a.argmax);
+                                                               static_cast<float *>(a.out), a.argmax, scale,
+                                                               scale_from);
     }
     PYG_LAUNCH_CHECK();
     return PYG_OK;
