@@ -154,19 +154,29 @@ int count_targets(const int64_t *dst, int64_t E, int64_t N, Out *out, void *ws, 
 // ------------------------------------------------------------- radix sort
 
 // The sort key of an edge: its target, or for a source-blocked CSR
-// (bsize > 0) the virtual row (source / bsize) * N + target, so that the
-// sorted order is by source block, then target, then edge id.
+// (bsize > 0) the source block above the target's bits,
+// (source / bsize) << tb | target, so that the sorted order is by source
+// block, then target, then edge id. The low digits then depend on the
+// target alone (the first pass reads no source ids); the sorted keys are
+// turned into virtual rows (source block) * N + target at the end.
 struct SortKey {
     int64_t bsize;  // 0: plain CSR
     int64_t N;
+    int tb;         // bits of a target id
 };
 
 __device__ __forceinline__ uint32_t first_key(const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64,
-                                              int64_t i, SortKey sk) {
+                                              int64_t i, SortKey sk, bool with_block = true) {
     const uint32_t t = static_cast<uint32_t>(dst64[i]);
-    if (sk.bsize == 0) return t;
+    if (sk.bsize == 0 || !with_block) return t;
     const uint32_t b = static_cast<uint32_t>(src64[i]) / static_cast<uint32_t>(sk.bsize);
-    return b * static_cast<uint32_t>(sk.N) + t;
+    return (b << sk.tb) | t;
+}
+
+// A sorted key as the row of the CSR it was sorted into.
+__device__ __forceinline__ uint32_t key_row(uint32_t k, SortKey sk) {
+    if (sk.bsize == 0) return k;
+    return (k >> sk.tb) * static_cast<uint32_t>(sk.N) + (k & ((1u << sk.tb) - 1u));
 }
 
 struct Payload {  // one sort buffer: key plus carried fields
@@ -191,7 +201,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const int64_t *__rest
     for (int r = 0; r < kItems; ++r) {
         const int64_t i = base + (int64_t)r * kSortBlock;
         if (i < E) {
-            const uint32_t key = dst64 ? first_key(dst64, src64, i, sk) : keys[i];
+            const uint32_t key = dst64 ? first_key(dst64, src64, i, sk, shift + bits > sk.tb) : keys[i];
             atomicAdd(&h[(key >> shift) & mask], 1u);
         }
     }
@@ -325,7 +335,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
     uint32_t *key_out = out.key;
     for (int64_t j = threadIdx.x; j < tlen; j += kSortBlock) {
         const int64_t pos = gbase[sdig[j]] + j;
-        if (pos >= 0 && pos < E) key_out[pos] = stage[j];  // bounds hold for a consistent ranking
+        if (pos >= 0 && pos < E) key_out[pos] = last ? key_row(stage[j], sk) : stage[j];  // bounds hold for a consistent ranking
     }
 
     // fields 1..3: edge id, source, weight
@@ -413,7 +423,8 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist64(const int64_t *__re
         const int64_t i = base + (int64_t)r * kSortBlock;
         if (i < E) {
             const uint64_t d = dig8 ? dig8[i]
-                                    : (dst64 ? (static_cast<uint64_t>(first_key(dst64, src64, i, pk.sk)) >> shift)
+                                    : (dst64 ? (static_cast<uint64_t>(first_key(dst64, src64, i, pk.sk,
+                                                                                shift + bits > pk.sk.tb)) >> shift)
                                              : (keys[i] >> (pk.nb + pk.ib + shift)));
             atomicAdd(&h[d & mask], 1u);
         }
@@ -470,7 +481,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter64(
         if (last) {
             if (perm) perm[pos] = static_cast<int64_t>(e & idmask);
             col[pos] = static_cast<int32_t>((e >> pk.ib) & nodemask);
-            sorted_key[pos] = static_cast<uint32_t>(e >> koff);
+            sorted_key[pos] = key_row(static_cast<uint32_t>(e >> koff), pk.sk);
         } else {
             out[pos] = e;
             // the next pass's digit, one byte: its histogram reads these instead of the 8-byte words
@@ -548,11 +559,8 @@ __global__ void k_validate_batch(const int64_t *__restrict__ b, int64_t N, int64
     if (local) atomicAdd(bad, local);
 }
 
-// Digit plan for keys in [0, nkeys): total key bits, passes, bits per pass
-// (at least one pass).
-void digit_plan(int64_t nkeys, int *nb, int *passes, int *bpp) {
-    int b = 1;
-    while (b < 31 && (int64_t(1) << b) < nkeys) ++b;
+// Digit plan for keys of b bits: passes and bits per pass (at least one pass).
+void digit_plan(int b, int *nb, int *passes, int *bpp) {
     *nb = b;
     *passes = (b + kMaxDigitBits - 1) / kMaxDigitBits;
     *bpp = (b + *passes - 1) / *passes;
@@ -564,13 +572,24 @@ SortKey sort_key(int64_t N, int64_t B) {
     SortKey sk{};
     sk.bsize = B > 1 ? (N + B - 1) / B : 0;
     sk.N = N;
+    sk.tb = 1;
+    while (sk.tb < 31 && (int64_t(1) << sk.tb) < N) ++sk.tb;
     return sk;
+}
+
+// Bits of the sort key for B source blocks (B = 1: the target alone).
+int key_bits(int64_t N, int64_t B) {
+    const SortKey sk = sort_key(N, B);
+    if (B <= 1) return sk.tb;
+    int bb = 0;
+    while ((int64_t(1) << bb) < B) ++bb;
+    return sk.tb + bb;
 }
 
 // Packed layout when a sort key, a node id and an edge id fit 64 bits.
 bool packed_plan(int64_t E, int64_t N, int64_t B, Packing *pk, int *passes, int *bpp) {
-    int kb = 1, nb = 1, ib = 1;
-    while (kb < 31 && (int64_t(1) << kb) < B * N) ++kb;
+    int nb = 1, ib = 1;
+    const int kb = key_bits(N, B);
     while (nb < 31 && (int64_t(1) << nb) < N) ++nb;
     while (ib < 62 && (int64_t(1) << ib) < E) ++ib;
     pk->kb = kb;
@@ -595,7 +614,7 @@ struct CsrWs {
 
 CsrWs carve_csr(void *base, int64_t E, int64_t N, int64_t B, bool weighted) {
     int nb, passes, bpp;
-    digit_plan(B * N, &nb, &passes, &bpp);
+    digit_plan(key_bits(N, B), &nb, &passes, &bpp);
     Packing pk;
     int ppasses, pbpp;
     const bool packed = packed_plan(E, N, B, &pk, &ppasses, &pbpp);
@@ -734,7 +753,7 @@ int coo_to_csr_impl(const int64_t *edge_index, int64_t E, int64_t N, int64_t B, 
         return PYG_OK;
     }
     int nb, passes, bpp;
-    digit_plan(rows, &nb, &passes, &bpp);
+    digit_plan(key_bits(N, B), &nb, &passes, &bpp);
     const SortKey sk = sort_key(N, B);
     Payload in{}, none{};
     int shift = 0;
