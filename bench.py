@@ -38,17 +38,19 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 
-# Byte counters of the step's propagate call (fp32 gcn-weighted sum on the
-# large power-law graph) from rocprofv3 --pmc runs of this script (FETCH_SIZE, then
-# WRITE_SIZE, then TCC_HIT_sum + TCC_MISS_sum; KiB / counts per propagate
-# call, summed over the call's launches), with FETCH_SIZE and WRITE_SIZE on a
-# plain 1024 MiB device copy for scale; see profiles/propagate_c5_counters.md.
+# Byte counters of the step's propagate call (pyg_gcn_propagate_blocked, fp32,
+# two source blocks, on the large power-law graph) from rocprofv3 --pmc runs
+# of this script (FETCH_SIZE, then WRITE_SIZE, then TCC_HIT_sum + TCC_MISS_sum;
+# KiB / counts per call, summed over the call's six launches: d^-1/2, window 0
+# forming the norms, the row pre-scaling, windows 1-3, the long-row fix-up and
+# the block fold), with FETCH_SIZE and WRITE_SIZE on a plain 1024 MiB device
+# copy for scale; see profiles/propagate_c5_counters.md.
 # They describe the sources with the recorded hash only: after any change to
 # those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "d9618da60b8bb337",
-    "fetch_kib": 18542300.7, "write_kib": 166694.0, "tcc_hit": 219795172.7, "tcc_miss": 298164150.0,
-    "copy_mib": 1024, "copy_fetch_kib": 524314.2, "copy_write_kib": 1048576.0,
+    "source_hash": "b82d64f5d155e005",
+    "fetch_kib": 13621325.6, "write_kib": 997135.6, "tcc_hit": 404773891.0, "tcc_miss": 226216936.0,
+    "copy_mib": 1024, "copy_fetch_kib": 524320.6, "copy_write_kib": 1048576.0,
 }
 # everything that decides which kernels a propagate call launches and how
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp",
@@ -804,11 +806,15 @@ def variants(pyg, torch, x, ei, csr, N, E, F, dev):
                 res[f"{kernel}-{aggr}-{dtname}"] = {"ms": ms, "edges_features_per_s": E * F / (ms * 1e-3),
                                                    "alg_GBps": b / (ms * 1e-3) / 1e9,
                                                    "hbm_frac": b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
-    # the source-blocked form (XCD-affine, partial rows folded): the blocking
-    # pass (preprocessing, per graph) and the gcn-weighted sum
-    for B in (2, 8):
+    # the source-blocked form (block-major virtual rows, fp32 partial rows
+    # folded): regrouping a built CSR, building it straight from the COO,
+    # and the gcn-weighted sum over it
+    for B in (2, 4, 8):
         bc = pyg.csr_blocks(csr, B)
         res[f"csr_blocks_build-B{B}"] = {"ms": cold(torch, lambda: pyg.csr_blocks(csr, B, out=bc))}
+        bd = pyg.coo_to_csr_blocked(ei, N, B)
+        res[f"coo_to_csr_blocked-B{B}"] = {"ms": cold(torch, lambda: pyg.coo_to_csr_blocked(ei, N, B, out=bd))}
+        del bd
         for dtname, xx, s in (("f32", x, 4), ("bf16", xb, 2)):
             o = torch.empty_like(xx)
             ws = torch.empty(pyg.propagate_blocked_workspace_bytes(xx, bc, "sum"), dtype=torch.uint8, device=dev)
