@@ -233,6 +233,9 @@ def parse():
     ap.add_argument("--blocks", type=int, default=2,
                     help="source blocks of the step's propagate (pyg_csr_blocks_build + pyg_gcn_propagate_blocked); "
                          "0 = the unblocked CSR propagate (pyg_gcn_propagate)")
+    ap.add_argument("--step-norms", action="store_true",
+                    help="the blocked step's propagate also forms and writes every edge's gcn norm (by default it "
+                         "applies d^-1/2 to the rows before and after the sum and forms no per-edge norm)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="also run one plain device copy of this size (for scaling rocprofv3 byte counters)")
     return ap.parse_args()
@@ -395,12 +398,14 @@ def main():
             mark("degree", 0)  # the in-degree, read off the virtual rows' boundaries
             pyg.degree_csr_blocks(bcsr, out=deg)
             mark("degree", 1)
-            # gcn_norm formed inside the propagate (pyg_gcn_propagate_blocked): d
-            # from the blocked CSR, the norms written to `norm` (blocked slot
-            # order) and summed with the gathered rows, one source block after
-            # another
+            # gcn_norm inside the propagate (pyg_gcn_propagate_blocked): d from
+            # the blocked CSR, the rows scaled by d_j^-1/2 before the sum and by
+            # d_i^-1/2 after it (with --step-norms: every edge's norm formed,
+            # written to `norm` in blocked slot order and used by window 0),
+            # one source block after another
             mark("gcn_norm+propagate", 0)
-            pyg.gcn_propagate_blocked(x, None, bcsr, norm_out=norm, out=out, workspace=ws_gcnb)
+            pyg.gcn_propagate_blocked(x, None, bcsr, norm_out=norm if args.step_norms else None, out=out,
+                                      workspace=ws_gcnb)
             mark("gcn_norm+propagate", 1)
         else:
             mark("coo_to_csr", 0)
@@ -452,6 +457,11 @@ def main():
     if B:  # B row pointers per target, and the fp32 partial rows written and folded
         balg += 8 * (B - 1) * N + 2 * B * N * F * 4
         buniq += 8 * (B - 1) * N
+        if not args.step_norms:
+            # no per-edge norm: no d^-1/2 gather per edge and no norm written,
+            # the rows pre-scaled (read and written once) instead
+            balg += -8 * E - 4 * E + 2 * N * F * 4
+            buniq += -4 * E + N * F * 4
     value = E * F / (ms_per_step * 1e-3)
     ladder = probe_ladder(probe, torch, dev, N * F * 4)
     log("probe ladder done")
@@ -477,8 +487,12 @@ def main():
                    "N": N, "E": E, "F": F, "seed": args.seed, "chunk": args.chunk or "default",
                    "source_blocks": B or None,
                    "step": ("coo_to_csr_blocked(B=%d: stable sort by source block, target, edge id)+degree(blocked "
-                            "row bounds)+[gcn_norm formed and written inside the propagate (sum, blocked csr, "
-                            "partials folded)]+global_pool(mean)" % B)
+                            "row bounds)+[gcn_norm inside the propagate: %s (sum, blocked csr, partials folded)]"
+                            "+global_pool(mean)" % (B, "every edge's norm formed and written, window 0 weighted by "
+                                                       "them, the other windows by pre-scaled rows"
+                                                    if args.step_norms else
+                                                    "d^-1/2 from the row bounds, rows scaled by d_j^-1/2 before "
+                                                    "and d_i^-1/2 after the sum, no per-edge norm"))
                            if B else
                            "coo_to_csr+degree(csr row bounds)+[gcn_norm(csr order) formed and written inside the "
                            "propagate (sum, csr)]+global_pool(mean)"},
@@ -490,24 +504,33 @@ def main():
                      "achieved_source": "bytes past L2 per call (FETCH_SIZE + WRITE_SIZE counters, copy-calibrated) "
                                         "/ the call's event time in the timed steps",
                      "l2_hit": measured_l2_hit(),
-                     "kernel": ("pyg_gcn_propagate_blocked, fp32, B=%d: k_segment over feature window 0 forming "
-                                "and writing the gcn norms, k_segment over windows 1-3 reading them (virtual rows "
-                                "b*N+i, fp32 partial rows), k_segment_fixup, k_block_fold" % B) if B else
+                     "kernel": ("pyg_gcn_propagate_blocked, fp32, B=%d: %s (virtual rows b*N+i, fp32 partial "
+                                "rows), k_segment_fixup, k_block_fold (times d_i^-1/2)" %
+                                (B, "k_segment over feature window 0 forming and writing the gcn norms, "
+                                    "k_prescale_rows, k_segment over windows 1-3"
+                                 if args.step_norms else "k_prescale_rows (d_j^-1/2 x), one k_segment over the four "
+                                                         "windows")) if B else
                                "pyg_gcn_propagate, fp32: k_segment over feature window 0 forming and writing the "
                                "gcn norms, k_segment over windows 1-3 reading them, k_segment_fixup",
                      "unit_of_work": "one gcn_norm+propagate call over the whole graph",
                      "avg_call_ms": t_prop * 1e3,
                      "algorithmic": {"bytes_per_call": balg, "GBps": balg / t_prop / 1e9, "hbm_peak": HBM_PEAK_GBS,
                                      "frac_of_hbm": balg / t_prop / 1e9 / HBM_PEAK_GBS,
-                                     "convention": "every edge gathers its source row and its source's d^-1/2 once "
-                                                   "(cache reuse counted as traffic), plus rowptr, columns, d^-1/2 "
-                                                   "per node, the norms written and one output write"
-                                                   + (", and the fp32 partial rows written and read by the fold"
-                                                      if B else "")},
+                                     "convention": ("every edge gathers its source row once (cache reuse counted "
+                                                    "as traffic), plus rowptr, columns, d^-1/2 per node, the rows "
+                                                    "pre-scaled, the fp32 partial rows written and read by the fold "
+                                                    "and one output write")
+                                                   if B and not args.step_norms else
+                                                   ("every edge gathers its source row and its source's d^-1/2 once "
+                                                    "(cache reuse counted as traffic), plus rowptr, columns, d^-1/2 "
+                                                    "per node, the norms written and one output write"
+                                                    + (", and the fp32 partial rows written and read by the fold"
+                                                       if B else ""))},
                      "compulsory": {"bytes_per_call": buniq, "GBps": buniq / t_prop / 1e9,
                                     "frac_of_hbm": buniq / t_prop / 1e9 / HBM_PEAK_GBS,
-                                    "convention": "every distinct byte once: rowptr, columns, d^-1/2, x, norms "
-                                                  "written, output"}},
+                                    "convention": "every distinct byte once: rowptr, columns, d^-1/2, x, "
+                                                  + ("the pre-scaled rows, " if B and not args.step_norms else
+                                                     "norms written, ") + "output"}},
         "probe": ladder,
         "detail": {"per_call_ms": {n: float(np.mean(times[n])) for n in names},
                    "per_call_cache": "in-step: each call follows the previous call of the same step",
@@ -519,6 +542,9 @@ def main():
                    "gcn_norm_csr_ms": cold(torch, lambda: pyg.gcn_norm_csr(csr, out=norm, workspace=ws_norm)),
                    "propagate_weighted_ms": cold(torch, lambda: pyg.propagate(x, csr=csr_w, aggr="sum", out=out,
                                                                               workspace=ws_prop)),
+                   # the step's call forming and writing every edge's norm
+                   "gcn_propagate_blocked_with_norms_ms": cold(torch, lambda: pyg.gcn_propagate_blocked(
+                       x, None, bcsr, norm_out=norm, out=out, workspace=ws_gcnb)) if B else None,
                    # the step's calls without source blocks: the plain CSR build and
                    # pyg_gcn_propagate over it
                    "coo_to_csr_unblocked_ms": cold(torch, lambda: pyg.coo_to_csr(ei, N, None, chunk=args.chunk,

@@ -358,11 +358,13 @@ int pyg_gcn_propagate_blocked_workspace(int dtype, int64_t N, int64_t F, int64_t
  * pyg_gcn_norm_csr takes it (row lengths, or csr->weight summed in fp64 in
  * CSR slot order) when csr is given, else from bcsr (the row lengths summed
  * over the blocks, or the weights summed in fp64 in blocked slot order),
- * formed in fp64 and rounded once per slot. The first 128-byte feature
- * window uses these norms (and writes them); for fp32 rows without edge
- * weights the later windows sum the rows d_j^-1/2 x_j (an fp64 product
- * rounded once, formed in the workspace) and the fold multiplies by
- * d_i^-1/2 (the same sum up to rounding), otherwise they read the norms.
+ * formed in fp64 and rounded once per slot. When norm_out is given, the
+ * first 128-byte feature window forms these norms, uses them and writes
+ * them. For fp32 rows the other windows (all of them when norm_out is NULL)
+ * instead sum w * (d_j^-1/2 x_j) (the rows pre-scaled in the workspace, an
+ * fp64 product rounded once) and the fold multiplies by d_i^-1/2 in fp64:
+ * the same sum up to rounding, with no per-slot norm; for bf16 rows they
+ * read the norms back.
  *   csr       the graph's CSR (pyg_coo_to_csr), for d, or NULL;
  *   bcsr      pyg_csr_blocks_build(csr, ...) or pyg_coo_to_csr_blocked,
  *             weighted iff csr is weighted;

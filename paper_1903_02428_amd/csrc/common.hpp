@@ -168,7 +168,8 @@ struct SegmentArgs {
     bool hint;          // allow the cache-policy hint for hub source rows
     const double *dinv; // kSegMsgGcn: d^-1/2 of every row [n_rows]
     float *norm_out;    // kSegMsgGcn: the slots' weights written here [E], or NULL
-    float *x_scaled;    // kSegMsgGcn, blocked, fp32 x, no weights: room for d^-1/2 x [n_rows, F], or NULL
+    float *x_scaled;    // kSegMsgGcn, blocked, fp32 x: room for d^-1/2 x [n_rows, F], or NULL
+    bool norms_wanted;  // kSegMsgGcn, blocked: the caller asked for the norms (norm_out is theirs)
 };
 // Internal message kind beyond pyg_msg (sum only): the backward of
 // max(x_j + e, 0) over the reversed graph, x = the scaled upstream gradient,

@@ -440,5 +440,6 @@ extern "C" int pyg_gcn_propagate_blocked(const void *x, int dtype, int64_t N, in
     a.dinv = dinv;
     a.norm_out = norm_out ? norm_out : norm_ws;  // the later feature windows read the weights back
     a.x_scaled = dtype == PYG_F32 ? xs : nullptr;
+    a.norms_wanted = norm_out != nullptr;
     return segment_reduce_blocked(a, B, seg_ws, ws_bytes - (static_cast<char *>(seg_ws) - static_cast<char *>(ws)), s);
 }

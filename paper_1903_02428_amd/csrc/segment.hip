@@ -1159,7 +1159,6 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     p.fbase = 0;
     p.fcnt = (int64_t(1) << lg) * ep;
     p.nwin = (F + p.fcnt - 1) / p.fcnt;
-    const int64_t win_feats = p.fcnt;  // features per window
     if (p.nchunks * p.nwin >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
     int mk = a.msg == PYG_MSG_DIFF ? kMsgDiff : (a.weight ? kMsgWeighted : kMsgSrc);
     if (a.msg == kSegMsgGcn) mk = kMsgGcn;
@@ -1171,30 +1170,37 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
         return a.dtype == PYG_BF16 ? launch_blocked_msg<uint16_t>(q, kind, maxa, light, s)
                                    : launch_blocked_msg<float>(q, kind, maxa, light, s);
     };
-    // GCN without edge weights on fp32 rows: the later windows propagate
-    // d^-1/2 x unweighted and the fold multiplies their features by d_i^-1/2
-    // (no weight stream; the norms are still formed and written by window 0)
-    const bool prescale = mk == kMsgGcn && p.nwin > 1 && !a.weight && a.dtype == PYG_F32 && a.x_scaled;
-    if (mk == kMsgGcn && p.nwin > 1) {
-        // window 0 forms every slot's weight and writes it; the later windows
-        // read those weights back (stream order), or gather pre-scaled rows
+    // GCN on fp32 rows: the windows that need no norms propagate the rows
+    // d_j^-1/2 x_j (times the edge weight, if any) and the fold multiplies
+    // them by d_i^-1/2 (no per-slot norm is formed there). When the caller
+    // wants the norms, window 0 still forms, uses and writes them.
+    const bool prescale = mk == kMsgGcn && a.dtype == PYG_F32 && a.x_scaled;
+    const int64_t first_scaled = (a.norms_wanted || !prescale) ? p.fcnt : 0;  // first pre-scaled feature
+    if (mk == kMsgGcn) {
         SegParams q = p;
-        q.nwin = 1;
-        rc = launch(q, kMsgGcn);
-        if (rc != PYG_OK) return rc;
-        q = p;
-        q.fbase = p.fcnt;
-        q.nwin = p.nwin - 1;
-        if (prescale) {
-            k_prescale_rows<<<grid_for(N * (F - p.fcnt) / 4, kBlock, 1 << 16), kBlock, 0, s>>>(
-                static_cast<const float *>(a.x), a.dinv, N, F, p.fcnt, a.x_scaled);
-            PYG_LAUNCH_CHECK();
-            q.x = a.x_scaled;
-            q.w = nullptr;
-            rc = launch(q, kMsgSrc);
-        } else {
-            q.w = p.norm_out;
-            rc = launch(q, kMsgWeighted);
+        if (first_scaled > 0) {
+            // window 0 forms every slot's weight (and writes it); without
+            // pre-scaled rows the later windows read those weights back
+            q.nwin = 1;
+            rc = launch(q, kMsgGcn);
+            if (rc != PYG_OK) return rc;
+        }
+        const int64_t rest = p.nwin - first_scaled / p.fcnt;  // windows after the norm-forming one
+        if (rest > 0) {
+            q = p;
+            q.fbase = first_scaled;
+            q.nwin = rest;
+            if (prescale) {
+                k_prescale_rows<<<grid_for(N * (F - first_scaled) / 4, kBlock, 1 << 16), kBlock, 0, s>>>(
+                    static_cast<const float *>(a.x), a.dinv, N, F, first_scaled, a.x_scaled);
+                PYG_LAUNCH_CHECK();
+                q.x = a.x_scaled;
+                q.w = a.weight;
+                rc = launch(q, a.weight ? kMsgWeighted : kMsgSrc);
+            } else {
+                q.w = p.norm_out;
+                rc = launch(q, kMsgWeighted);
+            }
         }
     } else {
         rc = launch(p, mk);
@@ -1210,7 +1216,7 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     const unsigned g = grid_for(N * F / 4, kBlock, 1 << 16);
     const int mean = a.aggr == PYG_MEAN;
     const double *scale = prescale ? a.dinv : nullptr;
-    const int64_t scale_from = win_feats;  // the pre-scaled windows: all but the first
+    const int64_t scale_from = first_scaled;
     if (a.dtype == PYG_BF16) {
         if (maxa) k_block_fold<uint16_t, true><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
                                                                       static_cast<uint16_t *>(a.out), a.argmax,

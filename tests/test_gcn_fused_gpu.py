@@ -102,7 +102,11 @@ def test_gcn_propagate_blocked_parity(pyg, N, E, F, B, weighted):
     w_or = oracle.gcn_norm(ei_np, N, w_np).astype(np.float32)
     ref, _, sabs = oracle.propagate(x_np, ei_np, w_or, aggr="sum")
     check_sum(out, ref, sabs, False, f"gcn_propagate_blocked B={B} N={N} E={E} F={F} weighted={weighted}")
-    # no norm_out: the workspace keeps them; bf16 rows (when they are 16-byte vectors)
+    # no norm_out: fp32 rows take every window pre-scaled (no norm formed)
+    out2 = pyg.gcn_propagate_blocked(to_dev(x_np), csr, bc)
+    torch.cuda.synchronize()
+    check_sum(out2, ref, sabs, False, f"gcn_propagate_blocked no norms B={B} N={N} E={E} F={F} w={weighted}")
+    # bf16 rows (when they are 16-byte vectors): window 0 forms the norms into the workspace
     if (F * 2) % 16 != 0:
         return
     outb = pyg.gcn_propagate_blocked(to_dev(x_np).to(torch.bfloat16), csr, bc)
@@ -161,3 +165,6 @@ def test_gcn_propagate_blocked_degree_from_blocks(pyg, N, E, F, weighted):
         assert np.all(np.abs(got.view(np.int32).astype(np.int64) - exp.view(np.int32).astype(np.int64)) <= 1)
     ref, _, sabs = oracle.propagate(x_np, ei_np, w_or, aggr="sum")
     check_sum(out, ref, sabs, False, f"gcn_propagate_blocked (d from blocks) N={N} E={E} F={F} w={weighted}")
+    out2 = pyg.gcn_propagate_blocked(to_dev(x_np), None, bc)
+    torch.cuda.synchronize()
+    check_sum(out2, ref, sabs, False, f"gcn_propagate_blocked (d from blocks, no norms) N={N} E={E} F={F}")

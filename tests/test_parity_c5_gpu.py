@@ -519,6 +519,12 @@ def test_c5_gcn_propagate_blocked_every_row(pyg, c5, dev_graph, c5_oracle_full):
     r = check_sum(out, c5_oracle_full["sum"][0], c5_oracle_full["sum"][2], False,
                   "C5 every row: blocked fused GCN propagate")
     del ref_norm
+    # without norms (the benchmark step's call): every window pre-scaled
+    out = pyg.gcn_propagate_blocked(to_dev(x_np), None, bplain)
+    torch.cuda.synchronize()
+    r2 = check_sum(out, c5_oracle_full["sum"][0], c5_oracle_full["sum"][2], False,
+                   "C5 every row: blocked GCN propagate, rows pre-scaled")
+    print(f"[c5] every row: blocked GCN propagate without norms ok (worst error / bound {r2:.3f})", flush=True)
     outb = pyg.gcn_propagate_blocked(to_dev(x_np).to(torch.bfloat16), None, bplain)
     torch.cuda.synchronize()
     check_sum(outb, c5_oracle_full["sum_bf16"][0], c5_oracle_full["sum_bf16"][2], True,
