@@ -39,18 +39,19 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 
 # Byte counters of the step's propagate call (pyg_gcn_propagate_blocked, fp32,
-# two source blocks, on the large power-law graph) from rocprofv3 --pmc runs
-# of this script (FETCH_SIZE, then WRITE_SIZE, then TCC_HIT_sum + TCC_MISS_sum;
-# KiB / counts per call, summed over the call's six launches: d^-1/2, window 0
-# forming the norms, the row pre-scaling, windows 1-3, the long-row fix-up and
-# the block fold), with FETCH_SIZE and WRITE_SIZE on a plain 1024 MiB device
-# copy for scale; see profiles/propagate_c5_counters.md.
+# two source blocks, no per-edge norms, on the large power-law graph) from
+# rocprofv3 --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE, then
+# TCC_HIT_sum + TCC_MISS_sum; KiB / counts per call, summed over the call's
+# five launches: d^-1/2, the row pre-scaling, the four windows, the long-row
+# fix-up and the block fold; the first three calls of each run, the timed
+# steps, before the detail calls), with FETCH_SIZE and WRITE_SIZE on a plain
+# 1024 MiB device copy for scale; see profiles/propagate_c5_counters.md.
 # They describe the sources with the recorded hash only: after any change to
 # those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "b82d64f5d155e005",
-    "fetch_kib": 13621325.6, "write_kib": 997135.6, "tcc_hit": 404773891.0, "tcc_miss": 226216936.0,
-    "copy_mib": 1024, "copy_fetch_kib": 524320.6, "copy_write_kib": 1048576.0,
+    "source_hash": "15849bb33678f42a",
+    "fetch_kib": 12903842.6, "write_kib": 510598.6, "tcc_hit": 300245831.7, "tcc_miss": 210719991.0,
+    "copy_mib": 1024, "copy_fetch_kib": 524319.5, "copy_write_kib": 1048576.0,
 }
 # everything that decides which kernels a propagate call launches and how
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp",
