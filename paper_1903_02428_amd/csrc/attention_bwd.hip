@@ -89,7 +89,7 @@ __global__ __launch_bounds__(kBlock) void k_head_dots(const T *__restrict__ g, c
             if (k < pairs && q == 0) grad_alpha[p * H + h] = acc;
         }
         if (t >= e1) break;
-        ++r;
+        r = next_row_with_slots(rowptr, N, r, t, lane);
     }
 }
 
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kBlock) void k_head_dots_vec(const T *__restrict__ 
             }
         }
         if (t >= e1) break;
-        ++r;
+        r = next_row_with_slots(rowptr, N, r, t, lane);
     }
 }
 
@@ -212,7 +212,7 @@ __global__ __launch_bounds__(kBlock) void k_gat_dv(const float *__restrict__ a_s
             dv[k] = v >= 0.f ? g[k] : slope * g[k];
         }
         if (t >= e1) break;
-        ++r;
+        r = next_row_with_slots(rowptr, N, r, t, lane);
     }
 }
 

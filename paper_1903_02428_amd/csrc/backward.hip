@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kBlock) void k_sddmm(const T *__restrict__ g, const
             if (p < b && q == 0) grad_w[perm ? perm[p] : p] = sc * acc;
         }
         if (t >= e1) break;
-        ++r;
+        r = next_row_with_slots(rowptr, N, r, t, lane);
     }
 }
 
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kBlock) void k_sddmm_vec(const T *__restrict__ g, c
             }
         }
         if (t >= e1) break;
-        ++r;
+        r = next_row_with_slots(rowptr, N, r, t, lane);
     }
 }
 
@@ -429,7 +429,7 @@ __global__ __launch_bounds__(kBlock) void k_edge_grad(const TG *__restrict__ gs,
             }
         }
         if (t >= e1) break;
-        ++r;
+        r = next_row_with_slots(rowptr, N, r, t, lane);
     }
 }
 

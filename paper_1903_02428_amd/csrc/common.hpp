@@ -100,6 +100,16 @@ __device__ inline int64_t wave_lower_bound(const int64_t *__restrict__ a, int64_
     return m ? lo + (__ffsll(static_cast<unsigned long long>(m)) - 1) : len - 1;
 }
 
+// The next row of a walk over a chunk's slots, after row r that ends at slot
+// t < E: row r + 1, or when that row is empty, the row that holds slot t.
+// A run of empty rows all starts at t, so it belongs to one chunk; stepping
+// through it row by row made that chunk's wavefront the whole call's tail.
+__device__ __forceinline__ int64_t next_row_with_slots(const int64_t *__restrict__ rowptr, int64_t N, int64_t r,
+                                                       int64_t t, int lane) {
+    if (uniform64(rowptr[r + 2]) != t) return r + 1;  // r + 2 <= N: row r + 1 exists, as t < rowptr[N]
+    return uniform64(wave_lower_bound(rowptr, N + 1, t + 1, lane)) - 1;
+}
+
 // Workgroups of a launch are dealt to the 8 XCDs in turn (workgroup w runs
 // on XCD w % 8). xcd_major(w, T) renumbers the T workgroups so that each XCD
 // takes one contiguous range of the new order: work items that are

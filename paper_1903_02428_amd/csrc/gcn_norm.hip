@@ -118,7 +118,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_edge_norm(const int64_t *__restr
             }
         }
         if (t >= e1) break;
-        ++r;
+        r = next_row_with_slots(rowptr, N, r, t, lane);
     }
 }
 
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_edge_norm_light(const int64_t *_
     if (e0 >= E) return;
     const int64_t e1 = (e0 + kNormLightChunk) < E ? (e0 + kNormLightChunk) : E;
     const int64_t r0 = uniform64(wave_lower_bound(rowptr, N + 1, e0 + 1, lane)) - 1;  // row holding slot e0
-    for (int64_t rb = r0;; rb += kWave) {
+    for (int64_t rb = r0;;) {
         const int64_t r = rb + lane;
         if (r < N) {
             const int64_t s = rowptr[r], t = rowptr[r + 1];
@@ -151,8 +151,15 @@ __global__ __launch_bounds__(kBlock) void k_csr_edge_norm_light(const int64_t *_
                     norm[p] = static_cast<float>(dinv[col[p]] * static_cast<double>(w ? w[p] : 1.f) * di);
             }
         }
-        const int64_t nxt = rb + kWave;  // the next batch of rows, if one still starts inside the chunk
-        if (nxt >= N || uniform64(rowptr[nxt]) >= e1) break;
+        int64_t nxt = rb + kWave;  // the next batch of rows, if one still starts inside the chunk
+        if (nxt >= N) break;
+        const int64_t pn = uniform64(rowptr[nxt]);
+        if (pn >= e1) break;
+        // a whole batch of empty rows ahead (a run of them all starts at pn):
+        // go on at the last row that starts at pn
+        if (uniform64(rowptr[(nxt + kWave) < N ? (nxt + kWave) : N]) == pn)
+            nxt = uniform64(wave_lower_bound(rowptr, N + 1, pn + 1, lane)) - 1;
+        rb = nxt;
     }
 }
 

@@ -36,6 +36,8 @@
 // is fixed, so results stay bit-reproducible.
 #include "common.hpp"
 
+#include <type_traits>
+
 #ifndef PYG_SEG_MAX_CHUNK
 #define PYG_SEG_MAX_CHUNK 1024  // default chunk of long-row graphs (slots per wavefront), at most
 #endif
@@ -84,6 +86,10 @@ struct SegParams {
     // virtual row r = (source block r / rpb, target r % rpb)
     int64_t blocks;
     int64_t rpb;
+    // > 0: the launch's first zero_items work items zero-fill every empty row
+    // (all F features), kZeroRows rows each; the row walkers skip empty rows,
+    // so one launch of every call must carry them
+    int64_t zero_items;
     // GCN messages (kMsgGcn): dinv [n_rows] fp64 (d^-1/2 of every row), the
     // slot weight w_p = dinv[col] * w_p * dinv[row] formed in fp64 and rounded
     // once; norm_out [E] (or NULL) receives it from the window at feature 0
@@ -565,6 +571,35 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
     }
 }
 
+// Empty rows (no slots) are written here, in parallel, rather than by the
+// chunk walkers: a run of empty rows all starts at one slot and so belongs to
+// one chunk, which would otherwise walk it row by row (a graph whose first
+// half of rows has no edges took 70 times longer than one without). Work
+// item z covers rows [z * kZeroRows, (z + 1) * kZeroRows): every empty row
+// gets 0 in all F features (and argmax = sentinel).
+constexpr int64_t kZeroRows = 2048;
+template <typename T, bool OF32>
+__device__ __forceinline__ void zero_empty_rows(const SegParams &p, int64_t z, int lane) {
+    using TO = typename std::conditional<OF32, float, T>::type;
+    TO *out = static_cast<TO *>(p.out);
+    const int64_t r_end = (z + 1) * kZeroRows < p.n_rows ? (z + 1) * kZeroRows : p.n_rows;
+    for (int64_t r0 = z * kZeroRows; r0 < r_end; r0 += kWave) {
+        const int64_t r = r0 + lane;
+        const bool in = r < r_end;
+        const int64_t a = in ? p.rowptr[r] : 0, b = in ? p.rowptr[r + 1] : 1;
+        uint64_t m = __ballot(in && a == b);
+        while (m) {
+            const int k = __ffsll(static_cast<unsigned long long>(m)) - 1;
+            m &= m - 1;
+            const int64_t row = r0 + k;
+            for (int64_t f = lane; f < p.F; f += kWave) {
+                out[row * p.F + f] = TO(0);
+                if (p.argmax) p.argmax[row * p.F + f] = p.sentinel;
+            }
+        }
+    }
+}
+
 // One wavefront's work on chunk c (features p.fbase .. p.fbase + p.fcnt).
 template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, bool LIGHT, bool OF32>
 __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c, int lane) {
@@ -590,9 +625,16 @@ __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c
         int64_t rb = rA;
         while (rb < p.n_rows) {
             const int64_t rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
-            // rows rb .. rb+cnt-1 start in the chunk; lane i+1 holds the end of row rb+i
-            const bool in = lane < kWave - 1 && rb + lane < p.n_rows && (last || rp < e1);
+            // rows rb .. rb+cnt-1 start in the chunk (rows starting at E are
+            // empty: zero-filled separately); lane i+1 holds the end of row rb+i
+            const bool in = lane < kWave - 1 && rb + lane < p.n_rows && rp < (last ? p.E : e1);
             const int cnt = __popcll(__ballot(in));
+            const int64_t s_first = uniform64(__shfl(rp, 0, kWave));
+            if (cnt == kWave - 1 && uniform64(__shfl(rp, kWave - 1, kWave)) == s_first) {
+                // 63 empty rows in a row: skip to the last row that starts at s_first
+                rb = uniform64(wave_lower_bound(p.rowptr, p.n_rows + 1, s_first + 1, lane)) - 1;
+                continue;
+            }
             for (int i0 = 0; i0 < cnt; i0 += S) {
                 const int i = i0 + sg;
                 const int ii = i < cnt ? i : cnt - 1;
@@ -600,7 +642,7 @@ __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c
                 const bool is_long = i < cnt && t - s > p.chunk;  // only the chunk's last row can be long
                 const uint64_t lm = __ballot(is_long);
                 if (lm) head = static_cast<int32_t>(rb + i0 + ((__ffsll(static_cast<unsigned long long>(lm)) - 1) >> p.lg_l));
-                light_row<T, VEC, U, MSG, MAXA, IDENT, OF32>(p, rb + i, s, t, i < cnt && !is_long, lane);
+                light_row<T, VEC, U, MSG, MAXA, IDENT, OF32>(p, rb + i, s, t, i < cnt && !is_long && t > s, lane);
             }
             if (cnt < kWave - 1) break;  // the chunk's rows end in this batch
             rb += cnt;
@@ -622,6 +664,16 @@ __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c
         const int64_t s = uniform64(__shfl(rp, (int)(r - rb), kWave));
         const int64_t t = uniform64(__shfl(rp, (int)(r + 1 - rb), kWave));
         if (!last && s >= e1) break;
+        if (s >= p.E) break;  // the rows left are empty (zero-filled separately)
+        if (s == t) {         // an empty row, zero-filled separately
+            if (uniform64(__shfl(rp, kWave - 1, kWave)) == s) {
+                // rows r .. rb+62 are empty too: go on at the last row that starts at s
+                r = uniform64(wave_lower_bound(p.rowptr, p.n_rows + 1, s + 1, lane)) - 2;
+                rb = r + 1;
+                rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
+            }
+            continue;
+        }
         if (t - s > p.chunk) {
             reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT, OF32>(p, r, s, e1, kPartial, 2 * c + 1, lane, hot);
             head = static_cast<int32_t>(r);
@@ -636,6 +688,11 @@ template <typename T, bool VEC, int NS, int U, int MSG, bool MAXA, bool IDENT, b
 __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
     const int lane = threadIdx.x & (kWave - 1);
     int64_t c = uniform64((int64_t)blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave));
+    if (c < p.zero_items) {  // the first work items: empty rows (short, dispatched first)
+        zero_empty_rows<T, OF32>(p, c, lane);
+        return;
+    }
+    c -= p.zero_items;
     if (p.nwin > 1) {  // all chunks of window 0, then of window 1, ...: one tail for all windows
         const int64_t w = c / p.nchunks;
         if (w >= p.nwin) return;
@@ -798,7 +855,7 @@ int launch_fixup(const SegParams &p, hipStream_t s) {
 template <typename T, bool VEC, int NS, int MSG, bool MAXA, bool IDENT>
 int launch_window(const SegParams &p, bool light, bool fixup, hipStream_t s) {
     constexpr int U = NS == 1 ? 8 : (NS == 2 ? 4 : 2);
-    const int64_t nc = p.nchunks * (p.nwin > 1 ? p.nwin : 1);
+    const int64_t nc = p.nchunks * (p.nwin > 1 ? p.nwin : 1) + p.zero_items;
     const unsigned grid = static_cast<unsigned>((nc + (kBlock / kWave) - 1) / (kBlock / kWave));
     if constexpr (NS == 1) {
         if (light) k_segment<T, VEC, NS, U, MSG, MAXA, IDENT, true><<<grid, kBlock, 0, s>>>(p);
@@ -880,6 +937,8 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     }
     // lane vectors covered by one launch (NS = 4, or one narrow window)
     const int64_t per_window = narrow ? kWindowBytes / 16 : 4 * kWave;
+    // the first launch also zero-fills the empty rows (all features)
+    p.zero_items = (a.n_rows + kZeroRows - 1) / kZeroRows;
     if (narrow && PYG_WINDOWS_ONE_LAUNCH) {
         // every window is the same width (rows are a multiple of a window): one
         // launch, window-major, then the fold of the long rows over all features
@@ -900,6 +959,7 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
             rc = launch_msg<T, true, false>(q, kMsgGcn, ident, 1, light, false, s);
             if (rc != PYG_OK) return rc;
             q = p;
+            q.zero_items = 0;
             q.fbase = p.fcnt;
             q.nwin = p.nwin - 1;
             q.w = p.norm_out;
@@ -933,6 +993,7 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
         else rc = maxa ? launch_msg<T, false, true>(p, mk, ident, ns, light, fixup, s)
                        : launch_msg<T, false, false>(p, mk, ident, ns, light, fixup, s);
         if (rc != PYG_OK) return rc;
+        p.zero_items = 0;
     }
     if (narrow) {
         p.fbase = 0;
@@ -1033,7 +1094,7 @@ __global__ __launch_bounds__(kBlock) void k_prescale_rows(const float *__restric
 template <typename T, int MSG, bool MAXA>
 int launch_blocked(const SegParams &p, bool light, hipStream_t s) {
     constexpr int U = 8;  // gathers in flight per lane, as in the unblocked kernel
-    const int64_t nc = p.nchunks * (p.nwin > 1 ? p.nwin : 1);
+    const int64_t nc = p.nchunks * (p.nwin > 1 ? p.nwin : 1) + p.zero_items;
     const unsigned grid = static_cast<unsigned>((nc + (kBlock / kWave) - 1) / (kBlock / kWave));
     if (light) k_segment<T, true, 1, U, MSG, MAXA, false, true, true><<<grid, kBlock, 0, s>>>(p);
     else k_segment<T, true, 1, U, MSG, MAXA, false, false, true><<<grid, kBlock, 0, s>>>(p);
@@ -1165,6 +1226,7 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     if (mk == kMsgGcn && (maxa || !a.dinv || !a.norm_out)) return PYG_ERR_INVALID_ARG;
     // short virtual rows on average: one sub-group per row
     const bool light = lg < 6 && E <= kLightMaxDegree * B * N;
+    p.zero_items = (B * N + kZeroRows - 1) / kZeroRows;  // the first launch zero-fills the empty virtual rows
     int rc;
     auto launch = [&](const SegParams &q, int kind) {
         return a.dtype == PYG_BF16 ? launch_blocked_msg<uint16_t>(q, kind, maxa, light, s)
@@ -1188,6 +1250,7 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
         const int64_t rest = p.nwin - first_scaled / p.fcnt;  // windows after the norm-forming one
         if (rest > 0) {
             q = p;
+            if (first_scaled > 0) q.zero_items = 0;  // the first launch did
             q.fbase = first_scaled;
             q.nwin = rest;
             if (prescale) {
