@@ -49,9 +49,9 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 # They describe the sources with the recorded hash only: after any change to
 # those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "15849bb33678f42a",
-    "fetch_kib": 12903842.6, "write_kib": 510598.6, "tcc_hit": 300245831.7, "tcc_miss": 210719991.0,
-    "copy_mib": 1024, "copy_fetch_kib": 524319.5, "copy_write_kib": 1048576.0,
+    "source_hash": "39c8f154b0290f46",
+    "fetch_kib": 12846548.6, "write_kib": 510338.7, "tcc_hit": 296644727.0, "tcc_miss": 209785118.0,
+    "copy_mib": 1024, "copy_fetch_kib": 524320.1, "copy_write_kib": 1048576.0,
 }
 # everything that decides which kernels a propagate call launches and how
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp",
