@@ -100,13 +100,31 @@ __device__ inline int64_t wave_lower_bound(const int64_t *__restrict__ a, int64_
     return m ? lo + (__ffsll(static_cast<unsigned long long>(m)) - 1) : len - 1;
 }
 
+// First index i in [0, len) with a[i] >= key (a non-decreasing, a[len - 1] >=
+// key), by a plain binary search on wave-uniform values: about log2(len)
+// dependent loads but almost no vector registers, for searches that are rare
+// (skipping a long run of empty rows) inside kernels whose occupancy is set
+// by their register use.
+__device__ inline int64_t uniform_lower_bound(const int64_t *__restrict__ a, int64_t len, int64_t key) {
+    int64_t lo = 0, hi = len - 1;
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (uniform64(a[mid]) >= key) hi = mid;
+        else lo = mid + 1;
+    }
+    return lo;
+}
+
 // The next row of a walk over a chunk's slots, after row r that ends at slot
-// t < E: row r + 1, or when that row is empty, the row that holds slot t.
+// t < E: row r + 1, or when a long run of empty rows follows, the row that
+// holds slot t.
 // A run of empty rows all starts at t, so it belongs to one chunk; stepping
 // through it row by row made that chunk's wavefront the whole call's tail.
 __device__ __forceinline__ int64_t next_row_with_slots(const int64_t *__restrict__ rowptr, int64_t N, int64_t r,
                                                        int64_t t, int lane) {
     if (uniform64(rowptr[r + 2]) != t) return r + 1;  // r + 2 <= N: row r + 1 exists, as t < rowptr[N]
+    // a few empty rows are stepped through; a run of 32 or more is searched past
+    if (uniform64(rowptr[(r + 33) < N ? (r + 33) : N]) != t) return r + 1;
     return uniform64(wave_lower_bound(rowptr, N + 1, t + 1, lane)) - 1;
 }
 

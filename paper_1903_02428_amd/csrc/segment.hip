@@ -87,9 +87,10 @@ struct SegParams {
     int64_t blocks;
     int64_t rpb;
     // > 0: the launch's first zero_items work items zero-fill every empty row
-    // (all F features), kZeroRows rows each; the row walkers skip empty rows,
-    // so one launch of every call must carry them
+    // (all F features), zero_rows rows each; the row walkers skip long runs
+    // of empty rows, so one launch of every call must carry them
     int64_t zero_items;
+    int64_t zero_rows;  // rows per zero-fill work item (a multiple of 64)
     // GCN messages (kMsgGcn): dinv [n_rows] fp64 (d^-1/2 of every row), the
     // slot weight w_p = dinv[col] * w_p * dinv[row] formed in fp64 and rounded
     // once; norm_out [E] (or NULL) receives it from the window at feature 0
@@ -575,15 +576,21 @@ __device__ __forceinline__ void light_row(const SegParams &p, int64_t r, int64_t
 // chunk walkers: a run of empty rows all starts at one slot and so belongs to
 // one chunk, which would otherwise walk it row by row (a graph whose first
 // half of rows has no edges took 70 times longer than one without). Work
-// item z covers rows [z * kZeroRows, (z + 1) * kZeroRows): every empty row
-// gets 0 in all F features (and argmax = sentinel).
-constexpr int64_t kZeroRows = 2048;
+// item z covers rows [z * zero_rows, (z + 1) * zero_rows): every empty row
+// gets 0 in all F features (and argmax = sentinel). About 1,024 items per
+// launch, each a few dependent loads of row bounds.
+inline void set_zero_items(SegParams &p, int64_t n_rows) {
+    int64_t per = (n_rows + 1023) / 1024;
+    per = (per + kWave - 1) / kWave * kWave;
+    p.zero_rows = per > kWave ? per : kWave;
+    p.zero_items = (n_rows + p.zero_rows - 1) / p.zero_rows;
+}
 template <typename T, bool OF32>
 __device__ __forceinline__ void zero_empty_rows(const SegParams &p, int64_t z, int lane) {
     using TO = typename std::conditional<OF32, float, T>::type;
     TO *out = static_cast<TO *>(p.out);
-    const int64_t r_end = (z + 1) * kZeroRows < p.n_rows ? (z + 1) * kZeroRows : p.n_rows;
-    for (int64_t r0 = z * kZeroRows; r0 < r_end; r0 += kWave) {
+    const int64_t r_end = (z + 1) * p.zero_rows < p.n_rows ? (z + 1) * p.zero_rows : p.n_rows;
+    for (int64_t r0 = z * p.zero_rows; r0 < r_end; r0 += kWave) {
         const int64_t r = r0 + lane;
         const bool in = r < r_end;
         const int64_t a = in ? p.rowptr[r] : 0, b = in ? p.rowptr[r + 1] : 1;
@@ -632,7 +639,7 @@ __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c
             const int64_t s_first = uniform64(__shfl(rp, 0, kWave));
             if (cnt == kWave - 1 && uniform64(__shfl(rp, kWave - 1, kWave)) == s_first) {
                 // 63 empty rows in a row: skip to the last row that starts at s_first
-                rb = uniform64(wave_lower_bound(p.rowptr, p.n_rows + 1, s_first + 1, lane)) - 1;
+                rb = uniform_lower_bound(p.rowptr, p.n_rows + 1, s_first + 1) - 1;
                 continue;
             }
             for (int i0 = 0; i0 < cnt; i0 += S) {
@@ -654,26 +661,26 @@ __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c
         p.head_row[c] = head;  // uniform: every lane stores the same value (no lane-0 branch)
         return;
     }
-    int64_t rb = rA;
-    int64_t rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
+    // rows are walked in batches of 64 row bounds; a batch that starts 63
+    // empty rows (a run of them, zero-filled separately) is searched past,
+    // while a shorter run is walked (each such row writes its zeros too)
+    int64_t rb = rA - kWave;  // the first iteration loads the batch at rA
+    int64_t rp = 0;
     for (int64_t r = rA; r < p.n_rows; ++r) {
         if (r + 1 - rb >= kWave) {
             rb = r;
             rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
+            const int64_t s0 = uniform64(__shfl(rp, 0, kWave));
+            if (rb + kWave - 1 <= p.n_rows && uniform64(__shfl(rp, kWave - 1, kWave)) == s0) {
+                if (s0 >= p.E || (!last && s0 >= e1)) break;
+                r = uniform64(wave_lower_bound(p.rowptr, p.n_rows + 1, s0 + 1, lane)) - 1;
+                rb = r;
+                rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
+            }
         }
         const int64_t s = uniform64(__shfl(rp, (int)(r - rb), kWave));
         const int64_t t = uniform64(__shfl(rp, (int)(r + 1 - rb), kWave));
         if (!last && s >= e1) break;
-        if (s >= p.E) break;  // the rows left are empty (zero-filled separately)
-        if (s == t) {         // an empty row, zero-filled separately
-            if (uniform64(__shfl(rp, kWave - 1, kWave)) == s) {
-                // rows r .. rb+62 are empty too: go on at the last row that starts at s
-                r = uniform64(wave_lower_bound(p.rowptr, p.n_rows + 1, s + 1, lane)) - 2;
-                rb = r + 1;
-                rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
-            }
-            continue;
-        }
         if (t - s > p.chunk) {
             reduce_piece<T, VEC, NS, U, MSG, MAXA, IDENT, OF32>(p, r, s, e1, kPartial, 2 * c + 1, lane, hot);
             head = static_cast<int32_t>(r);
@@ -938,7 +945,7 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
     // lane vectors covered by one launch (NS = 4, or one narrow window)
     const int64_t per_window = narrow ? kWindowBytes / 16 : 4 * kWave;
     // the first launch also zero-fills the empty rows (all features)
-    p.zero_items = (a.n_rows + kZeroRows - 1) / kZeroRows;
+    set_zero_items(p, a.n_rows);
     if (narrow && PYG_WINDOWS_ONE_LAUNCH) {
         // every window is the same width (rows are a multiple of a window): one
         // launch, window-major, then the fold of the long rows over all features
@@ -1226,7 +1233,7 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     if (mk == kMsgGcn && (maxa || !a.dinv || !a.norm_out)) return PYG_ERR_INVALID_ARG;
     // short virtual rows on average: one sub-group per row
     const bool light = lg < 6 && E <= kLightMaxDegree * B * N;
-    p.zero_items = (B * N + kZeroRows - 1) / kZeroRows;  // the first launch zero-fills the empty virtual rows
+    set_zero_items(p, B * N);  // the first launch zero-fills the empty virtual rows
     int rc;
     auto launch = [&](const SegParams &q, int kind) {
         return a.dtype == PYG_BF16 ? launch_blocked_msg<uint16_t>(q, kind, maxa, light, s)
