@@ -80,6 +80,14 @@ __device__ __forceinline__ int64_t uniform64(int64_t v) {
     return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
 }
 
+// The 64-bit value that lane l holds, read into scalar registers.
+__device__ __forceinline__ int64_t lane_value64(int64_t v, int l) {
+    const uint64_t u = static_cast<uint64_t>(v);
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(u), l);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(u >> 32), l);
+    return static_cast<int64_t>((uint64_t(hi) << 32) | lo);
+}
+
 // First index i in [0, len) with a[i] >= key; a is non-decreasing and
 // a[len - 1] >= key. 64-ary search: one coalesced probe per lane per level.
 __device__ inline int64_t wave_lower_bound(const int64_t *__restrict__ a, int64_t len, int64_t key, int lane) {
@@ -125,7 +133,7 @@ __device__ __forceinline__ int64_t next_row_with_slots(const int64_t *__restrict
     if (uniform64(rowptr[r + 2]) != t) return r + 1;  // r + 2 <= N: row r + 1 exists, as t < rowptr[N]
     // a few empty rows are stepped through; a run of 32 or more is searched past
     if (uniform64(rowptr[(r + 33) < N ? (r + 33) : N]) != t) return r + 1;
-    return uniform64(wave_lower_bound(rowptr, N + 1, t + 1, lane)) - 1;
+    return uniform_lower_bound(rowptr, N + 1, t + 1) - 1;
 }
 
 // Workgroups of a launch are dealt to the 8 XCDs in turn (workgroup w runs

@@ -158,7 +158,7 @@ __global__ __launch_bounds__(kBlock) void k_csr_edge_norm_light(const int64_t *_
         // a whole batch of empty rows ahead (a run of them all starts at pn):
         // go on at the last row that starts at pn
         if (uniform64(rowptr[(nxt + kWave) < N ? (nxt + kWave) : N]) == pn)
-            nxt = uniform64(wave_lower_bound(rowptr, N + 1, pn + 1, lane)) - 1;
+            nxt = uniform_lower_bound(rowptr, N + 1, pn + 1) - 1;
         rb = nxt;
     }
 }

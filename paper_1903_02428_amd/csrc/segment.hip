@@ -636,8 +636,8 @@ __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c
             // empty: zero-filled separately); lane i+1 holds the end of row rb+i
             const bool in = lane < kWave - 1 && rb + lane < p.n_rows && rp < (last ? p.E : e1);
             const int cnt = __popcll(__ballot(in));
-            const int64_t s_first = uniform64(__shfl(rp, 0, kWave));
-            if (cnt == kWave - 1 && uniform64(__shfl(rp, kWave - 1, kWave)) == s_first) {
+            const int64_t s_first = lane_value64(rp, 0);
+            if (cnt == kWave - 1 && lane_value64(rp, kWave - 1) == s_first) {
                 // 63 empty rows in a row: skip to the last row that starts at s_first
                 rb = uniform_lower_bound(p.rowptr, p.n_rows + 1, s_first + 1) - 1;
                 continue;
@@ -670,8 +670,8 @@ __device__ __forceinline__ void segment_chunk_work(const SegParams &p, int64_t c
         if (r + 1 - rb >= kWave) {
             rb = r;
             rp = p.rowptr[(rb + lane) < p.n_rows ? (rb + lane) : p.n_rows];
-            const int64_t s0 = uniform64(__shfl(rp, 0, kWave));
-            if (rb + kWave - 1 <= p.n_rows && uniform64(__shfl(rp, kWave - 1, kWave)) == s0) {
+            const int64_t s0 = lane_value64(rp, 0);
+            if (rb + kWave - 1 <= p.n_rows && lane_value64(rp, kWave - 1) == s0) {
                 if (s0 >= p.E || (!last && s0 >= e1)) break;
                 r = uniform64(wave_lower_bound(p.rowptr, p.n_rows + 1, s0 + 1, lane)) - 1;
                 rb = r;

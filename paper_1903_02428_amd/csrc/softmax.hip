@@ -557,10 +557,10 @@ __global__ __launch_bounds__(kBlock) void k_softmax(SmParams p) {
         // lanes 0 .. cnt-1 hold the starts of rows rb .. rb+cnt-1; lane i+1 the end of row rb+i
         const bool in = lane < kWave - 1 && rb + lane < p.n_rows && rp < e1;
         const int cnt = __popcll(__ballot(in));
-        const int64_t s_first = uniform64(__shfl(rp, 0, kWave));
-        if (cnt == kWave - 1 && uniform64(__shfl(rp, kWave - 1, kWave)) == s_first) {
+        const int64_t s_first = lane_value64(rp, 0);
+        if (cnt == kWave - 1 && lane_value64(rp, kWave - 1) == s_first) {
             // 63 empty rows in a row (no slots, no output): go on at the last row that starts at s_first
-            rb = uniform64(wave_lower_bound(p.rowptr, p.n_rows + 1, s_first + 1, lane)) - 1;
+            rb = uniform_lower_bound(p.rowptr, p.n_rows + 1, s_first + 1) - 1;
             continue;
         }
         for (int i0 = 0; i0 < cnt; i0 += S) {
