@@ -49,8 +49,8 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 # They describe the sources with the recorded hash only: after any change to
 # those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "39c8f154b0290f46",
-    "fetch_kib": 12846548.6, "write_kib": 510338.7, "tcc_hit": 296644727.0, "tcc_miss": 209785118.0,
+    "source_hash": "3b95164710432c50",
+    "fetch_kib": 12904502.5, "write_kib": 510976.4, "tcc_hit": 300426662.3, "tcc_miss": 210752965.3,
     "copy_mib": 1024, "copy_fetch_kib": 524320.1, "copy_write_kib": 1048576.0,
 }
 # everything that decides which kernels a propagate call launches and how
