@@ -404,33 +404,86 @@ __device__ __forceinline__ uint64_t pack_edge(const int64_t *__restrict__ dst64,
 }
 
 // Digit counts per tile (digit-major) of the packed elements; pass 0 packs
-// from the COO itself.
+// from the COO itself, later passes read the one-byte digits the previous
+// scatter wrote. One workgroup counts TPW neighbouring tiles into LDS
+// counters of its own per tile (K copies of each, lane % K picking one, so
+// that lanes of a skewed digit spread their LDS atomics) and writes them as
+// TPW neighbouring words per digit; the byte digits arrive 16 to a load.
+// (One workgroup per 2048-element tile spent 145 us on the 115 MB of digits
+// of the large power-law graph: launch and flush overhead, 4-byte scattered
+// writes.)
+constexpr int kHistTiles0 = 1;  // tiles per workgroup, pass 0 (reads the COO: 8 measured no faster)
+constexpr int kHistTiles = 8;   // tiles per workgroup, later passes (read byte digits)
+constexpr int kHistCopies = 4;  // counter copies (8 measured no faster, 1 slower on the skewed top digit)
+static_assert(kTile % 16 == 0, "a 16-byte digit load stays in one tile");
+
+template <int TPW, int K>
 __global__ __launch_bounds__(kSortBlock) void k_radix_hist64(const int64_t *__restrict__ dst64,
                                                          const int64_t *__restrict__ src64,
                                                          const uint64_t *__restrict__ keys,
                                                          const uint8_t *__restrict__ dig8, int64_t E, int shift,
                                                          int bits, int64_t ntiles, Packing pk,
                                                          uint32_t *__restrict__ hist) {
-    __shared__ uint32_t h[kMaxRadixP];
+    // 16-byte digit loads per thread, when a workgroup's digits split into whole loads
+    constexpr bool kVecOk = (TPW * kTile) % (16 * kSortBlock) == 0;
+    constexpr int kVec = kVecOk ? (int)(TPW * kTile / 16 / kSortBlock) : 1;
+    __shared__ uint32_t h[TPW * kMaxRadixP * K];  // [tile][digit][copy]
     const int radix = 1 << bits;
-    const uint64_t mask = radix - 1;
-    for (int i = threadIdx.x; i < radix; i += kSortBlock) h[i] = 0;
+    const uint32_t mask = radix - 1;
+    const int copy = K > 1 ? (int)(threadIdx.x % K) : 0;
+    for (int i = threadIdx.x; i < TPW * kMaxRadixP * K; i += kSortBlock) h[i] = 0;
     __syncthreads();
-    const int64_t tile = blockIdx.x;
-    const int64_t base = tile * kTile + threadIdx.x;
-#pragma unroll 4
-    for (int r = 0; r < kItems; ++r) {
-        const int64_t i = base + (int64_t)r * kSortBlock;
-        if (i < E) {
-            const uint64_t d = dig8 ? dig8[i]
-                                    : (dst64 ? (static_cast<uint64_t>(first_key(dst64, src64, i, pk.sk,
-                                                                                shift + bits > pk.sk.tb)) >> shift)
-                                             : (keys[i] >> (pk.nb + pk.ib + shift)));
-            atomicAdd(&h[d & mask], 1u);
+    const int64_t t0 = (int64_t)blockIdx.x * TPW;
+    const int64_t base = t0 * kTile;
+    const int64_t span = (E - base) < TPW * kTile ? (E - base) : TPW * kTile;  // elements here
+    if (kVecOk && dig8 && (reinterpret_cast<uintptr_t>(dig8) & 15) == 0) {
+        uint4 q[kVec];
+#pragma unroll
+        for (int r = 0; r < kVec; ++r) {
+            const int64_t o = (int64_t)(r * kSortBlock + threadIdx.x) * 16;
+            q[r] = (o + 16 <= span) ? *reinterpret_cast<const uint4 *>(dig8 + base + o) : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < kVec; ++r) {
+            const int64_t o = (int64_t)(r * kSortBlock + threadIdx.x) * 16;
+            uint32_t *hh = h + (o / kTile) * kMaxRadixP * K + copy;
+            if (o + 16 <= span) {
+                const uint32_t w4[4] = {q[r].x, q[r].y, q[r].z, q[r].w};
+#pragma unroll
+                for (int k = 0; k < 16; ++k) atomicAdd(&hh[((w4[k >> 2] >> (8 * (k & 3))) & mask) * K], 1u);
+            } else {
+                for (int64_t k = o; k < span; ++k) atomicAdd(&hh[(dig8[base + k] & mask) * K], 1u);
+            }
+        }
+    } else {
+        for (int64_t j0 = 0; j0 < span; j0 += (int64_t)kSortBlock * kItems) {
+            uint32_t d[kItems];
+#pragma unroll
+            for (int r = 0; r < kItems; ++r) {
+                const int64_t j = j0 + (int64_t)r * kSortBlock + threadIdx.x;
+                const int64_t i = base + j;
+                d[r] = j >= span ? 0xFFFFFFFFu
+                       : dig8 ? dig8[i]
+                       : dst64 ? static_cast<uint32_t>(
+                                     first_key(dst64, src64, i, pk.sk, shift + bits > pk.sk.tb) >> shift)
+                               : static_cast<uint32_t>(keys[i] >> (pk.nb + pk.ib + shift));
+            }
+            uint32_t *hh = h + (j0 / kTile) * kMaxRadixP * K + copy;
+#pragma unroll
+            for (int r = 0; r < kItems; ++r)
+                if (d[r] != 0xFFFFFFFFu) atomicAdd(&hh[(d[r] & mask) * K], 1u);
         }
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < radix; i += kSortBlock) hist[(int64_t)i * ntiles + tile] = h[i];
+    const int nt = (ntiles - t0) < TPW ? (int)(ntiles - t0) : TPW;
+    for (int k = threadIdx.x; k < radix * TPW; k += kSortBlock) {
+        const int d = k / TPW, tt = k % TPW;
+        if (tt >= nt) continue;
+        uint32_t c = 0;
+#pragma unroll
+        for (int cp = 0; cp < K; ++cp) c += h[(tt * kMaxRadixP + d) * K + cp];
+        hist[(int64_t)d * ntiles + t0 + tt] = c;
+    }
 }
 
 // One stable scatter pass over packed elements (same tile order and ranking
@@ -730,9 +783,13 @@ int coo_to_csr_impl(const int64_t *edge_index, int64_t E, int64_t N, int64_t B, 
             const int bits = (pk.kb - shift) < pbpp ? (pk.kb - shift) : pbpp;
             const bool last = p == ppasses - 1;
             const int64_t nhist = ntiles << bits;
-            k_radix_hist64<<<(unsigned)ntiles, kSortBlock, 0, s>>>(p == 0 ? dst : nullptr, src, pin,
-                                                                   p == 0 ? nullptr : w.next_dig, E, shift, bits,
-                                                                   ntiles, pk, w.hist);
+            if (p == 0)
+                k_radix_hist64<kHistTiles0, 1><<<(unsigned)((ntiles + kHistTiles0 - 1) / kHistTiles0), kSortBlock, 0, s>>>(
+                    dst, src, pin, nullptr, E, shift, bits, ntiles, pk, w.hist);
+            else
+                k_radix_hist64<kHistTiles, kHistCopies><<<(unsigned)((ntiles + kHistTiles - 1) / kHistTiles), kSortBlock, 0,
+                                                          s>>>(nullptr, src, pin, w.next_dig, E, shift, bits, ntiles, pk,
+                                                               w.hist);
             PYG_LAUNCH_CHECK();
             PYG_TRY(scan_u32(w.hist, w.hist, nhist, false, w.hist_scan, s));
             uint64_t *pout = last ? nullptr : w.pbuf[p & 1];
