@@ -383,12 +383,15 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(
 // 8 bytes per element and pass instead of 12 (the large power-law graph:
 // 3.63 -> 3.00 ms). Digits stay at most 7 bits (three 6-bit passes for 18-bit
 // ids): two 9-bit passes measured slower (3.71 ms), their 8-element runs per
-// tile write partial lines.
+// tile write partial lines; so did two passes of 10 and 9 bits with 2-byte
+// digits, 2048- or 4096-element tiles (3.2-4.0 ms against 2.1 ms).
 #ifndef PYG_RADIX_BITS_PACKED
 #define PYG_RADIX_BITS_PACKED 7
 #endif
 constexpr int kMaxDigitBitsP = PYG_RADIX_BITS_PACKED;
 constexpr int kMaxRadixP = 1 << kMaxDigitBitsP;
+// the scatter hands the next pass its digits as one byte per element
+static_assert(kMaxDigitBitsP <= 8, "packed-sort digits are stored in one byte");
 
 struct Packing {
     int kb;  // bits of the sort key (the target, or the virtual row of a blocked CSR)
