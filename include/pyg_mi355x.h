@@ -581,7 +581,11 @@ int pyg_propagate_heads_workspace(int dtype, int64_t N, int64_t H, int64_t C, in
 int pyg_propagate_heads(const void *x, int dtype, int64_t N, int64_t H, int64_t C, const pyg_csr *csr,
                         const float *alpha, void *out, void *ws, size_t ws_bytes, void *stream);
 
-/* Workspace bytes needed by pyg_csr_transpose_map. */
+/* Workspace bytes needed by pyg_csr_transpose_map: E int32 of inverse
+ * permutation, and from 2^20 edges on the scratch of its partition by edge
+ * id (two 8-byte words and one byte per edge, plus digit counts).
+ * Errors: PYG_ERR_INVALID_ARG (NULL bytes, E < 0), PYG_ERR_UNSUPPORTED
+ * (E >= 2^31). */
 int pyg_csr_transpose_map_workspace(int64_t E, size_t *bytes);
 
 /* The transpose map between the CSR of an edge list (csr) and the CSR of

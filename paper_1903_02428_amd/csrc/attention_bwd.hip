@@ -312,9 +312,16 @@ int transpose_map(const pyg_csr *csr, const pyg_csr *csr_t, int32_t *inv, int32_
 
 using namespace pyg;
 
+// Edges from which the map's inverse permutation is partitioned and written
+// block by block (inverse_perm_sorted) instead of scattered: below it the
+// scattered writes stay in the caches.
+constexpr int64_t kInvSortedMin = int64_t(1) << 20;
+
 extern "C" int pyg_csr_transpose_map_workspace(int64_t E, size_t *bytes) {
     if (!bytes || E < 0) return PYG_ERR_INVALID_ARG;
-    *bytes = align_up(static_cast<size_t>(E) * sizeof(int32_t), 256) + 256;
+    if (E >= (int64_t(1) << 31)) return PYG_ERR_UNSUPPORTED;
+    *bytes = align_up(static_cast<size_t>(E) * sizeof(int32_t), 256) + 256 +
+             (E >= kInvSortedMin ? inverse_perm_sorted_workspace(E) : 0);
     return PYG_OK;
 }
 
@@ -327,7 +334,14 @@ extern "C" int pyg_csr_transpose_map(const pyg_csr *csr, const pyg_csr *csr_t, i
     size_t need;
     PYG_TRY(pyg_csr_transpose_map_workspace(E, &need));
     if (ws_bytes < need || !ws) return PYG_ERR_WORKSPACE;
-    return transpose_map(csr, csr_t, static_cast<int32_t *>(ws), map_t, static_cast<hipStream_t>(stream));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (E < kInvSortedMin) return transpose_map(csr, csr_t, static_cast<int32_t *>(ws), map_t, s);
+    int32_t *inv = static_cast<int32_t *>(ws);
+    const size_t inv_bytes = align_up(static_cast<size_t>(E) * sizeof(int32_t), 256);
+    PYG_TRY(inverse_perm_sorted(csr->perm, E, inv, static_cast<char *>(ws) + inv_bytes, ws_bytes - inv_bytes, s));
+    k_compose<<<grid_for(E, kBlock * 4), kBlock, 0, s>>>(csr_t->perm, inv, E, map_t);
+    PYG_LAUNCH_CHECK();
+    return PYG_OK;
 }
 
 extern "C" int pyg_propagate_heads_backward_workspace(int dtype, int64_t N, int64_t H, int64_t C, int64_t E,

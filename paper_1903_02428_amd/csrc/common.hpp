@@ -230,6 +230,11 @@ int segment_reduce(const SegmentArgs &a, void *ws, size_t ws_bytes, hipStream_t 
 // slot q of csr_t (inv: E int32 of scratch).
 int inverse_perm(const int64_t *perm, int64_t E, int32_t *inv, hipStream_t s);
 int transpose_map(const pyg_csr *csr, const pyg_csr *csr_t, int32_t *inv, int32_t *map_t, hipStream_t s);
+// The same inverse with coalesced writes (a radix partition of the (id, slot)
+// pairs by the id's high bits, then one LDS block of ids per workgroup);
+// scratch inverse_perm_sorted_workspace(E) bytes.
+size_t inverse_perm_sorted_workspace(int64_t E);
+int inverse_perm_sorted(const int64_t *perm, int64_t E, int32_t *inv, void *ws, size_t ws_bytes, hipStream_t s);
 
 // Every argument check of pyg_propagate (nothing is launched); on success
 // *need is the workspace the call takes.

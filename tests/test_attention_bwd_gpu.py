@@ -47,12 +47,30 @@ def transpose_map_ref(ei, N):
 
 
 def test_csr_transpose_map(pyg):
-    for i, (N, E) in enumerate([(1, 0), (5, 1), (300, 5000), (3000, 90000)]):
+    # from 2^20 edges on, the inverse permutation is partitioned by edge id
+    # and written block by block: one and two radix passes over the id bits
+    # above the 2^14-id LDS blocks, ragged last blocks and tiles
+    for i, (N, E) in enumerate([(1, 0), (5, 1), (300, 5000), (3000, 90000), (40000, 1 << 20),
+                                (70000, 1_500_001), (300000, 2_200_037)]):
         rng = np.random.default_rng(870 + i)
-        ei, csr, csr_t, _ = graphs(pyg, rng, N, E, 64 if i == 3 else 0, hub=i == 3)
+        ei, csr, csr_t, _ = graphs(pyg, rng, N, E, 64 if i == 3 else 0, hub=i in (3, 6))
         got = pyg.csr_transpose_map(csr, csr_t)
         torch.cuda.synchronize()
         assert got.dtype == torch.int32 and np.array_equal(got.cpu().numpy(), transpose_map_ref(ei, N)), (N, E)
+
+
+def test_csr_transpose_map_malformed_perm_stays_in_bounds(pyg):
+    # a permutation with repeated ids (not one built by coo_to_csr): the map
+    # is meaningless but every entry lies in [0, E)
+    rng = np.random.default_rng(881)
+    N, E = 50000, 1_300_000
+    ei, csr, csr_t, _ = graphs(pyg, rng, N, E)
+    bad = csr.perm.clone()
+    bad[: E // 3] = bad[E // 3: 2 * (E // 3)]
+    got = pyg.csr_transpose_map(pyg.CSR(csr.rowptr, csr.col, bad, csr.weight, csr.N, csr.E, csr.chunk), csr_t)
+    torch.cuda.synchronize()
+    g = got.cpu().numpy()
+    assert g.min() >= 0 and g.max() < E
 
 
 def heads_bwd_case(pyg, N, E, H, C, seed, dtype, chunk=0, hub=False, use_map=False):
