@@ -39,14 +39,33 @@ __device__ __forceinline__ T block_exclusive_scan(T v, T *lds, T *total) {
     return before + incl - v;
 }
 
+// A thread's kItems consecutive elements, as 16-byte loads when they are
+// all in range and the array is 16-byte aligned (each thread's run starts at
+// a multiple of kItems elements).
+template <typename T>
+__device__ __forceinline__ void load_items(const T *p, int64_t base, int64_t n, T (&v)[kItems]) {
+    static_assert((kItems * sizeof(T)) % 16 == 0, "whole 16-byte loads per thread");
+    if (base + kItems <= n && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+#pragma unroll
+        for (int i = 0; i < kItems; i += 16 / (int)sizeof(T)) {
+            const uint4 q = *reinterpret_cast<const uint4 *>(p + base + i);
+            __builtin_memcpy(&v[i], &q, 16);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kItems; ++i) v[i] = (base + i < n) ? p[base + i] : T(0);
+    }
+}
+
 template <typename T>
 __global__ __launch_bounds__(kBlock) void k_scan_reduce(const T *__restrict__ in, int64_t n, T *__restrict__ sums) {
     __shared__ T lds[kBlock / kWave];
     const int64_t base = blockIdx.x * kSeg + (int64_t)threadIdx.x * kItems;
+    T v[kItems];
+    load_items(in, base, n, v);
     T s = 0;
 #pragma unroll
-    for (int i = 0; i < kItems; ++i)
-        if (base + i < n) s += in[base + i];
+    for (int i = 0; i < kItems; ++i) s += v[i];
     T total;
     block_exclusive_scan(s, lds, &total);
     if (threadIdx.x == 0) sums[blockIdx.x] = total;
@@ -58,19 +77,30 @@ __global__ __launch_bounds__(kBlock) void k_scan_apply(const T *in, T *out, int6
     __shared__ T lds[kBlock / kWave];
     const int64_t base = blockIdx.x * kSeg + (int64_t)threadIdx.x * kItems;
     T v[kItems];
+    load_items(in, base, n, v);
     T s = 0;
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
-        v[i] = (base + i < n) ? in[base + i] : T(0);
-        s += v[i];
-    }
+    for (int i = 0; i < kItems; ++i) s += v[i];
     T total;
     T run = block_exclusive_scan(s, lds, &total) + (offsets ? offsets[blockIdx.x] : T(0));
+    T r[kItems];
 #pragma unroll
     for (int i = 0; i < kItems; ++i) {
-        T next = run + v[i];
-        if (base + i < n) out[base + i] = inclusive ? next : run;
+        const T next = run + v[i];
+        r[i] = inclusive ? next : run;
         run = next;
+    }
+    if (base + kItems <= n && (reinterpret_cast<uintptr_t>(out) & 15) == 0) {
+#pragma unroll
+        for (int i = 0; i < kItems; i += 16 / (int)sizeof(T)) {
+            uint4 q;
+            __builtin_memcpy(&q, &r[i], 16);
+            *reinterpret_cast<uint4 *>(out + base + i) = q;
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < kItems; ++i)
+            if (base + i < n) out[base + i] = r[i];
     }
 }
 
