@@ -15,9 +15,13 @@
 //                              waves in order, stages a tile-local
 //                              permutation in LDS and writes every digit run
 //                              contiguously.
-//   then      k_row_bounds     rowptr from the key changes of the sorted keys.
+//   then      k_row_bounds     rowptr from the key changes of the sorted keys
+//                              (k_row_bounds_low when the packed sort kept
+//                              only each key's bits below its last digit).
 // Elements keep their order inside equal digits in every pass, so the slots
-// of a row end in ascending COO edge id and the result is unique.
+// of a row end in ascending COO edge id and the result is unique. The same
+// packed passes also partition (edge id, slot) pairs for the LDS-blocked
+// inverse permutation of the transpose map (inverse_perm_sorted).
 //
 // In-degree counting uses LDS-privatised histograms over slices of the node
 // range (no global atomics on the edge stream): every workgroup counts the
