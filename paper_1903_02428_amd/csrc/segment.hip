@@ -710,26 +710,29 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
     segment_chunk_work<T, VEC, NS, U, MSG, MAXA, IDENT, LIGHT, OF32>(p, c, lane);
 }
 
-// Fold the pieces of every long row: one workgroup per chunk that starts a
-// long row. Piece 0 is the head partial (slot 2c+1), piece m >= 1 the
-// continuation in chunk c+m (slot 2(c+m)). The four waves fold contiguous,
-// ordered ranges of pieces with 8 loads in flight, then wave 0 combines the
-// four results in wave order: a fixed order, so the fold is deterministic,
-// and for max the earliest piece wins ties.
-template <typename T, bool MAXA, int WAVES, bool OF32>
-__global__ __launch_bounds__(WAVES * kWave) void k_segment_fixup(SegParams p) {
-    constexpr int kW = WAVES;
-    constexpr int kU = WAVES > 4 ? 16 : 8;
-    __shared__ float sv[kW][kWave];
-    __shared__ int32_t sp[kW][kWave];
-    const int64_t c = blockIdx.x;
-    if (c >= p.nchunks) return;
-    const int64_t r = p.head_row[c];
-    if (r < 0) return;  // uniform over the workgroup
+// Folding the pieces of every long row. Piece 0 is the head partial (slot
+// 2c+1 of its head chunk c), piece m >= 1 the continuation in chunk c+m
+// (slot 2(c+m)). The waves of a workgroup (4, or 16 for a few very long
+// rows) fold contiguous, ordered ranges of the pieces with 8 (16) loads in
+// flight, then wave 0 combines their results in wave order: a fixed order,
+// so the fold is deterministic, and for max the earliest piece wins ties.
+// The slot of piece m of the long row whose head chunk is c.
+__device__ __forceinline__ int64_t piece_slot(int64_t c, int64_t m) { return m == 0 ? 2 * c + 1 : 2 * (c + m); }
+
+// Fold pieces g0, g0 + G, g0 + 2G, ... (below K) of the long row r with head
+// chunk c, in order. FINAL: write the row's result (mean divided, argmax as
+// an edge id); else write the fold into the slot of piece g0 (a group's
+// partial, for the second level of the grouped fold).
+template <typename T, bool MAXA, int kW, int kU, bool OF32, bool FINAL = true>
+__device__ __forceinline__ void fold_long_row(const SegParams &p, int64_t c, int64_t r, float (&sv)[kW][kWave],
+                                              int32_t (&sp)[kW][kWave], int64_t g0 = 0, int64_t G = 1,
+                                              int64_t gend = -1) {
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     const int64_t s = p.rowptr[r], t = p.rowptr[r + 1];
-    const int64_t K = (t - 1) / p.chunk - c + 1;  // pieces of this row
+    const int64_t Kall = (t - 1) / p.chunk - c + 1;  // pieces of this row
+    const int64_t pend = gend < 0 ? Kall : (gend < Kall ? gend : Kall);
+    const int64_t K = (pend - g0 + G - 1) / G;  // pieces folded here: g0 + G * [0, K)
     const int64_t m0 = K * wave / kW, m1 = K * (wave + 1) / kW;
     T *out = static_cast<T *>(p.out);
     for (int64_t fg = 0; fg < p.fcnt; fg += kWave) {
@@ -743,7 +746,7 @@ __global__ __launch_bounds__(WAVES * kWave) void k_segment_fixup(SegParams p) {
 #pragma unroll
             for (int u = 0; u < kU; ++u) {
                 const int64_t mm = m + u;
-                const int64_t slot = mm == 0 ? 2 * c + 1 : 2 * (c + mm);
+                const int64_t slot = piece_slot(c, g0 + G * mm);
                 const bool ok = on && mm < m1;
                 o[u] = ok ? p.part_val[slot * p.F + f] : 0.f;
                 op[u] = (ok && MAXA) ? p.part_pos[slot * p.F + f] : -1;
@@ -780,14 +783,70 @@ __global__ __launch_bounds__(WAVES * kWave) void k_segment_fixup(SegParams p) {
                     acc += o;
                 }
             }
-            if (!MAXA && p.mean) acc = acc / static_cast<float>(t - s);
-            if constexpr (OF32) static_cast<float *>(p.out)[r * p.F + f] = acc;
-            else if constexpr (sizeof(T) == 2) out[r * p.F + f] = f32_to_bf16_rne(acc);
-            else out[r * p.F + f] = acc;
-            if constexpr (MAXA) p.argmax[r * p.F + f] = p.perm ? p.perm[pos] : static_cast<int64_t>(pos);
+            if constexpr (!FINAL) {
+                const int64_t slot = piece_slot(c, g0);
+                p.part_val[slot * p.F + f] = acc;
+                if constexpr (MAXA) p.part_pos[slot * p.F + f] = pos;
+            } else {
+                if (!MAXA && p.mean) acc = acc / static_cast<float>(t - s);
+                if constexpr (OF32) static_cast<float *>(p.out)[r * p.F + f] = acc;
+                else if constexpr (sizeof(T) == 2) out[r * p.F + f] = f32_to_bf16_rne(acc);
+                else out[r * p.F + f] = acc;
+                if constexpr (MAXA) p.argmax[r * p.F + f] = p.perm ? p.perm[pos] : static_cast<int64_t>(pos);
+            }
         }
         __syncthreads();
     }
+}
+
+// Pieces per group of the grouped fold (few, very long rows).
+constexpr int64_t kFoldGroup = 64;
+
+// Level 1 of the grouped fold: workgroup c folds, in order, the group of
+// kFoldGroup pieces that starts at chunk c, of the long row chunk c
+// continues and of the long row that starts in it (if they have more than
+// kFoldGroup pieces), into the group's first piece slot. One workgroup on one
+// CU folding all 3,640 pieces of the large graph's whole-graph pool was held
+// to that CU's load bandwidth (63 us); the groups spread over the chip.
+template <typename T, bool MAXA, bool OF32>
+__global__ __launch_bounds__(kBlock) void k_segment_fold_groups(SegParams p) {
+    __shared__ float sv[kBlock / kWave][kWave];
+    __shared__ int32_t sp[kBlock / kWave][kWave];
+    const int64_t c = blockIdx.x;
+    if (c >= p.nchunks || p.n_rows <= 0) return;
+    const int64_t e0 = c * p.chunk;
+    // the row holding the chunk's first slot: the last r with rowptr[r] <= e0
+    int64_t lo = 0, hi = p.n_rows - 1;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (p.rowptr[mid] <= e0) lo = mid;
+        else hi = mid - 1;
+    }
+    const int64_t r1 = lo, s1 = p.rowptr[r1], t1 = p.rowptr[r1 + 1];
+    const int64_t h1 = s1 / p.chunk;  // its head chunk
+    if (h1 < c && t1 > e0 && t1 - s1 > p.chunk && (t1 - 1) / p.chunk - h1 + 1 > kFoldGroup && (c - h1) % kFoldGroup == 0)
+        fold_long_row<T, MAXA, kBlock / kWave, 8, OF32, false>(p, h1, r1, sv, sp, c - h1, 1, c - h1 + kFoldGroup);
+    const int64_t r2 = p.head_row[c];
+    if (r2 >= 0 && (p.rowptr[r2 + 1] - 1) / p.chunk - c + 1 > kFoldGroup)
+        fold_long_row<T, MAXA, kBlock / kWave, 8, OF32, false>(p, c, r2, sv, sp, 0, 1, kFoldGroup);
+}
+
+// The fold proper: one workgroup per chunk that starts a long row. GROUPED
+// (after k_segment_fold_groups): a row of more than kFoldGroup pieces folds
+// its groups' partials, pieces 0, kFoldGroup, 2 kFoldGroup, ... in order.
+template <typename T, bool MAXA, int WAVES, bool OF32, bool GROUPED>
+__global__ __launch_bounds__(WAVES * kWave) void k_segment_fixup(SegParams p) {
+    constexpr int kW = WAVES;
+    constexpr int kU = WAVES > 4 ? 16 : 8;
+    __shared__ float sv[kW][kWave];
+    __shared__ int32_t sp[kW][kWave];
+    const int64_t c = blockIdx.x;
+    if (c >= p.nchunks) return;
+    const int64_t r = p.head_row[c];
+    if (r < 0) return;  // uniform over the workgroup
+    const int64_t K = (p.rowptr[r + 1] - 1) / p.chunk - c + 1;
+    if (GROUPED && K > kFoldGroup) fold_long_row<T, MAXA, kW, kU, OF32>(p, c, r, sv, sp, 0, kFoldGroup);
+    else fold_long_row<T, MAXA, kW, kU, OF32>(p, c, r, sv, sp);
 }
 
 // Degree class of every row, and their histogram (hist must start at zero).
@@ -850,11 +909,15 @@ __global__ void k_empty_rows(T *__restrict__ out, int64_t *__restrict__ argmax, 
 template <typename T, bool MAXA, bool OF32 = false>
 int launch_fixup(const SegParams &p, hipStream_t s) {
     if (p.nchunks <= 1) return PYG_OK;
-    // few, very long rows (e.g. whole-graph pooling): 16 waves fold each row
-    if (p.E > 16 * p.chunk * (p.n_rows > 0 ? p.n_rows : 1))
-        k_segment_fixup<T, MAXA, 16, OF32><<<static_cast<unsigned>(p.nchunks), 16 * kWave, 0, s>>>(p);
-    else
-        k_segment_fixup<T, MAXA, 4, OF32><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
+    // few, very long rows (e.g. whole-graph pooling): groups of pieces folded
+    // across the chip first, then 16 waves fold each row's group partials
+    if (p.E > 16 * p.chunk * (p.n_rows > 0 ? p.n_rows : 1)) {
+        k_segment_fold_groups<T, MAXA, OF32><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
+        PYG_LAUNCH_CHECK();
+        k_segment_fixup<T, MAXA, 16, OF32, true><<<static_cast<unsigned>(p.nchunks), 16 * kWave, 0, s>>>(p);
+    } else {
+        k_segment_fixup<T, MAXA, 4, OF32, false><<<static_cast<unsigned>(p.nchunks), kBlock, 0, s>>>(p);
+    }
     PYG_LAUNCH_CHECK();
     return PYG_OK;
 }

@@ -248,6 +248,26 @@ def test_global_pool(pyg, aggr, dtype):
             check_sum(out, ref, sabs, dtype == BF16, f"pool {sizes[:5]}")
 
 
+@pytest.mark.parametrize("aggr", ["sum", "mean", "max"])
+@pytest.mark.parametrize("dtype", [F32, BF16])
+def test_global_pool_long_graphs_grouped_fold(pyg, aggr, dtype):
+    # graphs of many chunks: their pieces are folded in groups first, then
+    # the groups' partials in order; small integer features make the maxima
+    # tie across many nodes and groups (argmax: the lowest node id)
+    rng = np.random.default_rng(23)
+    for sizes, F in (((20000,), 8), ((9000, 3, 30000), 5), ((4100,), 130)):
+        B = len(sizes)
+        batch = np.repeat(np.arange(B), sizes).astype(np.int64)
+        N = batch.size
+        x = rng.integers(-3, 4, (N, F)).astype(np.float32)
+        out, arg = pyg.global_pool(to_dev(x).to(dtype), to_dev(batch), B, aggr)
+        ref, rarg, sabs = oracle.global_pool(x, batch, B, aggr)
+        if aggr == "max":
+            check_max(out, arg, ref, rarg, dtype == BF16, f"pool {sizes}")
+        else:
+            check_sum(out, ref, sabs, dtype == BF16, f"pool {sizes}")
+
+
 def test_validate(pyg):
     ei = to_dev(np.array([[0, 5, -1, 2], [1, 1, 1, 9]], np.int64))
     assert pyg.validate_coo(ei, 6) == 2   # -1 and 9
