@@ -164,16 +164,19 @@ int count_targets(const int64_t *dst, int64_t E, int64_t N, Out *out, void *ws, 
 // target alone (the first pass reads no source ids); the sorted keys are
 // turned into virtual rows (source block) * N + target at the end.
 struct SortKey {
-    int64_t bsize;  // 0: plain CSR
+    int64_t bsize;   // 0: plain CSR
     int64_t N;
-    int tb;         // bits of a target id
+    int tb;          // bits of a target id
+    uint64_t bmagic; // source / bsize = (source * bmagic) >> bshift for sources below 2^31
+    int bshift;
 };
 
 __device__ __forceinline__ uint32_t first_key(const int64_t *__restrict__ dst64, const int64_t *__restrict__ src64,
                                               int64_t i, SortKey sk, bool with_block = true) {
     const uint32_t t = static_cast<uint32_t>(dst64[i]);
     if (sk.bsize == 0 || !with_block) return t;
-    const uint32_t b = static_cast<uint32_t>(src64[i]) / static_cast<uint32_t>(sk.bsize);
+    const uint32_t b = static_cast<uint32_t>((static_cast<uint64_t>(static_cast<uint32_t>(src64[i])) * sk.bmagic) >>
+                                             sk.bshift);
     return (b << sk.tb) | t;
 }
 
@@ -698,13 +701,25 @@ void digit_plan(int b, int *nb, int *passes, int *bpp) {
 }
 
 // Source blocks: B blocks of ceil(N / B) consecutive source ids (B = 1: the
-// plain CSR, keyed by target alone).
+// plain CSR, keyed by target alone). The block of a source is a division by
+// the invariant bsize, done as a multiply and shift (Granlund and
+// Montgomery, division by invariant integers using multiplication, 1994):
+// with l = ceil(log2 bsize) and m = floor(2^(31+l) / bsize) + 1, floor(n /
+// bsize) = floor(n m / 2^(31+l)) for every 0 <= n < 2^31, and n m < 2^64
+// (m < 2^33). The GPU has no integer divide instruction: a division by a
+// runtime value is a reciprocal-and-correction sequence per edge.
 SortKey sort_key(int64_t N, int64_t B) {
     SortKey sk{};
     sk.bsize = B > 1 ? (N + B - 1) / B : 0;
     sk.N = N;
     sk.tb = 1;
     while (sk.tb < 31 && (int64_t(1) << sk.tb) < N) ++sk.tb;
+    if (sk.bsize > 0) {
+        int l = 0;
+        while ((int64_t(1) << l) < sk.bsize) ++l;
+        sk.bmagic = ((uint64_t(1) << (31 + l)) / static_cast<uint64_t>(sk.bsize)) + 1;
+        sk.bshift = 31 + l;
+    }
     return sk;
 }
 
