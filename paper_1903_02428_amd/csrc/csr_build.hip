@@ -423,6 +423,7 @@ __device__ __forceinline__ uint64_t pack_edge(const int64_t *__restrict__ dst64,
 // of the large power-law graph: launch and flush overhead, 4-byte scattered
 // writes.)
 constexpr int kHistTiles0 = 1;  // tiles per workgroup, pass 0 (reads the COO: 8 measured no faster)
+static_assert(kItems % 2 == 0, "pass 0 reads its 8-byte ids in pairs");
 constexpr int kHistTiles = 8;   // tiles per workgroup, later passes (read byte digits)
 constexpr int kHistCopies = 4;  // counter copies (8 measured no faster, 1 slower on the skewed top digit)
 static_assert(kTile % 16 == 0, "a 16-byte digit load stays in one tile");
@@ -465,6 +466,31 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist64(const int64_t *__re
                 for (int64_t k = o; k < span; ++k) atomicAdd(&hh[(dig8[base + k] & mask) * K], 1u);
             }
         }
+    } else if (TPW == 1 && dst64 && !(shift + bits > pk.sk.tb && pk.sk.bsize)) {
+        // pass 0 over the targets: pairs of 8-byte ids per 16-byte load, from
+        // the first 16-byte boundary (a leading odd element and a trailing
+        // single one taken alone)
+        const int64_t *d = dst64 + base;
+        const int a = (reinterpret_cast<uintptr_t>(d) & 15) ? 1 : 0;
+        const int64_t npair = (span - a) >> 1;
+        uint32_t *hh = h + copy;
+        constexpr int kP = kItems / 2;  // pairs per thread
+        longlong2 q[kP];
+#pragma unroll
+        for (int r = 0; r < kP; ++r) {
+            const int64_t j = (int64_t)r * kSortBlock + threadIdx.x;
+            q[r] = j < npair ? *reinterpret_cast<const longlong2 *>(d + a + 2 * j) : make_longlong2(0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < kP; ++r) {
+            const int64_t j = (int64_t)r * kSortBlock + threadIdx.x;
+            if (j < npair) {
+                atomicAdd(&hh[((static_cast<uint32_t>(q[r].x) >> shift) & mask) * K], 1u);
+                atomicAdd(&hh[((static_cast<uint32_t>(q[r].y) >> shift) & mask) * K], 1u);
+            }
+        }
+        if (threadIdx.x == 0 && a) atomicAdd(&hh[((static_cast<uint32_t>(d[0]) >> shift) & mask) * K], 1u);
+        if (threadIdx.x == 1 && ((span - a) & 1)) atomicAdd(&hh[((static_cast<uint32_t>(d[span - 1]) >> shift) & mask) * K], 1u);
     } else {
         for (int64_t j0 = 0; j0 < span; j0 += (int64_t)kSortBlock * kItems) {
             uint32_t d[kItems];
