@@ -50,9 +50,9 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published peak
 # They describe the sources with the recorded hash only: after any change to
 # those sources the traffic field is reported as null.
 COUNTERS = {
-    "source_hash": "1579b54a12b905a5",
-    "fetch_kib": 12905108.9, "write_kib": 510983.1, "tcc_hit": 300777434.7, "tcc_miss": 210730332.7,
-    "copy_mib": 1024, "copy_fetch_kib": 524321.0, "copy_write_kib": 1048576.0,
+    "source_hash": "a2d2b7630495b08d",
+    "fetch_kib": 12901985.6, "write_kib": 502042.8, "tcc_hit": 300259659.0, "tcc_miss": 210657761.3,
+    "copy_mib": 1024, "copy_fetch_kib": 524320.3, "copy_write_kib": 1048576.0,
 }
 # everything that decides which kernels a propagate call launches and how
 KERNEL_SOURCES = ["paper_1903_02428_amd/csrc/segment.hip", "paper_1903_02428_amd/csrc/common.hpp",

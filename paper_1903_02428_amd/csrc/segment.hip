@@ -1080,13 +1080,19 @@ int run_typed(const SegmentArgs &a, SegParams p, hipStream_t s) {
 // partial, equal values to the lower edge id, blocks without slots (argmax =
 // sentinel) skipped. A fixed order: deterministic. F % 4 == 0. With `scale`,
 // features from `scale_from` on (a multiple of 4) are multiplied by
-// scale[i] in fp64 and rounded once.
+// scale[i] in fp64 and rounded once. With `pieces` (sum and mean), a virtual
+// row longer than `chunk` slots is read as the sum of its pieces (head
+// partial, then one continuation per chunk, in order) instead of from P, so
+// that no fix-up launch folds them first: that launch, one workgroup per
+// chunk, took 47 us on the large power-law graph, nearly all of it spent on
+// workgroups with nothing to fold.
 template <typename T, bool MAXA>
 __global__ __launch_bounds__(kBlock) void k_block_fold(const float *__restrict__ P, const int64_t *__restrict__ Parg,
                                                        const int64_t *__restrict__ rowptr, int64_t N, int64_t F,
                                                        int64_t B, int mean, int64_t sentinel, T *__restrict__ out,
                                                        int64_t *__restrict__ argmax, const double *__restrict__ scale,
-                                                       int64_t scale_from) {
+                                                       int64_t scale_from, const float *__restrict__ pieces,
+                                                       int64_t chunk) {
     const int64_t nq = N * F / 4;
     const int64_t NF = N * F;
     for (int64_t q = blockIdx.x * (int64_t)kBlock + threadIdx.x; q < nq; q += (int64_t)gridDim.x * kBlock) {
@@ -1094,7 +1100,32 @@ __global__ __launch_bounds__(kBlock) void k_block_fold(const float *__restrict__
         float v[4] = {0.f, 0.f, 0.f, 0.f};
         int64_t a[4] = {sentinel, sentinel, sentinel, sentinel};
         for (int64_t b = 0; b < B; ++b) {
-            const float4 pv = *reinterpret_cast<const float4 *>(P + b * NF + e);
+            float4 pv;
+            int64_t s0 = 0, t0 = 0;
+            if (!MAXA && pieces) {
+                const int64_t r = b * N + e / F;
+                s0 = rowptr[r];
+                t0 = rowptr[r + 1];
+            }
+            if (!MAXA && pieces && t0 - s0 > chunk) {
+                const int64_t c = s0 / chunk, K = (t0 - 1) / chunk - c + 1, f = e % F;
+                pv = make_float4(0.f, 0.f, 0.f, 0.f);
+                int64_t m = 0;
+                for (; m + 4 <= K; m += 4) {  // four loads in flight, added in piece order
+                    float4 w[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u)
+                        w[u] = *reinterpret_cast<const float4 *>(pieces + piece_slot(c, m + u) * F + f);
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) pv.x += w[u].x, pv.y += w[u].y, pv.z += w[u].z, pv.w += w[u].w;
+                }
+                for (; m < K; ++m) {
+                    const float4 w = *reinterpret_cast<const float4 *>(pieces + piece_slot(c, m) * F + f);
+                    pv.x += w.x, pv.y += w.y, pv.z += w.z, pv.w += w.w;
+                }
+            } else {
+                pv = *reinterpret_cast<const float4 *>(P + b * NF + e);
+            }
             const float pw[4] = {pv.x, pv.y, pv.z, pv.w};
             if constexpr (MAXA) {
 #pragma unroll
@@ -1340,13 +1371,20 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
         rc = launch(p, mk);
     }
     if (rc != PYG_OK) return rc;
-    // long virtual rows: fold their pieces (all features) into P
+    // long virtual rows: their pieces (all features) folded into P by the
+    // fix-up (max, and few very long rows), or for sum and mean read by the
+    // block fold itself
     p.nwin = 1;
     p.fbase = 0;
     p.fcnt = F;
-    if (a.dtype == PYG_BF16) rc = maxa ? launch_fixup<uint16_t, true, true>(p, s) : launch_fixup<uint16_t, false, true>(p, s);
-    else rc = maxa ? launch_fixup<float, true, true>(p, s) : launch_fixup<float, false, true>(p, s);
-    if (rc != PYG_OK) return rc;
+    const bool fold_pieces = !maxa && p.nchunks > 1 && !(p.E > 16 * p.chunk * (p.n_rows > 0 ? p.n_rows : 1));
+    if (!fold_pieces) {
+        if (a.dtype == PYG_BF16)
+            rc = maxa ? launch_fixup<uint16_t, true, true>(p, s) : launch_fixup<uint16_t, false, true>(p, s);
+        else rc = maxa ? launch_fixup<float, true, true>(p, s) : launch_fixup<float, false, true>(p, s);
+        if (rc != PYG_OK) return rc;
+    }
+    const float *pieces = fold_pieces ? p.part_val : nullptr;
     const unsigned g = grid_for(N * F / 4, kBlock, 1 << 16);
     const int mean = a.aggr == PYG_MEAN;
     const double *scale = prescale ? a.dinv : nullptr;
@@ -1354,15 +1392,17 @@ int segment_reduce_blocked(const SegmentArgs &a, int64_t B, void *ws, size_t ws_
     if (a.dtype == PYG_BF16) {
         if (maxa) k_block_fold<uint16_t, true><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
                                                                       static_cast<uint16_t *>(a.out), a.argmax,
-                                                                      nullptr, 0);
+                                                                      nullptr, 0, nullptr, 0);
         else k_block_fold<uint16_t, false><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
-                                                                  static_cast<uint16_t *>(a.out), a.argmax, nullptr, 0);
+                                                                  static_cast<uint16_t *>(a.out), a.argmax, nullptr, 0,
+                                                                  pieces, p.chunk);
     } else {
         if (maxa) k_block_fold<float, true><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
-                                                                   static_cast<float *>(a.out), a.argmax, nullptr, 0);
+                                                                   static_cast<float *>(a.out), a.argmax, nullptr, 0,
+                                                                   nullptr, 0);
         else k_block_fold<float, false><<<g, kBlock, 0, s>>>(w.P, w.Parg, a.rowptr, N, F, B, mean, E,
                                                                static_cast<float *>(a.out), a.argmax, scale,
-                                                               scale_from);
+                                                               scale_from, pieces, p.chunk);
     }
     PYG_LAUNCH_CHECK();
     return PYG_OK;
