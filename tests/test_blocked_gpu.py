@@ -69,6 +69,21 @@ def test_csr_blocks_bit_exact(pyg, N, E, B):
 DIRECT = [(1, 0), (5, 40), (300, 5000), (7001, 90000), (2_100_000, 4_200_000)]
 
 
+@pytest.mark.parametrize("N,E,B", [(3_000_000, 400_000, 2), (1_500_000, 300_000, 4)])
+def test_coo_to_csr_blocked_wide_keys(pyg, N, E, B):
+    # 23-bit blocked keys, two blocks over 22-bit targets and four over
+    # 21-bit ones (packed passes of 5, 6, 6, 6 bits: the 17 bits below the
+    # last digit do not fit 2 bytes, so the keys are kept whole as rows)
+    rng = np.random.default_rng(N + 3 * E + B)
+    ei_np = synth.random_coo(rng, N, E)
+    brp, col, perm, _, _ = expected_blocks(ei_np, N, B, None)
+    bc = pyg.coo_to_csr_blocked(to_dev(ei_np), N, B, with_perm=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(bc.rowptr.cpu().numpy(), brp)
+    assert np.array_equal(bc.col.cpu().numpy().astype(np.int64), col)
+    assert np.array_equal(bc.perm.cpu().numpy(), perm)
+
+
 @pytest.mark.parametrize("N,E", DIRECT)
 @pytest.mark.parametrize("B", [2, 3, 8, 32])
 def test_coo_to_csr_blocked_bit_exact(pyg, N, E, B):

@@ -67,6 +67,22 @@ def test_csr_many_digits(pyg):
     assert np.array_equal(csr.col.cpu().numpy().astype(np.int64), col)
 
 
+@pytest.mark.parametrize("N,E", [(2_000_000, 300_000), (3_000_000, 300_000), (6_000_000, 200_000)])
+def test_csr_wide_keys(pyg, N, E):
+    # packed sorts of 21-bit targets (three passes, the sorted keys' low 14
+    # bits kept as 2 bytes), 22-bit targets (four passes of 5, 5, 6, 6 bits:
+    # low 16 bits, still 2 bytes) and 23-bit targets (5, 6, 6, 6: low 17 bits,
+    # the keys kept whole as rows)
+    rng = np.random.default_rng(N + E)
+    ei_np = np.stack([rng.integers(0, N, E), rng.integers(0, N, E)]).astype(np.int64)
+    ei_np[1, : E // 4] = ei_np[1, : E // 4] % 97  # a few hubs among the spread targets
+    csr = pyg.coo_to_csr(to_dev(ei_np), N)
+    rp, col, perm = oracle.coo_to_csr(ei_np, N)
+    assert np.array_equal(csr.rowptr.cpu().numpy(), rp)
+    assert np.array_equal(csr.perm.cpu().numpy(), perm)
+    assert np.array_equal(csr.col.cpu().numpy().astype(np.int64), col)
+
+
 @pytest.mark.parametrize("N,E,F", SMALL)
 @pytest.mark.parametrize("weighted", [False, True])
 def test_gcn_norm(pyg, N, E, F, weighted):
